@@ -1,0 +1,248 @@
+"""Reference oracle for SAME Gibbs sampling (arXiv 1511.06416) -- TEST INFRASTRUCTURE.
+
+A ctypes wrapper around ``same_oracle.c``, a plain fp64 CPU implementation of
+the SAME Gibbs sweep, the count histogram, the moving sum and the Dirichlet
+resample.  Only the test suite, ``__graft_entry__.smoke()`` and the CPU-baseline
+leg of ``bench.py`` may import this package.  It shares no code with the HIP
+library and never imports it; the two meet only on arrays produced by the
+seeded input generators in ``workloads``.
+
+Every wrapper takes numpy arrays and returns numpy arrays.  See the C file's
+header for the paper passages each routine follows and for the readings taken
+where the paper is silent.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+import threading
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "same_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lock = threading.Lock()
+_lib = None
+
+FLAG_BAND = 1e-6
+FLT_MIN = float(np.finfo(np.float32).tiny)
+
+
+def build(force: bool = False) -> str:
+    """Compile ``same_oracle.c`` with gcc into ``liboracle.so`` (in place)."""
+    if force or not os.path.exists(_LIB_PATH) or (
+        os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC)
+    ):
+        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+        subprocess.check_call(
+            ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-o", tmp, _SRC, "-lm"]
+        )
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _i32p(a):
+    return a.ctypes.data_as(C.POINTER(C.c_int32))
+
+
+def lib():
+    global _lib
+    with _lock:
+        if _lib is None:
+            build()
+            L = C.CDLL(_LIB_PATH)
+            P = C.c_void_p
+            L.oracle_philox4x32_10.argtypes = [P, P, P]
+            L.oracle_philox4x32_10.restype = None
+            L.oracle_gibbs_uniform.argtypes = [C.c_uint64, C.c_int32, C.c_int32, C.c_int64, C.c_uint32]
+            L.oracle_gibbs_uniform.restype = C.c_double
+            L.oracle_graph.argtypes = [C.c_int32, P, P, P, P, P, P, P]
+            L.oracle_graph.restype = C.c_int
+            L.oracle_moral.argtypes = [C.c_int32, P, P, P, P]
+            L.oracle_moral.restype = C.c_int
+            L.oracle_conditional.argtypes = [C.c_int32, P, P, P, P, P, C.c_int32, P]
+            L.oracle_conditional.restype = C.c_int
+            L.oracle_draw.argtypes = [P, C.c_int32, C.c_double, P]
+            L.oracle_draw.restype = C.c_int32
+            L.oracle_sweep.argtypes = [
+                C.c_int32, P, P, P, P, P, C.c_int32, P, P, C.c_int32, C.c_int64, C.c_int64,
+                C.c_int64, C.c_uint64, C.c_uint32, P, C.c_int64, C.c_int64, P, C.c_int32,
+                C.c_int32,
+            ]
+            L.oracle_sweep.restype = C.c_int64
+            L.oracle_counts.argtypes = [
+                C.c_int32, P, P, P, C.c_int32, P, C.c_int32, C.c_int64, C.c_int64, P, C.c_int32,
+            ]
+            L.oracle_counts.restype = C.c_int
+            L.oracle_gamma.argtypes = [C.c_double, C.c_uint64, C.c_uint32, C.c_uint32, P]
+            L.oracle_gamma.restype = C.c_double
+            L.oracle_dirichlet.argtypes = [
+                C.c_int32, P, P, P, P, C.c_double, C.c_uint64, C.c_uint32, P, P,
+            ]
+            L.oracle_dirichlet.restype = C.c_int
+            _lib = L
+        return _lib
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+def _check(rc):
+    if rc < 0:
+        raise OracleError("oracle returned error %d" % rc)
+    return rc
+
+
+def _dag(parents, card):
+    """(parent_ptr, parent_idx, card) int32 arrays from a list of parent lists."""
+    pptr = np.zeros(len(parents) + 1, dtype=np.int32)
+    for i, ps in enumerate(parents):
+        pptr[i + 1] = pptr[i] + len(ps)
+    pidx = np.array([p for ps in parents for p in ps] or [0], dtype=np.int32)
+    return pptr, pidx, np.ascontiguousarray(card, dtype=np.int32)
+
+
+def _ptr(a):
+    return C.c_void_p(a.ctypes.data) if a is not None else None
+
+
+# ----------------------------------------------------------------------------
+# Philox
+
+
+def philox4x32_10(ctr, key):
+    c = np.ascontiguousarray(ctr, dtype=np.uint32)
+    k = np.ascontiguousarray(key, dtype=np.uint32)
+    out = np.zeros(4, dtype=np.uint32)
+    lib().oracle_philox4x32_10(_ptr(c), _ptr(k), _ptr(out))
+    return out
+
+
+def gibbs_uniform(seed, node, replica, gcol, sweep_id):
+    return lib().oracle_gibbs_uniform(int(seed), int(node), int(replica), int(gcol), int(sweep_id))
+
+
+# ----------------------------------------------------------------------------
+# Graph
+
+
+def graph(parents, card):
+    """Returns dict(cpt_off[n+1], topo[n], color[n], n_colors)."""
+    pptr, pidx, card = _dag(parents, card)
+    n = len(card)
+    off = np.zeros(n + 1, dtype=np.int64)
+    topo = np.zeros(n, dtype=np.int32)
+    color = np.zeros(n, dtype=np.int32)
+    nc = C.c_int32(0)
+    _check(lib().oracle_graph(n, _ptr(pptr), _ptr(pidx), _ptr(card), _ptr(off), _ptr(topo),
+                              _ptr(color), C.byref(nc)))
+    return {"cpt_off": off, "topo": topo, "color": color, "n_colors": nc.value}
+
+
+def graph_rc(parents_ptr, parents_idx, card):
+    """Raw return code of the oracle's graph validation (for error tests)."""
+    pptr = np.ascontiguousarray(parents_ptr, dtype=np.int32)
+    pidx = np.ascontiguousarray(parents_idx if len(parents_idx) else [0], dtype=np.int32)
+    card = np.ascontiguousarray(card, dtype=np.int32)
+    return lib().oracle_graph(len(card), _ptr(pptr), _ptr(pidx), _ptr(card), None, None, None, None)
+
+
+def moral_adjacency(parents, card):
+    pptr, pidx, card = _dag(parents, card)
+    n = len(card)
+    adj = np.zeros((n, n), dtype=np.uint8)
+    _check(lib().oracle_moral(n, _ptr(pptr), _ptr(pidx), _ptr(card), _ptr(adj)))
+    return adj.astype(bool)
+
+
+# ----------------------------------------------------------------------------
+# Conditional and draw
+
+
+def conditional(parents, card, theta, x, node):
+    pptr, pidx, card = _dag(parents, card)
+    th = np.ascontiguousarray(theta, dtype=np.float32)
+    xv = np.ascontiguousarray(x, dtype=np.int32)
+    p = np.zeros(int(card[node]), dtype=np.float64)
+    _check(lib().oracle_conditional(len(card), _ptr(pptr), _ptr(pidx), _ptr(card), _ptr(th),
+                                    _ptr(xv), int(node), _ptr(p)))
+    return p
+
+
+def draw(weights, u):
+    w = np.ascontiguousarray(weights, dtype=np.float64)
+    f = C.c_int32(0)
+    k = lib().oracle_draw(_ptr(w), len(w), float(u), C.byref(f))
+    return int(k), bool(f.value)
+
+
+# ----------------------------------------------------------------------------
+# Sweep, counts, Dirichlet
+
+
+def sweep(parents, card, theta, color, states, obs, m, n_cols, col_offset, seed, sweep_id,
+          want_flags=False, win=None, n_threads=0):
+    """One sweep over one minibatch; ``states`` ([n][m][ld] int8/int16) is updated in place.
+
+    Returns dict(draws, flags (or None), probs (or None)).
+    ``win`` = (win_begin, win_len) asks for the conditionals of those columns.
+    """
+    pptr, pidx, card = _dag(parents, card)
+    th = np.ascontiguousarray(theta, dtype=np.float32)
+    col = np.ascontiguousarray(color, dtype=np.int32)
+    assert states.flags.c_contiguous and obs.flags.c_contiguous
+    n = len(card)
+    ld = states.shape[-1]
+    assert states.shape == (n, m, ld) and obs.shape == (n, ld)
+    sb = states.dtype.itemsize
+    flags = np.zeros(states.shape, dtype=np.uint8) if want_flags else None
+    probs = None
+    wb, wl, kmax = 0, 0, 1
+    if win is not None:
+        wb, wl = int(win[0]), int(win[1])
+        kmax = int(card.max())
+        probs = np.full((n, m, wl, kmax), np.nan, dtype=np.float64)
+    draws = lib().oracle_sweep(
+        n, _ptr(pptr), _ptr(pidx), _ptr(card), _ptr(th), _ptr(col), sb, _ptr(states), _ptr(obs),
+        int(m), int(n_cols), int(ld), int(col_offset), int(seed), int(sweep_id), _ptr(flags),
+        wb, wl, _ptr(probs), kmax, int(n_threads))
+    _check(draws)
+    return {"draws": int(draws), "flags": flags, "probs": probs}
+
+
+def counts(parents, card, states, m, n_cols, n_threads=0):
+    pptr, pidx, card = _dag(parents, card)
+    n = len(card)
+    ld = states.shape[-1]
+    assert states.shape == (n, m, ld) and states.flags.c_contiguous
+    total = graph(parents, card)["cpt_off"][-1]
+    out = np.zeros(int(total), dtype=np.int64)
+    _check(lib().oracle_counts(n, _ptr(pptr), _ptr(pidx), _ptr(card), states.dtype.itemsize,
+                               _ptr(states), int(m), int(n_cols), int(ld), _ptr(out),
+                               int(n_threads)))
+    return out
+
+
+def gamma(shape, seed, entry, update_id):
+    att = C.c_int32(0)
+    g = lib().oracle_gamma(float(shape), int(seed), int(entry), int(update_id), C.byref(att))
+    return g, att.value
+
+
+def dirichlet(parents, card, totals, alpha, seed, update_id, want_gamma=False):
+    pptr, pidx, card = _dag(parents, card)
+    tot = np.ascontiguousarray(totals, dtype=np.int64)
+    theta = np.zeros(len(tot), dtype=np.float32)
+    gv = np.zeros(len(tot), dtype=np.float64) if want_gamma else None
+    _check(lib().oracle_dirichlet(len(card), _ptr(pptr), _ptr(pidx), _ptr(card), _ptr(tot),
+                                  float(alpha), int(seed), int(update_id), _ptr(theta), _ptr(gv)))
+    return (theta, gv) if want_gamma else theta
+
+
+def moving_sum(totals, mb_prev, new):
+    """Exact moving sum of the per-minibatch counts (Sec. 4): subtract this
+    minibatch's previous counts from the total, add its new counts."""
+    return totals - mb_prev + new
