@@ -1,0 +1,218 @@
+"""Benchmark of one SAME Gibbs pass on one MI355X.
+
+Workload (default): the 1000-node random DAG, 2,000,000 columns in eight
+250,000-column minibatches, 40% of entries hidden, m = 10 SAME replicas; all
+minibatches resident in HBM (20 GB of int8 states + 2 GB of obs masks) when
+timing starts.  One step = one pass over all minibatches; per minibatch the
+library runs the colour-group sweep, the counts with their exact moving sum
+and the Dirichlet resample of every CPT row (the whole hot path).
+
+Prints one JSON line: node-samples/s (every (node, column, replica) slot of a
+pass), the sweep kernels' roofline figures measured with HIP events on the
+launch stream, and the oracle's rate on a bounded sample of the same workload
+timed on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "Gibbs node-samples/sec (incl. SAME replicas) + achieved HBM GB/s, 1 GPU"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=3)
+    p.add_argument("--warmup", type=int, default=1)
+    p.add_argument("--cfg", type=int, default=5)
+    p.add_argument("--n-cols", type=int, default=None, help="override the column count")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-sample-cols", type=int, default=32768)
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="also run a plain 1 GiB device copy (for HBM counter scaling)")
+    return p.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
+              "(see the design notes for how the sampler would shard columns)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_1511_06416_amd as same
+    from workloads import CONFIGS, make_workload
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    same.load_library()
+
+    t0 = time.time()
+    w = make_workload(args.cfg, n_cols=args.n_cols, device=dev)
+    torch.cuda.synchronize()
+    log("generated %s on the GPU in %.1f s: n=%d N=%d m=%d nb=%d M=%d ld=%d" % (
+        w.name, time.time() - t0, w.net.n, w.n_cols, w.m, w.nb, w.M, w.ld))
+    net = w.net
+    # the oracle's sample is taken from the generator's output, before any sweep
+    sample = None
+    if not args.no_cpu_baseline:
+        cols = min(args.cpu_sample_cols, w.mb_cols(0))
+        cols4 = (cols + 3) // 4 * 4
+        sample = (cols, np.ascontiguousarray(w.states[0][:, :, :cols4].cpu().numpy()),
+                  np.ascontiguousarray(w.obs[0][:, :cols4].cpu().numpy()))
+    pptr, pidx, card = net.csr()
+    ctx = same.same_create(pptr, pidx, card, w.alpha)
+    ws = ctx.new_workspace(dev)
+    cpts = torch.from_numpy(w.init_theta).to(dev)
+    mb = torch.zeros((w.M, ctx.cpt_total), dtype=torch.int32, device=dev)
+    tot = torch.zeros(ctx.cpt_total, dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream()
+    latent = sum(int((o[:, :w.mb_cols(b)] == 0).sum().item()) for b, o in enumerate(w.obs))
+    hidden = latent / float(net.n * w.n_cols)
+
+    # count-only pre-pass initialises the per-minibatch counts and their sum
+    for b in range(w.M):
+        same.same_counts(ctx, w.states[b], w.m, w.mb_cols(b), w.ld, mb[b], tot, ws)
+
+    sweep_ev = []
+
+    def one_pass(s, record):
+        for b in range(w.M):
+            if record:
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+            same.same_sweep(ctx, w.states[b], w.obs[b], cpts, w.m, w.mb_cols(b), w.ld,
+                            b * w.nb, w.seed, s, ws)
+            if record:
+                e1.record(stream)
+                sweep_ev.append((e0, e1))
+            same.same_counts(ctx, w.states[b], w.m, w.mb_cols(b), w.ld, mb[b], tot, ws)
+            same.same_sample_cpts(ctx, tot, cpts, w.seed, s * w.M + b, ws)
+
+    for s in range(args.warmup):
+        one_pass(s, False)
+    torch.cuda.synchronize()
+    log("warmup done")
+    t_start = time.perf_counter()
+    ev_start = torch.cuda.Event(enable_timing=True)
+    ev_end = torch.cuda.Event(enable_timing=True)
+    ev_start.record(stream)
+    for s in range(args.warmup, args.warmup + args.steps):
+        one_pass(s, True)
+    ev_end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    gpu_ms = ev_start.elapsed_time(ev_end)
+    elapsed = max(wall, gpu_ms / 1e3)
+    log("timed %d passes: wall %.3f s, events %.3f s" % (args.steps, wall, gpu_ms / 1e3))
+
+    node_samples = float(net.n) * w.n_cols * w.m * args.steps
+    value = node_samples / elapsed
+    sweep_s = sum(a.elapsed_time(b) for a, b in sweep_ev) / 1e3
+    launches = ctx.n_colors * w.M * args.steps
+    bytes_per_ns = 1.0 + hidden + 1.0 / w.m   # read each state, write each latent, obs per column
+    alg_bytes = node_samples * bytes_per_ns
+    achieved = alg_bytes / sweep_s / 1e9
+    roofline = {
+        "kernel": "sweep_color_kernel (all colour groups)",
+        "bound": "hbm",
+        "achieved": round(achieved, 1),
+        "peak": HBM_PEAK_GBS,
+        "unit": "GB/s",
+        "frac": round(achieved / HBM_PEAK_GBS, 4),
+        "traffic": None,
+        "bytes_per_node_sample": round(bytes_per_ns, 4),
+        "launches": launches,
+        "avg_launch_ms": round(sweep_s * 1e3 / launches, 4),
+        "sweep_share_of_step": round(sweep_s / elapsed, 3),
+    }
+
+    if args.copy_calibration:
+        a = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        b2 = torch.empty_like(a)
+        b2.copy_(a)
+        torch.cuda.synchronize()
+        del a, b2
+
+    cpu = None
+    if sample is not None:
+        cpu = cpu_baseline(w, *sample)
+
+    spec = CONFIGS[args.cfg]
+    out = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "node-samples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(elapsed * 1e3 / args.steps, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": "%s: %d-node random DAG, 0-%d parents, K in {%d..%d}, %d columns in "
+                        "%d-column minibatches resident in HBM, %.0f%% hidden, SAME m=%d" % (
+                            w.name, net.n, spec["graph"][2] if spec["graph"][0] == "random" else 0,
+                            int(net.card.min()), int(net.card.max()), w.n_cols, w.nb,
+                            100 * w.hidden, w.m) if args.cfg in (3, 5) else w.name,
+            "global_batch": w.n_cols,
+            "minibatch_cols": w.nb,
+            "replicas": w.m,
+            "nodes": net.n,
+            "colors": ctx.n_colors,
+            "hidden_fraction": round(hidden, 4),
+            "parallelism": "single-gpu",
+        },
+        "latent_draws_per_s": round(value * hidden, 1),
+        "hbm_gbs_algorithmic_step": round(alg_bytes / elapsed / 1e9, 1),
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(w, cols, st, ob):
+    """The oracle (fp64, OpenMP over columns) on the first `cols` columns of
+    minibatch 0 as generated: one sweep, its counts and one Dirichlet resample."""
+    import oracle
+
+    net = w.net
+    threads = len(os.sched_getaffinity(0))
+    color = oracle.graph(net.parents, net.card)["color"]
+    t = time.perf_counter()
+    oracle.sweep(net.parents, net.card, w.init_theta, color, st, ob, w.m, cols, 0, w.seed, 0,
+                 n_threads=threads)
+    cnt = oracle.counts(net.parents, net.card, st, w.m, cols, n_threads=threads)
+    oracle.dirichlet(net.parents, net.card, cnt, w.alpha, w.seed, 0)
+    dt = time.perf_counter() - t
+    ns = float(net.n) * cols * w.m
+    log("cpu baseline: %d columns, %.2f s, %d threads" % (cols, dt, threads))
+    return {"value": round(ns / dt, 1), "unit": "node-samples/s", "cores": threads,
+            "kind": "oracle",
+            "sample": "first %d columns of minibatch 0 (all %d nodes, m=%d): one sweep + counts "
+                      "+ one Dirichlet resample, %.1f s" % (cols, net.n, w.m, dt)}
+
+
+if __name__ == "__main__":
+    main()

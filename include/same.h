@@ -1,0 +1,169 @@
+/*
+ * same.h -- C ABI of libsame, an MI355X (gfx950) implementation of SAME Gibbs
+ * sampling for discrete Bayesian networks (Seita, Chen & Canny, arXiv
+ * 1511.06416).
+ *
+ * The problem (Sec. 1): a Bayesian network of known structure whose nodes take
+ * discrete states and whose conditional probability tables (CPTs) Theta are
+ * unknown; the data are a node x case matrix in which some entries are
+ * missing.  The sampler draws the missing states Z and the CPTs from
+ * P(Z, Theta | D).  SAME (Sec. 3, Eq. 1) replicates the latent states m times,
+ * all tied to one Theta.  The data are processed in same-sized minibatches of
+ * columns (Sec. 4); per minibatch the library runs one chromatic Gibbs sweep
+ * over the m replicas (Sec. 4, colour groups of the moralized graph visited
+ * in order), counts (parent configuration, state) pairs, keeps the exact
+ * moving sum of the per-minibatch counts, and resamples every CPT row from
+ * Dirichlet(prior + counts).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Graph:  nodes 0..n-1; parent lists in CSR form (parent_ptr[n+1],
+ *         parent_idx[parent_ptr[n]]).  The listed parent order fixes the CPT
+ *         row radix: row u = sum_j x_{pa_j} * stride_j with the LAST listed
+ *         parent fastest.
+ * CPTs:   one flat fp32 array of cpt_total entries; node i owns
+ *         [cpt_off[i], cpt_off[i+1]) = R_i rows of K_i entries, entry
+ *         cpt_off[i] + u*K_i + k = P(x_i = k | parents in configuration u).
+ * States: device array [n][m][ld] of int8 (every K_i <= 127) or int16
+ *         (some K_i >= 128), node-major, then replica, then column; column j
+ *         of a minibatch is global column col_offset + j.  Observed entries
+ *         must hold the observed value in every replica.  Values must lie in
+ *         [0, K_i) (out-of-range values are undefined behaviour).
+ * Obs:    device array [n][ld] of uint8, 1 = observed, 0 = latent; shared by
+ *         the m replicas.  Columns [n_cols, ld) are never drawn or counted.
+ * Counts: int32, laid out like the CPTs.
+ * Memory: the caller owns every state, obs, CPT, count and workspace buffer
+ *         (device memory; PyTorch tensors in the Python binding).  The
+ *         library owns only the context and its small per-device structure
+ *         tables, uploaded synchronously on the first device call.
+ * Streams: `stream` is a hipStream_t passed as void* (NULL = null stream);
+ *         device work is enqueued asynchronously on it.  Argument errors are
+ *         detected and returned before anything is enqueued.
+ * Errors: functions return SAME_OK (0) or a negative SAME_E* code;
+ *         same_last_error() gives a message for the calling thread's last
+ *         failure.  A context is used by one host thread at a time.
+ * Random numbers: Philox4x32-10 (Salmon et al., SC'11) keyed by the 64-bit
+ *         seed; the Gibbs draw of node i, replica r, global column g in sweep
+ *         s takes word g&3 of the block at counter {g>>2, i, r, s}; the Gamma
+ *         attempt t of CPT entry e at update q uses counter {e, t, 1<<24, q}.
+ */
+#ifndef SAME_H
+#define SAME_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct same_ctx same_ctx;
+
+enum {
+    SAME_OK = 0,
+    SAME_EINVAL = -1,  /* bad argument (null pointer, m < 1, n_cols > ld, ...) */
+    SAME_EGRAPH = -2,  /* cycle, self-loop, duplicate or out-of-range parent */
+    SAME_ECARD = -3,   /* a cardinality outside [2, 32767] */
+    SAME_ESIZE = -4,   /* a size that overflows the library's int32 indexing */
+    SAME_ENOMEM = -5,  /* host or device allocation failed */
+    SAME_EHIP = -6,    /* a HIP runtime call failed (message has the HIP error) */
+    SAME_EALIGN = -7   /* col_offset or ld not a multiple of 4, misaligned pointer */
+};
+
+typedef struct {
+    int32_t n_nodes;
+    int32_t n_colors;     /* colour groups of the moralized graph */
+    int64_t cpt_total;    /* CPT entries */
+    int64_t n_rows;       /* CPT rows (distributions) */
+    int32_t state_bytes;  /* 1: int8 states, 2: int16 states */
+    int32_t max_card;     /* largest K_i */
+} same_layout_t;
+
+/*
+ * Builds a context for one network (Sec. 1 problem statement; Sec. 4 colour
+ * groups).  Host only: validates the DAG, orders it topologically, builds the
+ * moralized graph (parents joined, directions dropped), colours it first-fit
+ * over a Kahn topological order that takes the smallest ready id, lays out
+ * the CPTs and the per-node Markov-blanket tables.  dirichlet_prior (> 0) is
+ * the Dirichlet parameter added to every count in same_sample_cpts.  The
+ * arrays are copied; the caller may free them after the call.
+ */
+int same_create(int32_t n_nodes, const int32_t *parent_ptr, const int32_t *parent_idx,
+                const int32_t *card, double dirichlet_prior, same_ctx **out);
+
+/* Frees the context and its device tables (on every device it used). */
+void same_destroy(same_ctx *ctx);
+
+/*
+ * Copies out the layout; cpt_off (n+1 entries) and color (n entries) are
+ * optional.  Host only.
+ */
+int same_layout(const same_ctx *ctx, same_layout_t *out, int64_t *cpt_off, int32_t *color);
+
+/*
+ * Bytes of device workspace that same_sweep, same_sweep_debug, same_counts
+ * and same_sample_cpts need (one buffer serves all of them; 256-byte aligned
+ * base required).  The workspace holds the sweep's regrouped CPT tables, the
+ * new-count histogram and the fp64 Gamma variates; its contents need not be
+ * preserved between calls.  Host only.
+ */
+int same_workspace_size(const same_ctx *ctx, size_t *bytes);
+
+/*
+ * One chromatic Gibbs sweep over one minibatch, in place (Sec. 4: colour
+ * groups in ascending order; inside a group every (node, column, replica) is
+ * independent).  For every latent entry the full conditional
+ *   P(x_i = k | rest) ~ theta_i(k | x_pa(i)) * prod_{h in ch(i)} theta_h(x_h | x_pa(h), x_i = k)
+ * is formed in fp32 from max(theta, FLT_MIN) and a state is drawn by inverse
+ * CDF: with S_k the running sum of the weights and Z = S_{K-1}, the smallest
+ * k with u*Z < S_k, else the largest k with positive weight.
+ * states [n][m][ld] (in/out), obs [n][ld], cpts [cpt_total]: device pointers.
+ * col_offset and ld must be multiples of 4 and states/obs 4-byte aligned.
+ * seed and sweep_id select the Philox stream.  The colour groups launch in
+ * order on `stream`.
+ */
+int same_sweep(same_ctx *ctx, void *states, const uint8_t *obs, const float *cpts, int32_t m,
+               int64_t n_cols, int64_t ld, int64_t col_offset, uint64_t seed, uint32_t sweep_id,
+               void *workspace, void *stream);
+
+/*
+ * same_sweep that also writes the fp32 conditionals of columns
+ * [win_begin, win_begin + win) to probs[((i*m + r)*win + (j - win_begin))*max_card + k]
+ * (device pointer, n*m*win*max_card floats); entries of observed columns and
+ * k >= K_i are left untouched.  For parity checks.
+ */
+int same_sweep_debug(same_ctx *ctx, void *states, const uint8_t *obs, const float *cpts,
+                     int32_t m, int64_t n_cols, int64_t ld, int64_t col_offset, uint64_t seed,
+                     uint32_t sweep_id, int64_t win_begin, int64_t win, float *probs,
+                     void *workspace, void *stream);
+
+/*
+ * Sufficient statistics and their moving sum (Sec. 4): histogram of
+ * (parent configuration, state) over columns [0, n_cols) and all m replicas of
+ * states [n][m][ld].  mb_counts [cpt_total] holds this minibatch's previous
+ * counts on entry (zeros on its first visit) and its new counts on return;
+ * totals [cpt_total] (nullable) += new - previous.  Device pointers.  Counts
+ * are exact (integer) and independent of launch order; n_cols * m * (number
+ * of minibatches) must stay below 2^31.
+ */
+int same_counts(same_ctx *ctx, const void *states, int32_t m, int64_t n_cols, int64_t ld,
+                int32_t *mb_counts, int32_t *totals, void *workspace, void *stream);
+
+/*
+ * Dirichlet resample of every CPT row (Sec. 4: counts plus the Dirichlet
+ * prior are the Dirichlet parameters from which the CPTs are sampled):
+ * g_e ~ Gamma(prior + totals[e], 1) (Marsaglia & Tsang, in fp64), then
+ * cpts_out[e] = fp32(g_e / sum of g over e's row).  update_id selects the
+ * Philox stream (one id per resample).  Device pointers.
+ */
+int same_sample_cpts(same_ctx *ctx, const int32_t *totals, float *cpts_out, uint64_t seed,
+                     uint32_t update_id, void *workspace, void *stream);
+
+/* Message for the calling thread's last failed call ("" if none). */
+const char *same_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SAME_H */

@@ -1,0 +1,191 @@
+"""MI355X (gfx950) SAME Gibbs sampling for discrete Bayesian networks.
+
+A thin ctypes binding over ``libsame.so`` (C ABI declared in
+``include/same.h``).  The functions carry the C names and only marshal
+arguments: tensors become device pointers, the stream defaults to torch's
+current stream.  Every step of the sampler runs in the library's HIP
+kernels; there is no Python or CPU fallback, and calling anything here
+without the built library raises ``SameError``.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import threading
+
+import numpy as np
+
+__all__ = [
+    "SameError", "Context", "same_create", "same_destroy", "same_layout", "same_workspace_size",
+    "same_sweep", "same_sweep_debug", "same_counts", "same_sample_cpts", "same_last_error",
+    "library_path", "load_library",
+]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "libsame.so")
+_lock = threading.Lock()
+_lib = None
+
+SAME_OK, SAME_EINVAL, SAME_EGRAPH, SAME_ECARD, SAME_ESIZE, SAME_ENOMEM, SAME_EHIP, SAME_EALIGN = (
+    0, -1, -2, -3, -4, -5, -6, -7)
+_NAMES = {0: "SAME_OK", -1: "SAME_EINVAL", -2: "SAME_EGRAPH", -3: "SAME_ECARD",
+          -4: "SAME_ESIZE", -5: "SAME_ENOMEM", -6: "SAME_EHIP", -7: "SAME_EALIGN"}
+
+
+class SameError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__("%s (%d): %s" % (_NAMES.get(code, "?"), code, msg))
+        self.code = code
+
+
+class _Layout(C.Structure):
+    _fields_ = [("n_nodes", C.c_int32), ("n_colors", C.c_int32), ("cpt_total", C.c_int64),
+                ("n_rows", C.c_int64), ("state_bytes", C.c_int32), ("max_card", C.c_int32)]
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def load_library():
+    """Loads libsame.so; raises SameError if it has not been built."""
+    global _lib
+    with _lock:
+        if _lib is not None:
+            return _lib
+        if not os.path.exists(_LIB_PATH):
+            raise SameError(SAME_EINVAL, "libsame.so is not built (run __graft_entry__.build())")
+        L = C.CDLL(_LIB_PATH)
+        P, I32, I64, U64, U32 = C.c_void_p, C.c_int32, C.c_int64, C.c_uint64, C.c_uint32
+        L.same_create.argtypes = [I32, P, P, P, C.c_double, C.POINTER(P)]
+        L.same_destroy.argtypes = [P]
+        L.same_destroy.restype = None
+        L.same_layout.argtypes = [P, C.POINTER(_Layout), P, P]
+        L.same_workspace_size.argtypes = [P, C.POINTER(C.c_size_t)]
+        L.same_sweep.argtypes = [P, P, P, P, I32, I64, I64, I64, U64, U32, P, P]
+        L.same_sweep_debug.argtypes = [P, P, P, P, I32, I64, I64, I64, U64, U32, I64, I64, P, P, P]
+        L.same_counts.argtypes = [P, P, I32, I64, I64, P, P, P, P]
+        L.same_sample_cpts.argtypes = [P, P, P, U64, U32, P, P]
+        L.same_last_error.argtypes = []
+        L.same_last_error.restype = C.c_char_p
+        for f in ("same_create", "same_layout", "same_workspace_size", "same_sweep",
+                  "same_sweep_debug", "same_counts", "same_sample_cpts"):
+            getattr(L, f).restype = C.c_int
+        _lib = L
+        return L
+
+
+def same_last_error() -> str:
+    return load_library().same_last_error().decode()
+
+
+def _check(rc):
+    if rc != SAME_OK:
+        raise SameError(rc, same_last_error())
+
+
+def _ptr(t):
+    """Device pointer of a tensor (or an int address, or None)."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return C.c_void_p(t)
+    return C.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, int):
+        return C.c_void_p(stream)
+    return C.c_void_p(stream.cuda_stream)
+
+
+class Context:
+    """Owns one same_ctx (one network)."""
+
+    def __init__(self, parent_ptr, parent_idx, card, dirichlet_prior=1.0):
+        L = load_library()
+        self._pptr = np.ascontiguousarray(parent_ptr, dtype=np.int32)
+        self._pidx = np.ascontiguousarray(parent_idx if len(parent_idx) else [0], dtype=np.int32)
+        self._card = np.ascontiguousarray(card, dtype=np.int32)
+        h = C.c_void_p()
+        _check(L.same_create(len(self._card), self._pptr.ctypes.data, self._pidx.ctypes.data,
+                             self._card.ctypes.data, float(dirichlet_prior), C.byref(h)))
+        self._h = h
+        lay = _Layout()
+        off = np.zeros(len(self._card) + 1, dtype=np.int64)
+        col = np.zeros(len(self._card), dtype=np.int32)
+        _check(L.same_layout(self._h, C.byref(lay), off.ctypes.data, col.ctypes.data))
+        self.n_nodes, self.n_colors = lay.n_nodes, lay.n_colors
+        self.cpt_total, self.n_rows = lay.cpt_total, lay.n_rows
+        self.state_bytes, self.max_card = lay.state_bytes, lay.max_card
+        self.cpt_off, self.color = off, col
+        ws = C.c_size_t()
+        _check(L.same_workspace_size(self._h, C.byref(ws)))
+        self.workspace_bytes = int(ws.value)
+
+    @property
+    def handle(self):
+        return self._h
+
+    def close(self):
+        if getattr(self, "_h", None) is not None and self._h.value:
+            load_library().same_destroy(self._h)
+            self._h = C.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def new_workspace(self, device="cuda"):
+        import torch
+        # torch's caching allocator returns >= 512-byte aligned blocks
+        return torch.empty(max(self.workspace_bytes, 1), dtype=torch.uint8, device=device)
+
+
+def same_create(parent_ptr, parent_idx, card, dirichlet_prior=1.0) -> Context:
+    return Context(parent_ptr, parent_idx, card, dirichlet_prior)
+
+
+def same_destroy(ctx: Context) -> None:
+    ctx.close()
+
+
+def same_layout(ctx: Context) -> dict:
+    return {"n_nodes": ctx.n_nodes, "n_colors": ctx.n_colors, "cpt_total": ctx.cpt_total,
+            "n_rows": ctx.n_rows, "state_bytes": ctx.state_bytes, "max_card": ctx.max_card,
+            "cpt_off": ctx.cpt_off.copy(), "color": ctx.color.copy()}
+
+
+def same_workspace_size(ctx: Context) -> int:
+    return ctx.workspace_bytes
+
+
+def same_sweep(ctx, states, obs, cpts, m, n_cols, ld, col_offset, seed, sweep_id, workspace,
+               stream=None):
+    _check(load_library().same_sweep(ctx.handle, _ptr(states), _ptr(obs), _ptr(cpts), int(m),
+                                     int(n_cols), int(ld), int(col_offset), int(seed),
+                                     int(sweep_id), _ptr(workspace), _stream(stream)))
+
+
+def same_sweep_debug(ctx, states, obs, cpts, m, n_cols, ld, col_offset, seed, sweep_id,
+                     win_begin, win, probs, workspace, stream=None):
+    _check(load_library().same_sweep_debug(ctx.handle, _ptr(states), _ptr(obs), _ptr(cpts), int(m),
+                                           int(n_cols), int(ld), int(col_offset), int(seed),
+                                           int(sweep_id), int(win_begin), int(win), _ptr(probs),
+                                           _ptr(workspace), _stream(stream)))
+
+
+def same_counts(ctx, states, m, n_cols, ld, mb_counts, totals, workspace, stream=None):
+    _check(load_library().same_counts(ctx.handle, _ptr(states), int(m), int(n_cols), int(ld),
+                                      _ptr(mb_counts), _ptr(totals), _ptr(workspace),
+                                      _stream(stream)))
+
+
+def same_sample_cpts(ctx, totals, cpts_out, seed, update_id, workspace, stream=None):
+    _check(load_library().same_sample_cpts(ctx.handle, _ptr(totals), _ptr(cpts_out), int(seed),
+                                           int(update_id), _ptr(workspace), _stream(stream)))

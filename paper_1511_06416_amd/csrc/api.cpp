@@ -1,0 +1,295 @@
+// C ABI of libsame (declared in include/same.h): argument validation, the
+// per-device structure tables, the workspace layout and the launch sequence of
+// each entry point.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/same.h"
+#include "graph.hpp"
+#include "launch.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int set_error(int code, const std::string &msg) {
+    g_last_error = msg;
+    return code;
+}
+
+constexpr size_t kAlign = 256;
+inline size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+}  // namespace
+
+struct same_ctx {
+    same::Compiled g;
+    double alpha = 1.0;
+    std::vector<same::DeviceTables> dev;  // indexed by device ordinal
+    std::mutex mu;
+    // workspace layout
+    size_t ws_table = 0, ws_counts = 0, ws_gamma = 0, ws_total = 0;
+};
+
+namespace {
+
+template <typename T>
+hipError_t upload(T **dst, const std::vector<T> &src) {
+    if (src.empty()) {
+        *dst = nullptr;
+        return hipSuccess;
+    }
+    hipError_t e = hipMalloc((void **)dst, src.size() * sizeof(T));
+    if (e != hipSuccess) return e;
+    return hipMemcpy(*dst, src.data(), src.size() * sizeof(T), hipMemcpyHostToDevice);
+}
+
+void free_tables(same::DeviceTables &t) {
+    if (t.device < 0) return;
+    int cur = -1;
+    (void)hipGetDevice(&cur);
+    (void)hipSetDevice(t.device);
+    void *ptrs[] = {t.desc, t.desc_off, t.order, t.cdesc, t.cdesc_off, t.segs,
+                    t.blk_seg, t.blk_first, t.row_off, t.row_k};
+    for (void *p : ptrs)
+        if (p) (void)hipFree(p);
+    if (cur >= 0) (void)hipSetDevice(cur);
+    t = same::DeviceTables();
+}
+
+// Device tables of the current device, uploaded on first use (synchronous).
+int tables_for_current_device(same_ctx *ctx, same::DeviceTables **out) {
+    int device = -1;
+    hipError_t e = hipGetDevice(&device);
+    if (e != hipSuccess) return set_error(SAME_EHIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+    std::lock_guard<std::mutex> lock(ctx->mu);
+    if ((int)ctx->dev.size() <= device) ctx->dev.resize(device + 1);
+    same::DeviceTables &t = ctx->dev[device];
+    if (t.device == device) {
+        *out = &t;
+        return SAME_OK;
+    }
+    const same::Compiled &g = ctx->g;
+    // table-build block map: each segment gets ceil(n_groups / 256) blocks
+    std::vector<int32_t> blk_seg, blk_first;
+    for (size_t s = 0; s < g.segments.size(); ++s)
+        for (int32_t f = 0; f < g.segments[s].n_groups; f += 256) {
+            blk_seg.push_back((int32_t)s);
+            blk_first.push_back(f);
+        }
+    same::DeviceTables nt;
+    nt.device = device;
+    nt.n_build_blocks = (int32_t)blk_seg.size();
+    hipError_t r = hipSuccess;
+    if (r == hipSuccess) r = upload(&nt.desc, g.desc);
+    if (r == hipSuccess) r = upload(&nt.desc_off, g.desc_off);
+    if (r == hipSuccess) r = upload(&nt.order, g.order);
+    if (r == hipSuccess) r = upload(&nt.cdesc, g.cdesc);
+    if (r == hipSuccess) r = upload(&nt.cdesc_off, g.cdesc_off);
+    if (r == hipSuccess) r = upload(&nt.segs, g.segments);
+    if (r == hipSuccess) r = upload(&nt.blk_seg, blk_seg);
+    if (r == hipSuccess) r = upload(&nt.blk_first, blk_first);
+    if (r == hipSuccess) r = upload(&nt.row_off, g.row_off);
+    if (r == hipSuccess) r = upload(&nt.row_k, g.row_k);
+    if (r != hipSuccess) {
+        free_tables(nt);
+        return set_error(r == hipErrorOutOfMemory ? SAME_ENOMEM : SAME_EHIP,
+                         std::string("uploading structure tables: ") + hipGetErrorString(r));
+    }
+    t = nt;
+    *out = &t;
+    return SAME_OK;
+}
+
+int check_hip(hipError_t e, const char *what) {
+    if (e == hipSuccess) return SAME_OK;
+    return set_error(SAME_EHIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+int check_minibatch(const same_ctx *ctx, const void *states, int32_t m, int64_t n_cols, int64_t ld) {
+    if (!ctx) return set_error(SAME_EINVAL, "ctx is null");
+    if (!states) return set_error(SAME_EINVAL, "states is null");
+    if (m < 1 || m > 65535) return set_error(SAME_EINVAL, "m must be in [1, 65535]");
+    if (n_cols < 0 || ld < n_cols) return set_error(SAME_EINVAL, "need 0 <= n_cols <= ld");
+    if (ld % 4 != 0) return set_error(SAME_EALIGN, "ld must be a multiple of 4");
+    if (!aligned(states, 4 * (size_t)ctx->g.state_bytes))
+        return set_error(SAME_EALIGN, "states must be aligned to 4 state elements");
+    if ((double)ctx->g.n * (double)m * (double)ld * ctx->g.state_bytes > 9.0e18)
+        return set_error(SAME_ESIZE, "states array too large");
+    return SAME_OK;
+}
+
+int do_sweep(same_ctx *ctx, void *states, const uint8_t *obs, const float *cpts, int32_t m,
+             int64_t n_cols, int64_t ld, int64_t col_offset, uint64_t seed, uint32_t sweep_id,
+             int64_t win_begin, int64_t win, float *probs, void *workspace, void *stream) {
+    int rc = check_minibatch(ctx, states, m, n_cols, ld);
+    if (rc) return rc;
+    if (!obs || !cpts || !workspace) return set_error(SAME_EINVAL, "obs, cpts and workspace must be non-null");
+    if (col_offset < 0 || col_offset % 4 != 0)
+        return set_error(SAME_EALIGN, "col_offset must be a non-negative multiple of 4");
+    if (((col_offset + n_cols) >> 2) > (int64_t)0xFFFFFFFFll)
+        return set_error(SAME_ESIZE, "global column index exceeds the Philox counter range");
+    if (!aligned(obs, 4)) return set_error(SAME_EALIGN, "obs must be 4-byte aligned");
+    if (!aligned(workspace, kAlign)) return set_error(SAME_EALIGN, "workspace must be 256-byte aligned");
+    if (win > 0) {
+        if (!probs) return set_error(SAME_EINVAL, "probs is null");
+        if (win_begin < 0) return set_error(SAME_EINVAL, "win_begin must be >= 0");
+    }
+    if (n_cols == 0) return SAME_OK;
+    same::DeviceTables *t = nullptr;
+    rc = tables_for_current_device(ctx, &t);
+    if (rc) return rc;
+    hipStream_t s = (hipStream_t)stream;
+    float *table = (float *)((char *)workspace + ctx->ws_table);
+    rc = check_hip(same::launch_build_tables(*t, cpts, table, s), "table build launch");
+    if (rc) return rc;
+    same::SweepArgs a;
+    a.t = t;
+    a.table = table;
+    a.states = states;
+    a.obs = obs;
+    a.m = m;
+    a.n_cols = n_cols;
+    a.ld = ld;
+    a.col_offset = col_offset;
+    a.key0 = (uint32_t)seed;
+    a.key1 = (uint32_t)(seed >> 32);
+    a.sweep_id = sweep_id;
+    a.win_begin = win_begin;
+    a.win = win > 0 ? win : 0;
+    a.probs = probs;
+    a.max_card = ctx->g.max_card;
+    const same::Compiled &g = ctx->g;
+    for (int32_t c = 0; c < g.n_colors; ++c) {
+        rc = check_hip(same::launch_sweep_color(a, g.color_start[c], g.color_start[c + 1] - g.color_start[c],
+                                                g.color_kp[c], g.state_bytes, s),
+                       "sweep launch");
+        if (rc) return rc;
+    }
+    return SAME_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *same_last_error(void) { return g_last_error.c_str(); }
+
+int same_create(int32_t n_nodes, const int32_t *parent_ptr, const int32_t *parent_idx,
+                const int32_t *card, double dirichlet_prior, same_ctx **out) {
+    if (!out) return set_error(SAME_EINVAL, "out is null");
+    *out = nullptr;
+    if (!(dirichlet_prior > 0.0)) return set_error(SAME_EINVAL, "dirichlet_prior must be > 0");
+    same_ctx *ctx = new (std::nothrow) same_ctx();
+    if (!ctx) return set_error(SAME_ENOMEM, "out of host memory");
+    std::string err;
+    int rc;
+    try {
+        rc = same::compile_graph(n_nodes, parent_ptr, parent_idx, card, ctx->g, err);
+    } catch (const std::bad_alloc &) {
+        rc = SAME_ENOMEM;
+        err = "out of host memory";
+    }
+    if (rc) {
+        delete ctx;
+        return set_error(rc, err);
+    }
+    ctx->alpha = dirichlet_prior;
+    ctx->ws_table = 0;
+    ctx->ws_counts = align_up(ctx->ws_table + (size_t)ctx->g.table_floats * sizeof(float));
+    ctx->ws_gamma = align_up(ctx->ws_counts + (size_t)ctx->g.off[n_nodes] * sizeof(int32_t));
+    ctx->ws_total = align_up(ctx->ws_gamma + (size_t)ctx->g.off[n_nodes] * sizeof(double));
+    *out = ctx;
+    return SAME_OK;
+}
+
+void same_destroy(same_ctx *ctx) {
+    if (!ctx) return;
+    for (auto &t : ctx->dev) free_tables(t);
+    delete ctx;
+}
+
+int same_layout(const same_ctx *ctx, same_layout_t *out, int64_t *cpt_off, int32_t *color) {
+    if (!ctx || !out) return set_error(SAME_EINVAL, "ctx and out must be non-null");
+    const same::Compiled &g = ctx->g;
+    out->n_nodes = g.n;
+    out->n_colors = g.n_colors;
+    out->cpt_total = g.off[g.n];
+    out->n_rows = g.n_rows;
+    out->state_bytes = g.state_bytes;
+    out->max_card = g.max_card;
+    if (cpt_off) std::memcpy(cpt_off, g.off.data(), sizeof(int64_t) * (g.n + 1));
+    if (color) std::memcpy(color, g.color.data(), sizeof(int32_t) * g.n);
+    return SAME_OK;
+}
+
+int same_workspace_size(const same_ctx *ctx, size_t *bytes) {
+    if (!ctx || !bytes) return set_error(SAME_EINVAL, "ctx and bytes must be non-null");
+    *bytes = ctx->ws_total;
+    return SAME_OK;
+}
+
+int same_sweep(same_ctx *ctx, void *states, const uint8_t *obs, const float *cpts, int32_t m,
+               int64_t n_cols, int64_t ld, int64_t col_offset, uint64_t seed, uint32_t sweep_id,
+               void *workspace, void *stream) {
+    return do_sweep(ctx, states, obs, cpts, m, n_cols, ld, col_offset, seed, sweep_id, 0, 0, nullptr,
+                    workspace, stream);
+}
+
+int same_sweep_debug(same_ctx *ctx, void *states, const uint8_t *obs, const float *cpts,
+                     int32_t m, int64_t n_cols, int64_t ld, int64_t col_offset, uint64_t seed,
+                     uint32_t sweep_id, int64_t win_begin, int64_t win, float *probs,
+                     void *workspace, void *stream) {
+    if (win <= 0) return set_error(SAME_EINVAL, "win must be positive");
+    return do_sweep(ctx, states, obs, cpts, m, n_cols, ld, col_offset, seed, sweep_id, win_begin, win,
+                    probs, workspace, stream);
+}
+
+int same_counts(same_ctx *ctx, const void *states, int32_t m, int64_t n_cols, int64_t ld,
+                int32_t *mb_counts, int32_t *totals, void *workspace, void *stream) {
+    int rc = check_minibatch(ctx, states, m, n_cols, ld);
+    if (rc) return rc;
+    if (!mb_counts || !workspace) return set_error(SAME_EINVAL, "mb_counts and workspace must be non-null");
+    if (!aligned(workspace, kAlign)) return set_error(SAME_EALIGN, "workspace must be 256-byte aligned");
+    if ((double)n_cols * (double)m >= 2147483648.0)
+        return set_error(SAME_ESIZE, "n_cols * m must stay below 2^31");
+    same::DeviceTables *t = nullptr;
+    rc = tables_for_current_device(ctx, &t);
+    if (rc) return rc;
+    hipStream_t s = (hipStream_t)stream;
+    const int64_t total = ctx->g.off[ctx->g.n];
+    int32_t *newc = (int32_t *)((char *)workspace + ctx->ws_counts);
+    rc = check_hip(same::launch_fill_zero(newc, total, s), "count clear launch");
+    if (rc) return rc;
+    rc = check_hip(same::launch_counts(*t, states, ctx->g.state_bytes, ctx->g.n, m, n_cols, ld, newc, s),
+                   "count launch");
+    if (rc) return rc;
+    return check_hip(same::launch_moving_sum(newc, mb_counts, totals, total, s), "moving-sum launch");
+}
+
+int same_sample_cpts(same_ctx *ctx, const int32_t *totals, float *cpts_out, uint64_t seed,
+                     uint32_t update_id, void *workspace, void *stream) {
+    if (!ctx || !totals || !cpts_out || !workspace)
+        return set_error(SAME_EINVAL, "ctx, totals, cpts_out and workspace must be non-null");
+    if (!aligned(workspace, kAlign)) return set_error(SAME_EALIGN, "workspace must be 256-byte aligned");
+    same::DeviceTables *t = nullptr;
+    int rc = tables_for_current_device(ctx, &t);
+    if (rc) return rc;
+    hipStream_t s = (hipStream_t)stream;
+    const int64_t total = ctx->g.off[ctx->g.n];
+    double *gv = (double *)((char *)workspace + ctx->ws_gamma);
+    rc = check_hip(same::launch_gamma(totals, ctx->alpha, (uint32_t)seed, (uint32_t)(seed >> 32), update_id,
+                                      gv, total, s),
+                   "gamma launch");
+    if (rc) return rc;
+    return check_hip(same::launch_normalize(*t, gv, cpts_out, ctx->g.n_rows, s), "normalize launch");
+}
+
+}  // extern "C"

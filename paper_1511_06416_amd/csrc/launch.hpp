@@ -1,0 +1,63 @@
+// Internal launch interface between the C ABI (api.cpp) and the gfx950
+// kernels (kernels.hip).  Plain device pointers only.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <cstdint>
+
+#include "graph.hpp"
+
+namespace same {
+
+// Device copies of the compiled structure tables (one set per device).
+struct DeviceTables {
+    int device = -1;
+    int32_t *desc = nullptr;       // sweep descriptor stream
+    int32_t *desc_off = nullptr;   // [n]
+    int32_t *order = nullptr;      // colour-ordered nodes
+    int32_t *cdesc = nullptr;      // count descriptor stream: [K, n_par, nbins, cpt_off, (p, stride)*]
+    int32_t *cdesc_off = nullptr;  // [n]
+    Segment *segs = nullptr;
+    int32_t *blk_seg = nullptr;    // table-build block -> segment
+    int32_t *blk_first = nullptr;  // table-build block -> first group
+    int32_t n_build_blocks = 0;
+    int32_t *row_off = nullptr;    // [n_rows]
+    int32_t *row_k = nullptr;      // [n_rows]
+};
+
+struct SweepArgs {
+    const DeviceTables *t;
+    const float *table;     // regrouped k-vector tables (workspace)
+    void *states;
+    const uint8_t *obs;
+    int32_t m;
+    int64_t n_cols, ld, col_offset;
+    uint32_t key0, key1, sweep_id;
+    int64_t win_begin, win;  // debug window (win == 0: none)
+    float *probs;
+    int32_t max_card;
+};
+
+hipError_t launch_build_tables(const DeviceTables &t, const float *cpts, float *table,
+                               hipStream_t stream);
+
+// One colour group: nodes order[begin .. begin+count), all with KP <= kp.
+hipError_t launch_sweep_color(const SweepArgs &a, int32_t begin, int32_t count, int32_t kp,
+                              int32_t state_bytes, hipStream_t stream);
+
+hipError_t launch_fill_zero(int32_t *p, int64_t count, hipStream_t stream);
+
+hipError_t launch_counts(const DeviceTables &t, const void *states, int32_t state_bytes,
+                         int32_t n, int32_t m, int64_t n_cols, int64_t ld, int32_t *counts,
+                         hipStream_t stream);
+
+hipError_t launch_moving_sum(const int32_t *newc, int32_t *mb, int32_t *totals, int64_t total,
+                             hipStream_t stream);
+
+hipError_t launch_gamma(const int32_t *totals, double alpha, uint32_t key0, uint32_t key1,
+                        uint32_t update_id, double *g, int64_t total, hipStream_t stream);
+
+hipError_t launch_normalize(const DeviceTables &t, const double *g, float *cpts, int64_t n_rows,
+                            hipStream_t stream);
+
+}  // namespace same

@@ -1,0 +1,94 @@
+"""Helpers for the GPU parity tests: run the library on workload arrays and
+compare with the oracle on the same arrays."""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+import oracle
+import paper_1511_06416_amd as same
+
+REL_TOL = 1e-5       # conditionals, fp32 vs fp64
+TINY = 1e-30         # below this the oracle's probability is not compared relatively
+
+
+def context_for(net, prior=1.0):
+    pptr, pidx, card = net.csr()
+    return same.same_create(pptr, pidx, card, prior)
+
+
+def gpu_sweep(ctx, states_np, obs_np, theta_np, m, n_cols, col_offset, seed, sweep_id, win=None,
+              stream=None):
+    """Runs one library sweep on copies of the given host arrays; returns
+    (states after, probs or None)."""
+    st = torch.from_numpy(np.ascontiguousarray(states_np)).cuda()
+    ob = torch.from_numpy(np.ascontiguousarray(obs_np)).cuda()
+    th = torch.from_numpy(np.ascontiguousarray(theta_np, dtype=np.float32)).cuda()
+    ws = ctx.new_workspace()
+    ld = st.shape[-1]
+    probs = None
+    if win is not None:
+        probs = torch.full((ctx.n_nodes, m, win[1], ctx.max_card), float("nan"), device="cuda")
+        same.same_sweep_debug(ctx, st, ob, th, m, n_cols, ld, col_offset, seed, sweep_id, win[0],
+                              win[1], probs, ws, stream)
+    else:
+        same.same_sweep(ctx, st, ob, th, m, n_cols, ld, col_offset, seed, sweep_id, ws, stream)
+    torch.cuda.synchronize()
+    return st.cpu().numpy(), (probs.cpu().numpy() if probs is not None else None)
+
+
+def visit_order(color):
+    return sorted(range(len(color)), key=lambda i: (int(color[i]), i))
+
+
+def compare_states(gpu, ref, flags, color, n_cols):
+    """States must agree chain by chain (column, replica) up to the first
+    differing draw in visit order, and that draw must be a flagged boundary
+    draw.  Returns dict with counts; raises AssertionError otherwise."""
+    assert gpu.shape == ref.shape
+    diff = gpu[:, :, :n_cols] != ref[:, :, :n_cols]
+    # untouched padding
+    assert np.array_equal(gpu[:, :, n_cols:], ref[:, :, n_cols:])
+    chains = np.argwhere(diff.any(axis=0))  # (r, j) pairs with any difference
+    order = visit_order(color)
+    excused = 0
+    for r, j in chains:
+        first = next(i for i in order if diff[i, r, j])
+        assert flags[first, r, j] == 1, (
+            "unflagged mismatch at node %d replica %d column %d: gpu %d oracle %d"
+            % (first, r, j, gpu[first, r, j], ref[first, r, j]))
+        excused += 1
+    return {"mismatched_chains": excused, "flagged": int(flags[:, :, :n_cols].sum()),
+            "diff_entries": int(diff.sum())}
+
+
+def compare_probs(gpu_p, ref_p, obs, card, win, diverged=None):
+    """Window conditionals: relative 1e-5 where the oracle's p >= 1e-30, else
+    the library's p below 1e-29.  Chains marked in diverged [m][win] (whose
+    states differed earlier in the sweep) are skipped."""
+    n, m, W, kmax = ref_p.shape
+    worst, checked = 0.0, 0
+    for i in range(n):
+        K = int(card[i])
+        lat = (obs[i, win[0]:win[0] + W] == 0)[None, :].repeat(m, axis=0)
+        if diverged is not None:
+            lat &= ~diverged
+        p = ref_p[i, :, :, :K][lat]
+        q = gpu_p[i, :, :, :K][lat].astype(np.float64)
+        if p.size == 0:
+            continue
+        big = p >= TINY
+        rel = np.abs(q[big] - p[big]) / p[big]
+        if rel.size:
+            worst = max(worst, float(rel.max()))
+        bad = np.argwhere(rel > REL_TOL)
+        assert bad.size == 0, ("node", i, "worst rel", float(rel.max()))
+        assert np.all(q[~big] < 1e-29), ("node", i)
+        checked += p.shape[0]
+    return {"checked": checked, "worst_rel": worst}
+
+
+def diverged_chains(gpu, ref, n_cols, win):
+    """[m][win] mask of chains whose states differ anywhere in the sweep."""
+    d = (gpu[:, :, :n_cols] != ref[:, :, :n_cols]).any(axis=0)
+    return d[:, win[0]:win[0] + win[1]]

@@ -1,0 +1,162 @@
+"""Host-side checks of libsame (no GPU needed): the library loads and exports
+every entry point include/same.h declares; the host graph compiler's layout
+and colouring agree with the oracle's independent graph code; invalid graphs
+and invalid arguments return their error codes before any device work."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_1511_06416_amd as same
+from tests import brute
+from workloads import CONFIGS, koller, make_network
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_symbols():
+    names = set()
+    for fn in os.listdir(os.path.join(ROOT, "include")):
+        if fn.endswith(".h"):
+            txt = open(os.path.join(ROOT, "include", fn)).read()
+            txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+            names |= set(re.findall(r"\b(same_[a-z_0-9]+)\s*\(", txt))
+    return names
+
+
+def test_library_exports_every_declared_symbol():
+    L = same.load_library()
+    names = _declared_symbols()
+    assert {"same_create", "same_sweep", "same_counts", "same_sample_cpts"} <= names
+    for name in sorted(names):
+        assert hasattr(L, name), name
+
+
+def _ctx(net, prior=1.0):
+    pptr, pidx, card = net.csr()
+    return same.same_create(pptr, pidx, card, prior)
+
+
+@pytest.mark.parametrize("cfg", sorted(CONFIGS))
+def test_layout_and_colouring_match_oracle(cfg):
+    net = make_network(cfg)
+    ctx = _ctx(net)
+    ref = oracle.graph(net.parents, net.card)
+    assert np.array_equal(ctx.cpt_off, ref["cpt_off"])
+    assert np.array_equal(ctx.color, ref["color"])
+    assert ctx.n_colors == ref["n_colors"]
+    assert ctx.cpt_total == ref["cpt_off"][-1]
+    assert ctx.state_bytes == 1
+    assert ctx.workspace_bytes > 4 * ctx.cpt_total
+    ctx.close()
+
+
+def test_student_layout():
+    ctx = _ctx(koller())
+    assert ctx.cpt_total == 26 and ctx.n_rows == 11 and ctx.n_colors == 3
+    assert ctx.max_card == 3
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_random_graphs_match_oracle(seed):
+    rng = np.random.default_rng(seed)
+    parents, card = brute.random_net(rng, 60, 5, 2, 9)
+    pptr = np.cumsum([0] + [len(p) for p in parents]).astype(np.int32)
+    pidx = np.array([p for ps in parents for p in ps], dtype=np.int32)
+    ctx = same.same_create(pptr, pidx, card)
+    ref = oracle.graph(parents, card)
+    assert np.array_equal(ctx.color, ref["color"])
+    assert np.array_equal(ctx.cpt_off, ref["cpt_off"])
+
+
+def test_int16_states_for_large_cardinality():
+    ctx = same.same_create([0, 0, 1], [0], [200, 3])
+    assert ctx.state_bytes == 2 and ctx.max_card == 200
+
+
+@pytest.mark.parametrize("pptr,pidx,card,code", [
+    ([0, 1], [0], [2], same.SAME_EGRAPH),               # self loop
+    ([0, 0, 2], [0, 0], [2, 2], same.SAME_EGRAPH),      # duplicate parent
+    ([0, 1], [5], [2], same.SAME_EGRAPH),               # parent out of range
+    ([0, 1, 2], [1, 0], [2, 2], same.SAME_EGRAPH),      # cycle
+    ([0, 2, 3, 4], [1, 2, 2, 0], [2, 2, 2], same.SAME_EGRAPH),  # 3-cycle
+    ([0, 0], [], [1], same.SAME_ECARD),
+    ([0, 0], [], [40000], same.SAME_ECARD),
+    ([1, 1], [0], [2], same.SAME_EGRAPH),               # parent_ptr[0] != 0
+])
+def test_invalid_graphs(pptr, pidx, card, code):
+    with pytest.raises(same.SameError) as ei:
+        same.same_create(pptr, pidx, card)
+    assert ei.value.code == code
+    assert same.same_last_error() != ""
+
+
+def test_row_overflow_is_esize():
+    # 12 parents of cardinality 8 -> 8^12 rows
+    n = 13
+    pptr = np.array([0] * 13 + [12], dtype=np.int32)
+    pidx = np.arange(12, dtype=np.int32)
+    card = np.full(n, 8, dtype=np.int32)
+    with pytest.raises(same.SameError) as ei:
+        same.same_create(pptr, pidx, card)
+    assert ei.value.code == same.SAME_ESIZE
+
+
+def test_bad_prior():
+    with pytest.raises(same.SameError) as ei:
+        same.same_create([0, 0], [], [2], 0.0)
+    assert ei.value.code == same.SAME_EINVAL
+
+
+# Argument validation happens before any HIP call, so these run without a GPU.
+# The fake addresses are never dereferenced.
+FAKE = 1 << 20
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(m=0), same.SAME_EINVAL),
+    (dict(n_cols=100, ld=96), same.SAME_EINVAL),
+    (dict(ld=98, n_cols=90), same.SAME_EALIGN),
+    (dict(col_offset=2), same.SAME_EALIGN),
+    (dict(col_offset=-4), same.SAME_EALIGN),
+    (dict(states=0), same.SAME_EINVAL),
+    (dict(obs=0), same.SAME_EINVAL),
+    (dict(workspace=FAKE + 8), same.SAME_EALIGN),
+    (dict(obs=FAKE + 1), same.SAME_EALIGN),
+    (dict(states=FAKE + 2), same.SAME_EALIGN),
+])
+def test_sweep_argument_errors(kw, code):
+    ctx = _ctx(koller())
+    L = same.load_library()
+    a = dict(states=FAKE, obs=FAKE, cpts=FAKE, m=2, n_cols=64, ld=64, col_offset=0, workspace=FAKE)
+    a.update(kw)
+    rc = L.same_sweep(ctx.handle, C.c_void_p(a["states"]), C.c_void_p(a["obs"]),
+                      C.c_void_p(a["cpts"]), a["m"], a["n_cols"], a["ld"], a["col_offset"], 1, 0,
+                      C.c_void_p(a["workspace"]), None)
+    assert rc == code
+
+
+def test_counts_and_sample_argument_errors():
+    ctx = _ctx(koller())
+    L = same.load_library()
+    assert L.same_counts(ctx.handle, C.c_void_p(FAKE), 0, 4, 4, C.c_void_p(FAKE), None,
+                         C.c_void_p(FAKE), None) == same.SAME_EINVAL
+    assert L.same_counts(ctx.handle, C.c_void_p(FAKE), 1, 4, 4, None, None,
+                         C.c_void_p(FAKE), None) == same.SAME_EINVAL
+    assert L.same_sample_cpts(ctx.handle, None, C.c_void_p(FAKE), 1, 0, C.c_void_p(FAKE),
+                              None) == same.SAME_EINVAL
+    assert L.same_sample_cpts(ctx.handle, C.c_void_p(FAKE), C.c_void_p(FAKE), 1, 0,
+                              C.c_void_p(FAKE + 16), None) == same.SAME_EALIGN
+    assert L.same_sweep_debug(ctx.handle, C.c_void_p(FAKE), C.c_void_p(FAKE), C.c_void_p(FAKE),
+                              1, 8, 8, 0, 1, 0, 0, 0, None, C.c_void_p(FAKE),
+                              None) == same.SAME_EINVAL
+
+
+def test_null_context():
+    L = same.load_library()
+    assert L.same_layout(None, None, None, None) == same.SAME_EINVAL
+    assert L.same_workspace_size(None, None) == same.SAME_EINVAL
+    L.same_destroy(None)
