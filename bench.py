@@ -43,6 +43,13 @@ def parse():
     p.add_argument("--cpu-sample-cols", type=int, default=32768)
     p.add_argument("--copy-calibration", action="store_true",
                    help="also run a plain 1 GiB device copy (for HBM counter scaling)")
+    p.add_argument("--gen-device", choices=["cuda", "cpu"], default="cuda",
+                   help="where the synthetic inputs are generated (cpu: only the library's "
+                        "kernels run on the GPU, for counter collection)")
+    p.add_argument("--table-limit", type=int, default=None,
+                   help="threshold-table size limit passed to same_create_ex (0: products only)")
+    p.add_argument("--minibatches", type=int, default=None,
+                   help="process only the first K minibatches (profiling runs)")
     return p.parse_args()
 
 
@@ -65,10 +72,17 @@ def main():
     same.load_library()
 
     t0 = time.time()
-    w = make_workload(args.cfg, n_cols=args.n_cols, device=dev)
+    probe = make_workload(args.cfg, n_cols=args.n_cols, device="cpu", minibatches=[])
+    mbs = list(range(probe.M if args.minibatches is None else min(args.minibatches, probe.M)))
+    gen_dev = dev if args.gen_device == "cuda" else torch.device("cpu")
+    w = make_workload(args.cfg, n_cols=args.n_cols, device=gen_dev, minibatches=mbs)
+    if args.gen_device == "cpu":
+        w.states = [s.to(dev) for s in w.states]
+        w.obs = [o.to(dev) for o in w.obs]
     torch.cuda.synchronize()
-    log("generated %s on the GPU in %.1f s: n=%d N=%d m=%d nb=%d M=%d ld=%d" % (
-        w.name, time.time() - t0, w.net.n, w.n_cols, w.m, w.nb, w.M, w.ld))
+    log("generated %s on %s in %.1f s: n=%d N=%d m=%d nb=%d M=%d ld=%d, timing %d minibatches" % (
+        w.name, args.gen_device, time.time() - t0, w.net.n, w.n_cols, w.m, w.nb, w.M, w.ld,
+        len(mbs)))
     net = w.net
     # the oracle's sample is taken from the generator's output, before any sweep
     sample = None
@@ -78,23 +92,29 @@ def main():
         sample = (cols, np.ascontiguousarray(w.states[0][:, :, :cols4].cpu().numpy()),
                   np.ascontiguousarray(w.obs[0][:, :cols4].cpu().numpy()))
     pptr, pidx, card = net.csr()
-    ctx = same.same_create(pptr, pidx, card, w.alpha)
+    if args.table_limit is None:
+        ctx = same.same_create(pptr, pidx, card, w.alpha)
+    else:
+        ctx = same.same_create_ex(pptr, pidx, card, w.alpha, args.table_limit)
     ws = ctx.new_workspace(dev)
     cpts = torch.from_numpy(w.init_theta).to(dev)
-    mb = torch.zeros((w.M, ctx.cpt_total), dtype=torch.int32, device=dev)
-    tot = torch.zeros(ctx.cpt_total, dtype=torch.int32, device=dev)
+    mb = torch.from_numpy(np.zeros((w.M, ctx.cpt_total), dtype=np.int32)).to(dev)
+    tot = torch.from_numpy(np.zeros(ctx.cpt_total, dtype=np.int32)).to(dev)
     stream = torch.cuda.current_stream()
-    latent = sum(int((o[:, :w.mb_cols(b)] == 0).sum().item()) for b, o in enumerate(w.obs))
-    hidden = latent / float(net.n * w.n_cols)
+    obs_host = [w.obs[b][:, :w.mb_cols(b)].cpu().numpy() for b in mbs]
+    latent = sum(int((o == 0).sum()) for o in obs_host)
+    cols_timed = sum(w.mb_cols(b) for b in mbs)
+    hidden = latent / float(net.n * cols_timed)
+    del obs_host
 
     # count-only pre-pass initialises the per-minibatch counts and their sum
-    for b in range(w.M):
+    for b in mbs:
         same.same_counts(ctx, w.states[b], w.m, w.mb_cols(b), w.ld, mb[b], tot, ws)
 
     sweep_ev = []
 
     def one_pass(s, record):
-        for b in range(w.M):
+        for b in mbs:
             if record:
                 e0 = torch.cuda.Event(enable_timing=True)
                 e1 = torch.cuda.Event(enable_timing=True)
@@ -124,10 +144,10 @@ def main():
     elapsed = max(wall, gpu_ms / 1e3)
     log("timed %d passes: wall %.3f s, events %.3f s" % (args.steps, wall, gpu_ms / 1e3))
 
-    node_samples = float(net.n) * w.n_cols * w.m * args.steps
+    node_samples = float(net.n) * cols_timed * w.m * args.steps
     value = node_samples / elapsed
     sweep_s = sum(a.elapsed_time(b) for a, b in sweep_ev) / 1e3
-    launches = ctx.n_colors * w.M * args.steps
+    launches = len(sweep_ev) * ctx.n_colors
     bytes_per_ns = 1.0 + hidden + 1.0 / w.m   # read each state, write each latent, obs per column
     alg_bytes = node_samples * bytes_per_ns
     achieved = alg_bytes / sweep_s / 1e9
@@ -146,8 +166,9 @@ def main():
     }
 
     if args.copy_calibration:
-        a = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
-        b2 = torch.empty_like(a)
+        # a plain device-to-device copy of exactly 1 GiB (runtime copy kernel)
+        a = torch.from_numpy(np.zeros(1 << 30, dtype=np.uint8)).to(dev)
+        b2 = torch.from_numpy(np.ones(1 << 30, dtype=np.uint8)).to(dev)
         b2.copy_(a)
         torch.cuda.synchronize()
         del a, b2
@@ -176,7 +197,8 @@ def main():
                             w.name, net.n, spec["graph"][2] if spec["graph"][0] == "random" else 0,
                             int(net.card.min()), int(net.card.max()), w.n_cols, w.nb,
                             100 * w.hidden, w.m) if args.cfg in (3, 5) else w.name,
-            "global_batch": w.n_cols,
+            "global_batch": cols_timed,
+            "minibatches_timed": len(mbs),
             "minibatch_cols": w.nb,
             "replicas": w.m,
             "nodes": net.n,

@@ -91,6 +91,22 @@ typedef struct {
 int same_create(int32_t n_nodes, const int32_t *parent_ptr, const int32_t *parent_idx,
                 const int32_t *card, double dirichlet_prior, same_ctx **out);
 
+/* Build options for same_create_ex. */
+typedef struct {
+    /* Largest (blanket configurations) x (thresholds per configuration) for
+     * which a node's full conditional is precomputed into a table of CDF
+     * thresholds (one table per CPT update; the draw becomes one table read).
+     * -1 selects the default (16384); 0 disables the tables, so every node
+     * forms its conditional from CPT entries during the sweep.  Either way the
+     * sweep draws from the same conditional with the same uniforms. */
+    int64_t table_limit;
+} same_options_t;
+
+/* same_create with options (opts may be NULL for the defaults). */
+int same_create_ex(int32_t n_nodes, const int32_t *parent_ptr, const int32_t *parent_idx,
+                   const int32_t *card, double dirichlet_prior, const same_options_t *opts,
+                   same_ctx **out);
+
 /* Frees the context and its device tables (on every device it used). */
 void same_destroy(same_ctx *ctx);
 
@@ -114,9 +130,13 @@ int same_workspace_size(const same_ctx *ctx, size_t *bytes);
  * groups in ascending order; inside a group every (node, column, replica) is
  * independent).  For every latent entry the full conditional
  *   P(x_i = k | rest) ~ theta_i(k | x_pa(i)) * prod_{h in ch(i)} theta_h(x_h | x_pa(h), x_i = k)
- * is formed in fp32 from max(theta, FLT_MIN) and a state is drawn by inverse
- * CDF: with S_k the running sum of the weights and Z = S_{K-1}, the smallest
- * k with u*Z < S_k, else the largest k with positive weight.
+ * is formed from max(theta, FLT_MIN) and a state is drawn by inverse CDF: with
+ * S_k the running sum of the weights and Z = S_{K-1}, the smallest k with
+ * u*Z < S_k, else the largest k with positive weight (u = 24-bit uniform).
+ * Nodes whose Markov blanket has few configurations (see same_options_t) read
+ * integer thresholds ceil(2^24 S_k / Z) precomputed in fp64 for every blanket
+ * configuration; the others multiply fp32 CPT entries (relative error below
+ * (1 + children) * 2^-24 per weight) at every draw.
  * states [n][m][ld] (in/out), obs [n][ld], cpts [cpt_total]: device pointers.
  * col_offset and ld must be multiples of 4 and states/obs 4-byte aligned.
  * seed and sweep_id select the Philox stream.  The colour groups launch in

@@ -16,7 +16,7 @@ import threading
 import numpy as np
 
 __all__ = [
-    "SameError", "Context", "same_create", "same_destroy", "same_layout", "same_workspace_size",
+    "SameError", "Context", "same_create", "same_create_ex", "same_destroy", "same_layout", "same_workspace_size",
     "same_sweep", "same_sweep_debug", "same_counts", "same_sample_cpts", "same_last_error",
     "library_path", "load_library",
 ]
@@ -36,6 +36,10 @@ class SameError(RuntimeError):
     def __init__(self, code, msg):
         super().__init__("%s (%d): %s" % (_NAMES.get(code, "?"), code, msg))
         self.code = code
+
+
+class _Options(C.Structure):
+    _fields_ = [("table_limit", C.c_int64)]
 
 
 class _Layout(C.Structure):
@@ -58,6 +62,7 @@ def load_library():
         L = C.CDLL(_LIB_PATH)
         P, I32, I64, U64, U32 = C.c_void_p, C.c_int32, C.c_int64, C.c_uint64, C.c_uint32
         L.same_create.argtypes = [I32, P, P, P, C.c_double, C.POINTER(P)]
+        L.same_create_ex.argtypes = [I32, P, P, P, C.c_double, C.POINTER(_Options), C.POINTER(P)]
         L.same_destroy.argtypes = [P]
         L.same_destroy.restype = None
         L.same_layout.argtypes = [P, C.POINTER(_Layout), P, P]
@@ -68,7 +73,7 @@ def load_library():
         L.same_sample_cpts.argtypes = [P, P, P, U64, U32, P, P]
         L.same_last_error.argtypes = []
         L.same_last_error.restype = C.c_char_p
-        for f in ("same_create", "same_layout", "same_workspace_size", "same_sweep",
+        for f in ("same_create", "same_create_ex", "same_layout", "same_workspace_size", "same_sweep",
                   "same_sweep_debug", "same_counts", "same_sample_cpts"):
             getattr(L, f).restype = C.c_int
         _lib = L
@@ -105,14 +110,20 @@ def _stream(stream):
 class Context:
     """Owns one same_ctx (one network)."""
 
-    def __init__(self, parent_ptr, parent_idx, card, dirichlet_prior=1.0):
+    def __init__(self, parent_ptr, parent_idx, card, dirichlet_prior=1.0, table_limit=None):
         L = load_library()
         self._pptr = np.ascontiguousarray(parent_ptr, dtype=np.int32)
         self._pidx = np.ascontiguousarray(parent_idx if len(parent_idx) else [0], dtype=np.int32)
         self._card = np.ascontiguousarray(card, dtype=np.int32)
         h = C.c_void_p()
-        _check(L.same_create(len(self._card), self._pptr.ctypes.data, self._pidx.ctypes.data,
-                             self._card.ctypes.data, float(dirichlet_prior), C.byref(h)))
+        if table_limit is None:
+            _check(L.same_create(len(self._card), self._pptr.ctypes.data, self._pidx.ctypes.data,
+                                 self._card.ctypes.data, float(dirichlet_prior), C.byref(h)))
+        else:
+            opts = _Options(int(table_limit))
+            _check(L.same_create_ex(len(self._card), self._pptr.ctypes.data,
+                                    self._pidx.ctypes.data, self._card.ctypes.data,
+                                    float(dirichlet_prior), C.byref(opts), C.byref(h)))
         self._h = h
         lay = _Layout()
         off = np.zeros(len(self._card) + 1, dtype=np.int64)
@@ -149,6 +160,10 @@ class Context:
 
 def same_create(parent_ptr, parent_idx, card, dirichlet_prior=1.0) -> Context:
     return Context(parent_ptr, parent_idx, card, dirichlet_prior)
+
+
+def same_create_ex(parent_ptr, parent_idx, card, dirichlet_prior=1.0, table_limit=-1) -> Context:
+    return Context(parent_ptr, parent_idx, card, dirichlet_prior, table_limit=table_limit)
 
 
 def same_destroy(ctx: Context) -> None:

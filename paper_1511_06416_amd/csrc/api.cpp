@@ -33,7 +33,7 @@ struct same_ctx {
     std::vector<same::DeviceTables> dev;  // indexed by device ordinal
     std::mutex mu;
     // workspace layout
-    size_t ws_table = 0, ws_counts = 0, ws_gamma = 0, ws_total = 0;
+    size_t ws_table = 0, ws_cond = 0, ws_counts = 0, ws_gamma = 0, ws_total = 0;
 };
 
 namespace {
@@ -54,8 +54,8 @@ void free_tables(same::DeviceTables &t) {
     int cur = -1;
     (void)hipGetDevice(&cur);
     (void)hipSetDevice(t.device);
-    void *ptrs[] = {t.desc, t.desc_off, t.order, t.cdesc, t.cdesc_off, t.segs,
-                    t.blk_seg, t.blk_first, t.row_off, t.row_k};
+    void *ptrs[] = {t.desc, t.desc_off, t.order, t.cdesc, t.cdesc_off, t.segs, t.blk_seg,
+                    t.blk_first, t.row_off, t.row_k, t.cprog, t.cprog_off, t.cblk_prog, t.cblk_first};
     for (void *p : ptrs)
         if (p) (void)hipFree(p);
     if (cur >= 0) (void)hipSetDevice(cur);
@@ -82,9 +82,18 @@ int tables_for_current_device(same_ctx *ctx, same::DeviceTables **out) {
             blk_seg.push_back((int32_t)s);
             blk_first.push_back(f);
         }
+    std::vector<int32_t> cblk_prog, cblk_first;
+    for (size_t t2 = 0; t2 < g.cprog_off.size(); ++t2) {
+        const int32_t ncfg = g.cprog[g.cprog_off[t2] + 3];
+        for (int32_t f = 0; f < ncfg; f += 256) {
+            cblk_prog.push_back((int32_t)t2);
+            cblk_first.push_back(f);
+        }
+    }
     same::DeviceTables nt;
     nt.device = device;
     nt.n_build_blocks = (int32_t)blk_seg.size();
+    nt.n_cond_blocks = (int32_t)cblk_prog.size();
     hipError_t r = hipSuccess;
     if (r == hipSuccess) r = upload(&nt.desc, g.desc);
     if (r == hipSuccess) r = upload(&nt.desc_off, g.desc_off);
@@ -96,6 +105,10 @@ int tables_for_current_device(same_ctx *ctx, same::DeviceTables **out) {
     if (r == hipSuccess) r = upload(&nt.blk_first, blk_first);
     if (r == hipSuccess) r = upload(&nt.row_off, g.row_off);
     if (r == hipSuccess) r = upload(&nt.row_k, g.row_k);
+    if (r == hipSuccess) r = upload(&nt.cprog, g.cprog);
+    if (r == hipSuccess) r = upload(&nt.cprog_off, g.cprog_off);
+    if (r == hipSuccess) r = upload(&nt.cblk_prog, cblk_prog);
+    if (r == hipSuccess) r = upload(&nt.cblk_first, cblk_first);
     if (r != hipSuccess) {
         free_tables(nt);
         return set_error(r == hipErrorOutOfMemory ? SAME_ENOMEM : SAME_EHIP,
@@ -121,6 +134,8 @@ int check_minibatch(const same_ctx *ctx, const void *states, int32_t m, int64_t 
     if (ld % 4 != 0) return set_error(SAME_EALIGN, "ld must be a multiple of 4");
     if (!aligned(states, 4 * (size_t)ctx->g.state_bytes))
         return set_error(SAME_EALIGN, "states must be aligned to 4 state elements");
+    if ((double)m * (double)ld * ctx->g.state_bytes >= 2147483648.0)
+        return set_error(SAME_ESIZE, "one node's replica block m * ld must stay below 2^31 bytes");
     if ((double)ctx->g.n * (double)m * (double)ld * ctx->g.state_bytes > 9.0e18)
         return set_error(SAME_ESIZE, "states array too large");
     return SAME_OK;
@@ -148,31 +163,39 @@ int do_sweep(same_ctx *ctx, void *states, const uint8_t *obs, const float *cpts,
     if (rc) return rc;
     hipStream_t s = (hipStream_t)stream;
     float *table = (float *)((char *)workspace + ctx->ws_table);
+    uint32_t *cond = (uint32_t *)((char *)workspace + ctx->ws_cond);
     rc = check_hip(same::launch_build_tables(*t, cpts, table, s), "table build launch");
     if (rc) return rc;
-    same::SweepArgs a;
-    a.t = t;
-    a.table = table;
-    a.states = states;
-    a.obs = obs;
-    a.m = m;
-    a.n_cols = n_cols;
-    a.ld = ld;
-    a.col_offset = col_offset;
-    a.key0 = (uint32_t)seed;
-    a.key1 = (uint32_t)(seed >> 32);
-    a.sweep_id = sweep_id;
-    a.win_begin = win_begin;
-    a.win = win > 0 ? win : 0;
-    a.probs = probs;
-    a.max_card = ctx->g.max_card;
+    rc = check_hip(same::launch_build_thresholds(*t, cpts, cond, s), "threshold build launch");
+    if (rc) return rc;
+    same::SweepParams P{};
+    P.desc = t->desc;
+    P.desc_off = t->desc_off;
+    P.order = t->order;
+    P.table = table;
+    P.cond = cond;
+    P.states = states;
+    P.obs = obs;
+    P.m = m;
+    P.n_cols = n_cols;
+    P.ld = ld;
+    P.col_offset = col_offset;
+    P.key0 = (uint32_t)seed;
+    P.key1 = (uint32_t)(seed >> 32);
+    P.sweep_id = sweep_id;
+    P.win_begin = win_begin;
+    P.win = win > 0 ? win : 0;
+    P.probs = probs;
+    P.max_card = ctx->g.max_card;
     const same::Compiled &g = ctx->g;
-    for (int32_t c = 0; c < g.n_colors; ++c) {
-        rc = check_hip(same::launch_sweep_color(a, g.color_start[c], g.color_start[c + 1] - g.color_start[c],
-                                                g.color_kp[c], g.state_bytes, s),
-                       "sweep launch");
-        if (rc) return rc;
-    }
+    const int32_t L = same::kLaunchClasses;
+    for (int32_t c = 0; c < g.n_colors; ++c)
+        for (int32_t k = 0; k < L; ++k) {
+            const int32_t b = g.launch[c * (L + 1) + k], e = g.launch[c * (L + 1) + k + 1];
+            rc = check_hip(same::launch_sweep(P, b, e - b, k, g.launch_lds[c * L + k], g.state_bytes, s),
+                           "sweep launch");
+            if (rc) return rc;
+        }
     return SAME_OK;
 }
 
@@ -184,7 +207,16 @@ const char *same_last_error(void) { return g_last_error.c_str(); }
 
 int same_create(int32_t n_nodes, const int32_t *parent_ptr, const int32_t *parent_idx,
                 const int32_t *card, double dirichlet_prior, same_ctx **out) {
+    return same_create_ex(n_nodes, parent_ptr, parent_idx, card, dirichlet_prior, nullptr, out);
+}
+
+int same_create_ex(int32_t n_nodes, const int32_t *parent_ptr, const int32_t *parent_idx,
+                   const int32_t *card, double dirichlet_prior, const same_options_t *opts,
+                   same_ctx **out) {
     if (!out) return set_error(SAME_EINVAL, "out is null");
+    int64_t table_limit = 16384;
+    if (opts && opts->table_limit >= 0) table_limit = opts->table_limit;
+    if (opts && opts->table_limit < -1) return set_error(SAME_EINVAL, "table_limit must be >= -1");
     *out = nullptr;
     if (!(dirichlet_prior > 0.0)) return set_error(SAME_EINVAL, "dirichlet_prior must be > 0");
     same_ctx *ctx = new (std::nothrow) same_ctx();
@@ -192,7 +224,7 @@ int same_create(int32_t n_nodes, const int32_t *parent_ptr, const int32_t *paren
     std::string err;
     int rc;
     try {
-        rc = same::compile_graph(n_nodes, parent_ptr, parent_idx, card, ctx->g, err);
+        rc = same::compile_graph(n_nodes, parent_ptr, parent_idx, card, ctx->g, err, table_limit);
     } catch (const std::bad_alloc &) {
         rc = SAME_ENOMEM;
         err = "out of host memory";
@@ -203,7 +235,8 @@ int same_create(int32_t n_nodes, const int32_t *parent_ptr, const int32_t *paren
     }
     ctx->alpha = dirichlet_prior;
     ctx->ws_table = 0;
-    ctx->ws_counts = align_up(ctx->ws_table + (size_t)ctx->g.table_floats * sizeof(float));
+    ctx->ws_cond = align_up(ctx->ws_table + (size_t)ctx->g.table_floats * sizeof(float));
+    ctx->ws_counts = align_up(ctx->ws_cond + (size_t)ctx->g.cond_words * sizeof(uint32_t));
     ctx->ws_gamma = align_up(ctx->ws_counts + (size_t)ctx->g.off[n_nodes] * sizeof(int32_t));
     ctx->ws_total = align_up(ctx->ws_gamma + (size_t)ctx->g.off[n_nodes] * sizeof(double));
     *out = ctx;

@@ -28,8 +28,14 @@ int fail(std::string &err, int code, const std::string &msg) {
 
 }  // namespace
 
+int32_t thresholds_per_config(int32_t K) {
+    int32_t t = 1;
+    while (t < K - 1) t <<= 1;
+    return t;
+}
+
 int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int32_t *card,
-                  Compiled &g, std::string &err) {
+                  Compiled &g, std::string &err, int64_t table_limit) {
     if (n <= 0) return fail(err, SAME_EINVAL, "n_nodes must be positive");
     if (!pptr || !card) return fail(err, SAME_EINVAL, "parent_ptr and card must be non-null");
     if (pptr[0] != 0) return fail(err, SAME_EGRAPH, "parent_ptr[0] must be 0");
@@ -133,34 +139,25 @@ int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int
     }
     g.groups.assign(g.n_colors, {});
     for (int32_t i = 0; i < n; ++i) g.groups[g.color[i]].push_back(i);
-    g.color_start.assign(1, 0);
-    for (int32_t c = 0; c < g.n_colors; ++c) {
-        int32_t kp = 2;
-        for (int32_t i : g.groups[c]) {
-            g.order.push_back(i);
-            kp = std::max(kp, padded_k(card[i]));
-        }
-        g.color_start.push_back((int32_t)g.order.size());
-        g.color_kp.push_back(kp);
-    }
 
-    // regrouped sweep tables and the segments that build them
+    // regrouped sweep tables and the segments that build them: one contiguous
+    // record per node (its own k-vectors, then one table per child), every
+    // record and sub-table on a 64-byte boundary so that the sweep can read a
+    // group with float2/float4 loads and stage a whole record in LDS
     g.kp.resize(n);
     g.own_off.resize(n);
-    // every k-vector table starts on a 64-byte boundary so that the sweep can
-    // read a group with float2/float4 loads
+    g.tab_begin.resize(n);
+    g.tab_len.resize(n);
     auto align16 = [](int64_t v) { return (v + 15) & ~int64_t(15); };
     int64_t pos = 0;
+    std::vector<std::vector<int32_t>> ctab_of(n);  // indices into ctabs per node
     for (int32_t i = 0; i < n; ++i) {
         g.kp[i] = padded_k(card[i]);
         pos = align16(pos);
+        g.tab_begin[i] = pos;
         g.own_off[i] = pos;
-        Segment s{pos, g.off[i], (int32_t)g.rows[i], card[i], g.kp[i], 1, 0, 1};
-        g.segments.push_back(s);
+        g.segments.push_back(Segment{pos, g.off[i], (int32_t)g.rows[i], card[i], g.kp[i], 1, 0, 1});
         pos += g.rows[i] * g.kp[i];
-    }
-    std::vector<std::vector<int32_t>> ctab_of(n);  // indices into ctabs per node
-    for (int32_t i = 0; i < n; ++i) {
         for (auto &c : kids[i]) {
             int32_t h = c.first;
             ChildTab t;
@@ -171,56 +168,167 @@ int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int
             pos = align16(pos);
             t.off = pos;
             int64_t s_i = g.pstride[pptr[h] + c.second];
-            Segment s{pos, g.off[h], (int32_t)t.groups, card[i], g.kp[i], card[h], (int32_t)s_i, 0};
-            g.segments.push_back(s);
+            g.segments.push_back(
+                Segment{pos, g.off[h], (int32_t)t.groups, card[i], g.kp[i], card[h], (int32_t)s_i, 0});
             pos += t.groups * g.kp[i];
             ctab_of[i].push_back((int32_t)g.ctabs.size());
             g.ctabs.push_back(t);
         }
+        pos = align16(pos);
+        g.tab_len[i] = pos - g.tab_begin[i];
     }
     g.table_floats = pos;
     if (pos > kI32Max) return fail(err, SAME_ESIZE, "sweep tables exceed 2^31 floats");
 
+    // Markov blankets (parents, children, co-parents; ascending id) and modes
+    std::vector<std::vector<int32_t>> blanket(n);
+    g.mode.assign(n, kModeKP2);
+    for (int32_t i = 0; i < n; ++i) {
+        std::vector<int32_t> &b = blanket[i];
+        for (int32_t a = pptr[i]; a < pptr[i + 1]; ++a) b.push_back(g.pidx[a]);
+        for (auto &c : kids[i]) {
+            int32_t h = c.first;
+            b.push_back(h);
+            for (int32_t a = pptr[h]; a < pptr[h + 1]; ++a)
+                if (g.pidx[a] != i) b.push_back(g.pidx[a]);
+        }
+        std::sort(b.begin(), b.end());
+        b.erase(std::unique(b.begin(), b.end()), b.end());
+        const int32_t K = card[i];
+        int32_t mode = K <= 2 ? kModeKP2 : K <= 4 ? kModeKP4 : K <= 8 ? kModeKP8
+                     : K <= 16 ? kModeKP16 : kModeGeneric;
+        if (table_limit > 0 && K <= 9) {
+            int64_t cfg = 1;
+            for (int32_t v : b) {
+                cfg *= card[v];
+                if (cfg * thresholds_per_config(K) > table_limit) break;
+            }
+            if (cfg * thresholds_per_config(K) <= table_limit && b.size() <= 24) mode = kModeTable;
+        }
+        g.mode[i] = mode;
+    }
+
+    // threshold tables and their build programs
+    std::vector<int64_t> cond_off(n, -1);
+    {
+        int64_t cpos = 0;
+        for (int32_t i = 0; i < n; ++i) {
+            if (g.mode[i] != kModeTable) continue;
+            const int32_t K = card[i], KT = thresholds_per_config(K);
+            const std::vector<int32_t> &b = blanket[i];
+            int64_t ncfg = 1;
+            for (int32_t v : b) ncfg *= card[v];
+            cpos = (cpos + 15) & ~int64_t(15);
+            cond_off[i] = cpos;
+            auto pos_of = [&](int32_t v) {
+                return (int32_t)(std::lower_bound(b.begin(), b.end(), v) - b.begin());
+            };
+            g.cprog_nodes.push_back(i);
+            g.cprog_off.push_back((int32_t)g.cprog.size());
+            std::vector<int32_t> &P = g.cprog;
+            P.push_back(K);
+            P.push_back(KT);
+            P.push_back((int32_t)cpos);
+            P.push_back((int32_t)ncfg);
+            P.push_back((int32_t)b.size());
+            for (int32_t v : b) P.push_back(card[v]);
+            P.push_back((int32_t)g.off[i]);
+            P.push_back(pptr[i + 1] - pptr[i]);
+            for (int32_t a = pptr[i]; a < pptr[i + 1]; ++a) {
+                P.push_back(pos_of(g.pidx[a]));
+                P.push_back((int32_t)g.pstride[a]);
+            }
+            P.push_back((int32_t)kids[i].size());
+            for (auto &c : kids[i]) {
+                const int32_t h = c.first;
+                P.push_back((int32_t)g.off[h]);
+                P.push_back(card[h]);
+                P.push_back((int32_t)g.pstride[pptr[h] + c.second]);
+                P.push_back(pos_of(h));
+                P.push_back(pptr[h + 1] - pptr[h] - 1);
+                for (int32_t a = pptr[h]; a < pptr[h + 1]; ++a) {
+                    if (g.pidx[a] == i) continue;
+                    P.push_back(pos_of(g.pidx[a]));
+                    P.push_back((int32_t)g.pstride[a]);
+                }
+            }
+            cpos += ncfg * KT;
+            if (cpos > kI32Max) return fail(err, SAME_ESIZE, "threshold tables exceed 2^31 words");
+        }
+        g.cond_words = cpos;
+    }
+
     // descriptor streams
     g.desc_off.resize(n);
     g.cdesc_off.resize(n);
+    g.lds_bytes.assign(n, 0);
     for (int32_t i = 0; i < n; ++i) {
         const int32_t KP = g.kp[i];
-        g.desc_off[i] = (int32_t)g.desc.size();
-        g.desc.push_back(card[i]);
-        g.desc.push_back(KP);
-        g.desc.push_back((int32_t)g.own_off[i]);
-        g.desc.push_back(pptr[i + 1] - pptr[i]);
-        g.desc.push_back((int32_t)kids[i].size());
-        for (int32_t a = pptr[i]; a < pptr[i + 1]; ++a) {
-            g.desc.push_back(g.pidx[a]);
-            int64_t mult = g.pstride[a] * KP;
+        const bool tab = g.mode[i] == kModeTable;
+        const std::vector<int32_t> &b = blanket[i];
+        const int32_t KT = tab ? thresholds_per_config(card[i]) : 0;
+        int64_t cond_len = 0;
+        if (tab) {
+            cond_len = KT;
+            for (int32_t v : b) cond_len *= card[v];
+        }
+        const int64_t stage = tab ? cond_len * 4 : g.tab_len[i] * 4;
+        if (mode_class(g.mode[i]) == 0 && stage <= kLdsBudgetBytes) g.lds_bytes[i] = (int32_t)stage;
+        const int32_t base = (int32_t)g.desc.size();
+        g.desc_off[i] = base;
+        g.desc.resize(base + kDescHeader, 0);
+        g.desc[base + 0] = card[i];
+        g.desc[base + 1] = KP;
+        g.desc[base + 2] = g.mode[i];
+        g.desc[base + 3] = (int32_t)g.tab_begin[i];
+        g.desc[base + 4] = (int32_t)g.tab_len[i];
+        g.desc[base + 5] = (int32_t)cond_off[i];
+        g.desc[base + 6] = (int32_t)cond_len;
+        g.desc[base + 7] = KT;
+        g.desc[base + 12] = g.lds_bytes[i] > 0 ? 1 : 0;
+        // entry lists: (node, mult, arg); arg -3 own row, -1 adds to the own
+        // (or threshold) index, -2 adds to the current child index, >= 0 starts
+        // a child whose k-vector table begins at relative offset arg
+        if (tab) {
+            g.desc[base + 8] = 1 + (int32_t)b.size();
+            g.desc[base + 9] = (int32_t)g.desc.size() - base;
+            g.desc.insert(g.desc.end(), {i, 0, -3});
+            std::vector<int64_t> st(b.size());
+            int64_t r = 1;
+            for (int32_t t = (int32_t)b.size() - 1; t >= 0; --t) {
+                st[t] = r;
+                r *= card[b[t]];
+            }
+            for (size_t t = 0; t < b.size(); ++t) g.desc.insert(g.desc.end(), {b[t], (int32_t)(st[t] * KT), -1});
+        }
+        const int32_t pstart = (int32_t)g.desc.size();
+        g.desc[base + 11] = pstart - base;
+        g.desc.insert(g.desc.end(), {i, 0, -3});
+        for (int32_t a2 = pptr[i]; a2 < pptr[i + 1]; ++a2) {
+            int64_t mult = g.pstride[a2] * KP;
             if (mult > kI32Max) return fail(err, SAME_ESIZE, "row stride overflow");
-            g.desc.push_back((int32_t)mult);
+            g.desc.insert(g.desc.end(), {g.pidx[a2], (int32_t)mult, -1});
         }
         for (int32_t t : ctab_of[i]) {
             const ChildTab &ct = g.ctabs[t];
             const int32_t h = ct.child, Kh = card[h];
-            g.desc.push_back(h);
-            g.desc.push_back((int32_t)ct.off);
-            g.desc.push_back(KP);
-            g.desc.push_back(pptr[h + 1] - pptr[h] - 1);
+            g.desc.insert(g.desc.end(), {h, KP, (int32_t)(ct.off - g.tab_begin[i])});
             // compact strides over h's parents without i, last listed fastest
             int64_t r = 1;
             std::vector<std::pair<int32_t, int64_t>> cops;
-            for (int32_t a = pptr[h + 1] - 1; a >= pptr[h]; --a) {
-                if (a - pptr[h] == ct.slot) continue;
-                cops.push_back({g.pidx[a], r});
-                r *= card[g.pidx[a]];
+            for (int32_t a2 = pptr[h + 1] - 1; a2 >= pptr[h]; --a2) {
+                if (a2 - pptr[h] == ct.slot) continue;
+                cops.push_back({g.pidx[a2], r});
+                r *= card[g.pidx[a2]];
             }
             std::reverse(cops.begin(), cops.end());
             for (auto &cp : cops) {
                 int64_t mult = cp.second * Kh * KP;
                 if (mult > kI32Max) return fail(err, SAME_ESIZE, "child stride overflow");
-                g.desc.push_back(cp.first);
-                g.desc.push_back((int32_t)mult);
+                g.desc.insert(g.desc.end(), {cp.first, (int32_t)mult, -2});
             }
         }
+        g.desc[base + 10] = ((int32_t)g.desc.size() - pstart) / 3;
         g.cdesc_off[i] = (int32_t)g.cdesc.size();
         g.cdesc.push_back(card[i]);
         g.cdesc.push_back(pptr[i + 1] - pptr[i]);
@@ -230,6 +338,27 @@ int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int
             g.cdesc.push_back(g.pidx[a]);
             g.cdesc.push_back((int32_t)g.pstride[a]);
         }
+    }
+
+    // launch order: per colour, the nodes of each launch class in turn
+    // (0: main kernel with LDS-staged tables, 1: main kernel reading tables
+    // from global memory, 2: KP 16, 3: generic), and per (colour, class) the
+    // LDS bytes the launch needs
+    g.launch.assign((size_t)g.n_colors * (kLaunchClasses + 1), 0);
+    g.launch_lds.assign((size_t)g.n_colors * kLaunchClasses, 0);
+    for (int32_t c = 0; c < g.n_colors; ++c) {
+        for (int32_t k = 0; k < kLaunchClasses; ++k) {
+            g.launch[c * (kLaunchClasses + 1) + k] = (int32_t)g.order.size();
+            for (int32_t i : g.groups[c]) {
+                const int32_t mc = mode_class(g.mode[i]);
+                const int32_t lc = mc == 0 ? (g.lds_bytes[i] > 0 ? 0 : 1) : mc + 1;
+                if (lc != k) continue;
+                g.order.push_back(i);
+                int32_t &lb = g.launch_lds[c * kLaunchClasses + k];
+                lb = std::max(lb, g.lds_bytes[i]);
+            }
+        }
+        g.launch[c * (kLaunchClasses + 1) + kLaunchClasses] = (int32_t)g.order.size();
     }
     if ((int64_t)g.desc.size() > kI32Max) return fail(err, SAME_ESIZE, "descriptor overflow");
 

@@ -41,6 +41,39 @@ struct Segment {
     int32_t own;       // 1: own rows of node i
 };
 
+// Sweep modes (descriptor field 5).
+enum SweepMode : int32_t {
+    kModeKP2 = 0,    // product of k-vectors, KP = 2
+    kModeKP4 = 1,
+    kModeKP8 = 2,
+    kModeTable = 3,  // precomputed CDF thresholds per blanket configuration
+    kModeKP16 = 4,   // product path with KP = 16 (own kernel: higher register use)
+    kModeGeneric = 5 // K > 16: extended-exponent product path (own kernel)
+};
+
+// Kernel class of a mode: 0 main kernel (KP2/4/8 and table), 1 KP16, 2 generic.
+inline int32_t mode_class(int32_t mode) {
+    return mode == kModeKP16 ? 1 : (mode == kModeGeneric ? 2 : 0);
+}
+
+constexpr int32_t kLaunchClasses = 4;
+constexpr int64_t kLdsBudgetBytes = 32768;  // largest table staged in LDS per block
+constexpr int32_t kDescHeader = 16;
+
+// Sweep descriptor of a node (int32 words at desc_off[i]):
+//   [0] K  [1] KP  [2] mode  [3] tab_begin  [4] tab_len (floats)
+//   [5] cond_off  [6] cond_len (threshold words)  [7] KT
+//   [8] n_tent  [9] tent (relative word index of the threshold-path entries)
+//   [10] n_pent  [11] pent (relative word index of the product-path entries)
+//   [12] staged (1: the block copies its table into LDS)
+// Entries are (node, mult, arg) triples walked in order: arg -3 is the node's
+// own row (read for the write-back), -1 adds mult * state to the running own
+// (or threshold) index, -2 adds to the running child index, and arg >= 0
+// starts a child whose k-vector table begins at relative float offset arg
+// (mult = KP multiplies the child's own state).  Product-path indices are
+// float offsets relative to tab_begin; threshold indices are word offsets
+// relative to cond_off.
+
 struct Compiled {
     int32_t n = 0;
     std::vector<int32_t> pptr, pidx, card;
@@ -62,29 +95,44 @@ struct Compiled {
     int64_t table_floats = 0;
     std::vector<Segment> segments;
 
-    // flat descriptor stream read by the sweep kernel, and per-node offsets
-    //   [K, KP, own_off, n_par, n_child,
-    //    (par_node, par_mult) * n_par,
-    //    per child: (h, ctab_off, xh_mult, n_cop, (cop_node, cop_mult) * n_cop)]
-    // par_mult = parent stride * KP; xh_mult = KP; cop_mult = compact stride * K_h * KP
+    // per-node table records and the sweep descriptors (layout above)
+    std::vector<int64_t> tab_begin, tab_len;  // [n], floats
+    std::vector<int32_t> lds_bytes;           // [n], 0: tables read from global memory
     std::vector<int32_t> desc;
     std::vector<int32_t> desc_off;   // [n]
+
+    // precomputed conditional tables: for a node in table mode, every
+    // configuration of its Markov blanket (blanket nodes in ascending id, last
+    // fastest) holds KT uint32 thresholds T_k = ceil(2^24 * S_k / Z), k < K-1,
+    // padded with 2^24; the draw is #{k : T_k <= u24}.
+    int64_t cond_words = 0;
+    // build program per table node, read by the threshold-build kernel:
+    //   [K, KT, cond_off, n_cfg, n_bl, bl_card * n_bl, own_cpt_off, n_par,
+    //    (bl_pos, stride) * n_par, n_child,
+    //    per child: (cpt_off_h, K_h, s_i, xh_pos, n_cop, (bl_pos, stride) * n_cop)]
+    std::vector<int32_t> cprog;
+    std::vector<int32_t> cprog_off;  // per table node
+    std::vector<int32_t> cprog_nodes;
     // same for the count kernel: [K, n_par, n_bins, cpt_off, (par_node, stride) * n_par]
     std::vector<int32_t> cdesc;
     std::vector<int32_t> cdesc_off;  // [n]
 
-    // colour-ordered node list (colour 0 nodes, then colour 1, ...) and the
-    // start of each colour in it, and each colour's largest KP
+    // colour-ordered node list (colour 0 nodes, then colour 1, ...; inside a
+    // colour grouped by launch class) and, per colour, the start of each class
+    // range: launch[c*5 + k] .. launch[c*5 + k + 1] for class k < 4
     std::vector<int32_t> order;
-    std::vector<int32_t> color_start;  // [n_colors+1]
-    std::vector<int32_t> color_kp;     // [n_colors]
+    std::vector<int32_t> launch;       // [n_colors * (kLaunchClasses + 1)]
+    std::vector<int32_t> launch_lds;   // [n_colors * kLaunchClasses]
+    std::vector<int32_t> mode;         // [n]
 
     // CPT rows, for the Dirichlet normalisation: entry offset and K of each row
     std::vector<int32_t> row_off, row_k;
 };
 
 // Returns 0 or a negative SAME_E* code with a message in err.
+// table_limit: largest KT * (number of blanket configurations) for which a
+// node gets a precomputed threshold table (0 disables the table path).
 int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int32_t *card,
-                  Compiled &out, std::string &err);
+                  Compiled &out, std::string &err, int64_t table_limit = 16384);
 
 }  // namespace same

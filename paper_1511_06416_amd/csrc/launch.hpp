@@ -23,17 +23,29 @@ struct DeviceTables {
     int32_t n_build_blocks = 0;
     int32_t *row_off = nullptr;    // [n_rows]
     int32_t *row_k = nullptr;      // [n_rows]
+    int32_t *cprog = nullptr;      // threshold build programs
+    int32_t *cprog_off = nullptr;
+    int32_t *cblk_prog = nullptr;  // threshold-build block -> program
+    int32_t *cblk_first = nullptr; // threshold-build block -> first configuration
+    int32_t n_cond_blocks = 0;
 };
 
-struct SweepArgs {
-    const DeviceTables *t;
-    const float *table;     // regrouped k-vector tables (workspace)
+// Kernel arguments of the sweep (passed by value).
+struct SweepParams {
+    const int32_t *desc;
+    const int32_t *desc_off;
+    const int32_t *order;
+    int32_t begin;                 // first entry of order[] in this launch
+    const float *table;            // regrouped k-vector tables (workspace)
+    const uint32_t *cond;          // threshold tables (workspace)
     void *states;
     const uint8_t *obs;
     int32_t m;
     int64_t n_cols, ld, col_offset;
     uint32_t key0, key1, sweep_id;
-    int64_t win_begin, win;  // debug window (win == 0: none)
+    int64_t quads_per_block;       // set by the launcher
+    int32_t reps_per_block;        // set by the launcher
+    int64_t win_begin, win;        // debug window (win == 0: none)
     float *probs;
     int32_t max_card;
 };
@@ -41,9 +53,14 @@ struct SweepArgs {
 hipError_t launch_build_tables(const DeviceTables &t, const float *cpts, float *table,
                                hipStream_t stream);
 
-// One colour group: nodes order[begin .. begin+count), all with KP <= kp.
-hipError_t launch_sweep_color(const SweepArgs &a, int32_t begin, int32_t count, int32_t kp,
-                              int32_t state_bytes, hipStream_t stream);
+hipError_t launch_build_thresholds(const DeviceTables &t, const float *cpts, uint32_t *cond,
+                                   hipStream_t stream);
+
+// Nodes order[begin .. begin+count) of one colour, all of launch class klass
+// (0: main kernel, tables staged in lds_bytes of LDS; 1: main kernel, tables
+// in global memory; 2: KP 16; 3: generic).
+hipError_t launch_sweep(SweepParams P, int32_t begin, int32_t count, int32_t klass,
+                        int32_t lds_bytes, int32_t state_bytes, hipStream_t stream);
 
 hipError_t launch_fill_zero(int32_t *p, int64_t count, hipStream_t stream);
 

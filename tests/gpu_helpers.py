@@ -12,9 +12,12 @@ REL_TOL = 1e-5       # conditionals, fp32 vs fp64
 TINY = 1e-30         # below this the oracle's probability is not compared relatively
 
 
-def context_for(net, prior=1.0):
+def context_for(net, prior=1.0, table_limit=None):
+    """Library context; table_limit=0 forces every node onto the product path."""
     pptr, pidx, card = net.csr()
-    return same.same_create(pptr, pidx, card, prior)
+    if table_limit is None:
+        return same.same_create(pptr, pidx, card, prior)
+    return same.same_create_ex(pptr, pidx, card, prior, table_limit)
 
 
 def gpu_sweep(ctx, states_np, obs_np, theta_np, m, n_cols, col_offset, seed, sweep_id, win=None,

@@ -27,9 +27,9 @@ def _gpu():
     same.load_library()
 
 
-def _sweep_case(w, b=0, sweep_id=3, win=None, theta=None, n_threads=0):
+def _sweep_case(w, b=0, sweep_id=3, win=None, theta=None, n_threads=0, table_limit=None):
     net = w.net
-    ctx = H.context_for(net)
+    ctx = H.context_for(net, table_limit=table_limit)
     color = oracle.graph(net.parents, net.card)["color"]
     assert np.array_equal(ctx.color, color)
     theta = w.init_theta if theta is None else theta
@@ -58,9 +58,10 @@ def _sweep_case(w, b=0, sweep_id=3, win=None, theta=None, n_threads=0):
     (4, {}, (0, 600)),                                   # two-layer concepts, m=20
     (5, dict(n_cols=5_000), (4_600, 400)),               # 1000-node random DAG, m=10
 ])
-def test_sweep_parity_configs(cfg, kw, win):
+@pytest.mark.parametrize("table_limit", [None, 0], ids=["tables", "products"])
+def test_sweep_parity_configs(cfg, kw, win, table_limit):
     w = make_workload(cfg, **kw)
-    out = _sweep_case(w, win=win)
+    out = _sweep_case(w, win=win, table_limit=table_limit)
     assert out["probs"]["checked"] > 0
 
 
@@ -111,8 +112,9 @@ def _custom(parents, card, n_cols, m, hidden, seed, ld=None, theta=None, alpha=0
     return Network("custom", parents, card), states, obs, theta
 
 
-def _custom_case(net, states, obs, theta, m, n_cols, col_offset=0, win=None, sweep_id=1, seed=5):
-    ctx = H.context_for(net)
+def _custom_case(net, states, obs, theta, m, n_cols, col_offset=0, win=None, sweep_id=1, seed=5,
+                 table_limit=None):
+    ctx = H.context_for(net, table_limit=table_limit)
     color = oracle.graph(net.parents, net.card)["color"]
     gpu, gp = H.gpu_sweep(ctx, states, obs, theta, m, n_cols, col_offset, seed, sweep_id, win=win)
     ref = states.copy()
@@ -155,21 +157,23 @@ def test_all_observed_and_all_latent():
     _custom_case(net, st, ob, th, 2, 512, win=(0, 512))
 
 
-@pytest.mark.parametrize("K", [5, 9, 16, 17, 40])
-def test_cardinality_classes(K):
-    # KP = 8 and 16 register paths, and the generic path for K > 16
+@pytest.mark.parametrize("table_limit", [None, 0], ids=["tables", "products"])
+@pytest.mark.parametrize("K", [2, 3, 5, 8, 9, 16, 17, 40])
+def test_cardinality_classes(K, table_limit):
+    # threshold tables for K <= 9, products with KP = 2/4/8/16, generic for K > 16
     parents = [[], [0], [0, 1], [1], [2, 3]]
     card = [K, 3, K, 2, 4]
     net, st, ob, th = _custom(parents, card, 700, 3, 0.6, K)
-    _custom_case(net, st, ob, th, 3, 700, win=(0, 128))
+    _custom_case(net, st, ob, th, 3, 700, win=(0, 128), table_limit=table_limit)
 
 
-def test_int16_states():
-    parents = [[], [0], [0, 1], [2]]
-    card = [130, 3, 200, 2]
+@pytest.mark.parametrize("table_limit", [None, 0], ids=["tables", "products"])
+def test_int16_states(table_limit):
+    parents = [[], [0], [0, 1], [2], [1]]
+    card = [130, 3, 200, 2, 5]
     net, st, ob, th = _custom(parents, card, 300, 2, 0.5, 17)
     assert st.dtype == np.int16
-    _custom_case(net, st, ob, th, 2, 300, win=(0, 64))
+    _custom_case(net, st, ob, th, 2, 300, win=(0, 64), table_limit=table_limit)
 
 
 def test_large_replica_count_and_column_offset():
@@ -196,9 +200,10 @@ def test_underflow_rescale_path():
     ob[0, :n_cols] = 0
     ob[1:, :n_cols] = 1
     st[1:, :, :n_cols] = 1
-    gpu, ref, _ = _custom_case(net, st, ob, theta, m, n_cols, win=(0, 64))
-    # the conditional of the root is exactly (1/2, 1/2); both states must appear
-    assert 0 < gpu[0, :, :n_cols].mean() < 1
+    for tl in (None, 0):
+        gpu, ref, _ = _custom_case(net, st, ob, theta, m, n_cols, win=(0, 64), table_limit=tl)
+        # the conditional of the root is exactly (1/2, 1/2); both states must appear
+        assert 0 < gpu[0, :, :n_cols].mean() < 1
 
 
 def test_zero_cpt_entries_clamped():
