@@ -48,6 +48,9 @@ def parse():
                         "kernels run on the GPU, for counter collection)")
     p.add_argument("--table-limit", type=int, default=None,
                    help="threshold-table size limit passed to same_create_ex (0: products only)")
+    p.add_argument("--no-stream", action="store_true",
+                   help="skip the out-of-core (pinned host memory) timing")
+    p.add_argument("--stream-steps", type=int, default=2)
     p.add_argument("--minibatches", type=int, default=None,
                    help="process only the first K minibatches (profiling runs)")
     return p.parse_args()
@@ -147,12 +150,12 @@ def main():
     node_samples = float(net.n) * cols_timed * w.m * args.steps
     value = node_samples / elapsed
     sweep_s = sum(a.elapsed_time(b) for a, b in sweep_ev) / 1e3
-    launches = len(sweep_ev) * ctx.n_colors
+    launches = len(sweep_ev) * ctx.sweep_launches
     bytes_per_ns = 1.0 + hidden + 1.0 / w.m   # read each state, write each latent, obs per column
     alg_bytes = node_samples * bytes_per_ns
     achieved = alg_bytes / sweep_s / 1e9
     roofline = {
-        "kernel": "sweep_color_kernel (all colour groups)",
+        "kernel": "sweep_main_kernel (every colour-group launch of a sweep)",
         "bound": "hbm",
         "achieved": round(achieved, 1),
         "peak": HBM_PEAK_GBS,
@@ -172,6 +175,10 @@ def main():
         b2.copy_(a)
         torch.cuda.synchronize()
         del a, b2
+
+    streamed = None
+    if not args.no_stream and len(mbs) == w.M:
+        streamed = stream_timing(w, ctx, cpts, ws, dev, args.stream_steps)
 
     cpu = None
     if sample is not None:
@@ -210,8 +217,57 @@ def main():
         "hbm_gbs_algorithmic_step": round(alg_bytes / elapsed / 1e9, 1),
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "streamed_from_host": streamed,
+        "table_nodes": ctx.table_nodes,
     }
     print(json.dumps(out), flush=True)
+
+
+def stream_timing(w, ctx, cpts, ws, dev, steps):
+    """End-to-end out-of-core passes: every minibatch is copied from pinned host
+    memory to the device, swept, counted and resampled, and copied back
+    (same_stream_pass).  Reported beside the HBM-resident value, never as it."""
+    import torch
+
+    import paper_1511_06416_amd as same
+
+    net = w.net
+    host_ld = (w.n_cols + 3) // 4 * 4
+    t0 = time.time()
+    hs = torch.empty((net.n, w.m, host_ld), dtype=w.states[0].dtype, pin_memory=True)
+    ho = torch.empty((net.n, host_ld), dtype=torch.uint8, pin_memory=True)
+    for b in range(w.M):
+        c0, nc = b * w.nb, w.mb_cols(b)
+        for i in range(net.n):
+            hs[i, :, c0:c0 + nc].copy_(w.states[b][i, :, :nc])
+            ho[i, c0:c0 + nc].copy_(w.obs[b][i, :nc])
+    torch.cuda.synchronize()
+    log("pinned host copy of the data (%.1f GB) in %.1f s" % (
+        (hs.numel() * hs.element_size() + ho.numel()) / 1e9, time.time() - t0))
+    slots = torch.empty(same.same_stream_slots_size(ctx, w.m, w.nb), dtype=torch.uint8, device=dev)
+    mb = torch.zeros((w.M, ctx.cpt_total), dtype=torch.int32, device=dev)
+    tot = torch.zeros(ctx.cpt_total, dtype=torch.int32, device=dev)
+    same.same_stream_pass(ctx, hs, ho, host_ld, w.n_cols, w.nb, w.m, cpts, mb, tot, w.seed, 0,
+                          same.SAME_STREAM_COUNTS_ONLY, slots, ws)
+    same.same_stream_pass(ctx, hs, ho, host_ld, w.n_cols, w.nb, w.m, cpts, mb, tot, w.seed, 0, 0,
+                          slots, ws)
+    torch.cuda.synchronize()
+    t = time.perf_counter()
+    for s in range(1, 1 + steps):
+        same.same_stream_pass(ctx, hs, ho, host_ld, w.n_cols, w.nb, w.m, cpts, mb, tot, w.seed, s,
+                              0, slots, ws)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t
+    ns = float(net.n) * w.n_cols * w.m * steps
+    state_bytes = float(net.n) * w.m * w.n_cols * hs.element_size()
+    h2d = state_bytes + float(net.n) * w.n_cols
+    log("streamed %d passes in %.3f s" % (steps, dt))
+    del hs, ho
+    return {"value": round(ns / dt, 1), "unit": "node-samples/s", "passes": steps,
+            "ms_per_pass": round(dt * 1e3 / steps, 2),
+            "pcie_bytes_per_pass": {"h2d": h2d, "d2h": state_bytes},
+            "pcie_gbs_each_way": {"h2d": round(h2d * steps / dt / 1e9, 1),
+                                  "d2h": round(state_bytes * steps / dt / 1e9, 1)}}
 
 
 def cpu_baseline(w, cols, st, ob):

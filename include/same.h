@@ -77,6 +77,8 @@ typedef struct {
     int64_t n_rows;       /* CPT rows (distributions) */
     int32_t state_bytes;  /* 1: int8 states, 2: int16 states */
     int32_t max_card;     /* largest K_i */
+    int32_t sweep_launches;  /* sweep kernel launches per same_sweep call */
+    int32_t table_nodes;     /* nodes drawing from precomputed threshold tables */
 } same_layout_t;
 
 /*
@@ -178,6 +180,41 @@ int same_counts(same_ctx *ctx, const void *states, int32_t m, int64_t n_cols, in
  */
 int same_sample_cpts(same_ctx *ctx, const int32_t *totals, float *cpts_out, uint64_t seed,
                      uint32_t update_id, void *workspace, void *stream);
+
+/*
+ * Out-of-core passes (Sec. 4: the sampler keeps only model-sized state on the
+ * device and streams the data; Sec. 6: the GPU's memory, not the data size,
+ * limits the problem).  The data stay in host memory -- pinned (page-locked)
+ * for the copies to overlap -- laid out like a device minibatch but with the
+ * full column range: states [n][m][host_ld], obs [n][host_ld], column j is
+ * global column j.  Minibatch b covers columns [b*nb, min((b+1)*nb, n_cols)).
+ *
+ * same_stream_pass runs one pass over all M = ceil(n_cols / nb) minibatches:
+ * per minibatch b it copies the minibatch to the device (upload stream), runs
+ * same_sweep (col_offset b*nb, sweep_id = pass_id), same_counts into
+ * mb_counts[b] and totals, and same_sample_cpts (update_id = pass_id*M + b)
+ * on `stream`, then copies the new states back to the host (download stream).
+ * Two device slots alternate, so the upload of b+1 and the download of b-1
+ * overlap the compute of b.  With flags & SAME_STREAM_COUNTS_ONLY it only
+ * uploads and counts (the count-only pre-pass that initialises mb_counts and
+ * totals before the first sweep; mb_counts and totals must be zero on entry).
+ *
+ * cpts [cpt_total] (device, in/out), mb_counts [M][cpt_total] and totals
+ * [cpt_total] (device) persist between passes.  slots (device, at least
+ * same_stream_slots_size bytes, 256-byte aligned) holds the two slots;
+ * workspace is the same_workspace_size buffer.  nb must be a multiple of 4.
+ * The call returns when everything is enqueued; the host states are final
+ * once `stream` has been synchronised.  The caller must not touch the host
+ * buffers or `stream`'s work until then.
+ */
+enum { SAME_STREAM_COUNTS_ONLY = 1 };
+
+int same_stream_slots_size(const same_ctx *ctx, int32_t m, int64_t nb, size_t *bytes);
+
+int same_stream_pass(same_ctx *ctx, void *host_states, const uint8_t *host_obs, int64_t host_ld,
+                     int64_t n_cols, int64_t nb, int32_t m, float *cpts, int32_t *mb_counts,
+                     int32_t *totals, uint64_t seed, uint32_t pass_id, int32_t flags, void *slots,
+                     void *workspace, void *stream);
 
 /* Message for the calling thread's last failed call ("" if none). */
 const char *same_last_error(void);

@@ -18,6 +18,7 @@ import numpy as np
 __all__ = [
     "SameError", "Context", "same_create", "same_create_ex", "same_destroy", "same_layout", "same_workspace_size",
     "same_sweep", "same_sweep_debug", "same_counts", "same_sample_cpts", "same_last_error",
+    "same_stream_slots_size", "same_stream_pass", "SAME_STREAM_COUNTS_ONLY",
     "library_path", "load_library",
 ]
 
@@ -28,6 +29,7 @@ _lib = None
 
 SAME_OK, SAME_EINVAL, SAME_EGRAPH, SAME_ECARD, SAME_ESIZE, SAME_ENOMEM, SAME_EHIP, SAME_EALIGN = (
     0, -1, -2, -3, -4, -5, -6, -7)
+SAME_STREAM_COUNTS_ONLY = 1
 _NAMES = {0: "SAME_OK", -1: "SAME_EINVAL", -2: "SAME_EGRAPH", -3: "SAME_ECARD",
           -4: "SAME_ESIZE", -5: "SAME_ENOMEM", -6: "SAME_EHIP", -7: "SAME_EALIGN"}
 
@@ -44,7 +46,8 @@ class _Options(C.Structure):
 
 class _Layout(C.Structure):
     _fields_ = [("n_nodes", C.c_int32), ("n_colors", C.c_int32), ("cpt_total", C.c_int64),
-                ("n_rows", C.c_int64), ("state_bytes", C.c_int32), ("max_card", C.c_int32)]
+                ("n_rows", C.c_int64), ("state_bytes", C.c_int32), ("max_card", C.c_int32),
+                ("sweep_launches", C.c_int32), ("table_nodes", C.c_int32)]
 
 
 def library_path() -> str:
@@ -71,10 +74,13 @@ def load_library():
         L.same_sweep_debug.argtypes = [P, P, P, P, I32, I64, I64, I64, U64, U32, I64, I64, P, P, P]
         L.same_counts.argtypes = [P, P, I32, I64, I64, P, P, P, P]
         L.same_sample_cpts.argtypes = [P, P, P, U64, U32, P, P]
+        L.same_stream_slots_size.argtypes = [P, I32, I64, C.POINTER(C.c_size_t)]
+        L.same_stream_pass.argtypes = [P, P, P, I64, I64, I64, I32, P, P, P, U64, U32, I32, P, P, P]
         L.same_last_error.argtypes = []
         L.same_last_error.restype = C.c_char_p
         for f in ("same_create", "same_create_ex", "same_layout", "same_workspace_size", "same_sweep",
-                  "same_sweep_debug", "same_counts", "same_sample_cpts"):
+                  "same_sweep_debug", "same_counts", "same_sample_cpts", "same_stream_slots_size",
+                  "same_stream_pass"):
             getattr(L, f).restype = C.c_int
         _lib = L
         return L
@@ -132,6 +138,7 @@ class Context:
         self.n_nodes, self.n_colors = lay.n_nodes, lay.n_colors
         self.cpt_total, self.n_rows = lay.cpt_total, lay.n_rows
         self.state_bytes, self.max_card = lay.state_bytes, lay.max_card
+        self.sweep_launches, self.table_nodes = lay.sweep_launches, lay.table_nodes
         self.cpt_off, self.color = off, col
         ws = C.c_size_t()
         _check(L.same_workspace_size(self._h, C.byref(ws)))
@@ -173,6 +180,7 @@ def same_destroy(ctx: Context) -> None:
 def same_layout(ctx: Context) -> dict:
     return {"n_nodes": ctx.n_nodes, "n_colors": ctx.n_colors, "cpt_total": ctx.cpt_total,
             "n_rows": ctx.n_rows, "state_bytes": ctx.state_bytes, "max_card": ctx.max_card,
+            "sweep_launches": ctx.sweep_launches, "table_nodes": ctx.table_nodes,
             "cpt_off": ctx.cpt_off.copy(), "color": ctx.color.copy()}
 
 
@@ -204,3 +212,19 @@ def same_counts(ctx, states, m, n_cols, ld, mb_counts, totals, workspace, stream
 def same_sample_cpts(ctx, totals, cpts_out, seed, update_id, workspace, stream=None):
     _check(load_library().same_sample_cpts(ctx.handle, _ptr(totals), _ptr(cpts_out), int(seed),
                                            int(update_id), _ptr(workspace), _stream(stream)))
+
+
+def same_stream_slots_size(ctx, m, nb) -> int:
+    out = C.c_size_t()
+    _check(load_library().same_stream_slots_size(ctx.handle, int(m), int(nb), C.byref(out)))
+    return int(out.value)
+
+
+def same_stream_pass(ctx, host_states, host_obs, host_ld, n_cols, nb, m, cpts, mb_counts, totals,
+                     seed, pass_id, flags, slots, workspace, stream=None):
+    """host_states / host_obs: pinned host tensors (or addresses); the rest device."""
+    _check(load_library().same_stream_pass(ctx.handle, _ptr(host_states), _ptr(host_obs),
+                                           int(host_ld), int(n_cols), int(nb), int(m), _ptr(cpts),
+                                           _ptr(mb_counts), _ptr(totals), int(seed), int(pass_id),
+                                           int(flags), _ptr(slots), _ptr(workspace),
+                                           _stream(stream)))

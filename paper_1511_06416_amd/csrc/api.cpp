@@ -27,10 +27,20 @@ inline size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
 }  // namespace
 
+// Copy streams and events of the out-of-core passes, per device.
+struct StreamRes {
+    int device = -1;
+    hipStream_t up = nullptr, down = nullptr;
+    hipEvent_t ev_up[2] = {nullptr, nullptr}, ev_comp[2] = {nullptr, nullptr},
+               ev_down[2] = {nullptr, nullptr};
+    bool slot_used[2] = {false, false};
+};
+
 struct same_ctx {
     same::Compiled g;
     double alpha = 1.0;
     std::vector<same::DeviceTables> dev;  // indexed by device ordinal
+    std::vector<StreamRes> sres;          // indexed by device ordinal
     std::mutex mu;
     // workspace layout
     size_t ws_table = 0, ws_cond = 0, ws_counts = 0, ws_gamma = 0, ws_total = 0;
@@ -119,6 +129,53 @@ int tables_for_current_device(same_ctx *ctx, same::DeviceTables **out) {
     return SAME_OK;
 }
 
+void free_stream_res(StreamRes &r) {
+    if (r.device < 0) return;
+    int cur = -1;
+    (void)hipGetDevice(&cur);
+    (void)hipSetDevice(r.device);
+    if (r.up) (void)hipStreamSynchronize(r.up);
+    if (r.down) (void)hipStreamSynchronize(r.down);
+    for (int i = 0; i < 2; ++i) {
+        if (r.ev_up[i]) (void)hipEventDestroy(r.ev_up[i]);
+        if (r.ev_comp[i]) (void)hipEventDestroy(r.ev_comp[i]);
+        if (r.ev_down[i]) (void)hipEventDestroy(r.ev_down[i]);
+    }
+    if (r.up) (void)hipStreamDestroy(r.up);
+    if (r.down) (void)hipStreamDestroy(r.down);
+    if (cur >= 0) (void)hipSetDevice(cur);
+    r = StreamRes();
+}
+
+int stream_res_for_current_device(same_ctx *ctx, StreamRes **out) {
+    int device = -1;
+    hipError_t e = hipGetDevice(&device);
+    if (e != hipSuccess) return set_error(SAME_EHIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+    std::lock_guard<std::mutex> lock(ctx->mu);
+    if ((int)ctx->sres.size() <= device) ctx->sres.resize(device + 1);
+    StreamRes &r = ctx->sres[device];
+    if (r.device == device) {
+        *out = &r;
+        return SAME_OK;
+    }
+    StreamRes nr;
+    nr.device = device;
+    hipError_t h = hipStreamCreateWithFlags(&nr.up, hipStreamNonBlocking);
+    if (h == hipSuccess) h = hipStreamCreateWithFlags(&nr.down, hipStreamNonBlocking);
+    for (int i = 0; i < 2 && h == hipSuccess; ++i) {
+        h = hipEventCreateWithFlags(&nr.ev_up[i], hipEventDisableTiming);
+        if (h == hipSuccess) h = hipEventCreateWithFlags(&nr.ev_comp[i], hipEventDisableTiming);
+        if (h == hipSuccess) h = hipEventCreateWithFlags(&nr.ev_down[i], hipEventDisableTiming);
+    }
+    if (h != hipSuccess) {
+        free_stream_res(nr);
+        return set_error(SAME_EHIP, std::string("creating copy streams: ") + hipGetErrorString(h));
+    }
+    r = nr;
+    *out = &r;
+    return SAME_OK;
+}
+
 int check_hip(hipError_t e, const char *what) {
     if (e == hipSuccess) return SAME_OK;
     return set_error(SAME_EHIP, std::string(what) + ": " + hipGetErrorString(e));
@@ -199,6 +256,21 @@ int do_sweep(same_ctx *ctx, void *states, const uint8_t *obs, const float *cpts,
     return SAME_OK;
 }
 
+// Device slot geometry of the out-of-core passes.
+struct SlotGeom {
+    int64_t ld = 0;          // leading dimension of a slot (columns)
+    size_t states = 0;       // bytes of the states part
+    size_t bytes = 0;        // bytes of one slot (states + obs)
+};
+
+SlotGeom slot_geom(const same_ctx *ctx, int32_t m, int64_t nb) {
+    SlotGeom s;
+    s.ld = (nb + 63) / 64 * 64;
+    s.states = align_up((size_t)ctx->g.n * (size_t)m * (size_t)s.ld * ctx->g.state_bytes);
+    s.bytes = s.states + align_up((size_t)ctx->g.n * (size_t)s.ld);
+    return s;
+}
+
 }  // namespace
 
 extern "C" {
@@ -245,6 +317,7 @@ int same_create_ex(int32_t n_nodes, const int32_t *parent_ptr, const int32_t *pa
 
 void same_destroy(same_ctx *ctx) {
     if (!ctx) return;
+    for (auto &r : ctx->sres) free_stream_res(r);
     for (auto &t : ctx->dev) free_tables(t);
     delete ctx;
 }
@@ -258,6 +331,17 @@ int same_layout(const same_ctx *ctx, same_layout_t *out, int64_t *cpt_off, int32
     out->n_rows = g.n_rows;
     out->state_bytes = g.state_bytes;
     out->max_card = g.max_card;
+    const int32_t L = same::kLaunchClasses;
+    int32_t launches = 0;
+    for (int32_t c = 0; c < g.n_colors; ++c)
+        for (int32_t k = 0; k < L; ++k) {
+            const int32_t cnt = g.launch[c * (L + 1) + k + 1] - g.launch[c * (L + 1) + k];
+            launches += (cnt + 65534) / 65535;
+        }
+    out->sweep_launches = launches;
+    int32_t tn = 0;
+    for (int32_t i = 0; i < g.n; ++i) tn += g.mode[i] == same::kModeTable ? 1 : 0;
+    out->table_nodes = tn;
     if (cpt_off) std::memcpy(cpt_off, g.off.data(), sizeof(int64_t) * (g.n + 1));
     if (color) std::memcpy(color, g.color.data(), sizeof(int32_t) * g.n);
     return SAME_OK;
@@ -323,6 +407,92 @@ int same_sample_cpts(same_ctx *ctx, const int32_t *totals, float *cpts_out, uint
                    "gamma launch");
     if (rc) return rc;
     return check_hip(same::launch_normalize(*t, gv, cpts_out, ctx->g.n_rows, s), "normalize launch");
+}
+
+int same_stream_slots_size(const same_ctx *ctx, int32_t m, int64_t nb, size_t *bytes) {
+    if (!ctx || !bytes) return set_error(SAME_EINVAL, "ctx and bytes must be non-null");
+    if (m < 1 || m > 65535 || nb < 4) return set_error(SAME_EINVAL, "need 1 <= m <= 65535 and nb >= 4");
+    *bytes = 2 * slot_geom(ctx, m, nb).bytes;
+    return SAME_OK;
+}
+
+int same_stream_pass(same_ctx *ctx, void *host_states, const uint8_t *host_obs, int64_t host_ld,
+                     int64_t n_cols, int64_t nb, int32_t m, float *cpts, int32_t *mb_counts,
+                     int32_t *totals, uint64_t seed, uint32_t pass_id, int32_t flags, void *slots,
+                     void *workspace, void *stream) {
+    if (!ctx) return set_error(SAME_EINVAL, "ctx is null");
+    if (!host_states || !host_obs || !cpts || !mb_counts || !totals || !slots || !workspace)
+        return set_error(SAME_EINVAL, "null pointer argument");
+    if (m < 1 || m > 65535) return set_error(SAME_EINVAL, "m must be in [1, 65535]");
+    if (nb < 4 || nb % 4 != 0) return set_error(SAME_EALIGN, "nb must be a positive multiple of 4");
+    if (n_cols < 0 || host_ld < n_cols) return set_error(SAME_EINVAL, "need 0 <= n_cols <= host_ld");
+    if (flags & ~SAME_STREAM_COUNTS_ONLY) return set_error(SAME_EINVAL, "unknown flags");
+    if (!aligned(slots, kAlign)) return set_error(SAME_EALIGN, "slots must be 256-byte aligned");
+    if (n_cols == 0) return SAME_OK;
+    const int64_t M = (n_cols + nb - 1) / nb;
+    if ((double)M * (double)pass_id + M > 4294967295.0)
+        return set_error(SAME_ESIZE, "pass_id * minibatches exceeds the update-id range");
+    const SlotGeom sg = slot_geom(ctx, m, nb);
+    StreamRes *sr = nullptr;
+    int rc = stream_res_for_current_device(ctx, &sr);
+    if (rc) return rc;
+    hipStream_t cs = (hipStream_t)stream;
+    const size_t sb = (size_t)ctx->g.state_bytes;
+    const int64_t rows = (int64_t)ctx->g.n * m;
+    const int64_t total = ctx->g.off[ctx->g.n];
+    const bool counts_only = (flags & SAME_STREAM_COUNTS_ONLY) != 0;
+    for (int64_t b = 0; b < M; ++b) {
+        const int s = (int)(b & 1);
+        const int64_t c0 = b * nb;
+        const int64_t cols = n_cols - c0 < nb ? n_cols - c0 : nb;
+        char *slot = (char *)slots + s * sg.bytes;
+        void *d_states = slot;
+        uint8_t *d_obs = (uint8_t *)(slot + sg.states);
+        // upload (after the slot's previous minibatch has left it)
+        if (sr->slot_used[s] && (rc = check_hip(hipStreamWaitEvent(sr->up, sr->ev_down[s], 0), "wait")))
+            return rc;
+        rc = check_hip(hipMemcpy2DAsync(d_states, sg.ld * sb, (char *)host_states + c0 * sb, host_ld * sb,
+                                        cols * sb, rows, hipMemcpyHostToDevice, sr->up),
+                       "state upload");
+        if (!rc)
+            rc = check_hip(hipMemcpy2DAsync(d_obs, sg.ld, host_obs + c0, host_ld, cols, ctx->g.n,
+                                            hipMemcpyHostToDevice, sr->up),
+                           "obs upload");
+        if (!rc) rc = check_hip(hipEventRecord(sr->ev_up[s], sr->up), "event");
+        if (!rc) rc = check_hip(hipStreamWaitEvent(cs, sr->ev_up[s], 0), "wait");
+        if (rc) return rc;
+        int32_t *mb = mb_counts + b * total;
+        if (!counts_only) {
+            rc = do_sweep(ctx, d_states, d_obs, cpts, m, cols, sg.ld, c0, seed, pass_id, 0, 0, nullptr,
+                          workspace, stream);
+            if (rc) return rc;
+        }
+        rc = same_counts(ctx, d_states, m, cols, sg.ld, mb, totals, workspace, stream);
+        if (rc) return rc;
+        if (!counts_only) {
+            rc = same_sample_cpts(ctx, totals, cpts, seed, (uint32_t)(pass_id * M + b), workspace, stream);
+            if (rc) return rc;
+        }
+        rc = check_hip(hipEventRecord(sr->ev_comp[s], cs), "event");
+        if (rc) return rc;
+        if (counts_only) {
+            rc = check_hip(hipEventRecord(sr->ev_down[s], cs), "event");
+        } else {
+            rc = check_hip(hipStreamWaitEvent(sr->down, sr->ev_comp[s], 0), "wait");
+            if (!rc)
+                rc = check_hip(hipMemcpy2DAsync((char *)host_states + c0 * sb, host_ld * sb, d_states,
+                                                sg.ld * sb, cols * sb, rows, hipMemcpyDeviceToHost, sr->down),
+                               "state download");
+            if (!rc) rc = check_hip(hipEventRecord(sr->ev_down[s], sr->down), "event");
+        }
+        if (rc) return rc;
+        sr->slot_used[s] = true;
+    }
+    // the caller's stream completes only after the last downloads
+    for (int s = 0; s < 2; ++s)
+        if (sr->slot_used[s] && (rc = check_hip(hipStreamWaitEvent(cs, sr->ev_down[s], 0), "wait")))
+            return rc;
+    return SAME_OK;
 }
 
 }  // extern "C"

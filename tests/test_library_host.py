@@ -160,3 +160,30 @@ def test_null_context():
     assert L.same_layout(None, None, None, None) == same.SAME_EINVAL
     assert L.same_workspace_size(None, None) == same.SAME_EINVAL
     L.same_destroy(None)
+
+
+def test_stream_argument_errors():
+    ctx = _ctx(koller())
+    L = same.load_library()
+    P = C.c_void_p
+    good = dict(hs=FAKE, ho=FAKE, host_ld=1000, n_cols=1000, nb=256, m=2, flags=0, slots=FAKE)
+
+    def call(**kw):
+        a = dict(good)
+        a.update(kw)
+        return L.same_stream_pass(ctx.handle, P(a["hs"]), P(a["ho"]), a["host_ld"], a["n_cols"],
+                                  a["nb"], a["m"], P(FAKE), P(FAKE), P(FAKE), 1, 0, a["flags"],
+                                  P(a["slots"]), P(FAKE), None)
+
+    assert call(nb=250) == same.SAME_EALIGN
+    assert call(nb=0) == same.SAME_EALIGN
+    assert call(host_ld=999) == same.SAME_EINVAL
+    assert call(m=0) == same.SAME_EINVAL
+    assert call(hs=0) == same.SAME_EINVAL
+    assert call(flags=4) == same.SAME_EINVAL
+    assert call(slots=FAKE + 64) == same.SAME_EALIGN
+    assert call(n_cols=0) == same.SAME_OK
+    size = C.c_size_t()
+    assert L.same_stream_slots_size(ctx.handle, 2, 256, C.byref(size)) == same.SAME_OK
+    # two slots of 5 nodes x 2 replicas x 256 columns plus 5 x 256 obs bytes
+    assert size.value >= 2 * (5 * 2 * 256 + 5 * 256)
