@@ -114,24 +114,13 @@ def main():
     for b in mbs:
         same.same_counts(ctx, w.states[b], w.m, w.mb_cols(b), w.ld, mb[b], tot, ws)
 
-    sweep_ev = []
-
-    def one_pass(s, record):
+    def one_pass(s):
         for b in mbs:
-            if record:
-                e0 = torch.cuda.Event(enable_timing=True)
-                e1 = torch.cuda.Event(enable_timing=True)
-                e0.record(stream)
-            same.same_sweep(ctx, w.states[b], w.obs[b], cpts, w.m, w.mb_cols(b), w.ld,
-                            b * w.nb, w.seed, s, ws)
-            if record:
-                e1.record(stream)
-                sweep_ev.append((e0, e1))
-            same.same_counts(ctx, w.states[b], w.m, w.mb_cols(b), w.ld, mb[b], tot, ws)
-            same.same_sample_cpts(ctx, tot, cpts, w.seed, s * w.M + b, ws)
+            same.same_step(ctx, w.states[b], w.obs[b], cpts, w.m, w.mb_cols(b), w.ld, b * w.nb,
+                           w.seed, s, mb[b], tot, s * w.M + b, ws)
 
     for s in range(args.warmup):
-        one_pass(s, False)
+        one_pass(s)
     torch.cuda.synchronize()
     log("warmup done")
     t_start = time.perf_counter()
@@ -139,21 +128,36 @@ def main():
     ev_end = torch.cuda.Event(enable_timing=True)
     ev_start.record(stream)
     for s in range(args.warmup, args.warmup + args.steps):
-        one_pass(s, True)
+        one_pass(s)
     ev_end.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
     gpu_ms = ev_start.elapsed_time(ev_end)
     elapsed = max(wall, gpu_ms / 1e3)
     log("timed %d passes: wall %.3f s, events %.3f s" % (args.steps, wall, gpu_ms / 1e3))
-
     node_samples = float(net.n) * cols_timed * w.m * args.steps
+
+    # the sweep kernels alone: HIP events around every same_sweep call of one
+    # further pass over the same minibatches (same launches as inside same_step)
+    sweep_ev = []
+    s_extra = args.warmup + args.steps
+    for b in mbs:
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        same.same_sweep(ctx, w.states[b], w.obs[b], cpts, w.m, w.mb_cols(b), w.ld, b * w.nb,
+                        w.seed, s_extra, ws)
+        e1.record(stream)
+        sweep_ev.append((e0, e1))
+    torch.cuda.synchronize()
+
     value = node_samples / elapsed
     sweep_s = sum(a.elapsed_time(b) for a, b in sweep_ev) / 1e3
-    launches = len(sweep_ev) * ctx.sweep_launches
+    launches = sum(same.same_sweep_plan(ctx, w.m, w.mb_cols(b))[1] for b in mbs)
+    node_samples_sweep = float(net.n) * cols_timed * w.m
     bytes_per_ns = 1.0 + hidden + 1.0 / w.m   # read each state, write each latent, obs per column
     alg_bytes = node_samples * bytes_per_ns
-    achieved = alg_bytes / sweep_s / 1e9
+    achieved = node_samples_sweep * bytes_per_ns / sweep_s / 1e9
     roofline = {
         "kernel": "sweep_main_kernel (every colour-group launch of a sweep)",
         "bound": "hbm",
@@ -165,7 +169,8 @@ def main():
         "bytes_per_node_sample": round(bytes_per_ns, 4),
         "launches": launches,
         "avg_launch_ms": round(sweep_s * 1e3 / launches, 4),
-        "sweep_share_of_step": round(sweep_s / elapsed, 3),
+        "sweep_share_of_step": round(sweep_s * args.steps / elapsed, 3),
+        "tile_cols": same.same_sweep_plan(ctx, w.m, w.mb_cols(0))[0],
     }
 
     if args.copy_calibration:

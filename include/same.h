@@ -102,6 +102,10 @@ typedef struct {
      * forms its conditional from CPT entries during the sweep.  Either way the
      * sweep draws from the same conditional with the same uniforms. */
     int64_t table_limit;
+    /* Target bytes of states + obs per column tile of a sweep (0: default,
+     * one tile = the whole minibatch).  Tiles are at least 1024 columns wide.
+     * Results do not depend on it. */
+    int64_t tile_bytes;
 } same_options_t;
 
 /* same_create with options (opts may be NULL for the defaults). */
@@ -180,6 +184,27 @@ int same_counts(same_ctx *ctx, const void *states, int32_t m, int64_t n_cols, in
  */
 int same_sample_cpts(same_ctx *ctx, const int32_t *totals, float *cpts_out, uint64_t seed,
                      uint32_t update_id, void *workspace, void *stream);
+
+/*
+ * How same_sweep splits a minibatch of n_cols columns with m replicas: the
+ * column-tile width and the number of sweep-kernel launches per call (for
+ * profiling; host only).
+ */
+int same_sweep_plan(const same_ctx *ctx, int32_t m, int64_t n_cols, int64_t *tile_cols,
+                    int32_t *launches);
+
+/*
+ * One whole SAME step over one minibatch (Sec. 4, Fig. 1): same_sweep, then
+ * same_counts into mb_counts and totals, then same_sample_cpts writing cpts in
+ * place with update_id.  The result equals those three calls in that order;
+ * the sweep and the counts run over column tiles sized for the device's
+ * last-level cache, so the count pass reads the tile the sweep just visited.
+ * Device pointers; cpts is read by the sweep and rewritten by the resample.
+ */
+int same_step(same_ctx *ctx, void *states, const uint8_t *obs, float *cpts, int32_t m,
+              int64_t n_cols, int64_t ld, int64_t col_offset, uint64_t seed, uint32_t sweep_id,
+              int32_t *mb_counts, int32_t *totals, uint32_t update_id, void *workspace,
+              void *stream);
 
 /*
  * Out-of-core passes (Sec. 4: the sampler keeps only model-sized state on the

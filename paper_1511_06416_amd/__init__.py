@@ -18,7 +18,7 @@ import numpy as np
 __all__ = [
     "SameError", "Context", "same_create", "same_create_ex", "same_destroy", "same_layout", "same_workspace_size",
     "same_sweep", "same_sweep_debug", "same_counts", "same_sample_cpts", "same_last_error",
-    "same_stream_slots_size", "same_stream_pass", "SAME_STREAM_COUNTS_ONLY",
+    "same_step", "same_sweep_plan", "same_stream_slots_size", "same_stream_pass", "SAME_STREAM_COUNTS_ONLY",
     "library_path", "load_library",
 ]
 
@@ -41,7 +41,7 @@ class SameError(RuntimeError):
 
 
 class _Options(C.Structure):
-    _fields_ = [("table_limit", C.c_int64)]
+    _fields_ = [("table_limit", C.c_int64), ("tile_bytes", C.c_int64)]
 
 
 class _Layout(C.Structure):
@@ -74,12 +74,15 @@ def load_library():
         L.same_sweep_debug.argtypes = [P, P, P, P, I32, I64, I64, I64, U64, U32, I64, I64, P, P, P]
         L.same_counts.argtypes = [P, P, I32, I64, I64, P, P, P, P]
         L.same_sample_cpts.argtypes = [P, P, P, U64, U32, P, P]
+        L.same_step.argtypes = [P, P, P, P, I32, I64, I64, I64, U64, U32, P, P, U32, P, P]
+        L.same_sweep_plan.argtypes = [P, I32, I64, C.POINTER(C.c_int64), C.POINTER(C.c_int32)]
         L.same_stream_slots_size.argtypes = [P, I32, I64, C.POINTER(C.c_size_t)]
         L.same_stream_pass.argtypes = [P, P, P, I64, I64, I64, I32, P, P, P, U64, U32, I32, P, P, P]
         L.same_last_error.argtypes = []
         L.same_last_error.restype = C.c_char_p
         for f in ("same_create", "same_create_ex", "same_layout", "same_workspace_size", "same_sweep",
-                  "same_sweep_debug", "same_counts", "same_sample_cpts", "same_stream_slots_size",
+                  "same_sweep_debug", "same_counts", "same_sample_cpts", "same_step", "same_sweep_plan",
+                  "same_stream_slots_size",
                   "same_stream_pass"):
             getattr(L, f).restype = C.c_int
         _lib = L
@@ -116,17 +119,18 @@ def _stream(stream):
 class Context:
     """Owns one same_ctx (one network)."""
 
-    def __init__(self, parent_ptr, parent_idx, card, dirichlet_prior=1.0, table_limit=None):
+    def __init__(self, parent_ptr, parent_idx, card, dirichlet_prior=1.0, table_limit=None,
+                 tile_bytes=0):
         L = load_library()
         self._pptr = np.ascontiguousarray(parent_ptr, dtype=np.int32)
         self._pidx = np.ascontiguousarray(parent_idx if len(parent_idx) else [0], dtype=np.int32)
         self._card = np.ascontiguousarray(card, dtype=np.int32)
         h = C.c_void_p()
-        if table_limit is None:
+        if table_limit is None and not tile_bytes:
             _check(L.same_create(len(self._card), self._pptr.ctypes.data, self._pidx.ctypes.data,
                                  self._card.ctypes.data, float(dirichlet_prior), C.byref(h)))
         else:
-            opts = _Options(int(table_limit))
+            opts = _Options(-1 if table_limit is None else int(table_limit), int(tile_bytes))
             _check(L.same_create_ex(len(self._card), self._pptr.ctypes.data,
                                     self._pidx.ctypes.data, self._card.ctypes.data,
                                     float(dirichlet_prior), C.byref(opts), C.byref(h)))
@@ -169,8 +173,10 @@ def same_create(parent_ptr, parent_idx, card, dirichlet_prior=1.0) -> Context:
     return Context(parent_ptr, parent_idx, card, dirichlet_prior)
 
 
-def same_create_ex(parent_ptr, parent_idx, card, dirichlet_prior=1.0, table_limit=-1) -> Context:
-    return Context(parent_ptr, parent_idx, card, dirichlet_prior, table_limit=table_limit)
+def same_create_ex(parent_ptr, parent_idx, card, dirichlet_prior=1.0, table_limit=-1,
+                   tile_bytes=0) -> Context:
+    return Context(parent_ptr, parent_idx, card, dirichlet_prior, table_limit=table_limit,
+                   tile_bytes=tile_bytes)
 
 
 def same_destroy(ctx: Context) -> None:
@@ -212,6 +218,21 @@ def same_counts(ctx, states, m, n_cols, ld, mb_counts, totals, workspace, stream
 def same_sample_cpts(ctx, totals, cpts_out, seed, update_id, workspace, stream=None):
     _check(load_library().same_sample_cpts(ctx.handle, _ptr(totals), _ptr(cpts_out), int(seed),
                                            int(update_id), _ptr(workspace), _stream(stream)))
+
+
+def same_step(ctx, states, obs, cpts, m, n_cols, ld, col_offset, seed, sweep_id, mb_counts, totals,
+              update_id, workspace, stream=None):
+    _check(load_library().same_step(ctx.handle, _ptr(states), _ptr(obs), _ptr(cpts), int(m),
+                                    int(n_cols), int(ld), int(col_offset), int(seed), int(sweep_id),
+                                    _ptr(mb_counts), _ptr(totals), int(update_id), _ptr(workspace),
+                                    _stream(stream)))
+
+
+def same_sweep_plan(ctx, m, n_cols):
+    """(tile width in columns, sweep-kernel launches per same_sweep call)."""
+    t, n = C.c_int64(), C.c_int32()
+    _check(load_library().same_sweep_plan(ctx.handle, int(m), int(n_cols), C.byref(t), C.byref(n)))
+    return int(t.value), int(n.value)
 
 
 def same_stream_slots_size(ctx, m, nb) -> int:

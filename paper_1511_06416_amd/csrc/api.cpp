@@ -44,6 +44,7 @@ struct same_ctx {
     std::mutex mu;
     // workspace layout
     size_t ws_table = 0, ws_cond = 0, ws_counts = 0, ws_gamma = 0, ws_total = 0;
+    double tile_bytes = 0.0;  // 0: one tile (the whole minibatch)
 };
 
 namespace {
@@ -198,9 +199,22 @@ int check_minibatch(const same_ctx *ctx, const void *states, int32_t m, int64_t 
     return SAME_OK;
 }
 
-int do_sweep(same_ctx *ctx, void *states, const uint8_t *obs, const float *cpts, int32_t m,
-             int64_t n_cols, int64_t ld, int64_t col_offset, uint64_t seed, uint32_t sweep_id,
-             int64_t win_begin, int64_t win, float *probs, void *workspace, void *stream) {
+// Column tiles (optional, same_options_t.tile_bytes): a sweep visits its
+// colour groups tile by tile, so that one tile's states can stay in the
+// last-level cache while every colour group re-reads them; counts of the tile
+// follow while it is still there.  Measured on MI355X the smaller launches
+// cost more than the cache saves, so the default is one tile.
+int64_t tile_cols(const same_ctx *ctx, int32_t m, int64_t n_cols) {
+    if (ctx->tile_bytes <= 0.0) return n_cols;
+    const double per_col = (double)ctx->g.n * ((double)m * ctx->g.state_bytes + 1.0);
+    int64_t t = (int64_t)(ctx->tile_bytes / per_col) / 1024 * 1024;
+    if (t < 1024) t = 1024;
+    return t >= n_cols ? n_cols : t;
+}
+
+int check_sweep_args(same_ctx *ctx, void *states, const uint8_t *obs, const float *cpts, int32_t m,
+                     int64_t n_cols, int64_t ld, int64_t col_offset, int64_t win_begin, int64_t win,
+                     float *probs, void *workspace) {
     int rc = check_minibatch(ctx, states, m, n_cols, ld);
     if (rc) return rc;
     if (!obs || !cpts || !workspace) return set_error(SAME_EINVAL, "obs, cpts and workspace must be non-null");
@@ -214,18 +228,21 @@ int do_sweep(same_ctx *ctx, void *states, const uint8_t *obs, const float *cpts,
         if (!probs) return set_error(SAME_EINVAL, "probs is null");
         if (win_begin < 0) return set_error(SAME_EINVAL, "win_begin must be >= 0");
     }
-    if (n_cols == 0) return SAME_OK;
-    same::DeviceTables *t = nullptr;
-    rc = tables_for_current_device(ctx, &t);
-    if (rc) return rc;
-    hipStream_t s = (hipStream_t)stream;
+    return SAME_OK;
+}
+
+// Builds this call's tables from cpts and fills the sweep parameters.
+int prepare_sweep(same_ctx *ctx, same::DeviceTables *t, void *states, const uint8_t *obs,
+                  const float *cpts, int32_t m, int64_t n_cols, int64_t ld, int64_t col_offset,
+                  uint64_t seed, uint32_t sweep_id, int64_t win_begin, int64_t win, float *probs,
+                  void *workspace, hipStream_t s, same::SweepParams &P) {
     float *table = (float *)((char *)workspace + ctx->ws_table);
     uint32_t *cond = (uint32_t *)((char *)workspace + ctx->ws_cond);
-    rc = check_hip(same::launch_build_tables(*t, cpts, table, s), "table build launch");
+    int rc = check_hip(same::launch_build_tables(*t, cpts, table, s), "table build launch");
     if (rc) return rc;
     rc = check_hip(same::launch_build_thresholds(*t, cpts, cond, s), "threshold build launch");
     if (rc) return rc;
-    same::SweepParams P{};
+    P = same::SweepParams{};
     P.desc = t->desc;
     P.desc_off = t->desc_off;
     P.order = t->order;
@@ -244,16 +261,86 @@ int do_sweep(same_ctx *ctx, void *states, const uint8_t *obs, const float *cpts,
     P.win = win > 0 ? win : 0;
     P.probs = probs;
     P.max_card = ctx->g.max_card;
+    return SAME_OK;
+}
+
+// All colour groups over columns [t0, t0 + nt) of the minibatch described by P.
+int sweep_tile(same_ctx *ctx, const same::SweepParams &P0, int64_t t0, int64_t nt, hipStream_t s) {
     const same::Compiled &g = ctx->g;
+    same::SweepParams P = P0;
+    P.states = (char *)P0.states + t0 * g.state_bytes;
+    P.obs = P0.obs + t0;
+    P.n_cols = nt;
+    P.col_offset = P0.col_offset + t0;
+    P.win_begin = P0.win_begin - t0;
     const int32_t L = same::kLaunchClasses;
     for (int32_t c = 0; c < g.n_colors; ++c)
         for (int32_t k = 0; k < L; ++k) {
             const int32_t b = g.launch[c * (L + 1) + k], e = g.launch[c * (L + 1) + k + 1];
-            rc = check_hip(same::launch_sweep(P, b, e - b, k, g.launch_lds[c * L + k], g.state_bytes, s),
-                           "sweep launch");
+            int rc = check_hip(same::launch_sweep(P, b, e - b, k, g.launch_lds[c * L + k], g.state_bytes, s),
+                               "sweep launch");
             if (rc) return rc;
         }
     return SAME_OK;
+}
+
+int do_sweep(same_ctx *ctx, void *states, const uint8_t *obs, const float *cpts, int32_t m,
+             int64_t n_cols, int64_t ld, int64_t col_offset, uint64_t seed, uint32_t sweep_id,
+             int64_t win_begin, int64_t win, float *probs, void *workspace, void *stream) {
+    int rc = check_sweep_args(ctx, states, obs, cpts, m, n_cols, ld, col_offset, win_begin, win, probs,
+                              workspace);
+    if (rc) return rc;
+    if (n_cols == 0) return SAME_OK;
+    same::DeviceTables *t = nullptr;
+    rc = tables_for_current_device(ctx, &t);
+    if (rc) return rc;
+    hipStream_t s = (hipStream_t)stream;
+    same::SweepParams P;
+    rc = prepare_sweep(ctx, t, states, obs, cpts, m, n_cols, ld, col_offset, seed, sweep_id, win_begin, win,
+                       probs, workspace, s, P);
+    if (rc) return rc;
+    const int64_t T = tile_cols(ctx, m, n_cols);
+    for (int64_t t0 = 0; t0 < n_cols; t0 += T) {
+        rc = sweep_tile(ctx, P, t0, n_cols - t0 < T ? n_cols - t0 : T, s);
+        if (rc) return rc;
+    }
+    return SAME_OK;
+}
+
+// Sweep, counts with the moving sum, and the Dirichlet resample of one
+// minibatch, tile by tile for the sweep and counts.
+int do_step(same_ctx *ctx, void *states, const uint8_t *obs, float *cpts, int32_t m, int64_t n_cols,
+            int64_t ld, int64_t col_offset, uint64_t seed, uint32_t sweep_id, int32_t *mb_counts,
+            int32_t *totals, uint32_t update_id, void *workspace, void *stream) {
+    int rc = check_sweep_args(ctx, states, obs, cpts, m, n_cols, ld, col_offset, 0, 0, nullptr, workspace);
+    if (rc) return rc;
+    if (!mb_counts || !totals) return set_error(SAME_EINVAL, "mb_counts and totals must be non-null");
+    if ((double)n_cols * (double)m >= 2147483648.0)
+        return set_error(SAME_ESIZE, "n_cols * m must stay below 2^31");
+    same::DeviceTables *t = nullptr;
+    rc = tables_for_current_device(ctx, &t);
+    if (rc) return rc;
+    hipStream_t s = (hipStream_t)stream;
+    const int64_t total = ctx->g.off[ctx->g.n];
+    int32_t *newc = (int32_t *)((char *)workspace + ctx->ws_counts);
+    same::SweepParams P;
+    rc = prepare_sweep(ctx, t, states, obs, cpts, m, n_cols, ld, col_offset, seed, sweep_id, 0, 0, nullptr,
+                       workspace, s, P);
+    if (!rc) rc = check_hip(same::launch_fill_zero(newc, total, s), "count clear launch");
+    if (rc) return rc;
+    const int64_t T = tile_cols(ctx, m, n_cols);
+    for (int64_t t0 = 0; t0 < n_cols; t0 += T) {
+        const int64_t nt = n_cols - t0 < T ? n_cols - t0 : T;
+        rc = sweep_tile(ctx, P, t0, nt, s);
+        if (rc) return rc;
+        rc = check_hip(same::launch_counts(*t, (const char *)states + t0 * ctx->g.state_bytes,
+                                           ctx->g.state_bytes, ctx->g.n, m, nt, ld, newc, s),
+                       "count launch");
+        if (rc) return rc;
+    }
+    rc = check_hip(same::launch_moving_sum(newc, mb_counts, totals, total, s), "moving-sum launch");
+    if (rc) return rc;
+    return same_sample_cpts(ctx, totals, cpts, seed, update_id, workspace, stream);
 }
 
 // Device slot geometry of the out-of-core passes.
@@ -289,6 +376,7 @@ int same_create_ex(int32_t n_nodes, const int32_t *parent_ptr, const int32_t *pa
     int64_t table_limit = 16384;
     if (opts && opts->table_limit >= 0) table_limit = opts->table_limit;
     if (opts && opts->table_limit < -1) return set_error(SAME_EINVAL, "table_limit must be >= -1");
+    if (opts && opts->tile_bytes < 0) return set_error(SAME_EINVAL, "tile_bytes must be >= 0");
     *out = nullptr;
     if (!(dirichlet_prior > 0.0)) return set_error(SAME_EINVAL, "dirichlet_prior must be > 0");
     same_ctx *ctx = new (std::nothrow) same_ctx();
@@ -306,6 +394,7 @@ int same_create_ex(int32_t n_nodes, const int32_t *parent_ptr, const int32_t *pa
         return set_error(rc, err);
     }
     ctx->alpha = dirichlet_prior;
+    if (opts && opts->tile_bytes > 0) ctx->tile_bytes = (double)opts->tile_bytes;
     ctx->ws_table = 0;
     ctx->ws_cond = align_up(ctx->ws_table + (size_t)ctx->g.table_floats * sizeof(float));
     ctx->ws_counts = align_up(ctx->ws_cond + (size_t)ctx->g.cond_words * sizeof(uint32_t));
@@ -409,6 +498,31 @@ int same_sample_cpts(same_ctx *ctx, const int32_t *totals, float *cpts_out, uint
     return check_hip(same::launch_normalize(*t, gv, cpts_out, ctx->g.n_rows, s), "normalize launch");
 }
 
+int same_sweep_plan(const same_ctx *ctx, int32_t m, int64_t n_cols, int64_t *tile_cols_out,
+                    int32_t *launches) {
+    if (!ctx || !tile_cols_out || !launches) return set_error(SAME_EINVAL, "null pointer argument");
+    if (m < 1 || n_cols < 0) return set_error(SAME_EINVAL, "need m >= 1 and n_cols >= 0");
+    if (n_cols == 0) {
+        *tile_cols_out = 0;
+        *launches = 0;
+        return SAME_OK;
+    }
+    const int64_t T = tile_cols(ctx, m, n_cols);
+    same_layout_t lay;
+    same_layout(ctx, &lay, nullptr, nullptr);
+    *tile_cols_out = T;
+    *launches = (int32_t)(((n_cols + T - 1) / T) * lay.sweep_launches);
+    return SAME_OK;
+}
+
+int same_step(same_ctx *ctx, void *states, const uint8_t *obs, float *cpts, int32_t m,
+              int64_t n_cols, int64_t ld, int64_t col_offset, uint64_t seed, uint32_t sweep_id,
+              int32_t *mb_counts, int32_t *totals, uint32_t update_id, void *workspace,
+              void *stream) {
+    return do_step(ctx, states, obs, cpts, m, n_cols, ld, col_offset, seed, sweep_id, mb_counts, totals,
+                   update_id, workspace, stream);
+}
+
 int same_stream_slots_size(const same_ctx *ctx, int32_t m, int64_t nb, size_t *bytes) {
     if (!ctx || !bytes) return set_error(SAME_EINVAL, "ctx and bytes must be non-null");
     if (m < 1 || m > 65535 || nb < 4) return set_error(SAME_EINVAL, "need 1 <= m <= 65535 and nb >= 4");
@@ -462,17 +576,12 @@ int same_stream_pass(same_ctx *ctx, void *host_states, const uint8_t *host_obs, 
         if (!rc) rc = check_hip(hipStreamWaitEvent(cs, sr->ev_up[s], 0), "wait");
         if (rc) return rc;
         int32_t *mb = mb_counts + b * total;
-        if (!counts_only) {
-            rc = do_sweep(ctx, d_states, d_obs, cpts, m, cols, sg.ld, c0, seed, pass_id, 0, 0, nullptr,
-                          workspace, stream);
-            if (rc) return rc;
-        }
-        rc = same_counts(ctx, d_states, m, cols, sg.ld, mb, totals, workspace, stream);
+        if (counts_only)
+            rc = same_counts(ctx, d_states, m, cols, sg.ld, mb, totals, workspace, stream);
+        else
+            rc = do_step(ctx, d_states, d_obs, cpts, m, cols, sg.ld, c0, seed, pass_id, mb, totals,
+                         (uint32_t)(pass_id * M + b), workspace, stream);
         if (rc) return rc;
-        if (!counts_only) {
-            rc = same_sample_cpts(ctx, totals, cpts, seed, (uint32_t)(pass_id * M + b), workspace, stream);
-            if (rc) return rc;
-        }
         rc = check_hip(hipEventRecord(sr->ev_comp[s], cs), "event");
         if (rc) return rc;
         if (counts_only) {

@@ -12,12 +12,14 @@ REL_TOL = 1e-5       # conditionals, fp32 vs fp64
 TINY = 1e-30         # below this the oracle's probability is not compared relatively
 
 
-def context_for(net, prior=1.0, table_limit=None):
-    """Library context; table_limit=0 forces every node onto the product path."""
+def context_for(net, prior=1.0, table_limit=None, tile_bytes=0):
+    """Library context; table_limit=0 forces every node onto the product path,
+    a small tile_bytes forces sweeps over several column tiles."""
     pptr, pidx, card = net.csr()
-    if table_limit is None:
+    if table_limit is None and not tile_bytes:
         return same.same_create(pptr, pidx, card, prior)
-    return same.same_create_ex(pptr, pidx, card, prior, table_limit)
+    return same.same_create_ex(pptr, pidx, card, prior,
+                               -1 if table_limit is None else table_limit, tile_bytes)
 
 
 def gpu_sweep(ctx, states_np, obs_np, theta_np, m, n_cols, col_offset, seed, sweep_id, win=None,

@@ -80,6 +80,42 @@ def test_sweep_parity_after_resampled_cpts():
     _sweep_case(w, theta=theta, win=(0, 256))
 
 
+def test_column_tiles_and_step_are_bit_identical():
+    """A sweep split into column tiles equals the untiled sweep, same_step
+    equals same_sweep + same_counts + same_sample_cpts, and the tiled sweep
+    matches the oracle."""
+    w = make_workload(5, n_cols=5_000, m=2)
+    net = w.net
+    pre, obs = w.states[0].numpy(), w.obs[0].numpy()
+    tiled = H.context_for(net, tile_bytes=1)          # 1024-column tiles
+    assert same.same_sweep_plan(tiled, w.m, 5_000)[0] == 1024
+    whole = H.context_for(net)
+    a, _ = H.gpu_sweep(tiled, pre, obs, w.init_theta, w.m, 5_000, 0, 9, 2)
+    b, _ = H.gpu_sweep(whole, pre, obs, w.init_theta, w.m, 5_000, 0, 9, 2)
+    assert np.array_equal(a, b)
+    _sweep_case(w, win=(3_000, 600), sweep_id=2)
+    outs = []
+    for ctx, fused in ((tiled, True), (whole, False)):
+        st = w.states[0].cuda()
+        ob = w.obs[0].cuda()
+        th = torch.from_numpy(w.init_theta).cuda()
+        mb = torch.zeros(ctx.cpt_total, dtype=torch.int32, device="cuda")
+        tot = torch.zeros(ctx.cpt_total, dtype=torch.int32, device="cuda")
+        ws = ctx.new_workspace()
+        same.same_counts(ctx, st, w.m, 5_000, w.ld, mb, tot, ws)
+        for s in range(2):
+            if fused:
+                same.same_step(ctx, st, ob, th, w.m, 5_000, w.ld, 0, w.seed, s, mb, tot, s, ws)
+            else:
+                same.same_sweep(ctx, st, ob, th, w.m, 5_000, w.ld, 0, w.seed, s, ws)
+                same.same_counts(ctx, st, w.m, 5_000, w.ld, mb, tot, ws)
+                same.same_sample_cpts(ctx, tot, th, w.seed, s, ws)
+        torch.cuda.synchronize()
+        outs.append([x.cpu().numpy() for x in (st, mb, tot, th)])
+    for x, y in zip(*outs):
+        assert np.array_equal(x, y)
+
+
 def test_sweep_deterministic_and_stream_independent():
     w = make_workload(3, n_cols=4_100, m=2)
     ctx = H.context_for(w.net)
