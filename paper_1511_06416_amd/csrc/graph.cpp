@@ -203,7 +203,8 @@ int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int
                 cfg *= card[v];
                 if (cfg * thresholds_per_config(K) > table_limit) break;
             }
-            if (cfg * thresholds_per_config(K) <= table_limit && b.size() <= 24) mode = kModeTable;
+            if (cfg * thresholds_per_config(K) <= table_limit && cfg <= kPackedLimit && b.size() <= 24)
+                mode = kModeTable;
         }
         g.mode[i] = mode;
     }
@@ -255,29 +256,51 @@ int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int
             cpos += ncfg * KT;
             if (cpos > kI32Max) return fail(err, SAME_ESIZE, "threshold tables exceed 2^31 words");
         }
-        g.cond_words = cpos;
+        g.cond_words = (cpos + 15) & ~int64_t(15);  // whole float4s for the LDS staging copy
     }
 
     // descriptor streams
     g.desc_off.resize(n);
     g.cdesc_off.resize(n);
     g.lds_bytes.assign(n, 0);
+    g.klass.assign(n, 0);
     for (int32_t i = 0; i < n; ++i) {
-        const int32_t KP = g.kp[i];
+        const int32_t KP = g.kp[i], K = card[i];
         const bool tab = g.mode[i] == kModeTable;
         const std::vector<int32_t> &b = blanket[i];
-        const int32_t KT = tab ? thresholds_per_config(card[i]) : 0;
-        int64_t cond_len = 0;
-        if (tab) {
-            cond_len = KT;
-            for (int32_t v : b) cond_len *= card[v];
+        const int32_t KT = tab ? thresholds_per_config(K) : 0;
+        int64_t ncfg = 1;
+        if (tab)
+            for (int32_t v : b) ncfg *= card[v];
+        const int64_t cond_len = tab ? ncfg * KT : 0;
+
+        // launch class and the unit of the fast list's indices (bytes)
+        int32_t klass;
+        int64_t unit = 0;
+        if (g.mode[i] == kModeGeneric) {
+            klass = 3;
+        } else if (g.mode[i] == kModeKP16) {
+            klass = 2;
+        } else {
+            const int64_t bytes = tab ? cond_len * 4 : g.tab_len[i] * 4;
+            const int64_t row_bytes = tab ? (int64_t)KT * 4 : (int64_t)KP * 4;
+            if (bytes <= kLdsBudgetBytes) {
+                klass = 0;
+                unit = 1;
+                g.lds_bytes[i] = (int32_t)((bytes + 15) & ~int64_t(15));  // staged in float4s
+            } else if (bytes / row_bytes <= kPackedLimit) {
+                klass = 1;
+                unit = row_bytes;
+            } else {
+                klass = 2;  // product modes only: tables always fit 16-bit rows
+            }
         }
-        const int64_t stage = tab ? cond_len * 4 : g.tab_len[i] * 4;
-        if (mode_class(g.mode[i]) == 0 && stage <= kLdsBudgetBytes) g.lds_bytes[i] = (int32_t)stage;
+        g.klass[i] = klass;
+
         const int32_t base = (int32_t)g.desc.size();
         g.desc_off[i] = base;
         g.desc.resize(base + kDescHeader, 0);
-        g.desc[base + 0] = card[i];
+        g.desc[base + 0] = K;
         g.desc[base + 1] = KP;
         g.desc[base + 2] = g.mode[i];
         g.desc[base + 3] = (int32_t)g.tab_begin[i];
@@ -285,54 +308,87 @@ int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int
         g.desc[base + 5] = (int32_t)cond_off[i];
         g.desc[base + 6] = (int32_t)cond_len;
         g.desc[base + 7] = KT;
-        g.desc[base + 12] = g.lds_bytes[i] > 0 ? 1 : 0;
-        // entry lists: (node, mult, arg); arg -3 own row, -1 adds to the own
-        // (or threshold) index, -2 adds to the current child index, >= 0 starts
-        // a child whose k-vector table begins at relative offset arg
-        if (tab) {
-            g.desc[base + 8] = 1 + (int32_t)b.size();
-            g.desc[base + 9] = (int32_t)g.desc.size() - base;
-            g.desc.insert(g.desc.end(), {i, 0, -3});
-            std::vector<int64_t> st(b.size());
-            int64_t r = 1;
-            for (int32_t t = (int32_t)b.size() - 1; t >= 0; --t) {
-                st[t] = r;
-                r *= card[b[t]];
-            }
-            for (size_t t = 0; t < b.size(); ++t) g.desc.insert(g.desc.end(), {b[t], (int32_t)(st[t] * KT), -1});
-        }
-        const int32_t pstart = (int32_t)g.desc.size();
-        g.desc[base + 11] = pstart - base;
-        g.desc.insert(g.desc.end(), {i, 0, -3});
-        for (int32_t a2 = pptr[i]; a2 < pptr[i + 1]; ++a2) {
-            int64_t mult = g.pstride[a2] * KP;
-            if (mult > kI32Max) return fail(err, SAME_ESIZE, "row stride overflow");
-            g.desc.insert(g.desc.end(), {g.pidx[a2], (int32_t)mult, -1});
+        g.desc[base + 12] = klass;
+
+        // product-path groups in float offsets: own row, then one per child
+        struct Group {
+            int64_t base;
+            std::vector<std::pair<int32_t, int64_t>> ent;
+        };
+        std::vector<Group> groups;
+        {
+            Group own{0, {}};
+            for (int32_t a2 = pptr[i]; a2 < pptr[i + 1]; ++a2)
+                own.ent.push_back({g.pidx[a2], g.pstride[a2] * KP});
+            groups.push_back(own);
         }
         for (int32_t t : ctab_of[i]) {
             const ChildTab &ct = g.ctabs[t];
             const int32_t h = ct.child, Kh = card[h];
-            g.desc.insert(g.desc.end(), {h, KP, (int32_t)(ct.off - g.tab_begin[i])});
-            // compact strides over h's parents without i, last listed fastest
+            Group cg{ct.off - g.tab_begin[i], {{h, (int64_t)KP}}};
+            // h's parents other than i, compact strides (last listed fastest)
             int64_t r = 1;
             std::vector<std::pair<int32_t, int64_t>> cops;
             for (int32_t a2 = pptr[h + 1] - 1; a2 >= pptr[h]; --a2) {
                 if (a2 - pptr[h] == ct.slot) continue;
-                cops.push_back({g.pidx[a2], r});
+                cops.push_back({g.pidx[a2], r * Kh * KP});
                 r *= card[g.pidx[a2]];
             }
             std::reverse(cops.begin(), cops.end());
-            for (auto &cp : cops) {
-                int64_t mult = cp.second * Kh * KP;
-                if (mult > kI32Max) return fail(err, SAME_ESIZE, "child stride overflow");
-                g.desc.insert(g.desc.end(), {cp.first, (int32_t)mult, -2});
-            }
+            cg.ent.insert(cg.ent.end(), cops.begin(), cops.end());
+            groups.push_back(cg);
         }
-        g.desc[base + 10] = ((int32_t)g.desc.size() - pstart) / 3;
+        auto emit = [&](const Group &gr, int64_t div, bool packed) -> bool {
+            auto word = [&](int64_t v) -> int64_t {
+                v /= div;
+                return packed ? (v | (v << 16)) : v;
+            };
+            if (gr.base % div || (packed && gr.base / div >= kPackedLimit)) return false;
+            if (!packed && gr.base > kI32Max) return false;
+            g.desc.push_back((int32_t)gr.ent.size());
+            g.desc.push_back((int32_t)(uint32_t)word(gr.base));
+            for (auto &e : gr.ent) {
+                if (e.second % div) return false;
+                if (packed ? e.second / div >= kPackedLimit : e.second > kI32Max) return false;
+                g.desc.push_back(e.first);
+                g.desc.push_back((int32_t)(uint32_t)word(e.second));
+            }
+            return true;
+        };
+        g.desc[base + 10] = (int32_t)groups.size();
+        g.desc[base + 11] = (int32_t)g.desc.size() - base;
+        for (auto &gr : groups)
+            if (!emit(gr, 1, false)) return fail(err, SAME_ESIZE, "sweep table offset overflow");
+        if (klass <= 1) {
+            g.desc[base + 9] = (int32_t)g.desc.size() - base;
+            bool ok = true;
+            if (tab) {
+                // one group over the blanket, last fastest, in threshold rows
+                Group bg{0, {}};
+                int64_t r = 1;
+                for (int32_t t = (int32_t)b.size() - 1; t >= 0; --t) {
+                    bg.ent.push_back({b[t], r * KT * 4});
+                    r *= card[b[t]];
+                }
+                std::reverse(bg.ent.begin(), bg.ent.end());
+                g.desc[base + 8] = 1;
+                ok = emit(bg, unit, true);
+            } else {
+                g.desc[base + 8] = (int32_t)groups.size();
+                for (auto &gr : groups) {
+                    Group gb{gr.base * 4, {}};
+                    for (auto &e : gr.ent) gb.ent.push_back({e.first, e.second * 4});
+                    ok = ok && emit(gb, unit, true);
+                }
+            }
+            // the class test above bounds every index below 2^16 units
+            if (!ok) return fail(err, SAME_ESIZE, "packed sweep index overflow");
+        }
+
         g.cdesc_off[i] = (int32_t)g.cdesc.size();
-        g.cdesc.push_back(card[i]);
+        g.cdesc.push_back(K);
         g.cdesc.push_back(pptr[i + 1] - pptr[i]);
-        g.cdesc.push_back((int32_t)(g.rows[i] * card[i]));
+        g.cdesc.push_back((int32_t)(g.rows[i] * K));
         g.cdesc.push_back((int32_t)g.off[i]);
         for (int32_t a = pptr[i]; a < pptr[i + 1]; ++a) {
             g.cdesc.push_back(g.pidx[a]);
@@ -340,19 +396,15 @@ int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int
         }
     }
 
-    // launch order: per colour, the nodes of each launch class in turn
-    // (0: main kernel with LDS-staged tables, 1: main kernel reading tables
-    // from global memory, 2: KP 16, 3: generic), and per (colour, class) the
-    // LDS bytes the launch needs
+    // launch order: per colour, the nodes of each launch class in turn, and
+    // per (colour, class) the LDS bytes the launch needs
     g.launch.assign((size_t)g.n_colors * (kLaunchClasses + 1), 0);
     g.launch_lds.assign((size_t)g.n_colors * kLaunchClasses, 0);
     for (int32_t c = 0; c < g.n_colors; ++c) {
         for (int32_t k = 0; k < kLaunchClasses; ++k) {
             g.launch[c * (kLaunchClasses + 1) + k] = (int32_t)g.order.size();
             for (int32_t i : g.groups[c]) {
-                const int32_t mc = mode_class(g.mode[i]);
-                const int32_t lc = mc == 0 ? (g.lds_bytes[i] > 0 ? 0 : 1) : mc + 1;
-                if (lc != k) continue;
+                if (g.klass[i] != k) continue;
                 g.order.push_back(i);
                 int32_t &lb = g.launch_lds[c * kLaunchClasses + k];
                 lb = std::max(lb, g.lds_bytes[i]);

@@ -41,38 +41,45 @@ struct Segment {
     int32_t own;       // 1: own rows of node i
 };
 
-// Sweep modes (descriptor field 5).
+// Sweep modes (descriptor field 2).
 enum SweepMode : int32_t {
     kModeKP2 = 0,    // product of k-vectors, KP = 2
     kModeKP4 = 1,
     kModeKP8 = 2,
     kModeTable = 3,  // precomputed CDF thresholds per blanket configuration
-    kModeKP16 = 4,   // product path with KP = 16 (own kernel: higher register use)
-    kModeGeneric = 5 // K > 16: extended-exponent product path (own kernel)
+    kModeKP16 = 4,   // product path with KP = 16
+    kModeGeneric = 5 // K > 16: extended-exponent product path
 };
 
-// Kernel class of a mode: 0 main kernel (KP2/4/8 and table), 1 KP16, 2 generic.
-inline int32_t mode_class(int32_t mode) {
-    return mode == kModeKP16 ? 1 : (mode == kModeGeneric ? 2 : 0);
-}
-
+// Launch classes (one kernel each):
+//   0 fast path, the node's table record (k-vectors or thresholds) staged in
+//     LDS, packed 16-bit byte indices;
+//   1 fast path, tables read from global memory, packed 16-bit indices in
+//     units of one k-vector (or one threshold row);
+//   2 wide path: product modes up to KP = 16 with 32-bit float indices;
+//   3 generic path (K > 16).
 constexpr int32_t kLaunchClasses = 4;
 constexpr int64_t kLdsBudgetBytes = 32768;  // largest table staged in LDS per block
 constexpr int32_t kDescHeader = 16;
+constexpr int64_t kPackedLimit = 65536;      // packed indices are 16-bit
 
 // Sweep descriptor of a node (int32 words at desc_off[i]):
 //   [0] K  [1] KP  [2] mode  [3] tab_begin  [4] tab_len (floats)
 //   [5] cond_off  [6] cond_len (threshold words)  [7] KT
-//   [8] n_tent  [9] tent (relative word index of the threshold-path entries)
-//   [10] n_pent  [11] pent (relative word index of the product-path entries)
-//   [12] staged (1: the block copies its table into LDS)
-// Entries are (node, mult, arg) triples walked in order: arg -3 is the node's
-// own row (read for the write-back), -1 adds mult * state to the running own
-// (or threshold) index, -2 adds to the running child index, and arg >= 0
-// starts a child whose k-vector table begins at relative float offset arg
-// (mult = KP multiplies the child's own state).  Product-path indices are
-// float offsets relative to tab_begin; threshold indices are word offsets
-// relative to cond_off.
+//   [8] n_fast  [9] fast (relative word index of the fast group list)
+//   [10] n_wide [11] wide (relative word index of the wide group list)
+//   [12] launch class
+// A group list is a sequence of groups [n_e, base, (node, mult) * n_e]; the
+// group's index is base + sum of mult * state over its entries.
+//   wide list (every node): group 0 is the node's own row (entries: its
+//     parents), then one group per child h (entries: h itself, then h's
+//     other parents); indices are float offsets into the node's table record.
+//   fast list (classes 0 and 1): product modes hold the same groups; the
+//     table mode holds one group over the Markov blanket (ascending id, last
+//     fastest) indexing the threshold rows.  Class 0 counts in bytes, class 1
+//     in k-vectors (KP floats) or threshold rows (KT words); base and mult are
+//     stored packed twice (v | v << 16) for the 2 x 16-bit lane arithmetic,
+//     and every index of the list stays below 2^16.
 
 struct Compiled {
     int32_t n = 0;
@@ -101,7 +108,8 @@ struct Compiled {
     std::vector<int32_t> desc;
     std::vector<int32_t> desc_off;   // [n]
 
-    // precomputed conditional tables: for a node in table mode, every
+    // precomputed conditional tables: for a node in table mode (at most
+    // kPackedLimit blanket configurations), every
     // configuration of its Markov blanket (blanket nodes in ascending id, last
     // fastest) holds KT uint32 thresholds T_k = ceil(2^24 * S_k / Z), k < K-1,
     // padded with 2^24; the draw is #{k : T_k <= u24}.
@@ -124,6 +132,7 @@ struct Compiled {
     std::vector<int32_t> launch;       // [n_colors * (kLaunchClasses + 1)]
     std::vector<int32_t> launch_lds;   // [n_colors * kLaunchClasses]
     std::vector<int32_t> mode;         // [n]
+    std::vector<int32_t> klass;        // [n] launch class
 
     // CPT rows, for the Dirichlet normalisation: entry offset and K of each row
     std::vector<int32_t> row_off, row_k;

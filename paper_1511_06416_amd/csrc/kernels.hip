@@ -26,8 +26,6 @@ typedef const __attribute__((address_space(4))) int32_t cint32_t;
 __device__ __forceinline__ cint32_t *as_const(const int32_t *p) { return (cint32_t *)p; }
 
 constexpr int kBlock = 256;          // 4 wavefronts of 64
-constexpr int kColsPerBlock = 4 * kBlock;
-constexpr float kUnderflowGuard = 0x1p-100f;
 
 // ---------------------------------------------------------------- state quads
 
@@ -38,6 +36,9 @@ template <>
 struct Quad<int8_t> {
     using V = uint32_t;
     __device__ static V load(const int8_t *p) { return *reinterpret_cast<const uint32_t *>(p); }
+    __device__ static V load_buffer(__amdgpu_buffer_rsrc_t r, uint32_t boff) {
+        return __builtin_amdgcn_raw_buffer_load_b32(r, (int)boff, 0, 0);
+    }
     __device__ static void store(int8_t *p, V v) { *reinterpret_cast<uint32_t *>(p) = v; }
     __device__ static int get(V v, int c) { return (int)((v >> (8 * c)) & 0xffu); }
     __device__ static V put(V v, int c, int x) {
@@ -47,12 +48,25 @@ struct Quad<int8_t> {
     __device__ static V keep(V v, int nvalid) {
         return nvalid >= 4 ? v : (v & ((1u << (8 * nvalid)) - 1u));
     }
+    // the 4 states as 16-bit lanes: p[0] = columns (0, 2), p[1] = (1, 3)
+    __device__ static void split(V v, uint32_t (&p)[2]) {
+        p[0] = v & 0x00ff00ffu;
+        p[1] = __builtin_amdgcn_perm(0u, v, 0x0c030c01u);
+    }
+    __device__ static constexpr int word_of(int c) { return c & 1; }
+    __device__ static constexpr int half_of(int c) { return c >> 1; }
 };
 
 template <>
 struct Quad<int16_t> {
     using V = uint2;
     __device__ static V load(const int16_t *p) { return *reinterpret_cast<const uint2 *>(p); }
+    // two 32-bit loads: the 64- and 128-bit raw buffer load builtins of this
+    // toolchain lower to a single dword load
+    __device__ static V load_buffer(__amdgpu_buffer_rsrc_t r, uint32_t boff) {
+        return make_uint2(__builtin_amdgcn_raw_buffer_load_b32(r, (int)boff, 0, 0),
+                          __builtin_amdgcn_raw_buffer_load_b32(r, (int)boff + 4, 0, 0));
+    }
     __device__ static void store(int16_t *p, V v) { *reinterpret_cast<uint2 *>(p) = v; }
     __device__ static int get(V v, int c) {
         const uint32_t w = c < 2 ? v.x : v.y;
@@ -74,12 +88,124 @@ struct Quad<int16_t> {
         }
         return v;
     }
+    // the 4 states as 16-bit lanes: p[0] = columns (0, 1), p[1] = (2, 3)
+    __device__ static void split(V v, uint32_t (&p)[2]) {
+        p[0] = v.x;
+        p[1] = v.y;
+    }
+    __device__ static constexpr int word_of(int c) { return c >> 1; }
+    __device__ static constexpr int half_of(int c) { return c & 1; }
 };
 
-// Reads one k-vector of KP floats (KP a power of two); p is 8-byte aligned
-// for KP == 2 and 16-byte aligned otherwise.
-template <int KP>
-__device__ __forceinline__ void load_kvec(const float *__restrict__ p, float (&f)[KP]) {
+// ---------------------------------------------------------------- entry walks
+
+// Two 16-bit lanes per 32-bit word: v_pk_mad_u16 computes a * b + c in both.
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ uint32_t pk_mad_u16(uint32_t a, uint32_t b, uint32_t c) {
+    const u16x2 r = __builtin_bit_cast(u16x2, a) * __builtin_bit_cast(u16x2, b) +
+                    __builtin_bit_cast(u16x2, c);
+    return __builtin_bit_cast(uint32_t, r);
+}
+
+// LDS bytes (address space 3: ds_read instructions, not flat loads).
+typedef const __attribute__((address_space(3))) char lds_char;
+
+// Buffer resource over n_bytes at base (uniform): raw buffer loads take a
+// 32-bit vector byte offset, with no 64-bit address arithmetic per lane, and
+// any offset at or past n_bytes reads 0 instead of touching memory.
+constexpr int32_t kBufferWord3 = 0x00020000;  // 32-bit data format, no swizzle
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void *base, uint32_t n_bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)n_bytes,
+                                             kBufferWord3);
+}
+
+// State quad of row `node` (n_bytes = m * ld * sizeof(state) < 2^31) at the
+// lane's byte offset.
+template <typename ST>
+__device__ __forceinline__ typename Quad<ST>::V load_row(const ST *__restrict__ states, int32_t node,
+                                                         int64_t vstride, uint32_t lane_boff) {
+    const __amdgpu_buffer_rsrc_t r =
+        buffer_rsrc(states + (int64_t)node * vstride, (uint32_t)(vstride * (int64_t)sizeof(ST)));
+    return Quad<ST>::load_buffer(r, lane_boff);
+}
+
+constexpr int kEntryBatch = 8;  // most state rows in flight per batch
+
+// Loads the state quads of the N entries (node, mult) at e, all before the
+// first use, and hands each to f with its multiplier.
+template <int N, typename ST, typename F>
+__device__ __forceinline__ void entry_batch(cint32_t *e, const ST *__restrict__ states,
+                                            int64_t vstride, uint32_t lane_boff, F &f) {
+    typename Quad<ST>::V s[N];
+#pragma unroll
+    for (int t = 0; t < N; ++t) s[t] = load_row<ST>(states, e[2 * t], vstride, lane_boff);
+#pragma unroll
+    for (int t = 0; t < N; ++t) f(s[t], (uint32_t)e[2 * t + 1]);
+}
+
+// Walks the n_e entries at e in batches of at most kEntryBatch.  n_e is
+// uniform, so the size switch is a scalar branch and no slot is wasted.
+template <typename ST, typename F>
+__device__ __forceinline__ void walk_entries(cint32_t *e, int n_e, const ST *__restrict__ states,
+                                             int64_t vstride, uint32_t lane_boff, F &f) {
+    for (; n_e > 0; n_e -= kEntryBatch, e += 2 * kEntryBatch) {
+        switch (n_e < kEntryBatch ? n_e : kEntryBatch) {
+        case 1: entry_batch<1, ST>(e, states, vstride, lane_boff, f); break;
+        case 2: entry_batch<2, ST>(e, states, vstride, lane_boff, f); break;
+        case 3: entry_batch<3, ST>(e, states, vstride, lane_boff, f); break;
+        case 4: entry_batch<4, ST>(e, states, vstride, lane_boff, f); break;
+        case 5: entry_batch<5, ST>(e, states, vstride, lane_boff, f); break;
+        case 6: entry_batch<6, ST>(e, states, vstride, lane_boff, f); break;
+        case 7: entry_batch<7, ST>(e, states, vstride, lane_boff, f); break;
+        default: entry_batch<8, ST>(e, states, vstride, lane_boff, f); break;
+        }
+    }
+}
+
+// Packed group index of a fast list: two words of 2 x 16-bit lanes, one lane
+// per column of the quad (lane layout in Quad<ST>::split).  Columns past
+// n_cols are cleared by vmask, so their index is 0: padding never steers an
+// access out of the node's table.  Advances g past the group.
+template <typename ST>
+__device__ __forceinline__ void packed_group(cint32_t *&g, const ST *__restrict__ states,
+                                             int64_t vstride, uint32_t lane_boff,
+                                             const uint32_t (&vmask)[2], uint32_t (&Pk)[2]) {
+    const int n_e = g[0];
+    Pk[0] = Pk[1] = (uint32_t)g[1];
+    auto acc = [&](typename Quad<ST>::V v, uint32_t mult) {
+        uint32_t p[2];
+        Quad<ST>::split(v, p);
+        Pk[0] = pk_mad_u16(p[0], mult, Pk[0]);
+        Pk[1] = pk_mad_u16(p[1], mult, Pk[1]);
+    };
+    walk_entries<ST>(g + 2, n_e, states, vstride, lane_boff, acc);
+    g += 2 + 2 * n_e;
+    Pk[0] &= vmask[0];
+    Pk[1] &= vmask[1];
+}
+
+template <typename ST>
+__device__ __forceinline__ uint32_t packed_index(const uint32_t (&Pk)[2], int c) {
+    const uint32_t v = Pk[Quad<ST>::word_of(c)];
+    return Quad<ST>::half_of(c) ? v >> 16 : v & 0xffffu;
+}
+
+// Lane masks of vmask: the 16-bit lanes of columns >= nvalid cleared.
+template <typename ST>
+__device__ __forceinline__ void valid_mask(int nvalid, uint32_t (&vmask)[2]) {
+    vmask[0] = vmask[1] = 0xffffffffu;
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+        if (c >= nvalid) vmask[Quad<ST>::word_of(c)] &= ~(0xffffu << (16 * Quad<ST>::half_of(c)));
+}
+
+// ---------------------------------------------------------------- k-vectors
+
+// Reads KP floats at p (8-byte aligned for KP == 2, 16-byte otherwise).
+template <int KP, typename PTR>
+__device__ __forceinline__ void read_kvec(PTR p, float (&f)[KP]) {
     if (KP == 2) {
         const float2 v = *reinterpret_cast<const float2 *>(p);
         f[0] = v.x;
@@ -96,6 +222,74 @@ __device__ __forceinline__ void load_kvec(const float *__restrict__ p, float (&f
     }
 }
 
+// Native vector types (HIP's float4 class cannot be read from LDS lvalues).
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+template <int KP>
+__device__ __forceinline__ void read_kvec_lds(lds_char *p, float (&f)[KP]) {
+    typedef const __attribute__((address_space(3))) f32x2 lf2;
+    typedef const __attribute__((address_space(3))) f32x4 lf4;
+    if (KP == 2) {
+        const f32x2 v = *reinterpret_cast<lf2 *>(p);
+        f[0] = v.x;
+        f[1] = v.y;
+        return;
+    }
+#pragma unroll
+    for (int q = 0; q < KP / 4; ++q) {
+        const f32x4 v = reinterpret_cast<lf4 *>(p)[q];
+        f[4 * q + 0] = v.x;
+        f[4 * q + 1] = v.y;
+        f[4 * q + 2] = v.z;
+        f[4 * q + 3] = v.w;
+    }
+}
+
+constexpr int log2i(int v) { return v <= 1 ? 0 : 1 + log2i(v / 2); }
+
+// Global-memory bytes (address space 1) from a scalar base: with a scalar
+// base and a 32-bit vector offset computed in the same block, the loads take
+// the scalar-base form (no 64-bit vector address arithmetic).
+typedef const __attribute__((address_space(1))) char global_char;
+
+__device__ __forceinline__ global_char *scalar_global_ptr(const void *p) {
+    const uint64_t a = reinterpret_cast<uint64_t>(p);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+    return reinterpret_cast<global_char *>(((uint64_t)hi << 32) | lo);
+}
+
+template <int KP>
+__device__ __forceinline__ void read_kvec_global(global_char *p, float (&f)[KP]) {
+    typedef const __attribute__((address_space(1))) f32x2 gf2;
+    typedef const __attribute__((address_space(1))) f32x4 gf4;
+    if (KP == 2) {
+        const f32x2 v = *reinterpret_cast<gf2 *>(p);
+        f[0] = v.x;
+        f[1] = v.y;
+        return;
+    }
+#pragma unroll
+    for (int q = 0; q < KP / 4; ++q) {
+        const f32x4 v = reinterpret_cast<gf4 *>(p)[q];
+        f[4 * q + 0] = v.x;
+        f[4 * q + 1] = v.y;
+        f[4 * q + 2] = v.z;
+        f[4 * q + 3] = v.w;
+    }
+}
+
+// The k-vector at packed index idx: a byte offset into the staged record
+// (STAGED) or a k-vector number in the node's global record.
+template <int KP, bool STAGED>
+__device__ __forceinline__ void fast_kvec(lds_char *lds, global_char *gtab, uint32_t idx, float (&f)[KP]) {
+    if (STAGED) read_kvec_lds<KP>(lds + idx, f);
+    else read_kvec_global<KP>(gtab + (idx << log2i(4 * KP)), f);
+}
+
 // Exact power-of-two rescale so that max_k w[k] lands in [0.5, 1).
 template <int KP>
 __device__ __forceinline__ void renorm(float (&w)[KP]) {
@@ -109,149 +303,103 @@ __device__ __forceinline__ void renorm(float (&w)[KP]) {
     }
 }
 
-constexpr int kEntryBatch = 8;  // state rows loaded per batch (one round trip)
-
-// Loads the state quads of up to kEntryBatch entries starting at e0.  Every
-// slot loads (slots past the end reload entry e0), so the whole batch is in
-// flight before the first use.
-//
-// Addressing: the row base states + node * m * ld is uniform (scalar), the
-// lane's offset (r * ld + col) is shared by every row and fits 32 bits (the
-// host requires m * ld * sizeof(state) < 2^31), so every load is a scalar
-// base plus one 32-bit vector offset.
-template <typename ST>
-__device__ __forceinline__ void load_batch(cint32_t *ent, int e0, int ne, const ST *__restrict__ states,
-                                           uint32_t lane_off, int64_t vstride,
-                                           typename Quad<ST>::V (&s)[kEntryBatch]) {
+// Unnormalised full conditional (Sec. 4: own CPT entry times the children's
+// entries, Eq. 4) of the quad's 4 columns from a fast product list: group 0
+// gives the own k-vector, each further group a child k-vector multiplied in.
+// With RESCALE every column's running product is renormalised after each
+// factor, which keeps it away from fp32 underflow.
+template <int KP, typename ST, bool STAGED, bool RESCALE>
+__device__ __forceinline__ void fast_product(cint32_t *g, int n_groups, lds_char *lds,
+                                             global_char *gtab,
+                                             const ST *__restrict__ states, int64_t vstride,
+                                             uint32_t lane_boff, const uint32_t (&vmask)[2],
+                                             float (&w)[4][KP]) {
+    uint32_t Pk[2];
+    packed_group<ST>(g, states, vstride, lane_boff, vmask, Pk);
 #pragma unroll
-    for (int t = 0; t < kEntryBatch; ++t) {
-        const int tt = t < ne ? e0 + t : e0;
-        const ST *row = states + (int64_t)ent[3 * tt] * vstride;
-        s[t] = Quad<ST>::load(row + lane_off);
+    for (int c = 0; c < 4; ++c) fast_kvec<KP, STAGED>(lds, gtab, packed_index<ST>(Pk, c), w[c]);
+    for (int j = 1; j < n_groups; ++j) {
+        packed_group<ST>(g, states, vstride, lane_boff, vmask, Pk);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            float f[KP];
+            fast_kvec<KP, STAGED>(lds, gtab, packed_index<ST>(Pk, c), f);
+#pragma unroll
+            for (int k = 0; k < KP; ++k) w[c][k] *= f[k];
+            if (RESCALE) renorm<KP>(w[c]);
+        }
     }
 }
 
-// Multiplies the k-vectors at tab + b[c] into w[c] (renormalising with RESCALE).
-template <int KP, bool RESCALE>
-__device__ __forceinline__ void mul_kvecs(const float *tab, const int (&b)[4], float (&w)[4][KP]) {
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-        float f[KP];
-        load_kvec<KP>(tab + b[c], f);
-#pragma unroll
-        for (int k = 0; k < KP; ++k) w[c][k] *= f[k];
-        if (RESCALE) renorm<KP>(w[c]);
-    }
-}
-
-// Unnormalised full conditional of a node for the 4 columns of one quad from
-// its product-path entry list: w[c][k] = own k-vector * product over children
-// of the child k-vectors, all read from tab (the node's table record, in LDS
-// or global memory).  cur receives the node's own state quad.  With RESCALE
-// each column's running product is renormalised after every factor, which
-// keeps it away from fp32 underflow; the default path checks the final
-// maximum instead.  Columns at or beyond n_cols (nvalid < 4, last quad only)
-// read their states as 0, so padding never steers a table index out of range.
+// Same conditional from the wide list (32-bit float offsets, any record
+// size): wide kernel, table-mode debug output.  Columns >= nvalid read their
+// states as 0.
 template <int KP, typename ST, bool RESCALE>
-__device__ __forceinline__ void product_walk(cint32_t *ent, int n_ent, const float *tab,
-                                             const ST *__restrict__ states, uint32_t lane_off,
-                                             int64_t vstride, int nvalid, float (&w)[4][KP],
-                                             typename Quad<ST>::V &cur) {
+__device__ __forceinline__ void wide_product(cint32_t *g, int n_groups, const float *__restrict__ tab,
+                                             const ST *__restrict__ states, int64_t vstride,
+                                             uint32_t lane_boff, int nvalid, float (&w)[4][KP]) {
     using Q = Quad<ST>;
-    int a[4] = {0, 0, 0, 0};
-    int b[4] = {0, 0, 0, 0};
-    bool in_child = false;
-    for (int e0 = 0; e0 < n_ent; e0 += kEntryBatch) {
-        const int ne = n_ent - e0 < kEntryBatch ? n_ent - e0 : kEntryBatch;
-        typename Q::V s[kEntryBatch];
-        load_batch<ST>(ent, e0, ne, states, lane_off, vstride, s);
+    for (int j = 0; j < n_groups; ++j) {
+        const int n_e = g[0];
+        uint32_t idx[4];
 #pragma unroll
-        for (int t = 0; t < kEntryBatch; ++t) {
-            if (t >= ne) break;
-            const int mult = ent[3 * (e0 + t) + 1], arg = ent[3 * (e0 + t) + 2];
-            if (arg == -3) {
-                cur = s[t];
-                continue;
-            }
-            const typename Q::V v = Q::keep(s[t], nvalid);
-            if (arg == -1) {
+        for (int c = 0; c < 4; ++c) idx[c] = (uint32_t)g[1];
+        auto acc = [&](typename Q::V v, uint32_t mult) {
+            v = Q::keep(v, nvalid);
 #pragma unroll
-                for (int c = 0; c < 4; ++c) a[c] += Q::get(v, c) * mult;
-            } else if (arg == -2) {
+            for (int c = 0; c < 4; ++c) idx[c] += (uint32_t)Q::get(v, c) * mult;
+        };
+        walk_entries<ST>(g + 2, n_e, states, vstride, lane_boff, acc);
+        g += 2 + 2 * n_e;
 #pragma unroll
-                for (int c = 0; c < 4; ++c) b[c] += Q::get(v, c) * mult;
+        for (int c = 0; c < 4; ++c) {
+            float f[KP];
+            read_kvec<KP>(tab + idx[c], f);
+            if (j == 0) {
+#pragma unroll
+                for (int k = 0; k < KP; ++k) w[c][k] = f[k];
             } else {
-                if (in_child) {
-                    mul_kvecs<KP, RESCALE>(tab, b, w);
-                } else {
 #pragma unroll
-                    for (int c = 0; c < 4; ++c) load_kvec<KP>(tab + a[c], w[c]);
-                }
-                in_child = true;
-#pragma unroll
-                for (int c = 0; c < 4; ++c) b[c] = arg + Q::get(v, c) * mult;
+                for (int k = 0; k < KP; ++k) w[c][k] *= f[k];
             }
-        }
-    }
-    if (in_child) {
-        mul_kvecs<KP, RESCALE>(tab, b, w);
-    } else {
-#pragma unroll
-        for (int c = 0; c < 4; ++c) load_kvec<KP>(tab + a[c], w[c]);
-    }
-}
-
-// Threshold-path index walk: idx[c] = sum of mult * state over the blanket;
-// cur receives the node's own state quad.
-template <typename ST>
-__device__ __forceinline__ void table_walk(cint32_t *ent, int n_ent, const ST *__restrict__ states,
-                                           uint32_t lane_off, int64_t vstride, int nvalid,
-                                           int (&idx)[4], typename Quad<ST>::V &cur) {
-    using Q = Quad<ST>;
-    for (int e0 = 0; e0 < n_ent; e0 += kEntryBatch) {
-        const int ne = n_ent - e0 < kEntryBatch ? n_ent - e0 : kEntryBatch;
-        typename Q::V s[kEntryBatch];
-        load_batch<ST>(ent, e0, ne, states, lane_off, vstride, s);
-#pragma unroll
-        for (int t = 0; t < kEntryBatch; ++t) {
-            if (t >= ne) break;
-            const int mult = ent[3 * (e0 + t) + 1], arg = ent[3 * (e0 + t) + 2];
-            if (arg == -3) {
-                cur = s[t];
-                continue;
-            }
-            const typename Q::V v = Q::keep(s[t], nvalid);
-#pragma unroll
-            for (int c = 0; c < 4; ++c) idx[c] += Q::get(v, c) * mult;
+            if (RESCALE) renorm<KP>(w[c]);
         }
     }
 }
 
-// Inverse-CDF draw from weights w[0..K) (entries K..KP-1 are zero): S_k running
-// sums in ascending k, Z = S_{K-1}; the smallest k with u*Z < S_k, else the
-// largest k with positive weight.
+// ---------------------------------------------------------------- draws
+
+// In-place running sums S_k = w_0 + ... + w_k.
 template <int KP>
-__device__ __forceinline__ int draw_kvec(const float (&w)[KP], int K, float u, float &Z) {
-    float S[KP];
-    float acc = 0.f;
+__device__ __forceinline__ void running_sums(float (&w)[KP]) {
 #pragma unroll
-    for (int k = 0; k < KP; ++k) {
-        acc += w[k];
-        S[k] = acc;
-    }
-    Z = acc;
-    const float t = u * Z;
+    for (int k = 1; k < KP; ++k) w[k] += w[k - 1];
+}
+
+// Inverse-CDF draw from running sums S (entries K..KP-1 repeat Z = S_{K-1}):
+// the smallest k with u*Z < S_k, i.e. the number of S_k <= u*Z.  When
+// rounding makes u*Z reach Z, the largest k whose weight is positive (whose
+// running sum grows) is taken.
+template <int KP>
+__device__ __forceinline__ int draw_sums(const float (&S)[KP], int K, float u) {
+    const float t = u * S[KP - 1];
     int pick = 0;
 #pragma unroll
     for (int k = 0; k < KP; ++k) pick += (S[k] <= t) ? 1 : 0;
     if (pick >= K) {
         pick = 0;
 #pragma unroll
-        for (int k = 0; k < KP; ++k)
-            if (k < K && w[k] > 0.f) pick = k;
+        for (int k = 1; k < KP; ++k)
+            if (k < K && S[k] > S[k - 1]) pick = k;
     }
     return pick;
 }
+
+// Z below this sends the quad through the renormalising walk: Z >= 2^-96
+// keeps the largest weight (>= Z / 16) at or above 2^-100.
+constexpr float kUnderflowZ = 0x1p-96f;
+
+// ---------------------------------------------------------------- block work
 
 // The block's share of the work: a run of column quads of one node and a
 // range of replicas.
@@ -297,71 +445,88 @@ __device__ __forceinline__ Philox4 gibbs_block(const SweepParams &P, int node, i
                          P.key0, P.key1);
 }
 
-// Product path: the conditional from the node's k-vector tables at tab.
-template <int KP, typename ST, bool DEBUG>
-__device__ void sweep_product(const SweepParams &P, const Work &W, const float *tab) {
+__device__ __forceinline__ float uniform24(uint32_t word) { return (float)(word >> 8) * 0x1p-24f; }
+
+// Fast product path (classes 0 and 1, KP <= 8).
+template <int KP, typename ST, bool DEBUG, bool STAGED>
+__device__ void sweep_product(const SweepParams &P, const Work &W, lds_char *lds, global_char *gtab) {
     using Q = Quad<ST>;
     cint32_t *d = W.d;
-    const int K = d[0], n_ent = d[10];
-    cint32_t *ent = d + d[11];
+    const int K = d[0], n_groups = d[8];
+    cint32_t *grp = d + d[9];
     ST *states = reinterpret_cast<ST *>(P.states);
     const int64_t vstride = (int64_t)P.m * P.ld;
     for (int64_t q = W.q0 + threadIdx.x; q < W.q1; q += kBlock) {
         const int64_t col = q * 4;
         const int lat = latent_bits(P, W.node, col);
         if (!lat) continue;
-        const int nvalid = P.n_cols - col < 4 ? (int)(P.n_cols - col) : 4;
+        uint32_t vmask[2];
+        valid_mask<ST>(P.n_cols - col < 4 ? (int)(P.n_cols - col) : 4, vmask);
         for (int r = W.r0; r < W.r1; ++r) {
-            const uint32_t lane_off = (uint32_t)(r * P.ld + col);
+            const uint32_t lane_boff = (uint32_t)(r * P.ld + col) * (uint32_t)sizeof(ST);
+            typename Q::V cur = load_row<ST>(states, W.node, vstride, lane_boff);
             float w[4][KP];
-            typename Q::V cur;
-            product_walk<KP, ST, false>(ent, n_ent, tab, states, lane_off, vstride, nvalid, w, cur);
+            fast_product<KP, ST, STAGED, false>(grp, n_groups, lds, gtab, states, vstride, lane_boff,
+                                                vmask, w);
+            float wd[4][KP];
+            if (DEBUG) {
+#pragma unroll
+                for (int c = 0; c < 4; ++c)
+#pragma unroll
+                    for (int k = 0; k < KP; ++k) wd[c][k] = w[c][k];
+            }
             bool low = false;
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
-                float mx = w[c][0];
-#pragma unroll
-                for (int k = 1; k < KP; ++k) mx = fmaxf(mx, w[c][k]);
-                low |= ((lat >> c) & 1) && !(mx >= kUnderflowGuard);
+                running_sums<KP>(w[c]);
+                low |= ((lat >> c) & 1) && !(w[c][KP - 1] >= kUnderflowZ);
             }
-            if (low)
-                product_walk<KP, ST, true>(ent, n_ent, tab, states, lane_off, vstride, nvalid, w, cur);
+            if (low) {
+                fast_product<KP, ST, STAGED, true>(grp, n_groups, lds, gtab, states, vstride, lane_boff,
+                                                   vmask, w);
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    if (DEBUG) {
+#pragma unroll
+                        for (int k = 0; k < KP; ++k) wd[c][k] = w[c][k];
+                    }
+                    running_sums<KP>(w[c]);
+                }
+            }
             const Philox4 rnd = gibbs_block(P, W.node, r, q);
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
                 if (!((lat >> c) & 1)) continue;
-                const float u = (float)(rnd.w[c] >> 8) * 0x1p-24f;
-                float Z;
-                cur = Q::put(cur, c, draw_kvec<KP>(w[c], K, u, Z));
-                if (DEBUG) write_probs(P, W.node, r, col + c, w[c], K, Z);
+                cur = Q::put(cur, c, draw_sums<KP>(w[c], K, uniform24(rnd.w[c])));
+                if (DEBUG) write_probs(P, W.node, r, col + c, wd[c], K, w[c][KP - 1]);
             }
-            Q::store(states + (int64_t)W.node * vstride + lane_off, cur);
+            Q::store(reinterpret_cast<ST *>(reinterpret_cast<char *>(states + (int64_t)W.node * vstride) +
+                                            lane_boff),
+                     cur);
         }
     }
 }
 
-// Debug conditionals of a table-mode node, from the product path (global tables).
+// Debug conditionals of a table-mode node, from its wide list (global tables).
 template <typename ST>
-__device__ void table_debug_probs(const SweepParams &P, const Work &W, int r, int64_t col,
-                                  int lat, int nvalid) {
+__device__ void table_debug_probs(const SweepParams &P, const Work &W, int r, int64_t col, int lat,
+                                  int nvalid) {
     cint32_t *d = W.d;
     const int K = d[0], KP = d[1];
     const ST *states = reinterpret_cast<const ST *>(P.states);
-    const uint32_t lane_off = (uint32_t)(r * P.ld + col);
+    const uint32_t lane_boff = (uint32_t)(r * P.ld + col) * (uint32_t)sizeof(ST);
     const int64_t vstride = (int64_t)P.m * P.ld;
     const float *tab = P.table + d[3];
-    typename Quad<ST>::V cur;
-#define SAME_TABLE_DEBUG(KPV)                                                                   \
-    {                                                                                           \
-        float w[4][KPV];                                                                        \
-        product_walk<KPV, ST, true>(d + d[11], d[10], tab, states, lane_off, vstride, nvalid, w,  \
-                                    cur);                                                       \
-        for (int c = 0; c < 4; ++c) {                                                           \
-            if (!((lat >> c) & 1)) continue;                                                    \
-            float Z = 0.f;                                                                      \
-            for (int k = 0; k < KPV; ++k) Z += w[c][k];                                         \
-            write_probs(P, W.node, r, col + c, w[c], K, Z);                                     \
-        }                                                                                       \
+#define SAME_TABLE_DEBUG(KPV)                                                                     \
+    {                                                                                             \
+        float w[4][KPV];                                                                          \
+        wide_product<KPV, ST, true>(d + d[11], d[10], tab, states, vstride, lane_boff, nvalid, w); \
+        for (int c = 0; c < 4; ++c) {                                                             \
+            if (!((lat >> c) & 1)) continue;                                                      \
+            float Z = 0.f;                                                                        \
+            for (int k = 0; k < KPV; ++k) Z += w[c][k];                                           \
+            write_probs(P, W.node, r, col + c, w[c], K, Z);                                       \
+        }                                                                                         \
     }
     if (KP == 2) SAME_TABLE_DEBUG(2)
     else if (KP == 4) SAME_TABLE_DEBUG(4)
@@ -370,15 +535,136 @@ __device__ void table_debug_probs(const SweepParams &P, const Work &W, int r, in
 #undef SAME_TABLE_DEBUG
 }
 
-// Table path: the blanket configuration indexes KT precomputed thresholds at
-// cond; the drawn state is the number of thresholds at or below the 24-bit
-// uniform.
-template <int KT, typename ST, bool DEBUG>
-__device__ void sweep_table(const SweepParams &P, const Work &W, const uint32_t *cond) {
+// Threshold path (classes 0 and 1): the blanket configuration selects KT
+// thresholds; the drawn state is the number of thresholds at or below the
+// 24-bit uniform.
+template <int KT, typename ST, bool DEBUG, bool STAGED>
+__device__ void sweep_table(const SweepParams &P, const Work &W, lds_char *lds, global_char *gcond) {
     using Q = Quad<ST>;
     cint32_t *d = W.d;
-    const int n_ent = d[8];
-    cint32_t *ent = d + d[9];
+    cint32_t *grp = d + d[9];
+    ST *states = reinterpret_cast<ST *>(P.states);
+    const int64_t vstride = (int64_t)P.m * P.ld;
+    for (int64_t q = W.q0 + threadIdx.x; q < W.q1; q += kBlock) {
+        const int64_t col = q * 4;
+        const int lat = latent_bits(P, W.node, col);
+        if (!lat) continue;
+        const int nvalid = P.n_cols - col < 4 ? (int)(P.n_cols - col) : 4;
+        uint32_t vmask[2];
+        valid_mask<ST>(nvalid, vmask);
+        for (int r = W.r0; r < W.r1; ++r) {
+            const uint32_t lane_boff = (uint32_t)(r * P.ld + col) * (uint32_t)sizeof(ST);
+            typename Q::V cur = load_row<ST>(states, W.node, vstride, lane_boff);
+            cint32_t *g = grp;
+            uint32_t Pk[2];
+            packed_group<ST>(g, states, vstride, lane_boff, vmask, Pk);
+            const Philox4 rnd = gibbs_block(P, W.node, r, q);
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                if (!((lat >> c) & 1)) continue;
+                const uint32_t u24 = rnd.w[c] >> 8;
+                const uint32_t idx = packed_index<ST>(Pk, c);
+                uint32_t th[KT];
+                if (STAGED) {
+                    typedef const __attribute__((address_space(3))) uint32_t lu32;
+                    typedef const __attribute__((address_space(3))) u32x2 lu2;
+                    typedef const __attribute__((address_space(3))) u32x4 lu4;
+                    lds_char *p = lds + idx;
+                    if (KT == 1) {
+                        th[0] = *reinterpret_cast<lu32 *>(p);
+                    } else if (KT == 2) {
+                        const u32x2 v = *reinterpret_cast<lu2 *>(p);
+                        th[0] = v.x;
+                        th[1] = v.y;
+                    } else {
+#pragma unroll
+                        for (int h = 0; h < KT / 4; ++h) {
+                            const u32x4 v = reinterpret_cast<lu4 *>(p)[h];
+                            th[4 * h] = v.x;
+                            th[4 * h + 1] = v.y;
+                            th[4 * h + 2] = v.z;
+                            th[4 * h + 3] = v.w;
+                        }
+                    }
+                } else {
+                    typedef const __attribute__((address_space(1))) uint32_t gu32;
+                    typedef const __attribute__((address_space(1))) u32x2 gu2;
+                    typedef const __attribute__((address_space(1))) u32x4 gu4;
+                    global_char *p = gcond + (idx << log2i(4 * KT));
+                    if (KT == 1) {
+                        th[0] = *reinterpret_cast<gu32 *>(p);
+                    } else if (KT == 2) {
+                        const u32x2 v = *reinterpret_cast<gu2 *>(p);
+                        th[0] = v.x;
+                        th[1] = v.y;
+                    } else {
+#pragma unroll
+                        for (int h = 0; h < KT / 4; ++h) {
+                            const u32x4 v = reinterpret_cast<gu4 *>(p)[h];
+                            th[4 * h] = v.x;
+                            th[4 * h + 1] = v.y;
+                            th[4 * h + 2] = v.z;
+                            th[4 * h + 3] = v.w;
+                        }
+                    }
+                }
+                int pick = 0;
+#pragma unroll
+                for (int k = 0; k < KT; ++k) pick += th[k] <= u24 ? 1 : 0;
+                cur = Q::put(cur, c, pick);
+            }
+            if (DEBUG) table_debug_probs<ST>(P, W, r, col, lat, nvalid);
+            Q::store(reinterpret_cast<ST *>(reinterpret_cast<char *>(states + (int64_t)W.node * vstride) +
+                                            lane_boff),
+                     cur);
+        }
+    }
+}
+
+// Fast kernel: one block = one node (blockIdx.y in the launch range) x a run
+// of column quads (blockIdx.x) x a range of replicas (blockIdx.z).  The
+// node's mode selects the product path for KP = 2, 4, 8 or the threshold
+// path.  With STAGED the block first copies its node's table record (k-vectors
+// or thresholds) into LDS, so every gather of the sweep is an LDS read.
+template <typename ST, bool DEBUG, bool STAGED>
+__global__ __launch_bounds__(kBlock) void sweep_fast_kernel(SweepParams P) {
+    extern __shared__ float4 lds4[];
+    const Work W = block_work(P);
+    cint32_t *d = W.d;
+    const int mode = d[2];
+    const float *tab = P.table + d[3];
+    const uint32_t *cond = P.cond + d[5];
+    if (STAGED) {
+        const float4 *src = reinterpret_cast<const float4 *>(mode == kModeTable ? (const void *)cond
+                                                                                : (const void *)tab);
+        const int len4 = mode == kModeTable ? (d[6] + 3) >> 2 : d[4] >> 2;
+        for (int i = threadIdx.x; i < len4; i += kBlock) lds4[i] = src[i];
+        __syncthreads();
+    }
+    lds_char *lds = (lds_char *)lds4;
+    global_char *gt = scalar_global_ptr(tab);
+    if (mode == kModeKP2) sweep_product<2, ST, DEBUG, STAGED>(P, W, lds, gt);
+    else if (mode == kModeKP4) sweep_product<4, ST, DEBUG, STAGED>(P, W, lds, gt);
+    else if (mode == kModeKP8) sweep_product<8, ST, DEBUG, STAGED>(P, W, lds, gt);
+    else {
+        const int KT = d[7];
+        global_char *gc = scalar_global_ptr(cond);
+        if (KT == 1) sweep_table<1, ST, DEBUG, STAGED>(P, W, lds, gc);
+        else if (KT == 2) sweep_table<2, ST, DEBUG, STAGED>(P, W, lds, gc);
+        else if (KT == 4) sweep_table<4, ST, DEBUG, STAGED>(P, W, lds, gc);
+        else sweep_table<8, ST, DEBUG, STAGED>(P, W, lds, gc);
+    }
+}
+
+// Wide path (class 2): product modes with KP up to 16 and any record size,
+// 32-bit float offsets, tables in global memory.
+template <int KP, typename ST, bool DEBUG>
+__device__ void sweep_wide(const SweepParams &P, const Work &W) {
+    using Q = Quad<ST>;
+    cint32_t *d = W.d;
+    const int K = d[0], n_groups = d[10];
+    cint32_t *grp = d + d[11];
+    const float *tab = P.table + d[3];
     ST *states = reinterpret_cast<ST *>(P.states);
     const int64_t vstride = (int64_t)P.m * P.ld;
     for (int64_t q = W.q0 + threadIdx.x; q < W.q1; q += kBlock) {
@@ -387,81 +673,47 @@ __device__ void sweep_table(const SweepParams &P, const Work &W, const uint32_t 
         if (!lat) continue;
         const int nvalid = P.n_cols - col < 4 ? (int)(P.n_cols - col) : 4;
         for (int r = W.r0; r < W.r1; ++r) {
-            const uint32_t lane_off = (uint32_t)(r * P.ld + col);
-            int idx[4] = {0, 0, 0, 0};
-            typename Q::V cur;
-            table_walk<ST>(ent, n_ent, states, lane_off, vstride, nvalid, idx, cur);
+            const uint32_t lane_boff = (uint32_t)(r * P.ld + col) * (uint32_t)sizeof(ST);
+            typename Q::V cur = load_row<ST>(states, W.node, vstride, lane_boff);
+            float w[4][KP];
+            wide_product<KP, ST, false>(grp, n_groups, tab, states, vstride, lane_boff, nvalid, w);
+            bool low = false;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                float Z = 0.f;
+#pragma unroll
+                for (int k = 0; k < KP; ++k) Z += w[c][k];
+                low |= ((lat >> c) & 1) && !(Z >= kUnderflowZ);
+            }
+            if (low) wide_product<KP, ST, true>(grp, n_groups, tab, states, vstride, lane_boff, nvalid, w);
             const Philox4 rnd = gibbs_block(P, W.node, r, q);
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
                 if (!((lat >> c) & 1)) continue;
-                const uint32_t u24 = rnd.w[c] >> 8;
-                const uint32_t *t = cond + idx[c];
-                int pick = 0;
-                if (KT == 1) {
-                    pick = t[0] <= u24;
-                } else if (KT == 2) {
-                    const uint2 v = *reinterpret_cast<const uint2 *>(t);
-                    pick = (v.x <= u24) + (v.y <= u24);
-                } else {
+                if (DEBUG) {
+                    float Z = 0.f;
 #pragma unroll
-                    for (int h = 0; h < KT / 4; ++h) {
-                        const uint4 v = reinterpret_cast<const uint4 *>(t)[h];
-                        pick += (v.x <= u24) + (v.y <= u24) + (v.z <= u24) + (v.w <= u24);
-                    }
+                    for (int k = 0; k < KP; ++k) Z += w[c][k];
+                    write_probs(P, W.node, r, col + c, w[c], K, Z);
                 }
-                cur = Q::put(cur, c, pick);
+                running_sums<KP>(w[c]);
+                cur = Q::put(cur, c, draw_sums<KP>(w[c], K, uniform24(rnd.w[c])));
             }
-            if (DEBUG) table_debug_probs<ST>(P, W, r, col, lat, nvalid);
-            Q::store(states + (int64_t)W.node * vstride + lane_off, cur);
+            Q::store(reinterpret_cast<ST *>(reinterpret_cast<char *>(states + (int64_t)W.node * vstride) +
+                                            lane_boff),
+                     cur);
         }
     }
 }
 
-// Main kernel: one block = one node (blockIdx.y in the launch range) x a run
-// of column quads (blockIdx.x) x a range of replicas (blockIdx.z).  The
-// node's mode selects the product path for KP = 2, 4, 8 or the threshold
-// path.  With STAGED the block first copies its node's table (k-vector record
-// or thresholds) into LDS, so every gather of the sweep is an LDS read.
-template <typename ST, bool DEBUG, bool STAGED>
-__global__ __launch_bounds__(kBlock) void sweep_main_kernel(SweepParams P) {
-    extern __shared__ float4 lds4[];
-    const Work W = block_work(P);
-    cint32_t *d = W.d;
-    const int mode = d[2];
-    const float *tab = P.table + d[3];
-    const uint32_t *cond = P.cond + d[5];
-    if (STAGED) {
-        if (mode == kModeTable) {
-            const int len = d[6];
-            uint32_t *dst = reinterpret_cast<uint32_t *>(lds4);
-            for (int i = threadIdx.x; i < len; i += kBlock) dst[i] = cond[i];
-            cond = dst;
-        } else {
-            const int len4 = d[4] >> 2;
-            const float4 *src = reinterpret_cast<const float4 *>(tab);
-            for (int i = threadIdx.x; i < len4; i += kBlock) lds4[i] = src[i];
-            tab = reinterpret_cast<const float *>(lds4);
-        }
-        __syncthreads();
-    }
-    if (mode == kModeKP2) sweep_product<2, ST, DEBUG>(P, W, tab);
-    else if (mode == kModeKP4) sweep_product<4, ST, DEBUG>(P, W, tab);
-    else if (mode == kModeKP8) sweep_product<8, ST, DEBUG>(P, W, tab);
-    else {
-        const int KT = d[7];
-        if (KT == 1) sweep_table<1, ST, DEBUG>(P, W, cond);
-        else if (KT == 2) sweep_table<2, ST, DEBUG>(P, W, cond);
-        else if (KT == 4) sweep_table<4, ST, DEBUG>(P, W, cond);
-        else sweep_table<8, ST, DEBUG>(P, W, cond);
-    }
-}
-
-// Nodes with 9 <= K <= 16 (KP = 16): kept apart because of their registers.
 template <typename ST, bool DEBUG>
-__global__ __launch_bounds__(kBlock) void sweep_kp16_kernel(SweepParams P) {
+__global__ __launch_bounds__(kBlock) void sweep_wide_kernel(SweepParams P) {
     const Work W = block_work(P);
-    sweep_product<16, ST, DEBUG>(P, W, P.table + W.d[3]);
+    const int KP = W.d[1];
+    if (KP == 2) sweep_wide<2, ST, DEBUG>(P, W);
+    else if (KP == 4) sweep_wide<4, ST, DEBUG>(P, W);
+    else if (KP == 8) sweep_wide<8, ST, DEBUG>(P, W);
+    else sweep_wide<16, ST, DEBUG>(P, W);
 }
 
 // ------------------------------------------------- generic path, K_i > 16
@@ -469,37 +721,28 @@ __global__ __launch_bounds__(kBlock) void sweep_kp16_kernel(SweepParams P) {
 // The weight of state k is kept as (mantissa in [0.5, 1), exponent) and
 // renormalised exactly after every factor, so any K fits in a few registers;
 // the three passes (largest exponent, total, search) each recompute the
-// products by walking the node's product-path entries for one column.
+// products by walking the node's wide list for one column.
 
 template <typename ST>
 __device__ float weight_ext(cint32_t *d, const float *__restrict__ tab, const ST *__restrict__ base,
                             int64_t vstride, int c, int k, int &e) {
     using Q = Quad<ST>;
-    const int n_ent = d[10];
-    cint32_t *ent = d + d[11];
-    int a = 0, b = 0;
-    bool in_child = false;
+    cint32_t *g = d + d[11];
+    const int n_groups = d[10];
     float mnt = 1.f;
     e = 0;
-    auto factor = [&](float f) {
-        mnt *= f;
+    for (int j = 0; j < n_groups; ++j) {
+        const int n_e = g[0];
+        uint32_t idx = (uint32_t)g[1];
+        for (int t = 0; t < n_e; ++t)
+            idx += (uint32_t)Q::get(Q::load(base + (int64_t)g[2 + 2 * t] * vstride), c) *
+                   (uint32_t)g[3 + 2 * t];
+        g += 2 + 2 * n_e;
+        mnt *= tab[idx + k];
         const int de = __builtin_amdgcn_frexp_expf(mnt);
         mnt = __builtin_ldexpf(mnt, -de);
         e += de;
-    };
-    for (int t = 0; t < n_ent; ++t) {
-        const int arg = ent[3 * t + 2];
-        if (arg == -3) continue;
-        const int v = Q::get(Q::load(base + (int64_t)ent[3 * t] * vstride), c) * ent[3 * t + 1];
-        if (arg == -1) a += v;
-        else if (arg == -2) b += v;
-        else {
-            factor(in_child ? tab[b + k] : tab[a + k]);
-            in_child = true;
-            b = arg + v;
-        }
     }
-    factor(in_child ? tab[b + k] : tab[a + k]);
     return mnt;
 }
 
@@ -535,7 +778,7 @@ __global__ __launch_bounds__(kBlock) void sweep_generic_kernel(SweepParams P) {
                     const float mk = weight_ext<ST>(d, tab, base, vstride, c, k, e);
                     Z += __builtin_ldexpf(mk, e - E);
                 }
-                const float t = (float)(rnd.w[c] >> 8) * 0x1p-24f * Z;
+                const float t = uniform24(rnd.w[c]) * Z;
                 float S = 0.f;
                 int pick = -1, last_pos = 0;
                 for (int k = 0; k < K; ++k) {
@@ -805,14 +1048,14 @@ void sweep_class(const SweepParams &P, int32_t klass, int32_t lds_bytes, dim3 gr
     const bool dbg = P.win > 0;
     const dim3 blk(dev::kBlock);
     if (klass == 0) {
-        if (dbg) hipLaunchKernelGGL((dev::sweep_main_kernel<ST, true, true>), grid, blk, lds_bytes, stream, P);
-        else hipLaunchKernelGGL((dev::sweep_main_kernel<ST, false, true>), grid, blk, lds_bytes, stream, P);
+        if (dbg) hipLaunchKernelGGL((dev::sweep_fast_kernel<ST, true, true>), grid, blk, lds_bytes, stream, P);
+        else hipLaunchKernelGGL((dev::sweep_fast_kernel<ST, false, true>), grid, blk, lds_bytes, stream, P);
     } else if (klass == 1) {
-        if (dbg) hipLaunchKernelGGL((dev::sweep_main_kernel<ST, true, false>), grid, blk, 0, stream, P);
-        else hipLaunchKernelGGL((dev::sweep_main_kernel<ST, false, false>), grid, blk, 0, stream, P);
+        if (dbg) hipLaunchKernelGGL((dev::sweep_fast_kernel<ST, true, false>), grid, blk, 0, stream, P);
+        else hipLaunchKernelGGL((dev::sweep_fast_kernel<ST, false, false>), grid, blk, 0, stream, P);
     } else if (klass == 2) {
-        if (dbg) hipLaunchKernelGGL((dev::sweep_kp16_kernel<ST, true>), grid, blk, 0, stream, P);
-        else hipLaunchKernelGGL((dev::sweep_kp16_kernel<ST, false>), grid, blk, 0, stream, P);
+        if (dbg) hipLaunchKernelGGL((dev::sweep_wide_kernel<ST, true>), grid, blk, 0, stream, P);
+        else hipLaunchKernelGGL((dev::sweep_wide_kernel<ST, false>), grid, blk, 0, stream, P);
     } else {
         if (dbg) hipLaunchKernelGGL((dev::sweep_generic_kernel<ST, true>), grid, blk, 0, stream, P);
         else hipLaunchKernelGGL((dev::sweep_generic_kernel<ST, false>), grid, blk, 0, stream, P);

@@ -57,8 +57,8 @@ hipError_t launch_build_thresholds(const DeviceTables &t, const float *cpts, uin
                                    hipStream_t stream);
 
 // Nodes order[begin .. begin+count) of one colour, all of launch class klass
-// (0: main kernel, tables staged in lds_bytes of LDS; 1: main kernel, tables
-// in global memory; 2: KP 16; 3: generic).
+// (0: fast kernel, tables staged in lds_bytes of LDS; 1: fast kernel, tables
+// in global memory; 2: wide kernel; 3: generic kernel).
 hipError_t launch_sweep(SweepParams P, int32_t begin, int32_t count, int32_t klass,
                         int32_t lds_bytes, int32_t state_bytes, hipStream_t stream);
 
