@@ -40,7 +40,10 @@ def parse():
     p.add_argument("--cfg", type=int, default=5)
     p.add_argument("--n-cols", type=int, default=None, help="override the column count")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-sample-cols", type=int, default=32768)
+    p.add_argument("--cpu-sample-cols", type=int, default=250_000,
+                   help="columns of minibatch 0 the oracle baseline runs on (all nodes, all replicas)")
+    p.add_argument("--cpu-sample-steps", type=int, default=2,
+                   help="SAME steps (sweep + counts + resample) of the oracle baseline")
     p.add_argument("--copy-calibration", action="store_true",
                    help="also run a plain 1 GiB device copy (for HBM counter scaling)")
     p.add_argument("--gen-device", choices=["cuda", "cpu"], default="cuda",
@@ -53,11 +56,17 @@ def parse():
     p.add_argument("--stream-steps", type=int, default=2)
     p.add_argument("--minibatches", type=int, default=None,
                    help="process only the first K minibatches (profiling runs)")
+    p.add_argument("--counters-summary", nargs="+", metavar="CSV", default=None,
+                   help="summarise rocprofv3 counter_collection CSVs (no GPU work): per-kernel "
+                        "averages, and the sweep kernel's HBM traffic scaled by the 1 GiB copy")
     return p.parse_args()
 
 
 def main():
     args = parse()
+    if args.counters_summary:
+        counters_summary(args.counters_summary, args.cfg)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
               "(see the design notes for how the sampler would shard columns)", file=sys.stderr)
@@ -123,6 +132,9 @@ def main():
         one_pass(s)
     torch.cuda.synchronize()
     log("warmup done")
+    # every sweep-kernel launch of the timed passes is bracketed by HIP events
+    # on the launch stream (the library records them; read after the region)
+    same.same_kernel_timing(ctx, True)
     t_start = time.perf_counter()
     ev_start = torch.cuda.Event(enable_timing=True)
     ev_end = torch.cuda.Event(enable_timing=True)
@@ -132,46 +144,16 @@ def main():
     ev_end.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
+    kt = same.same_kernel_times(ctx)
+    same.same_kernel_timing(ctx, False)
     gpu_ms = ev_start.elapsed_time(ev_end)
     elapsed = max(wall, gpu_ms / 1e3)
     log("timed %d passes: wall %.3f s, events %.3f s" % (args.steps, wall, gpu_ms / 1e3))
+    log("sweep kernels per class (ms, launches): %s" % list(zip(kt["ms"], kt["launches"])))
     node_samples = float(net.n) * cols_timed * w.m * args.steps
-
-    # the sweep kernels alone: HIP events around every same_sweep call of one
-    # further pass over the same minibatches (same launches as inside same_step)
-    sweep_ev = []
-    s_extra = args.warmup + args.steps
-    for b in mbs:
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        same.same_sweep(ctx, w.states[b], w.obs[b], cpts, w.m, w.mb_cols(b), w.ld, b * w.nb,
-                        w.seed, s_extra, ws)
-        e1.record(stream)
-        sweep_ev.append((e0, e1))
-    torch.cuda.synchronize()
-
     value = node_samples / elapsed
-    sweep_s = sum(a.elapsed_time(b) for a, b in sweep_ev) / 1e3
-    launches = sum(same.same_sweep_plan(ctx, w.m, w.mb_cols(b))[1] for b in mbs)
-    node_samples_sweep = float(net.n) * cols_timed * w.m
-    bytes_per_ns = 1.0 + hidden + 1.0 / w.m   # read each state, write each latent, obs per column
-    alg_bytes = node_samples * bytes_per_ns
-    achieved = node_samples_sweep * bytes_per_ns / sweep_s / 1e9
-    roofline = {
-        "kernel": "sweep_main_kernel (every colour-group launch of a sweep)",
-        "bound": "hbm",
-        "achieved": round(achieved, 1),
-        "peak": HBM_PEAK_GBS,
-        "unit": "GB/s",
-        "frac": round(achieved / HBM_PEAK_GBS, 4),
-        "traffic": None,
-        "bytes_per_node_sample": round(bytes_per_ns, 4),
-        "launches": launches,
-        "avg_launch_ms": round(sweep_s * 1e3 / launches, 4),
-        "sweep_share_of_step": round(sweep_s * args.steps / elapsed, 3),
-        "tile_cols": same.same_sweep_plan(ctx, w.m, w.mb_cols(0))[0],
-    }
+
+    roofline = sweep_roofline(w, net, mbs, hidden, node_samples, kt, elapsed, args)
 
     if args.copy_calibration:
         # a plain device-to-device copy of exactly 1 GiB (runtime copy kernel)
@@ -187,7 +169,7 @@ def main():
 
     cpu = None
     if sample is not None:
-        cpu = cpu_baseline(w, *sample)
+        cpu = cpu_baseline(w, *sample, args.cpu_sample_steps)
 
     spec = CONFIGS[args.cfg]
     out = {
@@ -219,13 +201,189 @@ def main():
             "parallelism": "single-gpu",
         },
         "latent_draws_per_s": round(value * hidden, 1),
-        "hbm_gbs_algorithmic_step": round(alg_bytes / elapsed / 1e9, 1),
+        "hbm_gbs_algorithmic_step": round(node_samples * (1.0 + hidden + 1.0 / w.m) / elapsed / 1e9, 1),
         "roofline": roofline,
         "cpu_baseline": cpu,
         "streamed_from_host": streamed,
         "table_nodes": ctx.table_nodes,
     }
     print(json.dumps(out), flush=True)
+
+
+ALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12   # one 32-bit VALU op per lane per clock
+PHILOX_OPS_PER_DRAW = 23                   # 80 ops per Philox4x32-10 block / 4 words + U24
+
+
+def alu_ops_per_draw(net):
+    """Algorithmic 32-bit operations of one latent draw of each node: one
+    multiply-add per blanket state term of the CPT row indices, K * (children)
+    multiplications of the conditional, K running sums, K comparisons, and a
+    quarter of a Philox4x32-10 block plus the uniform's conversion."""
+    import numpy as np
+    n = net.n
+    kids = [[] for _ in range(n)]
+    for h, ps in enumerate(net.parents):
+        for p in ps:
+            kids[p].append(h)
+    ops = np.zeros(n)
+    for i in range(n):
+        K = int(net.card[i])
+        terms = len(net.parents[i]) + sum(len(net.parents[h]) for h in kids[i])
+        ops[i] = terms + K * len(kids[i]) + 2 * K + PHILOX_OPS_PER_DRAW
+    return ops
+
+
+def source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("kernels.hip", "graph.cpp", "graph.hpp"):
+        with open(os.path.join(ROOT, "paper_1511_06416_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def traffic_path(cfg):
+    from workloads import CONFIGS
+    return os.path.join(ROOT, "profiles", "sweep_fast_kernel.%s.traffic.json" % CONFIGS[cfg]["name"])
+
+
+def measured_traffic(cfg):
+    """HBM bytes per sweep-kernel launch from the committed counter summary of
+    this workload, if it was taken on the current kernel sources (else None)."""
+    path = traffic_path(cfg)
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        t = json.load(fh)
+    if t.get("sources_sha256") != source_hash():
+        return None
+    return t
+
+
+def sweep_roofline(w, net, mbs, hidden, node_samples, kt, elapsed, args):
+    """Roofline of the dominant kernel (the fast sweep kernel, both variants):
+    algorithmic bytes per second against HBM peak; beside it, algorithmic 32-bit
+    operations per second against the VALU peak, and the HBM bytes the counters
+    measured per launch (when taken on the current kernel sources)."""
+    import numpy as np
+    fast_ms = kt["ms"][0] + kt["ms"][1]
+    fast_launches = kt["launches"][0] + kt["launches"][1]
+    all_ms = sum(kt["ms"])
+    assert kt["launches"][2] == 0 and kt["launches"][3] == 0, \
+        "this workload is expected to run entirely in the fast sweep kernel"
+    bytes_per_ns = 1.0 + hidden + 1.0 / w.m   # read each state, write each latent, obs per column
+    alg_bytes = node_samples * bytes_per_ns
+    # latent draws per node per step, from the obs masks of the timed minibatches
+    lat = np.zeros(net.n)
+    for b in mbs:
+        lat += (w.obs[b][:, :w.mb_cols(b)] == 0).sum(dim=1).cpu().numpy().astype(np.float64)
+    ops = float((alu_ops_per_draw(net) * lat).sum()) * w.m * args.steps
+    secs = fast_ms / 1e3
+    hbm = alg_bytes / secs / 1e9
+    alu = ops / secs / 1e12
+    traffic = measured_traffic(args.cfg)
+    avg_ms = fast_ms / fast_launches
+    out = {
+        "kernel": "sweep_fast_kernel (LDS-staged and global-table variants; every launch of the timed passes)",
+        "bound": "hbm",
+        "achieved": round(hbm, 1),
+        "peak": HBM_PEAK_GBS,
+        "unit": "GB/s",
+        "frac": round(hbm / HBM_PEAK_GBS, 4),
+        "traffic": None if traffic is None else traffic["hbm_bytes_per_launch"],
+        "algorithmic_bytes_per_launch": round(alg_bytes / fast_launches, 1),
+        "bytes_per_node_sample": round(bytes_per_ns, 4),
+        "launches": fast_launches,
+        "avg_launch_ms": round(avg_ms, 4),
+        "alu": {"achieved": round(alu, 3), "peak": round(ALU_PEAK_TOPS, 2), "unit": "TOP/s",
+                "frac": round(alu / ALU_PEAK_TOPS, 4),
+                "algorithmic_ops_per_launch": round(ops / fast_launches, 1)},
+        "sweep_share_of_step": round(all_ms / 1e3 / elapsed, 3),
+    }
+    if traffic is not None:
+        out["traffic_gbs"] = round(traffic["hbm_bytes_per_launch"] / (avg_ms / 1e3) / 1e9, 1)
+    return out
+
+
+COPY_BYTES = 1 << 30
+
+
+def counters_summary(paths, cfg):
+    """Per-kernel averages of rocprofv3 counter CSVs (one counter set per run).
+    FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of the sweep kernel are scaled by
+    what the same counters read for the 1 GiB device copy of --copy-calibration
+    (1 GiB read and 1 GiB written), giving HBM bytes per launch; the result is
+    written under profiles/ for later runs on the same kernel sources."""
+    import collections
+    import csv
+    import re
+    totals = collections.defaultdict(float)   # (kernel, counter) -> sum over dispatches
+    seen = collections.defaultdict(set)       # (kernel, counter) -> dispatches
+    dur = collections.defaultdict(dict)       # kernel -> dispatch -> microseconds
+    per_dispatch = {}
+    for path in paths:
+        with open(path) as fh:
+            for r in csv.DictReader(fh):
+                k, c, d = r["Kernel_Name"], r["Counter_Name"], (path, r["Dispatch_Id"])
+                totals[(k, c)] += float(r["Counter_Value"])
+                seen[(k, c)].add(d)
+                # largest value of each (kernel, counter, grid): finds single dispatches
+                key = (k, c, r["Grid_Size"])
+                per_dispatch[key] = max(per_dispatch.get(key, 0.0), float(r["Counter_Value"]))
+                dur[k][d] = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+
+    def avg(k, c):
+        return totals[(k, c)] / len(seen[(k, c)]) if (k, c) in seen else None
+
+    kernels = sorted(dur, key=lambda k: -sum(dur[k].values()))
+    counters = sorted({c for (_k, c) in totals})
+    print("| kernel | dispatches | avg us | " + " | ".join(counters) + " |")
+    print("|---|---|---|" + "---|" * len(counters))
+    for k in kernels:
+        vals = ["-" if avg(k, c) is None else "%.4g" % avg(k, c) for c in counters]
+        print("| %s | %d | %.1f | %s |" % (k[:100], len(dur[k]), sum(dur[k].values()) / len(dur[k]),
+                                         " | ".join(vals)))
+    sweep = [k for k in kernels if re.search(r"sweep_fast_kernel<[^,]+, false,", k)]
+    # the 1 GiB device copy: the non-library dispatch whose WRITE_SIZE is 1 GiB
+    # within 5%; its FETCH_SIZE is the same kernel and grid in the FETCH_SIZE run
+    copy = None
+    for (k, c, grid), v in per_dispatch.items():
+        if c == "WRITE_SIZE" and "same::" not in k and abs(v * 1024 - COPY_BYTES) < 0.05 * COPY_BYTES:
+            copy = (k, grid, v)
+    fetch_copy = None
+    if copy is not None:
+        fetch_copy = per_dispatch.get((copy[0], "FETCH_SIZE", copy[1]))
+    if copy is None or not fetch_copy or not sweep:
+        print("no copy calibration, FETCH_SIZE run or sweep kernel in these files")
+        return
+    f_scale = COPY_BYTES / (fetch_copy * 1024)
+    w_scale = COPY_BYTES / (copy[2] * 1024)
+
+    def per_launch(c):
+        n = sum(len(seen[(k, c)]) for k in sweep if (k, c) in seen)
+        return sum(totals.get((k, c), 0.0) for k in sweep) * 1024 / max(n, 1), n
+
+    fb, nf = per_launch("FETCH_SIZE")
+    wb, nw = per_launch("WRITE_SIZE")
+    fb *= f_scale
+    wb *= w_scale
+    out = {
+        "kernel": "sweep_fast_kernel (both variants, non-debug)",
+        "workload_cfg": cfg,
+        "copy_kernel": copy[0],
+        "copy_counters_kib": {"FETCH_SIZE": fetch_copy, "WRITE_SIZE": copy[2]},
+        "scale": {"fetch": round(f_scale, 4), "write": round(w_scale, 4)},
+        "fetch_bytes_per_launch": round(fb, 1),
+        "write_bytes_per_launch": round(wb, 1),
+        "hbm_bytes_per_launch": round(fb + wb, 1),
+        "dispatches": {"fetch": nf, "write": nw},
+        "sources_sha256": source_hash(),
+    }
+    path = traffic_path(cfg)
+    os.makedirs(os.path.dirname(path), exist_ok=True)
+    with open(path, "w") as fh:
+        json.dump(out, fh, indent=1)
+    print(json.dumps(out))
 
 
 def stream_timing(w, ctx, cpts, ws, dev, steps):
@@ -275,26 +433,29 @@ def stream_timing(w, ctx, cpts, ws, dev, steps):
                                   "d2h": round(state_bytes * steps / dt / 1e9, 1)}}
 
 
-def cpu_baseline(w, cols, st, ob):
+def cpu_baseline(w, cols, st, ob, steps):
     """The oracle (fp64, OpenMP over columns) on the first `cols` columns of
-    minibatch 0 as generated: one sweep, its counts and one Dirichlet resample."""
+    minibatch 0 as generated: `steps` SAME steps, each one sweep, its counts
+    and one Dirichlet resample."""
     import oracle
 
     net = w.net
     threads = len(os.sched_getaffinity(0))
     color = oracle.graph(net.parents, net.card)["color"]
+    theta = w.init_theta
     t = time.perf_counter()
-    oracle.sweep(net.parents, net.card, w.init_theta, color, st, ob, w.m, cols, 0, w.seed, 0,
-                 n_threads=threads)
-    cnt = oracle.counts(net.parents, net.card, st, w.m, cols, n_threads=threads)
-    oracle.dirichlet(net.parents, net.card, cnt, w.alpha, w.seed, 0)
+    for s in range(steps):
+        oracle.sweep(net.parents, net.card, theta, color, st, ob, w.m, cols, 0, w.seed, s,
+                     n_threads=threads)
+        cnt = oracle.counts(net.parents, net.card, st, w.m, cols, n_threads=threads)
+        theta = oracle.dirichlet(net.parents, net.card, cnt, w.alpha, w.seed, s)
     dt = time.perf_counter() - t
-    ns = float(net.n) * cols * w.m
-    log("cpu baseline: %d columns, %.2f s, %d threads" % (cols, dt, threads))
+    ns = float(net.n) * cols * w.m * steps
+    log("cpu baseline: %d columns x %d steps, %.2f s, %d threads" % (cols, steps, dt, threads))
     return {"value": round(ns / dt, 1), "unit": "node-samples/s", "cores": threads,
             "kind": "oracle",
-            "sample": "first %d columns of minibatch 0 (all %d nodes, m=%d): one sweep + counts "
-                      "+ one Dirichlet resample, %.1f s" % (cols, net.n, w.m, dt)}
+            "sample": "first %d columns of minibatch 0 (all %d nodes, m=%d), %d SAME steps (sweep + "
+                      "counts + Dirichlet resample each), %.1f s" % (cols, net.n, w.m, steps, dt)}
 
 
 if __name__ == "__main__":

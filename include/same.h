@@ -106,6 +106,14 @@ typedef struct {
      * one tile = the whole minibatch).  Tiles are at least 1024 columns wide.
      * Results do not depend on it. */
     int64_t tile_bytes;
+    /* Largest per-node table record (bytes) a sweep block copies into LDS
+     * before drawing; larger records are read from global memory.  -1 selects
+     * the default (32768); 0 stages nothing.  Results do not depend on it. */
+    int64_t lds_limit;
+    /* 1 (default): blanket indices of nodes with K <= 8 and records below
+     * 2^16 rows use packed 16-bit arithmetic; 0: every product-mode node uses
+     * the 32-bit path.  Results do not depend on it. */
+    int32_t packed_indices;
 } same_options_t;
 
 /* same_create with options (opts may be NULL for the defaults). */
@@ -196,10 +204,10 @@ int same_sweep_plan(const same_ctx *ctx, int32_t m, int64_t n_cols, int64_t *til
 /*
  * One whole SAME step over one minibatch (Sec. 4, Fig. 1): same_sweep, then
  * same_counts into mb_counts and totals, then same_sample_cpts writing cpts in
- * place with update_id.  The result equals those three calls in that order;
- * the sweep and the counts run over column tiles sized for the device's
- * last-level cache, so the count pass reads the tile the sweep just visited.
- * Device pointers; cpts is read by the sweep and rewritten by the resample.
+ * place with update_id.  The result equals those three calls in that order.
+ * With a tile_bytes option the sweep and the counts run tile by tile, so the
+ * count pass reads the tile the sweep just visited.  Device pointers; cpts is
+ * read by the sweep and rewritten by the resample.
  */
 int same_step(same_ctx *ctx, void *states, const uint8_t *obs, float *cpts, int32_t m,
               int64_t n_cols, int64_t ld, int64_t col_offset, uint64_t seed, uint32_t sweep_id,
@@ -240,6 +248,24 @@ int same_stream_pass(same_ctx *ctx, void *host_states, const uint8_t *host_obs, 
                      int64_t n_cols, int64_t nb, int32_t m, float *cpts, int32_t *mb_counts,
                      int32_t *totals, uint64_t seed, uint32_t pass_id, int32_t flags, void *slots,
                      void *workspace, void *stream);
+
+/*
+ * Measurement of the sweep kernels.  same_kernel_timing(ctx, 1) clears the
+ * totals and makes every later sweep of ctx bracket each of its kernel
+ * launches with a pair of HIP events on the launch stream; (ctx, 0) clears
+ * them and stops.  same_kernel_times waits for the recorded launches and
+ * returns, per launch class (0: tables staged in LDS, 1: tables in global
+ * memory, 2: 32-bit index path, 3: K > 16), the summed device milliseconds and
+ * the number of kernel launches since timing was enabled.  Host calls; the
+ * waits make them unsuitable inside a captured or latency-critical sequence.
+ */
+typedef struct {
+    double ms[4];
+    int64_t launches[4];
+} same_kernel_times_t;
+
+int same_kernel_timing(same_ctx *ctx, int32_t enable);
+int same_kernel_times(same_ctx *ctx, same_kernel_times_t *out);
 
 /* Message for the calling thread's last failed call ("" if none). */
 const char *same_last_error(void);

@@ -19,6 +19,7 @@ __all__ = [
     "SameError", "Context", "same_create", "same_create_ex", "same_destroy", "same_layout", "same_workspace_size",
     "same_sweep", "same_sweep_debug", "same_counts", "same_sample_cpts", "same_last_error",
     "same_step", "same_sweep_plan", "same_stream_slots_size", "same_stream_pass", "SAME_STREAM_COUNTS_ONLY",
+    "same_kernel_timing", "same_kernel_times",
     "library_path", "load_library",
 ]
 
@@ -41,7 +42,12 @@ class SameError(RuntimeError):
 
 
 class _Options(C.Structure):
-    _fields_ = [("table_limit", C.c_int64), ("tile_bytes", C.c_int64)]
+    _fields_ = [("table_limit", C.c_int64), ("tile_bytes", C.c_int64), ("lds_limit", C.c_int64),
+                ("packed_indices", C.c_int32)]
+
+
+class _KernelTimes(C.Structure):
+    _fields_ = [("ms", C.c_double * 4), ("launches", C.c_int64 * 4)]
 
 
 class _Layout(C.Structure):
@@ -78,12 +84,14 @@ def load_library():
         L.same_sweep_plan.argtypes = [P, I32, I64, C.POINTER(C.c_int64), C.POINTER(C.c_int32)]
         L.same_stream_slots_size.argtypes = [P, I32, I64, C.POINTER(C.c_size_t)]
         L.same_stream_pass.argtypes = [P, P, P, I64, I64, I64, I32, P, P, P, U64, U32, I32, P, P, P]
+        L.same_kernel_timing.argtypes = [P, I32]
+        L.same_kernel_times.argtypes = [P, C.POINTER(_KernelTimes)]
         L.same_last_error.argtypes = []
         L.same_last_error.restype = C.c_char_p
         for f in ("same_create", "same_create_ex", "same_layout", "same_workspace_size", "same_sweep",
                   "same_sweep_debug", "same_counts", "same_sample_cpts", "same_step", "same_sweep_plan",
-                  "same_stream_slots_size",
-                  "same_stream_pass"):
+                  "same_stream_slots_size", "same_stream_pass", "same_kernel_timing",
+                  "same_kernel_times"):
             getattr(L, f).restype = C.c_int
         _lib = L
         return L
@@ -120,17 +128,18 @@ class Context:
     """Owns one same_ctx (one network)."""
 
     def __init__(self, parent_ptr, parent_idx, card, dirichlet_prior=1.0, table_limit=None,
-                 tile_bytes=0):
+                 tile_bytes=0, lds_limit=None, packed_indices=True):
         L = load_library()
         self._pptr = np.ascontiguousarray(parent_ptr, dtype=np.int32)
         self._pidx = np.ascontiguousarray(parent_idx if len(parent_idx) else [0], dtype=np.int32)
         self._card = np.ascontiguousarray(card, dtype=np.int32)
         h = C.c_void_p()
-        if table_limit is None and not tile_bytes:
+        if table_limit is None and not tile_bytes and lds_limit is None and packed_indices:
             _check(L.same_create(len(self._card), self._pptr.ctypes.data, self._pidx.ctypes.data,
                                  self._card.ctypes.data, float(dirichlet_prior), C.byref(h)))
         else:
-            opts = _Options(-1 if table_limit is None else int(table_limit), int(tile_bytes))
+            opts = _Options(-1 if table_limit is None else int(table_limit), int(tile_bytes),
+                            -1 if lds_limit is None else int(lds_limit), 1 if packed_indices else 0)
             _check(L.same_create_ex(len(self._card), self._pptr.ctypes.data,
                                     self._pidx.ctypes.data, self._card.ctypes.data,
                                     float(dirichlet_prior), C.byref(opts), C.byref(h)))
@@ -174,9 +183,9 @@ def same_create(parent_ptr, parent_idx, card, dirichlet_prior=1.0) -> Context:
 
 
 def same_create_ex(parent_ptr, parent_idx, card, dirichlet_prior=1.0, table_limit=-1,
-                   tile_bytes=0) -> Context:
+                   tile_bytes=0, lds_limit=-1, packed_indices=True) -> Context:
     return Context(parent_ptr, parent_idx, card, dirichlet_prior, table_limit=table_limit,
-                   tile_bytes=tile_bytes)
+                   tile_bytes=tile_bytes, lds_limit=lds_limit, packed_indices=packed_indices)
 
 
 def same_destroy(ctx: Context) -> None:
@@ -249,3 +258,15 @@ def same_stream_pass(ctx, host_states, host_obs, host_ld, n_cols, nb, m, cpts, m
                                            _ptr(mb_counts), _ptr(totals), int(seed), int(pass_id),
                                            int(flags), _ptr(slots), _ptr(workspace),
                                            _stream(stream)))
+
+
+def same_kernel_timing(ctx, enable=True):
+    """Starts (or stops) per-launch event timing of ctx's sweep kernels; clears the totals."""
+    _check(load_library().same_kernel_timing(ctx.handle, 1 if enable else 0))
+
+
+def same_kernel_times(ctx):
+    """{'ms': [4 floats], 'launches': [4 ints]} per launch class since timing was enabled."""
+    t = _KernelTimes()
+    _check(load_library().same_kernel_times(ctx.handle, C.byref(t)))
+    return {"ms": list(t.ms), "launches": list(t.launches)}

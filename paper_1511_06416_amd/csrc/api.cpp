@@ -36,8 +36,21 @@ struct StreamRes {
     bool slot_used[2] = {false, false};
 };
 
+// Optional per-launch timing of the sweep kernels (same_kernel_timing).
+struct KernelTiming {
+    bool on = false;
+    struct Rec {
+        int32_t klass, launches;
+        hipEvent_t start, end;
+    };
+    std::vector<Rec> pending;
+    double ms[same::kLaunchClasses] = {};
+    int64_t launches[same::kLaunchClasses] = {};
+};
+
 struct same_ctx {
     same::Compiled g;
+    KernelTiming timing;
     double alpha = 1.0;
     std::vector<same::DeviceTables> dev;  // indexed by device ordinal
     std::vector<StreamRes> sres;          // indexed by device ordinal
@@ -277,11 +290,43 @@ int sweep_tile(same_ctx *ctx, const same::SweepParams &P0, int64_t t0, int64_t n
     for (int32_t c = 0; c < g.n_colors; ++c)
         for (int32_t k = 0; k < L; ++k) {
             const int32_t b = g.launch[c * (L + 1) + k], e = g.launch[c * (L + 1) + k + 1];
+            KernelTiming::Rec rec{k, (e - b + 65534) / 65535, nullptr, nullptr};
+            const bool timed = ctx->timing.on && e > b && nt > 0;
+            if (timed) {
+                int rc = check_hip(hipEventCreate(&rec.start), "hipEventCreate");
+                if (!rc) rc = check_hip(hipEventCreate(&rec.end), "hipEventCreate");
+                if (!rc) rc = check_hip(hipEventRecord(rec.start, s), "hipEventRecord");
+                if (rc) return rc;
+            }
             int rc = check_hip(same::launch_sweep(P, b, e - b, k, g.launch_lds[c * L + k], g.state_bytes, s),
                                "sweep launch");
             if (rc) return rc;
+            if (timed) {
+                rc = check_hip(hipEventRecord(rec.end, s), "hipEventRecord");
+                if (rc) return rc;
+                ctx->timing.pending.push_back(rec);
+            }
         }
     return SAME_OK;
+}
+
+// Folds the finished timing records into the totals (waits for each).
+int collect_timing(same_ctx *ctx) {
+    KernelTiming &t = ctx->timing;
+    int rc = SAME_OK;
+    for (const KernelTiming::Rec &r : t.pending) {
+        float ms = 0.f;
+        if (!rc) rc = check_hip(hipEventSynchronize(r.end), "hipEventSynchronize");
+        if (!rc) rc = check_hip(hipEventElapsedTime(&ms, r.start, r.end), "hipEventElapsedTime");
+        if (!rc) {
+            t.ms[r.klass] += ms;
+            t.launches[r.klass] += r.launches;
+        }
+        (void)hipEventDestroy(r.start);
+        (void)hipEventDestroy(r.end);
+    }
+    t.pending.clear();
+    return rc;
 }
 
 int do_sweep(same_ctx *ctx, void *states, const uint8_t *obs, const float *cpts, int32_t m,
@@ -377,6 +422,13 @@ int same_create_ex(int32_t n_nodes, const int32_t *parent_ptr, const int32_t *pa
     if (opts && opts->table_limit >= 0) table_limit = opts->table_limit;
     if (opts && opts->table_limit < -1) return set_error(SAME_EINVAL, "table_limit must be >= -1");
     if (opts && opts->tile_bytes < 0) return set_error(SAME_EINVAL, "tile_bytes must be >= 0");
+    int64_t lds_limit = same::kLdsBudgetBytes;
+    if (opts && opts->lds_limit >= 0) lds_limit = opts->lds_limit;
+    if (opts && (opts->lds_limit < -1 || opts->lds_limit > same::kLdsBudgetBytes))
+        return set_error(SAME_EINVAL, "lds_limit must be -1 or in [0, 32768]");
+    if (opts && opts->packed_indices != 0 && opts->packed_indices != 1)
+        return set_error(SAME_EINVAL, "packed_indices must be 0 or 1");
+    const bool packed = !opts || opts->packed_indices != 0;
     *out = nullptr;
     if (!(dirichlet_prior > 0.0)) return set_error(SAME_EINVAL, "dirichlet_prior must be > 0");
     same_ctx *ctx = new (std::nothrow) same_ctx();
@@ -384,7 +436,8 @@ int same_create_ex(int32_t n_nodes, const int32_t *parent_ptr, const int32_t *pa
     std::string err;
     int rc;
     try {
-        rc = same::compile_graph(n_nodes, parent_ptr, parent_idx, card, ctx->g, err, table_limit);
+        rc = same::compile_graph(n_nodes, parent_ptr, parent_idx, card, ctx->g, err, table_limit,
+                                 lds_limit, packed);
     } catch (const std::bad_alloc &) {
         rc = SAME_ENOMEM;
         err = "out of host memory";
@@ -406,6 +459,10 @@ int same_create_ex(int32_t n_nodes, const int32_t *parent_ptr, const int32_t *pa
 
 void same_destroy(same_ctx *ctx) {
     if (!ctx) return;
+    for (auto &r : ctx->timing.pending) {
+        (void)hipEventDestroy(r.start);
+        (void)hipEventDestroy(r.end);
+    }
     for (auto &r : ctx->sres) free_stream_res(r);
     for (auto &t : ctx->dev) free_tables(t);
     delete ctx;
@@ -605,3 +662,26 @@ int same_stream_pass(same_ctx *ctx, void *host_states, const uint8_t *host_obs, 
 }
 
 }  // extern "C"
+
+extern "C" int same_kernel_timing(same_ctx *ctx, int32_t enable) {
+    if (!ctx) return set_error(SAME_EINVAL, "null context");
+    std::lock_guard<std::mutex> lock(ctx->mu);
+    int rc = collect_timing(ctx);
+    ctx->timing.on = enable != 0;
+    for (int32_t k = 0; k < same::kLaunchClasses; ++k) {
+        ctx->timing.ms[k] = 0.0;
+        ctx->timing.launches[k] = 0;
+    }
+    return rc;
+}
+
+extern "C" int same_kernel_times(same_ctx *ctx, same_kernel_times_t *out) {
+    if (!ctx || !out) return set_error(SAME_EINVAL, "null argument");
+    std::lock_guard<std::mutex> lock(ctx->mu);
+    int rc = collect_timing(ctx);
+    for (int32_t k = 0; k < same::kLaunchClasses; ++k) {
+        out->ms[k] = ctx->timing.ms[k];
+        out->launches[k] = ctx->timing.launches[k];
+    }
+    return rc;
+}

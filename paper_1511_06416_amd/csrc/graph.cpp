@@ -35,7 +35,7 @@ int32_t thresholds_per_config(int32_t K) {
 }
 
 int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int32_t *card,
-                  Compiled &g, std::string &err, int64_t table_limit) {
+                  Compiled &g, std::string &err, int64_t table_limit, int64_t lds_limit, bool packed) {
     if (n <= 0) return fail(err, SAME_EINVAL, "n_nodes must be positive");
     if (!pptr || !card) return fail(err, SAME_EINVAL, "parent_ptr and card must be non-null");
     if (pptr[0] != 0) return fail(err, SAME_EGRAPH, "parent_ptr[0] must be 0");
@@ -284,7 +284,9 @@ int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int
         } else {
             const int64_t bytes = tab ? cond_len * 4 : g.tab_len[i] * 4;
             const int64_t row_bytes = tab ? (int64_t)KT * 4 : (int64_t)KP * 4;
-            if (bytes <= kLdsBudgetBytes) {
+            if (!packed && !tab) {
+                klass = 2;
+            } else if (bytes <= lds_limit) {
                 klass = 0;
                 unit = 1;
                 g.lds_bytes[i] = (int32_t)((bytes + 15) & ~int64_t(15));  // staged in float4s

@@ -141,7 +141,10 @@ struct Compiled {
 // Returns 0 or a negative SAME_E* code with a message in err.
 // table_limit: largest KT * (number of blanket configurations) for which a
 // node gets a precomputed threshold table (0 disables the table path).
+// lds_limit: largest table record (bytes) staged in LDS (class 0).
+// packed: false sends every product-mode node to the wide class.
 int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int32_t *card,
-                  Compiled &out, std::string &err, int64_t table_limit = 16384);
+                  Compiled &out, std::string &err, int64_t table_limit = 16384,
+                  int64_t lds_limit = kLdsBudgetBytes, bool packed = true);
 
 }  // namespace same

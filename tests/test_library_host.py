@@ -187,3 +187,43 @@ def test_stream_argument_errors():
     assert L.same_stream_slots_size(ctx.handle, 2, 256, C.byref(size)) == same.SAME_OK
     # two slots of 5 nodes x 2 replicas x 256 columns plus 5 x 256 obs bytes
     assert size.value >= 2 * (5 * 2 * 256 + 5 * 256)
+
+
+@pytest.mark.parametrize("field,value", [("lds_limit", -2), ("lds_limit", 40000),
+                                         ("packed_indices", 2), ("tile_bytes", -1),
+                                         ("table_limit", -5)])
+def test_bad_options(field, value):
+    net = koller()
+    pptr, pidx, card = net.csr()
+    L = same.load_library()
+    opts = same._Options(-1, 0, -1, 1)
+    setattr(opts, field, value)
+    h = C.c_void_p()
+    pptr = np.ascontiguousarray(pptr, dtype=np.int32)
+    pidx = np.ascontiguousarray(pidx, dtype=np.int32)
+    card = np.ascontiguousarray(card, dtype=np.int32)
+    rc = L.same_create_ex(len(card), pptr.ctypes.data, pidx.ctypes.data, card.ctypes.data, 1.0,
+                          C.byref(opts), C.byref(h))
+    assert rc == same.SAME_EINVAL
+
+
+@pytest.mark.parametrize("kw", [dict(lds_limit=0), dict(packed_indices=False),
+                                dict(lds_limit=0, packed_indices=False)])
+def test_kernel_class_options_keep_layout(kw):
+    net = make_network(3)
+    pptr, pidx, card = net.csr()
+    a = same.same_create(pptr, pidx, card)
+    b = same.same_create_ex(pptr, pidx, card, **kw)
+    assert np.array_equal(a.cpt_off, b.cpt_off) and np.array_equal(a.color, b.color)
+    assert a.workspace_bytes == b.workspace_bytes
+    assert b.sweep_launches >= a.sweep_launches or kw == dict(lds_limit=0)
+
+
+def test_kernel_timing_host_calls():
+    ctx = _ctx(koller())
+    assert same.same_kernel_times(ctx) == {"ms": [0.0] * 4, "launches": [0] * 4}
+    same.same_kernel_timing(ctx, True)
+    same.same_kernel_timing(ctx, False)
+    L = same.load_library()
+    assert L.same_kernel_timing(None, 1) == same.SAME_EINVAL
+    assert L.same_kernel_times(ctx.handle, None) == same.SAME_EINVAL

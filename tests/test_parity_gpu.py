@@ -27,9 +27,9 @@ def _gpu():
     same.load_library()
 
 
-def _sweep_case(w, b=0, sweep_id=3, win=None, theta=None, n_threads=0, table_limit=None):
+def _sweep_case(w, b=0, sweep_id=3, win=None, theta=None, n_threads=0, table_limit=None, **ctx_kw):
     net = w.net
-    ctx = H.context_for(net, table_limit=table_limit)
+    ctx = H.context_for(net, table_limit=table_limit, **ctx_kw)
     color = oracle.graph(net.parents, net.card)["color"]
     assert np.array_equal(ctx.color, color)
     theta = w.init_theta if theta is None else theta
@@ -40,7 +40,7 @@ def _sweep_case(w, b=0, sweep_id=3, win=None, theta=None, n_threads=0, table_lim
     ref = pre.copy()
     res = oracle.sweep(net.parents, net.card, theta, color, ref, obs, w.m, ncols, b * w.nb,
                        w.seed, sweep_id, want_flags=True, win=win, n_threads=n_threads)
-    st = H.compare_states(gpu, ref, res["flags"], color, ncols)
+    st = H.compare_states(gpu, ref, res["flags"], color, ncols, obs=obs)
     out = {"states": st, "draws": res["draws"]}
     if win is not None:
         div = H.diverged_chains(gpu, ref, ncols, win)
@@ -62,6 +62,22 @@ def _sweep_case(w, b=0, sweep_id=3, win=None, theta=None, n_threads=0, table_lim
 def test_sweep_parity_configs(cfg, kw, win, table_limit):
     w = make_workload(cfg, **kw)
     out = _sweep_case(w, win=win, table_limit=table_limit)
+    assert out["probs"]["checked"] > 0
+
+
+@pytest.mark.parametrize("cfg,kw,win", [
+    (2, dict(n_cols=6_000), (1000, 600)),
+    (3, dict(n_cols=9_001), (8_000, 1001)),              # ragged tail
+    (4, {}, (0, 600)),
+    (5, dict(n_cols=3_000, m=4), (2_600, 400)),
+])
+@pytest.mark.parametrize("variant", [dict(lds_limit=0), dict(packed=False), dict(lds_limit=0, packed=False)],
+                         ids=["global-tables", "wide-indices", "global-wide"])
+def test_sweep_parity_kernel_classes(cfg, kw, win, variant):
+    """The same conditionals and draws when every table is read from global
+    memory and/or every product-mode node takes the 32-bit index kernel."""
+    w = make_workload(cfg, **kw)
+    out = _sweep_case(w, win=win, **variant)
     assert out["probs"]["checked"] > 0
 
 
@@ -149,14 +165,14 @@ def _custom(parents, card, n_cols, m, hidden, seed, ld=None, theta=None, alpha=0
 
 
 def _custom_case(net, states, obs, theta, m, n_cols, col_offset=0, win=None, sweep_id=1, seed=5,
-                 table_limit=None):
-    ctx = H.context_for(net, table_limit=table_limit)
+                 table_limit=None, **ctx_kw):
+    ctx = H.context_for(net, table_limit=table_limit, **ctx_kw)
     color = oracle.graph(net.parents, net.card)["color"]
     gpu, gp = H.gpu_sweep(ctx, states, obs, theta, m, n_cols, col_offset, seed, sweep_id, win=win)
     ref = states.copy()
     res = oracle.sweep(net.parents, net.card, theta, color, ref, obs, m, n_cols, col_offset, seed,
                        sweep_id, want_flags=True, win=win)
-    st = H.compare_states(gpu, ref, res["flags"], color, n_cols)
+    st = H.compare_states(gpu, ref, res["flags"], color, n_cols, obs=obs)
     if win is not None:
         H.compare_probs(gp, res["probs"], obs, net.card, win,
                         H.diverged_chains(gpu, ref, n_cols, win))
@@ -193,23 +209,29 @@ def test_all_observed_and_all_latent():
     _custom_case(net, st, ob, th, 2, 512, win=(0, 512))
 
 
+KERNEL_VARIANTS = [dict(), dict(lds_limit=0), dict(packed=False)]
+KERNEL_VARIANT_IDS = ["default", "global-tables", "wide-indices"]
+
+
+@pytest.mark.parametrize("variant", KERNEL_VARIANTS, ids=KERNEL_VARIANT_IDS)
 @pytest.mark.parametrize("table_limit", [None, 0], ids=["tables", "products"])
 @pytest.mark.parametrize("K", [2, 3, 5, 8, 9, 16, 17, 40])
-def test_cardinality_classes(K, table_limit):
+def test_cardinality_classes(K, table_limit, variant):
     # threshold tables for K <= 9, products with KP = 2/4/8/16, generic for K > 16
     parents = [[], [0], [0, 1], [1], [2, 3]]
     card = [K, 3, K, 2, 4]
     net, st, ob, th = _custom(parents, card, 700, 3, 0.6, K)
-    _custom_case(net, st, ob, th, 3, 700, win=(0, 128), table_limit=table_limit)
+    _custom_case(net, st, ob, th, 3, 700, win=(0, 128), table_limit=table_limit, **variant)
 
 
+@pytest.mark.parametrize("variant", KERNEL_VARIANTS, ids=KERNEL_VARIANT_IDS)
 @pytest.mark.parametrize("table_limit", [None, 0], ids=["tables", "products"])
-def test_int16_states(table_limit):
+def test_int16_states(table_limit, variant):
     parents = [[], [0], [0, 1], [2], [1]]
     card = [130, 3, 200, 2, 5]
     net, st, ob, th = _custom(parents, card, 300, 2, 0.5, 17)
     assert st.dtype == np.int16
-    _custom_case(net, st, ob, th, 2, 300, win=(0, 64), table_limit=table_limit)
+    _custom_case(net, st, ob, th, 2, 300, win=(0, 64), table_limit=table_limit, **variant)
 
 
 def test_large_replica_count_and_column_offset():
