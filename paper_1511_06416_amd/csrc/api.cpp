@@ -290,7 +290,7 @@ int sweep_tile(same_ctx *ctx, const same::SweepParams &P0, int64_t t0, int64_t n
     for (int32_t c = 0; c < g.n_colors; ++c)
         for (int32_t k = 0; k < L; ++k) {
             const int32_t b = g.launch[c * (L + 1) + k], e = g.launch[c * (L + 1) + k + 1];
-            KernelTiming::Rec rec{k, (e - b + 65534) / 65535, nullptr, nullptr};
+            KernelTiming::Rec rec{k, 1, nullptr, nullptr};
             const bool timed = ctx->timing.on && e > b && nt > 0;
             if (timed) {
                 int rc = check_hip(hipEventCreate(&rec.start), "hipEventCreate");
@@ -482,7 +482,7 @@ int same_layout(const same_ctx *ctx, same_layout_t *out, int64_t *cpt_off, int32
     for (int32_t c = 0; c < g.n_colors; ++c)
         for (int32_t k = 0; k < L; ++k) {
             const int32_t cnt = g.launch[c * (L + 1) + k + 1] - g.launch[c * (L + 1) + k];
-            launches += (cnt + 65534) / 65535;
+            launches += cnt > 0 ? 1 : 0;
         }
     out->sweep_launches = launches;
     int32_t tn = 0;

@@ -410,14 +410,41 @@ struct Work {
     int r0, r1;
 };
 
+// Blocks are dealt to the XCDs round robin by linear block id.  The 1-D grid
+// is decoded so that the blocks one XCD receives in order take every node of
+// the launch for one slab (column chunk x replica range) before the next
+// slab: the blocks resident on an XCD then read the same columns of the
+// shared blanket rows, which stay in that XCD's L2.
+constexpr uint32_t kXcds = 8;
+constexpr int kSweepQuadsPerLane = 1;  // column quads per lane in one sweep block
+constexpr int kMinSweepBlocks = 4096;  // replicas are split below this many blocks
+constexpr int kCountQuadsPerLane = 1;  // column quads per lane in one count block
+
+__device__ __forceinline__ void decode_block(uint32_t b, uint32_t count, uint32_t &local,
+                                             int64_t &slab) {
+    const uint32_t xcd = b % kXcds, j = b / kXcds;
+    local = j % count;
+    slab = (int64_t)(j / count) * kXcds + xcd;
+}
+
 __device__ __forceinline__ Work block_work(const SweepParams &P) {
+    uint32_t local;
+    int64_t slab;
+    decode_block(blockIdx.x, (uint32_t)P.count, local, slab);
     Work w;
-    w.node = as_const(P.order)[P.begin + blockIdx.y];
+    w.node = as_const(P.order)[P.begin + (int32_t)local];
     w.d = as_const(P.desc) + as_const(P.desc_off)[w.node];
+    if (slab >= P.n_slabs) {  // padding block of the last round
+        w.q0 = w.q1 = 0;
+        w.r0 = w.r1 = 0;
+        return w;
+    }
+    const int64_t chunk = slab / P.rsplit;
+    const int rpart = (int)(slab % P.rsplit);
     const int64_t nquads = (P.n_cols + 3) >> 2;
-    w.q0 = (int64_t)blockIdx.x * P.quads_per_block;
+    w.q0 = chunk * P.quads_per_block;
     w.q1 = w.q0 + P.quads_per_block < nquads ? w.q0 + P.quads_per_block : nquads;
-    w.r0 = (int)blockIdx.z * P.reps_per_block;
+    w.r0 = rpart * P.reps_per_block;
     w.r1 = w.r0 + P.reps_per_block < P.m ? w.r0 + P.reps_per_block : P.m;
     return w;
 }
@@ -621,8 +648,8 @@ __device__ void sweep_table(const SweepParams &P, const Work &W, lds_char *lds, 
     }
 }
 
-// Fast kernel: one block = one node (blockIdx.y in the launch range) x a run
-// of column quads (blockIdx.x) x a range of replicas (blockIdx.z).  The
+// Fast kernel: one block = one node x a run of column quads x a range of
+// replicas (block_work).  The
 // node's mode selects the product path for KP = 2, 4, 8 or the threshold
 // path.  With STAGED the block first copies its node's table record (k-vectors
 // or thresholds) into LDS, so every gather of the sweep is an LDS read.
@@ -630,6 +657,7 @@ template <typename ST, bool DEBUG, bool STAGED>
 __global__ __launch_bounds__(kBlock) void sweep_fast_kernel(SweepParams P) {
     extern __shared__ float4 lds4[];
     const Work W = block_work(P);
+    if (W.q0 >= W.q1) return;  // uniform across the block
     cint32_t *d = W.d;
     const int mode = d[2];
     const float *tab = P.table + d[3];
@@ -907,44 +935,106 @@ constexpr int kRepBins = 256;
 constexpr int kLdsBins = 8192;
 static_assert(kCopies * kRepBins <= kLdsBins, "LDS budget");
 
+constexpr int kCountReps = 4;  // replicas whose rows are loaded together
+
+// Histogram of (parent row, state) for one node over a slab of columns and all
+// m replicas (block geometry as the sweep's, decode_block).  Bins are counted
+// with packed 16-bit arithmetic (two lanes per word, as in the sweep) when the
+// node has at most 2^16 bins, else with 32-bit indices.
 template <typename ST>
 __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict__ cdesc,
                                                       const int32_t *__restrict__ cdesc_off,
-                                                      int32_t node_base, int64_t cols_per_block,
+                                                      int32_t count, int64_t n_slabs,
+                                                      int64_t cols_per_block,
                                                       const ST *__restrict__ states, int32_t m,
                                                       int64_t n_cols, int64_t ld,
                                                       int32_t *__restrict__ counts) {
     using Q = Quad<ST>;
     __shared__ int32_t hist[kLdsBins];
-    const int node = node_base + (int)blockIdx.y;
-    const int32_t *__restrict__ d = cdesc + cdesc_off[node];
+    uint32_t node_u;
+    int64_t slab;
+    decode_block(blockIdx.x, (uint32_t)count, node_u, slab);
+    if (slab >= n_slabs) return;  // uniform across the block
+    const int node = (int)node_u;
+    cint32_t *d = as_const(cdesc) + as_const(cdesc_off)[node];
     const int K = d[0], n_par = d[1], nbins = d[2], off = d[3];
+    cint32_t *par = d + 4;
     const int mode = nbins <= kRepBins ? 0 : (nbins <= kLdsBins ? 1 : 2);
     const int lds_words = mode == 0 ? nbins * kCopies : (mode == 1 ? nbins : 0);
     for (int b = threadIdx.x; b < lds_words; b += kBlock) hist[b] = 0;
     __syncthreads();
     const int copy = threadIdx.x & (kCopies - 1);
-    const int64_t c0 = (int64_t)blockIdx.x * cols_per_block;
+    const int64_t c0 = slab * cols_per_block;
     const int64_t c1 = c0 + cols_per_block < n_cols ? c0 + cols_per_block : n_cols;
     const int64_t vstride = (int64_t)m * ld;
-    for (int r = 0; r < m; ++r) {
-        for (int64_t col = c0 + 4 * (int64_t)threadIdx.x; col < c1; col += 4 * kBlock) {
-            const ST *base = states + (int64_t)r * ld + col;
-            int u[4] = {0, 0, 0, 0};
-            const int32_t *p = d + 4;
-            for (int q = 0; q < n_par; ++q, p += 2) {
-                const typename Q::V s = Q::load(base + (int64_t)p[0] * vstride);
+    const bool packed = nbins <= 65536;
+    auto add = [&](int bin) {
+        if (mode == 0) atomicAdd(&hist[bin * kCopies + copy], 1);
+        else if (mode == 1) atomicAdd(&hist[bin], 1);
+        else atomicAdd(&counts[off + bin], 1);
+    };
+    for (int64_t col = c0 + 4 * (int64_t)threadIdx.x; col < c1; col += 4 * kBlock) {
+        const int nvalid = c1 - col < 4 ? (int)(c1 - col) : 4;
+        for (int r0 = 0; r0 < m; r0 += kCountReps) {
+            const int nr = m - r0 < kCountReps ? m - r0 : kCountReps;
+            uint32_t boff[kCountReps];
+            typename Q::V own[kCountReps];
 #pragma unroll
-                for (int c = 0; c < 4; ++c) u[c] += Q::get(s, c) * p[1];
+            for (int t = 0; t < kCountReps; ++t) {
+                const int rr = r0 + (t < nr ? t : 0);
+                boff[t] = (uint32_t)(rr * ld + col) * (uint32_t)sizeof(ST);
+                own[t] = load_row<ST>(states, node, vstride, boff[t]);
             }
-            const typename Q::V xs = Q::load(base + (int64_t)node * vstride);
+            if (packed) {
+                // bin = sum over parents of x_p * (stride_p * K) + x_node
+                uint32_t Pk[kCountReps][2];
 #pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                if (col + c >= c1) break;
-                const int bin = u[c] * K + Q::get(xs, c);
-                if (mode == 0) atomicAdd(&hist[bin * kCopies + copy], 1);
-                else if (mode == 1) atomicAdd(&hist[bin], 1);
-                else atomicAdd(&counts[off + bin], 1);
+                for (int t = 0; t < kCountReps; ++t) Q::split(own[t], Pk[t]);
+                for (int q = 0; q < n_par; ++q) {
+                    const uint32_t mult = (uint32_t)(par[2 * q + 1] * K) * 0x10001u;
+                    typename Q::V sp[kCountReps];
+#pragma unroll
+                    for (int t = 0; t < kCountReps; ++t)
+                        sp[t] = load_row<ST>(states, par[2 * q], vstride, boff[t]);
+#pragma unroll
+                    for (int t = 0; t < kCountReps; ++t) {
+                        uint32_t p2[2];
+                        Q::split(sp[t], p2);
+                        Pk[t][0] = pk_mad_u16(p2[0], mult, Pk[t][0]);
+                        Pk[t][1] = pk_mad_u16(p2[1], mult, Pk[t][1]);
+                    }
+                }
+#pragma unroll
+                for (int t = 0; t < kCountReps; ++t) {
+                    if (t >= nr) break;
+#pragma unroll
+                    for (int c = 0; c < 4; ++c)
+                        if (c < nvalid) add((int)packed_index<ST>(Pk[t], c));
+                }
+            } else {
+                uint32_t u[kCountReps][4];
+#pragma unroll
+                for (int t = 0; t < kCountReps; ++t)
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) u[t][c] = 0;
+                for (int q = 0; q < n_par; ++q) {
+                    const uint32_t stride = (uint32_t)par[2 * q + 1];
+                    typename Q::V sp[kCountReps];
+#pragma unroll
+                    for (int t = 0; t < kCountReps; ++t)
+                        sp[t] = load_row<ST>(states, par[2 * q], vstride, boff[t]);
+#pragma unroll
+                    for (int t = 0; t < kCountReps; ++t)
+#pragma unroll
+                        for (int c = 0; c < 4; ++c) u[t][c] += (uint32_t)Q::get(sp[t], c) * stride;
+                }
+#pragma unroll
+                for (int t = 0; t < kCountReps; ++t) {
+                    if (t >= nr) break;
+#pragma unroll
+                    for (int c = 0; c < 4; ++c)
+                        if (c < nvalid) add((int)(u[t][c] * (uint32_t)K + (uint32_t)Q::get(own[t], c)));
+                }
             }
         }
     }
@@ -1067,26 +1157,29 @@ void sweep_class(const SweepParams &P, int32_t klass, int32_t lds_bytes, dim3 gr
 hipError_t launch_sweep(SweepParams P, int32_t begin, int32_t count, int32_t klass,
                         int32_t lds_bytes, int32_t state_bytes, hipStream_t stream) {
     if (count <= 0 || P.n_cols <= 0) return hipSuccess;
-    // about 8192 blocks per launch: split the columns first, then the replicas
+    // Slabs of kSweepQuadsPerLane quads per lane.  A block that stages its
+    // node's table in LDS (class 0) takes all replicas, so that the copy is
+    // paid once per column chunk, and replicas are split only when that
+    // leaves fewer than kMinSweepBlocks blocks; the other classes take one
+    // replica per block: smaller slabs keep the blanket rows and the global
+    // tables that the resident blocks gather from in L2 (measured faster).
     const int64_t quads = (P.n_cols + 3) / 4;
-    const int64_t want = (8192 + count - 1) / count;
-    const int64_t max_chunks = (quads + dev::kBlock - 1) / dev::kBlock;
-    int64_t chunks = want < max_chunks ? want : max_chunks;
-    if (chunks < 1) chunks = 1;
-    int64_t rsplit = (want + chunks - 1) / chunks;
+    P.quads_per_block = (int64_t)dev::kBlock * dev::kSweepQuadsPerLane;
+    const int64_t chunks = (quads + P.quads_per_block - 1) / P.quads_per_block;
+    int64_t rsplit = klass == 0 ? (dev::kMinSweepBlocks + count * chunks - 1) / (count * chunks) : P.m;
     if (rsplit > P.m) rsplit = P.m;
     if (rsplit < 1) rsplit = 1;
-    P.quads_per_block = (quads + chunks - 1) / chunks;
     P.reps_per_block = (int32_t)((P.m + rsplit - 1) / rsplit);
-    const unsigned gx = (unsigned)((quads + P.quads_per_block - 1) / P.quads_per_block);
-    const unsigned gz = (unsigned)((P.m + P.reps_per_block - 1) / P.reps_per_block);
-    for (int32_t s = 0; s < count; s += 65535) {
-        const int32_t c = count - s < 65535 ? count - s : 65535;
-        P.begin = begin + s;
-        dim3 grid(gx, (unsigned)c, gz);
-        if (state_bytes == 1) sweep_class<int8_t>(P, klass, lds_bytes, grid, stream);
-        else sweep_class<int16_t>(P, klass, lds_bytes, grid, stream);
-    }
+    P.rsplit = (int32_t)((P.m + P.reps_per_block - 1) / P.reps_per_block);
+    P.n_slabs = chunks * P.rsplit;
+    P.count = count;
+    P.begin = begin;
+    const int64_t rounds = (P.n_slabs + dev::kXcds - 1) / dev::kXcds;
+    const int64_t blocks = rounds * dev::kXcds * count;
+    if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+    const dim3 grid((unsigned)blocks);
+    if (state_bytes == 1) sweep_class<int8_t>(P, klass, lds_bytes, grid, stream);
+    else sweep_class<int16_t>(P, klass, lds_bytes, grid, stream);
     return hipGetLastError();
 }
 
@@ -1110,26 +1203,22 @@ hipError_t launch_counts(const DeviceTables &t, const void *states, int32_t stat
                          int32_t n, int32_t m, int64_t n_cols, int64_t ld, int32_t *counts,
                          hipStream_t stream) {
     if (n_cols <= 0) return hipSuccess;
-    // about 8192 blocks in total, each a run of columns of one node (all replicas)
-    const int64_t quads = (n_cols + 3) / 4;
-    int64_t chunks = (8192 + n - 1) / n;
-    const int64_t max_chunks = (quads + dev::kBlock - 1) / dev::kBlock;
-    if (chunks > max_chunks) chunks = max_chunks;
-    if (chunks < 1) chunks = 1;
-    const int64_t cols_per_block = ((quads + chunks - 1) / chunks) * 4;
-    const unsigned gx = (unsigned)((n_cols + cols_per_block - 1) / cols_per_block);
-    for (int32_t s = 0; s < n; s += 65535) {
-        const int32_t c = n - s < 65535 ? n - s : 65535;
-        dim3 grid(gx, (unsigned)c, 1);
-        if (state_bytes == 1)
-            hipLaunchKernelGGL(dev::count_kernel<int8_t>, grid, dim3(dev::kBlock), 0, stream, t.cdesc,
-                               t.cdesc_off, s, cols_per_block, (const int8_t *)states, m, n_cols, ld,
-                               counts);
-        else
-            hipLaunchKernelGGL(dev::count_kernel<int16_t>, grid, dim3(dev::kBlock), 0, stream, t.cdesc,
-                               t.cdesc_off, s, cols_per_block, (const int16_t *)states, m, n_cols, ld,
-                               counts);
-    }
+    // one node x kCountQuadsPerLane quads per lane x all replicas per block,
+    // XCD-swizzled like the sweep
+    const int64_t cols_per_block = 4 * dev::kBlock * dev::kCountQuadsPerLane;
+    const int64_t n_slabs = (n_cols + cols_per_block - 1) / cols_per_block;
+    const int64_t rounds = (n_slabs + dev::kXcds - 1) / dev::kXcds;
+    const int64_t blocks = rounds * dev::kXcds * n;
+    if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+    const dim3 grid((unsigned)blocks);
+    if (state_bytes == 1)
+        hipLaunchKernelGGL(dev::count_kernel<int8_t>, grid, dim3(dev::kBlock), 0, stream, t.cdesc,
+                           t.cdesc_off, n, n_slabs, cols_per_block, (const int8_t *)states, m, n_cols,
+                           ld, counts);
+    else
+        hipLaunchKernelGGL(dev::count_kernel<int16_t>, grid, dim3(dev::kBlock), 0, stream, t.cdesc,
+                           t.cdesc_off, n, n_slabs, cols_per_block, (const int16_t *)states, m, n_cols,
+                           ld, counts);
     return hipGetLastError();
 }
 

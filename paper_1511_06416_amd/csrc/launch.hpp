@@ -43,8 +43,14 @@ struct SweepParams {
     int32_t m;
     int64_t n_cols, ld, col_offset;
     uint32_t key0, key1, sweep_id;
-    int64_t quads_per_block;       // set by the launcher
-    int32_t reps_per_block;        // set by the launcher
+    // block geometry, set by the launcher: a launch covers `count` nodes x
+    // `n_slabs` slabs (a column chunk of quads_per_block quads x a replica
+    // range of reps_per_block); see block_work in kernels.hip
+    int64_t quads_per_block;
+    int32_t reps_per_block;
+    int32_t count;
+    int32_t rsplit;
+    int64_t n_slabs;
     int64_t win_begin, win;        // debug window (win == 0: none)
     float *probs;
     int32_t max_card;
