@@ -418,7 +418,7 @@ struct Work {
 constexpr uint32_t kXcds = 8;
 constexpr int kSweepQuadsPerLane = 1;  // column quads per lane in one sweep block
 constexpr int kMinSweepBlocks = 4096;  // replicas are split below this many blocks
-constexpr int kCountQuadsPerLane = 1;  // column quads per lane in one count block
+constexpr int kCountQuadsPerLane = 2;  // column quads per lane in one count block
 
 __device__ __forceinline__ void decode_block(uint32_t b, uint32_t count, uint32_t &local,
                                              int64_t &slab) {
@@ -935,7 +935,7 @@ constexpr int kRepBins = 256;
 constexpr int kLdsBins = 8192;
 static_assert(kCopies * kRepBins <= kLdsBins, "LDS budget");
 
-constexpr int kCountReps = 4;  // replicas whose rows are loaded together
+constexpr int kCountReps = 10;  // replicas whose rows are loaded together (measured best on m = 10)
 
 // Histogram of (parent row, state) for one node over a slab of columns and all
 // m replicas (block geometry as the sweep's, decode_block).  Bins are counted
@@ -981,9 +981,8 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
             typename Q::V own[kCountReps];
 #pragma unroll
             for (int t = 0; t < kCountReps; ++t) {
-                const int rr = r0 + (t < nr ? t : 0);
-                boff[t] = (uint32_t)(rr * ld + col) * (uint32_t)sizeof(ST);
-                own[t] = load_row<ST>(states, node, vstride, boff[t]);
+                boff[t] = (uint32_t)((r0 + t) * ld + col) * (uint32_t)sizeof(ST);
+                if (t < nr) own[t] = load_row<ST>(states, node, vstride, boff[t]);
             }
             if (packed) {
                 // bin = sum over parents of x_p * (stride_p * K) + x_node
@@ -995,9 +994,10 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
                     typename Q::V sp[kCountReps];
 #pragma unroll
                     for (int t = 0; t < kCountReps; ++t)
-                        sp[t] = load_row<ST>(states, par[2 * q], vstride, boff[t]);
+                        if (t < nr) sp[t] = load_row<ST>(states, par[2 * q], vstride, boff[t]);
 #pragma unroll
                     for (int t = 0; t < kCountReps; ++t) {
+                        if (t >= nr) break;
                         uint32_t p2[2];
                         Q::split(sp[t], p2);
                         Pk[t][0] = pk_mad_u16(p2[0], mult, Pk[t][0]);
@@ -1022,11 +1022,13 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
                     typename Q::V sp[kCountReps];
 #pragma unroll
                     for (int t = 0; t < kCountReps; ++t)
-                        sp[t] = load_row<ST>(states, par[2 * q], vstride, boff[t]);
+                        if (t < nr) sp[t] = load_row<ST>(states, par[2 * q], vstride, boff[t]);
 #pragma unroll
-                    for (int t = 0; t < kCountReps; ++t)
+                    for (int t = 0; t < kCountReps; ++t) {
+                        if (t >= nr) break;
 #pragma unroll
                         for (int c = 0; c < 4; ++c) u[t][c] += (uint32_t)Q::get(sp[t], c) * stride;
+                    }
                 }
 #pragma unroll
                 for (int t = 0; t < kCountReps; ++t) {
