@@ -51,6 +51,8 @@ def parse():
                         "kernels run on the GPU, for counter collection)")
     p.add_argument("--table-limit", type=int, default=None,
                    help="threshold-table size limit passed to same_create_ex (0: products only)")
+    p.add_argument("--no-ingest", action="store_true",
+                   help="skip the timing of the sparse-input expansion and the latent initialisation")
     p.add_argument("--no-stream", action="store_true",
                    help="skip the out-of-core (pinned host memory) timing")
     p.add_argument("--stream-steps", type=int, default=2)
@@ -163,6 +165,8 @@ def main():
         torch.cuda.synchronize()
         del a, b2
 
+    ingest = None if args.no_ingest else ingest_timing(w, ctx, mbs[0], dev, stream)
+
     streamed = None
     if not args.no_stream and len(mbs) == w.M:
         streamed = stream_timing(w, ctx, cpts, ws, dev, args.stream_steps)
@@ -205,6 +209,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "streamed_from_host": streamed,
+        "ingest": ingest,
         "table_nodes": ctx.table_nodes,
     }
     print(json.dumps(out), flush=True)
@@ -384,6 +389,61 @@ def counters_summary(paths, cfg):
     with open(path, "w") as fh:
         json.dump(out, fh, indent=1)
     print(json.dumps(out))
+
+
+def ingest_timing(w, ctx, b, dev, stream, reps=5):
+    """Data ingest of minibatch b (Sec. 4 sparse input; Sec. 5.2 random start):
+    same_expand_observed from the minibatch's known entries in CSR form (rows =
+    nodes), then same_init_latent, each timed with HIP events on the launch
+    stream (into scratch copies; the benchmark's states are not touched).  The
+    CSR arrays are built with torch from the dense minibatch (input
+    preparation).  Algorithmic bytes: expand reads row_ptr, the column indices
+    and the values and writes the obs array and m copies of every known value;
+    the initialisation reads the obs array and writes every latent state."""
+    import numpy as np
+    import torch
+
+    import paper_1511_06416_amd as same
+    n, m, ld, nc = w.net.n, w.m, w.ld, w.mb_cols(b)
+    sb = w.states[b].element_size()
+    ob = w.obs[b]
+    known = ob[:, :nc].bool()
+    rows, cols = torch.nonzero(known, as_tuple=True)
+    nnz = int(rows.numel())
+    row_ptr = torch.zeros(n + 1, dtype=torch.int64, device=dev)
+    row_ptr[1:] = torch.cumsum(torch.bincount(rows, minlength=n), 0)
+    col_idx = cols.to(torch.int32)
+    values = w.states[b][:, 0, :nc][known].contiguous()
+    del rows, cols, known
+    st = torch.empty_like(w.states[b])
+    obs = torch.empty_like(ob)
+    torch.cuda.synchronize()
+
+    def timed(fn):
+        fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    t_exp = timed(lambda: same.same_expand_observed(ctx, row_ptr, col_idx, values, nnz, m, nc, ld, st, obs))
+    t_init = timed(lambda: same.same_init_latent(ctx, st, obs, m, nc, ld, b * w.nb, w.seed + 1))
+    latent = n * nc - nnz
+    b_exp = 8 * (n + 1) + (4 + sb) * nnz + n * ld + m * sb * nnz
+    b_init = n * ld + m * sb * latent
+    del st, obs, row_ptr, col_idx, values
+    return {
+        "minibatch_cols": nc, "nnz": nnz, "density": round(nnz / float(n * nc), 4),
+        "expand": {"ms": round(t_exp, 4), "algorithmic_bytes": b_exp,
+                   "gbs": round(b_exp / t_exp / 1e6, 1), "frac": round(b_exp / t_exp / 1e6 / HBM_PEAK_GBS, 4)},
+        "init_latent": {"ms": round(t_init, 4), "algorithmic_bytes": b_init,
+                        "gbs": round(b_init / t_init / 1e6, 1),
+                        "frac": round(b_init / t_init / 1e6 / HBM_PEAK_GBS, 4)},
+        "upload_bytes": {"sparse_csr": 8 * (n + 1) + (4 + sb) * nnz, "dense": n * ld * (1 + m * sb)},
+    }
 
 
 def stream_timing(w, ctx, cpts, ws, dev, steps):

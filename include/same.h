@@ -45,7 +45,8 @@
  * Random numbers: Philox4x32-10 (Salmon et al., SC'11) keyed by the 64-bit
  *         seed; the Gibbs draw of node i, replica r, global column g in sweep
  *         s takes word g&3 of the block at counter {g>>2, i, r, s}; the Gamma
- *         attempt t of CPT entry e at update q uses counter {e, t, 1<<24, q}.
+ *         attempt t of CPT entry e at update q uses counter {e, t, 1<<24, q};
+ *         the initial latent state uses {g>>2, i, r | 2<<24, 0}.
  */
 #ifndef SAME_H
 #define SAME_H
@@ -248,6 +249,37 @@ int same_stream_pass(same_ctx *ctx, void *host_states, const uint8_t *host_obs, 
                      int64_t n_cols, int64_t nb, int32_t m, float *cpts, int32_t *mb_counts,
                      int32_t *totals, uint64_t seed, uint32_t pass_id, int32_t flags, void *slots,
                      void *workspace, void *stream);
+
+/*
+ * Dense minibatch from its known entries (Sec. 4: the sampler takes a
+ * typically sparse data matrix with rows = variables and columns = cases, and
+ * forms m copies of the known data per minibatch).  The known entries are in
+ * CSR form by node: row i holds entries [row_ptr[i], row_ptr[i+1]) of col_idx
+ * (minibatch column, ascending within the row) and values (int8 or int16 like
+ * the states); nnz = row_ptr[n].  obs [n][ld] is cleared, then for every
+ * entry with col_idx in [0, n_cols): obs[i][j] = 1 and states[i][r][j] = value
+ * for every replica r < m.  Entries with a column outside [0, n_cols) are
+ * skipped; of repeated columns in a row the last entry is kept.  Latent
+ * entries of states are left as they are (see same_init_latent).  All
+ * pointers are device pointers owned by the caller; values must lie in
+ * [0, K_i).  Errors: SAME_EINVAL for null pointers or bad sizes, SAME_EALIGN
+ * for misaligned states/obs or ld, SAME_EHIP for launch failures.
+ */
+int same_expand_observed(same_ctx *ctx, const int64_t *row_ptr, const int32_t *col_idx,
+                         const void *values, int64_t nnz, int32_t m, int64_t n_cols, int64_t ld,
+                         void *states, uint8_t *obs, void *stream);
+
+/*
+ * Random initial states of the latent entries (Sec. 5.2: the sampler starts
+ * from a random initialisation): for every node i, replica r < m and column
+ * j < n_cols with obs[i][j] == 0, states[i][r][j] = floor(U * K_i) with U the
+ * 24-bit uniform (w >> 8) * 2^-24 of word g & 3 of the Philox block at counter
+ * {g >> 2, i, r | 2 << 24, 0}, g = col_offset + j (computed exactly as
+ * ((w >> 8) * K_i) >> 24).  Observed entries are left as they are.  Device
+ * pointers; col_offset a multiple of 4.  Errors as same_sweep's.
+ */
+int same_init_latent(same_ctx *ctx, void *states, const uint8_t *obs, int32_t m, int64_t n_cols,
+                     int64_t ld, int64_t col_offset, uint64_t seed, void *stream);
 
 /*
  * Measurement of the sweep kernels.  same_kernel_timing(ctx, 1) clears the

@@ -82,6 +82,12 @@ def lib():
                 C.c_int32, P, P, P, P, C.c_double, C.c_uint64, C.c_uint32, P, P,
             ]
             L.oracle_dirichlet.restype = C.c_int
+            L.oracle_expand.argtypes = [C.c_int32, C.c_int64, C.c_int32, C.c_int64, P, P, P, C.c_int32,
+                                        P, P]
+            L.oracle_expand.restype = C.c_int
+            L.oracle_init_latent.argtypes = [C.c_int32, P, C.c_int64, C.c_int32, C.c_int64, C.c_int64,
+                                             C.c_uint64, C.c_int32, P, P]
+            L.oracle_init_latent.restype = C.c_int
             _lib = L
         return _lib
 
@@ -246,3 +252,29 @@ def moving_sum(totals, mb_prev, new):
     """Exact moving sum of the per-minibatch counts (Sec. 4): subtract this
     minibatch's previous counts from the total, add its new counts."""
     return totals - mb_prev + new
+
+
+def expand(n, n_cols, m, ld, row_ptr, col_idx, values, states, obs):
+    """Dense minibatch from its known entries in CSR form (rows = variables,
+    Sec. 4): obs is cleared, then every stored entry is marked observed and
+    written into all m replicas of states (in place); latent entries of states
+    are left as they are."""
+    row_ptr = np.ascontiguousarray(row_ptr, dtype=np.int64)
+    col_idx = np.ascontiguousarray(col_idx, dtype=np.int32)
+    values = np.ascontiguousarray(values, dtype=states.dtype)
+    assert states.shape == (n, m, ld) and states.flags.c_contiguous
+    assert obs.shape == (n, ld) and obs.dtype == np.uint8 and obs.flags.c_contiguous
+    _check(lib().oracle_expand(int(n), int(n_cols), int(m), int(ld), _ptr(row_ptr), _ptr(col_idx),
+                               _ptr(values), states.dtype.itemsize, _ptr(states), _ptr(obs)))
+
+
+def init_latent(card, n_cols, m, col_offset, seed, states, obs):
+    """Random initial latent states (Sec. 5.2), in place: every latent entry
+    of every replica becomes floor(U * K_i) from its Philox uniform (tag 2)."""
+    card = np.ascontiguousarray(card, dtype=np.int32)
+    n = len(card)
+    ld = states.shape[-1]
+    assert states.shape == (n, m, ld) and states.flags.c_contiguous and obs.shape == (n, ld)
+    _check(lib().oracle_init_latent(n, _ptr(card), int(n_cols), int(m), int(ld), int(col_offset),
+                                    int(seed), states.dtype.itemsize, _ptr(states),
+                                    _ptr(np.ascontiguousarray(obs, dtype=np.uint8))))

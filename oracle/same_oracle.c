@@ -610,3 +610,68 @@ int oracle_dirichlet(int32_t n, const int32_t *pptr, const int32_t *pidx, const 
     graph_free(&g);
     return OR_OK;
 }
+
+/* ------------------------------------------------------------------ */
+/* Data ingest: the (typically sparse) node x case matrix of known     */
+/* entries (Sec. 4) and the random initial latent states (Sec. 5.2).   */
+/* ------------------------------------------------------------------ */
+
+#define TAG_INIT 2u
+
+static void put_state(void *states, int32_t state_bytes, int64_t idx, int32_t v) {
+    if (state_bytes == 1) ((int8_t *)states)[idx] = (int8_t)v;
+    else ((int16_t *)states)[idx] = (int16_t)v;
+}
+
+/*
+ * Dense minibatch from its known entries (Sec. 4: the sampler takes a
+ * typically sparse matrix with rows = variables and columns = cases, and forms
+ * m copies of the known data).  Row i of the sparse matrix holds entries
+ * [row_ptr[i], row_ptr[i+1]) with column indices col_idx (relative to the
+ * minibatch) and values (state_bytes: 1 = int8, 2 = int16).  obs[n][ld] is set
+ * to 0, then for every entry with a column in [0, n_cols): obs[i][j] = 1 and
+ * states[i][r][j] = value for r < m.  A row listing a column twice keeps the
+ * later entry.  Latent entries of states are not touched.
+ */
+int oracle_expand(int32_t n, int64_t n_cols, int32_t m, int64_t ld, const int64_t *row_ptr,
+                  const int32_t *col_idx, const void *values, int32_t state_bytes, void *states,
+                  uint8_t *obs) {
+    if (n <= 0 || m < 1 || n_cols < 0 || ld < n_cols || (state_bytes != 1 && state_bytes != 2))
+        return OR_EINVAL;
+    memset(obs, 0, (size_t)n * (size_t)ld);
+    for (int32_t i = 0; i < n; ++i) {
+        for (int64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) {
+            int64_t j = col_idx[e];
+            if (j < 0 || j >= n_cols) continue;
+            int32_t v = state_bytes == 1 ? ((const int8_t *)values)[e] : ((const int16_t *)values)[e];
+            obs[(int64_t)i * ld + j] = 1;
+            for (int32_t r = 0; r < m; ++r) put_state(states, state_bytes, ((int64_t)i * m + r) * ld + j, v);
+        }
+    }
+    return OR_OK;
+}
+
+/*
+ * Random initial latent states (Sec. 5.2: the sampler starts from a random
+ * initialisation).  For node i, replica r and column j < n_cols with
+ * obs[i][j] == 0: states[i][r][j] = floor(U * K_i), U = (w >> 8) * 2^-24 with
+ * w word (g & 3) of Philox(ctr = {g >> 2, i, r | (2 << 24), 0}),
+ * g = col_offset + j.  floor(U * K_i) is formed exactly as ((w >> 8) * K_i) >> 24.
+ */
+int oracle_init_latent(int32_t n, const int32_t *card, int64_t n_cols, int32_t m, int64_t ld,
+                       int64_t col_offset, uint64_t seed, int32_t state_bytes, void *states,
+                       const uint8_t *obs) {
+    if (n <= 0 || m < 1 || n_cols < 0 || ld < n_cols || (state_bytes != 1 && state_bytes != 2))
+        return OR_EINVAL;
+    for (int32_t i = 0; i < n; ++i)
+        for (int32_t r = 0; r < m; ++r)
+            for (int64_t j = 0; j < n_cols; ++j) {
+                if (obs[(int64_t)i * ld + j]) continue;
+                int64_t g = col_offset + j;
+                uint32_t w = philox_word(seed, (uint32_t)(g >> 2), (uint32_t)i,
+                                         (uint32_t)r | (TAG_INIT << 24), 0u, (int)(g & 3));
+                int32_t v = (int32_t)(((uint64_t)(w >> 8) * (uint64_t)card[i]) >> 24);
+                put_state(states, state_bytes, ((int64_t)i * m + r) * ld + j, v);
+            }
+    return OR_OK;
+}

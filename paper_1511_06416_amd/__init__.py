@@ -19,7 +19,7 @@ __all__ = [
     "SameError", "Context", "same_create", "same_create_ex", "same_destroy", "same_layout", "same_workspace_size",
     "same_sweep", "same_sweep_debug", "same_counts", "same_sample_cpts", "same_last_error",
     "same_step", "same_sweep_plan", "same_stream_slots_size", "same_stream_pass", "SAME_STREAM_COUNTS_ONLY",
-    "same_kernel_timing", "same_kernel_times",
+    "same_kernel_timing", "same_kernel_times", "same_expand_observed", "same_init_latent",
     "library_path", "load_library",
 ]
 
@@ -86,12 +86,14 @@ def load_library():
         L.same_stream_pass.argtypes = [P, P, P, I64, I64, I64, I32, P, P, P, U64, U32, I32, P, P, P]
         L.same_kernel_timing.argtypes = [P, I32]
         L.same_kernel_times.argtypes = [P, C.POINTER(_KernelTimes)]
+        L.same_expand_observed.argtypes = [P, P, P, P, I64, I32, I64, I64, P, P, P]
+        L.same_init_latent.argtypes = [P, P, P, I32, I64, I64, I64, U64, P]
         L.same_last_error.argtypes = []
         L.same_last_error.restype = C.c_char_p
         for f in ("same_create", "same_create_ex", "same_layout", "same_workspace_size", "same_sweep",
                   "same_sweep_debug", "same_counts", "same_sample_cpts", "same_step", "same_sweep_plan",
                   "same_stream_slots_size", "same_stream_pass", "same_kernel_timing",
-                  "same_kernel_times"):
+                  "same_kernel_times", "same_expand_observed", "same_init_latent"):
             getattr(L, f).restype = C.c_int
         _lib = L
         return L
@@ -270,3 +272,14 @@ def same_kernel_times(ctx):
     t = _KernelTimes()
     _check(load_library().same_kernel_times(ctx.handle, C.byref(t)))
     return {"ms": list(t.ms), "launches": list(t.launches)}
+
+
+def same_expand_observed(ctx, row_ptr, col_idx, values, nnz, m, n_cols, ld, states, obs, stream=None):
+    _check(load_library().same_expand_observed(ctx.handle, _ptr(row_ptr), _ptr(col_idx), _ptr(values),
+                                               int(nnz), int(m), int(n_cols), int(ld), _ptr(states),
+                                               _ptr(obs), _stream(stream)))
+
+
+def same_init_latent(ctx, states, obs, m, n_cols, ld, col_offset, seed, stream=None):
+    _check(load_library().same_init_latent(ctx.handle, _ptr(states), _ptr(obs), int(m), int(n_cols),
+                                           int(ld), int(col_offset), int(seed), _stream(stream)))

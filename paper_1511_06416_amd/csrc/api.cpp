@@ -663,6 +663,39 @@ int same_stream_pass(same_ctx *ctx, void *host_states, const uint8_t *host_obs, 
 
 }  // extern "C"
 
+extern "C" int same_expand_observed(same_ctx *ctx, const int64_t *row_ptr, const int32_t *col_idx,
+                                    const void *values, int64_t nnz, int32_t m, int64_t n_cols, int64_t ld,
+                                    void *states, uint8_t *obs, void *stream) {
+    int rc = check_minibatch(ctx, states, m, n_cols, ld);
+    if (rc) return rc;
+    if (!row_ptr || !obs) return set_error(SAME_EINVAL, "row_ptr and obs must be non-null");
+    if (nnz < 0) return set_error(SAME_EINVAL, "nnz must be >= 0");
+    if (nnz > 0 && (!col_idx || !values)) return set_error(SAME_EINVAL, "col_idx and values must be non-null");
+    if (!aligned(obs, 4)) return set_error(SAME_EALIGN, "obs must be 4-byte aligned");
+    return check_hip(same::launch_expand(row_ptr, ctx->g.n, col_idx, values, nnz, m, n_cols, ld,
+                                         ctx->g.state_bytes, states, obs, (hipStream_t)stream),
+                     "expand launch");
+}
+
+extern "C" int same_init_latent(same_ctx *ctx, void *states, const uint8_t *obs, int32_t m, int64_t n_cols,
+                                int64_t ld, int64_t col_offset, uint64_t seed, void *stream) {
+    int rc = check_minibatch(ctx, states, m, n_cols, ld);
+    if (rc) return rc;
+    if (!obs) return set_error(SAME_EINVAL, "obs is null");
+    if (!aligned(obs, 4)) return set_error(SAME_EALIGN, "obs must be 4-byte aligned");
+    if (col_offset < 0 || col_offset % 4 != 0)
+        return set_error(SAME_EALIGN, "col_offset must be a non-negative multiple of 4");
+    if (((col_offset + n_cols) >> 2) > (int64_t)0xFFFFFFFFll)
+        return set_error(SAME_ESIZE, "global column index exceeds the Philox counter range");
+    same::DeviceTables *t = nullptr;
+    rc = tables_for_current_device(ctx, &t);
+    if (rc) return rc;
+    return check_hip(same::launch_init_latent(*t, ctx->g.n, m, n_cols, ld, col_offset, (uint32_t)seed,
+                                              (uint32_t)(seed >> 32), ctx->g.state_bytes, states, obs,
+                                              (hipStream_t)stream),
+                     "latent init launch");
+}
+
 extern "C" int same_kernel_timing(same_ctx *ctx, int32_t enable) {
     if (!ctx) return set_error(SAME_EINVAL, "null context");
     std::lock_guard<std::mutex> lock(ctx->mu);

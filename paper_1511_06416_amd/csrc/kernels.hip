@@ -1116,6 +1116,87 @@ __global__ void normalize_kernel(const int32_t *__restrict__ row_off, const int3
     for (int k = 0; k < K; ++k) cpts[o + k] = (float)(s > 0.0 ? g[o + k] / s : 1.0 / K);
 }
 
+// ---------------------------------------------------------------- ingest
+
+// Known entries of one minibatch, CSR with rows = nodes (Sec. 4: a typically
+// sparse variables x cases matrix), into the dense layout: one thread per
+// stored entry.  Two lanes find the rows of the block's first and last
+// entries (the largest i with row_ptr[i] <= e), and each thread searches only
+// between them (usually one or two rows).  The entry's value goes to every
+// replica (Sec. 4: m copies of the known data) and its obs byte is set; obs was
+// cleared by the launcher.  Of repeated (ascending) columns in a row only the
+// last entry writes.
+__device__ __forceinline__ int row_of(const int64_t *__restrict__ row_ptr, int lo, int hi, int64_t e) {
+    while (hi - lo > 1) {  // row_ptr[lo] <= e < row_ptr[hi]
+        const int mid = (lo + hi) >> 1;
+        if (row_ptr[mid] <= e) lo = mid;
+        else hi = mid;
+    }
+    return lo;
+}
+
+template <typename ST>
+__global__ __launch_bounds__(kBlock) void expand_kernel(const int64_t *__restrict__ row_ptr, int32_t n,
+                                                        const int32_t *__restrict__ col_idx,
+                                                        const ST *__restrict__ values, int64_t nnz,
+                                                        int32_t m, int64_t n_cols, int64_t ld,
+                                                        ST *__restrict__ states, uint8_t *__restrict__ obs) {
+    __shared__ int32_t span[2];
+    const int64_t e0 = (int64_t)blockIdx.x * kBlock;
+    const int64_t e_last = e0 + kBlock <= nnz ? e0 + kBlock - 1 : nnz - 1;
+    if (threadIdx.x < 2) span[threadIdx.x] = row_of(row_ptr, 0, n, threadIdx.x == 0 ? e0 : e_last);
+    __syncthreads();
+    const int64_t e = e0 + threadIdx.x;
+    if (e >= nnz) return;
+    const int lo = row_of(row_ptr, span[0], span[1] + 1, e);
+    const int64_t j = col_idx[e];
+    if (j < 0 || j >= n_cols) return;
+    if (e + 1 < row_ptr[lo + 1] && col_idx[e + 1] == j) return;  // a later entry of this column
+    obs[(int64_t)lo * ld + j] = 1;
+    const ST v = values[e];
+    ST *dst = states + (int64_t)lo * m * ld + j;
+    for (int r = 0; r < m; ++r) dst[(int64_t)r * ld] = v;
+}
+
+// Random initial latent states (Sec. 5.2): one thread per (node, column
+// quad), looping over the replicas; the quad's Philox block at counter
+// {g >> 2, i, r | 2 << 24, 0} gives word c to column c, and the state is
+// ((w >> 8) * K_i) >> 24 = floor(U * K_i) exactly.  The quad's obs dword is
+// read once; each replica's state quad is read, its latent columns replaced,
+// and written back.  Observed entries keep their values.
+template <typename ST>
+__global__ __launch_bounds__(kBlock) void init_latent_kernel(const int32_t *__restrict__ cdesc,
+                                                             const int32_t *__restrict__ cdesc_off,
+                                                             int32_t n, int32_t m, int64_t n_cols,
+                                                             int64_t ld, int64_t col_offset, uint32_t k0,
+                                                             uint32_t k1, ST *__restrict__ states,
+                                                             const uint8_t *__restrict__ obs) {
+    using Q = Quad<ST>;
+    const int64_t quads = (n_cols + 3) >> 2;
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= (int64_t)n * quads) return;
+    const int64_t q = t % quads;
+    const int i = (int)(t / quads);
+    const int64_t col = 4 * q;
+    const uint32_t ob = *reinterpret_cast<const uint32_t *>(obs + (int64_t)i * ld + col);
+    int lat = 0;
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+        if (((ob >> (8 * c)) & 0xffu) == 0 && col + c < n_cols) lat |= 1 << c;
+    if (!lat) return;
+    const uint32_t K = (uint32_t)cdesc[cdesc_off[i]];
+    for (int r = 0; r < m; ++r) {
+        const Philox4 b = philox4x32_10((uint32_t)((col_offset >> 2) + q), (uint32_t)i,
+                                        (uint32_t)r | (2u << 24), 0u, k0, k1);
+        ST *p = states + ((int64_t)i * m + r) * ld + col;
+        typename Q::V v = Q::load(p);
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+            if ((lat >> c) & 1) v = Q::put(v, c, (int)(((uint64_t)(b.w[c] >> 8) * K) >> 24));
+        Q::store(p, v);
+    }
+}
+
 }  // namespace dev
 
 // ================================================================= launchers
@@ -1221,6 +1302,42 @@ hipError_t launch_counts(const DeviceTables &t, const void *states, int32_t stat
         hipLaunchKernelGGL(dev::count_kernel<int16_t>, grid, dim3(dev::kBlock), 0, stream, t.cdesc,
                            t.cdesc_off, n, n_slabs, cols_per_block, (const int16_t *)states, m, n_cols,
                            ld, counts);
+    return hipGetLastError();
+}
+
+hipError_t launch_expand(const int64_t *row_ptr, int32_t n, const int32_t *col_idx, const void *values,
+                         int64_t nnz, int32_t m, int64_t n_cols, int64_t ld, int32_t state_bytes,
+                         void *states, uint8_t *obs, hipStream_t stream) {
+    // obs [n][ld] bytes (ld a multiple of 4) cleared as words, then the entries
+    hipError_t e = launch_fill_zero(reinterpret_cast<int32_t *>(obs), (int64_t)n * ld / 4, stream);
+    if (e != hipSuccess || nnz <= 0) return e;
+    const int64_t blocks = (nnz + dev::kBlock - 1) / dev::kBlock;
+    if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+    if (state_bytes == 1)
+        hipLaunchKernelGGL(dev::expand_kernel<int8_t>, dim3((unsigned)blocks), dim3(dev::kBlock), 0, stream,
+                           row_ptr, n, col_idx, (const int8_t *)values, nnz, m, n_cols, ld, (int8_t *)states,
+                           obs);
+    else
+        hipLaunchKernelGGL(dev::expand_kernel<int16_t>, dim3((unsigned)blocks), dim3(dev::kBlock), 0, stream,
+                           row_ptr, n, col_idx, (const int16_t *)values, nnz, m, n_cols, ld,
+                           (int16_t *)states, obs);
+    return hipGetLastError();
+}
+
+hipError_t launch_init_latent(const DeviceTables &t, int32_t n, int32_t m, int64_t n_cols, int64_t ld,
+                              int64_t col_offset, uint32_t key0, uint32_t key1, int32_t state_bytes,
+                              void *states, const uint8_t *obs, hipStream_t stream) {
+    const int64_t items = (int64_t)n * ((n_cols + 3) / 4);
+    if (items <= 0) return hipSuccess;
+    const int64_t blocks = (items + dev::kBlock - 1) / dev::kBlock;
+    if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+    if (state_bytes == 1)
+        hipLaunchKernelGGL(dev::init_latent_kernel<int8_t>, dim3((unsigned)blocks), dim3(dev::kBlock), 0, stream,
+                           t.cdesc, t.cdesc_off, n, m, n_cols, ld, col_offset, key0, key1, (int8_t *)states, obs);
+    else
+        hipLaunchKernelGGL(dev::init_latent_kernel<int16_t>, dim3((unsigned)blocks), dim3(dev::kBlock), 0,
+                           stream, t.cdesc, t.cdesc_off, n, m, n_cols, ld, col_offset, key0, key1,
+                           (int16_t *)states, obs);
     return hipGetLastError();
 }
 

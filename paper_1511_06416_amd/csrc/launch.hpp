@@ -74,6 +74,17 @@ hipError_t launch_counts(const DeviceTables &t, const void *states, int32_t stat
                          int32_t n, int32_t m, int64_t n_cols, int64_t ld, int32_t *counts,
                          hipStream_t stream);
 
+// Dense minibatch from CSR known entries (rows = nodes): clears obs, then
+// one thread per entry writes obs and every replica's state.
+hipError_t launch_expand(const int64_t *row_ptr, int32_t n, const int32_t *col_idx, const void *values,
+                         int64_t nnz, int32_t m, int64_t n_cols, int64_t ld, int32_t state_bytes,
+                         void *states, uint8_t *obs, hipStream_t stream);
+
+// Random initial states of the latent entries (Philox tag 2).
+hipError_t launch_init_latent(const DeviceTables &t, int32_t n, int32_t m, int64_t n_cols, int64_t ld,
+                              int64_t col_offset, uint32_t key0, uint32_t key1, int32_t state_bytes,
+                              void *states, const uint8_t *obs, hipStream_t stream);
+
 hipError_t launch_moving_sum(const int32_t *newc, int32_t *mb, int32_t *totals, int64_t total,
                              hipStream_t stream);
 

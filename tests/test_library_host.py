@@ -227,3 +227,29 @@ def test_kernel_timing_host_calls():
     L = same.load_library()
     assert L.same_kernel_timing(None, 1) == same.SAME_EINVAL
     assert L.same_kernel_times(ctx.handle, None) == same.SAME_EINVAL
+
+
+def test_ingest_argument_errors():
+    # argument checks return before any device work (no GPU needed)
+    L = same.load_library()
+    ctx = _ctx(koller())
+    h = ctx.handle
+    P = C.c_void_p
+    fake = P(1 << 20)  # never dereferenced: every call below fails its checks first
+    rp = P(1 << 21)
+    # null states / obs / row_ptr
+    assert L.same_expand_observed(h, rp, fake, fake, 4, 2, 8, 8, None, fake, None) == same.SAME_EINVAL
+    assert L.same_expand_observed(h, None, fake, fake, 4, 2, 8, 8, fake, fake, None) == same.SAME_EINVAL
+    assert L.same_expand_observed(h, rp, None, fake, 4, 2, 8, 8, fake, fake, None) == same.SAME_EINVAL
+    assert L.same_expand_observed(h, rp, fake, fake, -1, 2, 8, 8, fake, fake, None) == same.SAME_EINVAL
+    # m, n_cols > ld, ld not a multiple of 4, misaligned obs
+    assert L.same_expand_observed(h, rp, fake, fake, 4, 0, 8, 8, fake, fake, None) == same.SAME_EINVAL
+    assert L.same_expand_observed(h, rp, fake, fake, 4, 2, 9, 8, fake, fake, None) == same.SAME_EINVAL
+    assert L.same_expand_observed(h, rp, fake, fake, 4, 2, 6, 6, fake, fake, None) == same.SAME_EALIGN
+    assert L.same_expand_observed(h, rp, fake, fake, 4, 2, 8, 8, fake, P((1 << 20) + 1), None) == \
+        same.SAME_EALIGN
+    assert L.same_init_latent(h, None, fake, 2, 8, 8, 0, 1, None) == same.SAME_EINVAL
+    assert L.same_init_latent(h, fake, None, 2, 8, 8, 0, 1, None) == same.SAME_EINVAL
+    assert L.same_init_latent(h, fake, fake, 2, 8, 8, 2, 1, None) == same.SAME_EALIGN
+    assert L.same_init_latent(None, fake, fake, 2, 8, 8, 0, 1, None) == same.SAME_EINVAL
+    ctx.close()
