@@ -51,6 +51,8 @@ def parse():
                         "kernels run on the GPU, for counter collection)")
     p.add_argument("--table-limit", type=int, default=None,
                    help="threshold-table size limit passed to same_create_ex (0: products only)")
+    p.add_argument("--no-heldout", action="store_true",
+                   help="skip the held-out prediction run (two-layer network) and the hit-count timing")
     p.add_argument("--no-ingest", action="store_true",
                    help="skip the timing of the sparse-input expansion and the latent initialisation")
     p.add_argument("--no-stream", action="store_true",
@@ -166,6 +168,7 @@ def main():
         del a, b2
 
     ingest = None if args.no_ingest else ingest_timing(w, ctx, mbs[0], dev, stream)
+    heldout = None if args.no_heldout else heldout_timing(w, ctx, mbs[0], dev, stream)
 
     streamed = None
     if not args.no_stream and len(mbs) == w.M:
@@ -210,6 +213,7 @@ def main():
         "cpu_baseline": cpu,
         "streamed_from_host": streamed,
         "ingest": ingest,
+        "heldout": heldout,
         "table_nodes": ctx.table_nodes,
     }
     print(json.dumps(out), flush=True)
@@ -443,6 +447,80 @@ def ingest_timing(w, ctx, b, dev, stream, reps=5):
                         "gbs": round(b_init / t_init / 1e6, 1),
                         "frac": round(b_init / t_init / 1e6 / HBM_PEAK_GBS, 4)},
         "upload_bytes": {"sparse_csr": 8 * (n + 1) + (4 + sb) * nnz, "dense": n * ld * (1 + m * sb)},
+    }
+
+
+def heldout_timing(w, ctx, b, dev, stream, train_steps=60, pred_sweeps=20):
+    """Held-out prediction (Sec. 6).  (1) On the two-layer network
+    (concepts30-items300-4k, the shape of the paper's MOOC network): 20% of
+    the known entries are held out, the sampler trains on the rest for
+    train_steps SAME steps, then same_predict samples pred_sweeps sweeps with
+    the CPTs frozen; the AUC of the estimated probabilities of the held-out
+    states is reported with the prediction pass's time.  (2) On minibatch b
+    of the benchmark workload, same_accumulate_hits against a 20% held-out
+    target, timed with HIP events; algorithmic bytes: the states once, the
+    targets once, the hit counters read and written."""
+    import numpy as np
+    import torch
+
+    import paper_1511_06416_amd as same
+    from paper_1511_06416_amd import evaluate
+    from workloads import holdout, make_workload
+
+    h = make_workload(4, device=dev)
+    net = h.net
+    obs_train, target = holdout(h, 0, 0.2)
+    pptr, pidx, card = net.csr()
+    hctx = same.same_create(pptr, pidx, card, h.alpha)
+    hws = hctx.new_workspace(dev)
+    st = h.states[0]
+    ob = torch.from_numpy(obs_train).to(dev)
+    tg = torch.from_numpy(target).to(dev)
+    same.same_init_latent(hctx, st, ob, h.m, h.n_cols, h.ld, 0, h.seed + 17)
+    cpts = torch.from_numpy(h.init_theta).to(dev)
+    mbc = torch.zeros(hctx.cpt_total, dtype=torch.int32, device=dev)
+    tot = torch.zeros(hctx.cpt_total, dtype=torch.int32, device=dev)
+    same.same_counts(hctx, st, h.m, h.n_cols, h.ld, mbc, tot, hws)
+    for s in range(train_steps):
+        same.same_step(hctx, st, ob, cpts, h.m, h.n_cols, h.ld, 0, h.seed, s, mbc, tot, s, hws)
+    hits = torch.zeros(target.shape, dtype=torch.int32, device=dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    same.same_predict(hctx, st, ob, cpts, tg, h.m, h.n_cols, h.ld, 0, h.seed, 1 << 20, pred_sweeps, hits, hws)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    t_pred = e0.elapsed_time(e1)
+    sc, lab = evaluate.binary_scores(hits.cpu().numpy(), target, pred_sweeps * h.m)
+    a = evaluate.auc(sc, lab)
+    hctx.close()
+    del st, ob, tg, hits, h
+
+    # hit-count kernel on the benchmark minibatch
+    n, m, ld, nc = w.net.n, w.m, w.ld, w.mb_cols(b)
+    sb = w.states[b].element_size()
+    g = torch.Generator(device=dev)
+    g.manual_seed(6)
+    pick = (torch.rand(w.obs[b].shape, generator=g, device=dev) < 0.2) & (w.obs[b] == 1)
+    tgt = torch.where(pick, w.states[b][:, 0, :], torch.full_like(w.states[b][:, 0, :], -1)).contiguous()
+    hc = torch.zeros((n, ld), dtype=torch.int32, device=dev)
+    same.same_accumulate_hits(ctx, w.states[b], tgt, m, nc, ld, hc)
+    torch.cuda.synchronize()
+    reps = 5
+    e0.record(stream)
+    for _ in range(reps):
+        same.same_accumulate_hits(ctx, w.states[b], tgt, m, nc, ld, hc)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    t_hits = e0.elapsed_time(e1) / reps
+    b_hits = n * m * ld * sb + n * ld * sb + 8 * n * ld
+    del hc, tgt, pick
+    return {
+        "two_layer": {"workload": "concepts30-items300-4k, 20% of known entries held out",
+                      "train_steps": train_steps, "pred_sweeps": pred_sweeps, "replicas": 20,
+                      "test_entries": int(len(lab)), "auc": round(a, 5), "predict_ms": round(t_pred, 3)},
+        "hits_kernel": {"ms": round(t_hits, 4), "algorithmic_bytes": b_hits, "gbs": round(b_hits / t_hits / 1e6, 1),
+                        "frac": round(b_hits / t_hits / 1e6 / HBM_PEAK_GBS, 4)},
     }
 
 

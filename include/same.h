@@ -282,6 +282,31 @@ int same_init_latent(same_ctx *ctx, void *states, const uint8_t *obs, int32_t m,
                      int64_t ld, int64_t col_offset, uint64_t seed, void *stream);
 
 /*
+ * Held-out prediction (Sec. 6, testing phase): with the CPTs frozen, the
+ * states a test entry takes over repeated sweeps estimate the probability of
+ * its true state.  same_accumulate_hits adds, for every entry (i, j < n_cols)
+ * with target[i][j] >= 0, the number of replicas r < m with
+ * states[i][r][j] == target[i][j] to hits[i][j].  target [n][ld] has the
+ * state type (-1: not a test entry; test entries must be latent in the obs
+ * the sweeps use); hits [n][ld] is int32, 16-byte aligned.  Device pointers
+ * owned by the caller; the caller zeroes hits before the first call.
+ *
+ * same_predict runs n_sweeps sweeps (same_sweep with sweep ids sweep_id0,
+ * sweep_id0 + 1, ...) with cpts unchanged and accumulates the hits after each;
+ * hits / (n_sweeps * m) is then the estimated probability of each test
+ * entry's true state.  states is updated in place.  Errors as same_sweep's,
+ * plus SAME_EINVAL for null target/hits or n_sweeps < 0 and SAME_EALIGN for
+ * a misaligned target or hits.
+ */
+int same_accumulate_hits(same_ctx *ctx, const void *states, const void *target, int32_t m,
+                         int64_t n_cols, int64_t ld, int32_t *hits, void *stream);
+
+int same_predict(same_ctx *ctx, void *states, const uint8_t *obs, const float *cpts,
+                 const void *target, int32_t m, int64_t n_cols, int64_t ld, int64_t col_offset,
+                 uint64_t seed, uint32_t sweep_id0, int32_t n_sweeps, int32_t *hits,
+                 void *workspace, void *stream);
+
+/*
  * Measurement of the sweep kernels.  same_kernel_timing(ctx, 1) clears the
  * totals and makes every later sweep of ctx bracket each of its kernel
  * launches with a pair of HIP events on the launch stream; (ctx, 0) clears

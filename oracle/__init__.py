@@ -88,6 +88,9 @@ def lib():
             L.oracle_init_latent.argtypes = [C.c_int32, P, C.c_int64, C.c_int32, C.c_int64, C.c_int64,
                                              C.c_uint64, C.c_int32, P, P]
             L.oracle_init_latent.restype = C.c_int
+            L.oracle_accumulate_hits.argtypes = [C.c_int32, C.c_int64, C.c_int32, C.c_int64, C.c_int32,
+                                                 P, P, P]
+            L.oracle_accumulate_hits.restype = C.c_int
             _lib = L
         return _lib
 
@@ -278,3 +281,26 @@ def init_latent(card, n_cols, m, col_offset, seed, states, obs):
     _check(lib().oracle_init_latent(n, _ptr(card), int(n_cols), int(m), int(ld), int(col_offset),
                                     int(seed), states.dtype.itemsize, _ptr(states),
                                     _ptr(np.ascontiguousarray(obs, dtype=np.uint8))))
+
+
+def accumulate_hits(states, target, m, n_cols, hits):
+    """Held-out prediction (Sec. 6), in place: hits[i][j] += number of replicas
+    whose state equals target[i][j] at every test entry (target >= 0)."""
+    n, _, ld = states.shape
+    assert target.shape == (n, ld) and target.dtype == states.dtype and target.flags.c_contiguous
+    assert hits.shape == (n, ld) and hits.dtype == np.int32 and hits.flags.c_contiguous
+    _check(lib().oracle_accumulate_hits(int(n), int(n_cols), int(m), int(ld), states.dtype.itemsize,
+                                        _ptr(np.ascontiguousarray(states)), _ptr(target), _ptr(hits)))
+
+
+def predict(parents, card, theta, color, states, obs, target, m, n_cols, col_offset, seed,
+            sweep_id0, n_sweeps):
+    """Testing phase of Sec. 6: n_sweeps sequential-scan sweeps with the CPTs
+    frozen (test entries latent in obs), the hits accumulated after each.
+    states is updated in place; returns hits (int32 [n][ld])."""
+    n, _, ld = states.shape
+    hits = np.zeros((n, ld), dtype=np.int32)
+    for s in range(n_sweeps):
+        sweep(parents, card, theta, color, states, obs, m, n_cols, col_offset, seed, sweep_id0 + s)
+        accumulate_hits(states, target, m, n_cols, hits)
+    return hits

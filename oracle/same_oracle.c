@@ -675,3 +675,32 @@ int oracle_init_latent(int32_t n, const int32_t *card, int64_t n_cols, int32_t m
             }
     return OR_OK;
 }
+
+/* ------------------------------------------------------------------ */
+/* Held-out prediction (Sec. 6).                                       */
+/* ------------------------------------------------------------------ */
+
+static int32_t get_state(const void *a, int32_t state_bytes, int64_t idx) {
+    return state_bytes == 1 ? ((const int8_t *)a)[idx] : ((const int16_t *)a)[idx];
+}
+
+/*
+ * With the CPTs frozen, the states a test entry takes over n sweeps estimate
+ * the probability of its true state (Sec. 6, testing phase).  One call adds,
+ * for every entry (i, j < n_cols) with target[i][j] >= 0 (target [n][ld] in
+ * the state type, -1 = not a test entry), the number of replicas r < m with
+ * states[i][r][j] == target[i][j] to hits[i][j] (int32 [n][ld]).
+ */
+int oracle_accumulate_hits(int32_t n, int64_t n_cols, int32_t m, int64_t ld, int32_t state_bytes,
+                           const void *states, const void *target, int32_t *hits) {
+    if (n <= 0 || m < 1 || n_cols < 0 || ld < n_cols || (state_bytes != 1 && state_bytes != 2))
+        return OR_EINVAL;
+    for (int32_t i = 0; i < n; ++i)
+        for (int64_t j = 0; j < n_cols; ++j) {
+            int32_t t = get_state(target, state_bytes, (int64_t)i * ld + j);
+            if (t < 0) continue;
+            for (int32_t r = 0; r < m; ++r)
+                if (get_state(states, state_bytes, ((int64_t)i * m + r) * ld + j) == t) hits[(int64_t)i * ld + j] += 1;
+        }
+    return OR_OK;
+}

@@ -20,6 +20,7 @@ __all__ = [
     "same_sweep", "same_sweep_debug", "same_counts", "same_sample_cpts", "same_last_error",
     "same_step", "same_sweep_plan", "same_stream_slots_size", "same_stream_pass", "SAME_STREAM_COUNTS_ONLY",
     "same_kernel_timing", "same_kernel_times", "same_expand_observed", "same_init_latent",
+    "same_accumulate_hits", "same_predict",
     "library_path", "load_library",
 ]
 
@@ -88,12 +89,15 @@ def load_library():
         L.same_kernel_times.argtypes = [P, C.POINTER(_KernelTimes)]
         L.same_expand_observed.argtypes = [P, P, P, P, I64, I32, I64, I64, P, P, P]
         L.same_init_latent.argtypes = [P, P, P, I32, I64, I64, I64, U64, P]
+        L.same_accumulate_hits.argtypes = [P, P, P, I32, I64, I64, P, P]
+        L.same_predict.argtypes = [P, P, P, P, P, I32, I64, I64, I64, U64, U32, I32, P, P, P]
         L.same_last_error.argtypes = []
         L.same_last_error.restype = C.c_char_p
         for f in ("same_create", "same_create_ex", "same_layout", "same_workspace_size", "same_sweep",
                   "same_sweep_debug", "same_counts", "same_sample_cpts", "same_step", "same_sweep_plan",
                   "same_stream_slots_size", "same_stream_pass", "same_kernel_timing",
-                  "same_kernel_times", "same_expand_observed", "same_init_latent"):
+                  "same_kernel_times", "same_expand_observed", "same_init_latent",
+                  "same_accumulate_hits", "same_predict"):
             getattr(L, f).restype = C.c_int
         _lib = L
         return L
@@ -283,3 +287,15 @@ def same_expand_observed(ctx, row_ptr, col_idx, values, nnz, m, n_cols, ld, stat
 def same_init_latent(ctx, states, obs, m, n_cols, ld, col_offset, seed, stream=None):
     _check(load_library().same_init_latent(ctx.handle, _ptr(states), _ptr(obs), int(m), int(n_cols),
                                            int(ld), int(col_offset), int(seed), _stream(stream)))
+
+
+def same_accumulate_hits(ctx, states, target, m, n_cols, ld, hits, stream=None):
+    _check(load_library().same_accumulate_hits(ctx.handle, _ptr(states), _ptr(target), int(m), int(n_cols),
+                                               int(ld), _ptr(hits), _stream(stream)))
+
+
+def same_predict(ctx, states, obs, cpts, target, m, n_cols, ld, col_offset, seed, sweep_id0, n_sweeps, hits,
+                 workspace, stream=None):
+    _check(load_library().same_predict(ctx.handle, _ptr(states), _ptr(obs), _ptr(cpts), _ptr(target), int(m),
+                                       int(n_cols), int(ld), int(col_offset), int(seed), int(sweep_id0),
+                                       int(n_sweeps), _ptr(hits), _ptr(workspace), _stream(stream)))

@@ -696,6 +696,46 @@ extern "C" int same_init_latent(same_ctx *ctx, void *states, const uint8_t *obs,
                      "latent init launch");
 }
 
+namespace {
+int check_hits_args(same_ctx *ctx, const void *states, const void *target, int32_t m, int64_t n_cols, int64_t ld,
+                    int32_t *hits) {
+    int rc = check_minibatch(ctx, states, m, n_cols, ld);
+    if (rc) return rc;
+    if (!target || !hits) return set_error(SAME_EINVAL, "target and hits must be non-null");
+    if (!aligned(target, 4 * (size_t)ctx->g.state_bytes))
+        return set_error(SAME_EALIGN, "target must be aligned to 4 state elements");
+    if (!aligned(hits, 16)) return set_error(SAME_EALIGN, "hits must be 16-byte aligned");
+    return SAME_OK;
+}
+}  // namespace
+
+extern "C" int same_accumulate_hits(same_ctx *ctx, const void *states, const void *target, int32_t m,
+                                    int64_t n_cols, int64_t ld, int32_t *hits, void *stream) {
+    int rc = check_hits_args(ctx, states, target, m, n_cols, ld, hits);
+    if (rc) return rc;
+    return check_hip(same::launch_hits(states, target, ctx->g.n, m, n_cols, ld, ctx->g.state_bytes, hits,
+                                       (hipStream_t)stream),
+                     "hits launch");
+}
+
+extern "C" int same_predict(same_ctx *ctx, void *states, const uint8_t *obs, const float *cpts, const void *target,
+                            int32_t m, int64_t n_cols, int64_t ld, int64_t col_offset, uint64_t seed,
+                            uint32_t sweep_id0, int32_t n_sweeps, int32_t *hits, void *workspace, void *stream) {
+    int rc = check_hits_args(ctx, states, target, m, n_cols, ld, hits);
+    if (rc) return rc;
+    if (n_sweeps < 0) return set_error(SAME_EINVAL, "n_sweeps must be >= 0");
+    for (int32_t s = 0; s < n_sweeps; ++s) {
+        rc = do_sweep(ctx, states, obs, cpts, m, n_cols, ld, col_offset, seed, sweep_id0 + (uint32_t)s, 0, 0,
+                      nullptr, workspace, stream);
+        if (rc) return rc;
+        rc = check_hip(same::launch_hits(states, target, ctx->g.n, m, n_cols, ld, ctx->g.state_bytes, hits,
+                                         (hipStream_t)stream),
+                       "hits launch");
+        if (rc) return rc;
+    }
+    return SAME_OK;
+}
+
 extern "C" int same_kernel_timing(same_ctx *ctx, int32_t enable) {
     if (!ctx) return set_error(SAME_EINVAL, "null context");
     std::lock_guard<std::mutex> lock(ctx->mu);

@@ -1197,6 +1197,48 @@ __global__ __launch_bounds__(kBlock) void init_latent_kernel(const int32_t *__re
     }
 }
 
+// ---------------------------------------------------------------- prediction
+
+// Held-out prediction (Sec. 6): with the CPTs frozen, hits[i][j] counts the
+// replicas whose state equals the test entry's true value target[i][j] (-1:
+// not a test entry).  One thread per (node, column quad): the quad's targets
+// and hit counters are read once, the replicas' state quads are compared in
+// turn, and the counters are written back.
+template <typename ST>
+__global__ __launch_bounds__(kBlock) void hits_kernel(const ST *__restrict__ states, const ST *__restrict__ target,
+                                                      int32_t n, int32_t m, int64_t n_cols, int64_t ld,
+                                                      int32_t *__restrict__ hits) {
+    using Q = Quad<ST>;
+    const int64_t quads = (n_cols + 3) >> 2;
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= (int64_t)n * quads) return;
+    const int64_t q = t % quads;
+    const int i = (int)(t / quads);
+    const int64_t col = 4 * q;
+    const typename Q::V tg = Q::load(target + (int64_t)i * ld + col);
+    int want[4], any = 0;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        want[c] = (int)(sizeof(ST) == 1 ? (int8_t)Q::get(tg, c) : (int16_t)Q::get(tg, c));
+        if (col + c >= n_cols) want[c] = -1;
+        any |= want[c] >= 0;
+    }
+    if (!any) return;
+    int add[4] = {0, 0, 0, 0};
+    for (int r = 0; r < m; ++r) {
+        const typename Q::V v = Q::load(states + ((int64_t)i * m + r) * ld + col);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) add[c] += Q::get(v, c) == (want[c] & (sizeof(ST) == 1 ? 0xff : 0xffff)) ? 1 : 0;
+    }
+    int4 *h = reinterpret_cast<int4 *>(hits + (int64_t)i * ld + col);
+    int4 cur = *h;
+    if (want[0] >= 0) cur.x += add[0];
+    if (want[1] >= 0) cur.y += add[1];
+    if (want[2] >= 0) cur.z += add[2];
+    if (want[3] >= 0) cur.w += add[3];
+    *h = cur;
+}
+
 }  // namespace dev
 
 // ================================================================= launchers
@@ -1338,6 +1380,21 @@ hipError_t launch_init_latent(const DeviceTables &t, int32_t n, int32_t m, int64
         hipLaunchKernelGGL(dev::init_latent_kernel<int16_t>, dim3((unsigned)blocks), dim3(dev::kBlock), 0,
                            stream, t.cdesc, t.cdesc_off, n, m, n_cols, ld, col_offset, key0, key1,
                            (int16_t *)states, obs);
+    return hipGetLastError();
+}
+
+hipError_t launch_hits(const void *states, const void *target, int32_t n, int32_t m, int64_t n_cols, int64_t ld,
+                       int32_t state_bytes, int32_t *hits, hipStream_t stream) {
+    const int64_t items = (int64_t)n * ((n_cols + 3) / 4);
+    if (items <= 0) return hipSuccess;
+    const int64_t blocks = (items + dev::kBlock - 1) / dev::kBlock;
+    if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+    if (state_bytes == 1)
+        hipLaunchKernelGGL(dev::hits_kernel<int8_t>, dim3((unsigned)blocks), dim3(dev::kBlock), 0, stream,
+                           (const int8_t *)states, (const int8_t *)target, n, m, n_cols, ld, hits);
+    else
+        hipLaunchKernelGGL(dev::hits_kernel<int16_t>, dim3((unsigned)blocks), dim3(dev::kBlock), 0, stream,
+                           (const int16_t *)states, (const int16_t *)target, n, m, n_cols, ld, hits);
     return hipGetLastError();
 }
 

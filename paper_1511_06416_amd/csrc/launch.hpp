@@ -85,6 +85,10 @@ hipError_t launch_init_latent(const DeviceTables &t, int32_t n, int32_t m, int64
                               int64_t col_offset, uint32_t key0, uint32_t key1, int32_t state_bytes,
                               void *states, const uint8_t *obs, hipStream_t stream);
 
+// Held-out prediction: hits[i][j] += replicas whose state equals target[i][j] >= 0.
+hipError_t launch_hits(const void *states, const void *target, int32_t n, int32_t m, int64_t n_cols, int64_t ld,
+                       int32_t state_bytes, int32_t *hits, hipStream_t stream);
+
 hipError_t launch_moving_sum(const int32_t *newc, int32_t *mb, int32_t *totals, int64_t total,
                              hipStream_t stream);
 

@@ -11,6 +11,7 @@ from .synth import (  # noqa: F401
     Network,
     Workload,
     cpt_layout,
+    holdout,
     koller,
     make_network,
     make_workload,

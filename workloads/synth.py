@@ -42,7 +42,7 @@ import torch
 BASE_SEED = 151106416
 
 # purposes for the seed sequences
-_P_DAG, _P_TRUE, _P_DATA, _P_MASK, _P_INIT_THETA, _P_INIT_STATES = range(6)
+_P_DAG, _P_TRUE, _P_DATA, _P_MASK, _P_INIT_THETA, _P_INIT_STATES, _P_HOLDOUT = range(7)
 
 CONFIGS = {
     1: dict(name="student-2k", graph="student", n_cols=2_000, hidden=0.5, m=1, sweeps=20,
@@ -277,3 +277,23 @@ def make_workload(cfg_id: int, n_cols: Optional[int] = None, m: Optional[int] = 
                     init_theta=init_theta, n_cols=N, nb=nb, M=M, ld=ld, m=m, hidden=hid,
                     sweeps=spec["sweeps"], alpha=PRIOR_ALPHA, seed=sampler_seed(cfg_id),
                     states=states, obs=obs, data=datas if keep_data else None)
+
+
+def holdout(w: "Workload", b: int = 0, frac: float = 0.2):
+    """Held-out split of minibatch b (Sec. 6: 80% of the known entries train,
+    the rest test): each known entry of the real columns is a test entry with
+    probability frac (numpy generator seeded for purpose 6).  Returns
+    (obs_train, target): obs_train is obs with the test entries hidden;
+    target [n][ld] holds the true value of every test entry and -1 elsewhere
+    (numpy arrays, the states' dtype for target)."""
+    obs = w.obs[b].cpu().numpy()
+    st = w.states[b].cpu().numpy()
+    n_cols = w.mb_cols(b)
+    rng = _rng(w.cfg_id, _P_HOLDOUT, b)
+    pick = (rng.random(obs.shape) < frac) & (obs == 1)
+    pick[:, n_cols:] = False
+    obs_train = obs.copy()
+    obs_train[pick] = 0
+    target = np.full(obs.shape, -1, dtype=st.dtype)
+    target[pick] = st[:, 0, :][pick]
+    return obs_train, target
