@@ -563,12 +563,30 @@ def stream_timing(w, ctx, cpts, ws, dev, steps):
     state_bytes = float(net.n) * w.m * w.n_cols * hs.element_size()
     h2d = state_bytes + float(net.n) * w.n_cols
     log("streamed %d passes in %.3f s" % (steps, dt))
+    # the same passes with the exponential moving sum of the counts (Sec. 4
+    # footnote): no per-minibatch count storage, decay 1 - 1/M
+    decay = 1.0 - 1.0 / w.M
+    tot_e = torch.zeros(ctx.cpt_total, dtype=torch.float64, device=dev)
+    cp_e = cpts.clone()
+    same.same_stream_pass_ema(ctx, hs, ho, host_ld, w.n_cols, w.nb, w.m, cp_e, tot_e, decay, w.seed, 0,
+                              same.SAME_STREAM_COUNTS_ONLY, slots, ws)
+    torch.cuda.synchronize()
+    t = time.perf_counter()
+    for s in range(1, 1 + steps):
+        same.same_stream_pass_ema(ctx, hs, ho, host_ld, w.n_cols, w.nb, w.m, cp_e, tot_e, decay, w.seed,
+                                  100 + s, 0, slots, ws)
+    torch.cuda.synchronize()
+    dt_e = time.perf_counter() - t
+    log("streamed %d moving-sum passes in %.3f s" % (steps, dt_e))
     del hs, ho
     return {"value": round(ns / dt, 1), "unit": "node-samples/s", "passes": steps,
             "ms_per_pass": round(dt * 1e3 / steps, 2),
             "pcie_bytes_per_pass": {"h2d": h2d, "d2h": state_bytes},
             "pcie_gbs_each_way": {"h2d": round(h2d * steps / dt / 1e9, 1),
-                                  "d2h": round(state_bytes * steps / dt / 1e9, 1)}}
+                                  "d2h": round(state_bytes * steps / dt / 1e9, 1)},
+            "exponential_moving_sum": {"value": round(ns / dt_e, 1), "ms_per_pass": round(dt_e * 1e3 / steps, 2),
+                                       "decay": round(decay, 6),
+                                       "count_bytes_not_stored": int(w.M * ctx.cpt_total * 4)}}
 
 
 def cpu_baseline(w, cols, st, ob, steps):

@@ -251,6 +251,40 @@ int same_stream_pass(same_ctx *ctx, void *host_states, const uint8_t *host_obs, 
                      void *workspace, void *stream);
 
 /*
+ * Exponential moving sum of the counts (Sec. 4: for datasets too large to keep
+ * every minibatch's counts, the counts are maintained as an exponential
+ * moving sum, so memory scales with the model, not the data).
+ *
+ * same_counts_ema: the (parent configuration, state) histogram of the
+ * minibatch (as same_counts) folded into fp64 totals [cpt_total] as
+ * totals = decay * totals + new (the product rounded before the sum), with
+ * decay in [0, 1].  decay = 1 - 1/M keeps the totals on the scale of the exact
+ * moving sum over M minibatches (its fixed point for equal minibatches is M
+ * times one minibatch's counts); decay = 0 keeps only the newest minibatch.
+ *
+ * same_sample_cpts_ema: the Dirichlet resample of same_sample_cpts from fp64
+ * totals: g_e ~ Gamma(prior + totals[e], 1), cpts_out[e] = fp32(g_e / row sum).
+ *
+ * same_stream_pass_ema: same_stream_pass with the exponential moving sum in
+ * place of the per-minibatch counts: per minibatch b, same_sweep,
+ * same_counts_ema and same_sample_cpts_ema (update_id = pass_id * M + b); with
+ * SAME_STREAM_COUNTS_ONLY only same_counts_ema (the pre-pass).  No
+ * per-minibatch count storage.  Device pointers as in same_stream_pass;
+ * totals is fp64, 8-byte aligned.  Errors as same_counts / same_stream_pass,
+ * plus SAME_EINVAL for decay outside [0, 1].
+ */
+int same_counts_ema(same_ctx *ctx, const void *states, int32_t m, int64_t n_cols, int64_t ld,
+                    double decay, double *totals, void *workspace, void *stream);
+
+int same_sample_cpts_ema(same_ctx *ctx, const double *totals, float *cpts_out, uint64_t seed,
+                         uint32_t update_id, void *workspace, void *stream);
+
+int same_stream_pass_ema(same_ctx *ctx, void *host_states, const uint8_t *host_obs, int64_t host_ld,
+                         int64_t n_cols, int64_t nb, int32_t m, float *cpts, double *totals,
+                         double decay, uint64_t seed, uint32_t pass_id, int32_t flags, void *slots,
+                         void *workspace, void *stream);
+
+/*
  * Dense minibatch from its known entries (Sec. 4: the sampler takes a
  * typically sparse data matrix with rows = variables and columns = cases, and
  * forms m copies of the known data per minibatch).  The known entries are in

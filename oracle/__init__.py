@@ -91,6 +91,10 @@ def lib():
             L.oracle_accumulate_hits.argtypes = [C.c_int32, C.c_int64, C.c_int32, C.c_int64, C.c_int32,
                                                  P, P, P]
             L.oracle_accumulate_hits.restype = C.c_int
+            L.oracle_dirichlet_f64.argtypes = [C.c_int32, P, P, P, P, C.c_double, C.c_uint64, C.c_uint32, P, P]
+            L.oracle_dirichlet_f64.restype = C.c_int
+            L.oracle_ema.argtypes = [C.c_int64, C.c_double, P, P]
+            L.oracle_ema.restype = None
             _lib = L
         return _lib
 
@@ -304,3 +308,23 @@ def predict(parents, card, theta, color, states, obs, target, m, n_cols, col_off
         sweep(parents, card, theta, color, states, obs, m, n_cols, col_offset, seed, sweep_id0 + s)
         accumulate_hits(states, target, m, n_cols, hits)
     return hits
+
+
+def ema(totals, decay, new):
+    """Exponential moving sum (Sec. 4 footnote), in place on fp64 totals:
+    totals = decay * totals + new."""
+    assert totals.dtype == np.float64 and totals.flags.c_contiguous
+    nc = np.ascontiguousarray(new, dtype=np.int64)
+    assert nc.shape == totals.shape
+    lib().oracle_ema(int(totals.size), float(decay), _ptr(nc), _ptr(totals))
+
+
+def dirichlet_f64(parents, card, totals, alpha, seed, update_id, want_gamma=False):
+    """Dirichlet resample from fp64 (moving-sum) totals."""
+    pptr, pidx, card = _dag(parents, card)
+    tot = np.ascontiguousarray(totals, dtype=np.float64)
+    theta = np.zeros(len(tot), dtype=np.float32)
+    gv = np.zeros(len(tot), dtype=np.float64) if want_gamma else None
+    _check(lib().oracle_dirichlet_f64(len(card), _ptr(pptr), _ptr(pidx), _ptr(card), _ptr(tot), float(alpha),
+                                      int(seed), int(update_id), _ptr(theta), _ptr(gv)))
+    return (theta, gv) if want_gamma else theta

@@ -581,11 +581,28 @@ double oracle_gamma(double shape, uint64_t seed, uint32_t entry, uint32_t update
 /*
  * theta_out[e] = fp32( g_e / sum of g over e's CPT row ), g_e ~ Gamma(alpha +
  * totals[e]).  A row whose Gamma variates all underflow to zero becomes
- * uniform.  gamma_out (nullable) receives the fp64 variates.
+ * uniform.  gamma_out (nullable) receives the fp64 variates.  totals are
+ * integer counts (oracle_dirichlet) or fp64 moving sums (oracle_dirichlet_f64).
  */
+static int dirichlet_impl(int32_t n, const int32_t *pptr, const int32_t *pidx, const int32_t *card,
+                          const int64_t *itot, const double *dtot, double alpha, uint64_t seed,
+                          uint32_t update_id, float *theta_out, double *gamma_out);
+
 int oracle_dirichlet(int32_t n, const int32_t *pptr, const int32_t *pidx, const int32_t *card,
                      const int64_t *totals, double alpha, uint64_t seed, uint32_t update_id,
                      float *theta_out, double *gamma_out) {
+    return dirichlet_impl(n, pptr, pidx, card, totals, NULL, alpha, seed, update_id, theta_out, gamma_out);
+}
+
+int oracle_dirichlet_f64(int32_t n, const int32_t *pptr, const int32_t *pidx, const int32_t *card,
+                         const double *totals, double alpha, uint64_t seed, uint32_t update_id,
+                         float *theta_out, double *gamma_out) {
+    return dirichlet_impl(n, pptr, pidx, card, NULL, totals, alpha, seed, update_id, theta_out, gamma_out);
+}
+
+static int dirichlet_impl(int32_t n, const int32_t *pptr, const int32_t *pidx, const int32_t *card,
+                          const int64_t *itot, const double *dtot, double alpha, uint64_t seed,
+                          uint32_t update_id, float *theta_out, double *gamma_out) {
     graph_t g;
     int rc = graph_build(&g, n, pptr, pidx, card);
     if (rc) return rc;
@@ -594,7 +611,7 @@ int oracle_dirichlet(int32_t n, const int32_t *pptr, const int32_t *pidx, const 
     if (!gv) { graph_free(&g); return OR_ENOMEM; }
 #pragma omp parallel for schedule(static)
     for (int64_t e = 0; e < g.off[n]; ++e)
-        gv[e] = oracle_gamma(alpha + (double)totals[e], seed, (uint32_t)e, update_id, NULL);
+        gv[e] = oracle_gamma(alpha + (itot ? (double)itot[e] : dtot[e]), seed, (uint32_t)e, update_id, NULL);
     for (int32_t i = 0; i < n; ++i) {
         int32_t K = card[i];
         for (int64_t u = 0; u < g.rows[i]; ++u) {
@@ -703,4 +720,16 @@ int oracle_accumulate_hits(int32_t n, int64_t n_cols, int32_t m, int64_t ld, int
                 if (get_state(states, state_bytes, ((int64_t)i * m + r) * ld + j) == t) hits[(int64_t)i * ld + j] += 1;
         }
     return OR_OK;
+}
+
+/*
+ * Exponential moving sum of the counts (Sec. 4 footnote: for datasets whose
+ * per-minibatch counts are not kept): totals[e] = decay * totals[e] + newc[e]
+ * in fp64, the product rounded before the sum.
+ */
+void oracle_ema(int64_t total, double decay, const int64_t *newc, double *totals) {
+    for (int64_t e = 0; e < total; ++e) {
+        double p = decay * totals[e];
+        totals[e] = p + (double)newc[e];
+    }
 }

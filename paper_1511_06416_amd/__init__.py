@@ -20,7 +20,7 @@ __all__ = [
     "same_sweep", "same_sweep_debug", "same_counts", "same_sample_cpts", "same_last_error",
     "same_step", "same_sweep_plan", "same_stream_slots_size", "same_stream_pass", "SAME_STREAM_COUNTS_ONLY",
     "same_kernel_timing", "same_kernel_times", "same_expand_observed", "same_init_latent",
-    "same_accumulate_hits", "same_predict",
+    "same_accumulate_hits", "same_predict", "same_counts_ema", "same_sample_cpts_ema", "same_stream_pass_ema",
     "library_path", "load_library",
 ]
 
@@ -90,6 +90,10 @@ def load_library():
         L.same_expand_observed.argtypes = [P, P, P, P, I64, I32, I64, I64, P, P, P]
         L.same_init_latent.argtypes = [P, P, P, I32, I64, I64, I64, U64, P]
         L.same_accumulate_hits.argtypes = [P, P, P, I32, I64, I64, P, P]
+        L.same_counts_ema.argtypes = [P, P, I32, I64, I64, C.c_double, P, P, P]
+        L.same_sample_cpts_ema.argtypes = [P, P, P, U64, U32, P, P]
+        L.same_stream_pass_ema.argtypes = [P, P, P, I64, I64, I64, I32, P, P, C.c_double, U64, U32, I32, P, P,
+                                           P]
         L.same_predict.argtypes = [P, P, P, P, P, I32, I64, I64, I64, U64, U32, I32, P, P, P]
         L.same_last_error.argtypes = []
         L.same_last_error.restype = C.c_char_p
@@ -97,7 +101,8 @@ def load_library():
                   "same_sweep_debug", "same_counts", "same_sample_cpts", "same_step", "same_sweep_plan",
                   "same_stream_slots_size", "same_stream_pass", "same_kernel_timing",
                   "same_kernel_times", "same_expand_observed", "same_init_latent",
-                  "same_accumulate_hits", "same_predict"):
+                  "same_accumulate_hits", "same_predict", "same_counts_ema", "same_sample_cpts_ema", "same_stream_pass_ema", "same_counts_ema", "same_sample_cpts_ema",
+                  "same_stream_pass_ema"):
             getattr(L, f).restype = C.c_int
         _lib = L
         return L
@@ -299,3 +304,22 @@ def same_predict(ctx, states, obs, cpts, target, m, n_cols, ld, col_offset, seed
     _check(load_library().same_predict(ctx.handle, _ptr(states), _ptr(obs), _ptr(cpts), _ptr(target), int(m),
                                        int(n_cols), int(ld), int(col_offset), int(seed), int(sweep_id0),
                                        int(n_sweeps), _ptr(hits), _ptr(workspace), _stream(stream)))
+
+
+def same_counts_ema(ctx, states, m, n_cols, ld, decay, totals, workspace, stream=None):
+    _check(load_library().same_counts_ema(ctx.handle, _ptr(states), int(m), int(n_cols), int(ld), float(decay),
+                                          _ptr(totals), _ptr(workspace), _stream(stream)))
+
+
+def same_sample_cpts_ema(ctx, totals, cpts_out, seed, update_id, workspace, stream=None):
+    _check(load_library().same_sample_cpts_ema(ctx.handle, _ptr(totals), _ptr(cpts_out), int(seed),
+                                               int(update_id), _ptr(workspace), _stream(stream)))
+
+
+def same_stream_pass_ema(ctx, host_states, host_obs, host_ld, n_cols, nb, m, cpts, totals, decay, seed, pass_id,
+                         flags, slots, workspace, stream=None):
+    """host_states / host_obs: pinned host tensors (or addresses); the rest device (totals fp64)."""
+    _check(load_library().same_stream_pass_ema(ctx.handle, _ptr(host_states), _ptr(host_obs), int(host_ld),
+                                               int(n_cols), int(nb), int(m), _ptr(cpts), _ptr(totals),
+                                               float(decay), int(seed), int(pass_id), int(flags), _ptr(slots),
+                                               _ptr(workspace), _stream(stream)))

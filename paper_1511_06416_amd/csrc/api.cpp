@@ -587,22 +587,17 @@ int same_stream_slots_size(const same_ctx *ctx, int32_t m, int64_t nb, size_t *b
     return SAME_OK;
 }
 
-int same_stream_pass(same_ctx *ctx, void *host_states, const uint8_t *host_obs, int64_t host_ld,
-                     int64_t n_cols, int64_t nb, int32_t m, float *cpts, int32_t *mb_counts,
-                     int32_t *totals, uint64_t seed, uint32_t pass_id, int32_t flags, void *slots,
-                     void *workspace, void *stream) {
-    if (!ctx) return set_error(SAME_EINVAL, "ctx is null");
-    if (!host_states || !host_obs || !cpts || !mb_counts || !totals || !slots || !workspace)
-        return set_error(SAME_EINVAL, "null pointer argument");
-    if (m < 1 || m > 65535) return set_error(SAME_EINVAL, "m must be in [1, 65535]");
-    if (nb < 4 || nb % 4 != 0) return set_error(SAME_EALIGN, "nb must be a positive multiple of 4");
-    if (n_cols < 0 || host_ld < n_cols) return set_error(SAME_EINVAL, "need 0 <= n_cols <= host_ld");
-    if (flags & ~SAME_STREAM_COUNTS_ONLY) return set_error(SAME_EINVAL, "unknown flags");
-    if (!aligned(slots, kAlign)) return set_error(SAME_EALIGN, "slots must be 256-byte aligned");
-    if (n_cols == 0) return SAME_OK;
-    const int64_t M = (n_cols + nb - 1) / nb;
-    if ((double)M * (double)pass_id + M > 4294967295.0)
-        return set_error(SAME_ESIZE, "pass_id * minibatches exceeds the update-id range");
+}  // extern "C"
+
+namespace {
+
+// One out-of-core pass (layout and overlap as documented for same_stream_pass):
+// per minibatch b the upload, then compute(b, device states, device obs,
+// columns, first column) on `stream`, then (with download) the copy back.
+template <typename F>
+int stream_pass_impl(same_ctx *ctx, void *host_states, const uint8_t *host_obs, int64_t host_ld,
+                     int64_t n_cols, int64_t nb, int32_t m, void *slots, void *stream, bool download,
+                     F &&compute) {
     const SlotGeom sg = slot_geom(ctx, m, nb);
     StreamRes *sr = nullptr;
     int rc = stream_res_for_current_device(ctx, &sr);
@@ -610,8 +605,7 @@ int same_stream_pass(same_ctx *ctx, void *host_states, const uint8_t *host_obs, 
     hipStream_t cs = (hipStream_t)stream;
     const size_t sb = (size_t)ctx->g.state_bytes;
     const int64_t rows = (int64_t)ctx->g.n * m;
-    const int64_t total = ctx->g.off[ctx->g.n];
-    const bool counts_only = (flags & SAME_STREAM_COUNTS_ONLY) != 0;
+    const int64_t M = (n_cols + nb - 1) / nb;
     for (int64_t b = 0; b < M; ++b) {
         const int s = (int)(b & 1);
         const int64_t c0 = b * nb;
@@ -632,16 +626,11 @@ int same_stream_pass(same_ctx *ctx, void *host_states, const uint8_t *host_obs, 
         if (!rc) rc = check_hip(hipEventRecord(sr->ev_up[s], sr->up), "event");
         if (!rc) rc = check_hip(hipStreamWaitEvent(cs, sr->ev_up[s], 0), "wait");
         if (rc) return rc;
-        int32_t *mb = mb_counts + b * total;
-        if (counts_only)
-            rc = same_counts(ctx, d_states, m, cols, sg.ld, mb, totals, workspace, stream);
-        else
-            rc = do_step(ctx, d_states, d_obs, cpts, m, cols, sg.ld, c0, seed, pass_id, mb, totals,
-                         (uint32_t)(pass_id * M + b), workspace, stream);
+        rc = compute(b, d_states, d_obs, cols, c0, sg.ld);
         if (rc) return rc;
         rc = check_hip(hipEventRecord(sr->ev_comp[s], cs), "event");
         if (rc) return rc;
-        if (counts_only) {
+        if (!download) {
             rc = check_hip(hipEventRecord(sr->ev_down[s], cs), "event");
         } else {
             rc = check_hip(hipStreamWaitEvent(sr->down, sr->ev_comp[s], 0), "wait");
@@ -659,6 +648,114 @@ int same_stream_pass(same_ctx *ctx, void *host_states, const uint8_t *host_obs, 
         if (sr->slot_used[s] && (rc = check_hip(hipStreamWaitEvent(cs, sr->ev_down[s], 0), "wait")))
             return rc;
     return SAME_OK;
+}
+
+int check_stream_args(same_ctx *ctx, const void *host_states, const uint8_t *host_obs, int64_t host_ld,
+                      int64_t n_cols, int64_t nb, int32_t m, const void *cpts, const void *counts,
+                      const void *totals, uint32_t pass_id, int32_t flags, const void *slots,
+                      const void *workspace) {
+    if (!ctx) return set_error(SAME_EINVAL, "ctx is null");
+    if (!host_states || !host_obs || !cpts || !counts || !totals || !slots || !workspace)
+        return set_error(SAME_EINVAL, "null pointer argument");
+    if (m < 1 || m > 65535) return set_error(SAME_EINVAL, "m must be in [1, 65535]");
+    if (nb < 4 || nb % 4 != 0) return set_error(SAME_EALIGN, "nb must be a positive multiple of 4");
+    if (n_cols < 0 || host_ld < n_cols) return set_error(SAME_EINVAL, "need 0 <= n_cols <= host_ld");
+    if (flags & ~SAME_STREAM_COUNTS_ONLY) return set_error(SAME_EINVAL, "unknown flags");
+    if (!aligned(slots, kAlign)) return set_error(SAME_EALIGN, "slots must be 256-byte aligned");
+    const int64_t M = n_cols > 0 ? (n_cols + nb - 1) / nb : 0;
+    if ((double)M * (double)pass_id + M > 4294967295.0)
+        return set_error(SAME_ESIZE, "pass_id * minibatches exceeds the update-id range");
+    return SAME_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int same_stream_pass(same_ctx *ctx, void *host_states, const uint8_t *host_obs, int64_t host_ld,
+                     int64_t n_cols, int64_t nb, int32_t m, float *cpts, int32_t *mb_counts,
+                     int32_t *totals, uint64_t seed, uint32_t pass_id, int32_t flags, void *slots,
+                     void *workspace, void *stream) {
+    int rc = check_stream_args(ctx, host_states, host_obs, host_ld, n_cols, nb, m, cpts, mb_counts, totals,
+                               pass_id, flags, slots, workspace);
+    if (rc || n_cols == 0) return rc;
+    const int64_t M = (n_cols + nb - 1) / nb;
+    const int64_t total = ctx->g.off[ctx->g.n];
+    const bool counts_only = (flags & SAME_STREAM_COUNTS_ONLY) != 0;
+    return stream_pass_impl(
+        ctx, host_states, host_obs, host_ld, n_cols, nb, m, slots, stream, !counts_only,
+        [&](int64_t b, void *d_states, uint8_t *d_obs, int64_t cols, int64_t c0, int64_t ld) {
+            int32_t *mb = mb_counts + b * total;
+            if (counts_only) return same_counts(ctx, d_states, m, cols, ld, mb, totals, workspace, stream);
+            return do_step(ctx, d_states, d_obs, cpts, m, cols, ld, c0, seed, pass_id, mb, totals,
+                           (uint32_t)(pass_id * M + b), workspace, stream);
+        });
+}
+
+int same_counts_ema(same_ctx *ctx, const void *states, int32_t m, int64_t n_cols, int64_t ld, double decay,
+                    double *totals, void *workspace, void *stream) {
+    int rc = check_minibatch(ctx, states, m, n_cols, ld);
+    if (rc) return rc;
+    if (!totals || !workspace) return set_error(SAME_EINVAL, "totals and workspace must be non-null");
+    if (!(decay >= 0.0 && decay <= 1.0)) return set_error(SAME_EINVAL, "decay must be in [0, 1]");
+    if (!aligned(workspace, kAlign)) return set_error(SAME_EALIGN, "workspace must be 256-byte aligned");
+    if (!aligned(totals, 8)) return set_error(SAME_EALIGN, "totals must be 8-byte aligned");
+    if ((double)n_cols * (double)m >= 2147483648.0)
+        return set_error(SAME_ESIZE, "n_cols * m must stay below 2^31");
+    same::DeviceTables *t = nullptr;
+    rc = tables_for_current_device(ctx, &t);
+    if (rc) return rc;
+    hipStream_t s = (hipStream_t)stream;
+    const int64_t total = ctx->g.off[ctx->g.n];
+    int32_t *newc = (int32_t *)((char *)workspace + ctx->ws_counts);
+    rc = check_hip(same::launch_fill_zero(newc, total, s), "count clear launch");
+    if (rc) return rc;
+    rc = check_hip(same::launch_counts(*t, states, ctx->g.state_bytes, ctx->g.n, m, n_cols, ld, newc, s),
+                   "count launch");
+    if (rc) return rc;
+    return check_hip(same::launch_ema(newc, totals, decay, total, s), "moving-sum launch");
+}
+
+int same_sample_cpts_ema(same_ctx *ctx, const double *totals, float *cpts_out, uint64_t seed, uint32_t update_id,
+                         void *workspace, void *stream) {
+    if (!ctx || !totals || !cpts_out || !workspace)
+        return set_error(SAME_EINVAL, "ctx, totals, cpts_out and workspace must be non-null");
+    if (!aligned(workspace, kAlign)) return set_error(SAME_EALIGN, "workspace must be 256-byte aligned");
+    same::DeviceTables *t = nullptr;
+    int rc = tables_for_current_device(ctx, &t);
+    if (rc) return rc;
+    hipStream_t s = (hipStream_t)stream;
+    const int64_t total = ctx->g.off[ctx->g.n];
+    double *gv = (double *)((char *)workspace + ctx->ws_gamma);
+    rc = check_hip(same::launch_gamma(totals, ctx->alpha, (uint32_t)seed, (uint32_t)(seed >> 32), update_id,
+                                      gv, total, s),
+                   "gamma launch");
+    if (rc) return rc;
+    return check_hip(same::launch_normalize(*t, gv, cpts_out, ctx->g.n_rows, s), "normalize launch");
+}
+
+int same_stream_pass_ema(same_ctx *ctx, void *host_states, const uint8_t *host_obs, int64_t host_ld,
+                         int64_t n_cols, int64_t nb, int32_t m, float *cpts, double *totals, double decay,
+                         uint64_t seed, uint32_t pass_id, int32_t flags, void *slots, void *workspace,
+                         void *stream) {
+    int rc = check_stream_args(ctx, host_states, host_obs, host_ld, n_cols, nb, m, cpts, totals, totals, pass_id,
+                               flags, slots, workspace);
+    if (rc || n_cols == 0) return rc;
+    if (!(decay >= 0.0 && decay <= 1.0)) return set_error(SAME_EINVAL, "decay must be in [0, 1]");
+    const int64_t M = (n_cols + nb - 1) / nb;
+    const bool counts_only = (flags & SAME_STREAM_COUNTS_ONLY) != 0;
+    return stream_pass_impl(
+        ctx, host_states, host_obs, host_ld, n_cols, nb, m, slots, stream, !counts_only,
+        [&](int64_t b, void *d_states, uint8_t *d_obs, int64_t cols, int64_t c0, int64_t ld) {
+            if (!counts_only) {
+                int r2 = do_sweep(ctx, d_states, d_obs, cpts, m, cols, ld, c0, seed, pass_id, 0, 0, nullptr,
+                                  workspace, stream);
+                if (r2) return r2;
+            }
+            int r2 = same_counts_ema(ctx, d_states, m, cols, ld, decay, totals, workspace, stream);
+            if (r2 || counts_only) return r2;
+            return same_sample_cpts_ema(ctx, totals, cpts, seed, (uint32_t)(pass_id * M + b), workspace, stream);
+        });
 }
 
 }  // extern "C"

@@ -1096,11 +1096,23 @@ __device__ double gamma_mt(double a, uint32_t e, uint32_t q, uint32_t k0, uint32
     return d;
 }
 
-__global__ void gamma_kernel(const int32_t *__restrict__ totals, double alpha, uint32_t k0,
-                             uint32_t k1, uint32_t update_id, double *__restrict__ g, int64_t total) {
+template <typename T>
+__global__ void gamma_kernel(const T *__restrict__ totals, double alpha, uint32_t k0, uint32_t k1,
+                             uint32_t update_id, double *__restrict__ g, int64_t total) {
     const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (e >= total) return;
     g[e] = gamma_mt(alpha + (double)totals[e], (uint32_t)e, update_id, k0, k1);
+}
+
+// Exponential moving sum of the counts (Sec. 4, for datasets whose
+// per-minibatch counts are not kept): totals = decay * totals + new, in fp64
+// with the product rounded before the sum.
+__global__ void ema_kernel(const int32_t *__restrict__ newc, double *__restrict__ totals, double decay,
+                           int64_t total) {
+#pragma clang fp contract(off)
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+         e += (int64_t)gridDim.x * blockDim.x)
+        totals[e] = decay * totals[e] + (double)newc[e];
 }
 
 __global__ void normalize_kernel(const int32_t *__restrict__ row_off, const int32_t *__restrict__ row_k,
@@ -1408,11 +1420,30 @@ hipError_t launch_moving_sum(const int32_t *newc, int32_t *mb, int32_t *totals, 
     return hipGetLastError();
 }
 
+template <typename T>
+hipError_t launch_gamma_t(const T *totals, double alpha, uint32_t key0, uint32_t key1, uint32_t update_id,
+                          double *g, int64_t total, hipStream_t stream) {
+    if (total <= 0) return hipSuccess;
+    hipLaunchKernelGGL(dev::gamma_kernel<T>, dim3(blocks_for(total, dev::kBlock)), dim3(dev::kBlock), 0, stream,
+                       totals, alpha, key0, key1, update_id, g, total);
+    return hipGetLastError();
+}
+
 hipError_t launch_gamma(const int32_t *totals, double alpha, uint32_t key0, uint32_t key1,
                         uint32_t update_id, double *g, int64_t total, hipStream_t stream) {
+    return launch_gamma_t(totals, alpha, key0, key1, update_id, g, total, stream);
+}
+
+hipError_t launch_gamma(const double *totals, double alpha, uint32_t key0, uint32_t key1,
+                        uint32_t update_id, double *g, int64_t total, hipStream_t stream) {
+    return launch_gamma_t(totals, alpha, key0, key1, update_id, g, total, stream);
+}
+
+hipError_t launch_ema(const int32_t *newc, double *totals, double decay, int64_t total, hipStream_t stream) {
     if (total <= 0) return hipSuccess;
-    hipLaunchKernelGGL(dev::gamma_kernel, dim3(blocks_for(total, dev::kBlock)), dim3(dev::kBlock), 0,
-                       stream, totals, alpha, key0, key1, update_id, g, total);
+    unsigned nb = blocks_for(total, dev::kBlock);
+    if (nb > 4096) nb = 4096;
+    hipLaunchKernelGGL(dev::ema_kernel, dim3(nb), dim3(dev::kBlock), 0, stream, newc, totals, decay, total);
     return hipGetLastError();
 }
 

@@ -94,6 +94,11 @@ hipError_t launch_moving_sum(const int32_t *newc, int32_t *mb, int32_t *totals, 
 
 hipError_t launch_gamma(const int32_t *totals, double alpha, uint32_t key0, uint32_t key1,
                         uint32_t update_id, double *g, int64_t total, hipStream_t stream);
+hipError_t launch_gamma(const double *totals, double alpha, uint32_t key0, uint32_t key1,
+                        uint32_t update_id, double *g, int64_t total, hipStream_t stream);
+
+// Exponential moving sum: totals = decay * totals + newc (fp64).
+hipError_t launch_ema(const int32_t *newc, double *totals, double decay, int64_t total, hipStream_t stream);
 
 hipError_t launch_normalize(const DeviceTables &t, const double *g, float *cpts, int64_t n_rows,
                             hipStream_t stream);
