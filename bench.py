@@ -51,6 +51,8 @@ def parse():
                         "kernels run on the GPU, for counter collection)")
     p.add_argument("--table-limit", type=int, default=None,
                    help="threshold-table size limit passed to same_create_ex (0: products only)")
+    p.add_argument("--no-m-study", action="store_true",
+                   help="skip the KL_avg-vs-time study of the SAME replication factor (two-layer network)")
     p.add_argument("--no-heldout", action="store_true",
                    help="skip the held-out prediction run (two-layer network) and the hit-count timing")
     p.add_argument("--no-ingest", action="store_true",
@@ -169,6 +171,7 @@ def main():
 
     ingest = None if args.no_ingest else ingest_timing(w, ctx, mbs[0], dev, stream)
     heldout = None if args.no_heldout else heldout_timing(w, ctx, mbs[0], dev, stream)
+    m_study = None if args.no_m_study else m_study_run(dev, stream)
 
     streamed = None
     if not args.no_stream and len(mbs) == w.M:
@@ -214,6 +217,7 @@ def main():
         "streamed_from_host": streamed,
         "ingest": ingest,
         "heldout": heldout,
+        "m_study": m_study,
         "table_nodes": ctx.table_nodes,
     }
     print(json.dumps(out), flush=True)
@@ -522,6 +526,75 @@ def heldout_timing(w, ctx, b, dev, stream, train_steps=60, pred_sweeps=20):
         "hits_kernel": {"ms": round(t_hits, 4), "algorithmic_bytes": b_hits, "gbs": round(b_hits / t_hits / 1e6, 1),
                         "frac": round(b_hits / t_hits / 1e6 / HBM_PEAK_GBS, 4)},
     }
+
+
+def m_study_run(dev, stream):
+    """KL_avg-vs-time studies of the SAME replication factor (m_study_cfg) on
+    the student network (identifiable: every node is observed half the time)
+    and on the two-layer network (its concepts are never observed, so their
+    states may swap labels and KL_avg against the generating CPTs need not
+    fall)."""
+    return {"student-100k": m_study_cfg(2, dev, stream), "concepts30-items300-4k": m_study_cfg(4, dev, stream)}
+
+
+def m_study_cfg(cfg, dev, stream, steps=200, checkpoints=(10, 25, 50, 100, 150, 200)):
+    """KL_avg (Sec. 5.1) of the sampled CPTs against the generator's true CPTs
+    as a function of device time on workload cfg (Secs. 5.1 and 6 plot KL_avg
+    against passes and time for m = 1, 2, 5, 20), for fixed m and for an
+    annealed run (Sec. 3: m raised during sampling,
+    here 1 -> 2 -> 5 -> 20 at equal step intervals with same_grow_replicas and
+    a recount).  Each run takes `steps` SAME steps from the same start."""
+    import numpy as np
+    import torch
+
+    import paper_1511_06416_amd as same
+    from paper_1511_06416_amd import evaluate
+    from workloads import make_workload
+
+    base = make_workload(cfg, m=1, device=dev)
+    net = base.net
+    pptr, pidx, card = net.csr()
+    ctx = same.same_create(pptr, pidx, card, base.alpha)
+    ws = ctx.new_workspace(dev)
+    off = ctx.cpt_off
+    ld, nc = base.ld, base.n_cols
+
+    def run(schedule):
+        m = schedule(0)
+        st = base.states[0][:, :1, :].expand(-1, m, -1).contiguous() if m > 1 else base.states[0].clone()
+        cpts = torch.from_numpy(base.init_theta).to(dev)
+        mb = torch.zeros(ctx.cpt_total, dtype=torch.int32, device=dev)
+        tot = torch.zeros(ctx.cpt_total, dtype=torch.int32, device=dev)
+        same.same_init_latent(ctx, st, base.obs[0], m, nc, ld, 0, base.seed + 3)
+        same.same_counts(ctx, st, m, nc, ld, mb, tot, ws)
+        out, t_ms = [], 0.0
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        for s in range(steps):
+            e0.record(stream)
+            m2 = schedule(s)
+            if m2 != m:  # anneal: more replicas, then the counts over all of them
+                grown = torch.empty((net.n, m2, ld), dtype=st.dtype, device=dev)
+                same.same_grow_replicas(ctx, st, m, grown, m2, ld)
+                st, m = grown, m2
+                mb.zero_()
+                tot.zero_()
+                same.same_counts(ctx, st, m, nc, ld, mb, tot, ws)
+            same.same_step(ctx, st, base.obs[0], cpts, m, nc, ld, 0, base.seed, s, mb, tot, s, ws)
+            e1.record(stream)
+            e1.synchronize()
+            t_ms += e0.elapsed_time(e1)
+            if s + 1 in checkpoints:
+                kl = evaluate.kl_avg(base.true_theta, cpts.cpu().numpy(), off, net.card)
+                out.append({"step": s + 1, "device_ms": round(t_ms, 2), "m": m, "kl_avg": round(kl, 5)})
+        return out
+
+    res = {}
+    for m in (1, 2, 5, 20):
+        res["m=%d" % m] = run(lambda s, m=m: m)
+    res["annealed 1-2-5-20"] = run(lambda s: (1, 2, 5, 20)[min(3, s * 4 // steps)])
+    ctx.close()
+    return {"workload": "%s, %d columns, %.0f%% hidden; KL_avg against the generating CPTs" % (
+        base.name, nc, 100 * base.hidden), "runs": res}
 
 
 def stream_timing(w, ctx, cpts, ws, dev, steps):

@@ -341,6 +341,21 @@ int same_predict(same_ctx *ctx, void *states, const uint8_t *obs, const float *c
                  void *workspace, void *stream);
 
 /*
+ * SAME annealing (Sec. 3: the replication factor m acts as a temperature and
+ * can be raised during sampling to anneal the sampler): copies states
+ * [n][m][ld] into dst [n][m2][ld], m2 >= m.  Replica r < m is copied and
+ * replica r >= m starts as a copy of replica r mod m, a valid state of the
+ * enlarged SAME joint (every copy agrees with the known data).  All ld columns
+ * are copied.  After growing, the counts of the minibatch must be recomputed
+ * over the m2 replicas (same_counts with zeroed previous counts, or the
+ * count-only pre-pass).  Device pointers owned by the caller; states and dst
+ * must not overlap.  Errors: SAME_EINVAL (null, m2 < m, overlap), SAME_EALIGN,
+ * SAME_ESIZE, SAME_EHIP.
+ */
+int same_grow_replicas(same_ctx *ctx, const void *states, int32_t m, void *dst, int32_t m2, int64_t ld,
+                       void *stream);
+
+/*
  * Measurement of the sweep kernels.  same_kernel_timing(ctx, 1) clears the
  * totals and makes every later sweep of ctx bracket each of its kernel
  * launches with a pair of HIP events on the launch stream; (ctx, 0) clears

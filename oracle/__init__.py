@@ -95,6 +95,8 @@ def lib():
             L.oracle_dirichlet_f64.restype = C.c_int
             L.oracle_ema.argtypes = [C.c_int64, C.c_double, P, P]
             L.oracle_ema.restype = None
+            L.oracle_grow_replicas.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.c_int64, C.c_int32, P, P]
+            L.oracle_grow_replicas.restype = C.c_int
             _lib = L
         return _lib
 
@@ -328,3 +330,14 @@ def dirichlet_f64(parents, card, totals, alpha, seed, update_id, want_gamma=Fals
     _check(lib().oracle_dirichlet_f64(len(card), _ptr(pptr), _ptr(pidx), _ptr(card), _ptr(tot), float(alpha),
                                       int(seed), int(update_id), _ptr(theta), _ptr(gv)))
     return (theta, gv) if want_gamma else theta
+
+
+def grow_replicas(states, m2):
+    """SAME annealing (Sec. 3): states [n][m][ld] -> [n][m2][ld]; replica r >= m
+    starts as a copy of replica r mod m."""
+    n, m, ld = states.shape
+    src = np.ascontiguousarray(states)
+    out = np.zeros((n, m2, ld), dtype=states.dtype)
+    _check(lib().oracle_grow_replicas(int(n), int(m), int(m2), int(ld), states.dtype.itemsize, _ptr(src),
+                                      _ptr(out)))
+    return out

@@ -733,3 +733,24 @@ void oracle_ema(int64_t total, double decay, const int64_t *newc, double *totals
         totals[e] = p + (double)newc[e];
     }
 }
+
+/* ------------------------------------------------------------------ */
+/* SAME annealing (Sec. 3): more replicas as the sampler proceeds.      */
+/* ------------------------------------------------------------------ */
+
+/*
+ * The replication factor acts as a temperature that can be raised during
+ * sampling (Sec. 3).  dst [n][m2][ld] (m2 >= m) takes replica r of states
+ * [n][m][ld] for r < m, and a copy of replica r mod m for r >= m (a valid
+ * state of the enlarged SAME joint: every copy of a column agrees with its
+ * known data).  All ld columns are copied.
+ */
+int oracle_grow_replicas(int32_t n, int32_t m, int32_t m2, int64_t ld, int32_t state_bytes, const void *states,
+                         void *dst) {
+    if (n <= 0 || m < 1 || m2 < m || ld < 0 || (state_bytes != 1 && state_bytes != 2)) return OR_EINVAL;
+    for (int32_t i = 0; i < n; ++i)
+        for (int32_t r = 0; r < m2; ++r)
+            memcpy((char *)dst + ((int64_t)i * m2 + r) * ld * state_bytes,
+                   (const char *)states + ((int64_t)i * m + r % m) * ld * state_bytes, (size_t)ld * state_bytes);
+    return OR_OK;
+}

@@ -21,6 +21,7 @@ __all__ = [
     "same_step", "same_sweep_plan", "same_stream_slots_size", "same_stream_pass", "SAME_STREAM_COUNTS_ONLY",
     "same_kernel_timing", "same_kernel_times", "same_expand_observed", "same_init_latent",
     "same_accumulate_hits", "same_predict", "same_counts_ema", "same_sample_cpts_ema", "same_stream_pass_ema",
+    "same_grow_replicas",
     "library_path", "load_library",
 ]
 
@@ -91,6 +92,7 @@ def load_library():
         L.same_init_latent.argtypes = [P, P, P, I32, I64, I64, I64, U64, P]
         L.same_accumulate_hits.argtypes = [P, P, P, I32, I64, I64, P, P]
         L.same_counts_ema.argtypes = [P, P, I32, I64, I64, C.c_double, P, P, P]
+        L.same_grow_replicas.argtypes = [P, P, I32, P, I32, I64, P]
         L.same_sample_cpts_ema.argtypes = [P, P, P, U64, U32, P, P]
         L.same_stream_pass_ema.argtypes = [P, P, P, I64, I64, I64, I32, P, P, C.c_double, U64, U32, I32, P, P,
                                            P]
@@ -101,8 +103,9 @@ def load_library():
                   "same_sweep_debug", "same_counts", "same_sample_cpts", "same_step", "same_sweep_plan",
                   "same_stream_slots_size", "same_stream_pass", "same_kernel_timing",
                   "same_kernel_times", "same_expand_observed", "same_init_latent",
-                  "same_accumulate_hits", "same_predict", "same_counts_ema", "same_sample_cpts_ema", "same_stream_pass_ema", "same_counts_ema", "same_sample_cpts_ema",
-                  "same_stream_pass_ema"):
+                  "same_accumulate_hits", "same_predict", "same_counts_ema", "same_sample_cpts_ema", "same_stream_pass_ema",
+    "same_grow_replicas", "same_counts_ema", "same_sample_cpts_ema",
+                  "same_stream_pass_ema", "same_grow_replicas"):
             getattr(L, f).restype = C.c_int
         _lib = L
         return L
@@ -323,3 +326,8 @@ def same_stream_pass_ema(ctx, host_states, host_obs, host_ld, n_cols, nb, m, cpt
                                                int(n_cols), int(nb), int(m), _ptr(cpts), _ptr(totals),
                                                float(decay), int(seed), int(pass_id), int(flags), _ptr(slots),
                                                _ptr(workspace), _stream(stream)))
+
+
+def same_grow_replicas(ctx, states, m, dst, m2, ld, stream=None):
+    _check(load_library().same_grow_replicas(ctx.handle, _ptr(states), int(m), _ptr(dst), int(m2), int(ld),
+                                             _stream(stream)))

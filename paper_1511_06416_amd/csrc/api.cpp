@@ -833,6 +833,21 @@ extern "C" int same_predict(same_ctx *ctx, void *states, const uint8_t *obs, con
     return SAME_OK;
 }
 
+extern "C" int same_grow_replicas(same_ctx *ctx, const void *states, int32_t m, void *dst, int32_t m2, int64_t ld,
+                                  void *stream) {
+    int rc = check_minibatch(ctx, states, m, ld, ld);
+    if (rc) return rc;
+    rc = check_minibatch(ctx, dst, m2, ld, ld);
+    if (rc) return rc;
+    if (m2 < m) return set_error(SAME_EINVAL, "m2 must be >= m");
+    const char *a = (const char *)states, *b = (const char *)dst;
+    const size_t sb = (size_t)ctx->g.state_bytes;
+    if (a < b + (size_t)ctx->g.n * m2 * ld * sb && b < a + (size_t)ctx->g.n * m * ld * sb)
+        return set_error(SAME_EINVAL, "states and dst must not overlap");
+    return check_hip(same::launch_grow(states, m, dst, m2, ctx->g.n, ld * (int64_t)sb, (hipStream_t)stream),
+                     "replica growth launch");
+}
+
 extern "C" int same_kernel_timing(same_ctx *ctx, int32_t enable) {
     if (!ctx) return set_error(SAME_EINVAL, "null context");
     std::lock_guard<std::mutex> lock(ctx->mu);

@@ -1251,6 +1251,30 @@ __global__ __launch_bounds__(kBlock) void hits_kernel(const ST *__restrict__ sta
     *h = cur;
 }
 
+// ---------------------------------------------------------------- annealing
+
+// SAME annealing (Sec. 3: raising the replication factor during sampling):
+// dst [n][m2][ld] takes replica r < m of states [n][m][ld] and, for r >= m, a
+// copy of replica r mod m.  One thread per 16 bytes of a destination row
+// (row bytes ld * sizeof(state) are a multiple of 4; the tail of a row that is
+// not a whole 16 bytes is copied in words).
+__global__ __launch_bounds__(kBlock) void grow_kernel(const uint8_t *__restrict__ src, int32_t m, uint8_t *__restrict__ dst,
+                                                      int32_t m2, int64_t row_bytes, int64_t rows2) {
+    const int64_t per_row = (row_bytes + 15) >> 4;
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= rows2 * per_row) return;
+    const int64_t row = t / per_row, off = (t - row * per_row) * 16;
+    const int64_t i = row / m2, r = row - i * m2;
+    const uint8_t *s = src + (i * m + r % m) * row_bytes + off;
+    uint8_t *d = dst + row * row_bytes + off;
+    if (off + 16 <= row_bytes && ((reinterpret_cast<uintptr_t>(s) | reinterpret_cast<uintptr_t>(d)) & 15) == 0) {
+        *reinterpret_cast<uint4 *>(d) = *reinterpret_cast<const uint4 *>(s);
+    } else {
+        for (int64_t k = 0; k < 16 && off + k < row_bytes; k += 4)
+            *reinterpret_cast<uint32_t *>(d + k) = *reinterpret_cast<const uint32_t *>(s + k);
+    }
+}
+
 }  // namespace dev
 
 // ================================================================= launchers
@@ -1407,6 +1431,18 @@ hipError_t launch_hits(const void *states, const void *target, int32_t n, int32_
     else
         hipLaunchKernelGGL(dev::hits_kernel<int16_t>, dim3((unsigned)blocks), dim3(dev::kBlock), 0, stream,
                            (const int16_t *)states, (const int16_t *)target, n, m, n_cols, ld, hits);
+    return hipGetLastError();
+}
+
+hipError_t launch_grow(const void *src, int32_t m, void *dst, int32_t m2, int32_t n, int64_t row_bytes,
+                       hipStream_t stream) {
+    const int64_t rows2 = (int64_t)n * m2;
+    const int64_t items = rows2 * ((row_bytes + 15) / 16);
+    if (items <= 0) return hipSuccess;
+    const int64_t blocks = (items + dev::kBlock - 1) / dev::kBlock;
+    if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(dev::grow_kernel, dim3((unsigned)blocks), dim3(dev::kBlock), 0, stream,
+                       (const uint8_t *)src, m, (uint8_t *)dst, m2, row_bytes, rows2);
     return hipGetLastError();
 }
 

@@ -89,6 +89,10 @@ hipError_t launch_init_latent(const DeviceTables &t, int32_t n, int32_t m, int64
 hipError_t launch_hits(const void *states, const void *target, int32_t n, int32_t m, int64_t n_cols, int64_t ld,
                        int32_t state_bytes, int32_t *hits, hipStream_t stream);
 
+// SAME annealing: dst [n][m2] rows from src [n][m] rows (replica r mod m).
+hipError_t launch_grow(const void *src, int32_t m, void *dst, int32_t m2, int32_t n, int64_t row_bytes,
+                       hipStream_t stream);
+
 hipError_t launch_moving_sum(const int32_t *newc, int32_t *mb, int32_t *totals, int64_t total,
                              hipStream_t stream);
 

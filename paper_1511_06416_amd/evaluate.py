@@ -42,3 +42,23 @@ def binary_scores(hits, target, n_samples, positive=1):
     p_true = hits[q].astype(np.float64) / float(n_samples)
     lab = target[q] == positive
     return np.where(lab, p_true, 1.0 - p_true), lab
+
+
+def kl_avg(true_theta, est_theta, cpt_off, card) -> float:
+    """KL_avg (Sec. 5.1): the mean over every CPT row (every distribution of
+    a node given one parent configuration) of sum_x p(x) log(p(x) / q(x)),
+    p the true row and q the estimated one, summing over x with q(x) > 0 (and
+    p(x) log p(x) = 0 where p(x) = 0)."""
+    p_all = np.asarray(true_theta, dtype=np.float64)
+    q_all = np.asarray(est_theta, dtype=np.float64)
+    total, rows = 0.0, 0
+    for i in range(len(card)):
+        K = int(card[i])
+        p = p_all[cpt_off[i]:cpt_off[i + 1]].reshape(-1, K)
+        q = q_all[cpt_off[i]:cpt_off[i + 1]].reshape(-1, K)
+        use = (q > 0) & (p > 0)
+        with np.errstate(divide="ignore", invalid="ignore"):
+            terms = np.where(use, p * np.log(np.where(use, p / q, 1.0)), 0.0)
+        total += terms.sum()
+        rows += p.shape[0]
+    return float(total / rows)

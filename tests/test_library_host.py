@@ -253,3 +253,16 @@ def test_ingest_argument_errors():
     assert L.same_init_latent(h, fake, fake, 2, 8, 8, 2, 1, None) == same.SAME_EALIGN
     assert L.same_init_latent(None, fake, fake, 2, 8, 8, 0, 1, None) == same.SAME_EINVAL
     ctx.close()
+
+
+def test_grow_replicas_argument_errors():
+    L = same.load_library()
+    ctx = _ctx(koller())
+    h = ctx.handle
+    P = C.c_void_p
+    a, b = P(1 << 20), P(1 << 30)
+    assert L.same_grow_replicas(h, a, 3, b, 2, 8, None) == same.SAME_EINVAL          # m2 < m
+    assert L.same_grow_replicas(h, None, 3, b, 4, 8, None) == same.SAME_EINVAL
+    assert L.same_grow_replicas(h, a, 3, P((1 << 20) + 16), 4, 8, None) == same.SAME_EINVAL  # overlap
+    assert L.same_grow_replicas(h, a, 3, b, 4, 6, None) == same.SAME_EALIGN          # ld % 4
+    ctx.close()
