@@ -155,7 +155,12 @@ int same_workspace_size(const same_ctx *ctx, size_t *bytes);
  * states [n][m][ld] (in/out), obs [n][ld], cpts [cpt_total]: device pointers.
  * col_offset and ld must be multiples of 4 and states/obs 4-byte aligned.
  * seed and sweep_id select the Philox stream.  The colour groups launch in
- * order on `stream`.
+ * order on `stream`.  Inside a group, the nodes whose tables are read from
+ * global memory (launch class 1) run on a side stream that the context keeps
+ * per device, forked from and joined back into `stream` with events, beside
+ * the group's LDS-staged launch; the call's work is still ordered on `stream`
+ * as a whole.  Sweeps issued on several streams of one context share that side
+ * stream, so their class-1 launches run in issue order.
  */
 int same_sweep(same_ctx *ctx, void *states, const uint8_t *obs, const float *cpts, int32_t m,
                int64_t n_cols, int64_t ld, int64_t col_offset, uint64_t seed, uint32_t sweep_id,
@@ -362,12 +367,19 @@ int same_grow_replicas(same_ctx *ctx, const void *states, int32_t m, void *dst, 
  * them and stops.  same_kernel_times waits for the recorded launches and
  * returns, per launch class (0: tables staged in LDS, 1: tables in global
  * memory, 2: 32-bit index path, 3: K > 16), the summed device milliseconds and
- * the number of kernel launches since timing was enabled.  Host calls; the
- * waits make them unsuitable inside a captured or latency-critical sequence.
+ * the number of kernel launches since timing was enabled, and the summed
+ * device milliseconds of the colour phases (one per colour group and column
+ * tile: from before the group's first launch to after its last, on the
+ * caller's stream).  A group's class-1 launch runs beside its class-0 launch
+ * (see same_sweep), so the per-class sums count their shared time twice and
+ * phase_ms is the sweep's own device time.  Host calls; the waits make them
+ * unsuitable inside a captured or latency-critical sequence.
  */
 typedef struct {
     double ms[4];
     int64_t launches[4];
+    double phase_ms;
+    int64_t phases;
 } same_kernel_times_t;
 
 int same_kernel_timing(same_ctx *ctx, int32_t enable);

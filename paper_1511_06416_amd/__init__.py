@@ -49,7 +49,8 @@ class _Options(C.Structure):
 
 
 class _KernelTimes(C.Structure):
-    _fields_ = [("ms", C.c_double * 4), ("launches", C.c_int64 * 4)]
+    _fields_ = [("ms", C.c_double * 4), ("launches", C.c_int64 * 4), ("phase_ms", C.c_double),
+                ("phases", C.c_int64)]
 
 
 class _Layout(C.Structure):
@@ -103,8 +104,7 @@ def load_library():
                   "same_sweep_debug", "same_counts", "same_sample_cpts", "same_step", "same_sweep_plan",
                   "same_stream_slots_size", "same_stream_pass", "same_kernel_timing",
                   "same_kernel_times", "same_expand_observed", "same_init_latent",
-                  "same_accumulate_hits", "same_predict", "same_counts_ema", "same_sample_cpts_ema", "same_stream_pass_ema",
-    "same_grow_replicas", "same_counts_ema", "same_sample_cpts_ema",
+                  "same_accumulate_hits", "same_predict", "same_counts_ema", "same_sample_cpts_ema",
                   "same_stream_pass_ema", "same_grow_replicas"):
             getattr(L, f).restype = C.c_int
         _lib = L
@@ -280,10 +280,11 @@ def same_kernel_timing(ctx, enable=True):
 
 
 def same_kernel_times(ctx):
-    """{'ms': [4 floats], 'launches': [4 ints]} per launch class since timing was enabled."""
+    """{'ms': [4 floats], 'launches': [4 ints]} per launch class since timing was
+    enabled, and the summed colour-phase time 'phase_ms' over 'phases' phases."""
     t = _KernelTimes()
     _check(load_library().same_kernel_times(ctx.handle, C.byref(t)))
-    return {"ms": list(t.ms), "launches": list(t.launches)}
+    return {"ms": list(t.ms), "launches": list(t.launches), "phase_ms": t.phase_ms, "phases": t.phases}
 
 
 def same_expand_observed(ctx, row_ptr, col_idx, values, nnz, m, n_cols, ld, states, obs, stream=None):

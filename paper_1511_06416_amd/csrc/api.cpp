@@ -34,6 +34,10 @@ struct StreamRes {
     hipEvent_t ev_up[2] = {nullptr, nullptr}, ev_comp[2] = {nullptr, nullptr},
                ev_down[2] = {nullptr, nullptr};
     bool slot_used[2] = {false, false};
+    // sweeps: a colour's global-table launch runs on `side`, beside the
+    // colour's other launches on the caller's stream (fork / join events)
+    hipStream_t side = nullptr;
+    hipEvent_t ev_fork = nullptr, ev_join = nullptr;
 };
 
 // Optional per-launch timing of the sweep kernels (same_kernel_timing).
@@ -46,6 +50,10 @@ struct KernelTiming {
     std::vector<Rec> pending;
     double ms[same::kLaunchClasses] = {};
     int64_t launches[same::kLaunchClasses] = {};
+    // colour phases: from before a colour's first launch to after its last
+    // (joined) launch, on the caller's stream; records with klass < 0
+    double phase_ms = 0.0;
+    int64_t phases = 0;
 };
 
 struct same_ctx {
@@ -150,6 +158,10 @@ void free_stream_res(StreamRes &r) {
     (void)hipSetDevice(r.device);
     if (r.up) (void)hipStreamSynchronize(r.up);
     if (r.down) (void)hipStreamSynchronize(r.down);
+    if (r.side) (void)hipStreamSynchronize(r.side);
+    if (r.ev_fork) (void)hipEventDestroy(r.ev_fork);
+    if (r.ev_join) (void)hipEventDestroy(r.ev_join);
+    if (r.side) (void)hipStreamDestroy(r.side);
     for (int i = 0; i < 2; ++i) {
         if (r.ev_up[i]) (void)hipEventDestroy(r.ev_up[i]);
         if (r.ev_comp[i]) (void)hipEventDestroy(r.ev_comp[i]);
@@ -176,6 +188,9 @@ int stream_res_for_current_device(same_ctx *ctx, StreamRes **out) {
     nr.device = device;
     hipError_t h = hipStreamCreateWithFlags(&nr.up, hipStreamNonBlocking);
     if (h == hipSuccess) h = hipStreamCreateWithFlags(&nr.down, hipStreamNonBlocking);
+    if (h == hipSuccess) h = hipStreamCreateWithFlags(&nr.side, hipStreamNonBlocking);
+    if (h == hipSuccess) h = hipEventCreateWithFlags(&nr.ev_fork, hipEventDisableTiming);
+    if (h == hipSuccess) h = hipEventCreateWithFlags(&nr.ev_join, hipEventDisableTiming);
     for (int i = 0; i < 2 && h == hipSuccess; ++i) {
         h = hipEventCreateWithFlags(&nr.ev_up[i], hipEventDisableTiming);
         if (h == hipSuccess) h = hipEventCreateWithFlags(&nr.ev_comp[i], hipEventDisableTiming);
@@ -286,27 +301,59 @@ int sweep_tile(same_ctx *ctx, const same::SweepParams &P0, int64_t t0, int64_t n
     P.n_cols = nt;
     P.col_offset = P0.col_offset + t0;
     P.win_begin = P0.win_begin - t0;
+    StreamRes *sr = nullptr;
+    int rc = stream_res_for_current_device(ctx, &sr);
+    if (rc) return rc;
     const int32_t L = same::kLaunchClasses;
-    for (int32_t c = 0; c < g.n_colors; ++c)
+    for (int32_t c = 0; c < g.n_colors; ++c) {
+        // the nodes of one colour are independent: the global-table launch
+        // (bound by the texture addresser) runs beside the LDS-bound one
+        const int32_t b1 = g.launch[c * (L + 1) + 1], e1 = g.launch[c * (L + 1) + 2];
+        const bool fork = e1 > b1 && nt > 0;
+        KernelTiming::Rec phase{-1, 1, nullptr, nullptr};
+        const bool phase_timed = ctx->timing.on && nt > 0 && g.launch[c * (L + 1) + L] > g.launch[c * (L + 1)];
+        if (phase_timed) {
+            rc = check_hip(hipEventCreate(&phase.start), "hipEventCreate");
+            if (!rc) rc = check_hip(hipEventCreate(&phase.end), "hipEventCreate");
+            if (!rc) rc = check_hip(hipEventRecord(phase.start, s), "hipEventRecord");
+            if (rc) return rc;
+        }
+        if (fork) {
+            rc = check_hip(hipEventRecord(sr->ev_fork, s), "hipEventRecord");
+            if (!rc) rc = check_hip(hipStreamWaitEvent(sr->side, sr->ev_fork, 0), "hipStreamWaitEvent");
+            if (rc) return rc;
+        }
         for (int32_t k = 0; k < L; ++k) {
             const int32_t b = g.launch[c * (L + 1) + k], e = g.launch[c * (L + 1) + k + 1];
+            hipStream_t ls = (fork && k == 1) ? sr->side : s;
             KernelTiming::Rec rec{k, 1, nullptr, nullptr};
             const bool timed = ctx->timing.on && e > b && nt > 0;
             if (timed) {
-                int rc = check_hip(hipEventCreate(&rec.start), "hipEventCreate");
+                rc = check_hip(hipEventCreate(&rec.start), "hipEventCreate");
                 if (!rc) rc = check_hip(hipEventCreate(&rec.end), "hipEventCreate");
-                if (!rc) rc = check_hip(hipEventRecord(rec.start, s), "hipEventRecord");
+                if (!rc) rc = check_hip(hipEventRecord(rec.start, ls), "hipEventRecord");
                 if (rc) return rc;
             }
-            int rc = check_hip(same::launch_sweep(P, b, e - b, k, g.launch_lds[c * L + k], g.state_bytes, s),
-                               "sweep launch");
+            rc = check_hip(same::launch_sweep(P, b, e - b, k, g.launch_lds[c * L + k], g.state_bytes, ls),
+                           "sweep launch");
             if (rc) return rc;
             if (timed) {
-                rc = check_hip(hipEventRecord(rec.end, s), "hipEventRecord");
+                rc = check_hip(hipEventRecord(rec.end, ls), "hipEventRecord");
                 if (rc) return rc;
                 ctx->timing.pending.push_back(rec);
             }
         }
+        if (fork) {
+            rc = check_hip(hipEventRecord(sr->ev_join, sr->side), "hipEventRecord");
+            if (!rc) rc = check_hip(hipStreamWaitEvent(s, sr->ev_join, 0), "hipStreamWaitEvent");
+            if (rc) return rc;
+        }
+        if (phase_timed) {
+            rc = check_hip(hipEventRecord(phase.end, s), "hipEventRecord");
+            if (rc) return rc;
+            ctx->timing.pending.push_back(phase);
+        }
+    }
     return SAME_OK;
 }
 
@@ -318,7 +365,10 @@ int collect_timing(same_ctx *ctx) {
         float ms = 0.f;
         if (!rc) rc = check_hip(hipEventSynchronize(r.end), "hipEventSynchronize");
         if (!rc) rc = check_hip(hipEventElapsedTime(&ms, r.start, r.end), "hipEventElapsedTime");
-        if (!rc) {
+        if (!rc && r.klass < 0) {
+            t.phase_ms += ms;
+            t.phases += r.launches;
+        } else if (!rc) {
             t.ms[r.klass] += ms;
             t.launches[r.klass] += r.launches;
         }
@@ -857,6 +907,8 @@ extern "C" int same_kernel_timing(same_ctx *ctx, int32_t enable) {
         ctx->timing.ms[k] = 0.0;
         ctx->timing.launches[k] = 0;
     }
+    ctx->timing.phase_ms = 0.0;
+    ctx->timing.phases = 0;
     return rc;
 }
 
@@ -868,5 +920,7 @@ extern "C" int same_kernel_times(same_ctx *ctx, same_kernel_times_t *out) {
         out->ms[k] = ctx->timing.ms[k];
         out->launches[k] = ctx->timing.launches[k];
     }
+    out->phase_ms = ctx->timing.phase_ms;
+    out->phases = ctx->timing.phases;
     return rc;
 }

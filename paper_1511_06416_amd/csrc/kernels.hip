@@ -979,10 +979,14 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
             const int nr = m - r0 < kCountReps ? m - r0 : kCountReps;
             uint32_t boff[kCountReps];
             typename Q::V own[kCountReps];
+            // every slot loads (a fixed count keeps all loads in flight at
+            // once); slots past the last replica read through the node's
+            // buffer resource past its end, which returns 0 without a memory
+            // access, and their values are never used
 #pragma unroll
             for (int t = 0; t < kCountReps; ++t) {
                 boff[t] = (uint32_t)((r0 + t) * ld + col) * (uint32_t)sizeof(ST);
-                if (t < nr) own[t] = load_row<ST>(states, node, vstride, boff[t]);
+                own[t] = load_row<ST>(states, node, vstride, boff[t]);
             }
             if (packed) {
                 // bin = sum over parents of x_p * (stride_p * K) + x_node
@@ -994,7 +998,7 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
                     typename Q::V sp[kCountReps];
 #pragma unroll
                     for (int t = 0; t < kCountReps; ++t)
-                        if (t < nr) sp[t] = load_row<ST>(states, par[2 * q], vstride, boff[t]);
+                        sp[t] = load_row<ST>(states, par[2 * q], vstride, boff[t]);
 #pragma unroll
                     for (int t = 0; t < kCountReps; ++t) {
                         if (t >= nr) break;
@@ -1022,7 +1026,7 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
                     typename Q::V sp[kCountReps];
 #pragma unroll
                     for (int t = 0; t < kCountReps; ++t)
-                        if (t < nr) sp[t] = load_row<ST>(states, par[2 * q], vstride, boff[t]);
+                        sp[t] = load_row<ST>(states, par[2 * q], vstride, boff[t]);
 #pragma unroll
                     for (int t = 0; t < kCountReps; ++t) {
                         if (t >= nr) break;

@@ -71,11 +71,14 @@ def test_sweep_parity_configs(cfg, kw, win, table_limit):
     (4, {}, (0, 600)),
     (5, dict(n_cols=3_000, m=4), (2_600, 400)),
 ])
-@pytest.mark.parametrize("variant", [dict(lds_limit=0), dict(packed=False), dict(lds_limit=0, packed=False)],
-                         ids=["global-tables", "wide-indices", "global-wide"])
+@pytest.mark.parametrize("variant", [dict(lds_limit=0), dict(lds_limit=1024), dict(packed=False),
+                                     dict(lds_limit=0, packed=False)],
+                         ids=["global-tables", "mixed-tables", "wide-indices", "global-wide"])
 def test_sweep_parity_kernel_classes(cfg, kw, win, variant):
     """The same conditionals and draws when every table is read from global
-    memory and/or every product-mode node takes the 32-bit index kernel."""
+    memory, when a colour's nodes split between LDS-staged and global tables
+    (two concurrent launches per colour), and/or every product-mode node takes
+    the 32-bit index kernel."""
     w = make_workload(cfg, **kw)
     out = _sweep_case(w, win=win, **variant)
     assert out["probs"]["checked"] > 0
@@ -424,3 +427,21 @@ def test_independent_loops_agree_until_first_flagged_draw():
             print("CPTs differ in the last bit at sweep", s)
             return
     print("identical over all", w.sweeps, "sweeps")
+
+
+def test_kernel_timing_counts_launches_and_phases():
+    """With timing on, every launch of a sweep is counted in its class and every
+    colour group in one phase; the phase time covers the group's launches."""
+    w = make_workload(5, n_cols=3_000, m=2)
+    net = w.net
+    ctx = H.context_for(net, lds_limit=1024)
+    lay = same.same_layout(ctx)
+    same.same_kernel_timing(ctx, True)
+    H.gpu_sweep(ctx, w.states[0].numpy(), w.obs[0].numpy(), w.init_theta, w.m, 3_000, 0, w.seed, 3)
+    kt = same.same_kernel_times(ctx)
+    same.same_kernel_timing(ctx, False)
+    assert sum(kt["launches"]) == lay["sweep_launches"]
+    assert kt["launches"][0] > 0 and kt["launches"][1] > 0
+    assert kt["phases"] == lay["n_colors"]
+    assert kt["phase_ms"] > 0.0
+    assert same.same_kernel_times(ctx) == {"ms": [0.0] * 4, "launches": [0] * 4, "phase_ms": 0.0, "phases": 0}
