@@ -275,13 +275,16 @@ def measured_traffic(cfg):
 
 
 def sweep_roofline(w, net, mbs, hidden, node_samples, kt, elapsed, args):
-    """Roofline of the dominant kernel (the fast sweep kernel, both variants):
-    algorithmic bytes per second against HBM peak; beside it, algorithmic 32-bit
-    operations per second against the VALU peak, and the HBM bytes the counters
-    measured per launch (when taken on the current kernel sources)."""
+    """Roofline of the dominant kernel, the LDS-staged sweep kernel
+    (sweep_fast_kernel<int8, false, true>, launch class 0), which draws almost
+    every node of the workload in one launch per colour group: the algorithmic
+    bytes of the (node, column, replica) slots its launches covered per second
+    of its own launch time, against HBM peak.  Beside it: algorithmic 32-bit
+    operations per second against the VALU peak, the HBM bytes the counters
+    measured per launch (when taken on the current kernel sources), the
+    global-table launches (class 1, beside class 0 on a second stream) and the
+    colour phases (the sweep's own device time, all classes)."""
     import numpy as np
-    fast_ms = kt["ms"][0] + kt["ms"][1]
-    fast_launches = kt["launches"][0] + kt["launches"][1]
     assert kt["launches"][2] == 0 and kt["launches"][3] == 0, \
         "this workload is expected to run entirely in the fast sweep kernel"
     bytes_per_ns = 1.0 + hidden + 1.0 / w.m   # read each state, write each latent, obs per column
@@ -291,38 +294,46 @@ def sweep_roofline(w, net, mbs, hidden, node_samples, kt, elapsed, args):
     for b in mbs:
         lat += (w.obs[b][:, :w.mb_cols(b)] == 0).sum(dim=1).cpu().numpy().astype(np.float64)
     ops = float((alu_ops_per_draw(net) * lat).sum()) * w.m * args.steps
-    secs = fast_ms / 1e3
-    hbm = alg_bytes / secs / 1e9
-    alu = ops / secs / 1e12
+    ms0, n0, ns0 = kt["ms"][0], kt["launches"][0], kt["node_samples"][0]
+    bytes0 = ns0 * bytes_per_ns
+    ops0 = ops * ns0 / node_samples   # at the workload's mean operations per slot
+    secs0 = ms0 / 1e3
+    hbm = bytes0 / secs0 / 1e9
+    alu = ops0 / secs0 / 1e12
     traffic = measured_traffic(args.cfg)
-    avg_ms = fast_ms / fast_launches
+    avg_ms = ms0 / n0
+    phase_s = kt["phase_ms"] / 1e3
     out = {
-        "kernel": "sweep_fast_kernel (LDS-staged and global-table variants; every launch of the timed passes)",
+        "kernel": "sweep_fast_kernel<int8, false, true> (tables staged in LDS, whole or in part; "
+                  "every launch of the timed passes)",
         "bound": "hbm",
         "achieved": round(hbm, 1),
         "peak": HBM_PEAK_GBS,
         "unit": "GB/s",
         "frac": round(hbm / HBM_PEAK_GBS, 4),
         "traffic": None if traffic is None else traffic["hbm_bytes_per_launch"],
-        "algorithmic_bytes_per_launch": round(alg_bytes / fast_launches, 1),
+        "algorithmic_bytes_per_launch": round(bytes0 / n0, 1),
         "bytes_per_node_sample": round(bytes_per_ns, 4),
-        "launches": fast_launches,
+        "node_samples_share": round(ns0 / node_samples, 4),
+        "launches": n0,
         "avg_launch_ms": round(avg_ms, 4),
         "alu": {"achieved": round(alu, 3), "peak": round(ALU_PEAK_TOPS, 2), "unit": "TOP/s",
                 "frac": round(alu / ALU_PEAK_TOPS, 4),
-                "algorithmic_ops_per_launch": round(ops / fast_launches, 1)},
-        # each colour's class-1 launch overlaps its class-0 launch (side stream),
-        # so the launch durations above include shared time; the colour phases
-        # (first launch to joined last launch of a colour) are the sweep's own
-        # device time
+                "algorithmic_ops_per_launch": round(ops0 / n0, 1)},
+        "global_table_launches": {
+            "launches": kt["launches"][1], "ms": round(kt["ms"][1], 3),
+            "node_samples_share": round(kt["node_samples"][1] / node_samples, 4)},
+        # class-1 launches run beside the class-0 launch of their colour (side
+        # stream); the colour phases (first launch to joined last launch of a
+        # colour) are the sweep's own device time
         "colour_phases": {
             "phases": int(kt["phases"]),
             "ms": round(kt["phase_ms"], 3),
-            "achieved": round(alg_bytes / (kt["phase_ms"] / 1e3) / 1e9, 1) if kt["phase_ms"] > 0 else None,
-            "frac": round(alg_bytes / (kt["phase_ms"] / 1e3) / 1e9 / HBM_PEAK_GBS, 4) if kt["phase_ms"] > 0 else None,
-            "alu_frac": round(ops / (kt["phase_ms"] / 1e3) / 1e12 / ALU_PEAK_TOPS, 4) if kt["phase_ms"] > 0 else None,
+            "achieved": round(alg_bytes / phase_s / 1e9, 1) if phase_s > 0 else None,
+            "frac": round(alg_bytes / phase_s / 1e9 / HBM_PEAK_GBS, 4) if phase_s > 0 else None,
+            "alu_frac": round(ops / phase_s / 1e12 / ALU_PEAK_TOPS, 4) if phase_s > 0 else None,
         },
-        "sweep_share_of_step": round(kt["phase_ms"] / 1e3 / elapsed, 3),
+        "sweep_share_of_step": round(phase_s / elapsed, 3),
     }
     if traffic is not None:
         out["traffic_gbs"] = round(traffic["hbm_bytes_per_launch"] / (avg_ms / 1e3) / 1e9, 1)
@@ -367,7 +378,7 @@ def counters_summary(paths, cfg):
         vals = ["-" if avg(k, c) is None else "%.4g" % avg(k, c) for c in counters]
         print("| %s | %d | %.1f | %s |" % (k[:100], len(dur[k]), sum(dur[k].values()) / len(dur[k]),
                                          " | ".join(vals)))
-    sweep = [k for k in kernels if re.search(r"sweep_fast_kernel<[^,]+, false,", k)]
+    sweep = [k for k in kernels if re.search(r"sweep_fast_kernel<[^,]+, false, true>", k)]
     # the 1 GiB device copy: the non-library dispatch whose WRITE_SIZE is 1 GiB
     # within 5%; its FETCH_SIZE is the same kernel and grid in the FETCH_SIZE run
     copy = None
@@ -392,7 +403,7 @@ def counters_summary(paths, cfg):
     fb *= f_scale
     wb *= w_scale
     out = {
-        "kernel": "sweep_fast_kernel (both variants, non-debug)",
+        "kernel": "sweep_fast_kernel<int8, false, true> (LDS-staged, non-debug)",
         "workload_cfg": cfg,
         "copy_kernel": copy[0],
         "copy_counters_kib": {"FETCH_SIZE": fetch_copy, "WRITE_SIZE": copy[2]},

@@ -107,9 +107,11 @@ typedef struct {
      * one tile = the whole minibatch).  Tiles are at least 1024 columns wide.
      * Results do not depend on it. */
     int64_t tile_bytes;
-    /* Largest per-node table record (bytes) a sweep block copies into LDS
-     * before drawing; larger records are read from global memory.  -1 selects
-     * the default (32768); 0 stages nothing.  Results do not depend on it. */
+    /* LDS staging budget of a sweep block (bytes): a node's table record up
+     * to this size is copied into LDS before drawing; a larger record stages
+     * its smallest CPT groups up to this size and reads the rest from global
+     * memory.  -1 selects the default (24576); at most 32768; 0 stages
+     * nothing.  Results do not depend on it. */
     int64_t lds_limit;
     /* 1 (default): blanket indices of nodes with K <= 8 and records below
      * 2^16 rows use packed 16-bit arithmetic; 0: every product-mode node uses
@@ -365,21 +367,23 @@ int same_grow_replicas(same_ctx *ctx, const void *states, int32_t m, void *dst, 
  * totals and makes every later sweep of ctx bracket each of its kernel
  * launches with a pair of HIP events on the launch stream; (ctx, 0) clears
  * them and stops.  same_kernel_times waits for the recorded launches and
- * returns, per launch class (0: tables staged in LDS, 1: tables in global
- * memory, 2: 32-bit index path, 3: K > 16), the summed device milliseconds and
- * the number of kernel launches since timing was enabled, and the summed
- * device milliseconds of the colour phases (one per colour group and column
- * tile: from before the group's first launch to after its last, on the
- * caller's stream).  A group's class-1 launch runs beside its class-0 launch
- * (see same_sweep), so the per-class sums count their shared time twice and
- * phase_ms is the sweep's own device time.  Host calls; the waits make them
- * unsuitable inside a captured or latency-critical sequence.
+ * returns, per launch class (0: tables staged in LDS, whole or in part, 1:
+ * tables in global memory, 2: 32-bit index path, 3: K > 16), the summed
+ * device milliseconds, the number of kernel launches and the (node, column,
+ * replica) slots those launches covered since timing was enabled, and the
+ * summed device milliseconds of the colour phases (one per colour group and
+ * column tile: from before the group's first launch to after its last, on
+ * the caller's stream).  A group's class-1 launch runs beside its class-0
+ * launch (see same_sweep), so the per-class sums count their shared time
+ * twice and phase_ms is the sweep's own device time.  Host calls; the waits
+ * make them unsuitable inside a captured or latency-critical sequence.
  */
 typedef struct {
     double ms[4];
     int64_t launches[4];
     double phase_ms;
     int64_t phases;
+    double node_samples[4];
 } same_kernel_times_t;
 
 int same_kernel_timing(same_ctx *ctx, int32_t enable);

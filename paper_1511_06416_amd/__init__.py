@@ -50,7 +50,7 @@ class _Options(C.Structure):
 
 class _KernelTimes(C.Structure):
     _fields_ = [("ms", C.c_double * 4), ("launches", C.c_int64 * 4), ("phase_ms", C.c_double),
-                ("phases", C.c_int64)]
+                ("phases", C.c_int64), ("node_samples", C.c_double * 4)]
 
 
 class _Layout(C.Structure):
@@ -280,11 +280,13 @@ def same_kernel_timing(ctx, enable=True):
 
 
 def same_kernel_times(ctx):
-    """{'ms': [4 floats], 'launches': [4 ints]} per launch class since timing was
-    enabled, and the summed colour-phase time 'phase_ms' over 'phases' phases."""
+    """{'ms': [4 floats], 'launches': [4 ints], 'node_samples': [4 floats]} per
+    launch class since timing was enabled, and the summed colour-phase time
+    'phase_ms' over 'phases' phases."""
     t = _KernelTimes()
     _check(load_library().same_kernel_times(ctx.handle, C.byref(t)))
-    return {"ms": list(t.ms), "launches": list(t.launches), "phase_ms": t.phase_ms, "phases": t.phases}
+    return {"ms": list(t.ms), "launches": list(t.launches), "phase_ms": t.phase_ms, "phases": t.phases,
+            "node_samples": list(t.node_samples)}
 
 
 def same_expand_observed(ctx, row_ptr, col_idx, values, nnz, m, n_cols, ld, states, obs, stream=None):

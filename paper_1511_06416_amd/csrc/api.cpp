@@ -3,6 +3,7 @@
 // each entry point.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdint>
 #include <cstring>
 #include <mutex>
@@ -46,10 +47,12 @@ struct KernelTiming {
     struct Rec {
         int32_t klass, launches;
         hipEvent_t start, end;
+        double node_samples;  // (node, column, replica) slots the launch covers
     };
     std::vector<Rec> pending;
     double ms[same::kLaunchClasses] = {};
     int64_t launches[same::kLaunchClasses] = {};
+    double node_samples[same::kLaunchClasses] = {};
     // colour phases: from before a colour's first launch to after its last
     // (joined) launch, on the caller's stream; records with klass < 0
     double phase_ms = 0.0;
@@ -310,7 +313,7 @@ int sweep_tile(same_ctx *ctx, const same::SweepParams &P0, int64_t t0, int64_t n
         // (bound by the texture addresser) runs beside the LDS-bound one
         const int32_t b1 = g.launch[c * (L + 1) + 1], e1 = g.launch[c * (L + 1) + 2];
         const bool fork = e1 > b1 && nt > 0;
-        KernelTiming::Rec phase{-1, 1, nullptr, nullptr};
+        KernelTiming::Rec phase{-1, 1, nullptr, nullptr, 0.0};
         const bool phase_timed = ctx->timing.on && nt > 0 && g.launch[c * (L + 1) + L] > g.launch[c * (L + 1)];
         if (phase_timed) {
             rc = check_hip(hipEventCreate(&phase.start), "hipEventCreate");
@@ -326,7 +329,7 @@ int sweep_tile(same_ctx *ctx, const same::SweepParams &P0, int64_t t0, int64_t n
         for (int32_t k = 0; k < L; ++k) {
             const int32_t b = g.launch[c * (L + 1) + k], e = g.launch[c * (L + 1) + k + 1];
             hipStream_t ls = (fork && k == 1) ? sr->side : s;
-            KernelTiming::Rec rec{k, 1, nullptr, nullptr};
+            KernelTiming::Rec rec{k, 1, nullptr, nullptr, (double)(e - b) * (double)nt * (double)P.m};
             const bool timed = ctx->timing.on && e > b && nt > 0;
             if (timed) {
                 rc = check_hip(hipEventCreate(&rec.start), "hipEventCreate");
@@ -371,6 +374,7 @@ int collect_timing(same_ctx *ctx) {
         } else if (!rc) {
             t.ms[r.klass] += ms;
             t.launches[r.klass] += r.launches;
+            t.node_samples[r.klass] += r.node_samples;
         }
         (void)hipEventDestroy(r.start);
         (void)hipEventDestroy(r.end);
@@ -472,7 +476,7 @@ int same_create_ex(int32_t n_nodes, const int32_t *parent_ptr, const int32_t *pa
     if (opts && opts->table_limit >= 0) table_limit = opts->table_limit;
     if (opts && opts->table_limit < -1) return set_error(SAME_EINVAL, "table_limit must be >= -1");
     if (opts && opts->tile_bytes < 0) return set_error(SAME_EINVAL, "tile_bytes must be >= 0");
-    int64_t lds_limit = same::kLdsBudgetBytes;
+    int64_t lds_limit = same::kDefaultLdsBytes;
     if (opts && opts->lds_limit >= 0) lds_limit = opts->lds_limit;
     if (opts && (opts->lds_limit < -1 || opts->lds_limit > same::kLdsBudgetBytes))
         return set_error(SAME_EINVAL, "lds_limit must be -1 or in [0, 32768]");
@@ -906,6 +910,7 @@ extern "C" int same_kernel_timing(same_ctx *ctx, int32_t enable) {
     for (int32_t k = 0; k < same::kLaunchClasses; ++k) {
         ctx->timing.ms[k] = 0.0;
         ctx->timing.launches[k] = 0;
+        ctx->timing.node_samples[k] = 0.0;
     }
     ctx->timing.phase_ms = 0.0;
     ctx->timing.phases = 0;
@@ -919,6 +924,7 @@ extern "C" int same_kernel_times(same_ctx *ctx, same_kernel_times_t *out) {
     for (int32_t k = 0; k < same::kLaunchClasses; ++k) {
         out->ms[k] = ctx->timing.ms[k];
         out->launches[k] = ctx->timing.launches[k];
+        out->node_samples[k] = ctx->timing.node_samples[k];
     }
     out->phase_ms = ctx->timing.phase_ms;
     out->phases = ctx->timing.phases;

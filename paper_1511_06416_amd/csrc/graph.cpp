@@ -141,40 +141,78 @@ int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int
     for (int32_t i = 0; i < n; ++i) g.groups[g.color[i]].push_back(i);
 
     // regrouped sweep tables and the segments that build them: one contiguous
-    // record per node (its own k-vectors, then one table per child), every
+    // record per node (its own k-vectors and one table per child), every
     // record and sub-table on a 64-byte boundary so that the sweep can read a
-    // group with float2/float4 loads and stage a whole record in LDS
+    // group with float2/float4 loads and stage a record in LDS.  A record
+    // larger than lds_limit puts the groups it can stage first (smallest
+    // first, up to lds_limit bytes), so that the staged part is a prefix of
+    // the record.
     g.kp.resize(n);
     g.own_off.resize(n);
     g.tab_begin.resize(n);
     g.tab_len.resize(n);
+    g.group_order.assign(n, {});
+    g.stage_groups.assign(n, 0);
+    g.stage_floats.assign(n, 0);
     auto align16 = [](int64_t v) { return (v + 15) & ~int64_t(15); };
     int64_t pos = 0;
-    std::vector<std::vector<int32_t>> ctab_of(n);  // indices into ctabs per node
+    std::vector<std::vector<int32_t>> ctab_of(n);  // indices into ctabs per node (children order)
     for (int32_t i = 0; i < n; ++i) {
         g.kp[i] = padded_k(card[i]);
+        // group sizes in floats: 0 = own rows, 1 + c = child c (kids order)
+        std::vector<int64_t> gsz;
+        gsz.push_back(align16(g.rows[i] * g.kp[i]));
+        for (auto &c : kids[i]) gsz.push_back(align16(g.rows[c.first] / card[i] * card[c.first] * g.kp[i]));
+        int64_t total = 0;
+        for (int64_t v : gsz) total += v;
+        std::vector<int32_t> &order = g.group_order[i];
+        if (total * 4 <= lds_limit) {
+            for (int32_t t = 0; t < (int32_t)gsz.size(); ++t) order.push_back(t);
+            g.stage_groups[i] = (int32_t)gsz.size();
+            g.stage_floats[i] = total;
+        } else {
+            std::vector<int32_t> by_size(gsz.size());
+            for (int32_t t = 0; t < (int32_t)gsz.size(); ++t) by_size[t] = t;
+            std::stable_sort(by_size.begin(), by_size.end(),
+                             [&](int32_t a, int32_t b) { return gsz[a] < gsz[b]; });
+            std::vector<char> staged(gsz.size(), 0);
+            int64_t cum = 0;
+            for (int32_t t : by_size) {
+                if ((cum + gsz[t]) * 4 > lds_limit) break;
+                cum += gsz[t];
+                staged[t] = 1;
+                g.stage_groups[i] += 1;
+            }
+            g.stage_floats[i] = cum;
+            for (int32_t t = 0; t < (int32_t)gsz.size(); ++t)
+                if (staged[t]) order.push_back(t);
+            for (int32_t t = 0; t < (int32_t)gsz.size(); ++t)
+                if (!staged[t]) order.push_back(t);
+        }
         pos = align16(pos);
         g.tab_begin[i] = pos;
-        g.own_off[i] = pos;
-        g.segments.push_back(Segment{pos, g.off[i], (int32_t)g.rows[i], card[i], g.kp[i], 1, 0, 1});
-        pos += g.rows[i] * g.kp[i];
-        for (auto &c : kids[i]) {
+        std::vector<int64_t> at(gsz.size());
+        for (int32_t t : order) {
+            at[t] = pos;
+            pos += gsz[t];
+        }
+        g.own_off[i] = at[0];
+        g.segments.push_back(Segment{at[0], g.off[i], (int32_t)g.rows[i], card[i], g.kp[i], 1, 0, 1});
+        for (size_t ci = 0; ci < kids[i].size(); ++ci) {
+            const auto &c = kids[i][ci];
             int32_t h = c.first;
             ChildTab t;
             t.node = i;
             t.child = h;
             t.slot = c.second;
             t.groups = g.rows[h] / card[i] * card[h];
-            pos = align16(pos);
-            t.off = pos;
+            t.off = at[ci + 1];
             int64_t s_i = g.pstride[pptr[h] + c.second];
             g.segments.push_back(
-                Segment{pos, g.off[h], (int32_t)t.groups, card[i], g.kp[i], card[h], (int32_t)s_i, 0});
-            pos += t.groups * g.kp[i];
+                Segment{t.off, g.off[h], (int32_t)t.groups, card[i], g.kp[i], card[h], (int32_t)s_i, 0});
             ctab_of[i].push_back((int32_t)g.ctabs.size());
             g.ctabs.push_back(t);
         }
-        pos = align16(pos);
         g.tab_len[i] = pos - g.tab_begin[i];
     }
     g.table_floats = pos;
@@ -277,6 +315,8 @@ int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int
         // launch class and the unit of the fast list's indices (bytes)
         int32_t klass;
         int64_t unit = 0;
+        int32_t n_staged = 0;   // fast-list groups (or the threshold table) read from LDS
+        int64_t stage_words = 0;  // words the block copies into LDS
         if (g.mode[i] == kModeGeneric) {
             klass = 3;
         } else if (g.mode[i] == kModeKP16) {
@@ -289,13 +329,20 @@ int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int
             } else if (bytes <= lds_limit) {
                 klass = 0;
                 unit = 1;
-                g.lds_bytes[i] = (int32_t)((bytes + 15) & ~int64_t(15));  // staged in float4s
+                n_staged = tab ? 1 : g.stage_groups[i];
+                stage_words = tab ? ((cond_len + 3) & ~int64_t(3)) : g.tab_len[i];
             } else if (bytes / row_bytes <= kPackedLimit) {
-                klass = 1;
+                // staged groups (if any) count bytes, the others k-vectors
                 unit = row_bytes;
+                if (!tab) {
+                    n_staged = g.stage_groups[i];
+                    stage_words = g.stage_floats[i];
+                }
+                klass = n_staged > 0 ? 0 : 1;
             } else {
                 klass = 2;  // product modes only: tables always fit 16-bit rows
             }
+            g.lds_bytes[i] = (int32_t)(stage_words * 4);  // staged in float4s
         }
         g.klass[i] = klass;
 
@@ -311,6 +358,8 @@ int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int
         g.desc[base + 6] = (int32_t)cond_len;
         g.desc[base + 7] = KT;
         g.desc[base + 12] = klass;
+        g.desc[base + 13] = n_staged;
+        g.desc[base + 14] = (int32_t)stage_words;
 
         // product-path groups in float offsets: own row, then one per child
         struct Group {
@@ -319,7 +368,7 @@ int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int
         };
         std::vector<Group> groups;
         {
-            Group own{0, {}};
+            Group own{g.own_off[i] - g.tab_begin[i], {}};
             for (int32_t a2 = pptr[i]; a2 < pptr[i + 1]; ++a2)
                 own.ent.push_back({g.pidx[a2], g.pstride[a2] * KP});
             groups.push_back(own);
@@ -339,6 +388,12 @@ int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int
             std::reverse(cops.begin(), cops.end());
             cg.ent.insert(cg.ent.end(), cops.begin(), cops.end());
             groups.push_back(cg);
+        }
+        {
+            // record order: the staged groups first
+            std::vector<Group> ordered;
+            for (int32_t t : g.group_order[i]) ordered.push_back(groups[t]);
+            groups.swap(ordered);
         }
         auto emit = [&](const Group &gr, int64_t div, bool packed) -> bool {
             auto word = [&](int64_t v) -> int64_t {
@@ -377,10 +432,12 @@ int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int
                 ok = emit(bg, unit, true);
             } else {
                 g.desc[base + 8] = (int32_t)groups.size();
-                for (auto &gr : groups) {
+                for (size_t t = 0; t < groups.size(); ++t) {
+                    const Group &gr = groups[t];
                     Group gb{gr.base * 4, {}};
                     for (auto &e : gr.ent) gb.ent.push_back({e.first, e.second * 4});
-                    ok = ok && emit(gb, unit, true);
+                    // staged groups count bytes into LDS, the rest k-vectors
+                    ok = ok && emit(gb, (int32_t)t < n_staged ? 1 : unit, true);
                 }
             }
             // the class test above bounds every index below 2^16 units

@@ -52,14 +52,19 @@ enum SweepMode : int32_t {
 };
 
 // Launch classes (one kernel each):
-//   0 fast path, the node's table record (k-vectors or thresholds) staged in
-//     LDS, packed 16-bit byte indices;
-//   1 fast path, tables read from global memory, packed 16-bit indices in
-//     units of one k-vector (or one threshold row);
+//   0 fast path with LDS staging: the node's whole table record (k-vectors
+//     or thresholds) when it fits the budget, else the record's smallest
+//     k-vector groups (a prefix of the record); staged groups are indexed in
+//     bytes, the rest are read from global memory with packed 16-bit indices
+//     in units of one k-vector;
+//   1 fast path with nothing staged (threshold tables beyond the budget, or
+//     no k-vector group that fits): packed 16-bit indices in units of one
+//     k-vector (or one threshold row);
 //   2 wide path: product modes up to KP = 16 with 32-bit float indices;
 //   3 generic path (K > 16).
 constexpr int32_t kLaunchClasses = 4;
-constexpr int64_t kLdsBudgetBytes = 32768;  // largest table staged in LDS per block
+constexpr int64_t kLdsBudgetBytes = 32768;   // largest LDS staging budget per block
+constexpr int64_t kDefaultLdsBytes = 24576;  // default budget: 6 blocks per CU (measured best)
 constexpr int32_t kDescHeader = 16;
 constexpr int64_t kPackedLimit = 65536;      // packed indices are 16-bit
 
@@ -69,6 +74,10 @@ constexpr int64_t kPackedLimit = 65536;      // packed indices are 16-bit
 //   [8] n_fast  [9] fast (relative word index of the fast group list)
 //   [10] n_wide [11] wide (relative word index of the wide group list)
 //   [12] launch class
+//   [13] staged groups: the first [13] groups of the fast list are read from
+//        LDS (byte indices), the rest from global memory; in table mode 1
+//        when the threshold table is staged
+//   [14] words a block copies into LDS before drawing (multiple of 4)
 // A group list is a sequence of groups [n_e, base, (node, mult) * n_e]; the
 // group's index is base + sum of mult * state over its entries.
 //   wide list (every node): group 0 is the node's own row (entries: its
@@ -105,6 +114,12 @@ struct Compiled {
     // per-node table records and the sweep descriptors (layout above)
     std::vector<int64_t> tab_begin, tab_len;  // [n], floats
     std::vector<int32_t> lds_bytes;           // [n], 0: tables read from global memory
+    // record layout: group_order[i] lists the groups (0 = own rows, 1 + c =
+    // child c) in record order; the first stage_groups[i] of them, of
+    // stage_floats[i] floats, are the part a block stages in LDS
+    std::vector<std::vector<int32_t>> group_order;
+    std::vector<int32_t> stage_groups;
+    std::vector<int64_t> stage_floats;
     std::vector<int32_t> desc;
     std::vector<int32_t> desc_off;   // [n]
 
@@ -141,10 +156,11 @@ struct Compiled {
 // Returns 0 or a negative SAME_E* code with a message in err.
 // table_limit: largest KT * (number of blanket configurations) for which a
 // node gets a precomputed threshold table (0 disables the table path).
-// lds_limit: largest table record (bytes) staged in LDS (class 0).
+// lds_limit: LDS staging budget per block in bytes (class 0): the largest
+// record staged whole, and the most a larger record stages of its groups.
 // packed: false sends every product-mode node to the wide class.
 int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int32_t *card,
                   Compiled &out, std::string &err, int64_t table_limit = 16384,
-                  int64_t lds_limit = kLdsBudgetBytes, bool packed = true);
+                  int64_t lds_limit = kDefaultLdsBytes, bool packed = true);
 
 }  // namespace same

@@ -26,6 +26,7 @@ typedef const __attribute__((address_space(4))) int32_t cint32_t;
 __device__ __forceinline__ cint32_t *as_const(const int32_t *p) { return (cint32_t *)p; }
 
 constexpr int kBlock = 256;          // 4 wavefronts of 64
+constexpr int kSweepBlock = 256;     // threads of a sweep block
 
 // ---------------------------------------------------------------- state quads
 
@@ -305,29 +306,46 @@ __device__ __forceinline__ void renorm(float (&w)[KP]) {
 
 // Unnormalised full conditional (Sec. 4: own CPT entry times the children's
 // entries, Eq. 4) of the quad's 4 columns from a fast product list: group 0
-// gives the own k-vector, each further group a child k-vector multiplied in.
-// With RESCALE every column's running product is renormalised after each
-// factor, which keeps it away from fp32 underflow.
+// gives the first k-vector, each further group a k-vector multiplied in.  The
+// first n_staged groups are read from the LDS copy of the record (byte
+// indices), the others from global memory (k-vector indices); n_staged is
+// uniform, so the choice is a scalar branch.  With RESCALE every column's
+// running product is renormalised after each factor, which keeps it away
+// from fp32 underflow.
+// Multiplies the k-vectors at the quad's packed indices into w (from LDS
+// when FROM_LDS, else from global memory).
+template <int KP, typename ST, bool FROM_LDS, bool RESCALE>
+__device__ __forceinline__ void multiply_group(lds_char *lds, global_char *gtab, const uint32_t (&Pk)[2],
+                                               float (&w)[4][KP]) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        float f[KP];
+        fast_kvec<KP, FROM_LDS>(lds, gtab, packed_index<ST>(Pk, c), f);
+#pragma unroll
+        for (int k = 0; k < KP; ++k) w[c][k] *= f[k];
+        if (RESCALE) renorm<KP>(w[c]);
+    }
+}
+
 template <int KP, typename ST, bool STAGED, bool RESCALE>
-__device__ __forceinline__ void fast_product(cint32_t *g, int n_groups, lds_char *lds,
+__device__ __forceinline__ void fast_product(cint32_t *g, int n_groups, int n_staged, lds_char *lds,
                                              global_char *gtab,
                                              const ST *__restrict__ states, int64_t vstride,
                                              uint32_t lane_boff, const uint32_t (&vmask)[2],
                                              float (&w)[4][KP]) {
     uint32_t Pk[2];
     packed_group<ST>(g, states, vstride, lane_boff, vmask, Pk);
+    if (STAGED && n_staged > 0) {
 #pragma unroll
-    for (int c = 0; c < 4; ++c) fast_kvec<KP, STAGED>(lds, gtab, packed_index<ST>(Pk, c), w[c]);
+        for (int c = 0; c < 4; ++c) fast_kvec<KP, true>(lds, gtab, packed_index<ST>(Pk, c), w[c]);
+    } else {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) fast_kvec<KP, false>(lds, gtab, packed_index<ST>(Pk, c), w[c]);
+    }
     for (int j = 1; j < n_groups; ++j) {
         packed_group<ST>(g, states, vstride, lane_boff, vmask, Pk);
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            float f[KP];
-            fast_kvec<KP, STAGED>(lds, gtab, packed_index<ST>(Pk, c), f);
-#pragma unroll
-            for (int k = 0; k < KP; ++k) w[c][k] *= f[k];
-            if (RESCALE) renorm<KP>(w[c]);
-        }
+        if (STAGED && j < n_staged) multiply_group<KP, ST, true, RESCALE>(lds, gtab, Pk, w);
+        else multiply_group<KP, ST, false, RESCALE>(lds, gtab, Pk, w);
     }
 }
 
@@ -479,11 +497,11 @@ template <int KP, typename ST, bool DEBUG, bool STAGED>
 __device__ void sweep_product(const SweepParams &P, const Work &W, lds_char *lds, global_char *gtab) {
     using Q = Quad<ST>;
     cint32_t *d = W.d;
-    const int K = d[0], n_groups = d[8];
+    const int K = d[0], n_groups = d[8], n_staged = STAGED ? d[13] : 0;
     cint32_t *grp = d + d[9];
     ST *states = reinterpret_cast<ST *>(P.states);
     const int64_t vstride = (int64_t)P.m * P.ld;
-    for (int64_t q = W.q0 + threadIdx.x; q < W.q1; q += kBlock) {
+    for (int64_t q = W.q0 + threadIdx.x; q < W.q1; q += kSweepBlock) {
         const int64_t col = q * 4;
         const int lat = latent_bits(P, W.node, col);
         if (!lat) continue;
@@ -493,8 +511,8 @@ __device__ void sweep_product(const SweepParams &P, const Work &W, lds_char *lds
             const uint32_t lane_boff = (uint32_t)(r * P.ld + col) * (uint32_t)sizeof(ST);
             typename Q::V cur = load_row<ST>(states, W.node, vstride, lane_boff);
             float w[4][KP];
-            fast_product<KP, ST, STAGED, false>(grp, n_groups, lds, gtab, states, vstride, lane_boff,
-                                                vmask, w);
+            fast_product<KP, ST, STAGED, false>(grp, n_groups, n_staged, lds, gtab, states, vstride,
+                                                lane_boff, vmask, w);
             float wd[4][KP];
             if (DEBUG) {
 #pragma unroll
@@ -509,8 +527,8 @@ __device__ void sweep_product(const SweepParams &P, const Work &W, lds_char *lds
                 low |= ((lat >> c) & 1) && !(w[c][KP - 1] >= kUnderflowZ);
             }
             if (low) {
-                fast_product<KP, ST, STAGED, true>(grp, n_groups, lds, gtab, states, vstride, lane_boff,
-                                                   vmask, w);
+                fast_product<KP, ST, STAGED, true>(grp, n_groups, n_staged, lds, gtab, states, vstride,
+                                                   lane_boff, vmask, w);
 #pragma unroll
                 for (int c = 0; c < 4; ++c) {
                     if (DEBUG) {
@@ -570,9 +588,10 @@ __device__ void sweep_table(const SweepParams &P, const Work &W, lds_char *lds, 
     using Q = Quad<ST>;
     cint32_t *d = W.d;
     cint32_t *grp = d + d[9];
+    const bool tab_lds = STAGED && d[13] > 0;  // uniform: thresholds staged in LDS
     ST *states = reinterpret_cast<ST *>(P.states);
     const int64_t vstride = (int64_t)P.m * P.ld;
-    for (int64_t q = W.q0 + threadIdx.x; q < W.q1; q += kBlock) {
+    for (int64_t q = W.q0 + threadIdx.x; q < W.q1; q += kSweepBlock) {
         const int64_t col = q * 4;
         const int lat = latent_bits(P, W.node, col);
         if (!lat) continue;
@@ -592,7 +611,7 @@ __device__ void sweep_table(const SweepParams &P, const Work &W, lds_char *lds, 
                 const uint32_t u24 = rnd.w[c] >> 8;
                 const uint32_t idx = packed_index<ST>(Pk, c);
                 uint32_t th[KT];
-                if (STAGED) {
+                if (tab_lds) {
                     typedef const __attribute__((address_space(3))) uint32_t lu32;
                     typedef const __attribute__((address_space(3))) u32x2 lu2;
                     typedef const __attribute__((address_space(3))) u32x4 lu4;
@@ -649,12 +668,13 @@ __device__ void sweep_table(const SweepParams &P, const Work &W, lds_char *lds, 
 }
 
 // Fast kernel: one block = one node x a run of column quads x a range of
-// replicas (block_work).  The
-// node's mode selects the product path for KP = 2, 4, 8 or the threshold
-// path.  With STAGED the block first copies its node's table record (k-vectors
-// or thresholds) into LDS, so every gather of the sweep is an LDS read.
+// replicas (block_work).  The node's mode selects the product path for KP =
+// 2, 4, 8 or the threshold path.  With STAGED the block first copies the
+// staged part of its node's table record (the whole record of a class-0 node:
+// k-vectors or thresholds; the smallest k-vector groups of a larger record)
+// into LDS, and the gathers of those groups are LDS reads.
 template <typename ST, bool DEBUG, bool STAGED>
-__global__ __launch_bounds__(kBlock) void sweep_fast_kernel(SweepParams P) {
+__global__ __launch_bounds__(kSweepBlock) void sweep_fast_kernel(SweepParams P) {
     extern __shared__ float4 lds4[];
     const Work W = block_work(P);
     if (W.q0 >= W.q1) return;  // uniform across the block
@@ -665,8 +685,8 @@ __global__ __launch_bounds__(kBlock) void sweep_fast_kernel(SweepParams P) {
     if (STAGED) {
         const float4 *src = reinterpret_cast<const float4 *>(mode == kModeTable ? (const void *)cond
                                                                                 : (const void *)tab);
-        const int len4 = mode == kModeTable ? (d[6] + 3) >> 2 : d[4] >> 2;
-        for (int i = threadIdx.x; i < len4; i += kBlock) lds4[i] = src[i];
+        const int len4 = d[14] >> 2;
+        for (int i = threadIdx.x; i < len4; i += kSweepBlock) lds4[i] = src[i];
         __syncthreads();
     }
     lds_char *lds = (lds_char *)lds4;
@@ -695,7 +715,7 @@ __device__ void sweep_wide(const SweepParams &P, const Work &W) {
     const float *tab = P.table + d[3];
     ST *states = reinterpret_cast<ST *>(P.states);
     const int64_t vstride = (int64_t)P.m * P.ld;
-    for (int64_t q = W.q0 + threadIdx.x; q < W.q1; q += kBlock) {
+    for (int64_t q = W.q0 + threadIdx.x; q < W.q1; q += kSweepBlock) {
         const int64_t col = q * 4;
         const int lat = latent_bits(P, W.node, col);
         if (!lat) continue;
@@ -735,7 +755,7 @@ __device__ void sweep_wide(const SweepParams &P, const Work &W) {
 }
 
 template <typename ST, bool DEBUG>
-__global__ __launch_bounds__(kBlock) void sweep_wide_kernel(SweepParams P) {
+__global__ __launch_bounds__(kSweepBlock) void sweep_wide_kernel(SweepParams P) {
     const Work W = block_work(P);
     const int KP = W.d[1];
     if (KP == 2) sweep_wide<2, ST, DEBUG>(P, W);
@@ -775,7 +795,7 @@ __device__ float weight_ext(cint32_t *d, const float *__restrict__ tab, const ST
 }
 
 template <typename ST, bool DEBUG>
-__global__ __launch_bounds__(kBlock) void sweep_generic_kernel(SweepParams P) {
+__global__ __launch_bounds__(kSweepBlock) void sweep_generic_kernel(SweepParams P) {
     using Q = Quad<ST>;
     const Work W = block_work(P);
     cint32_t *d = W.d;
@@ -783,7 +803,7 @@ __global__ __launch_bounds__(kBlock) void sweep_generic_kernel(SweepParams P) {
     const float *tab = P.table + d[3];
     ST *states = reinterpret_cast<ST *>(P.states);
     const int64_t vstride = (int64_t)P.m * P.ld;
-    for (int64_t q = W.q0 + threadIdx.x; q < W.q1; q += kBlock) {
+    for (int64_t q = W.q0 + threadIdx.x; q < W.q1; q += kSweepBlock) {
         const int64_t col = q * 4;
         const int lat = latent_bits(P, W.node, col);
         if (!lat) continue;
@@ -1301,8 +1321,12 @@ template <typename ST>
 void sweep_class(const SweepParams &P, int32_t klass, int32_t lds_bytes, dim3 grid,
                  hipStream_t stream) {
     const bool dbg = P.win > 0;
-    const dim3 blk(dev::kBlock);
+    const dim3 blk(dev::kSweepBlock);
     if (klass == 0) {
+        if (dbg) hipLaunchKernelGGL((dev::sweep_fast_kernel<ST, true, true>), grid, blk, lds_bytes, stream, P);
+        else hipLaunchKernelGGL((dev::sweep_fast_kernel<ST, false, true>), grid, blk, lds_bytes, stream, P);
+    } else if (klass == 1 && lds_bytes > 0) {
+        // partially staged records
         if (dbg) hipLaunchKernelGGL((dev::sweep_fast_kernel<ST, true, true>), grid, blk, lds_bytes, stream, P);
         else hipLaunchKernelGGL((dev::sweep_fast_kernel<ST, false, true>), grid, blk, lds_bytes, stream, P);
     } else if (klass == 1) {
@@ -1329,7 +1353,7 @@ hipError_t launch_sweep(SweepParams P, int32_t begin, int32_t count, int32_t kla
     // replica per block: smaller slabs keep the blanket rows and the global
     // tables that the resident blocks gather from in L2 (measured faster).
     const int64_t quads = (P.n_cols + 3) / 4;
-    P.quads_per_block = (int64_t)dev::kBlock * dev::kSweepQuadsPerLane;
+    P.quads_per_block = (int64_t)dev::kSweepBlock * dev::kSweepQuadsPerLane;
     const int64_t chunks = (quads + P.quads_per_block - 1) / P.quads_per_block;
     int64_t rsplit = klass == 0 ? (dev::kMinSweepBlocks + count * chunks - 1) / (count * chunks) : P.m;
     if (rsplit > P.m) rsplit = P.m;

@@ -221,7 +221,8 @@ def test_kernel_class_options_keep_layout(kw):
 
 def test_kernel_timing_host_calls():
     ctx = _ctx(koller())
-    assert same.same_kernel_times(ctx) == {"ms": [0.0] * 4, "launches": [0] * 4, "phase_ms": 0.0, "phases": 0}
+    assert same.same_kernel_times(ctx) == {"ms": [0.0] * 4, "launches": [0] * 4, "phase_ms": 0.0, "phases": 0,
+                                           "node_samples": [0.0] * 4}
     same.same_kernel_timing(ctx, True)
     same.same_kernel_timing(ctx, False)
     L = same.load_library()

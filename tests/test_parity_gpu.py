@@ -71,14 +71,16 @@ def test_sweep_parity_configs(cfg, kw, win, table_limit):
     (4, {}, (0, 600)),
     (5, dict(n_cols=3_000, m=4), (2_600, 400)),
 ])
-@pytest.mark.parametrize("variant", [dict(lds_limit=0), dict(lds_limit=1024), dict(packed=False),
-                                     dict(lds_limit=0, packed=False)],
-                         ids=["global-tables", "mixed-tables", "wide-indices", "global-wide"])
+@pytest.mark.parametrize("variant", [dict(lds_limit=0), dict(lds_limit=1024), dict(lds_limit=4096),
+                                     dict(packed=False), dict(lds_limit=0, packed=False)],
+                         ids=["global-tables", "mixed-tables", "partial-records", "wide-indices", "global-wide"])
 def test_sweep_parity_kernel_classes(cfg, kw, win, variant):
     """The same conditionals and draws when every table is read from global
     memory, when a colour's nodes split between LDS-staged and global tables
-    (two concurrent launches per colour), and/or every product-mode node takes
-    the 32-bit index kernel."""
+    (two concurrent launches per colour), when records larger than the LDS
+    budget stage only their smallest CPT groups and gather the rest from
+    global memory, and/or every product-mode node takes the 32-bit index
+    kernel."""
     w = make_workload(cfg, **kw)
     out = _sweep_case(w, win=win, **variant)
     assert out["probs"]["checked"] > 0
@@ -444,4 +446,7 @@ def test_kernel_timing_counts_launches_and_phases():
     assert kt["launches"][0] > 0 and kt["launches"][1] > 0
     assert kt["phases"] == lay["n_colors"]
     assert kt["phase_ms"] > 0.0
-    assert same.same_kernel_times(ctx) == {"ms": [0.0] * 4, "launches": [0] * 4, "phase_ms": 0.0, "phases": 0}
+    # every (node, column, replica) slot is covered by exactly one launch
+    assert sum(kt["node_samples"]) == float(net.n * 3_000 * w.m)
+    assert same.same_kernel_times(ctx) == {"ms": [0.0] * 4, "launches": [0] * 4, "phase_ms": 0.0, "phases": 0,
+                                           "node_samples": [0.0] * 4}
