@@ -27,6 +27,7 @@ __device__ __forceinline__ cint32_t *as_const(const int32_t *p) { return (cint32
 
 constexpr int kBlock = 256;          // 4 wavefronts of 64
 constexpr int kSweepBlock = 256;     // threads of a sweep block
+constexpr int kSweepWaves = 6;       // waves per SIMD the fast sweep kernel is compiled for
 
 // ---------------------------------------------------------------- state quads
 
@@ -342,10 +343,18 @@ __device__ __forceinline__ void fast_product(cint32_t *g, int n_groups, int n_st
 #pragma unroll
         for (int c = 0; c < 4; ++c) fast_kvec<KP, false>(lds, gtab, packed_index<ST>(Pk, c), w[c]);
     }
-    for (int j = 1; j < n_groups; ++j) {
+    // the staged groups, then the global ones: two loops, so that each keeps
+    // only its own addressing live
+    int j = 1;
+    if (STAGED) {
+        for (; j < n_staged; ++j) {
+            packed_group<ST>(g, states, vstride, lane_boff, vmask, Pk);
+            multiply_group<KP, ST, true, RESCALE>(lds, gtab, Pk, w);
+        }
+    }
+    for (; j < n_groups; ++j) {
         packed_group<ST>(g, states, vstride, lane_boff, vmask, Pk);
-        if (STAGED && j < n_staged) multiply_group<KP, ST, true, RESCALE>(lds, gtab, Pk, w);
-        else multiply_group<KP, ST, false, RESCALE>(lds, gtab, Pk, w);
+        multiply_group<KP, ST, false, RESCALE>(lds, gtab, Pk, w);
     }
 }
 
@@ -673,8 +682,12 @@ __device__ void sweep_table(const SweepParams &P, const Work &W, lds_char *lds, 
 // staged part of its node's table record (the whole record of a class-0 node:
 // k-vectors or thresholds; the smallest k-vector groups of a larger record)
 // into LDS, and the gathers of those groups are LDS reads.
+// At least kSweepWaves waves per SIMD: without the bound the compiler
+// schedules the staged kernel into 85 VGPRs (5 waves); with it, 66 VGPRs and
+// no spills, so the LDS budget (6 blocks of 24 KB per CU) sets the occupancy.
+// The debug variant (conditionals written out) keeps the default bound.
 template <typename ST, bool DEBUG, bool STAGED>
-__global__ __launch_bounds__(kSweepBlock) void sweep_fast_kernel(SweepParams P) {
+__global__ __launch_bounds__(kSweepBlock, DEBUG ? 1 : kSweepWaves) void sweep_fast_kernel(SweepParams P) {
     extern __shared__ float4 lds4[];
     const Work W = block_work(P);
     if (W.q0 >= W.q1) return;  // uniform across the block
