@@ -28,6 +28,11 @@ __device__ __forceinline__ cint32_t *as_const(const int32_t *p) { return (cint32
 constexpr int kBlock = 256;          // 4 wavefronts of 64
 constexpr int kSweepBlock = 256;     // threads of a sweep block
 constexpr int kSweepWaves = 6;       // waves per SIMD the fast sweep kernel is compiled for
+// replicas a lane draws together (their loads in flight at once), per path
+constexpr int kPairTable = 2;
+constexpr int kPairKP2 = 2;
+constexpr int kPairKP4 = 2;
+constexpr int kPairKP8 = 1;
 
 // ---------------------------------------------------------------- state quads
 
@@ -166,6 +171,44 @@ __device__ __forceinline__ void walk_entries(cint32_t *e, int n_e, const ST *__r
     }
 }
 
+// The same for NR replicas of the lane's column quad at once (byte offsets
+// boff): the NR rows of an entry share its buffer resource, and every load
+// of the batch is in flight before the first use, so NR replicas cost one
+// round trip per batch instead of NR.
+template <int N, int NR, typename ST, typename F>
+__device__ __forceinline__ void entry_batch_r(cint32_t *e, const ST *__restrict__ states, int64_t vstride,
+                                              const uint32_t (&boff)[NR], F &f) {
+    typename Quad<ST>::V s[N][NR];
+#pragma unroll
+    for (int t = 0; t < N; ++t)
+#pragma unroll
+        for (int r = 0; r < NR; ++r) s[t][r] = load_row<ST>(states, e[2 * t], vstride, boff[r]);
+#pragma unroll
+    for (int t = 0; t < N; ++t)
+#pragma unroll
+        for (int r = 0; r < NR; ++r) f(r, s[t][r], (uint32_t)e[2 * t + 1]);
+}
+
+// Batches of at most kEntryBatch / NR entries (kEntryBatch rows in flight).
+template <int NR, typename ST, typename F>
+__device__ __forceinline__ void walk_entries_r(cint32_t *e, int n_e, const ST *__restrict__ states,
+                                               int64_t vstride, const uint32_t (&boff)[NR], F &f) {
+    constexpr int B = kEntryBatch / NR;
+    for (; n_e > 0; n_e -= B, e += 2 * B) {
+        const int nb = n_e < B ? n_e : B;
+        if (nb == 1) entry_batch_r<1, NR, ST>(e, states, vstride, boff, f);
+        else if (nb == 2) entry_batch_r<2, NR, ST>(e, states, vstride, boff, f);
+        else if (nb == 3) entry_batch_r<3, NR, ST>(e, states, vstride, boff, f);
+        else if (nb == 4) entry_batch_r<4, NR, ST>(e, states, vstride, boff, f);
+        else if constexpr (B > 4) {
+            if (nb == 5) entry_batch_r<5, NR, ST>(e, states, vstride, boff, f);
+            else if (nb == 6) entry_batch_r<6, NR, ST>(e, states, vstride, boff, f);
+            else if (nb == 7) entry_batch_r<7, NR, ST>(e, states, vstride, boff, f);
+            else entry_batch_r<8, NR, ST>(e, states, vstride, boff, f);
+        }
+    }
+}
+
 // Packed group index of a fast list: two words of 2 x 16-bit lanes, one lane
 // per column of the quad (lane layout in Quad<ST>::split).  Columns past
 // n_cols are cleared by vmask, so their index is 0: padding never steers an
@@ -192,6 +235,29 @@ template <typename ST>
 __device__ __forceinline__ uint32_t packed_index(const uint32_t (&Pk)[2], int c) {
     const uint32_t v = Pk[Quad<ST>::word_of(c)];
     return Quad<ST>::half_of(c) ? v >> 16 : v & 0xffffu;
+}
+
+// packed_group for NR replicas (Pk[r] belongs to byte offset boff[r]).
+template <int NR, typename ST>
+__device__ __forceinline__ void packed_group_r(cint32_t *&g, const ST *__restrict__ states, int64_t vstride,
+                                               const uint32_t (&boff)[NR], const uint32_t (&vmask)[2],
+                                               uint32_t (&Pk)[NR][2]) {
+    const int n_e = g[0];
+#pragma unroll
+    for (int r = 0; r < NR; ++r) Pk[r][0] = Pk[r][1] = (uint32_t)g[1];
+    auto acc = [&](int r, typename Quad<ST>::V v, uint32_t mult) {
+        uint32_t p[2];
+        Quad<ST>::split(v, p);
+        Pk[r][0] = pk_mad_u16(p[0], mult, Pk[r][0]);
+        Pk[r][1] = pk_mad_u16(p[1], mult, Pk[r][1]);
+    };
+    walk_entries_r<NR, ST>(g + 2, n_e, states, vstride, boff, acc);
+    g += 2 + 2 * n_e;
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+        Pk[r][0] &= vmask[0];
+        Pk[r][1] &= vmask[1];
+    }
 }
 
 // Lane masks of vmask: the 16-bit lanes of columns >= nvalid cleared.
@@ -328,33 +394,39 @@ __device__ __forceinline__ void multiply_group(lds_char *lds, global_char *gtab,
     }
 }
 
-template <int KP, typename ST, bool STAGED, bool RESCALE>
+template <int KP, typename ST, bool STAGED, bool RESCALE, int NR>
 __device__ __forceinline__ void fast_product(cint32_t *g, int n_groups, int n_staged, lds_char *lds,
                                              global_char *gtab,
                                              const ST *__restrict__ states, int64_t vstride,
-                                             uint32_t lane_boff, const uint32_t (&vmask)[2],
-                                             float (&w)[4][KP]) {
-    uint32_t Pk[2];
-    packed_group<ST>(g, states, vstride, lane_boff, vmask, Pk);
+                                             const uint32_t (&boff)[NR], const uint32_t (&vmask)[2],
+                                             float (&w)[NR][4][KP]) {
+    uint32_t Pk[NR][2];
+    packed_group_r<NR, ST>(g, states, vstride, boff, vmask, Pk);
     if (STAGED && n_staged > 0) {
 #pragma unroll
-        for (int c = 0; c < 4; ++c) fast_kvec<KP, true>(lds, gtab, packed_index<ST>(Pk, c), w[c]);
+        for (int r = 0; r < NR; ++r)
+#pragma unroll
+            for (int c = 0; c < 4; ++c) fast_kvec<KP, true>(lds, gtab, packed_index<ST>(Pk[r], c), w[r][c]);
     } else {
 #pragma unroll
-        for (int c = 0; c < 4; ++c) fast_kvec<KP, false>(lds, gtab, packed_index<ST>(Pk, c), w[c]);
+        for (int r = 0; r < NR; ++r)
+#pragma unroll
+            for (int c = 0; c < 4; ++c) fast_kvec<KP, false>(lds, gtab, packed_index<ST>(Pk[r], c), w[r][c]);
     }
     // the staged groups, then the global ones: two loops, so that each keeps
     // only its own addressing live
     int j = 1;
     if (STAGED) {
         for (; j < n_staged; ++j) {
-            packed_group<ST>(g, states, vstride, lane_boff, vmask, Pk);
-            multiply_group<KP, ST, true, RESCALE>(lds, gtab, Pk, w);
+            packed_group_r<NR, ST>(g, states, vstride, boff, vmask, Pk);
+#pragma unroll
+            for (int r = 0; r < NR; ++r) multiply_group<KP, ST, true, RESCALE>(lds, gtab, Pk[r], w[r]);
         }
     }
     for (; j < n_groups; ++j) {
-        packed_group<ST>(g, states, vstride, lane_boff, vmask, Pk);
-        multiply_group<KP, ST, false, RESCALE>(lds, gtab, Pk, w);
+        packed_group_r<NR, ST>(g, states, vstride, boff, vmask, Pk);
+#pragma unroll
+        for (int r = 0; r < NR; ++r) multiply_group<KP, ST, false, RESCALE>(lds, gtab, Pk[r], w[r]);
     }
 }
 
@@ -501,63 +573,92 @@ __device__ __forceinline__ Philox4 gibbs_block(const SweepParams &P, int node, i
 
 __device__ __forceinline__ float uniform24(uint32_t word) { return (float)(word >> 8) * 0x1p-24f; }
 
-// Fast product path (classes 0 and 1, KP <= 8).
-template <int KP, typename ST, bool DEBUG, bool STAGED>
-__device__ void sweep_product(const SweepParams &P, const Work &W, lds_char *lds, global_char *gtab) {
+// Replicas r0 .. r0+NR-1 of one column quad on the product path: all their
+// blanket loads in flight together, then the products, the draws and the
+// stores.
+template <int KP, typename ST, bool DEBUG, bool STAGED, int NR>
+__device__ __forceinline__ void product_replicas(const SweepParams &P, const Work &W, lds_char *lds,
+                                                 global_char *gtab, cint32_t *grp, int K, int n_groups,
+                                                 int n_staged, int64_t q, int lat,
+                                                 const uint32_t (&vmask)[2], int r0) {
     using Q = Quad<ST>;
+    ST *states = reinterpret_cast<ST *>(P.states);
+    const int64_t vstride = (int64_t)P.m * P.ld;
+    const int64_t col = q * 4;
+    uint32_t boff[NR];
+    typename Q::V cur[NR];
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+        boff[r] = (uint32_t)((r0 + r) * P.ld + col) * (uint32_t)sizeof(ST);
+        cur[r] = load_row<ST>(states, W.node, vstride, boff[r]);
+    }
+    float w[NR][4][KP];
+    fast_product<KP, ST, STAGED, false, NR>(grp, n_groups, n_staged, lds, gtab, states, vstride, boff, vmask, w);
+    float wd[4][KP];
+    if (DEBUG) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+#pragma unroll
+            for (int k = 0; k < KP; ++k) wd[c][k] = w[0][c][k];
+    }
+    bool low = false;
+#pragma unroll
+    for (int r = 0; r < NR; ++r)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            running_sums<KP>(w[r][c]);
+            low |= ((lat >> c) & 1) && !(w[r][c][KP - 1] >= kUnderflowZ);
+        }
+    if (low) {
+        fast_product<KP, ST, STAGED, true, NR>(grp, n_groups, n_staged, lds, gtab, states, vstride, boff, vmask,
+                                               w);
+#pragma unroll
+        for (int r = 0; r < NR; ++r)
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                if (DEBUG) {
+#pragma unroll
+                    for (int k = 0; k < KP; ++k) wd[c][k] = w[0][c][k];
+                }
+                running_sums<KP>(w[r][c]);
+            }
+    }
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+        const Philox4 rnd = gibbs_block(P, W.node, r0 + r, q);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            if (!((lat >> c) & 1)) continue;
+            cur[r] = Q::put(cur[r], c, draw_sums<KP>(w[r][c], K, uniform24(rnd.w[c])));
+            if (DEBUG) write_probs(P, W.node, r0, col + c, wd[c], K, w[0][c][KP - 1]);
+        }
+        Q::store(reinterpret_cast<ST *>(reinterpret_cast<char *>(states + (int64_t)W.node * vstride) + boff[r]),
+                 cur[r]);
+    }
+}
+
+// Fast product path (classes 0 and 1, KP <= 8): replicas in groups of NR
+// (one at a time in debug mode, where the conditionals are written out).
+template <int KP, typename ST, bool DEBUG, bool STAGED, int NR>
+__device__ void sweep_product(const SweepParams &P, const Work &W, lds_char *lds, global_char *gtab) {
     cint32_t *d = W.d;
     const int K = d[0], n_groups = d[8], n_staged = STAGED ? d[13] : 0;
     cint32_t *grp = d + d[9];
-    ST *states = reinterpret_cast<ST *>(P.states);
-    const int64_t vstride = (int64_t)P.m * P.ld;
+    constexpr int R = DEBUG ? 1 : NR;
     for (int64_t q = W.q0 + threadIdx.x; q < W.q1; q += kSweepBlock) {
         const int64_t col = q * 4;
         const int lat = latent_bits(P, W.node, col);
         if (!lat) continue;
         uint32_t vmask[2];
         valid_mask<ST>(P.n_cols - col < 4 ? (int)(P.n_cols - col) : 4, vmask);
-        for (int r = W.r0; r < W.r1; ++r) {
-            const uint32_t lane_boff = (uint32_t)(r * P.ld + col) * (uint32_t)sizeof(ST);
-            typename Q::V cur = load_row<ST>(states, W.node, vstride, lane_boff);
-            float w[4][KP];
-            fast_product<KP, ST, STAGED, false>(grp, n_groups, n_staged, lds, gtab, states, vstride,
-                                                lane_boff, vmask, w);
-            float wd[4][KP];
-            if (DEBUG) {
-#pragma unroll
-                for (int c = 0; c < 4; ++c)
-#pragma unroll
-                    for (int k = 0; k < KP; ++k) wd[c][k] = w[c][k];
-            }
-            bool low = false;
-#pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                running_sums<KP>(w[c]);
-                low |= ((lat >> c) & 1) && !(w[c][KP - 1] >= kUnderflowZ);
-            }
-            if (low) {
-                fast_product<KP, ST, STAGED, true>(grp, n_groups, n_staged, lds, gtab, states, vstride,
-                                                   lane_boff, vmask, w);
-#pragma unroll
-                for (int c = 0; c < 4; ++c) {
-                    if (DEBUG) {
-#pragma unroll
-                        for (int k = 0; k < KP; ++k) wd[c][k] = w[c][k];
-                    }
-                    running_sums<KP>(w[c]);
-                }
-            }
-            const Philox4 rnd = gibbs_block(P, W.node, r, q);
-#pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                if (!((lat >> c) & 1)) continue;
-                cur = Q::put(cur, c, draw_sums<KP>(w[c], K, uniform24(rnd.w[c])));
-                if (DEBUG) write_probs(P, W.node, r, col + c, wd[c], K, w[c][KP - 1]);
-            }
-            Q::store(reinterpret_cast<ST *>(reinterpret_cast<char *>(states + (int64_t)W.node * vstride) +
-                                            lane_boff),
-                     cur);
-        }
+        int r = W.r0;
+        if (R > 1)
+            for (; r + R <= W.r1; r += R)
+                product_replicas<KP, ST, DEBUG, STAGED, R>(P, W, lds, gtab, grp, K, n_groups, n_staged, q, lat,
+                                                           vmask, r);
+        for (; r < W.r1; ++r)
+            product_replicas<KP, ST, DEBUG, STAGED, 1>(P, W, lds, gtab, grp, K, n_groups, n_staged, q, lat, vmask,
+                                                       r);
     }
 }
 
@@ -589,17 +690,104 @@ __device__ void table_debug_probs(const SweepParams &P, const Work &W, int r, in
 #undef SAME_TABLE_DEBUG
 }
 
+// KT thresholds of a blanket configuration: the row at byte offset idx of the
+// staged table (LDS) or row idx of the table in global memory.
+template <int KT>
+__device__ __forceinline__ void read_thresholds(bool from_lds, lds_char *lds, global_char *gcond, uint32_t idx,
+                                                uint32_t (&th)[KT]) {
+    if (from_lds) {
+        typedef const __attribute__((address_space(3))) uint32_t lu32;
+        typedef const __attribute__((address_space(3))) u32x2 lu2;
+        typedef const __attribute__((address_space(3))) u32x4 lu4;
+        lds_char *p = lds + idx;
+        if (KT == 1) {
+            th[0] = *reinterpret_cast<lu32 *>(p);
+        } else if (KT == 2) {
+            const u32x2 v = *reinterpret_cast<lu2 *>(p);
+            th[0] = v.x;
+            th[1] = v.y;
+        } else {
+#pragma unroll
+            for (int h = 0; h < KT / 4; ++h) {
+                const u32x4 v = reinterpret_cast<lu4 *>(p)[h];
+                th[4 * h] = v.x;
+                th[4 * h + 1] = v.y;
+                th[4 * h + 2] = v.z;
+                th[4 * h + 3] = v.w;
+            }
+        }
+    } else {
+        typedef const __attribute__((address_space(1))) uint32_t gu32;
+        typedef const __attribute__((address_space(1))) u32x2 gu2;
+        typedef const __attribute__((address_space(1))) u32x4 gu4;
+        global_char *p = gcond + (idx << log2i(4 * KT));
+        if (KT == 1) {
+            th[0] = *reinterpret_cast<gu32 *>(p);
+        } else if (KT == 2) {
+            const u32x2 v = *reinterpret_cast<gu2 *>(p);
+            th[0] = v.x;
+            th[1] = v.y;
+        } else {
+#pragma unroll
+            for (int h = 0; h < KT / 4; ++h) {
+                const u32x4 v = reinterpret_cast<gu4 *>(p)[h];
+                th[4 * h] = v.x;
+                th[4 * h + 1] = v.y;
+                th[4 * h + 2] = v.z;
+                th[4 * h + 3] = v.w;
+            }
+        }
+    }
+}
+
+// Replicas r0 .. r0+NR-1 of one column quad on the threshold path.
+template <int KT, typename ST, bool DEBUG, bool STAGED, int NR>
+__device__ __forceinline__ void table_replicas(const SweepParams &P, const Work &W, lds_char *lds,
+                                               global_char *gcond, cint32_t *grp, bool tab_lds, int64_t q,
+                                               int lat, int nvalid, const uint32_t (&vmask)[2], int r0) {
+    using Q = Quad<ST>;
+    ST *states = reinterpret_cast<ST *>(P.states);
+    const int64_t vstride = (int64_t)P.m * P.ld;
+    const int64_t col = q * 4;
+    uint32_t boff[NR];
+    typename Q::V cur[NR];
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+        boff[r] = (uint32_t)((r0 + r) * P.ld + col) * (uint32_t)sizeof(ST);
+        cur[r] = load_row<ST>(states, W.node, vstride, boff[r]);
+    }
+    cint32_t *g = grp;
+    uint32_t Pk[NR][2];
+    packed_group_r<NR, ST>(g, states, vstride, boff, vmask, Pk);
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+        const Philox4 rnd = gibbs_block(P, W.node, r0 + r, q);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            if (!((lat >> c) & 1)) continue;
+            const uint32_t u24 = rnd.w[c] >> 8;
+            uint32_t th[KT];
+            read_thresholds<KT>(tab_lds, lds, gcond, packed_index<ST>(Pk[r], c), th);
+            int pick = 0;
+#pragma unroll
+            for (int k = 0; k < KT; ++k) pick += th[k] <= u24 ? 1 : 0;
+            cur[r] = Q::put(cur[r], c, pick);
+        }
+        if (DEBUG) table_debug_probs<ST>(P, W, r0 + r, col, lat, nvalid);
+        Q::store(reinterpret_cast<ST *>(reinterpret_cast<char *>(states + (int64_t)W.node * vstride) + boff[r]),
+                 cur[r]);
+    }
+}
+
 // Threshold path (classes 0 and 1): the blanket configuration selects KT
 // thresholds; the drawn state is the number of thresholds at or below the
-// 24-bit uniform.
-template <int KT, typename ST, bool DEBUG, bool STAGED>
+// 24-bit uniform.  Replicas in groups of NR (one at a time in debug mode).
+template <int KT, typename ST, bool DEBUG, bool STAGED, int NR>
 __device__ void sweep_table(const SweepParams &P, const Work &W, lds_char *lds, global_char *gcond) {
-    using Q = Quad<ST>;
     cint32_t *d = W.d;
     cint32_t *grp = d + d[9];
     const bool tab_lds = STAGED && d[13] > 0;  // uniform: thresholds staged in LDS
-    ST *states = reinterpret_cast<ST *>(P.states);
-    const int64_t vstride = (int64_t)P.m * P.ld;
+    constexpr int R = DEBUG ? 1 : NR;
     for (int64_t q = W.q0 + threadIdx.x; q < W.q1; q += kSweepBlock) {
         const int64_t col = q * 4;
         const int lat = latent_bits(P, W.node, col);
@@ -607,72 +795,12 @@ __device__ void sweep_table(const SweepParams &P, const Work &W, lds_char *lds, 
         const int nvalid = P.n_cols - col < 4 ? (int)(P.n_cols - col) : 4;
         uint32_t vmask[2];
         valid_mask<ST>(nvalid, vmask);
-        for (int r = W.r0; r < W.r1; ++r) {
-            const uint32_t lane_boff = (uint32_t)(r * P.ld + col) * (uint32_t)sizeof(ST);
-            typename Q::V cur = load_row<ST>(states, W.node, vstride, lane_boff);
-            cint32_t *g = grp;
-            uint32_t Pk[2];
-            packed_group<ST>(g, states, vstride, lane_boff, vmask, Pk);
-            const Philox4 rnd = gibbs_block(P, W.node, r, q);
-#pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                if (!((lat >> c) & 1)) continue;
-                const uint32_t u24 = rnd.w[c] >> 8;
-                const uint32_t idx = packed_index<ST>(Pk, c);
-                uint32_t th[KT];
-                if (tab_lds) {
-                    typedef const __attribute__((address_space(3))) uint32_t lu32;
-                    typedef const __attribute__((address_space(3))) u32x2 lu2;
-                    typedef const __attribute__((address_space(3))) u32x4 lu4;
-                    lds_char *p = lds + idx;
-                    if (KT == 1) {
-                        th[0] = *reinterpret_cast<lu32 *>(p);
-                    } else if (KT == 2) {
-                        const u32x2 v = *reinterpret_cast<lu2 *>(p);
-                        th[0] = v.x;
-                        th[1] = v.y;
-                    } else {
-#pragma unroll
-                        for (int h = 0; h < KT / 4; ++h) {
-                            const u32x4 v = reinterpret_cast<lu4 *>(p)[h];
-                            th[4 * h] = v.x;
-                            th[4 * h + 1] = v.y;
-                            th[4 * h + 2] = v.z;
-                            th[4 * h + 3] = v.w;
-                        }
-                    }
-                } else {
-                    typedef const __attribute__((address_space(1))) uint32_t gu32;
-                    typedef const __attribute__((address_space(1))) u32x2 gu2;
-                    typedef const __attribute__((address_space(1))) u32x4 gu4;
-                    global_char *p = gcond + (idx << log2i(4 * KT));
-                    if (KT == 1) {
-                        th[0] = *reinterpret_cast<gu32 *>(p);
-                    } else if (KT == 2) {
-                        const u32x2 v = *reinterpret_cast<gu2 *>(p);
-                        th[0] = v.x;
-                        th[1] = v.y;
-                    } else {
-#pragma unroll
-                        for (int h = 0; h < KT / 4; ++h) {
-                            const u32x4 v = reinterpret_cast<gu4 *>(p)[h];
-                            th[4 * h] = v.x;
-                            th[4 * h + 1] = v.y;
-                            th[4 * h + 2] = v.z;
-                            th[4 * h + 3] = v.w;
-                        }
-                    }
-                }
-                int pick = 0;
-#pragma unroll
-                for (int k = 0; k < KT; ++k) pick += th[k] <= u24 ? 1 : 0;
-                cur = Q::put(cur, c, pick);
-            }
-            if (DEBUG) table_debug_probs<ST>(P, W, r, col, lat, nvalid);
-            Q::store(reinterpret_cast<ST *>(reinterpret_cast<char *>(states + (int64_t)W.node * vstride) +
-                                            lane_boff),
-                     cur);
-        }
+        int r = W.r0;
+        if (R > 1)
+            for (; r + R <= W.r1; r += R)
+                table_replicas<KT, ST, DEBUG, STAGED, R>(P, W, lds, gcond, grp, tab_lds, q, lat, nvalid, vmask, r);
+        for (; r < W.r1; ++r)
+            table_replicas<KT, ST, DEBUG, STAGED, 1>(P, W, lds, gcond, grp, tab_lds, q, lat, nvalid, vmask, r);
     }
 }
 
@@ -704,16 +832,16 @@ __global__ __launch_bounds__(kSweepBlock, DEBUG ? 1 : kSweepWaves) void sweep_fa
     }
     lds_char *lds = (lds_char *)lds4;
     global_char *gt = scalar_global_ptr(tab);
-    if (mode == kModeKP2) sweep_product<2, ST, DEBUG, STAGED>(P, W, lds, gt);
-    else if (mode == kModeKP4) sweep_product<4, ST, DEBUG, STAGED>(P, W, lds, gt);
-    else if (mode == kModeKP8) sweep_product<8, ST, DEBUG, STAGED>(P, W, lds, gt);
+    if (mode == kModeKP2) sweep_product<2, ST, DEBUG, STAGED, kPairKP2>(P, W, lds, gt);
+    else if (mode == kModeKP4) sweep_product<4, ST, DEBUG, STAGED, kPairKP4>(P, W, lds, gt);
+    else if (mode == kModeKP8) sweep_product<8, ST, DEBUG, STAGED, kPairKP8>(P, W, lds, gt);
     else {
         const int KT = d[7];
         global_char *gc = scalar_global_ptr(cond);
-        if (KT == 1) sweep_table<1, ST, DEBUG, STAGED>(P, W, lds, gc);
-        else if (KT == 2) sweep_table<2, ST, DEBUG, STAGED>(P, W, lds, gc);
-        else if (KT == 4) sweep_table<4, ST, DEBUG, STAGED>(P, W, lds, gc);
-        else sweep_table<8, ST, DEBUG, STAGED>(P, W, lds, gc);
+        if (KT == 1) sweep_table<1, ST, DEBUG, STAGED, kPairTable>(P, W, lds, gc);
+        else if (KT == 2) sweep_table<2, ST, DEBUG, STAGED, kPairTable>(P, W, lds, gc);
+        else if (KT == 4) sweep_table<4, ST, DEBUG, STAGED, kPairTable>(P, W, lds, gc);
+        else sweep_table<8, ST, DEBUG, STAGED, kPairTable>(P, W, lds, gc);
     }
 }
 
