@@ -111,7 +111,10 @@ typedef struct {
      * to this size is copied into LDS before drawing; a larger record stages
      * its smallest CPT groups up to this size and reads the rest from global
      * memory.  -1 selects the default (24576); at most 32768; 0 stages
-     * nothing.  Results do not depend on it. */
+     * nothing.  Such a record is laid out with its staged groups first, and
+     * the fp32 product of a conditional is formed in record order, so the
+     * budget can change a conditional in its last bits: draws agree except
+     * where a uniform lies within rounding of a CDF boundary. */
     int64_t lds_limit;
     /* 1 (default): blanket indices of nodes with K <= 8 and records below
      * 2^16 rows use packed 16-bit arithmetic; 0: every product-mode node uses
