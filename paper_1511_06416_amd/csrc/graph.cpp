@@ -16,6 +16,7 @@ constexpr int64_t kI32Max = (int64_t(1) << 31) - 1;
 int32_t padded_k(int32_t K) {
     if (K <= 2) return 2;
     if (K <= 4) return 4;
+    if (K <= 6) return 6;
     if (K <= 8) return 8;
     if (K <= 16) return 16;
     return (K + 3) & ~3;
@@ -233,7 +234,7 @@ int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int
         std::sort(b.begin(), b.end());
         b.erase(std::unique(b.begin(), b.end()), b.end());
         const int32_t K = card[i];
-        int32_t mode = K <= 2 ? kModeKP2 : K <= 4 ? kModeKP4 : K <= 8 ? kModeKP8
+        int32_t mode = K <= 2 ? kModeKP2 : K <= 4 ? kModeKP4 : K <= 6 ? kModeKP6 : K <= 8 ? kModeKP8
                      : K <= 16 ? kModeKP16 : kModeGeneric;
         if (table_limit > 0 && K <= 9) {
             int64_t cfg = 1;
@@ -323,7 +324,9 @@ int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int
             klass = 2;
         } else {
             const int64_t bytes = tab ? cond_len * 4 : g.tab_len[i] * 4;
-            const int64_t row_bytes = tab ? (int64_t)KT * 4 : (int64_t)KP * 4;
+            // index unit of the global fast list: a threshold row, a k-vector,
+            // or 8 bytes for KP = 6 (24-byte k-vectors in 64-byte aligned groups)
+            const int64_t row_bytes = tab ? (int64_t)KT * 4 : KP == 6 ? 8 : (int64_t)KP * 4;
             if (!packed && !tab) {
                 klass = 2;
             } else if (bytes <= lds_limit) {

@@ -48,7 +48,8 @@ enum SweepMode : int32_t {
     kModeKP8 = 2,
     kModeTable = 3,  // precomputed CDF thresholds per blanket configuration
     kModeKP16 = 4,   // product path with KP = 16
-    kModeGeneric = 5 // K > 16: extended-exponent product path
+    kModeGeneric = 5, // K > 16: extended-exponent product path
+    kModeKP6 = 6     // product path with KP = 6 (K = 5, 6)
 };
 
 // Launch classes (one kernel each):

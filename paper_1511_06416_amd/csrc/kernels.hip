@@ -32,6 +32,7 @@ constexpr int kSweepWaves = 6;       // waves per SIMD the fast sweep kernel is 
 constexpr int kPairTable = 2;
 constexpr int kPairKP2 = 2;
 constexpr int kPairKP4 = 2;
+constexpr int kPairKP6 = 1;
 constexpr int kPairKP8 = 1;
 
 // ---------------------------------------------------------------- state quads
@@ -271,13 +272,16 @@ __device__ __forceinline__ void valid_mask(int nvalid, uint32_t (&vmask)[2]) {
 
 // ---------------------------------------------------------------- k-vectors
 
-// Reads KP floats at p (8-byte aligned for KP == 2, 16-byte otherwise).
+// Reads KP floats at p (8-byte aligned for KP == 2 or 6, 16-byte otherwise).
 template <int KP, typename PTR>
 __device__ __forceinline__ void read_kvec(PTR p, float (&f)[KP]) {
-    if (KP == 2) {
-        const float2 v = *reinterpret_cast<const float2 *>(p);
-        f[0] = v.x;
-        f[1] = v.y;
+    if (KP == 2 || KP == 6) {
+#pragma unroll
+        for (int q = 0; q < KP / 2; ++q) {
+            const float2 v = reinterpret_cast<const float2 *>(p)[q];
+            f[2 * q] = v.x;
+            f[2 * q + 1] = v.y;
+        }
         return;
     }
 #pragma unroll
@@ -300,10 +304,13 @@ template <int KP>
 __device__ __forceinline__ void read_kvec_lds(lds_char *p, float (&f)[KP]) {
     typedef const __attribute__((address_space(3))) f32x2 lf2;
     typedef const __attribute__((address_space(3))) f32x4 lf4;
-    if (KP == 2) {
-        const f32x2 v = *reinterpret_cast<lf2 *>(p);
-        f[0] = v.x;
-        f[1] = v.y;
+    if (KP == 2 || KP == 6) {
+#pragma unroll
+        for (int q = 0; q < KP / 2; ++q) {
+            const f32x2 v = reinterpret_cast<lf2 *>(p)[q];
+            f[2 * q] = v.x;
+            f[2 * q + 1] = v.y;
+        }
         return;
     }
 #pragma unroll
@@ -334,10 +341,13 @@ template <int KP>
 __device__ __forceinline__ void read_kvec_global(global_char *p, float (&f)[KP]) {
     typedef const __attribute__((address_space(1))) f32x2 gf2;
     typedef const __attribute__((address_space(1))) f32x4 gf4;
-    if (KP == 2) {
-        const f32x2 v = *reinterpret_cast<gf2 *>(p);
-        f[0] = v.x;
-        f[1] = v.y;
+    if (KP == 2 || KP == 6) {
+#pragma unroll
+        for (int q = 0; q < KP / 2; ++q) {
+            const f32x2 v = reinterpret_cast<gf2 *>(p)[q];
+            f[2 * q] = v.x;
+            f[2 * q + 1] = v.y;
+        }
         return;
     }
 #pragma unroll
@@ -350,12 +360,18 @@ __device__ __forceinline__ void read_kvec_global(global_char *p, float (&f)[KP])
     }
 }
 
+// Unit of a global fast-list index: one k-vector (KP floats), or 8 bytes for
+// KP = 6, whose 24-byte k-vectors do not divide the records' 64-byte group
+// alignment.
+template <int KP>
+constexpr int kvec_unit_shift() { return KP == 6 ? 3 : log2i(4 * KP); }
+
 // The k-vector at packed index idx: a byte offset into the staged record
-// (STAGED) or a k-vector number in the node's global record.
+// (STAGED) or an index in kvec_unit_shift units into the node's global record.
 template <int KP, bool STAGED>
 __device__ __forceinline__ void fast_kvec(lds_char *lds, global_char *gtab, uint32_t idx, float (&f)[KP]) {
     if (STAGED) read_kvec_lds<KP>(lds + idx, f);
-    else read_kvec_global<KP>(gtab + (idx << log2i(4 * KP)), f);
+    else read_kvec_global<KP>(gtab + (idx << kvec_unit_shift<KP>()), f);
 }
 
 // Exact power-of-two rescale so that max_k w[k] lands in [0.5, 1).
@@ -640,7 +656,7 @@ __device__ __forceinline__ void product_replicas(const SweepParams &P, const Wor
 // Fast product path (classes 0 and 1, KP <= 8): replicas in groups of NR
 // (one at a time in debug mode, where the conditionals are written out).
 template <int KP, typename ST, bool DEBUG, bool STAGED, int NR>
-__device__ void sweep_product(const SweepParams &P, const Work &W, lds_char *lds, global_char *gtab) {
+__device__ __forceinline__ void sweep_product(const SweepParams &P, const Work &W, lds_char *lds, global_char *gtab) {
     cint32_t *d = W.d;
     const int K = d[0], n_groups = d[8], n_staged = STAGED ? d[13] : 0;
     cint32_t *grp = d + d[9];
@@ -685,6 +701,7 @@ __device__ void table_debug_probs(const SweepParams &P, const Work &W, int r, in
     }
     if (KP == 2) SAME_TABLE_DEBUG(2)
     else if (KP == 4) SAME_TABLE_DEBUG(4)
+    else if (KP == 6) SAME_TABLE_DEBUG(6)
     else if (KP == 8) SAME_TABLE_DEBUG(8)
     else SAME_TABLE_DEBUG(16)
 #undef SAME_TABLE_DEBUG
@@ -783,7 +800,7 @@ __device__ __forceinline__ void table_replicas(const SweepParams &P, const Work 
 // thresholds; the drawn state is the number of thresholds at or below the
 // 24-bit uniform.  Replicas in groups of NR (one at a time in debug mode).
 template <int KT, typename ST, bool DEBUG, bool STAGED, int NR>
-__device__ void sweep_table(const SweepParams &P, const Work &W, lds_char *lds, global_char *gcond) {
+__device__ __forceinline__ void sweep_table(const SweepParams &P, const Work &W, lds_char *lds, global_char *gcond) {
     cint32_t *d = W.d;
     cint32_t *grp = d + d[9];
     const bool tab_lds = STAGED && d[13] > 0;  // uniform: thresholds staged in LDS
@@ -834,6 +851,7 @@ __global__ __launch_bounds__(kSweepBlock, DEBUG ? 1 : kSweepWaves) void sweep_fa
     global_char *gt = scalar_global_ptr(tab);
     if (mode == kModeKP2) sweep_product<2, ST, DEBUG, STAGED, kPairKP2>(P, W, lds, gt);
     else if (mode == kModeKP4) sweep_product<4, ST, DEBUG, STAGED, kPairKP4>(P, W, lds, gt);
+    else if (mode == kModeKP6) sweep_product<6, ST, DEBUG, STAGED, kPairKP6>(P, W, lds, gt);
     else if (mode == kModeKP8) sweep_product<8, ST, DEBUG, STAGED, kPairKP8>(P, W, lds, gt);
     else {
         const int KT = d[7];
@@ -901,6 +919,7 @@ __global__ __launch_bounds__(kSweepBlock) void sweep_wide_kernel(SweepParams P) 
     const int KP = W.d[1];
     if (KP == 2) sweep_wide<2, ST, DEBUG>(P, W);
     else if (KP == 4) sweep_wide<4, ST, DEBUG>(P, W);
+    else if (KP == 6) sweep_wide<6, ST, DEBUG>(P, W);
     else if (KP == 8) sweep_wide<8, ST, DEBUG>(P, W);
     else sweep_wide<16, ST, DEBUG>(P, W);
 }
