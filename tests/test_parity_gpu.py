@@ -220,9 +220,9 @@ KERNEL_VARIANT_IDS = ["default", "global-tables", "wide-indices"]
 
 @pytest.mark.parametrize("variant", KERNEL_VARIANTS, ids=KERNEL_VARIANT_IDS)
 @pytest.mark.parametrize("table_limit", [None, 0], ids=["tables", "products"])
-@pytest.mark.parametrize("K", [2, 3, 5, 8, 9, 16, 17, 40])
+@pytest.mark.parametrize("K", [2, 3, 5, 6, 7, 8, 9, 16, 17, 40])
 def test_cardinality_classes(K, table_limit, variant):
-    # threshold tables for K <= 9, products with KP = 2/4/8/16, generic for K > 16
+    # threshold tables for K <= 9, products with KP = 2/4/6/8/16, generic for K > 16
     parents = [[], [0], [0, 1], [1], [2, 3]]
     card = [K, 3, K, 2, 4]
     net, st, ob, th = _custom(parents, card, 700, 3, 0.6, K)
