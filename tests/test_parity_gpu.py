@@ -214,8 +214,8 @@ def test_all_observed_and_all_latent():
     _custom_case(net, st, ob, th, 2, 512, win=(0, 512))
 
 
-KERNEL_VARIANTS = [dict(), dict(lds_limit=0), dict(packed=False)]
-KERNEL_VARIANT_IDS = ["default", "global-tables", "wide-indices"]
+KERNEL_VARIANTS = [dict(), dict(lds_limit=0), dict(lds_limit=256), dict(packed=False)]
+KERNEL_VARIANT_IDS = ["default", "global-tables", "partial-records", "wide-indices"]
 
 
 @pytest.mark.parametrize("variant", KERNEL_VARIANTS, ids=KERNEL_VARIANT_IDS)
@@ -263,8 +263,9 @@ def test_underflow_rescale_path():
     ob[0, :n_cols] = 0
     ob[1:, :n_cols] = 1
     st[1:, :, :n_cols] = 1
-    for tl in (None, 0):
-        gpu, ref, _ = _custom_case(net, st, ob, theta, m, n_cols, win=(0, 64), table_limit=tl)
+    # products from staged, global and partly staged records (budget 0 or 64 bytes)
+    for tl, lds in ((None, None), (0, None), (0, 0), (0, 64)):
+        gpu, ref, _ = _custom_case(net, st, ob, theta, m, n_cols, win=(0, 64), table_limit=tl, lds_limit=lds)
         # the conditional of the root is exactly (1/2, 1/2); both states must appear
         assert 0 < gpu[0, :, :n_cols].mean() < 1
 
