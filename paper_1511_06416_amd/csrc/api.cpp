@@ -89,7 +89,7 @@ void free_tables(same::DeviceTables &t) {
     int cur = -1;
     (void)hipGetDevice(&cur);
     (void)hipSetDevice(t.device);
-    void *ptrs[] = {t.desc, t.desc_off, t.order, t.cdesc, t.cdesc_off, t.segs, t.blk_seg,
+    void *ptrs[] = {t.desc, t.desc_off, t.order, t.cdesc, t.cdesc_off, t.cwork, t.segs, t.blk_seg,
                     t.blk_first, t.row_off, t.row_k, t.cprog, t.cprog_off, t.cblk_prog, t.cblk_first};
     for (void *p : ptrs)
         if (p) (void)hipFree(p);
@@ -135,6 +135,8 @@ int tables_for_current_device(same_ctx *ctx, same::DeviceTables **out) {
     if (r == hipSuccess) r = upload(&nt.order, g.order);
     if (r == hipSuccess) r = upload(&nt.cdesc, g.cdesc);
     if (r == hipSuccess) r = upload(&nt.cdesc_off, g.cdesc_off);
+    if (r == hipSuccess) r = upload(&nt.cwork, g.cwork);
+    nt.n_cwork = (int32_t)(g.cwork.size() / 2);
     if (r == hipSuccess) r = upload(&nt.segs, g.segments);
     if (r == hipSuccess) r = upload(&nt.blk_seg, blk_seg);
     if (r == hipSuccess) r = upload(&nt.blk_first, blk_first);
@@ -433,7 +435,7 @@ int do_step(same_ctx *ctx, void *states, const uint8_t *obs, float *cpts, int32_
         rc = sweep_tile(ctx, P, t0, nt, s);
         if (rc) return rc;
         rc = check_hip(same::launch_counts(*t, (const char *)states + t0 * ctx->g.state_bytes,
-                                           ctx->g.state_bytes, ctx->g.n, m, nt, ld, newc, s),
+                                           ctx->g.state_bytes, m, nt, ld, newc, s),
                        "count launch");
         if (rc) return rc;
     }
@@ -585,7 +587,7 @@ int same_counts(same_ctx *ctx, const void *states, int32_t m, int64_t n_cols, in
     int32_t *newc = (int32_t *)((char *)workspace + ctx->ws_counts);
     rc = check_hip(same::launch_fill_zero(newc, total, s), "count clear launch");
     if (rc) return rc;
-    rc = check_hip(same::launch_counts(*t, states, ctx->g.state_bytes, ctx->g.n, m, n_cols, ld, newc, s),
+    rc = check_hip(same::launch_counts(*t, states, ctx->g.state_bytes, m, n_cols, ld, newc, s),
                    "count launch");
     if (rc) return rc;
     return check_hip(same::launch_moving_sum(newc, mb_counts, totals, total, s), "moving-sum launch");
@@ -764,7 +766,7 @@ int same_counts_ema(same_ctx *ctx, const void *states, int32_t m, int64_t n_cols
     int32_t *newc = (int32_t *)((char *)workspace + ctx->ws_counts);
     rc = check_hip(same::launch_fill_zero(newc, total, s), "count clear launch");
     if (rc) return rc;
-    rc = check_hip(same::launch_counts(*t, states, ctx->g.state_bytes, ctx->g.n, m, n_cols, ld, newc, s),
+    rc = check_hip(same::launch_counts(*t, states, ctx->g.state_bytes, m, n_cols, ld, newc, s),
                    "count launch");
     if (rc) return rc;
     return check_hip(same::launch_ema(newc, totals, decay, total, s), "moving-sum launch");

@@ -447,6 +447,15 @@ int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int
             if (!ok) return fail(err, SAME_ESIZE, "packed sweep index overflow");
         }
 
+        if (g.rows[i] * K > kCountSplitBins) {
+            g.cwork.push_back(i);
+            g.cwork.push_back(-1);
+        } else {
+            for (int64_t lo = 0; lo == 0 || lo < g.rows[i] * K; lo += kCountLdsBins) {
+                g.cwork.push_back(i);
+                g.cwork.push_back((int32_t)lo);
+            }
+        }
         g.cdesc_off[i] = (int32_t)g.cdesc.size();
         g.cdesc.push_back(K);
         g.cdesc.push_back(pptr[i + 1] - pptr[i]);

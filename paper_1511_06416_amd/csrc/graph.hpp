@@ -68,6 +68,8 @@ constexpr int64_t kLdsBudgetBytes = 32768;   // largest LDS staging budget per b
 constexpr int64_t kDefaultLdsBytes = 24576;  // default budget: 6 blocks per CU (measured best)
 constexpr int32_t kDescHeader = 16;
 constexpr int64_t kPackedLimit = 65536;      // packed indices are 16-bit
+constexpr int32_t kCountLdsBins = 8192;      // bins of the count kernel's LDS histogram
+constexpr int64_t kCountSplitBins = 4 * kCountLdsBins;  // largest CPT counted in ranges
 
 // Sweep descriptor of a node (int32 words at desc_off[i]):
 //   [0] K  [1] KP  [2] mode  [3] tab_begin  [4] tab_len (floats)
@@ -140,6 +142,12 @@ struct Compiled {
     // same for the count kernel: [K, n_par, n_bins, cpt_off, (par_node, stride) * n_par]
     std::vector<int32_t> cdesc;
     std::vector<int32_t> cdesc_off;  // [n]
+    // count work items (node, first bin): one per node, and one per range of
+    // kCountLdsBins bins for a CPT larger than the count kernel's LDS
+    // histogram, up to kCountSplitBins bins (each range's blocks read the
+    // node's rows again); a larger CPT has one item with first bin -1, whose
+    // blocks add to global memory directly
+    std::vector<int32_t> cwork;
 
     // colour-ordered node list (colour 0 nodes, then colour 1, ...; inside a
     // colour grouped by launch class) and, per colour, the start of each class

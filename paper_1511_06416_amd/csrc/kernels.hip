@@ -1108,11 +1108,15 @@ __global__ void fill_zero_kernel(int32_t *p, int64_t count) {
 // Histogram of (parent row, state) for one node over a run of columns and all
 // m replicas.  Small CPTs (<= kRepBins bins) use kCopies interleaved LDS
 // copies, lane l adding into copy l % kCopies, so lanes hitting the same bin
-// rarely collide; mid-size CPTs share one LDS histogram; CPTs beyond LDS go
-// straight to global atomics.  Each block flushes its non-zero bins once.
+// rarely collide; larger CPTs share one LDS histogram of at most kLdsBins
+// bins: a count work item covers the bins [lo, lo + kLdsBins) of its node,
+// and a CPT with more bins has one work item per range, each reading the
+// node's rows and counting only its own bins.  CPTs beyond kCountSplitBins
+// (lo = -1) go straight to global atomics.  Each block flushes its non-zero
+// bins once.
 constexpr int kCopies = 32;
 constexpr int kRepBins = 256;
-constexpr int kLdsBins = 8192;
+constexpr int kLdsBins = kCountLdsBins;
 static_assert(kCopies * kRepBins <= kLdsBins, "LDS budget");
 
 constexpr int kCountReps = 10;  // replicas whose rows are loaded together (measured best on m = 10)
@@ -1124,6 +1128,7 @@ constexpr int kCountReps = 10;  // replicas whose rows are loaded together (meas
 template <typename ST>
 __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict__ cdesc,
                                                       const int32_t *__restrict__ cdesc_off,
+                                                      const int32_t *__restrict__ cwork,
                                                       int32_t count, int64_t n_slabs,
                                                       int64_t cols_per_block,
                                                       const ST *__restrict__ states, int32_t m,
@@ -1135,12 +1140,14 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
     int64_t slab;
     decode_block(blockIdx.x, (uint32_t)count, node_u, slab);
     if (slab >= n_slabs) return;  // uniform across the block
-    const int node = (int)node_u;
+    const int node = as_const(cwork)[2 * node_u];
+    const int lo = as_const(cwork)[2 * node_u + 1];
     cint32_t *d = as_const(cdesc) + as_const(cdesc_off)[node];
     const int K = d[0], n_par = d[1], nbins = d[2], off = d[3];
     cint32_t *par = d + 4;
-    const int mode = nbins <= kRepBins ? 0 : (nbins <= kLdsBins ? 1 : 2);
-    const int lds_words = mode == 0 ? nbins * kCopies : (mode == 1 ? nbins : 0);
+    const int mode = nbins <= kRepBins ? 0 : (lo >= 0 ? 1 : 2);
+    const int range = nbins - lo < kLdsBins ? nbins - lo : kLdsBins;  // mode 1: this item's bins
+    const int lds_words = mode == 0 ? nbins * kCopies : (mode == 1 ? range : 0);
     for (int b = threadIdx.x; b < lds_words; b += kBlock) hist[b] = 0;
     __syncthreads();
     const int copy = threadIdx.x & (kCopies - 1);
@@ -1149,9 +1156,14 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
     const int64_t vstride = (int64_t)m * ld;
     const bool packed = nbins <= 65536;
     auto add = [&](int bin) {
-        if (mode == 0) atomicAdd(&hist[bin * kCopies + copy], 1);
-        else if (mode == 1) atomicAdd(&hist[bin], 1);
-        else atomicAdd(&counts[off + bin], 1);
+        if (mode == 0) {
+            atomicAdd(&hist[bin * kCopies + copy], 1);
+        } else if (mode == 1) {
+            const uint32_t hb = (uint32_t)(bin - lo);
+            if (hb < (uint32_t)range) atomicAdd(&hist[hb], 1);
+        } else {
+            atomicAdd(&counts[off + bin], 1);
+        }
     };
     for (int64_t col = c0 + 4 * (int64_t)threadIdx.x; col < c1; col += 4 * kBlock) {
         const int nvalid = c1 - col < 4 ? (int)(c1 - col) : 4;
@@ -1226,7 +1238,7 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
     }
     if (mode == 2) return;
     __syncthreads();
-    for (int b = threadIdx.x; b < nbins; b += kBlock) {
+    for (int b = threadIdx.x; b < (mode == 0 ? nbins : range); b += kBlock) {
         int v;
         if (mode == 0) {
             v = 0;
@@ -1235,7 +1247,7 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
         } else {
             v = hist[b];
         }
-        if (v) atomicAdd(&counts[off + b], v);
+        if (v) atomicAdd(&counts[off + lo + b], v);
     }
 }
 
@@ -1549,9 +1561,9 @@ hipError_t launch_fill_zero(int32_t *p, int64_t count, hipStream_t stream) {
 }
 
 hipError_t launch_counts(const DeviceTables &t, const void *states, int32_t state_bytes,
-                         int32_t n, int32_t m, int64_t n_cols, int64_t ld, int32_t *counts,
-                         hipStream_t stream) {
+                         int32_t m, int64_t n_cols, int64_t ld, int32_t *counts, hipStream_t stream) {
     if (n_cols <= 0) return hipSuccess;
+    const int32_t n = t.n_cwork;
     // one node x kCountQuadsPerLane quads per lane x all replicas per block,
     // XCD-swizzled like the sweep
     const int64_t cols_per_block = 4 * dev::kBlock * dev::kCountQuadsPerLane;
@@ -1562,12 +1574,12 @@ hipError_t launch_counts(const DeviceTables &t, const void *states, int32_t stat
     const dim3 grid((unsigned)blocks);
     if (state_bytes == 1)
         hipLaunchKernelGGL(dev::count_kernel<int8_t>, grid, dim3(dev::kBlock), 0, stream, t.cdesc,
-                           t.cdesc_off, n, n_slabs, cols_per_block, (const int8_t *)states, m, n_cols,
-                           ld, counts);
+                           t.cdesc_off, t.cwork, n, n_slabs, cols_per_block, (const int8_t *)states, m,
+                           n_cols, ld, counts);
     else
         hipLaunchKernelGGL(dev::count_kernel<int16_t>, grid, dim3(dev::kBlock), 0, stream, t.cdesc,
-                           t.cdesc_off, n, n_slabs, cols_per_block, (const int16_t *)states, m, n_cols,
-                           ld, counts);
+                           t.cdesc_off, t.cwork, n, n_slabs, cols_per_block, (const int16_t *)states, m,
+                           n_cols, ld, counts);
     return hipGetLastError();
 }
 

@@ -17,6 +17,8 @@ struct DeviceTables {
     int32_t *order = nullptr;      // colour-ordered nodes
     int32_t *cdesc = nullptr;      // count descriptor stream: [K, n_par, nbins, cpt_off, (p, stride)*]
     int32_t *cdesc_off = nullptr;  // [n]
+    int32_t *cwork = nullptr;      // count work items (node, first bin)
+    int32_t n_cwork = 0;
     Segment *segs = nullptr;
     int32_t *blk_seg = nullptr;    // table-build block -> segment
     int32_t *blk_first = nullptr;  // table-build block -> first group
@@ -70,9 +72,9 @@ hipError_t launch_sweep(SweepParams P, int32_t begin, int32_t count, int32_t kla
 
 hipError_t launch_fill_zero(int32_t *p, int64_t count, hipStream_t stream);
 
+// Histograms of every node's family (the count work items of t).
 hipError_t launch_counts(const DeviceTables &t, const void *states, int32_t state_bytes,
-                         int32_t n, int32_t m, int64_t n_cols, int64_t ld, int32_t *counts,
-                         hipStream_t stream);
+                         int32_t m, int64_t n_cols, int64_t ld, int32_t *counts, hipStream_t stream);
 
 // Dense minibatch from CSR known entries (rows = nodes): clears obs, then
 // one thread per entry writes obs and every replica's state.

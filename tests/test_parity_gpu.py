@@ -310,10 +310,14 @@ def test_counts_bit_exact_and_moving_sum(cfg, kw):
     assert np.array_equal(mb.cpu().numpy(), want)
 
 
-def test_counts_large_cpt_uses_global_atomics():
-    # one node with 4 parents of cardinality 8 and K=3: 12288 bins > LDS capacity
-    parents = [[], [], [], [], [0, 1, 2, 3]]
-    card = [8, 8, 8, 8, 3]
+@pytest.mark.parametrize("n_par,K", [(4, 3), (4, 4), (4, 9), (5, 3)],
+                         ids=["12288-bins-2-ranges", "16384-bins-2-ranges", "36864-bins-global",
+                              "98304-bins-32bit-global"])
+def test_counts_large_cpt(n_par, K):
+    # one node whose CPT exceeds the count kernel's 8192-bin LDS histogram:
+    # counted in LDS ranges up to 32768 bins, with global atomics beyond
+    parents = [[] for _ in range(n_par)] + [list(range(n_par))]
+    card = [8] * n_par + [K]
     net, st, _, _ = _custom(parents, card, 5000, 3, 0.0, 12)
     ctx = H.context_for(net)
     mb = torch.zeros(ctx.cpt_total, dtype=torch.int32, device="cuda")
