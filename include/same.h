@@ -99,7 +99,8 @@ typedef struct {
     /* Largest (blanket configurations) x (thresholds per configuration) for
      * which a node's full conditional is precomputed into a table of CDF
      * thresholds (one table per CPT update; the draw becomes one table read).
-     * -1 selects the default (16384); 0 disables the tables, so every node
+     * -1 selects the default (6144, so that a table fits the default LDS
+     * staging budget below); 0 disables the tables, so every node
      * forms its conditional from CPT entries during the sweep.  Either way the
      * sweep draws from the same conditional with the same uniforms. */
     int64_t table_limit;

@@ -474,7 +474,7 @@ int same_create_ex(int32_t n_nodes, const int32_t *parent_ptr, const int32_t *pa
                    const int32_t *card, double dirichlet_prior, const same_options_t *opts,
                    same_ctx **out) {
     if (!out) return set_error(SAME_EINVAL, "out is null");
-    int64_t table_limit = 16384;
+    int64_t table_limit = same::kDefaultTableLimit;
     if (opts && opts->table_limit >= 0) table_limit = opts->table_limit;
     if (opts && opts->table_limit < -1) return set_error(SAME_EINVAL, "table_limit must be >= -1");
     if (opts && opts->tile_bytes < 0) return set_error(SAME_EINVAL, "tile_bytes must be >= 0");

@@ -66,6 +66,9 @@ enum SweepMode : int32_t {
 constexpr int32_t kLaunchClasses = 4;
 constexpr int64_t kLdsBudgetBytes = 32768;   // largest LDS staging budget per block
 constexpr int64_t kDefaultLdsBytes = 24576;  // default budget: 6 blocks per CU (measured best)
+// default threshold-table limit (entries): a table then fits the default LDS
+// budget, so no threshold node gathers from global memory (measured best)
+constexpr int64_t kDefaultTableLimit = kDefaultLdsBytes / 4;
 constexpr int32_t kDescHeader = 16;
 constexpr int64_t kPackedLimit = 65536;      // packed indices are 16-bit
 constexpr int32_t kCountLdsBins = 8192;      // bins of the count kernel's LDS histogram
@@ -169,7 +172,7 @@ struct Compiled {
 // record staged whole, and the most a larger record stages of its groups.
 // packed: false sends every product-mode node to the wide class.
 int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int32_t *card,
-                  Compiled &out, std::string &err, int64_t table_limit = 16384,
+                  Compiled &out, std::string &err, int64_t table_limit = kDefaultTableLimit,
                   int64_t lds_limit = kDefaultLdsBytes, bool packed = true);
 
 }  // namespace same
