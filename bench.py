@@ -690,23 +690,38 @@ def cpu_baseline(w, cols, st, ob, steps):
     and one Dirichlet resample."""
     import oracle
 
+    import numpy as np
     net = w.net
     threads = len(os.sched_getaffinity(0))
     color = oracle.graph(net.parents, net.card)["color"]
-    theta = w.init_theta
-    t = time.perf_counter()
-    for s in range(steps):
-        oracle.sweep(net.parents, net.card, theta, color, st, ob, w.m, cols, 0, w.seed, s,
-                     n_threads=threads)
-        cnt = oracle.counts(net.parents, net.card, st, w.m, cols, n_threads=threads)
-        theta = oracle.dirichlet(net.parents, net.card, cnt, w.alpha, w.seed, s)
-    dt = time.perf_counter() - t
+    # a smaller sample for the one-thread rate, cut before the states change
+    cols1 = min(cols, 10_000) // 4 * 4
+    st1 = np.ascontiguousarray(st[:, :, :cols1])
+    ob1 = np.ascontiguousarray(ob[:, :cols1])
+
+    def run(st, ob, cols, steps, n_threads):
+        theta = w.init_theta
+        t = time.perf_counter()
+        for s in range(steps):
+            oracle.sweep(net.parents, net.card, theta, color, st, ob, w.m, cols, 0, w.seed, s,
+                         n_threads=n_threads)
+            cnt = oracle.counts(net.parents, net.card, st, w.m, cols, n_threads=n_threads)
+            theta = oracle.dirichlet(net.parents, net.card, cnt, w.alpha, w.seed, s)
+        return time.perf_counter() - t
+
+    dt = run(st, ob, cols, steps, threads)
     ns = float(net.n) * cols * w.m * steps
     log("cpu baseline: %d columns x %d steps, %.2f s, %d threads" % (cols, steps, dt, threads))
+    dt1 = run(st1, ob1, cols1, 1, 1) if cols1 > 0 else 0.0
+    ns1 = float(net.n) * cols1 * w.m
+    log("cpu baseline, one thread: %d columns x 1 step, %.2f s" % (cols1, dt1))
     return {"value": round(ns / dt, 1), "unit": "node-samples/s", "cores": threads,
             "kind": "oracle",
             "sample": "first %d columns of minibatch 0 (all %d nodes, m=%d), %d SAME steps (sweep + "
-                      "counts + Dirichlet resample each), %.1f s" % (cols, net.n, w.m, steps, dt)}
+                      "counts + Dirichlet resample each), %.1f s" % (cols, net.n, w.m, steps, dt),
+            "one_thread": None if dt1 <= 0 else {
+                "value": round(ns1 / dt1, 1),
+                "sample": "first %d columns of minibatch 0, 1 SAME step, %.1f s" % (cols1, dt1)}}
 
 
 if __name__ == "__main__":
