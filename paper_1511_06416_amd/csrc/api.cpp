@@ -3,7 +3,6 @@
 // each entry point.
 #include <hip/hip_runtime.h>
 
-#include <algorithm>
 #include <cstdint>
 #include <cstring>
 #include <mutex>
