@@ -533,7 +533,7 @@ struct Work {
 constexpr uint32_t kXcds = 8;
 constexpr int kSweepQuadsPerLane = 1;  // column quads per lane in one sweep block
 constexpr int kMinSweepBlocks = 4096;  // replicas are split below this many blocks
-constexpr int kCountQuadsPerLane = 2;  // column quads per lane in one count block
+constexpr int kCountQuadsPerLane = 2;  // column quads per lane in one count block (one pair)
 
 __device__ __forceinline__ void decode_block(uint32_t b, uint32_t count, uint32_t &local,
                                              int64_t &slab) {
@@ -1119,13 +1119,76 @@ constexpr int kRepBins = 256;
 constexpr int kLdsBins = kCountLdsBins;
 static_assert(kCopies * kRepBins <= kLdsBins, "LDS budget");
 
+// Eight consecutive states of one row (two column quads) at byte offset boff,
+// as W = (quad 0, quad 1).  WIDE (rows of at least 8 columns): one 8-byte
+// load for int8 states, 16 for int16; where the pair would run past the end of
+// the row (pair false: a last quad with col + 8 > ld, so col >= 8) the load
+// starts one quad earlier, stays inside the row, and quad 1 reads as 0.  The
+// choice is a select, not a branch, so that the loads of all replicas and
+// parents stay in flight together.  Not WIDE: one load per quad, each wholly
+// inside or wholly past the node's buffer.
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+template <typename ST>
+struct Oct;
+
+template <>
+struct Oct<int8_t> {
+    using W = u32x2;
+    template <bool WIDE>
+    __device__ static W load(const int8_t *__restrict__ states, int32_t node, int64_t vstride, uint32_t boff,
+                             bool pair) {
+        const __amdgpu_buffer_rsrc_t r = buffer_rsrc(states + (int64_t)node * vstride, (uint32_t)vstride);
+        W w;
+        if (WIDE) {
+            const W v = __builtin_amdgcn_raw_buffer_load_b64(r, (int)(pair ? boff : boff - 4u), 0, 0);
+            w.x = pair ? v.x : v.y;
+            w.y = pair ? v.y : 0u;
+        } else {
+            w.x = __builtin_amdgcn_raw_buffer_load_b32(r, (int)boff, 0, 0);
+            w.y = __builtin_amdgcn_raw_buffer_load_b32(r, (int)boff + 4, 0, 0);
+        }
+        return w;
+    }
+    __device__ static uint32_t quad(W w, int h) { return h ? w.y : w.x; }
+};
+
+template <>
+struct Oct<int16_t> {
+    using W = u32x4;
+    template <bool WIDE>
+    __device__ static W load(const int16_t *__restrict__ states, int32_t node, int64_t vstride, uint32_t boff,
+                             bool pair) {
+        const __amdgpu_buffer_rsrc_t r =
+            buffer_rsrc(states + (int64_t)node * vstride, (uint32_t)(vstride * (int64_t)sizeof(int16_t)));
+        W w;
+        if (WIDE) {
+            const W v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)(pair ? boff : boff - 8u), 0, 0);
+            w.x = pair ? v.x : v.z;
+            w.y = pair ? v.y : v.w;
+            w.z = pair ? v.z : 0u;
+            w.w = pair ? v.w : 0u;
+        } else {
+            const u32x2 lo = __builtin_amdgcn_raw_buffer_load_b64(r, (int)boff, 0, 0);
+            const u32x2 hi = __builtin_amdgcn_raw_buffer_load_b64(r, (int)boff + 8, 0, 0);
+            w.x = lo.x;
+            w.y = lo.y;
+            w.z = hi.x;
+            w.w = hi.y;
+        }
+        return w;
+    }
+    __device__ static uint2 quad(W w, int h) { return h ? make_uint2(w.z, w.w) : make_uint2(w.x, w.y); }
+};
+
 constexpr int kCountReps = 10;  // replicas whose rows are loaded together (measured best on m = 10)
 
 // Histogram of (parent row, state) for one node over a slab of columns and all
 // m replicas (block geometry as the sweep's, decode_block).  Bins are counted
 // with packed 16-bit arithmetic (two lanes per word, as in the sweep) when the
 // node has at most 2^16 bins, else with 32-bit indices.
-template <typename ST>
+template <typename ST, bool WIDE>
 __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict__ cdesc,
                                                       const int32_t *__restrict__ cdesc_off,
                                                       const int32_t *__restrict__ cwork,
@@ -1165,12 +1228,14 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
             atomicAdd(&counts[off + bin], 1);
         }
     };
-    for (int64_t col = c0 + 4 * (int64_t)threadIdx.x; col < c1; col += 4 * kBlock) {
-        const int nvalid = c1 - col < 4 ? (int)(c1 - col) : 4;
+    // a lane covers two adjacent column quads, read with one load per row
+    for (int64_t col = c0 + 8 * (int64_t)threadIdx.x; col < c1; col += 8 * kBlock) {
+        const int nvalid = c1 - col < 8 ? (int)(c1 - col) : 8;
+        const bool pair = col + 8 <= ld;
         for (int r0 = 0; r0 < m; r0 += kCountReps) {
             const int nr = m - r0 < kCountReps ? m - r0 : kCountReps;
             uint32_t boff[kCountReps];
-            typename Q::V own[kCountReps];
+            typename Oct<ST>::W own[kCountReps];
             // every slot loads (a fixed count keeps all loads in flight at
             // once); slots past the last replica read through the node's
             // buffer resource past its end, which returns 0 without a memory
@@ -1178,60 +1243,71 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
 #pragma unroll
             for (int t = 0; t < kCountReps; ++t) {
                 boff[t] = (uint32_t)((r0 + t) * ld + col) * (uint32_t)sizeof(ST);
-                own[t] = load_row<ST>(states, node, vstride, boff[t]);
+                own[t] = Oct<ST>::template load<WIDE>(states, node, vstride, boff[t], pair);
             }
             if (packed) {
                 // bin = sum over parents of x_p * (stride_p * K) + x_node
-                uint32_t Pk[kCountReps][2];
-#pragma unroll
-                for (int t = 0; t < kCountReps; ++t) Q::split(own[t], Pk[t]);
-                for (int q = 0; q < n_par; ++q) {
-                    const uint32_t mult = (uint32_t)(par[2 * q + 1] * K) * 0x10001u;
-                    typename Q::V sp[kCountReps];
-#pragma unroll
-                    for (int t = 0; t < kCountReps; ++t)
-                        sp[t] = load_row<ST>(states, par[2 * q], vstride, boff[t]);
-#pragma unroll
-                    for (int t = 0; t < kCountReps; ++t) {
-                        if (t >= nr) break;
-                        uint32_t p2[2];
-                        Q::split(sp[t], p2);
-                        Pk[t][0] = pk_mad_u16(p2[0], mult, Pk[t][0]);
-                        Pk[t][1] = pk_mad_u16(p2[1], mult, Pk[t][1]);
-                    }
-                }
-#pragma unroll
-                for (int t = 0; t < kCountReps; ++t) {
-                    if (t >= nr) break;
-#pragma unroll
-                    for (int c = 0; c < 4; ++c)
-                        if (c < nvalid) add((int)packed_index<ST>(Pk[t], c));
-                }
-            } else {
-                uint32_t u[kCountReps][4];
+                uint32_t Pk[kCountReps][2][2];
 #pragma unroll
                 for (int t = 0; t < kCountReps; ++t)
 #pragma unroll
-                    for (int c = 0; c < 4; ++c) u[t][c] = 0;
+                    for (int h = 0; h < 2; ++h) Q::split(Oct<ST>::quad(own[t], h), Pk[t][h]);
                 for (int q = 0; q < n_par; ++q) {
-                    const uint32_t stride = (uint32_t)par[2 * q + 1];
-                    typename Q::V sp[kCountReps];
+                    const uint32_t mult = (uint32_t)(par[2 * q + 1] * K) * 0x10001u;
+                    typename Oct<ST>::W sp[kCountReps];
 #pragma unroll
                     for (int t = 0; t < kCountReps; ++t)
-                        sp[t] = load_row<ST>(states, par[2 * q], vstride, boff[t]);
+                        sp[t] = Oct<ST>::template load<WIDE>(states, par[2 * q], vstride, boff[t], pair);
+                    // slots past the last replica compute on zeros and are
+                    // never counted: no exit from the unrolled loop
 #pragma unroll
                     for (int t = 0; t < kCountReps; ++t) {
-                        if (t >= nr) break;
 #pragma unroll
-                        for (int c = 0; c < 4; ++c) u[t][c] += (uint32_t)Q::get(sp[t], c) * stride;
+                        for (int h = 0; h < 2; ++h) {
+                            uint32_t p2[2];
+                            Q::split(Oct<ST>::quad(sp[t], h), p2);
+                            Pk[t][h][0] = pk_mad_u16(p2[0], mult, Pk[t][h][0]);
+                            Pk[t][h][1] = pk_mad_u16(p2[1], mult, Pk[t][h][1]);
+                        }
                     }
                 }
 #pragma unroll
                 for (int t = 0; t < kCountReps; ++t) {
-                    if (t >= nr) break;
+                    if (t < nr) {  // uniform
 #pragma unroll
-                    for (int c = 0; c < 4; ++c)
-                        if (c < nvalid) add((int)(u[t][c] * (uint32_t)K + (uint32_t)Q::get(own[t], c)));
+                        for (int h = 0; h < 2; ++h)
+#pragma unroll
+                            for (int c = 0; c < 4; ++c)
+                                if (4 * h + c < nvalid) add((int)packed_index<ST>(Pk[t][h], c));
+                    }
+                }
+            } else {
+                // 32-bit indices (more than 2^16 bins): one quad at a time
+                for (int h = 0; h < 2; ++h) {
+                    uint32_t u[kCountReps][4];
+#pragma unroll
+                    for (int t = 0; t < kCountReps; ++t)
+#pragma unroll
+                        for (int c = 0; c < 4; ++c) u[t][c] = 0;
+                    for (int q = 0; q < n_par; ++q) {
+                        const uint32_t stride = (uint32_t)par[2 * q + 1];
+#pragma unroll
+                        for (int t = 0; t < kCountReps; ++t) {
+                            if (t >= nr) break;
+                            const typename Q::V sp =
+                                Oct<ST>::quad(Oct<ST>::template load<WIDE>(states, par[2 * q], vstride, boff[t], pair), h);
+#pragma unroll
+                            for (int c = 0; c < 4; ++c) u[t][c] += (uint32_t)Q::get(sp, c) * stride;
+                        }
+                    }
+#pragma unroll
+                    for (int t = 0; t < kCountReps; ++t) {
+                        if (t >= nr) break;
+                        const typename Q::V ov = Oct<ST>::quad(own[t], h);
+#pragma unroll
+                        for (int c = 0; c < 4; ++c)
+                            if (4 * h + c < nvalid) add((int)(u[t][c] * (uint32_t)K + (uint32_t)Q::get(ov, c)));
+                    }
                 }
             }
         }
@@ -1572,14 +1648,18 @@ hipError_t launch_counts(const DeviceTables &t, const void *states, int32_t stat
     const int64_t blocks = rounds * dev::kXcds * n;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
     const dim3 grid((unsigned)blocks);
-    if (state_bytes == 1)
-        hipLaunchKernelGGL(dev::count_kernel<int8_t>, grid, dim3(dev::kBlock), 0, stream, t.cdesc,
-                           t.cdesc_off, t.cwork, n, n_slabs, cols_per_block, (const int8_t *)states, m,
-                           n_cols, ld, counts);
-    else
-        hipLaunchKernelGGL(dev::count_kernel<int16_t>, grid, dim3(dev::kBlock), 0, stream, t.cdesc,
-                           t.cdesc_off, t.cwork, n, n_slabs, cols_per_block, (const int16_t *)states, m,
-                           n_cols, ld, counts);
+#define SAME_LAUNCH_COUNTS(ST, WIDE)                                                                    \
+    hipLaunchKernelGGL((dev::count_kernel<ST, WIDE>), grid, dim3(dev::kBlock), 0, stream, t.cdesc, t.cdesc_off, \
+                       t.cwork, n, n_slabs, cols_per_block, (const ST *)states, m, n_cols, ld, counts)
+    // rows of at least 8 columns take one load per column pair
+    if (state_bytes == 1) {
+        if (ld >= 8) SAME_LAUNCH_COUNTS(int8_t, true);
+        else SAME_LAUNCH_COUNTS(int8_t, false);
+    } else {
+        if (ld >= 8) SAME_LAUNCH_COUNTS(int16_t, true);
+        else SAME_LAUNCH_COUNTS(int16_t, false);
+    }
+#undef SAME_LAUNCH_COUNTS
     return hipGetLastError();
 }
 

@@ -327,6 +327,22 @@ def test_counts_large_cpt(n_par, K):
     assert np.array_equal(mb.cpu().numpy(), oracle.counts(parents, card, st, 3, 5000))
 
 
+@pytest.mark.parametrize("n_cols,ld", [(3, 4), (4097, 4100), (2049, 2052), (6000, 6004)])
+@pytest.mark.parametrize("big", [False, True], ids=["int8", "int16"])
+def test_counts_ragged_rows(n_cols, ld, big):
+    # rows whose length ld is not a multiple of 8 columns: the last column pair
+    # of a row is read as one quad; padding holds out-of-range states
+    card = [130 if big else 3, 3, 200 if big else 4, 2, 5]
+    parents = [[], [0], [0, 1], [2], [1, 2, 3]]
+    net, st, _, _ = _custom(parents, card, n_cols, 3, 0.0, 21, ld=ld)
+    st[:, :, n_cols:] = 120
+    ctx = H.context_for(net)
+    mb = torch.zeros(ctx.cpt_total, dtype=torch.int32, device="cuda")
+    same.same_counts(ctx, torch.from_numpy(st).cuda(), 3, n_cols, ld, mb, None, ctx.new_workspace())
+    torch.cuda.synchronize()
+    assert np.array_equal(mb.cpu().numpy(), oracle.counts(parents, card, st, 3, n_cols))
+
+
 # ------------------------------------------------------------ Dirichlet
 
 @pytest.mark.parametrize("cfg,alpha", [(1, 1.0), (3, 1.0), (5, 1.0), (4, 0.3)])
