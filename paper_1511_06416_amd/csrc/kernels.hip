@@ -533,7 +533,7 @@ struct Work {
 constexpr uint32_t kXcds = 8;
 constexpr int kSweepQuadsPerLane = 1;  // column quads per lane in one sweep block
 constexpr int kMinSweepBlocks = 4096;  // replicas are split below this many blocks
-constexpr int kCountQuadsPerLane = 2;  // column quads per lane in one count block (one pair)
+constexpr int kCountQuadsPerLane = 4;  // adjacent column quads per lane in one count block
 
 __device__ __forceinline__ void decode_block(uint32_t b, uint32_t count, uint32_t &local,
                                              int64_t &slab) {
@@ -1119,70 +1119,59 @@ constexpr int kRepBins = 256;
 constexpr int kLdsBins = kCountLdsBins;
 static_assert(kCopies * kRepBins <= kLdsBins, "LDS budget");
 
-// Eight consecutive states of one row (two column quads) at byte offset boff,
-// as W = (quad 0, quad 1).  WIDE (rows of at least 8 columns): one 8-byte
-// load for int8 states, 16 for int16; where the pair would run past the end of
-// the row (pair false: a last quad with col + 8 > ld, so col >= 8) the load
-// starts one quad earlier, stays inside the row, and quad 1 reads as 0.  The
-// choice is a select, not a branch, so that the loads of all replicas and
-// parents stay in flight together.  Not WIDE: one load per quad, each wholly
-// inside or wholly past the node's buffer.
+// kCountQuadsPerLane adjacent column quads of one row at byte offset boff.
+// WIDE (rows of at least 4 * NQ columns): one 16-byte load per 16 bytes of
+// states (8-byte for two int8 quads); a lane whose quads would run past the
+// end of the row (whole false) loads them one at a time instead, each wholly
+// inside or wholly past the node's buffer.  Not WIDE: always one at a time.
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-template <typename ST>
-struct Oct;
+template <typename ST, int NQ>
+struct Span {
+    using V = typename Quad<ST>::V;
+    static constexpr int kWords = NQ * (int)sizeof(ST);  // 32-bit words of NQ quads
+    V q[NQ];
 
-template <>
-struct Oct<int8_t> {
-    using W = u32x2;
     template <bool WIDE>
-    __device__ static W load(const int8_t *__restrict__ states, int32_t node, int64_t vstride, uint32_t boff,
-                             bool pair) {
-        const __amdgpu_buffer_rsrc_t r = buffer_rsrc(states + (int64_t)node * vstride, (uint32_t)vstride);
-        W w;
-        if (WIDE) {
-            const W v = __builtin_amdgcn_raw_buffer_load_b64(r, (int)(pair ? boff : boff - 4u), 0, 0);
-            w.x = pair ? v.x : v.y;
-            w.y = pair ? v.y : 0u;
-        } else {
-            w.x = __builtin_amdgcn_raw_buffer_load_b32(r, (int)boff, 0, 0);
-            w.y = __builtin_amdgcn_raw_buffer_load_b32(r, (int)boff + 4, 0, 0);
-        }
-        return w;
-    }
-    __device__ static uint32_t quad(W w, int h) { return h ? w.y : w.x; }
-};
-
-template <>
-struct Oct<int16_t> {
-    using W = u32x4;
-    template <bool WIDE>
-    __device__ static W load(const int16_t *__restrict__ states, int32_t node, int64_t vstride, uint32_t boff,
-                             bool pair) {
+    __device__ void load(const ST *__restrict__ states, int32_t node, int64_t vstride, uint32_t boff,
+                         bool whole) {
         const __amdgpu_buffer_rsrc_t r =
-            buffer_rsrc(states + (int64_t)node * vstride, (uint32_t)(vstride * (int64_t)sizeof(int16_t)));
-        W w;
-        if (WIDE) {
-            const W v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)(pair ? boff : boff - 8u), 0, 0);
-            w.x = pair ? v.x : v.z;
-            w.y = pair ? v.y : v.w;
-            w.z = pair ? v.z : 0u;
-            w.w = pair ? v.w : 0u;
+            buffer_rsrc(states + (int64_t)node * vstride, (uint32_t)(vstride * (int64_t)sizeof(ST)));
+        if (WIDE && whole) {
+            uint32_t w[kWords];
+            if constexpr (kWords == 2) {
+                const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, (int)boff, 0, 0);
+                w[0] = v.x;
+                w[1] = v.y;
+            } else {
+                static_assert(kWords % 4 == 0, "16-byte pieces");
+#pragma unroll
+                for (int i = 0; i < kWords / 4; ++i) {
+                    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)boff + 16 * i, 0, 0);
+                    w[4 * i] = v.x;
+                    w[4 * i + 1] = v.y;
+                    w[4 * i + 2] = v.z;
+                    w[4 * i + 3] = v.w;
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < NQ; ++j) q[j] = from_words(w, j);
         } else {
-            const u32x2 lo = __builtin_amdgcn_raw_buffer_load_b64(r, (int)boff, 0, 0);
-            const u32x2 hi = __builtin_amdgcn_raw_buffer_load_b64(r, (int)boff + 8, 0, 0);
-            w.x = lo.x;
-            w.y = lo.y;
-            w.z = hi.x;
-            w.w = hi.y;
+#pragma unroll
+            for (int j = 0; j < NQ; ++j) q[j] = Quad<ST>::load_buffer(r, boff + 4u * j * (uint32_t)sizeof(ST));
         }
-        return w;
     }
-    __device__ static uint2 quad(W w, int h) { return h ? make_uint2(w.z, w.w) : make_uint2(w.x, w.y); }
+
+  private:
+    template <int N>
+    __device__ static V from_words(const uint32_t (&w)[N], int j) {
+        if constexpr (sizeof(ST) == 1) return w[j];
+        else return make_uint2(w[2 * j], w[2 * j + 1]);
+    }
 };
 
-constexpr int kCountReps = 10;  // replicas whose rows are loaded together (measured best on m = 10)
+constexpr int kCountReps = 5;  // replicas whose rows are loaded together (measured best on m = 10)
 
 // Histogram of (parent row, state) for one node over a slab of columns and all
 // m replicas (block geometry as the sweep's, decode_block).  Bins are counted
@@ -1228,14 +1217,44 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
             atomicAdd(&counts[off + bin], 1);
         }
     };
-    // a lane covers two adjacent column quads, read with one load per row
-    for (int64_t col = c0 + 8 * (int64_t)threadIdx.x; col < c1; col += 8 * kBlock) {
-        const int nvalid = c1 - col < 8 ? (int)(c1 - col) : 8;
-        const bool pair = col + 8 <= ld;
+    // a lane covers NQ adjacent column quads, read with wide loads per row
+    constexpr int NQ = kCountQuadsPerLane;
+    using S = Span<ST, NQ>;
+    for (int64_t col = c0 + 4 * NQ * (int64_t)threadIdx.x; col < c1; col += 4 * NQ * kBlock) {
+        const int nvalid = c1 - col < 4 * NQ ? (int)(c1 - col) : 4 * NQ;
+        const bool whole = col + 4 * NQ <= ld;
+        if (!packed) {
+            // 32-bit indices (more than 2^16 bins): one replica at a time
+            for (int r = 0; r < m; ++r) {
+                const uint32_t boff = (uint32_t)(r * ld + col) * (uint32_t)sizeof(ST);
+                S own;
+                own.template load<WIDE>(states, node, vstride, boff, whole);
+                uint32_t u[NQ][4];
+#pragma unroll
+                for (int h = 0; h < NQ; ++h)
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) u[h][c] = 0;
+                for (int q = 0; q < n_par; ++q) {
+                    const uint32_t stride = (uint32_t)par[2 * q + 1];
+                    S sp;
+                    sp.template load<WIDE>(states, par[2 * q], vstride, boff, whole);
+#pragma unroll
+                    for (int h = 0; h < NQ; ++h)
+#pragma unroll
+                        for (int c = 0; c < 4; ++c) u[h][c] += (uint32_t)Q::get(sp.q[h], c) * stride;
+                }
+#pragma unroll
+                for (int h = 0; h < NQ; ++h)
+#pragma unroll
+                    for (int c = 0; c < 4; ++c)
+                        if (4 * h + c < nvalid) add((int)(u[h][c] * (uint32_t)K + (uint32_t)Q::get(own.q[h], c)));
+            }
+            continue;
+        }
         for (int r0 = 0; r0 < m; r0 += kCountReps) {
             const int nr = m - r0 < kCountReps ? m - r0 : kCountReps;
             uint32_t boff[kCountReps];
-            typename Oct<ST>::W own[kCountReps];
+            S own[kCountReps];
             // every slot loads (a fixed count keeps all loads in flight at
             // once); slots past the last replica read through the node's
             // buffer resource past its end, which returns 0 without a memory
@@ -1243,71 +1262,41 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
 #pragma unroll
             for (int t = 0; t < kCountReps; ++t) {
                 boff[t] = (uint32_t)((r0 + t) * ld + col) * (uint32_t)sizeof(ST);
-                own[t] = Oct<ST>::template load<WIDE>(states, node, vstride, boff[t], pair);
+                own[t].template load<WIDE>(states, node, vstride, boff[t], whole);
             }
-            if (packed) {
-                // bin = sum over parents of x_p * (stride_p * K) + x_node
-                uint32_t Pk[kCountReps][2][2];
+            // bin = sum over parents of x_p * (stride_p * K) + x_node
+            uint32_t Pk[kCountReps][NQ][2];
+#pragma unroll
+            for (int t = 0; t < kCountReps; ++t)
+#pragma unroll
+                for (int h = 0; h < NQ; ++h) Q::split(own[t].q[h], Pk[t][h]);
+            for (int q = 0; q < n_par; ++q) {
+                const uint32_t mult = (uint32_t)(par[2 * q + 1] * K) * 0x10001u;
+                S sp[kCountReps];
 #pragma unroll
                 for (int t = 0; t < kCountReps; ++t)
-#pragma unroll
-                    for (int h = 0; h < 2; ++h) Q::split(Oct<ST>::quad(own[t], h), Pk[t][h]);
-                for (int q = 0; q < n_par; ++q) {
-                    const uint32_t mult = (uint32_t)(par[2 * q + 1] * K) * 0x10001u;
-                    typename Oct<ST>::W sp[kCountReps];
-#pragma unroll
-                    for (int t = 0; t < kCountReps; ++t)
-                        sp[t] = Oct<ST>::template load<WIDE>(states, par[2 * q], vstride, boff[t], pair);
-                    // slots past the last replica compute on zeros and are
-                    // never counted: no exit from the unrolled loop
-#pragma unroll
-                    for (int t = 0; t < kCountReps; ++t) {
-#pragma unroll
-                        for (int h = 0; h < 2; ++h) {
-                            uint32_t p2[2];
-                            Q::split(Oct<ST>::quad(sp[t], h), p2);
-                            Pk[t][h][0] = pk_mad_u16(p2[0], mult, Pk[t][h][0]);
-                            Pk[t][h][1] = pk_mad_u16(p2[1], mult, Pk[t][h][1]);
-                        }
-                    }
-                }
+                    sp[t].template load<WIDE>(states, par[2 * q], vstride, boff[t], whole);
+                // slots past the last replica compute on zeros and are never
+                // counted: no exit from the unrolled loop
 #pragma unroll
                 for (int t = 0; t < kCountReps; ++t) {
-                    if (t < nr) {  // uniform
 #pragma unroll
-                        for (int h = 0; h < 2; ++h)
-#pragma unroll
-                            for (int c = 0; c < 4; ++c)
-                                if (4 * h + c < nvalid) add((int)packed_index<ST>(Pk[t][h], c));
+                    for (int h = 0; h < NQ; ++h) {
+                        uint32_t p2[2];
+                        Q::split(sp[t].q[h], p2);
+                        Pk[t][h][0] = pk_mad_u16(p2[0], mult, Pk[t][h][0]);
+                        Pk[t][h][1] = pk_mad_u16(p2[1], mult, Pk[t][h][1]);
                     }
                 }
-            } else {
-                // 32-bit indices (more than 2^16 bins): one quad at a time
-                for (int h = 0; h < 2; ++h) {
-                    uint32_t u[kCountReps][4];
+            }
 #pragma unroll
-                    for (int t = 0; t < kCountReps; ++t)
+            for (int t = 0; t < kCountReps; ++t) {
+                if (t < nr) {  // uniform
 #pragma unroll
-                        for (int c = 0; c < 4; ++c) u[t][c] = 0;
-                    for (int q = 0; q < n_par; ++q) {
-                        const uint32_t stride = (uint32_t)par[2 * q + 1];
-#pragma unroll
-                        for (int t = 0; t < kCountReps; ++t) {
-                            if (t >= nr) break;
-                            const typename Q::V sp =
-                                Oct<ST>::quad(Oct<ST>::template load<WIDE>(states, par[2 * q], vstride, boff[t], pair), h);
-#pragma unroll
-                            for (int c = 0; c < 4; ++c) u[t][c] += (uint32_t)Q::get(sp, c) * stride;
-                        }
-                    }
-#pragma unroll
-                    for (int t = 0; t < kCountReps; ++t) {
-                        if (t >= nr) break;
-                        const typename Q::V ov = Oct<ST>::quad(own[t], h);
+                    for (int h = 0; h < NQ; ++h)
 #pragma unroll
                         for (int c = 0; c < 4; ++c)
-                            if (4 * h + c < nvalid) add((int)(u[t][c] * (uint32_t)K + (uint32_t)Q::get(ov, c)));
-                    }
+                            if (4 * h + c < nvalid) add((int)packed_index<ST>(Pk[t][h], c));
                 }
             }
         }
@@ -1651,12 +1640,12 @@ hipError_t launch_counts(const DeviceTables &t, const void *states, int32_t stat
 #define SAME_LAUNCH_COUNTS(ST, WIDE)                                                                    \
     hipLaunchKernelGGL((dev::count_kernel<ST, WIDE>), grid, dim3(dev::kBlock), 0, stream, t.cdesc, t.cdesc_off, \
                        t.cwork, n, n_slabs, cols_per_block, (const ST *)states, m, n_cols, ld, counts)
-    // rows of at least 8 columns take one load per column pair
+    // rows of at least 4 * kCountQuadsPerLane columns take the wide loads
     if (state_bytes == 1) {
-        if (ld >= 8) SAME_LAUNCH_COUNTS(int8_t, true);
+        if (ld >= 4 * dev::kCountQuadsPerLane) SAME_LAUNCH_COUNTS(int8_t, true);
         else SAME_LAUNCH_COUNTS(int8_t, false);
     } else {
-        if (ld >= 8) SAME_LAUNCH_COUNTS(int16_t, true);
+        if (ld >= 4 * dev::kCountQuadsPerLane) SAME_LAUNCH_COUNTS(int16_t, true);
         else SAME_LAUNCH_COUNTS(int16_t, false);
     }
 #undef SAME_LAUNCH_COUNTS
