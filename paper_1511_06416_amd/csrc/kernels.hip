@@ -69,11 +69,11 @@ template <>
 struct Quad<int16_t> {
     using V = uint2;
     __device__ static V load(const int16_t *p) { return *reinterpret_cast<const uint2 *>(p); }
-    // two 32-bit loads: the 64- and 128-bit raw buffer load builtins of this
-    // toolchain lower to a single dword load
+    // one 8-byte load (the quad's offset is a multiple of 8 bytes)
     __device__ static V load_buffer(__amdgpu_buffer_rsrc_t r, uint32_t boff) {
-        return make_uint2(__builtin_amdgcn_raw_buffer_load_b32(r, (int)boff, 0, 0),
-                          __builtin_amdgcn_raw_buffer_load_b32(r, (int)boff + 4, 0, 0));
+        typedef uint32_t w2 __attribute__((ext_vector_type(2)));
+        const w2 v = __builtin_amdgcn_raw_buffer_load_b64(r, (int)boff, 0, 0);
+        return make_uint2(v.x, v.y);
     }
     __device__ static void store(int16_t *p, V v) { *reinterpret_cast<uint2 *>(p) = v; }
     __device__ static int get(V v, int c) {
