@@ -184,6 +184,26 @@ int same_sweep_debug(same_ctx *ctx, void *states, const uint8_t *obs, const floa
                      void *workspace, void *stream);
 
 /*
+ * Parity/debug: the CDF threshold tables same_sweep draws from for the CPTs
+ * `cpts` (nodes whose Markov blanket has few configurations; see
+ * same_options_t.table_limit).  Such a node's table has one row of KT uint32
+ * words per configuration of its Markov blanket -- its parents, children and
+ * the children's other parents, each once, in ascending node id, the last
+ * one varying fastest -- holding T_k = ceil(2^24 S_k / Z) for k < K - 1 and
+ * 2^24 after that, where S_k / Z is the cumulative conditional of Sec. 4's
+ * Gibbs draw (own CPT entry times the children's entries) formed in fp64.
+ * The sweep's draw with 24-bit uniform u24 is #{k : T_k <= u24}.
+ * Host outputs: node_off[n] (word offset of node i's table, -1 for nodes that
+ * form their conditional from CPT entries), node_kt[n] (KT, 0 for those) and
+ * *words (total table words).  cond_out (device, nullable, 4-byte aligned,
+ * *words entries) receives the tables, built on `stream` in the workspace
+ * and copied out.  Errors: SAME_EINVAL for null ctx, outputs or (with
+ * cond_out) cpts/workspace; SAME_EALIGN; SAME_EHIP.
+ */
+int same_debug_thresholds(same_ctx *ctx, const float *cpts, int64_t *node_off, int32_t *node_kt,
+                          int64_t *words, uint32_t *cond_out, void *workspace, void *stream);
+
+/*
  * Sufficient statistics and their moving sum (Sec. 4): histogram of
  * (parent configuration, state) over columns [0, n_cols) and all m replicas of
  * states [n][m][ld].  mb_counts [cpt_total] holds this minibatch's previous

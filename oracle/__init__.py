@@ -64,6 +64,8 @@ def lib():
             L.oracle_moral.restype = C.c_int
             L.oracle_conditional.argtypes = [C.c_int32, P, P, P, P, P, C.c_int32, P]
             L.oracle_conditional.restype = C.c_int
+            L.oracle_conditionals.argtypes = [C.c_int32, P, P, P, P, P, C.c_int64, C.c_int32, P]
+            L.oracle_conditionals.restype = C.c_int
             L.oracle_draw.argtypes = [P, C.c_int32, C.c_double, P]
             L.oracle_draw.restype = C.c_int32
             L.oracle_sweep.argtypes = [
@@ -184,6 +186,18 @@ def conditional(parents, card, theta, x, node):
     p = np.zeros(int(card[node]), dtype=np.float64)
     _check(lib().oracle_conditional(len(card), _ptr(pptr), _ptr(pidx), _ptr(card), _ptr(th),
                                     _ptr(xv), int(node), _ptr(p)))
+    return p
+
+
+def conditionals(parents, card, theta, X, node):
+    """conditional() for every row of X ([count][n] states), as [count][K]."""
+    pptr, pidx, card = _dag(parents, card)
+    th = np.ascontiguousarray(theta, dtype=np.float32)
+    xv = np.ascontiguousarray(X, dtype=np.int32)
+    assert xv.ndim == 2 and xv.shape[1] == len(card)
+    p = np.zeros((xv.shape[0], int(card[node])), dtype=np.float64)
+    _check(lib().oracle_conditionals(len(card), _ptr(pptr), _ptr(pidx), _ptr(card), _ptr(th), _ptr(xv),
+                                     int(xv.shape[0]), int(node), _ptr(p)))
     return p
 
 

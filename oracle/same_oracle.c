@@ -413,6 +413,30 @@ int oracle_conditional(int32_t n, const int32_t *pptr, const int32_t *pidx, cons
     return K;
 }
 
+/*
+ * The same normalised conditional for `count` state vectors X[count][n]
+ * (int32), into P[count][K_node]: the graph is built once for all of them.
+ */
+int oracle_conditionals(int32_t n, const int32_t *pptr, const int32_t *pidx, const int32_t *card,
+                        const float *theta, const int32_t *X, int64_t count, int32_t node, double *P) {
+    graph_t g;
+    int rc = graph_build(&g, n, pptr, pidx, card);
+    if (rc) return rc;
+    if (node < 0 || node >= n) { graph_free(&g); return OR_EINVAL; }
+    const int32_t K = card[node];
+    int16_t *xs = (int16_t *)malloc(sizeof(int16_t) * (size_t)n);
+    double *l = (double *)malloc(sizeof(double) * (size_t)K);
+    if (!xs || !l) { free(xs); free(l); graph_free(&g); return OR_ENOMEM; }
+    for (int64_t c = 0; c < count; ++c) {
+        for (int32_t v = 0; v < n; ++v) xs[v] = (int16_t)X[c * n + v];
+        log_conditional(&g, theta, node, xs, 2, 0, 1, l);
+        draw_from_logits(l, K, 0.0, P + c * K, NULL);
+    }
+    free(xs); free(l);
+    graph_free(&g);
+    return K;
+}
+
 /* The draw rule alone, for hand-built (weights, u) cases.  Weights must be >= 0. */
 int32_t oracle_draw(const double *weights, int32_t K, double u, int32_t *flagged) {
     int f = 0;

@@ -21,7 +21,7 @@ __all__ = [
     "same_step", "same_sweep_plan", "same_stream_slots_size", "same_stream_pass", "SAME_STREAM_COUNTS_ONLY",
     "same_kernel_timing", "same_kernel_times", "same_expand_observed", "same_init_latent",
     "same_accumulate_hits", "same_predict", "same_counts_ema", "same_sample_cpts_ema", "same_stream_pass_ema",
-    "same_grow_replicas",
+    "same_grow_replicas", "same_debug_thresholds",
     "library_path", "load_library",
 ]
 
@@ -98,6 +98,7 @@ def load_library():
         L.same_stream_pass_ema.argtypes = [P, P, P, I64, I64, I64, I32, P, P, C.c_double, U64, U32, I32, P, P,
                                            P]
         L.same_predict.argtypes = [P, P, P, P, P, I32, I64, I64, I64, U64, U32, I32, P, P, P]
+        L.same_debug_thresholds.argtypes = [P, P, P, P, C.POINTER(C.c_int64), P, P, P]
         L.same_last_error.argtypes = []
         L.same_last_error.restype = C.c_char_p
         for f in ("same_create", "same_create_ex", "same_layout", "same_workspace_size", "same_sweep",
@@ -105,7 +106,7 @@ def load_library():
                   "same_stream_slots_size", "same_stream_pass", "same_kernel_timing",
                   "same_kernel_times", "same_expand_observed", "same_init_latent",
                   "same_accumulate_hits", "same_predict", "same_counts_ema", "same_sample_cpts_ema",
-                  "same_stream_pass_ema", "same_grow_replicas"):
+                  "same_stream_pass_ema", "same_grow_replicas", "same_debug_thresholds"):
             getattr(L, f).restype = C.c_int
         _lib = L
         return L
@@ -334,3 +335,24 @@ def same_stream_pass_ema(ctx, host_states, host_obs, host_ld, n_cols, nb, m, cpt
 def same_grow_replicas(ctx, states, m, dst, m2, ld, stream=None):
     _check(load_library().same_grow_replicas(ctx.handle, _ptr(states), int(m), _ptr(dst), int(m2), int(ld),
                                              _stream(stream)))
+
+
+def same_debug_thresholds(ctx, cpts=None, workspace=None, stream=None):
+    """(node_off [n] int64, node_kt [n] int32, tables) -- the threshold tables
+    the sweep reads for cpts, as a uint32 tensor on cpts' device (None when
+    cpts is None: layout only)."""
+    n = ctx.n_nodes
+    off = np.zeros(n, dtype=np.int64)
+    kt = np.zeros(n, dtype=np.int32)
+    words = C.c_int64()
+    L = load_library()
+    _check(L.same_debug_thresholds(ctx.handle, None, off.ctypes.data, kt.ctypes.data, C.byref(words), None,
+                                   None, None))
+    if cpts is None:
+        return off, kt, None
+    import torch
+    out = torch.zeros(max(int(words.value), 1), dtype=torch.int32, device=cpts.device)
+    if int(words.value) > 0:
+        _check(L.same_debug_thresholds(ctx.handle, _ptr(cpts), off.ctypes.data, kt.ctypes.data, C.byref(words),
+                                       _ptr(out), _ptr(workspace), _stream(stream)))
+    return off, kt, out

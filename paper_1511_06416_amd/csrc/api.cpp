@@ -433,8 +433,7 @@ int do_step(same_ctx *ctx, void *states, const uint8_t *obs, float *cpts, int32_
         const int64_t nt = n_cols - t0 < T ? n_cols - t0 : T;
         rc = sweep_tile(ctx, P, t0, nt, s);
         if (rc) return rc;
-        rc = check_hip(same::launch_counts(*t, (const char *)states + t0 * ctx->g.state_bytes,
-                                           ctx->g.state_bytes, m, nt, ld, newc, s),
+        rc = check_hip(same::launch_counts(*t, states, ctx->g.state_bytes, m, t0, nt, ld, newc, s),
                        "count launch");
         if (rc) return rc;
     }
@@ -570,6 +569,34 @@ int same_sweep_debug(same_ctx *ctx, void *states, const uint8_t *obs, const floa
                     probs, workspace, stream);
 }
 
+int same_debug_thresholds(same_ctx *ctx, const float *cpts, int64_t *node_off, int32_t *node_kt,
+                          int64_t *words, uint32_t *cond_out, void *workspace, void *stream) {
+    if (!ctx || !node_off || !node_kt || !words)
+        return set_error(SAME_EINVAL, "ctx, node_off, node_kt and words must be non-null");
+    const same::Compiled &g = ctx->g;
+    for (int32_t i = 0; i < g.n; ++i) {
+        const int32_t *d = g.desc.data() + g.desc_off[i];
+        const bool tab = g.mode[i] == same::kModeTable;
+        node_off[i] = tab ? (int64_t)d[5] : -1;
+        node_kt[i] = tab ? d[7] : 0;
+    }
+    *words = g.cond_words;
+    if (!cond_out || g.cond_words == 0) return SAME_OK;
+    if (!cpts || !workspace) return set_error(SAME_EINVAL, "cpts and workspace must be non-null");
+    if (!aligned(cond_out, 4)) return set_error(SAME_EALIGN, "cond_out must be 4-byte aligned");
+    if (!aligned(workspace, kAlign)) return set_error(SAME_EALIGN, "workspace must be 256-byte aligned");
+    same::DeviceTables *t = nullptr;
+    int rc = tables_for_current_device(ctx, &t);
+    if (rc) return rc;
+    hipStream_t s = (hipStream_t)stream;
+    uint32_t *cond = (uint32_t *)((char *)workspace + ctx->ws_cond);
+    rc = check_hip(same::launch_build_thresholds(*t, cpts, cond, s), "threshold build launch");
+    if (rc) return rc;
+    return check_hip(hipMemcpyAsync(cond_out, cond, (size_t)g.cond_words * sizeof(uint32_t),
+                                    hipMemcpyDeviceToDevice, s),
+                     "threshold copy");
+}
+
 int same_counts(same_ctx *ctx, const void *states, int32_t m, int64_t n_cols, int64_t ld,
                 int32_t *mb_counts, int32_t *totals, void *workspace, void *stream) {
     int rc = check_minibatch(ctx, states, m, n_cols, ld);
@@ -586,7 +613,7 @@ int same_counts(same_ctx *ctx, const void *states, int32_t m, int64_t n_cols, in
     int32_t *newc = (int32_t *)((char *)workspace + ctx->ws_counts);
     rc = check_hip(same::launch_fill_zero(newc, total, s), "count clear launch");
     if (rc) return rc;
-    rc = check_hip(same::launch_counts(*t, states, ctx->g.state_bytes, m, n_cols, ld, newc, s),
+    rc = check_hip(same::launch_counts(*t, states, ctx->g.state_bytes, m, 0, n_cols, ld, newc, s),
                    "count launch");
     if (rc) return rc;
     return check_hip(same::launch_moving_sum(newc, mb_counts, totals, total, s), "moving-sum launch");
@@ -765,7 +792,7 @@ int same_counts_ema(same_ctx *ctx, const void *states, int32_t m, int64_t n_cols
     int32_t *newc = (int32_t *)((char *)workspace + ctx->ws_counts);
     rc = check_hip(same::launch_fill_zero(newc, total, s), "count clear launch");
     if (rc) return rc;
-    rc = check_hip(same::launch_counts(*t, states, ctx->g.state_bytes, m, n_cols, ld, newc, s),
+    rc = check_hip(same::launch_counts(*t, states, ctx->g.state_bytes, m, 0, n_cols, ld, newc, s),
                    "count launch");
     if (rc) return rc;
     return check_hip(same::launch_ema(newc, totals, decay, total, s), "moving-sum launch");

@@ -1184,7 +1184,7 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
                                                       int32_t count, int64_t n_slabs,
                                                       int64_t cols_per_block,
                                                       const ST *__restrict__ states, int32_t m,
-                                                      int64_t n_cols, int64_t ld,
+                                                      int64_t col0, int64_t n_cols, int64_t ld,
                                                       int32_t *__restrict__ counts) {
     using Q = Quad<ST>;
     __shared__ int32_t hist[kLdsBins];
@@ -1203,8 +1203,9 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
     for (int b = threadIdx.x; b < lds_words; b += kBlock) hist[b] = 0;
     __syncthreads();
     const int copy = threadIdx.x & (kCopies - 1);
-    const int64_t c0 = slab * cols_per_block;
-    const int64_t c1 = c0 + cols_per_block < n_cols ? c0 + cols_per_block : n_cols;
+    // absolute columns of the row: [c0, c1) inside [col0, col0 + n_cols)
+    const int64_t c0 = col0 + slab * cols_per_block;
+    const int64_t c1 = c0 + cols_per_block < col0 + n_cols ? c0 + cols_per_block : col0 + n_cols;
     const int64_t vstride = (int64_t)m * ld;
     const bool packed = nbins <= 65536;
     auto add = [&](int bin) {
@@ -1626,7 +1627,8 @@ hipError_t launch_fill_zero(int32_t *p, int64_t count, hipStream_t stream) {
 }
 
 hipError_t launch_counts(const DeviceTables &t, const void *states, int32_t state_bytes,
-                         int32_t m, int64_t n_cols, int64_t ld, int32_t *counts, hipStream_t stream) {
+                         int32_t m, int64_t col0, int64_t n_cols, int64_t ld, int32_t *counts,
+                         hipStream_t stream) {
     if (n_cols <= 0) return hipSuccess;
     const int32_t n = t.n_cwork;
     // one node x kCountQuadsPerLane quads per lane x all replicas per block,
@@ -1639,7 +1641,7 @@ hipError_t launch_counts(const DeviceTables &t, const void *states, int32_t stat
     const dim3 grid((unsigned)blocks);
 #define SAME_LAUNCH_COUNTS(ST, WIDE)                                                                    \
     hipLaunchKernelGGL((dev::count_kernel<ST, WIDE>), grid, dim3(dev::kBlock), 0, stream, t.cdesc, t.cdesc_off, \
-                       t.cwork, n, n_slabs, cols_per_block, (const ST *)states, m, n_cols, ld, counts)
+                       t.cwork, n, n_slabs, cols_per_block, (const ST *)states, m, col0, n_cols, ld, counts)
     // rows of at least 4 * kCountQuadsPerLane columns take the wide loads
     if (state_bytes == 1) {
         if (ld >= 4 * dev::kCountQuadsPerLane) SAME_LAUNCH_COUNTS(int8_t, true);

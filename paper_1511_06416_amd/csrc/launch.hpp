@@ -72,9 +72,11 @@ hipError_t launch_sweep(SweepParams P, int32_t begin, int32_t count, int32_t kla
 
 hipError_t launch_fill_zero(int32_t *p, int64_t count, hipStream_t stream);
 
-// Histograms of every node's family (the count work items of t).
+// Histograms of every node's family (the count work items of t) over the
+// columns [col0, col0 + n_cols) of states [n][m][ld].
 hipError_t launch_counts(const DeviceTables &t, const void *states, int32_t state_bytes,
-                         int32_t m, int64_t n_cols, int64_t ld, int32_t *counts, hipStream_t stream);
+                         int32_t m, int64_t col0, int64_t n_cols, int64_t ld, int32_t *counts,
+                         hipStream_t stream);
 
 // Dense minibatch from CSR known entries (rows = nodes): clears obs, then
 // one thread per entry writes obs and every replica's state.

@@ -45,6 +45,20 @@ def gpu_sweep(ctx, states_np, obs_np, theta_np, m, n_cols, col_offset, seed, swe
     return st.cpu().numpy(), (probs.cpu().numpy() if probs is not None else None)
 
 
+def gpu_sweep_both(ctx, states_np, obs_np, theta_np, m, n_cols, col_offset, seed, sweep_id, win=None):
+    """The production sweep (same_sweep) on one copy of the inputs and, when a
+    window is asked for, the debug sweep (same_sweep_debug, which also writes
+    the conditionals) on another.  The two are separate kernel builds (the
+    production one draws replica pairs at a higher occupancy bound), so each
+    is compared with the oracle on its own.  Returns (production states,
+    debug states or None, probs or None)."""
+    prod, _ = gpu_sweep(ctx, states_np, obs_np, theta_np, m, n_cols, col_offset, seed, sweep_id)
+    if win is None:
+        return prod, None, None
+    dbg, probs = gpu_sweep(ctx, states_np, obs_np, theta_np, m, n_cols, col_offset, seed, sweep_id, win=win)
+    return prod, dbg, probs
+
+
 def visit_order(color):
     return sorted(range(len(color)), key=lambda i: (int(color[i]), i))
 

@@ -97,3 +97,19 @@ def test_draw_frequencies_match_weights():
     picks = np.array([oracle.draw(w, u)[0] for u in us])
     freq = np.bincount(picks, minlength=4) / len(us)
     np.testing.assert_allclose(freq, w, atol=1e-3)
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_batched_conditionals_equal_joint_ratio(seed):
+    # the batched form (one graph build for many state vectors) against the
+    # full-joint ratio, row by row
+    rng = np.random.default_rng(300 + seed)
+    n = int(rng.integers(4, 7))
+    parents, card = brute.random_net(rng, n, 3, 2, 5)
+    theta = brute.random_theta(rng, parents, card, alpha=0.6)
+    X = np.stack([[int(rng.integers(0, card[i])) for i in range(n)] for _ in range(40)])
+    for node in range(n):
+        got = oracle.conditionals(parents, card, theta, X, node)
+        for row, x in enumerate(X):
+            want = brute.conditional_by_joint(parents, card, theta, list(x), node)
+            np.testing.assert_allclose(got[row], want, rtol=1e-12, atol=0)

@@ -36,14 +36,16 @@ def _sweep_case(w, b=0, sweep_id=3, win=None, theta=None, n_threads=0, table_lim
     pre = w.states[b].cpu().numpy()
     obs = w.obs[b].cpu().numpy()
     ncols = w.mb_cols(b)
-    gpu, gp = H.gpu_sweep(ctx, pre, obs, theta, w.m, ncols, b * w.nb, w.seed, sweep_id, win=win)
+    gpu, dbg, gp = H.gpu_sweep_both(ctx, pre, obs, theta, w.m, ncols, b * w.nb, w.seed, sweep_id, win=win)
     ref = pre.copy()
     res = oracle.sweep(net.parents, net.card, theta, color, ref, obs, w.m, ncols, b * w.nb,
                        w.seed, sweep_id, want_flags=True, win=win, n_threads=n_threads)
+    # the production kernels, then the debug build that wrote the conditionals
     st = H.compare_states(gpu, ref, res["flags"], color, ncols, obs=obs)
     out = {"states": st, "draws": res["draws"]}
     if win is not None:
-        div = H.diverged_chains(gpu, ref, ncols, win)
+        out["debug_states"] = H.compare_states(dbg, ref, res["flags"], color, ncols, obs=obs)
+        div = H.diverged_chains(dbg, ref, ncols, win)
         out["probs"] = H.compare_probs(gp, res["probs"], obs, net.card, win, div)
     print(w.name, out)
     return out
@@ -57,6 +59,8 @@ def _sweep_case(w, b=0, sweep_id=3, win=None, theta=None, n_threads=0, table_lim
     (3, dict(n_cols=9_000), (8_000, 1000)),              # 100-node random DAG, ragged tail
     (4, {}, (0, 600)),                                   # two-layer concepts, m=20
     (5, dict(n_cols=5_000), (4_600, 400)),               # 1000-node random DAG, m=10
+    (5, dict(n_cols=3_000, m=5), (0, 300)),              # odd m: replica pairs, then one
+    (5, dict(n_cols=2_001, m=7), (1_700, 301)),          # odd m and a ragged tail
 ])
 @pytest.mark.parametrize("table_limit", [None, 0], ids=["tables", "products"])
 def test_sweep_parity_configs(cfg, kw, win, table_limit):
@@ -173,14 +177,16 @@ def _custom_case(net, states, obs, theta, m, n_cols, col_offset=0, win=None, swe
                  table_limit=None, **ctx_kw):
     ctx = H.context_for(net, table_limit=table_limit, **ctx_kw)
     color = oracle.graph(net.parents, net.card)["color"]
-    gpu, gp = H.gpu_sweep(ctx, states, obs, theta, m, n_cols, col_offset, seed, sweep_id, win=win)
+    gpu, dbg, gp = H.gpu_sweep_both(ctx, states, obs, theta, m, n_cols, col_offset, seed, sweep_id, win=win)
     ref = states.copy()
     res = oracle.sweep(net.parents, net.card, theta, color, ref, obs, m, n_cols, col_offset, seed,
                        sweep_id, want_flags=True, win=win)
+    # production kernels first, then the debug build and its conditionals
     st = H.compare_states(gpu, ref, res["flags"], color, n_cols, obs=obs)
     if win is not None:
+        H.compare_states(dbg, ref, res["flags"], color, n_cols, obs=obs)
         H.compare_probs(gp, res["probs"], obs, net.card, win,
-                        H.diverged_chains(gpu, ref, n_cols, win))
+                        H.diverged_chains(dbg, ref, n_cols, win))
     return gpu, ref, st
 
 
@@ -471,3 +477,30 @@ def test_kernel_timing_counts_launches_and_phases():
     assert sum(kt["node_samples"]) == float(net.n * 3_000 * w.m)
     assert same.same_kernel_times(ctx) == {"ms": [0.0] * 4, "launches": [0] * 4, "phase_ms": 0.0, "phases": 0,
                                            "node_samples": [0.0] * 4}
+
+
+@pytest.mark.parametrize("big", [False, True], ids=["int8", "int16"])
+def test_tiled_step_counts_with_unaligned_rows(big):
+    """same_step over 1024-column tiles with rows of ld = 5004 (not a multiple
+    of 16): the count pass of the last tile reads its rows' ragged ends one
+    quad at a time, and the tiled step equals the untiled one bit for bit
+    (states, counts, moving sum, CPTs); the counts equal the oracle's."""
+    card = [130 if big else 3, 3, 200 if big else 4, 2, 5]
+    parents = [[], [0], [0, 1], [2], [1, 2, 3]]
+    n_cols, ld, m = 5001, 5004, 3
+    net, st, ob, th = _custom(parents, card, n_cols, m, 0.5, 23, ld=ld)
+    outs = []
+    for tb in (1, 0):
+        ctx = H.context_for(net, tile_bytes=tb)
+        d_st = torch.from_numpy(st.copy()).cuda()
+        d_ob = torch.from_numpy(ob).cuda()
+        d_th = torch.from_numpy(th.astype(np.float32)).cuda()
+        mb = torch.zeros(ctx.cpt_total, dtype=torch.int32, device="cuda")
+        tot = torch.zeros(ctx.cpt_total, dtype=torch.int32, device="cuda")
+        ws = ctx.new_workspace()
+        same.same_step(ctx, d_st, d_ob, d_th, m, n_cols, ld, 0, 5, 0, mb, tot, 0, ws)
+        torch.cuda.synchronize()
+        outs.append([x.cpu().numpy() for x in (d_st, mb, tot, d_th)])
+    for x, y in zip(*outs):
+        assert np.array_equal(x, y)
+    assert np.array_equal(outs[0][1], oracle.counts(parents, card, outs[0][0], m, n_cols))
