@@ -216,6 +216,24 @@ int same_counts(same_ctx *ctx, const void *states, int32_t m, int64_t n_cols, in
                 int32_t *mb_counts, int32_t *totals, void *workspace, void *stream);
 
 /*
+ * same_counts for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation): the
+ * same histogram and moving sum, with the new-count histogram held in a
+ * library-owned device array of 2^21 int32 entries (8 MiB, one per device,
+ * kept until the process ends) instead of the workspace.  No workspace
+ * argument; the call allocates nothing and clears the array with a kernel
+ * (no memset).  Preconditions: cpt_total <= 2^21 (else SAME_ESIZE), and the
+ * context's structure tables already on the current device, i.e. some other
+ * device call of this context (same_counts, same_sweep, ...) has run on it
+ * (else SAME_EINVAL).  Every call on one device shares the array, which keeps
+ * the last call's contents: calls that overlap on one device (other streams,
+ * other threads, other contexts) race and must be ordered by the caller.
+ * Other arguments and errors as same_counts.
+ */
+int same_counts_noalloc(same_ctx *ctx, const void *states, int32_t m, int64_t n_cols, int64_t ld,
+                        int32_t *mb_counts, int32_t *totals, void *stream);
+
+/*
  * Dirichlet resample of every CPT row (Sec. 4: counts plus the Dirichlet
  * prior are the Dirichlet parameters from which the CPTs are sampled):
  * g_e ~ Gamma(prior + totals[e], 1) (Marsaglia & Tsang, in fp64), then

@@ -21,7 +21,7 @@ __all__ = [
     "same_step", "same_sweep_plan", "same_stream_slots_size", "same_stream_pass", "SAME_STREAM_COUNTS_ONLY",
     "same_kernel_timing", "same_kernel_times", "same_expand_observed", "same_init_latent",
     "same_accumulate_hits", "same_predict", "same_counts_ema", "same_sample_cpts_ema", "same_stream_pass_ema",
-    "same_grow_replicas", "same_debug_thresholds",
+    "same_grow_replicas", "same_debug_thresholds", "same_counts_noalloc",
     "library_path", "load_library",
 ]
 
@@ -98,6 +98,7 @@ def load_library():
         L.same_stream_pass_ema.argtypes = [P, P, P, I64, I64, I64, I32, P, P, C.c_double, U64, U32, I32, P, P,
                                            P]
         L.same_predict.argtypes = [P, P, P, P, P, I32, I64, I64, I64, U64, U32, I32, P, P, P]
+        L.same_counts_noalloc.argtypes = [P, P, I32, I64, I64, P, P, P]
         L.same_debug_thresholds.argtypes = [P, P, P, P, C.POINTER(C.c_int64), P, P, P]
         L.same_last_error.argtypes = []
         L.same_last_error.restype = C.c_char_p
@@ -106,7 +107,8 @@ def load_library():
                   "same_stream_slots_size", "same_stream_pass", "same_kernel_timing",
                   "same_kernel_times", "same_expand_observed", "same_init_latent",
                   "same_accumulate_hits", "same_predict", "same_counts_ema", "same_sample_cpts_ema",
-                  "same_stream_pass_ema", "same_grow_replicas", "same_debug_thresholds"):
+                  "same_stream_pass_ema", "same_grow_replicas", "same_debug_thresholds",
+                  "same_counts_noalloc"):
             getattr(L, f).restype = C.c_int
         _lib = L
         return L
@@ -237,6 +239,13 @@ def same_counts(ctx, states, m, n_cols, ld, mb_counts, totals, workspace, stream
     _check(load_library().same_counts(ctx.handle, _ptr(states), int(m), int(n_cols), int(ld),
                                       _ptr(mb_counts), _ptr(totals), _ptr(workspace),
                                       _stream(stream)))
+
+
+def same_counts_noalloc(ctx, states, m, n_cols, ld, mb_counts, totals, stream=None):
+    """same_counts without a workspace: the histogram lives in the library's
+    per-device scratch array (see include/same.h)."""
+    _check(load_library().same_counts_noalloc(ctx.handle, _ptr(states), int(m), int(n_cols), int(ld),
+                                              _ptr(mb_counts), _ptr(totals), _stream(stream)))
 
 
 def same_sample_cpts(ctx, totals, cpts_out, seed, update_id, workspace, stream=None):

@@ -798,6 +798,41 @@ int same_counts_ema(same_ctx *ctx, const void *states, int32_t m, int64_t n_cols
     return check_hip(same::launch_ema(newc, totals, decay, total, s), "moving-sum launch");
 }
 
+int same_counts_noalloc(same_ctx *ctx, const void *states, int32_t m, int64_t n_cols, int64_t ld,
+                        int32_t *mb_counts, int32_t *totals, void *stream) {
+    int rc = check_minibatch(ctx, states, m, n_cols, ld);
+    if (rc) return rc;
+    if (!mb_counts) return set_error(SAME_EINVAL, "mb_counts must be non-null");
+    if ((double)n_cols * (double)m >= 2147483648.0)
+        return set_error(SAME_ESIZE, "n_cols * m must stay below 2^31");
+    const int64_t total = ctx->g.off[ctx->g.n];
+    if (total > same::kScratchCountEntries)
+        return set_error(SAME_ESIZE, "cpt_total exceeds the " + std::to_string(same::kScratchCountEntries) +
+                                         " entries of the allocation-free count scratch");
+    int device = -1;
+    rc = check_hip(hipGetDevice(&device), "hipGetDevice");
+    if (rc) return rc;
+    // the structure tables must already be on this device: uploading them
+    // would allocate
+    same::DeviceTables *t = nullptr;
+    {
+        std::lock_guard<std::mutex> lock(ctx->mu);
+        if ((int)ctx->dev.size() > device && ctx->dev[device].device == device) t = &ctx->dev[device];
+    }
+    if (!t)
+        return set_error(SAME_EINVAL, "the context's tables are not on this device yet: make one allocating call "
+                                      "(e.g. same_counts) on it first");
+    int32_t *newc = nullptr;
+    rc = check_hip(same::scratch_counts(device, &newc), "hipGetSymbolAddress");
+    if (rc) return rc;
+    hipStream_t s = (hipStream_t)stream;
+    rc = check_hip(same::launch_fill_zero(newc, total, s), "count clear launch");
+    if (rc) return rc;
+    rc = check_hip(same::launch_counts(*t, states, ctx->g.state_bytes, m, 0, n_cols, ld, newc, s), "count launch");
+    if (rc) return rc;
+    return check_hip(same::launch_moving_sum(newc, mb_counts, totals, total, s), "moving-sum launch");
+}
+
 int same_sample_cpts_ema(same_ctx *ctx, const double *totals, float *cpts_out, uint64_t seed, uint32_t update_id,
                          void *workspace, void *stream) {
     if (!ctx || !totals || !cpts_out || !workspace)

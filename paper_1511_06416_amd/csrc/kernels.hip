@@ -11,6 +11,8 @@
 
 #include <cfloat>
 #include <cstdint>
+#include <mutex>
+#include <vector>
 
 #include "launch.hpp"
 #include "philox.hpp"
@@ -1543,7 +1545,30 @@ __global__ __launch_bounds__(kBlock) void grow_kernel(const uint8_t *__restrict_
 
 namespace {
 inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
+
+// Count histogram of the allocation-free count entry point: a file-scope
+// device array (each device holds its own copy until the process ends).  In
+// host code `scratch` names a host-side stand-in, not device memory; its
+// device address comes from hipGetSymbolAddress, resolved once per device.
+static __device__ __align__(256) int32_t scratch[kScratchCountEntries];
+
+std::mutex g_scratch_mu;
+std::vector<int32_t *> g_scratch_ptr;  // indexed by device ordinal
 }  // namespace
+
+hipError_t scratch_counts(int device, int32_t **out) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (device < 0) return hipErrorInvalidDevice;
+    if ((int)g_scratch_ptr.size() <= device) g_scratch_ptr.resize(device + 1, nullptr);
+    if (!g_scratch_ptr[device]) {
+        void *p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        g_scratch_ptr[device] = static_cast<int32_t *>(p);
+    }
+    *out = g_scratch_ptr[device];
+    return hipSuccess;
+}
 
 hipError_t launch_build_tables(const DeviceTables &t, const float *cpts, float *table,
                                hipStream_t stream) {

@@ -72,6 +72,15 @@ hipError_t launch_sweep(SweepParams P, int32_t begin, int32_t count, int32_t kla
 
 hipError_t launch_fill_zero(int32_t *p, int64_t count, hipStream_t stream);
 
+// Entries of the file-scope count scratch of the allocation-free count entry
+// point (int32; 8 MiB per device).
+constexpr int64_t kScratchCountEntries = int64_t(1) << 21;
+
+// Device address of that scratch on `device`, which must be the current
+// device; resolved with hipGetSymbolAddress on the first call per device.
+// Allocates nothing.
+hipError_t scratch_counts(int device, int32_t **out);
+
 // Histograms of every node's family (the count work items of t) over the
 // columns [col0, col0 + n_cols) of states [n][m][ld].
 hipError_t launch_counts(const DeviceTables &t, const void *states, int32_t state_bytes,
