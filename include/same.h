@@ -44,7 +44,8 @@
  *         failure.  A context is used by one host thread at a time.
  * Random numbers: Philox4x32-10 (Salmon et al., SC'11) keyed by the 64-bit
  *         seed; the Gibbs draw of node i, replica r, global column g in sweep
- *         s takes word g&3 of the block at counter {g>>2, i, r, s}; the Gamma
+ *         s takes word r&3 of the block at counter {g, i, r>>2, s} (one block
+ *         per column and quad of replicas; g < 2^32); the Gamma
  *         attempt t of CPT entry e at update q uses counter {e, t, 1<<24, q};
  *         the initial latent state uses {g>>2, i, r | 2<<24, 0}.
  */

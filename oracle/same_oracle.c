@@ -32,7 +32,7 @@
  *     used by an already coloured moral neighbour.
  *   - Random numbers: Philox4x32-10 (Salmon, Moraes, Dror & Shaw, SC'11).
  *     Gibbs draw for node i, replica r, global column g, sweep s uses word
- *     (g & 3) of Philox(ctr = {g>>2, i, r | (0<<24), s}, key = {seed_lo, seed_hi});
+ *     (r & 3) of Philox(ctr = {g, i, (r>>2) | (0<<24), s}, key = {seed_lo, seed_hi});
  *     U24(w) = (w >> 8) * 2^-24.
  *   - Draw rule (inverse CDF): w_k = exp(l_k - max l), S_k = w_0 + ... + w_k,
  *     Z = S_{K-1}; pick the smallest k with u*Z < S_k, else the largest k with
@@ -107,11 +107,15 @@ static uint32_t philox_word(uint64_t seed, uint32_t c0, uint32_t c1, uint32_t c2
     return out[word];
 }
 
-/* The Gibbs uniform of one (node, replica, global column, sweep). */
+/*
+ * The Gibbs uniform of one (node, replica, global column, sweep): word r & 3
+ * of the block at counter {g, node, (r >> 2) | TAG_GIBBS << 24, sweep}, so
+ * that one block serves four replicas of one column.
+ */
 double oracle_gibbs_uniform(uint64_t seed, int32_t node, int32_t replica, int64_t gcol,
                             uint32_t sweep_id) {
-    uint32_t w = philox_word(seed, (uint32_t)(gcol >> 2), (uint32_t)node,
-                             (uint32_t)replica | (TAG_GIBBS << 24), sweep_id, (int)(gcol & 3));
+    uint32_t w = philox_word(seed, (uint32_t)gcol, (uint32_t)node,
+                             ((uint32_t)replica >> 2) | (TAG_GIBBS << 24), sweep_id, (int)(replica & 3));
     return (double)(w >> 8) * (1.0 / 16777216.0);
 }
 

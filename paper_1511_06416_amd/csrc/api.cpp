@@ -252,8 +252,8 @@ int check_sweep_args(same_ctx *ctx, void *states, const uint8_t *obs, const floa
     if (!obs || !cpts || !workspace) return set_error(SAME_EINVAL, "obs, cpts and workspace must be non-null");
     if (col_offset < 0 || col_offset % 4 != 0)
         return set_error(SAME_EALIGN, "col_offset must be a non-negative multiple of 4");
-    if (((col_offset + n_cols) >> 2) > (int64_t)0xFFFFFFFFll)
-        return set_error(SAME_ESIZE, "global column index exceeds the Philox counter range");
+    if (col_offset + n_cols > ((int64_t)1 << 32))
+        return set_error(SAME_ESIZE, "global column index exceeds the Philox counter range (2^32 columns)");
     if (!aligned(obs, 4)) return set_error(SAME_EALIGN, "obs must be 4-byte aligned");
     if (!aligned(workspace, kAlign)) return set_error(SAME_EALIGN, "workspace must be 256-byte aligned");
     if (win > 0) {
@@ -900,7 +900,7 @@ extern "C" int same_init_latent(same_ctx *ctx, void *states, const uint8_t *obs,
     if (col_offset < 0 || col_offset % 4 != 0)
         return set_error(SAME_EALIGN, "col_offset must be a non-negative multiple of 4");
     if (((col_offset + n_cols) >> 2) > (int64_t)0xFFFFFFFFll)
-        return set_error(SAME_ESIZE, "global column index exceeds the Philox counter range");
+        return set_error(SAME_ESIZE, "global column index exceeds the Philox counter range (2^34 columns)");
     same::DeviceTables *t = nullptr;
     rc = tables_for_current_device(ctx, &t);
     if (rc) return rc;

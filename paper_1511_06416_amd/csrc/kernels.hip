@@ -2,11 +2,11 @@
 // histogram, moving sum, Gamma/Dirichlet resample.
 //
 // Data layout (HBM): states [n][m][ld] int8 (or int16), obs [n][ld] uint8.
-// A lane owns 4 consecutive columns of one (node, replica): one dword of int8
-// states (8 bytes for int16), one dword of obs bytes, and exactly one Philox
-// block (4 words = the 4 columns' uniforms).  Consecutive lanes own
-// consecutive column quads, so every state and obs load of a wavefront is a
-// contiguous 256-byte (int8) segment.
+// The fast sweep kernel works on items: one latent column of a node and a
+// quad of its replicas, whose four draws take the four words of one Philox
+// block; consecutive lanes take consecutive latent columns, so the state
+// loads of a wavefront fall in a few cache lines per replica row.  The count
+// and ingest kernels read whole column quads (dwords) per lane.
 #include <hip/hip_runtime.h>
 
 #include <cfloat>
@@ -29,13 +29,7 @@ __device__ __forceinline__ cint32_t *as_const(const int32_t *p) { return (cint32
 
 constexpr int kBlock = 256;          // 4 wavefronts of 64
 constexpr int kSweepBlock = 256;     // threads of a sweep block
-constexpr int kSweepWaves = 6;       // waves per SIMD the fast sweep kernel is compiled for
-// replicas a lane draws together (their loads in flight at once), per path
-constexpr int kPairTable = 2;
-constexpr int kPairKP2 = 2;
-constexpr int kPairKP4 = 2;
-constexpr int kPairKP6 = 1;
-constexpr int kPairKP8 = 1;
+constexpr int kSweepWaves = 5;       // waves per SIMD the fast sweep kernel is compiled for
 
 // ---------------------------------------------------------------- state quads
 
@@ -174,102 +168,11 @@ __device__ __forceinline__ void walk_entries(cint32_t *e, int n_e, const ST *__r
     }
 }
 
-// The same for NR replicas of the lane's column quad at once (byte offsets
-// boff): the NR rows of an entry share its buffer resource, and every load
-// of the batch is in flight before the first use, so NR replicas cost one
-// round trip per batch instead of NR.
-template <int N, int NR, typename ST, typename F>
-__device__ __forceinline__ void entry_batch_r(cint32_t *e, const ST *__restrict__ states, int64_t vstride,
-                                              const uint32_t (&boff)[NR], F &f) {
-    typename Quad<ST>::V s[N][NR];
-#pragma unroll
-    for (int t = 0; t < N; ++t)
-#pragma unroll
-        for (int r = 0; r < NR; ++r) s[t][r] = load_row<ST>(states, e[2 * t], vstride, boff[r]);
-#pragma unroll
-    for (int t = 0; t < N; ++t)
-#pragma unroll
-        for (int r = 0; r < NR; ++r) f(r, s[t][r], (uint32_t)e[2 * t + 1]);
-}
-
-// Batches of at most kEntryBatch / NR entries (kEntryBatch rows in flight).
-template <int NR, typename ST, typename F>
-__device__ __forceinline__ void walk_entries_r(cint32_t *e, int n_e, const ST *__restrict__ states,
-                                               int64_t vstride, const uint32_t (&boff)[NR], F &f) {
-    constexpr int B = kEntryBatch / NR;
-    for (; n_e > 0; n_e -= B, e += 2 * B) {
-        const int nb = n_e < B ? n_e : B;
-        if (nb == 1) entry_batch_r<1, NR, ST>(e, states, vstride, boff, f);
-        else if (nb == 2) entry_batch_r<2, NR, ST>(e, states, vstride, boff, f);
-        else if (nb == 3) entry_batch_r<3, NR, ST>(e, states, vstride, boff, f);
-        else if (nb == 4) entry_batch_r<4, NR, ST>(e, states, vstride, boff, f);
-        else if constexpr (B > 4) {
-            if (nb == 5) entry_batch_r<5, NR, ST>(e, states, vstride, boff, f);
-            else if (nb == 6) entry_batch_r<6, NR, ST>(e, states, vstride, boff, f);
-            else if (nb == 7) entry_batch_r<7, NR, ST>(e, states, vstride, boff, f);
-            else entry_batch_r<8, NR, ST>(e, states, vstride, boff, f);
-        }
-    }
-}
-
-// Packed group index of a fast list: two words of 2 x 16-bit lanes, one lane
-// per column of the quad (lane layout in Quad<ST>::split).  Columns past
-// n_cols are cleared by vmask, so their index is 0: padding never steers an
-// access out of the node's table.  Advances g past the group.
-template <typename ST>
-__device__ __forceinline__ void packed_group(cint32_t *&g, const ST *__restrict__ states,
-                                             int64_t vstride, uint32_t lane_boff,
-                                             const uint32_t (&vmask)[2], uint32_t (&Pk)[2]) {
-    const int n_e = g[0];
-    Pk[0] = Pk[1] = (uint32_t)g[1];
-    auto acc = [&](typename Quad<ST>::V v, uint32_t mult) {
-        uint32_t p[2];
-        Quad<ST>::split(v, p);
-        Pk[0] = pk_mad_u16(p[0], mult, Pk[0]);
-        Pk[1] = pk_mad_u16(p[1], mult, Pk[1]);
-    };
-    walk_entries<ST>(g + 2, n_e, states, vstride, lane_boff, acc);
-    g += 2 + 2 * n_e;
-    Pk[0] &= vmask[0];
-    Pk[1] &= vmask[1];
-}
-
+// 16-bit lane c of a packed index pair (lane layout in Quad<ST>::split).
 template <typename ST>
 __device__ __forceinline__ uint32_t packed_index(const uint32_t (&Pk)[2], int c) {
     const uint32_t v = Pk[Quad<ST>::word_of(c)];
     return Quad<ST>::half_of(c) ? v >> 16 : v & 0xffffu;
-}
-
-// packed_group for NR replicas (Pk[r] belongs to byte offset boff[r]).
-template <int NR, typename ST>
-__device__ __forceinline__ void packed_group_r(cint32_t *&g, const ST *__restrict__ states, int64_t vstride,
-                                               const uint32_t (&boff)[NR], const uint32_t (&vmask)[2],
-                                               uint32_t (&Pk)[NR][2]) {
-    const int n_e = g[0];
-#pragma unroll
-    for (int r = 0; r < NR; ++r) Pk[r][0] = Pk[r][1] = (uint32_t)g[1];
-    auto acc = [&](int r, typename Quad<ST>::V v, uint32_t mult) {
-        uint32_t p[2];
-        Quad<ST>::split(v, p);
-        Pk[r][0] = pk_mad_u16(p[0], mult, Pk[r][0]);
-        Pk[r][1] = pk_mad_u16(p[1], mult, Pk[r][1]);
-    };
-    walk_entries_r<NR, ST>(g + 2, n_e, states, vstride, boff, acc);
-    g += 2 + 2 * n_e;
-#pragma unroll
-    for (int r = 0; r < NR; ++r) {
-        Pk[r][0] &= vmask[0];
-        Pk[r][1] &= vmask[1];
-    }
-}
-
-// Lane masks of vmask: the 16-bit lanes of columns >= nvalid cleared.
-template <typename ST>
-__device__ __forceinline__ void valid_mask(int nvalid, uint32_t (&vmask)[2]) {
-    vmask[0] = vmask[1] = 0xffffffffu;
-#pragma unroll
-    for (int c = 0; c < 4; ++c)
-        if (c >= nvalid) vmask[Quad<ST>::word_of(c)] &= ~(0xffffu << (16 * Quad<ST>::half_of(c)));
 }
 
 // ---------------------------------------------------------------- k-vectors
@@ -386,65 +289,6 @@ __device__ __forceinline__ void renorm(float (&w)[KP]) {
         const int e = __builtin_amdgcn_frexp_expf(mx);
 #pragma unroll
         for (int k = 0; k < KP; ++k) w[k] = __builtin_ldexpf(w[k], -e);
-    }
-}
-
-// Unnormalised full conditional (Sec. 4: own CPT entry times the children's
-// entries, Eq. 4) of the quad's 4 columns from a fast product list: group 0
-// gives the first k-vector, each further group a k-vector multiplied in.  The
-// first n_staged groups are read from the LDS copy of the record (byte
-// indices), the others from global memory (k-vector indices); n_staged is
-// uniform, so the choice is a scalar branch.  With RESCALE every column's
-// running product is renormalised after each factor, which keeps it away
-// from fp32 underflow.
-// Multiplies the k-vectors at the quad's packed indices into w (from LDS
-// when FROM_LDS, else from global memory).
-template <int KP, typename ST, bool FROM_LDS, bool RESCALE>
-__device__ __forceinline__ void multiply_group(lds_char *lds, global_char *gtab, const uint32_t (&Pk)[2],
-                                               float (&w)[4][KP]) {
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-        float f[KP];
-        fast_kvec<KP, FROM_LDS>(lds, gtab, packed_index<ST>(Pk, c), f);
-#pragma unroll
-        for (int k = 0; k < KP; ++k) w[c][k] *= f[k];
-        if (RESCALE) renorm<KP>(w[c]);
-    }
-}
-
-template <int KP, typename ST, bool STAGED, bool RESCALE, int NR>
-__device__ __forceinline__ void fast_product(cint32_t *g, int n_groups, int n_staged, lds_char *lds,
-                                             global_char *gtab,
-                                             const ST *__restrict__ states, int64_t vstride,
-                                             const uint32_t (&boff)[NR], const uint32_t (&vmask)[2],
-                                             float (&w)[NR][4][KP]) {
-    uint32_t Pk[NR][2];
-    packed_group_r<NR, ST>(g, states, vstride, boff, vmask, Pk);
-    if (STAGED && n_staged > 0) {
-#pragma unroll
-        for (int r = 0; r < NR; ++r)
-#pragma unroll
-            for (int c = 0; c < 4; ++c) fast_kvec<KP, true>(lds, gtab, packed_index<ST>(Pk[r], c), w[r][c]);
-    } else {
-#pragma unroll
-        for (int r = 0; r < NR; ++r)
-#pragma unroll
-            for (int c = 0; c < 4; ++c) fast_kvec<KP, false>(lds, gtab, packed_index<ST>(Pk[r], c), w[r][c]);
-    }
-    // the staged groups, then the global ones: two loops, so that each keeps
-    // only its own addressing live
-    int j = 1;
-    if (STAGED) {
-        for (; j < n_staged; ++j) {
-            packed_group_r<NR, ST>(g, states, vstride, boff, vmask, Pk);
-#pragma unroll
-            for (int r = 0; r < NR; ++r) multiply_group<KP, ST, true, RESCALE>(lds, gtab, Pk[r], w[r]);
-        }
-    }
-    for (; j < n_groups; ++j) {
-        packed_group_r<NR, ST>(g, states, vstride, boff, vmask, Pk);
-#pragma unroll
-        for (int r = 0; r < NR; ++r) multiply_group<KP, ST, false, RESCALE>(lds, gtab, Pk[r], w[r]);
     }
 }
 
@@ -584,109 +428,234 @@ __device__ __forceinline__ void write_probs(const SweepParams &P, int node, int 
     }
 }
 
-__device__ __forceinline__ Philox4 gibbs_block(const SweepParams &P, int node, int r, int64_t q) {
-    return philox4x32_10((uint32_t)((P.col_offset >> 2) + q), (uint32_t)node, (uint32_t)r, P.sweep_id,
-                         P.key0, P.key1);
+// The Philox block of the Gibbs draws of node `node`, minibatch column j and
+// the replica quad 4 rq .. 4 rq + 3: counter {g, node, rq, sweep} with g =
+// col_offset + j the global column; word c is replica 4 rq + c's uniform.
+__device__ __forceinline__ Philox4 gibbs_block(const SweepParams &P, int node, int rq, int64_t j) {
+    return philox4x32_10((uint32_t)(P.col_offset + j), (uint32_t)node, (uint32_t)rq, P.sweep_id, P.key0,
+                         P.key1);
+}
+
+// The Gibbs uniform word of one (node, replica r, minibatch column j).
+__device__ __forceinline__ uint32_t gibbs_word(const SweepParams &P, int node, int r, int64_t j) {
+    const Philox4 b = gibbs_block(P, node, r >> 2, j);
+    const int c = r & 3;
+    return c == 0 ? b.w[0] : c == 1 ? b.w[1] : c == 2 ? b.w[2] : b.w[3];
 }
 
 __device__ __forceinline__ float uniform24(uint32_t word) { return (float)(word >> 8) * 0x1p-24f; }
 
-// Replicas r0 .. r0+NR-1 of one column quad on the product path: all their
-// blanket loads in flight together, then the products, the draws and the
-// stores.
-template <int KP, typename ST, bool DEBUG, bool STAGED, int NR>
-__device__ __forceinline__ void product_replicas(const SweepParams &P, const Work &W, lds_char *lds,
-                                                 global_char *gtab, cint32_t *grp, int K, int n_groups,
-                                                 int n_staged, int64_t q, int lat,
-                                                 const uint32_t (&vmask)[2], int r0) {
-    using Q = Quad<ST>;
+// ------------------------------------------------------- sweep items
+//
+// The fast kernel's unit of work is an item: one latent column j of the
+// block's column chunk and a quad of replicas 4 rq .. 4 rq + 3 (fewer at the
+// end of the replica range).  All four draws of an item are latent -- the
+// obs mask is shared by the replicas -- so no lane computes a conditional
+// that nobody draws, and one Philox block gives the item's four uniforms.
+// Replica slot c of an item reads row (node, 4 rq + c) at column j; the four
+// slots' states are packed as two words of 16-bit lanes, slots (0, 2) and
+// (1, 3), for the v_pk_mad_u16 index arithmetic.
+
+// Packed index of replica slot c.
+__device__ __forceinline__ uint32_t slot_index(const uint32_t (&Pk)[2], int c) {
+    const uint32_t v = Pk[c & 1];
+    return (c >> 1) ? v >> 16 : v & 0xffffu;
+}
+
+template <typename ST>
+__device__ __forceinline__ uint32_t load_state(__amdgpu_buffer_rsrc_t r, uint32_t boff) {
+    if constexpr (sizeof(ST) == 1) return (uint32_t)__builtin_amdgcn_raw_buffer_load_b8(r, (int)boff, 0, 0);
+    else return (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(r, (int)boff, 0, 0);
+}
+
+template <typename ST>
+__device__ __forceinline__ void store_state(__amdgpu_buffer_rsrc_t r, uint32_t boff, int x) {
+    if constexpr (sizeof(ST) == 1) __builtin_amdgcn_raw_buffer_store_b8((uint8_t)x, r, (int)boff, 0, 0);
+    else __builtin_amdgcn_raw_buffer_store_b16((uint16_t)x, r, (int)boff, 0, 0);
+}
+
+// Buffer resource over node `node`'s m replica rows (offsets past them read 0).
+template <typename ST>
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t node_rsrc(const ST *states, int32_t node, int64_t vstride) {
+    return buffer_rsrc(states + (int64_t)node * vstride, (uint32_t)(vstride * (int64_t)sizeof(ST)));
+}
+
+constexpr int kItemBatch = 4;  // blanket entries whose 4 replica loads are in flight together
+
+// Adds the N entries (node, mult) at e to the item's packed index: every
+// entry's four replica states are loaded before the first is used.
+template <int N, typename ST>
+__device__ __forceinline__ void item_entries(cint32_t *e, const ST *__restrict__ states, int64_t vstride,
+                                             const uint32_t (&boff)[4], uint32_t (&Pk)[2]) {
+    uint32_t v[N][4];
+#pragma unroll
+    for (int t = 0; t < N; ++t) {
+        const __amdgpu_buffer_rsrc_t r = node_rsrc<ST>(states, e[2 * t], vstride);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) v[t][c] = load_state<ST>(r, boff[c]);
+    }
+#pragma unroll
+    for (int t = 0; t < N; ++t) {
+        const uint32_t mult = (uint32_t)e[2 * t + 1];
+        Pk[0] = pk_mad_u16(v[t][0] | (v[t][2] << 16), mult, Pk[0]);
+        Pk[1] = pk_mad_u16(v[t][1] | (v[t][3] << 16), mult, Pk[1]);
+    }
+}
+
+// Packed index of one group of a fast list for an item; advances g.
+template <typename ST>
+__device__ __forceinline__ void item_group(cint32_t *&g, const ST *__restrict__ states, int64_t vstride,
+                                           const uint32_t (&boff)[4], uint32_t (&Pk)[2]) {
+    int n_e = g[0];
+    Pk[0] = Pk[1] = (uint32_t)g[1];
+    cint32_t *e = g + 2;
+    g += 2 + 2 * n_e;
+    for (; n_e > 0; n_e -= kItemBatch, e += 2 * kItemBatch) {
+        switch (n_e < kItemBatch ? n_e : kItemBatch) {
+        case 1: item_entries<1, ST>(e, states, vstride, boff, Pk); break;
+        case 2: item_entries<2, ST>(e, states, vstride, boff, Pk); break;
+        case 3: item_entries<3, ST>(e, states, vstride, boff, Pk); break;
+        default: item_entries<4, ST>(e, states, vstride, boff, Pk); break;
+        }
+    }
+}
+
+// Multiplies the k-vectors of a group into the four slots' weights (from LDS
+// when FROM_LDS, else from global memory).
+template <int KP, bool FROM_LDS, bool RESCALE>
+__device__ __forceinline__ void item_multiply(lds_char *lds, global_char *gtab, const uint32_t (&Pk)[2],
+                                              float (&w)[4][KP]) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        float f[KP];
+        fast_kvec<KP, FROM_LDS>(lds, gtab, slot_index(Pk, c), f);
+#pragma unroll
+        for (int k = 0; k < KP; ++k) w[c][k] *= f[k];
+        if (RESCALE) renorm<KP>(w[c]);
+    }
+}
+
+// Unnormalised full conditional (Sec. 4: own CPT entry times the children's
+// entries) of the item's four replica slots from a fast product list: the
+// first n_staged groups read their k-vectors from the LDS copy of the record
+// (byte indices), the others from global memory (k-vector units).  The
+// weights start at one (exact).  With RESCALE every running product is
+// renormalised after each factor, which keeps it away from fp32 underflow.
+template <int KP, typename ST, bool STAGED, bool RESCALE>
+__device__ __forceinline__ void item_product(cint32_t *g, int n_groups, int n_staged, lds_char *lds,
+                                             global_char *gtab, const ST *__restrict__ states, int64_t vstride,
+                                             const uint32_t (&boff)[4], float (&w)[4][KP]) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+#pragma unroll
+        for (int k = 0; k < KP; ++k) w[c][k] = 1.f;
+    uint32_t Pk[2];
+    // the staged groups, then the global ones: two loops, so that each keeps
+    // only its own addressing live
+    int j = 0;
+    if (STAGED) {
+        for (; j < n_staged; ++j) {
+            item_group<ST>(g, states, vstride, boff, Pk);
+            item_multiply<KP, true, RESCALE>(lds, gtab, Pk, w);
+        }
+    }
+    for (; j < n_groups; ++j) {
+        item_group<ST>(g, states, vstride, boff, Pk);
+        item_multiply<KP, false, RESCALE>(lds, gtab, Pk, w);
+    }
+}
+
+// The block's latent columns and its replica range, as items.
+struct Items {
+    const uint16_t *col;  // latent columns of the chunk, as offsets from c0 (LDS)
+    int64_t c0;
+    int ncl, nrq, r0, r1;
+    float inv;            // 1 / ncl
+};
+
+// Item t -> (column j, first replica rb, replicas nrep).
+__device__ __forceinline__ void item_of(const Items &I, int t, int64_t &j, int &rb, int &nrep) {
+    int rq = (int)((float)t * I.inv);  // t, ncl < 2^24: off by at most one
+    int k = t - rq * I.ncl;
+    if (k < 0) {
+        --rq;
+        k += I.ncl;
+    } else if (k >= I.ncl) {
+        ++rq;
+        k -= I.ncl;
+    }
+    j = I.c0 + I.col[k];
+    rb = I.r0 + 4 * rq;
+    nrep = I.r1 - rb < 4 ? I.r1 - rb : 4;
+}
+
+// Product path (classes 0 and 1, KP <= 8): the block's items, one per lane
+// at a time.
+template <int KP, typename ST, bool DEBUG, bool STAGED>
+__device__ __forceinline__ void sweep_product(const SweepParams &P, const Work &W, const Items &I, lds_char *lds,
+                                              global_char *gtab) {
+    cint32_t *d = W.d;
+    const int K = d[0], n_groups = d[8], n_staged = STAGED ? d[13] : 0;
+    cint32_t *grp = d + d[9];
     ST *states = reinterpret_cast<ST *>(P.states);
     const int64_t vstride = (int64_t)P.m * P.ld;
-    const int64_t col = q * 4;
-    uint32_t boff[NR];
-    typename Q::V cur[NR];
+    const __amdgpu_buffer_rsrc_t own = node_rsrc<ST>(states, W.node, vstride);
+    const int n_items = I.ncl * I.nrq;
+    for (int t = threadIdx.x; t < n_items; t += kSweepBlock) {
+        int64_t j;
+        int rb, nrep;
+        item_of(I, t, j, rb, nrep);
+        uint32_t boff[4];
 #pragma unroll
-    for (int r = 0; r < NR; ++r) {
-        boff[r] = (uint32_t)((r0 + r) * P.ld + col) * (uint32_t)sizeof(ST);
-        cur[r] = load_row<ST>(states, W.node, vstride, boff[r]);
-    }
-    float w[NR][4][KP];
-    fast_product<KP, ST, STAGED, false, NR>(grp, n_groups, n_staged, lds, gtab, states, vstride, boff, vmask, w);
-    float wd[4][KP];
-    if (DEBUG) {
+        for (int c = 0; c < 4; ++c) boff[c] = (uint32_t)((rb + c) * P.ld + j) * (uint32_t)sizeof(ST);
+        float w[4][KP];
+        item_product<KP, ST, STAGED, false>(grp, n_groups, n_staged, lds, gtab, states, vstride, boff, w);
+        float wd[4][KP];
+        if (DEBUG) {
 #pragma unroll
-        for (int c = 0; c < 4; ++c)
+            for (int c = 0; c < 4; ++c)
 #pragma unroll
-            for (int k = 0; k < KP; ++k) wd[c][k] = w[0][c][k];
-    }
-    bool low = false;
-#pragma unroll
-    for (int r = 0; r < NR; ++r)
+                for (int k = 0; k < KP; ++k) wd[c][k] = w[c][k];
+        }
+        bool low = false;
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
-            running_sums<KP>(w[r][c]);
-            low |= ((lat >> c) & 1) && !(w[r][c][KP - 1] >= kUnderflowZ);
+            running_sums<KP>(w[c]);
+            low |= c < nrep && !(w[c][KP - 1] >= kUnderflowZ);
         }
-    if (low) {
-        fast_product<KP, ST, STAGED, true, NR>(grp, n_groups, n_staged, lds, gtab, states, vstride, boff, vmask,
-                                               w);
-#pragma unroll
-        for (int r = 0; r < NR; ++r)
+        if (low) {
+            item_product<KP, ST, STAGED, true>(grp, n_groups, n_staged, lds, gtab, states, vstride, boff, w);
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
                 if (DEBUG) {
 #pragma unroll
-                    for (int k = 0; k < KP; ++k) wd[c][k] = w[0][c][k];
+                    for (int k = 0; k < KP; ++k) wd[c][k] = w[c][k];
                 }
-                running_sums<KP>(w[r][c]);
+                running_sums<KP>(w[c]);
             }
-    }
-#pragma unroll
-    for (int r = 0; r < NR; ++r) {
-        const Philox4 rnd = gibbs_block(P, W.node, r0 + r, q);
+        }
+        const Philox4 rnd = gibbs_block(P, W.node, rb >> 2, j);
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
-            if (!((lat >> c) & 1)) continue;
-            cur[r] = Q::put(cur[r], c, draw_sums<KP>(w[r][c], K, uniform24(rnd.w[c])));
-            if (DEBUG) write_probs(P, W.node, r0, col + c, wd[c], K, w[0][c][KP - 1]);
+            if (c < nrep) {
+                store_state<ST>(own, boff[c], draw_sums<KP>(w[c], K, uniform24(rnd.w[c])));
+                if (DEBUG) write_probs(P, W.node, rb + c, j, wd[c], K, w[c][KP - 1]);
+            }
         }
-        Q::store(reinterpret_cast<ST *>(reinterpret_cast<char *>(states + (int64_t)W.node * vstride) + boff[r]),
-                 cur[r]);
     }
 }
 
-// Fast product path (classes 0 and 1, KP <= 8): replicas in groups of NR
-// (one at a time in debug mode, where the conditionals are written out).
-template <int KP, typename ST, bool DEBUG, bool STAGED, int NR>
-__device__ __forceinline__ void sweep_product(const SweepParams &P, const Work &W, lds_char *lds, global_char *gtab) {
-    cint32_t *d = W.d;
-    const int K = d[0], n_groups = d[8], n_staged = STAGED ? d[13] : 0;
-    cint32_t *grp = d + d[9];
-    constexpr int R = DEBUG ? 1 : NR;
-    for (int64_t q = W.q0 + threadIdx.x; q < W.q1; q += kSweepBlock) {
-        const int64_t col = q * 4;
-        const int lat = latent_bits(P, W.node, col);
-        if (!lat) continue;
-        uint32_t vmask[2];
-        valid_mask<ST>(P.n_cols - col < 4 ? (int)(P.n_cols - col) : 4, vmask);
-        int r = W.r0;
-        if (R > 1)
-            for (; r + R <= W.r1; r += R)
-                product_replicas<KP, ST, DEBUG, STAGED, R>(P, W, lds, gtab, grp, K, n_groups, n_staged, q, lat,
-                                                           vmask, r);
-        for (; r < W.r1; ++r)
-            product_replicas<KP, ST, DEBUG, STAGED, 1>(P, W, lds, gtab, grp, K, n_groups, n_staged, q, lat, vmask,
-                                                       r);
-    }
-}
-
-// Debug conditionals of a table-mode node, from its wide list (global tables).
+// Debug conditional of a table-mode node for replica r and column j, from
+// its wide list (global tables): the product over the quad of columns that
+// holds j, of which column j is written out.
 template <typename ST>
-__device__ void table_debug_probs(const SweepParams &P, const Work &W, int r, int64_t col, int lat,
-                                  int nvalid) {
+__device__ void table_debug_prob(const SweepParams &P, const Work &W, int r, int64_t j) {
     cint32_t *d = W.d;
     const int K = d[0], KP = d[1];
     const ST *states = reinterpret_cast<const ST *>(P.states);
+    const int64_t col = j & ~int64_t(3);
+    const int nvalid = P.n_cols - col < 4 ? (int)(P.n_cols - col) : 4;
+    const int c = (int)(j - col);
     const uint32_t lane_boff = (uint32_t)(r * P.ld + col) * (uint32_t)sizeof(ST);
     const int64_t vstride = (int64_t)P.m * P.ld;
     const float *tab = P.table + d[3];
@@ -694,12 +663,9 @@ __device__ void table_debug_probs(const SweepParams &P, const Work &W, int r, in
     {                                                                                             \
         float w[4][KPV];                                                                          \
         wide_product<KPV, ST, true>(d + d[11], d[10], tab, states, vstride, lane_boff, nvalid, w); \
-        for (int c = 0; c < 4; ++c) {                                                             \
-            if (!((lat >> c) & 1)) continue;                                                      \
-            float Z = 0.f;                                                                        \
-            for (int k = 0; k < KPV; ++k) Z += w[c][k];                                           \
-            write_probs(P, W.node, r, col + c, w[c], K, Z);                                       \
-        }                                                                                         \
+        float Z = 0.f;                                                                            \
+        for (int k = 0; k < KPV; ++k) Z += w[c][k];                                               \
+        write_probs(P, W.node, r, j, w[c], K, Z);                                                 \
     }
     if (KP == 2) SAME_TABLE_DEBUG(2)
     else if (KP == 4) SAME_TABLE_DEBUG(4)
@@ -759,109 +725,122 @@ __device__ __forceinline__ void read_thresholds(bool from_lds, lds_char *lds, gl
     }
 }
 
-// Replicas r0 .. r0+NR-1 of one column quad on the threshold path.
-template <int KT, typename ST, bool DEBUG, bool STAGED, int NR>
-__device__ __forceinline__ void table_replicas(const SweepParams &P, const Work &W, lds_char *lds,
-                                               global_char *gcond, cint32_t *grp, bool tab_lds, int64_t q,
-                                               int lat, int nvalid, const uint32_t (&vmask)[2], int r0) {
-    using Q = Quad<ST>;
-    ST *states = reinterpret_cast<ST *>(P.states);
-    const int64_t vstride = (int64_t)P.m * P.ld;
-    const int64_t col = q * 4;
-    uint32_t boff[NR];
-    typename Q::V cur[NR];
-#pragma unroll
-    for (int r = 0; r < NR; ++r) {
-        boff[r] = (uint32_t)((r0 + r) * P.ld + col) * (uint32_t)sizeof(ST);
-        cur[r] = load_row<ST>(states, W.node, vstride, boff[r]);
-    }
-    cint32_t *g = grp;
-    uint32_t Pk[NR][2];
-    packed_group_r<NR, ST>(g, states, vstride, boff, vmask, Pk);
-#pragma unroll
-    for (int r = 0; r < NR; ++r) {
-        const Philox4 rnd = gibbs_block(P, W.node, r0 + r, q);
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            if (!((lat >> c) & 1)) continue;
-            const uint32_t u24 = rnd.w[c] >> 8;
-            uint32_t th[KT];
-            read_thresholds<KT>(tab_lds, lds, gcond, packed_index<ST>(Pk[r], c), th);
-            int pick = 0;
-#pragma unroll
-            for (int k = 0; k < KT; ++k) pick += th[k] <= u24 ? 1 : 0;
-            cur[r] = Q::put(cur[r], c, pick);
-        }
-        if (DEBUG) table_debug_probs<ST>(P, W, r0 + r, col, lat, nvalid);
-        Q::store(reinterpret_cast<ST *>(reinterpret_cast<char *>(states + (int64_t)W.node * vstride) + boff[r]),
-                 cur[r]);
-    }
-}
-
-// Threshold path (classes 0 and 1): the blanket configuration selects KT
-// thresholds; the drawn state is the number of thresholds at or below the
-// 24-bit uniform.  Replicas in groups of NR (one at a time in debug mode).
-template <int KT, typename ST, bool DEBUG, bool STAGED, int NR>
-__device__ __forceinline__ void sweep_table(const SweepParams &P, const Work &W, lds_char *lds, global_char *gcond) {
+// Threshold path (classes 0 and 1): the blanket configuration of each
+// replica slot selects KT thresholds; the drawn state is the number of them
+// at or below the 24-bit uniform.
+template <int KT, typename ST, bool DEBUG, bool STAGED>
+__device__ __forceinline__ void sweep_table(const SweepParams &P, const Work &W, const Items &I, lds_char *lds,
+                                            global_char *gcond) {
     cint32_t *d = W.d;
     cint32_t *grp = d + d[9];
     const bool tab_lds = STAGED && d[13] > 0;  // uniform: thresholds staged in LDS
-    constexpr int R = DEBUG ? 1 : NR;
-    for (int64_t q = W.q0 + threadIdx.x; q < W.q1; q += kSweepBlock) {
-        const int64_t col = q * 4;
-        const int lat = latent_bits(P, W.node, col);
-        if (!lat) continue;
-        const int nvalid = P.n_cols - col < 4 ? (int)(P.n_cols - col) : 4;
-        uint32_t vmask[2];
-        valid_mask<ST>(nvalid, vmask);
-        int r = W.r0;
-        if (R > 1)
-            for (; r + R <= W.r1; r += R)
-                table_replicas<KT, ST, DEBUG, STAGED, R>(P, W, lds, gcond, grp, tab_lds, q, lat, nvalid, vmask, r);
-        for (; r < W.r1; ++r)
-            table_replicas<KT, ST, DEBUG, STAGED, 1>(P, W, lds, gcond, grp, tab_lds, q, lat, nvalid, vmask, r);
+    ST *states = reinterpret_cast<ST *>(P.states);
+    const int64_t vstride = (int64_t)P.m * P.ld;
+    const __amdgpu_buffer_rsrc_t own = node_rsrc<ST>(states, W.node, vstride);
+    const int n_items = I.ncl * I.nrq;
+    for (int t = threadIdx.x; t < n_items; t += kSweepBlock) {
+        int64_t j;
+        int rb, nrep;
+        item_of(I, t, j, rb, nrep);
+        uint32_t boff[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) boff[c] = (uint32_t)((rb + c) * P.ld + j) * (uint32_t)sizeof(ST);
+        cint32_t *g = grp;
+        uint32_t Pk[2];
+        item_group<ST>(g, states, vstride, boff, Pk);
+        const Philox4 rnd = gibbs_block(P, W.node, rb >> 2, j);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            if (c < nrep) {
+                const uint32_t u24 = rnd.w[c] >> 8;
+                uint32_t th[KT];
+                read_thresholds<KT>(tab_lds, lds, gcond, slot_index(Pk, c), th);
+                int pick = 0;
+#pragma unroll
+                for (int k = 0; k < KT; ++k) pick += th[k] <= u24 ? 1 : 0;
+                store_state<ST>(own, boff[c], pick);
+                if (DEBUG) table_debug_prob<ST>(P, W, rb + c, j);
+            }
+        }
     }
 }
 
-// Fast kernel: one block = one node x a run of column quads x a range of
-// replicas (block_work).  The node's mode selects the product path for KP =
-// 2, 4, 8 or the threshold path.  With STAGED the block first copies the
-// staged part of its node's table record (the whole record of a class-0 node:
-// k-vectors or thresholds; the smallest k-vector groups of a larger record)
-// into LDS, and the gathers of those groups are LDS reads.
-// At least kSweepWaves waves per SIMD: without the bound the compiler
-// schedules the staged kernel into 85 VGPRs (5 waves); with it, 66 VGPRs and
-// no spills, so the LDS budget (6 blocks of 24 KB per CU) sets the occupancy.
-// The debug variant (conditionals written out) keeps the default bound.
+// Fast kernel: one block = one node x a chunk of columns x a range of
+// replicas (block_work).  The block first lists the chunk's latent columns
+// of its node in LDS (a block-wide prefix sum over the lanes' obs words) and,
+// with STAGED, copies the staged part of its node's table record (the whole
+// record of a class-0 node: k-vectors or thresholds; the smallest k-vector
+// groups of a larger record) into LDS; then its lanes take the items
+// (latent column, replica quad) in turn.  The node's mode selects the
+// product path for KP = 2, 4, 6, 8 or the threshold path.
+// At least kSweepWaves waves per SIMD (the debug variant keeps the default
+// bound).
 template <typename ST, bool DEBUG, bool STAGED>
 __global__ __launch_bounds__(kSweepBlock, DEBUG ? 1 : kSweepWaves) void sweep_fast_kernel(SweepParams P) {
     extern __shared__ float4 lds4[];
+    __shared__ uint16_t lcol[4 * kSweepBlock];
+    __shared__ int32_t wave_n[kSweepBlock / 64];
     const Work W = block_work(P);
     if (W.q0 >= W.q1) return;  // uniform across the block
     cint32_t *d = W.d;
     const int mode = d[2];
     const float *tab = P.table + d[3];
     const uint32_t *cond = P.cond + d[5];
+    // latent columns of the chunk: lane l reads the obs word of columns
+    // c0 + 4l .. c0 + 4l + 3
+    const int64_t c0 = W.q0 * 4;
+    const int64_t col = c0 + 4 * (int64_t)threadIdx.x;
+    const int lat = col < W.q1 * 4 ? latent_bits(P, W.node, col) : 0;
+    const int cnt = __builtin_popcount(lat);
+    const uint64_t b0 = __ballot(cnt & 1), b1 = __ballot(cnt & 2), b2 = __ballot(cnt & 4);
+    auto below = [](uint64_t b) {  // set lanes below this one
+        return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(b >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)b, 0u));
+    };
+    const int pre = below(b0) + 2 * below(b1) + 4 * below(b2);
+    const int wave = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0)
+        wave_n[wave] = __builtin_popcountll(b0) + 2 * __builtin_popcountll(b1) + 4 * __builtin_popcountll(b2);
     if (STAGED) {
         const float4 *src = reinterpret_cast<const float4 *>(mode == kModeTable ? (const void *)cond
                                                                                 : (const void *)tab);
         const int len4 = d[14] >> 2;
         for (int i = threadIdx.x; i < len4; i += kSweepBlock) lds4[i] = src[i];
-        __syncthreads();
     }
+    __syncthreads();
+    int base = 0, ncl = 0;
+#pragma unroll
+    for (int v = 0; v < kSweepBlock / 64; ++v) {
+        const int nv = wave_n[v];
+        base += v < wave ? nv : 0;
+        ncl += nv;
+    }
+    int pos = base + pre;
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+        if ((lat >> c) & 1) lcol[pos++] = (uint16_t)(4 * threadIdx.x + c);
+    __syncthreads();
+    if (ncl == 0) return;  // uniform
+    Items I;
+    I.col = lcol;
+    I.c0 = c0;
+    I.ncl = ncl;
+    I.r0 = W.r0;
+    I.r1 = W.r1;
+    I.nrq = (W.r1 - W.r0 + 3) >> 2;
+    I.inv = 1.f / (float)ncl;
     lds_char *lds = (lds_char *)lds4;
     global_char *gt = scalar_global_ptr(tab);
-    if (mode == kModeKP2) sweep_product<2, ST, DEBUG, STAGED, kPairKP2>(P, W, lds, gt);
-    else if (mode == kModeKP4) sweep_product<4, ST, DEBUG, STAGED, kPairKP4>(P, W, lds, gt);
-    else if (mode == kModeKP6) sweep_product<6, ST, DEBUG, STAGED, kPairKP6>(P, W, lds, gt);
-    else if (mode == kModeKP8) sweep_product<8, ST, DEBUG, STAGED, kPairKP8>(P, W, lds, gt);
+    if (mode == kModeKP2) sweep_product<2, ST, DEBUG, STAGED>(P, W, I, lds, gt);
+    else if (mode == kModeKP4) sweep_product<4, ST, DEBUG, STAGED>(P, W, I, lds, gt);
+    else if (mode == kModeKP6) sweep_product<6, ST, DEBUG, STAGED>(P, W, I, lds, gt);
+    else if (mode == kModeKP8) sweep_product<8, ST, DEBUG, STAGED>(P, W, I, lds, gt);
     else {
         const int KT = d[7];
         global_char *gc = scalar_global_ptr(cond);
-        if (KT == 1) sweep_table<1, ST, DEBUG, STAGED, kPairTable>(P, W, lds, gc);
-        else if (KT == 2) sweep_table<2, ST, DEBUG, STAGED, kPairTable>(P, W, lds, gc);
-        else if (KT == 4) sweep_table<4, ST, DEBUG, STAGED, kPairTable>(P, W, lds, gc);
-        else sweep_table<8, ST, DEBUG, STAGED, kPairTable>(P, W, lds, gc);
+        if (KT == 1) sweep_table<1, ST, DEBUG, STAGED>(P, W, I, lds, gc);
+        else if (KT == 2) sweep_table<2, ST, DEBUG, STAGED>(P, W, I, lds, gc);
+        else if (KT == 4) sweep_table<4, ST, DEBUG, STAGED>(P, W, I, lds, gc);
+        else sweep_table<8, ST, DEBUG, STAGED>(P, W, I, lds, gc);
     }
 }
 
@@ -895,10 +874,10 @@ __device__ void sweep_wide(const SweepParams &P, const Work &W) {
                 low |= ((lat >> c) & 1) && !(Z >= kUnderflowZ);
             }
             if (low) wide_product<KP, ST, true>(grp, n_groups, tab, states, vstride, lane_boff, nvalid, w);
-            const Philox4 rnd = gibbs_block(P, W.node, r, q);
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
                 if (!((lat >> c) & 1)) continue;
+                const uint32_t word = gibbs_word(P, W.node, r, col + c);
                 if (DEBUG) {
                     float Z = 0.f;
 #pragma unroll
@@ -906,7 +885,7 @@ __device__ void sweep_wide(const SweepParams &P, const Work &W) {
                     write_probs(P, W.node, r, col + c, w[c], K, Z);
                 }
                 running_sums<KP>(w[c]);
-                cur = Q::put(cur, c, draw_sums<KP>(w[c], K, uniform24(rnd.w[c])));
+                cur = Q::put(cur, c, draw_sums<KP>(w[c], K, uniform24(word)));
             }
             Q::store(reinterpret_cast<ST *>(reinterpret_cast<char *>(states + (int64_t)W.node * vstride) +
                                             lane_boff),
@@ -971,7 +950,6 @@ __global__ __launch_bounds__(kSweepBlock) void sweep_generic_kernel(SweepParams 
         if (!lat) continue;
         for (int r = W.r0; r < W.r1; ++r) {
             const ST *base = states + (int64_t)r * P.ld + col;
-            const Philox4 rnd = gibbs_block(P, W.node, r, q);
             ST *own = states + ((int64_t)W.node * P.m + r) * P.ld + col;
             typename Q::V cur = Q::load(own);
             for (int c = 0; c < 4; ++c) {
@@ -988,7 +966,7 @@ __global__ __launch_bounds__(kSweepBlock) void sweep_generic_kernel(SweepParams 
                     const float mk = weight_ext<ST>(d, tab, base, vstride, c, k, e);
                     Z += __builtin_ldexpf(mk, e - E);
                 }
-                const float t = uniform24(rnd.w[c]) * Z;
+                const float t = uniform24(gibbs_word(P, W.node, r, col + c)) * Z;
                 float S = 0.f;
                 int pick = -1, last_pos = 0;
                 for (int k = 0; k < K; ++k) {
@@ -1618,10 +1596,19 @@ hipError_t launch_sweep(SweepParams P, int32_t begin, int32_t count, int32_t kla
     const int64_t quads = (P.n_cols + 3) / 4;
     P.quads_per_block = (int64_t)dev::kSweepBlock * dev::kSweepQuadsPerLane;
     const int64_t chunks = (quads + P.quads_per_block - 1) / P.quads_per_block;
-    int64_t rsplit = klass == 0 ? (dev::kMinSweepBlocks + count * chunks - 1) / (count * chunks) : P.m;
-    if (rsplit > P.m) rsplit = P.m;
+    // the fast kernel draws replicas in quads (one Philox block each), so a
+    // block's replica range is whole quads except at the end
+    const int64_t m_quads = (P.m + 3) / 4;
+    int64_t rsplit = klass == 0 ? (dev::kMinSweepBlocks + count * chunks - 1) / (count * chunks) : m_quads;
+    if (klass >= 2) rsplit = P.m;
+    if (rsplit > (klass >= 2 ? P.m : m_quads)) rsplit = klass >= 2 ? P.m : m_quads;
     if (rsplit < 1) rsplit = 1;
-    P.reps_per_block = (int32_t)((P.m + rsplit - 1) / rsplit);
+    if (klass >= 2) {
+        P.reps_per_block = (int32_t)((P.m + rsplit - 1) / rsplit);
+    } else {
+        P.reps_per_block = (int32_t)(4 * ((m_quads + rsplit - 1) / rsplit));
+        if (P.reps_per_block > P.m) P.reps_per_block = P.m;
+    }
     P.rsplit = (int32_t)((P.m + P.reps_per_block - 1) / P.reps_per_block);
     P.n_slabs = chunks * P.rsplit;
     P.count = count;

@@ -30,14 +30,23 @@ def test_philox_known_answers(golden_dir):
 
 
 def test_gibbs_uniform_is_word_of_block():
-    # column g uses word g&3 of the block at counter g>>2; U24 = (w>>8) * 2^-24
+    # replica r of column g uses word r&3 of the block at counter
+    # {g, node, r>>2, sweep}; U24 = (w>>8) * 2^-24
     seed = 0x0123456789ABCDEF
-    for g in [0, 1, 2, 3, 4, 7, 1 << 20, (1 << 33) + 3]:
-        blk = oracle.philox4x32_10([g >> 2, 9, 3 | (0 << 24), 17],
-                                   [seed & 0xFFFFFFFF, seed >> 32])
-        u = oracle.gibbs_uniform(seed, 9, 3, g, 17)
-        assert u == (int(blk[g & 3]) >> 8) / 2.0 ** 24
-        assert 0.0 <= u < 1.0
+    for g in [0, 1, 2, 3, 4, 7, 1 << 20, (1 << 32) - 1]:
+        for r in [0, 1, 2, 3, 4, 7, 9, 37]:
+            blk = oracle.philox4x32_10([g, 9, (r >> 2) | (0 << 24), 17],
+                                       [seed & 0xFFFFFFFF, seed >> 32])
+            u = oracle.gibbs_uniform(seed, 9, r, g, 17)
+            assert u == (int(blk[r & 3]) >> 8) / 2.0 ** 24
+            assert 0.0 <= u < 1.0
+
+
+def test_gibbs_uniforms_distinct_across_replicas_and_columns():
+    # every (replica, column) pair of a node and sweep gets its own word
+    seed = 99
+    us = {(r, g): oracle.gibbs_uniform(seed, 4, r, g, 2) for r in range(12) for g in range(50)}
+    assert len(set(us.values())) == len(us)
 
 
 def test_uniform_chi_square():

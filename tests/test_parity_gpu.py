@@ -247,7 +247,7 @@ def test_int16_states(table_limit, variant):
 
 def test_large_replica_count_and_column_offset():
     net, st, ob, th = _custom([[], [0], [0, 1], [2], [3, 1]], [2, 3, 2, 4, 2], 256, 37, 0.5, 4)
-    _custom_case(net, st, ob, th, 37, 256, col_offset=(1 << 33) + 4096, win=(0, 32))
+    _custom_case(net, st, ob, th, 37, 256, col_offset=(1 << 32) - 8192, win=(0, 32))
 
 
 def test_underflow_rescale_path():
