@@ -45,7 +45,12 @@ def parse():
     p.add_argument("--cpu-sample-steps", type=int, default=2,
                    help="SAME steps (sweep + counts + resample) of the oracle baseline")
     p.add_argument("--copy-calibration", action="store_true",
-                   help="also run a plain 1 GiB device copy (for HBM counter scaling)")
+                   help="(kept for older profile commands: the 1 GiB copy now always runs)")
+    p.add_argument("--roofline-steps", type=int, default=1,
+                   help="instrumented passes after the timed ones, for the per-launch roofline")
+    p.add_argument("--parity-cols", type=int, default=32_768,
+                   help="columns of minibatch 0 on which the first GPU sweep is compared with the "
+                        "oracle's (flagged fraction, mismatch rate; 0 to skip)")
     p.add_argument("--gen-device", choices=["cuda", "cpu"], default="cuda",
                    help="where the synthetic inputs are generated (cpu: only the library's "
                         "kernels run on the GPU, for counter collection)")
@@ -116,6 +121,7 @@ def main():
         ctx = same.same_create_ex(pptr, pidx, card, w.alpha, args.table_limit)
     ws = ctx.new_workspace(dev)
     cpts = torch.from_numpy(w.init_theta).to(dev)
+    cpts0 = cpts.clone()
     mb = torch.from_numpy(np.zeros((w.M, ctx.cpt_total), dtype=np.int32)).to(dev)
     tot = torch.from_numpy(np.zeros(ctx.cpt_total, dtype=np.int32)).to(dev)
     stream = torch.cuda.current_stream()
@@ -138,9 +144,7 @@ def main():
         one_pass(s)
     torch.cuda.synchronize()
     log("warmup done")
-    # every sweep-kernel launch of the timed passes is bracketed by HIP events
-    # on the launch stream (the library records them; read after the region)
-    same.same_kernel_timing(ctx, True)
+    # the timed passes run without any per-launch instrumentation
     t_start = time.perf_counter()
     ev_start = torch.cuda.Event(enable_timing=True)
     ev_end = torch.cuda.Event(enable_timing=True)
@@ -150,25 +154,32 @@ def main():
     ev_end.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
-    kt = same.same_kernel_times(ctx)
-    same.same_kernel_timing(ctx, False)
     gpu_ms = ev_start.elapsed_time(ev_end)
     elapsed = max(wall, gpu_ms / 1e3)
     log("timed %d passes: wall %.3f s, events %.3f s" % (args.steps, wall, gpu_ms / 1e3))
-    log("sweep kernels per class (ms, launches): %s" % list(zip(kt["ms"], kt["launches"])))
-    log("colour phases: %.2f ms over %d" % (kt["phase_ms"], kt["phases"]))
     node_samples = float(net.n) * cols_timed * w.m * args.steps
     value = node_samples / elapsed
 
-    roofline = sweep_roofline(w, net, mbs, hidden, node_samples, kt, elapsed, args)
+    # then more passes of the same loop with every sweep-kernel launch
+    # bracketed by HIP events on its launch stream (the library records them)
+    # for the per-launch roofline figures
+    rsteps = max(1, args.roofline_steps)
+    same.same_kernel_timing(ctx, True)
+    t_r = time.perf_counter()
+    for s in range(args.warmup + args.steps, args.warmup + args.steps + rsteps):
+        one_pass(s)
+    torch.cuda.synchronize()
+    wall_r = time.perf_counter() - t_r
+    kt = same.same_kernel_times(ctx)
+    same.same_kernel_timing(ctx, False)
+    log("instrumented %d passes: %.3f s; sweep kernels per class (ms, launches): %s; colour phases %.2f ms" % (
+        rsteps, wall_r, list(zip(kt["ms"], kt["launches"])), kt["phase_ms"]))
+    node_samples_r = float(net.n) * cols_timed * w.m * rsteps
 
-    if args.copy_calibration:
-        # a plain device-to-device copy of exactly 1 GiB (runtime copy kernel)
-        a = torch.from_numpy(np.zeros(1 << 30, dtype=np.uint8)).to(dev)
-        b2 = torch.from_numpy(np.ones(1 << 30, dtype=np.uint8)).to(dev)
-        b2.copy_(a)
-        torch.cuda.synchronize()
-        del a, b2
+    copy_gbs = copy_peak(dev, stream)
+    roofline = sweep_roofline(w, net, mbs, hidden, node_samples_r, kt, wall_r, args, copy_gbs)
+
+
 
     ingest = None if args.no_ingest else ingest_timing(w, ctx, mbs[0], dev, stream)
     heldout = None if args.no_heldout else heldout_timing(w, ctx, mbs[0], dev, stream)
@@ -178,8 +189,12 @@ def main():
     if not args.no_stream and len(mbs) == w.M:
         streamed = stream_timing(w, ctx, cpts, ws, dev, args.stream_steps)
 
-    cpu = None
+    cpu = parity = None
     if sample is not None:
+        # untimed: the GPU's first sweep of the sample's leading columns
+        # against the oracle's, then the timed oracle baseline
+        if args.parity_cols > 0:
+            parity = first_sweep_parity(w, ctx, cpts0, ws, sample, args.parity_cols, dev)
         cpu = cpu_baseline(w, *sample, args.cpu_sample_steps)
 
     spec = CONFIGS[args.cfg]
@@ -214,6 +229,7 @@ def main():
         "latent_draws_per_s": round(value * hidden, 1),
         "hbm_gbs_algorithmic_step": round(node_samples * (1.0 + hidden + 1.0 / w.m) / elapsed / 1e9, 1),
         "roofline": roofline,
+        "parity": parity,
         "cpu_baseline": cpu,
         "streamed_from_host": streamed,
         "ingest": ingest,
@@ -274,7 +290,71 @@ def measured_traffic(cfg):
     return t
 
 
-def sweep_roofline(w, net, mbs, hidden, node_samples, kt, elapsed, args):
+def copy_peak(dev, stream, reps=5):
+    """Device-to-device copy rate of 1 GiB (torch's copy kernel), GB/s counting
+    the bytes read and written: the practical HBM ceiling beside the 8 TB/s
+    spec."""
+    import torch
+    a = torch.zeros(COPY_BYTES, dtype=torch.uint8, device=dev)
+    b = torch.ones(COPY_BYTES, dtype=torch.uint8, device=dev)
+    b.copy_(a)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        b.copy_(a)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del a, b
+    return 2.0 * COPY_BYTES / (ms / 1e3) / 1e9
+
+
+def first_sweep_parity(w, ctx, cpts0, ws, sample, cols, dev):
+    """The library's production sweep (same_sweep) and the oracle's sweep from
+    the same generated states of the first `cols` columns of minibatch 0, with
+    the starting CPTs, seed and sweep id 0.  A chain (column, replica) may
+    differ only from a flagged draw on (a uniform within 1e-6 of a CDF
+    boundary) in visit order; reports the flagged fraction of the latent draws
+    and the mismatch rate (chains that differ, per latent draw)."""
+    import numpy as np
+    import torch
+
+    import oracle
+    import paper_1511_06416_amd as same
+    net = w.net
+    _cols, st, ob, = sample
+    cols = min(cols, _cols) // 4 * 4
+    pre = np.ascontiguousarray(st[:, :, :cols])
+    obs = np.ascontiguousarray(ob[:, :cols])
+    d_st = torch.from_numpy(pre).to(dev)
+    d_ob = torch.from_numpy(obs).to(dev)
+    same.same_sweep(ctx, d_st, d_ob, cpts0, w.m, cols, cols, 0, w.seed, 0, ws)
+    torch.cuda.synchronize()
+    gpu = d_st.cpu().numpy()
+    del d_st, d_ob
+    ref = pre.copy()
+    color = oracle.graph(net.parents, net.card)["color"]
+    res = oracle.sweep(net.parents, net.card, cpts0.cpu().numpy(), color, ref, obs, w.m, cols, 0, w.seed, 0,
+                       want_flags=True)
+    flags = res["flags"]
+    draws = int((obs == 0).sum()) * w.m
+    order = np.array(sorted(range(net.n), key=lambda i: (int(color[i]), i)))
+    diff = (gpu != ref)[order]
+    chains = diff.any(axis=0)
+    first = diff.argmax(axis=0)
+    fl = np.take_along_axis(flags[order], first[None], axis=0)[0]
+    n_chains = int(chains.sum())
+    unexcused = int((chains & (fl == 0)).sum())
+    n_flag = int(flags.sum())
+    return {"sample": "first %d columns of minibatch 0 (all nodes, m=%d), sweep 0 from the generated states"
+                      % (cols, w.m),
+            "latent_draws": draws, "flagged_draws": n_flag, "flagged_fraction": n_flag / max(draws, 1),
+            "mismatched_chains": n_chains, "mismatch_rate": n_chains / max(draws, 1),
+            "unexcused_mismatches": unexcused, "ok": unexcused == 0 and n_chains < 1e-5 * draws}
+
+
+def sweep_roofline(w, net, mbs, hidden, node_samples, kt, elapsed, args, copy_gbs):
     """Roofline of the dominant kernel, the LDS-staged sweep kernel
     (sweep_fast_kernel<int8, false, true>, launch class 0), which draws almost
     every node of the workload in one launch per colour group: the algorithmic
@@ -293,7 +373,7 @@ def sweep_roofline(w, net, mbs, hidden, node_samples, kt, elapsed, args):
     lat = np.zeros(net.n)
     for b in mbs:
         lat += (w.obs[b][:, :w.mb_cols(b)] == 0).sum(dim=1).cpu().numpy().astype(np.float64)
-    ops = float((alu_ops_per_draw(net) * lat).sum()) * w.m * args.steps
+    ops = float((alu_ops_per_draw(net) * lat).sum()) * w.m * max(1, args.roofline_steps)
     ms0, n0, ns0 = kt["ms"][0], kt["launches"][0], kt["node_samples"][0]
     bytes0 = ns0 * bytes_per_ns
     ops0 = ops * ns0 / node_samples   # at the workload's mean operations per slot
@@ -312,6 +392,8 @@ def sweep_roofline(w, net, mbs, hidden, node_samples, kt, elapsed, args):
         "unit": "GB/s",
         "frac": round(hbm / HBM_PEAK_GBS, 4),
         "traffic": None if traffic is None else traffic["hbm_bytes_per_launch"],
+        "copy_peak_gbs": round(copy_gbs, 1),
+        "frac_of_copy_peak": round(hbm / copy_gbs, 4),
         "algorithmic_bytes_per_launch": round(bytes0 / n0, 1),
         "bytes_per_node_sample": round(bytes_per_ns, 4),
         "node_samples_share": round(ns0 / node_samples, 4),
@@ -337,6 +419,14 @@ def sweep_roofline(w, net, mbs, hidden, node_samples, kt, elapsed, args):
     }
     if traffic is not None:
         out["traffic_gbs"] = round(traffic["hbm_bytes_per_launch"] / (avg_ms / 1e3) / 1e9, 1)
+        if traffic.get("valu_insts_per_launch"):
+            # executed VALU wave instructions (counters) beside the algorithmic
+            # operation count: 64 lanes x 4 cycles each on a 16-lane SIMD
+            out["alu"]["valu_insts_per_node_sample"] = round(
+                traffic["valu_insts_per_launch"] / (ns0 / n0), 4)
+            out["alu"]["valu_issue_frac"] = round(
+                traffic["valu_insts_per_launch"] * 4 / 1024 / (avg_ms / 1e3 * 2.4e9), 4)
+    out["timing"] = "per-launch figures from %d instrumented pass(es) after the timed ones" % args.roofline_steps
     return out
 
 
@@ -412,6 +502,8 @@ def counters_summary(paths, cfg):
         "write_bytes_per_launch": round(wb, 1),
         "hbm_bytes_per_launch": round(fb + wb, 1),
         "dispatches": {"fetch": nf, "write": nw},
+        "valu_insts_per_launch": (round(per_launch("SQ_INSTS_VALU")[0] / 1024, 1)
+                                  if any((k, "SQ_INSTS_VALU") in seen for k in sweep) else None),
         "sources_sha256": source_hash(),
     }
     path = traffic_path(cfg)
