@@ -87,7 +87,12 @@ typedef struct {
  * Builds a context for one network (Sec. 1 problem statement; Sec. 4 colour
  * groups).  Host only: validates the DAG, orders it topologically, builds the
  * moralized graph (parents joined, directions dropped), colours it first-fit
- * over a Kahn topological order that takes the smallest ready id, lays out
+ * over a Kahn topological order that takes the smallest ready id and then
+ * balances the colour groups (Sec. 4 asks for groups of balanced size):
+ * repeatedly, the first node -- scanning groups from the largest (ties:
+ * lower colour), nodes by ascending id -- that can move to a group at least
+ * two nodes smaller (scanning from the smallest, ties: lower colour) without
+ * a moral neighbour there moves to it, until no such move is left; lays out
  * the CPTs and the per-node Markov-blanket tables.  dirichlet_prior (> 0) is
  * the Dirichlet parameter added to every count in same_sample_cpts.  The
  * arrays are copied; the caller may free them after the call.
@@ -122,6 +127,11 @@ typedef struct {
      * 2^16 rows use packed 16-bit arithmetic; 0: every product-mode node uses
      * the 32-bit path.  Results do not depend on it. */
     int32_t packed_indices;
+    /* 0 (default): the first-fit colouring is balanced by single-node moves
+     * between colour groups that keep it proper (see same_create); 1: the
+     * first-fit colouring as it is.  The colouring fixes the order of the
+     * sequential scan the sweep equals, so it changes the sample path. */
+    int32_t first_fit_colours;
 } same_options_t;
 
 /* same_create with options (opts may be NULL for the defaults). */

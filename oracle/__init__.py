@@ -60,6 +60,8 @@ def lib():
             L.oracle_gibbs_uniform.restype = C.c_double
             L.oracle_graph.argtypes = [C.c_int32, P, P, P, P, P, P, P]
             L.oracle_graph.restype = C.c_int
+            L.oracle_graph_ex.argtypes = [C.c_int32, P, P, P, C.c_int32, P, P, P, P]
+            L.oracle_graph_ex.restype = C.c_int
             L.oracle_moral.argtypes = [C.c_int32, P, P, P, P]
             L.oracle_moral.restype = C.c_int
             L.oracle_conditional.argtypes = [C.c_int32, P, P, P, P, P, C.c_int32, P]
@@ -146,16 +148,17 @@ def gibbs_uniform(seed, node, replica, gcol, sweep_id):
 # Graph
 
 
-def graph(parents, card):
-    """Returns dict(cpt_off[n+1], topo[n], color[n], n_colors)."""
+def graph(parents, card, balance=True):
+    """Returns dict(cpt_off[n+1], topo[n], color[n], n_colors); balance=False
+    gives the first-fit colouring before the balancing moves."""
     pptr, pidx, card = _dag(parents, card)
     n = len(card)
     off = np.zeros(n + 1, dtype=np.int64)
     topo = np.zeros(n, dtype=np.int32)
     color = np.zeros(n, dtype=np.int32)
     nc = C.c_int32(0)
-    _check(lib().oracle_graph(n, _ptr(pptr), _ptr(pidx), _ptr(card), _ptr(off), _ptr(topo),
-                              _ptr(color), C.byref(nc)))
+    _check(lib().oracle_graph_ex(n, _ptr(pptr), _ptr(pidx), _ptr(card), 1 if balance else 0, _ptr(off),
+                                 _ptr(topo), _ptr(color), C.byref(nc)))
     return {"cpt_off": off, "topo": topo, "color": color, "n_colors": nc.value}
 
 

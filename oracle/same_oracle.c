@@ -29,7 +29,9 @@
  *     parent order with the LAST parent fastest; entry = off_i + u*K_i + k.
  *   - Colouring: first-fit greedy over a Kahn topological order that always
  *     takes the smallest ready node id; each node gets the smallest colour not
- *     used by an already coloured moral neighbour.
+ *     used by an already coloured moral neighbour; then the groups are
+ *     balanced by single-node moves that keep the colouring proper
+ *     (balance_colouring).
  *   - Random numbers: Philox4x32-10 (Salmon, Moraes, Dror & Shaw, SC'11).
  *     Gibbs draw for node i, replica r, global column g, sweep s uses word
  *     (r & 3) of Philox(ctr = {g, i, (r>>2) | (0<<24), s}, key = {seed_lo, seed_hi});
@@ -217,12 +219,71 @@ static int graph_build(graph_t *g, int32_t n, const int32_t *pptr, const int32_t
 }
 
 /*
+ * Balancing of a proper colouring (Sec. 4 asks for colour groups of balanced
+ * size): repeatedly move one node from a larger group to a group at least two
+ * smaller, when none of its moral neighbours is in that group (so the
+ * colouring stays proper).  Which move: groups by decreasing size (ties:
+ * lower colour first), inside a group nodes by ascending id, targets by
+ * increasing size (ties: lower colour first); the first valid move is made
+ * and the search starts again.  Every move lowers the sum of squared group
+ * sizes, so this ends; no group empties.  adj is the dense moral adjacency.
+ */
+static void balance_colouring(int32_t n, const char *adj, int32_t ncol, int32_t *col) {
+    int32_t *size = (int32_t *)calloc((size_t)ncol, sizeof(int32_t));
+    int32_t *by_desc = (int32_t *)calloc((size_t)ncol, sizeof(int32_t));
+    int32_t *by_asc = (int32_t *)calloc((size_t)ncol, sizeof(int32_t));
+    for (;;) {
+        for (int32_t c = 0; c < ncol; ++c) size[c] = 0;
+        for (int32_t v = 0; v < n; ++v) size[col[v]]++;
+        /* the two orders, by insertion sort */
+        for (int32_t c = 0; c < ncol; ++c) by_desc[c] = by_asc[c] = c;
+        for (int32_t i = 1; i < ncol; ++i)
+            for (int32_t j = i; j > 0; --j) {
+                int32_t x = by_desc[j - 1], y = by_desc[j];
+                if (size[y] > size[x] || (size[y] == size[x] && y < x)) {
+                    by_desc[j - 1] = y; by_desc[j] = x;
+                }
+                x = by_asc[j - 1]; y = by_asc[j];
+                if (size[y] < size[x] || (size[y] == size[x] && y < x)) {
+                    by_asc[j - 1] = y; by_asc[j] = x;
+                }
+            }
+        int moved = 0;
+        for (int32_t ia = 0; ia < ncol && !moved; ++ia) {
+            int32_t a = by_desc[ia];
+            for (int32_t v = 0; v < n && !moved; ++v) {
+                if (col[v] != a) continue;
+                for (int32_t ib = 0; ib < ncol; ++ib) {
+                    int32_t b = by_asc[ib];
+                    if (size[b] + 1 >= size[a]) break;
+                    int clash = 0;
+                    for (int32_t w = 0; w < n; ++w)
+                        if (adj[(size_t)v * n + w] && col[w] == b) { clash = 1; break; }
+                    if (!clash) { col[v] = b; moved = 1; break; }
+                }
+            }
+        }
+        if (!moved) break;
+    }
+    free(size); free(by_desc); free(by_asc);
+}
+
+/*
  * Topological order (Kahn, smallest ready id first), moral graph and the
- * first-fit colouring.  Outputs: cpt_off[n+1], topo[n], color[n], *n_colors.
+ * colouring: first-fit over the topological order, then (balance != 0) the
+ * balancing above.  Outputs: cpt_off[n+1], topo[n], color[n], *n_colors.
  * Any output pointer may be NULL.
  */
+int oracle_graph_ex(int32_t n, const int32_t *pptr, const int32_t *pidx, const int32_t *card,
+                    int32_t balance, int64_t *cpt_off, int32_t *topo, int32_t *color, int32_t *n_colors);
+
 int oracle_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int32_t *card,
                  int64_t *cpt_off, int32_t *topo, int32_t *color, int32_t *n_colors) {
+    return oracle_graph_ex(n, pptr, pidx, card, 1, cpt_off, topo, color, n_colors);
+}
+
+int oracle_graph_ex(int32_t n, const int32_t *pptr, const int32_t *pidx, const int32_t *card,
+                    int32_t balance, int64_t *cpt_off, int32_t *topo, int32_t *color, int32_t *n_colors) {
     graph_t g;
     int rc = graph_build(&g, n, pptr, pidx, card);
     if (rc) return rc;
@@ -271,6 +332,7 @@ int oracle_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int3
         col[v] = c;
         if (c + 1 > ncol) ncol = c + 1;
     }
+    if (balance) balance_colouring(n, adj, ncol, col);
     if (topo) memcpy(topo, order, sizeof(int32_t) * (size_t)n);
     if (color) memcpy(color, col, sizeof(int32_t) * (size_t)n);
     if (n_colors) *n_colors = ncol;

@@ -45,7 +45,7 @@ class SameError(RuntimeError):
 
 class _Options(C.Structure):
     _fields_ = [("table_limit", C.c_int64), ("tile_bytes", C.c_int64), ("lds_limit", C.c_int64),
-                ("packed_indices", C.c_int32)]
+                ("packed_indices", C.c_int32), ("first_fit_colours", C.c_int32)]
 
 
 class _KernelTimes(C.Structure):
@@ -145,18 +145,19 @@ class Context:
     """Owns one same_ctx (one network)."""
 
     def __init__(self, parent_ptr, parent_idx, card, dirichlet_prior=1.0, table_limit=None,
-                 tile_bytes=0, lds_limit=None, packed_indices=True):
+                 tile_bytes=0, lds_limit=None, packed_indices=True, first_fit_colours=False):
         L = load_library()
         self._pptr = np.ascontiguousarray(parent_ptr, dtype=np.int32)
         self._pidx = np.ascontiguousarray(parent_idx if len(parent_idx) else [0], dtype=np.int32)
         self._card = np.ascontiguousarray(card, dtype=np.int32)
         h = C.c_void_p()
-        if table_limit is None and not tile_bytes and lds_limit is None and packed_indices:
+        if table_limit is None and not tile_bytes and lds_limit is None and packed_indices and not first_fit_colours:
             _check(L.same_create(len(self._card), self._pptr.ctypes.data, self._pidx.ctypes.data,
                                  self._card.ctypes.data, float(dirichlet_prior), C.byref(h)))
         else:
             opts = _Options(-1 if table_limit is None else int(table_limit), int(tile_bytes),
-                            -1 if lds_limit is None else int(lds_limit), 1 if packed_indices else 0)
+                            -1 if lds_limit is None else int(lds_limit), 1 if packed_indices else 0,
+                            1 if first_fit_colours else 0)
             _check(L.same_create_ex(len(self._card), self._pptr.ctypes.data,
                                     self._pidx.ctypes.data, self._card.ctypes.data,
                                     float(dirichlet_prior), C.byref(opts), C.byref(h)))
@@ -200,9 +201,10 @@ def same_create(parent_ptr, parent_idx, card, dirichlet_prior=1.0) -> Context:
 
 
 def same_create_ex(parent_ptr, parent_idx, card, dirichlet_prior=1.0, table_limit=-1,
-                   tile_bytes=0, lds_limit=-1, packed_indices=True) -> Context:
+                   tile_bytes=0, lds_limit=-1, packed_indices=True, first_fit_colours=False) -> Context:
     return Context(parent_ptr, parent_idx, card, dirichlet_prior, table_limit=table_limit,
-                   tile_bytes=tile_bytes, lds_limit=lds_limit, packed_indices=packed_indices)
+                   tile_bytes=tile_bytes, lds_limit=lds_limit, packed_indices=packed_indices,
+                   first_fit_colours=first_fit_colours)
 
 
 def same_destroy(ctx: Context) -> None:

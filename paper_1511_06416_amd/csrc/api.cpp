@@ -483,6 +483,9 @@ int same_create_ex(int32_t n_nodes, const int32_t *parent_ptr, const int32_t *pa
     if (opts && opts->packed_indices != 0 && opts->packed_indices != 1)
         return set_error(SAME_EINVAL, "packed_indices must be 0 or 1");
     const bool packed = !opts || opts->packed_indices != 0;
+    if (opts && opts->first_fit_colours != 0 && opts->first_fit_colours != 1)
+        return set_error(SAME_EINVAL, "first_fit_colours must be 0 or 1");
+    const bool balance = !opts || opts->first_fit_colours == 0;
     *out = nullptr;
     if (!(dirichlet_prior > 0.0)) return set_error(SAME_EINVAL, "dirichlet_prior must be > 0");
     same_ctx *ctx = new (std::nothrow) same_ctx();
@@ -491,7 +494,7 @@ int same_create_ex(int32_t n_nodes, const int32_t *parent_ptr, const int32_t *pa
     int rc;
     try {
         rc = same::compile_graph(n_nodes, parent_ptr, parent_idx, card, ctx->g, err, table_limit,
-                                 lds_limit, packed);
+                                 lds_limit, packed, balance);
     } catch (const std::bad_alloc &) {
         rc = SAME_ENOMEM;
         err = "out of host memory";

@@ -4,6 +4,7 @@
 #include <algorithm>
 #include <functional>
 #include <queue>
+#include <set>
 
 #include "../../include/same.h"
 
@@ -35,8 +36,59 @@ int32_t thresholds_per_config(int32_t K) {
     return t;
 }
 
+// Balanced colour groups (Sec. 4 colours the moralized graph with groups of
+// balanced size): single-node moves from a group to one at least two nodes
+// smaller, allowed only when the node has no moral neighbour in the target
+// group.  The move taken is the first found scanning source groups from the
+// largest (ties: lower colour), their nodes by ascending id, and target
+// groups from the smallest (ties: lower colour); then the scan restarts.
+// Each move lowers the sum of squared group sizes, so the loop ends, and
+// no group empties.  nbc[v][c] counts v's neighbours of colour c.
+static void balance_colours(const std::vector<std::vector<int32_t>> &nb, int32_t n_colors, std::vector<int32_t> &color) {
+    const int32_t n = (int32_t)color.size();
+    if (n_colors < 2) return;
+    std::vector<std::vector<int32_t>> nbc(n, std::vector<int32_t>(n_colors, 0));
+    std::vector<std::set<int32_t>> members(n_colors);
+    for (int32_t v = 0; v < n; ++v) {
+        members[color[v]].insert(v);
+        for (int32_t w : nb[v]) nbc[v][color[w]]++;
+    }
+    std::vector<int32_t> desc(n_colors), asc(n_colors);
+    for (;;) {
+        for (int32_t c = 0; c < n_colors; ++c) desc[c] = asc[c] = c;
+        auto sz = [&](int32_t c) { return (int32_t)members[c].size(); };
+        std::stable_sort(desc.begin(), desc.end(), [&](int32_t x, int32_t y) { return sz(x) > sz(y); });
+        std::stable_sort(asc.begin(), asc.end(), [&](int32_t x, int32_t y) { return sz(x) < sz(y); });
+        int32_t mv = -1, to = -1;
+        for (int32_t a : desc) {
+            for (int32_t v : members[a]) {
+                for (int32_t b : asc) {
+                    if (sz(b) + 1 >= sz(a)) break;
+                    if (nbc[v][b] == 0) {
+                        mv = v;
+                        to = b;
+                        break;
+                    }
+                }
+                if (mv >= 0) break;
+            }
+            if (mv >= 0) break;
+        }
+        if (mv < 0) return;
+        const int32_t from = color[mv];
+        members[from].erase(mv);
+        members[to].insert(mv);
+        color[mv] = to;
+        for (int32_t w : nb[mv]) {
+            nbc[w][from]--;
+            nbc[w][to]++;
+        }
+    }
+}
+
 int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int32_t *card,
-                  Compiled &g, std::string &err, int64_t table_limit, int64_t lds_limit, bool packed) {
+                  Compiled &g, std::string &err, int64_t table_limit, int64_t lds_limit, bool packed,
+                  bool balance) {
     if (n <= 0) return fail(err, SAME_EINVAL, "n_nodes must be positive");
     if (!pptr || !card) return fail(err, SAME_EINVAL, "parent_ptr and card must be non-null");
     if (pptr[0] != 0) return fail(err, SAME_EGRAPH, "parent_ptr[0] must be 0");
@@ -138,6 +190,7 @@ int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int
         g.color[v] = c;
         g.n_colors = std::max(g.n_colors, c + 1);
     }
+    if (balance) balance_colours(nb, g.n_colors, g.color);
     g.groups.assign(g.n_colors, {});
     for (int32_t i = 0; i < n; ++i) g.groups[g.color[i]].push_back(i);
 

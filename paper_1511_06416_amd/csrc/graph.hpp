@@ -171,8 +171,9 @@ struct Compiled {
 // lds_limit: LDS staging budget per block in bytes (class 0): the largest
 // record staged whole, and the most a larger record stages of its groups.
 // packed: false sends every product-mode node to the wide class.
+// balance: false keeps the first-fit colouring (no balancing moves).
 int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int32_t *card,
                   Compiled &out, std::string &err, int64_t table_limit = kDefaultTableLimit,
-                  int64_t lds_limit = kDefaultLdsBytes, bool packed = true);
+                  int64_t lds_limit = kDefaultLdsBytes, bool packed = true, bool balance = true);
 
 }  // namespace same

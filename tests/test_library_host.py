@@ -54,6 +54,30 @@ def test_layout_and_colouring_match_oracle(cfg):
     ctx.close()
 
 
+@pytest.mark.parametrize("cfg", sorted(CONFIGS))
+def test_first_fit_colouring_option_matches_oracle(cfg):
+    # the option that skips the balancing moves gives the oracle's first-fit
+    # colouring; the default gives its balanced one
+    net = make_network(cfg)
+    pptr, pidx, card = net.csr()
+    ff = same.same_create_ex(pptr, pidx, card, 1.0, first_fit_colours=True)
+    assert np.array_equal(ff.color, oracle.graph(net.parents, net.card, balance=False)["color"])
+    assert np.array_equal(_ctx(net).color, oracle.graph(net.parents, net.card)["color"])
+    ff.close()
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_random_graphs_balanced_colours_match_oracle(seed):
+    rng = np.random.default_rng(1000 + seed)
+    parents, card = brute.random_net(rng, 200, 4, 2, 6)
+    pptr = np.cumsum([0] + [len(p) for p in parents]).astype(np.int32)
+    pidx = np.array([p for ps in parents for p in ps], dtype=np.int32)
+    for ffc in (False, True):
+        ctx = same.same_create_ex(pptr, pidx, card, 1.0, first_fit_colours=ffc)
+        assert np.array_equal(ctx.color, oracle.graph(parents, card, balance=not ffc)["color"])
+        ctx.close()
+
+
 def test_student_layout():
     ctx = _ctx(koller())
     assert ctx.cpt_total == 26 and ctx.n_rows == 11 and ctx.n_colors == 3
