@@ -379,6 +379,7 @@ struct Work {
 constexpr uint32_t kXcds = 8;
 constexpr int kSweepQuadsPerLane = 1;  // column quads per lane in one sweep block
 constexpr int kMinSweepBlocks = 4096;  // replicas are split below this many blocks
+constexpr int64_t kMinSweepQuads = 64;  // narrowest column chunk of a fast sweep block (quads)
 constexpr int kCountQuadsPerLane = 4;  // adjacent column quads per lane in one count block
 
 __device__ __forceinline__ void decode_block(uint32_t b, uint32_t count, uint32_t &local,
@@ -1595,10 +1596,17 @@ hipError_t launch_sweep(SweepParams P, int32_t begin, int32_t count, int32_t kla
     // tables that the resident blocks gather from in L2 (measured faster).
     const int64_t quads = (P.n_cols + 3) / 4;
     P.quads_per_block = (int64_t)dev::kSweepBlock * dev::kSweepQuadsPerLane;
-    const int64_t chunks = (quads + P.quads_per_block - 1) / P.quads_per_block;
     // the fast kernel draws replicas in quads (one Philox block each), so a
     // block's replica range is whole quads except at the end
     const int64_t m_quads = (P.m + 3) / 4;
+    // small launches (few nodes or columns) take narrower column chunks, down
+    // to 256 columns, so that even with one replica quad per block they fill
+    // the device with blocks
+    if (klass <= 1)
+        while (P.quads_per_block > dev::kMinSweepQuads &&
+               count * ((quads + P.quads_per_block - 1) / P.quads_per_block) * m_quads < dev::kMinSweepBlocks)
+            P.quads_per_block /= 2;
+    const int64_t chunks = (quads + P.quads_per_block - 1) / P.quads_per_block;
     int64_t rsplit = klass == 0 ? (dev::kMinSweepBlocks + count * chunks - 1) / (count * chunks) : m_quads;
     if (klass >= 2) rsplit = P.m;
     if (rsplit > (klass >= 2 ? P.m : m_quads)) rsplit = klass >= 2 ? P.m : m_quads;
