@@ -1163,7 +1163,8 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
                                                       const int32_t *__restrict__ cdesc_off,
                                                       const int32_t *__restrict__ cwork,
                                                       int32_t count, int64_t n_slabs,
-                                                      int64_t cols_per_block,
+                                                      int64_t cols_per_block, int32_t rsplit,
+                                                      int32_t reps_per_block,
                                                       const ST *__restrict__ states, int32_t m,
                                                       int64_t col0, int64_t n_cols, int64_t ld,
                                                       int32_t *__restrict__ counts) {
@@ -1184,7 +1185,12 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
     for (int b = threadIdx.x; b < lds_words; b += kBlock) hist[b] = 0;
     __syncthreads();
     const int copy = threadIdx.x & (kCopies - 1);
-    // absolute columns of the row: [c0, c1) inside [col0, col0 + n_cols)
+    // a slab is a column run and a replica range [rb, re); absolute columns
+    // of the row: [c0, c1) inside [col0, col0 + n_cols)
+    const int rpart = (int)(slab % rsplit);
+    slab /= rsplit;
+    const int rb = rpart * reps_per_block;
+    const int re = rb + reps_per_block < m ? rb + reps_per_block : m;
     const int64_t c0 = col0 + slab * cols_per_block;
     const int64_t c1 = c0 + cols_per_block < col0 + n_cols ? c0 + cols_per_block : col0 + n_cols;
     const int64_t vstride = (int64_t)m * ld;
@@ -1207,7 +1213,7 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
         const bool whole = col + 4 * NQ <= ld;
         if (!packed) {
             // 32-bit indices (more than 2^16 bins): one replica at a time
-            for (int r = 0; r < m; ++r) {
+            for (int r = rb; r < re; ++r) {
                 const uint32_t boff = (uint32_t)(r * ld + col) * (uint32_t)sizeof(ST);
                 S own;
                 own.template load<WIDE>(states, node, vstride, boff, whole);
@@ -1233,8 +1239,8 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
             }
             continue;
         }
-        for (int r0 = 0; r0 < m; r0 += kCountReps) {
-            const int nr = m - r0 < kCountReps ? m - r0 : kCountReps;
+        for (int r0 = rb; r0 < re; r0 += kCountReps) {
+            const int nr = re - r0 < kCountReps ? re - r0 : kCountReps;
             uint32_t boff[kCountReps];
             S own[kCountReps];
             // every slot loads (a fixed count keeps all loads in flight at
@@ -1654,14 +1660,24 @@ hipError_t launch_counts(const DeviceTables &t, const void *states, int32_t stat
     // one node x kCountQuadsPerLane quads per lane x all replicas per block,
     // XCD-swizzled like the sweep
     const int64_t cols_per_block = 4 * dev::kBlock * dev::kCountQuadsPerLane;
-    const int64_t n_slabs = (n_cols + cols_per_block - 1) / cols_per_block;
+    const int64_t col_slabs = (n_cols + cols_per_block - 1) / cols_per_block;
+    // small launches split the replicas (in runs of kCountReps) over blocks
+    // until there are kMinSweepBlocks blocks, so that they fill the device
+    const int64_t rep_runs = (m + dev::kCountReps - 1) / dev::kCountReps;
+    int64_t rparts = (dev::kMinSweepBlocks + (int64_t)n * col_slabs - 1) / ((int64_t)n * col_slabs);
+    if (rparts > rep_runs) rparts = rep_runs;
+    if (rparts < 1) rparts = 1;
+    const int32_t reps_per_block = (int32_t)(dev::kCountReps * ((rep_runs + rparts - 1) / rparts));
+    const int32_t rsplit = (int32_t)((m + reps_per_block - 1) / reps_per_block);
+    const int64_t n_slabs = col_slabs * rsplit;
     const int64_t rounds = (n_slabs + dev::kXcds - 1) / dev::kXcds;
     const int64_t blocks = rounds * dev::kXcds * n;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
     const dim3 grid((unsigned)blocks);
 #define SAME_LAUNCH_COUNTS(ST, WIDE)                                                                    \
     hipLaunchKernelGGL((dev::count_kernel<ST, WIDE>), grid, dim3(dev::kBlock), 0, stream, t.cdesc, t.cdesc_off, \
-                       t.cwork, n, n_slabs, cols_per_block, (const ST *)states, m, col0, n_cols, ld, counts)
+                       t.cwork, n, n_slabs, cols_per_block, rsplit, reps_per_block, (const ST *)states, m, col0, \
+                       n_cols, ld, counts)
     // rows of at least 4 * kCountQuadsPerLane columns take the wide loads
     if (state_bytes == 1) {
         if (ld >= 4 * dev::kCountQuadsPerLane) SAME_LAUNCH_COUNTS(int8_t, true);
