@@ -647,17 +647,26 @@ def m_study_run(dev, stream):
     the student network (identifiable: every node is observed half the time)
     and on the two-layer network (its concepts are never observed, so their
     states may swap labels and KL_avg against the generating CPTs need not
-    fall)."""
-    return {"student-100k": m_study_cfg(2, dev, stream), "concepts30-items300-4k": m_study_cfg(4, dev, stream)}
+    fall; there the held-out AUC, which is label-invariant, tracks the
+    sampler)."""
+    return {"student-100k": m_study_cfg(2, dev, stream),
+            "concepts30-items300-4k": m_study_cfg(4, dev, stream, heldout=0.2)}
 
 
-def m_study_cfg(cfg, dev, stream, steps=200, checkpoints=(10, 25, 50, 100, 150, 200)):
+def m_study_cfg(cfg, dev, stream, steps=200, checkpoints=(10, 25, 50, 100, 150, 200), heldout=None,
+                pred_sweeps=20):
     """KL_avg (Sec. 5.1) of the sampled CPTs against the generator's true CPTs
     as a function of device time on workload cfg (Secs. 5.1 and 6 plot KL_avg
     against passes and time for m = 1, 2, 5, 20), for fixed m and for an
     annealed run (Sec. 3: m raised during sampling,
     here 1 -> 2 -> 5 -> 20 at equal step intervals with same_grow_replicas and
-    a recount).  Each run takes `steps` SAME steps from the same start."""
+    a recount).  Each run takes `steps` SAME steps from the same start.
+    With heldout (a fraction), that fraction of the known entries is held out
+    of training (workloads.holdout), and at every checkpoint a prediction pass
+    (Sec. 6: pred_sweeps frozen-CPT sweeps on a copy of the chains) scores the
+    held-out entries; their AUC does not depend on how the sampler labels
+    states that are never observed.  The prediction passes are not counted
+    in the device time."""
     import numpy as np
     import torch
 
@@ -665,6 +674,7 @@ def m_study_cfg(cfg, dev, stream, steps=200, checkpoints=(10, 25, 50, 100, 150, 
     from paper_1511_06416_amd import evaluate
     from workloads import make_workload
 
+    from workloads import holdout
     base = make_workload(cfg, m=1, device=dev)
     net = base.net
     pptr, pidx, card = net.csr()
@@ -672,6 +682,20 @@ def m_study_cfg(cfg, dev, stream, steps=200, checkpoints=(10, 25, 50, 100, 150, 
     ws = ctx.new_workspace(dev)
     off = ctx.cpt_off
     ld, nc = base.ld, base.n_cols
+    obs = base.obs[0]
+    target_np = tg = None
+    if heldout:
+        obs_train, target_np = holdout(base, 0, heldout)
+        obs = torch.from_numpy(obs_train).to(dev)
+        tg = torch.from_numpy(target_np).to(dev)
+
+    def predict_auc(st, m, cpts):
+        sc = st.clone()
+        hits = torch.zeros((net.n, ld), dtype=torch.int32, device=dev)
+        same.same_predict(ctx, sc, obs, cpts, tg, m, nc, ld, 0, base.seed, 1 << 20, pred_sweeps, hits, ws)
+        torch.cuda.synchronize()
+        scores, labels = evaluate.binary_scores(hits.cpu().numpy(), target_np, pred_sweeps * m)
+        return evaluate.auc(scores, labels)
 
     def run(schedule):
         m = schedule(0)
@@ -679,7 +703,7 @@ def m_study_cfg(cfg, dev, stream, steps=200, checkpoints=(10, 25, 50, 100, 150, 
         cpts = torch.from_numpy(base.init_theta).to(dev)
         mb = torch.zeros(ctx.cpt_total, dtype=torch.int32, device=dev)
         tot = torch.zeros(ctx.cpt_total, dtype=torch.int32, device=dev)
-        same.same_init_latent(ctx, st, base.obs[0], m, nc, ld, 0, base.seed + 3)
+        same.same_init_latent(ctx, st, obs, m, nc, ld, 0, base.seed + 3)
         same.same_counts(ctx, st, m, nc, ld, mb, tot, ws)
         out, t_ms = [], 0.0
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -693,13 +717,16 @@ def m_study_cfg(cfg, dev, stream, steps=200, checkpoints=(10, 25, 50, 100, 150, 
                 mb.zero_()
                 tot.zero_()
                 same.same_counts(ctx, st, m, nc, ld, mb, tot, ws)
-            same.same_step(ctx, st, base.obs[0], cpts, m, nc, ld, 0, base.seed, s, mb, tot, s, ws)
+            same.same_step(ctx, st, obs, cpts, m, nc, ld, 0, base.seed, s, mb, tot, s, ws)
             e1.record(stream)
             e1.synchronize()
             t_ms += e0.elapsed_time(e1)
             if s + 1 in checkpoints:
                 kl = evaluate.kl_avg(base.true_theta, cpts.cpu().numpy(), off, net.card)
-                out.append({"step": s + 1, "device_ms": round(t_ms, 2), "m": m, "kl_avg": round(kl, 5)})
+                rec = {"step": s + 1, "device_ms": round(t_ms, 2), "m": m, "kl_avg": round(kl, 5)}
+                if heldout:
+                    rec["heldout_auc"] = round(predict_auc(st, m, cpts), 5)
+                out.append(rec)
         return out
 
     res = {}
@@ -707,8 +734,12 @@ def m_study_cfg(cfg, dev, stream, steps=200, checkpoints=(10, 25, 50, 100, 150, 
         res["m=%d" % m] = run(lambda s, m=m: m)
     res["annealed 1-2-5-20"] = run(lambda s: (1, 2, 5, 20)[min(3, s * 4 // steps)])
     ctx.close()
-    return {"workload": "%s, %d columns, %.0f%% hidden; KL_avg against the generating CPTs" % (
-        base.name, nc, 100 * base.hidden), "runs": res}
+    what = "KL_avg against the generating CPTs"
+    if heldout:
+        what += ("; AUC of %d%% of the known entries held out, from %d frozen-CPT sweeps per checkpoint"
+                 % (round(100 * heldout), pred_sweeps))
+    return {"workload": "%s, %d columns, %.0f%% hidden; %s" % (base.name, nc, 100 * base.hidden, what),
+            "runs": res}
 
 
 def stream_timing(w, ctx, cpts, ws, dev, steps):
