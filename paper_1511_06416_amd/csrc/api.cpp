@@ -23,6 +23,7 @@ int set_error(int code, const std::string &msg) {
 }
 
 constexpr size_t kAlign = 256;
+
 inline size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
 }  // namespace
@@ -310,6 +311,7 @@ int sweep_tile(same_ctx *ctx, const same::SweepParams &P0, int64_t t0, int64_t n
     if (rc) return rc;
     const int32_t L = same::kLaunchClasses;
     for (int32_t c = 0; c < g.n_colors; ++c) {
+        P.reverse = c & 1;
         // the nodes of one colour are independent: the global-table launch
         // (bound by the texture addresser) runs beside the LDS-bound one
         const int32_t b1 = g.launch[c * (L + 1) + 1], e1 = g.launch[c * (L + 1) + 2];

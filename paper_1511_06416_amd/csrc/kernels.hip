@@ -401,6 +401,10 @@ __device__ __forceinline__ Work block_work(const SweepParams &P) {
         w.r0 = w.r1 = 0;
         return w;
     }
+    // consecutive colour launches walk the columns in opposite directions, so
+    // that a launch starts on the columns the previous one touched last (still
+    // in the memory-side cache)
+    if (P.reverse) slab = P.n_slabs - 1 - slab;
     const int64_t chunk = slab / P.rsplit;
     const int rpart = (int)(slab % P.rsplit);
     const int64_t nquads = (P.n_cols + 3) >> 2;

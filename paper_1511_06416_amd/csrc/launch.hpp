@@ -54,6 +54,7 @@ struct SweepParams {
     int32_t rsplit;
     int64_t n_slabs;
     int64_t win_begin, win;        // debug window (win == 0: none)
+    int32_t reverse;               // 1: slabs in descending order (see block_work)
     float *probs;
     int32_t max_card;
 };
