@@ -470,14 +470,14 @@ def counters_summary(paths, cfg):
                                          " | ".join(vals)))
     sweep = [k for k in kernels if re.search(r"sweep_fast_kernel<[^,]+, false, true>", k)]
     # the 1 GiB device copy: the non-library dispatch whose WRITE_SIZE is 1 GiB
-    # within 5%; its FETCH_SIZE is the same kernel and grid in the FETCH_SIZE run
-    copy = None
+    # within 5% and that also reads (the fills that create the buffers read
+    # nothing); its FETCH_SIZE is the same kernel and grid in the FETCH_SIZE run
+    copy = fetch_copy = None
     for (k, c, grid), v in per_dispatch.items():
         if c == "WRITE_SIZE" and "same::" not in k and abs(v * 1024 - COPY_BYTES) < 0.05 * COPY_BYTES:
-            copy = (k, grid, v)
-    fetch_copy = None
-    if copy is not None:
-        fetch_copy = per_dispatch.get((copy[0], "FETCH_SIZE", copy[1]))
+            f = per_dispatch.get((k, "FETCH_SIZE", grid))
+            if f and f * 1024 > 0.25 * COPY_BYTES:
+                copy, fetch_copy = (k, grid, v), f
     if copy is None or not fetch_copy or not sweep:
         print("no copy calibration, FETCH_SIZE run or sweep kernel in these files")
         return
