@@ -311,6 +311,41 @@ int same_stream_pass(same_ctx *ctx, void *host_states, const uint8_t *host_obs, 
                      void *workspace, void *stream);
 
 /*
+ * Out-of-core passes with compact host state (Sec. 4: the data are typically
+ * sparse and only model-sized state need live on the device; Sec. 6: the
+ * GPU's memory, not the data, limits the problem).  The known data stay on
+ * the device -- obs_dev [n][ld_dev] (1 = observed) and data_dev [n][ld_dev]
+ * (the observed values, state type; latent entries ignored) for all n_cols
+ * columns -- and the host keeps only the m replicas' latent states,
+ * compacted: for minibatch b (columns [b*nb, min((b+1)*nb, n_cols))) and
+ * node i with L latent columns in it, replica r's states at those columns in
+ * ascending order are lat_host[lat_off[b*n + i] + r*L + k], k < L.  Per
+ * minibatch only the compact block crosses PCIe each way (the dense
+ * same_stream_pass moves every state and the obs bytes).
+ *
+ * same_stream_compact_layout fills lat_off[M*n + 1] (host) from obs_dev (a
+ * device pass over the obs array, synchronous on `stream`) and the bytes
+ * *slot_bytes of device memory the passes need (two dense minibatch slots,
+ * two staging buffers of the largest compact block, offsets and scratch).
+ * same_stream_pass_compact then runs one pass exactly as same_stream_pass --
+ * per minibatch: upload of the compact block, expansion into the dense slot,
+ * same_sweep (col_offset b*nb, sweep_id pass_id), same_counts into
+ * mb_counts[b] and totals, same_sample_cpts (update_id pass_id*M + b),
+ * compaction and download -- with the same results; SAME_STREAM_COUNTS_ONLY
+ * uploads, expands and counts (the pre-pass).  lat_host should be pinned
+ * memory for the copies to overlap the compute; nb a multiple of 4, ld_dev a
+ * multiple of 4 with n_cols <= ld_dev, obs_dev 4-byte and data_dev 4-element
+ * aligned, slots and workspace 256-byte aligned.  Errors as same_stream_pass.
+ */
+int same_stream_compact_layout(same_ctx *ctx, const uint8_t *obs_dev, int64_t ld_dev, int64_t n_cols, int64_t nb,
+                               int32_t m, int64_t *lat_off, size_t *slot_bytes, void *workspace, void *stream);
+
+int same_stream_pass_compact(same_ctx *ctx, void *lat_host, const int64_t *lat_off, const uint8_t *obs_dev,
+                             const void *data_dev, int64_t ld_dev, int64_t n_cols, int64_t nb, int32_t m,
+                             float *cpts, int32_t *mb_counts, int32_t *totals, uint64_t seed, uint32_t pass_id,
+                             int32_t flags, void *slots, void *workspace, void *stream);
+
+/*
  * Exponential moving sum of the counts (Sec. 4: for datasets too large to keep
  * every minibatch's counts, the counts are maintained as an exponential
  * moving sum, so memory scales with the model, not the data).

@@ -21,7 +21,8 @@ __all__ = [
     "same_step", "same_sweep_plan", "same_stream_slots_size", "same_stream_pass", "SAME_STREAM_COUNTS_ONLY",
     "same_kernel_timing", "same_kernel_times", "same_expand_observed", "same_init_latent",
     "same_accumulate_hits", "same_predict", "same_counts_ema", "same_sample_cpts_ema", "same_stream_pass_ema",
-    "same_grow_replicas", "same_debug_thresholds", "same_counts_noalloc",
+    "same_grow_replicas", "same_debug_thresholds", "same_counts_noalloc", "same_stream_compact_layout",
+    "same_stream_pass_compact",
     "library_path", "load_library",
 ]
 
@@ -99,6 +100,8 @@ def load_library():
                                            P]
         L.same_predict.argtypes = [P, P, P, P, P, I32, I64, I64, I64, U64, U32, I32, P, P, P]
         L.same_counts_noalloc.argtypes = [P, P, I32, I64, I64, P, P, P]
+        L.same_stream_compact_layout.argtypes = [P, P, I64, I64, I64, I32, P, C.POINTER(C.c_size_t), P, P]
+        L.same_stream_pass_compact.argtypes = [P, P, P, P, P, I64, I64, I64, I32, P, P, P, U64, U32, I32, P, P, P]
         L.same_debug_thresholds.argtypes = [P, P, P, P, C.POINTER(C.c_int64), P, P, P]
         L.same_last_error.argtypes = []
         L.same_last_error.restype = C.c_char_p
@@ -108,7 +111,7 @@ def load_library():
                   "same_kernel_times", "same_expand_observed", "same_init_latent",
                   "same_accumulate_hits", "same_predict", "same_counts_ema", "same_sample_cpts_ema",
                   "same_stream_pass_ema", "same_grow_replicas", "same_debug_thresholds",
-                  "same_counts_noalloc"):
+                  "same_counts_noalloc", "same_stream_compact_layout", "same_stream_pass_compact"):
             getattr(L, f).restype = C.c_int
         _lib = L
         return L
@@ -367,3 +370,26 @@ def same_debug_thresholds(ctx, cpts=None, workspace=None, stream=None):
         _check(L.same_debug_thresholds(ctx.handle, _ptr(cpts), off.ctypes.data, kt.ctypes.data, C.byref(words),
                                        _ptr(out), _ptr(workspace), _stream(stream)))
     return off, kt, out
+
+
+def same_stream_compact_layout(ctx, obs_dev, ld_dev, n_cols, nb, m, workspace, stream=None):
+    """(lat_off int64 numpy [M*n + 1], slot bytes) of the compact host layout."""
+    M = (int(n_cols) + int(nb) - 1) // int(nb)
+    off = np.zeros(M * ctx.n_nodes + 1, dtype=np.int64)
+    sz = C.c_size_t()
+    _check(load_library().same_stream_compact_layout(ctx.handle, _ptr(obs_dev), int(ld_dev), int(n_cols), int(nb),
+                                                     int(m), off.ctypes.data, C.byref(sz), _ptr(workspace),
+                                                     _stream(stream)))
+    return off, int(sz.value)
+
+
+def same_stream_pass_compact(ctx, lat_host, lat_off, obs_dev, data_dev, ld_dev, n_cols, nb, m, cpts, mb_counts, totals,
+                             seed, pass_id, flags, slots, workspace, stream=None):
+    """lat_host: pinned host tensor of the compact latent states; lat_off: the
+    layout's host offsets (numpy int64); obs_dev, data_dev and the rest on the
+    device."""
+    off = np.ascontiguousarray(lat_off, dtype=np.int64)
+    _check(load_library().same_stream_pass_compact(ctx.handle, _ptr(lat_host), off.ctypes.data, _ptr(obs_dev),
+                                                   _ptr(data_dev), int(ld_dev), int(n_cols), int(nb), int(m),
+                                                   _ptr(cpts), _ptr(mb_counts), _ptr(totals), int(seed), int(pass_id),
+                                                   int(flags), _ptr(slots), _ptr(workspace), _stream(stream)))

@@ -23,6 +23,7 @@ int set_error(int code, const std::string &msg) {
 }
 
 constexpr size_t kAlign = 256;
+constexpr int64_t kCompactChunkCols = 1024;  // columns per block of the compact-state kernels
 
 inline size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
@@ -998,3 +999,163 @@ extern "C" int same_kernel_times(same_ctx *ctx, same_kernel_times_t *out) {
     out->phases = ctx->timing.phases;
     return rc;
 }
+
+namespace {
+
+// Device layout of the compact-pass slots: two dense slots (states + obs),
+// two staging buffers of the largest compact minibatch, the chunk prefix
+// sums of the current minibatch and the per-(minibatch, node) offsets.
+struct CompactGeom {
+    SlotGeom dense;
+    size_t staging = 0, prefix = 0, offsets = 0, bytes = 0;
+    int64_t chunks = 0;
+};
+
+CompactGeom compact_geom(const same_ctx *ctx, int32_t m, int64_t nb, int64_t n_cols, int64_t max_block) {
+    CompactGeom c;
+    c.dense = slot_geom(ctx, m, nb);
+    const int64_t M = (n_cols + nb - 1) / nb;
+    c.chunks = (nb + kCompactChunkCols - 1) / kCompactChunkCols;
+    c.staging = align_up((size_t)max_block * ctx->g.state_bytes + 8);
+    c.prefix = align_up((size_t)ctx->g.n * (size_t)c.chunks * sizeof(int32_t));
+    c.offsets = align_up((size_t)(M * ctx->g.n + 1) * sizeof(int64_t));
+    c.bytes = 2 * c.dense.bytes + 2 * c.staging + c.prefix + c.offsets;
+    return c;
+}
+
+int check_compact_args(same_ctx *ctx, const uint8_t *obs_dev, int64_t ld_dev, int64_t n_cols, int64_t nb,
+                       int32_t m) {
+    if (!ctx || !obs_dev) return set_error(SAME_EINVAL, "ctx and obs_dev must be non-null");
+    if (m < 1 || m > 65535) return set_error(SAME_EINVAL, "m must be in [1, 65535]");
+    if (nb < 4 || nb % 4 != 0) return set_error(SAME_EALIGN, "nb must be a positive multiple of 4");
+    if (n_cols < 0 || ld_dev < n_cols || ld_dev % 4 != 0)
+        return set_error(SAME_EINVAL, "need 0 <= n_cols <= ld_dev, ld_dev a multiple of 4");
+    if (!aligned(obs_dev, 4)) return set_error(SAME_EALIGN, "obs_dev must be 4-byte aligned");
+    return SAME_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int same_stream_compact_layout(same_ctx *ctx, const uint8_t *obs_dev, int64_t ld_dev, int64_t n_cols, int64_t nb,
+                               int32_t m, int64_t *lat_off, size_t *slot_bytes, void *workspace, void *stream) {
+    int rc = check_compact_args(ctx, obs_dev, ld_dev, n_cols, nb, m);
+    if (rc) return rc;
+    if (!lat_off || !slot_bytes || !workspace) return set_error(SAME_EINVAL, "null pointer argument");
+    if (!aligned(workspace, kAlign)) return set_error(SAME_EALIGN, "workspace must be 256-byte aligned");
+    const int32_t n = ctx->g.n;
+    const int64_t M = n_cols > 0 ? (n_cols + nb - 1) / nb : 0;
+    hipStream_t s = (hipStream_t)stream;
+    // per node counts in the workspace's count scratch (cpt_total >= 2n entries)
+    int32_t *counts = (int32_t *)((char *)workspace + ctx->ws_counts);
+    std::vector<int32_t> host((size_t)n);
+    int64_t run = 0, max_block = 0;
+    for (int64_t b = 0; b < M; ++b) {
+        const int64_t c0 = b * nb, cols = n_cols - c0 < nb ? n_cols - c0 : nb;
+        rc = check_hip(same::launch_compact_node_counts(obs_dev, ld_dev, c0, cols, n, counts, s), "count launch");
+        if (!rc) rc = check_hip(hipMemcpyAsync(host.data(), counts, (size_t)n * sizeof(int32_t),
+                                               hipMemcpyDeviceToHost, s), "count copy");
+        if (!rc) rc = check_hip(hipStreamSynchronize(s), "hipStreamSynchronize");
+        if (rc) return rc;
+        const int64_t start = run;
+        for (int32_t i = 0; i < n; ++i) {
+            lat_off[b * n + i] = run;
+            run += (int64_t)m * host[i];
+        }
+        max_block = std::max(max_block, run - start);
+    }
+    lat_off[M * n] = run;
+    *slot_bytes = compact_geom(ctx, m, nb, n_cols, max_block).bytes;
+    return SAME_OK;
+}
+
+int same_stream_pass_compact(same_ctx *ctx, void *lat_host, const int64_t *lat_off, const uint8_t *obs_dev,
+                             const void *data_dev, int64_t ld_dev, int64_t n_cols, int64_t nb, int32_t m,
+                             float *cpts, int32_t *mb_counts, int32_t *totals, uint64_t seed, uint32_t pass_id,
+                             int32_t flags, void *slots, void *workspace, void *stream) {
+    int rc = check_compact_args(ctx, obs_dev, ld_dev, n_cols, nb, m);
+    if (rc) return rc;
+    if (!lat_host || !lat_off || !data_dev || !cpts || !mb_counts || !totals || !slots || !workspace)
+        return set_error(SAME_EINVAL, "null pointer argument");
+    if (flags & ~SAME_STREAM_COUNTS_ONLY) return set_error(SAME_EINVAL, "unknown flags");
+    if (!aligned(slots, kAlign) || !aligned(workspace, kAlign))
+        return set_error(SAME_EALIGN, "slots and workspace must be 256-byte aligned");
+    if (!aligned(data_dev, 4 * (size_t)ctx->g.state_bytes))
+        return set_error(SAME_EALIGN, "data_dev must be aligned to 4 state elements");
+    if (n_cols == 0) return SAME_OK;
+    const int32_t n = ctx->g.n;
+    const int64_t M = (n_cols + nb - 1) / nb;
+    if ((double)M * (double)pass_id + M > 4294967295.0)
+        return set_error(SAME_ESIZE, "pass_id * minibatches exceeds the update-id range");
+    int64_t max_block = 0;
+    for (int64_t b = 0; b < M; ++b) max_block = std::max(max_block, lat_off[(b + 1) * n] - lat_off[b * n]);
+    const CompactGeom cg = compact_geom(ctx, m, nb, n_cols, max_block);
+    StreamRes *sr = nullptr;
+    rc = stream_res_for_current_device(ctx, &sr);
+    if (rc) return rc;
+    hipStream_t cs = (hipStream_t)stream;
+    const size_t sb = (size_t)ctx->g.state_bytes;
+    const int64_t total = ctx->g.off[n];
+    const bool counts_only = (flags & SAME_STREAM_COUNTS_ONLY) != 0;
+    char *base = (char *)slots;
+    char *staging[2] = {base + 2 * cg.dense.bytes, base + 2 * cg.dense.bytes + cg.staging};
+    int32_t *prefix = (int32_t *)(base + 2 * cg.dense.bytes + 2 * cg.staging);
+    int64_t *d_off = (int64_t *)((char *)prefix + cg.prefix);
+    // the offsets on the device (the kernels subtract each minibatch's first)
+    rc = check_hip(hipMemcpyAsync(d_off, lat_off, (size_t)(M * n + 1) * sizeof(int64_t), hipMemcpyHostToDevice, cs),
+                   "offset upload");
+    if (rc) return rc;
+    for (int64_t b = 0; b < M; ++b) {
+        const int sl = (int)(b & 1);
+        const int64_t c0 = b * nb, cols = n_cols - c0 < nb ? n_cols - c0 : nb;
+        char *slot = base + sl * cg.dense.bytes;
+        void *d_states = slot;
+        uint8_t *d_obs = (uint8_t *)(slot + cg.dense.states);
+        const int64_t blk0 = lat_off[b * n], blk = lat_off[(b + 1) * n] - blk0;
+        // upload the compact block (after the staging buffer's previous block left it)
+        if (sr->slot_used[sl] && (rc = check_hip(hipStreamWaitEvent(sr->up, sr->ev_down[sl], 0), "wait")))
+            return rc;
+        rc = check_hip(hipMemcpyAsync(staging[sl], (char *)lat_host + blk0 * sb, (size_t)blk * sb,
+                                      hipMemcpyHostToDevice, sr->up), "latent upload");
+        if (!rc) rc = check_hip(hipEventRecord(sr->ev_up[sl], sr->up), "event");
+        if (!rc) rc = check_hip(hipStreamWaitEvent(cs, sr->ev_up[sl], 0), "wait");
+        if (rc) return rc;
+        // chunk ranks, then the dense slot
+        rc = check_hip(same::launch_compact_counts(obs_dev, ld_dev, c0, cols, n, prefix, true, cs), "count launch");
+        if (!rc)
+            rc = check_hip(same::launch_expand_compact(obs_dev, data_dev, ld_dev, c0, cols, n, m, prefix,
+                                                       d_off + b * n, blk0, staging[sl], d_states, d_obs,
+                                                       cg.dense.ld, ctx->g.state_bytes, cs),
+                           "expand launch");
+        if (rc) return rc;
+        int32_t *mb = mb_counts + b * total;
+        if (counts_only) rc = same_counts(ctx, d_states, m, cols, cg.dense.ld, mb, totals, workspace, stream);
+        else
+            rc = do_step(ctx, d_states, d_obs, cpts, m, cols, cg.dense.ld, c0, seed, pass_id, mb, totals,
+                         (uint32_t)(pass_id * M + b), workspace, stream);
+        if (rc) return rc;
+        if (counts_only) {
+            rc = check_hip(hipEventRecord(sr->ev_down[sl], cs), "event");
+        } else {
+            rc = check_hip(same::launch_gather_compact(obs_dev, ld_dev, c0, cols, n, m, prefix, d_off + b * n,
+                                                       blk0, d_states, cg.dense.ld, staging[sl],
+                                                       ctx->g.state_bytes, cs),
+                           "gather launch");
+            if (!rc) rc = check_hip(hipEventRecord(sr->ev_comp[sl], cs), "event");
+            if (!rc) rc = check_hip(hipStreamWaitEvent(sr->down, sr->ev_comp[sl], 0), "wait");
+            if (!rc)
+                rc = check_hip(hipMemcpyAsync((char *)lat_host + blk0 * sb, staging[sl], (size_t)blk * sb,
+                                              hipMemcpyDeviceToHost, sr->down), "latent download");
+            if (!rc) rc = check_hip(hipEventRecord(sr->ev_down[sl], sr->down), "event");
+        }
+        if (rc) return rc;
+        sr->slot_used[sl] = true;
+    }
+    for (int sl = 0; sl < 2; ++sl)
+        if (sr->slot_used[sl] && (rc = check_hip(hipStreamWaitEvent(cs, sr->ev_down[sl], 0), "wait")))
+            return rc;
+    return SAME_OK;
+}
+
+}  // extern "C"

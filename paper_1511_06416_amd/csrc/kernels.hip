@@ -1504,6 +1504,158 @@ __global__ __launch_bounds__(kBlock) void hits_kernel(const ST *__restrict__ sta
     *h = cur;
 }
 
+// ------------------------------------------------------ compact host state
+//
+// Out-of-core passes that keep only the latent entries on the host (the
+// known data stay on the device): per minibatch, the latent states of node i
+// are stored compactly, replica r's at [node_off[i] + r * L_i, + L_i), in
+// ascending column order (L_i = the node's latent columns in the minibatch).
+// node_off holds the offsets of the whole host array; off0 is the first of
+// the minibatch, where the device buffer starts.  A block of these kernels
+// takes one node and one chunk of kCompactChunk columns; a lane reads the obs
+// word of its 4 columns.
+
+constexpr int kCompactChunk = 4 * kBlock;
+
+// Latent columns of each (node, chunk) of the minibatch [c0, c0 + cols).
+__global__ __launch_bounds__(kBlock) void compact_counts_kernel(const uint8_t *__restrict__ obs, int64_t obs_ld,
+                                                                int64_t c0, int64_t cols, int32_t chunks,
+                                                                int32_t *__restrict__ counts) {
+    __shared__ int32_t total;
+    const int node = (int)(blockIdx.x / chunks), chunk = (int)(blockIdx.x % chunks);
+    if (threadIdx.x == 0) total = 0;
+    __syncthreads();
+    const int64_t j = (int64_t)chunk * kCompactChunk + 4 * threadIdx.x;
+    int cnt = 0;
+    if (j < cols) {
+        const uint32_t ob = *reinterpret_cast<const uint32_t *>(obs + (int64_t)node * obs_ld + c0 + j);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) cnt += (((ob >> (8 * c)) & 0xffu) == 0 && j + c < cols) ? 1 : 0;
+    }
+    if (cnt) atomicAdd(&total, cnt);
+    __syncthreads();
+    if (threadIdx.x == 0) counts[blockIdx.x] = total;
+}
+
+// Latent columns of each node in the minibatch [c0, c0 + cols): one block per
+// node walks the columns.
+__global__ __launch_bounds__(kBlock) void compact_node_counts_kernel(const uint8_t *__restrict__ obs, int64_t obs_ld,
+                                                                     int64_t c0, int64_t cols,
+                                                                     int32_t *__restrict__ counts) {
+    __shared__ int32_t total;
+    const int node = blockIdx.x;
+    if (threadIdx.x == 0) total = 0;
+    __syncthreads();
+    int cnt = 0;
+    for (int64_t j = 4 * (int64_t)threadIdx.x; j < cols; j += kCompactChunk) {
+        const uint32_t ob = *reinterpret_cast<const uint32_t *>(obs + (int64_t)node * obs_ld + c0 + j);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) cnt += (((ob >> (8 * c)) & 0xffu) == 0 && j + c < cols) ? 1 : 0;
+    }
+    if (cnt) atomicAdd(&total, cnt);
+    __syncthreads();
+    if (threadIdx.x == 0) counts[node] = total;
+}
+
+// Per node, the counts of its chunks become their exclusive prefix sums.
+__global__ __launch_bounds__(kBlock) void compact_prefix_kernel(int32_t *__restrict__ counts, int32_t n,
+                                                                int32_t chunks) {
+    const int node = blockIdx.x * kBlock + threadIdx.x;
+    if (node >= n) return;
+    int32_t *c = counts + (int64_t)node * chunks, run = 0;
+    for (int k = 0; k < chunks; ++k) {
+        const int32_t v = c[k];
+        c[k] = run;
+        run += v;
+    }
+}
+
+// Rank, among the node's latent columns of the minibatch, of the first latent
+// column of each lane's quad (block-wide prefix sum over the lanes' obs words),
+// and the lane's latent mask.
+__device__ __forceinline__ int compact_rank(const uint8_t *__restrict__ obs, int64_t obs_ld, int64_t c0,
+                                            int64_t cols, int node, int chunk, const int32_t *__restrict__ prefix,
+                                            int32_t chunks, int32_t *wave_n, int &lat) {
+    const int64_t j = (int64_t)chunk * kCompactChunk + 4 * threadIdx.x;
+    lat = 0;
+    if (j < cols) {
+        const uint32_t ob = *reinterpret_cast<const uint32_t *>(obs + (int64_t)node * obs_ld + c0 + j);
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+            if (((ob >> (8 * c)) & 0xffu) == 0 && j + c < cols) lat |= 1 << c;
+    }
+    const int cnt = __builtin_popcount(lat);
+    const uint64_t b0 = __ballot(cnt & 1), b1 = __ballot(cnt & 2), b2 = __ballot(cnt & 4);
+    auto below = [](uint64_t b) {
+        return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(b >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)b, 0u));
+    };
+    const int pre = below(b0) + 2 * below(b1) + 4 * below(b2);
+    const int wave = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0)
+        wave_n[wave] = __builtin_popcountll(b0) + 2 * __builtin_popcountll(b1) + 4 * __builtin_popcountll(b2);
+    __syncthreads();
+    int base = prefix[(int64_t)node * chunks + chunk];
+#pragma unroll
+    for (int v = 0; v < kBlock / 64; ++v) base += v < wave ? wave_n[v] : 0;
+    return base + pre;
+}
+
+// Dense slot of a minibatch from the device-resident known data and the
+// compact latent states: every replica's row takes the known value at an
+// observed column and its compact latent state at a latent one; the slot's
+// obs rows are copied as well.  Columns [cols, slot_ld) are left untouched.
+template <typename ST>
+__global__ __launch_bounds__(kBlock) void expand_compact_kernel(
+    const uint8_t *__restrict__ obs, const ST *__restrict__ data, int64_t obs_ld, int64_t c0, int64_t cols,
+    int32_t m, int32_t chunks, const int32_t *__restrict__ prefix, const int64_t *__restrict__ node_off,
+    int64_t off0, const ST *__restrict__ lat_states, ST *__restrict__ states, uint8_t *__restrict__ obs_slot,
+    int64_t slot_ld) {
+    using Q = Quad<ST>;
+    __shared__ int32_t wave_n[kBlock / 64];
+    const int node = (int)(blockIdx.x / chunks), chunk = (int)(blockIdx.x % chunks);
+    int lat;
+    const int rank = compact_rank(obs, obs_ld, c0, cols, node, chunk, prefix, chunks, wave_n, lat);
+    const int64_t j = (int64_t)chunk * kCompactChunk + 4 * threadIdx.x;
+    if (j >= cols) return;
+    const int64_t L = (node_off[node + 1] - node_off[node]) / m;
+    const ST *lat_node = lat_states + (node_off[node] - off0);
+    *reinterpret_cast<uint32_t *>(obs_slot + (int64_t)node * slot_ld + j) =
+        *reinterpret_cast<const uint32_t *>(obs + (int64_t)node * obs_ld + c0 + j);
+    const typename Q::V known = Q::load(data + (int64_t)node * obs_ld + c0 + j);
+    for (int r = 0; r < m; ++r) {
+        typename Q::V v = known;
+        int k = rank;
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+            if ((lat >> c) & 1) v = Q::put(v, c, (int)lat_node[(int64_t)r * L + k++]);
+        Q::store(states + ((int64_t)node * m + r) * slot_ld + j, v);
+    }
+}
+
+// The inverse: the latent states of the dense slot back into compact form.
+template <typename ST>
+__global__ __launch_bounds__(kBlock) void gather_compact_kernel(
+    const uint8_t *__restrict__ obs, int64_t obs_ld, int64_t c0, int64_t cols, int32_t m, int32_t chunks,
+    const int32_t *__restrict__ prefix, const int64_t *__restrict__ node_off, int64_t off0,
+    const ST *__restrict__ states, int64_t slot_ld, ST *__restrict__ lat_states) {
+    using Q = Quad<ST>;
+    __shared__ int32_t wave_n[kBlock / 64];
+    const int node = (int)(blockIdx.x / chunks), chunk = (int)(blockIdx.x % chunks);
+    int lat;
+    const int rank = compact_rank(obs, obs_ld, c0, cols, node, chunk, prefix, chunks, wave_n, lat);
+    const int64_t j = (int64_t)chunk * kCompactChunk + 4 * threadIdx.x;
+    if (j >= cols || !lat) return;
+    const int64_t L = (node_off[node + 1] - node_off[node]) / m;
+    ST *lat_node = lat_states + (node_off[node] - off0);
+    for (int r = 0; r < m; ++r) {
+        const typename Q::V v = Q::load(states + ((int64_t)node * m + r) * slot_ld + j);
+        int k = rank;
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+            if ((lat >> c) & 1) lat_node[(int64_t)r * L + k++] = (ST)Q::get(v, c);
+    }
+}
+
 // ---------------------------------------------------------------- annealing
 
 // SAME annealing (Sec. 3: raising the replication factor during sampling):
@@ -1742,6 +1894,61 @@ hipError_t launch_hits(const void *states, const void *target, int32_t n, int32_
     else
         hipLaunchKernelGGL(dev::hits_kernel<int16_t>, dim3((unsigned)blocks), dim3(dev::kBlock), 0, stream,
                            (const int16_t *)states, (const int16_t *)target, n, m, n_cols, ld, hits);
+    return hipGetLastError();
+}
+
+hipError_t launch_compact_node_counts(const uint8_t *obs, int64_t obs_ld, int64_t c0, int64_t cols, int32_t n,
+                                      int32_t *counts, hipStream_t stream) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(dev::compact_node_counts_kernel, dim3((unsigned)n), dim3(dev::kBlock), 0, stream, obs, obs_ld,
+                       c0, cols, counts);
+    return hipGetLastError();
+}
+
+hipError_t launch_compact_counts(const uint8_t *obs, int64_t obs_ld, int64_t c0, int64_t cols, int32_t n,
+                                 int32_t *counts, bool prefix, hipStream_t stream) {
+    const int32_t chunks = (int32_t)((cols + dev::kCompactChunk - 1) / dev::kCompactChunk);
+    if (cols <= 0 || n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(dev::compact_counts_kernel, dim3((unsigned)((int64_t)n * chunks)), dim3(dev::kBlock), 0,
+                       stream, obs, obs_ld, c0, cols, chunks, counts);
+    if (prefix)
+        hipLaunchKernelGGL(dev::compact_prefix_kernel, dim3(blocks_for(n, dev::kBlock)), dim3(dev::kBlock), 0,
+                           stream, counts, n, chunks);
+    return hipGetLastError();
+}
+
+hipError_t launch_expand_compact(const uint8_t *obs, const void *data, int64_t obs_ld, int64_t c0, int64_t cols,
+                                 int32_t n, int32_t m, const int32_t *prefix, const int64_t *node_off, int64_t off0,
+                                 const void *lat_states, void *states, uint8_t *obs_slot, int64_t slot_ld,
+                                 int32_t state_bytes, hipStream_t stream) {
+    const int32_t chunks = (int32_t)((cols + dev::kCompactChunk - 1) / dev::kCompactChunk);
+    if (cols <= 0 || n <= 0) return hipSuccess;
+    const dim3 grid((unsigned)((int64_t)n * chunks));
+    if (state_bytes == 1)
+        hipLaunchKernelGGL(dev::expand_compact_kernel<int8_t>, grid, dim3(dev::kBlock), 0, stream, obs,
+                           (const int8_t *)data, obs_ld, c0, cols, m, chunks, prefix, node_off, off0,
+                           (const int8_t *)lat_states, (int8_t *)states, obs_slot, slot_ld);
+    else
+        hipLaunchKernelGGL(dev::expand_compact_kernel<int16_t>, grid, dim3(dev::kBlock), 0, stream, obs,
+                           (const int16_t *)data, obs_ld, c0, cols, m, chunks, prefix, node_off, off0,
+                           (const int16_t *)lat_states, (int16_t *)states, obs_slot, slot_ld);
+    return hipGetLastError();
+}
+
+hipError_t launch_gather_compact(const uint8_t *obs, int64_t obs_ld, int64_t c0, int64_t cols, int32_t n, int32_t m,
+                                 const int32_t *prefix, const int64_t *node_off, int64_t off0, const void *states,
+                                 int64_t slot_ld, void *lat_states, int32_t state_bytes, hipStream_t stream) {
+    const int32_t chunks = (int32_t)((cols + dev::kCompactChunk - 1) / dev::kCompactChunk);
+    if (cols <= 0 || n <= 0) return hipSuccess;
+    const dim3 grid((unsigned)((int64_t)n * chunks));
+    if (state_bytes == 1)
+        hipLaunchKernelGGL(dev::gather_compact_kernel<int8_t>, grid, dim3(dev::kBlock), 0, stream, obs, obs_ld, c0,
+                           cols, m, chunks, prefix, node_off, off0, (const int8_t *)states, slot_ld,
+                           (int8_t *)lat_states);
+    else
+        hipLaunchKernelGGL(dev::gather_compact_kernel<int16_t>, grid, dim3(dev::kBlock), 0, stream, obs, obs_ld,
+                           c0, cols, m, chunks, prefix, node_off, off0, (const int16_t *)states, slot_ld,
+                           (int16_t *)lat_states);
     return hipGetLastError();
 }
 

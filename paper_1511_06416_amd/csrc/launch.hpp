@@ -103,6 +103,25 @@ hipError_t launch_init_latent(const DeviceTables &t, int32_t n, int32_t m, int64
 hipError_t launch_hits(const void *states, const void *target, int32_t n, int32_t m, int64_t n_cols, int64_t ld,
                        int32_t state_bytes, int32_t *hits, hipStream_t stream);
 
+// Compact host state of the out-of-core passes: latent columns per (node,
+// chunk of 1024 columns) of the minibatch [c0, c0 + cols) of obs [n][obs_ld]
+// into counts [n][chunks] (with prefix, turned into per-node exclusive
+// prefix sums); the dense slot from the device-resident known data and the
+// compact latent states (node i's block at lat_states + node_off[i] - off0);
+// and the latent states back into compact form.
+hipError_t launch_compact_counts(const uint8_t *obs, int64_t obs_ld, int64_t c0, int64_t cols, int32_t n,
+                                 int32_t *counts, bool prefix, hipStream_t stream);
+// Latent columns of each node of the minibatch into counts [n].
+hipError_t launch_compact_node_counts(const uint8_t *obs, int64_t obs_ld, int64_t c0, int64_t cols, int32_t n,
+                                      int32_t *counts, hipStream_t stream);
+hipError_t launch_expand_compact(const uint8_t *obs, const void *data, int64_t obs_ld, int64_t c0, int64_t cols,
+                                 int32_t n, int32_t m, const int32_t *prefix, const int64_t *node_off, int64_t off0,
+                                 const void *lat_states, void *states, uint8_t *obs_slot, int64_t slot_ld,
+                                 int32_t state_bytes, hipStream_t stream);
+hipError_t launch_gather_compact(const uint8_t *obs, int64_t obs_ld, int64_t c0, int64_t cols, int32_t n, int32_t m,
+                                 const int32_t *prefix, const int64_t *node_off, int64_t off0, const void *states,
+                                 int64_t slot_ld, void *lat_states, int32_t state_bytes, hipStream_t stream);
+
 // SAME annealing: dst [n][m2] rows from src [n][m] rows (replica r mod m).
 hipError_t launch_grow(const void *src, int32_t m, void *dst, int32_t m2, int32_t n, int64_t row_bytes,
                        hipStream_t stream);

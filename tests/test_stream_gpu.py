@@ -140,3 +140,77 @@ def test_stream_follows_oracle_loop():
 
     _streamed(w, ctx, passes=4, on_pass=on_pass)
     assert state["checked"] >= 1 or state["diverged"]
+
+
+def _compact_case(w, ctx, passes):
+    """Compact-state passes: the known data on the device, the latent replica
+    states compacted on the host (built here with numpy from the dense
+    minibatches); returns the dense states expanded back from the compact host
+    array after the passes, and the counts, totals and CPTs."""
+    n, m = w.net.n, w.m
+    ld_dev = (w.n_cols + 3) // 4 * 4
+    obs = np.ones((n, ld_dev), dtype=np.uint8)
+    data = np.zeros((n, ld_dev), dtype=w.states[0].numpy().dtype)
+    for b in range(w.M):
+        c0, nc = b * w.nb, w.mb_cols(b)
+        obs[:, c0:c0 + nc] = w.obs[b].numpy()[:, :nc]
+        data[:, c0:c0 + nc] = w.states[b].numpy()[:, 0, :nc]
+    d_obs = torch.from_numpy(obs).cuda()
+    d_data = torch.from_numpy(data).cuda()
+    ws = ctx.new_workspace()
+    off, slot_bytes = same.same_stream_compact_layout(ctx, d_obs, ld_dev, w.n_cols, w.nb, m, ws)
+    # the compact host array: per (minibatch, node), replica-major latent states
+    host = np.zeros(int(off[-1]), dtype=data.dtype)
+    latcols = {}
+    for b in range(w.M):
+        c0, nc = b * w.nb, w.mb_cols(b)
+        st = w.states[b].numpy()
+        for i in range(n):
+            cols = np.nonzero(obs[i, c0:c0 + nc] == 0)[0]
+            latcols[b, i] = cols
+            L = len(cols)
+            assert off[b * n + i + 1] - off[b * n + i] == m * L
+            host[off[b * n + i]:off[b * n + i] + m * L] = st[i][:, cols].reshape(-1)
+    lat = torch.from_numpy(host).pin_memory() if host.size else torch.zeros(1, dtype=torch.int8).pin_memory()
+    slots = torch.empty(slot_bytes, dtype=torch.uint8, device="cuda")
+    cpts = torch.from_numpy(w.init_theta).cuda()
+    mb = torch.zeros((w.M, ctx.cpt_total), dtype=torch.int32, device="cuda")
+    tot = torch.zeros(ctx.cpt_total, dtype=torch.int32, device="cuda")
+    same.same_stream_pass_compact(ctx, lat, off, d_obs, d_data, ld_dev, w.n_cols, w.nb, m, cpts, mb, tot, w.seed,
+                                  0, same.SAME_STREAM_COUNTS_ONLY, slots, ws)
+    for s in range(passes):
+        same.same_stream_pass_compact(ctx, lat, off, d_obs, d_data, ld_dev, w.n_cols, w.nb, m, cpts, mb, tot,
+                                      w.seed, s, 0, slots, ws)
+    torch.cuda.synchronize()
+    out = lat.numpy()
+    dense = []
+    for b in range(w.M):
+        c0, nc = b * w.nb, w.mb_cols(b)
+        d = np.repeat(data[:, None, c0:c0 + nc], m, axis=1).copy()
+        for i in range(n):
+            cols = latcols[b, i]
+            d[i][:, cols] = out[off[b * n + i]:off[b * n + i] + m * len(cols)].reshape(m, len(cols))
+        dense.append(d)
+    return dense, mb.cpu(), tot.cpu(), cpts.cpu()
+
+
+@pytest.mark.parametrize("cfg,kw", [
+    (3, dict(n_cols=10_000, nb=2_048, m=3)),     # ragged last minibatch, m not a multiple of 4
+    (5, dict(n_cols=6_000, nb=1_500, m=2)),
+    (1, dict(n_cols=1_000, nb=4_096, m=2)),
+    (4, dict(n_cols=3_000, nb=1_000, m=5)),      # concepts never observed
+])
+def test_compact_stream_equals_resident(cfg, kw):
+    """Out-of-core passes that move only the compacted latent states over PCIe
+    (known data resident on the device) equal the device-resident call
+    sequence bit for bit: states, per-minibatch counts, totals and CPTs."""
+    w = make_workload(cfg, **kw)
+    ctx = H.context_for(w.net)
+    res_states, res_mb, res_tot, res_cpts = _resident(w, ctx, passes=2)
+    dense, mb, tot, cpts = _compact_case(w, ctx, passes=2)
+    for b in range(w.M):
+        nc = w.mb_cols(b)
+        assert np.array_equal(dense[b], res_states[b].numpy()[:, :, :nc]), b
+    assert torch.equal(mb, res_mb)
+    assert torch.equal(tot, res_tot)
+    assert torch.equal(cpts, res_cpts)
