@@ -178,6 +178,9 @@ def main():
 
     copy_gbs = copy_peak(dev, stream)
     roofline = sweep_roofline(w, net, mbs, hidden, node_samples_r, kt, wall_r, args, copy_gbs)
+    graphed = graph_timing(w, ctx, mbs, cpts, mb, tot, ws, args.warmup + args.steps + rsteps, args.steps, dev,
+                           stream)
+    log("graphed %d passes: %.3f ms per pass" % (args.steps, graphed["ms_per_step"]))
 
 
 
@@ -229,6 +232,7 @@ def main():
         "latent_draws_per_s": round(value * hidden, 1),
         "hbm_gbs_algorithmic_step": round(node_samples * (1.0 + hidden + 1.0 / w.m) / elapsed / 1e9, 1),
         "roofline": roofline,
+        "graphed": graphed,
         "parity": parity,
         "cpu_baseline": cpu,
         "streamed_from_host": streamed,
@@ -242,6 +246,36 @@ def main():
 
 ALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12   # one 32-bit VALU op per lane per clock
 PHILOX_OPS_PER_DRAW = 23                   # 80 ops per Philox4x32-10 block / 4 words + U24
+
+
+def graph_timing(w, ctx, mbs, cpts, mb, tot, ws, first_pass, passes, dev, stream):
+    """The timed loop again with every minibatch's step replayed from a
+    captured HIP graph (same_step_graph, one per minibatch, ids advanced on the
+    device) instead of issued launch by launch; beside `value`, never it."""
+    import torch
+
+    import paper_1511_06416_amd as same
+    ids = torch.tensor([[first_pass, first_pass * w.M + b] for b in mbs], dtype=torch.int32, device=dev)
+    graphs = [same.same_step_graph(ctx, w.states[b], w.obs[b], cpts, w.m, w.mb_cols(b), w.ld, b * w.nb, w.seed,
+                                   mb[b], tot, ids[i], w.M, 1, ws) for i, b in enumerate(mbs)]
+    for g in graphs:
+        g.launch(stream)
+    torch.cuda.synchronize()
+    t = time.perf_counter()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    for _ in range(passes):
+        for g in graphs:
+            g.launch(stream)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    el = max(time.perf_counter() - t, ev0.elapsed_time(ev1) / 1e3)
+    for g in graphs:
+        g.close()
+    ns = float(w.net.n) * sum(w.mb_cols(b) for b in mbs) * w.m * passes
+    return {"value": round(ns / el, 1), "unit": "node-samples/s", "passes": passes,
+            "ms_per_step": round(el * 1e3 / passes, 4)}
 
 
 def alu_ops_per_draw(net):

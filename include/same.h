@@ -477,6 +477,47 @@ typedef struct {
 int same_kernel_timing(same_ctx *ctx, int32_t enable);
 int same_kernel_times(same_ctx *ctx, same_kernel_times_t *out);
 
+/*
+ * Replayable step graphs (Sec. 4 fuses colour groups into few large kernel
+ * calls to hide the GPU's per-kernel overhead; on a small minibatch the
+ * launches of one step -- table builds, one or two sweep launches per
+ * colour group, counts, moving sum, Gamma and normalisation -- cost more
+ * than their work).  same_step_graph captures `steps` consecutive same_step
+ * calls over one resident minibatch into a HIP graph; same_graph_launch
+ * replays it on `stream` with one launch.
+ *
+ * ids (device, two uint32 words, 4-byte aligned, caller-owned) carries the
+ * sweep id (ids[0]) and the update id (ids[1]).  Step k of a replay reads
+ * them on the device as they stand when it starts, runs exactly what
+ * same_step(..., sweep_id = ids[0], ..., update_id = ids[1], ...) runs, and
+ * then adds 1 to ids[0] and update_stride to ids[1] (a final one-thread
+ * kernel).  So a replay from ids = {s, u} equals the eager calls with sweep
+ * ids s, s+1, ... and update ids u, u + update_stride, ...  (update_stride M
+ * gives the ids of a resident pass over M minibatches, where minibatch b's
+ * graph starts from {pass, pass * M + b}).
+ *
+ * The graph keeps the pointers it was captured with: states, obs, cpts,
+ * mb_counts, totals, ids and workspace must stay valid, and in place, while
+ * it is replayed.  It holds kernel nodes and their stream-order
+ * dependencies only (no memory-set or copy nodes).  Capture uses the
+ * context's per-device side stream (see same_sweep), so no other call of this
+ * context may run while same_step_graph runs; per-launch timing
+ * (same_kernel_timing) does not apply to replays.  Replays on one device
+ * must be ordered by the caller like the eager calls they stand for.
+ * Errors: SAME_EINVAL (null arguments, n_cols < 1, steps outside [1, 64], a
+ * launch on a device other than the capture's), SAME_EALIGN, SAME_ESIZE, and
+ * the argument errors of same_step; SAME_EHIP if the capture or
+ * instantiation fails.  same_graph_destroy frees the graph (null is a no-op).
+ */
+typedef struct same_graph same_graph;
+
+int same_step_graph(same_ctx *ctx, void *states, const uint8_t *obs, float *cpts, int32_t m,
+                    int64_t n_cols, int64_t ld, int64_t col_offset, uint64_t seed,
+                    int32_t *mb_counts, int32_t *totals, uint32_t *ids, uint32_t update_stride,
+                    int32_t steps, void *workspace, same_graph **out);
+int same_graph_launch(same_graph *graph, void *stream);
+void same_graph_destroy(same_graph *graph);
+
 /* Message for the calling thread's last failed call ("" if none). */
 const char *same_last_error(void);
 

@@ -22,7 +22,7 @@ __all__ = [
     "same_kernel_timing", "same_kernel_times", "same_expand_observed", "same_init_latent",
     "same_accumulate_hits", "same_predict", "same_counts_ema", "same_sample_cpts_ema", "same_stream_pass_ema",
     "same_grow_replicas", "same_debug_thresholds", "same_counts_noalloc", "same_stream_compact_layout",
-    "same_stream_pass_compact",
+    "same_stream_pass_compact", "same_step_graph", "same_graph_launch", "same_graph_destroy", "StepGraph",
     "library_path", "load_library",
 ]
 
@@ -103,6 +103,10 @@ def load_library():
         L.same_stream_compact_layout.argtypes = [P, P, I64, I64, I64, I32, P, C.POINTER(C.c_size_t), P, P]
         L.same_stream_pass_compact.argtypes = [P, P, P, P, P, I64, I64, I64, I32, P, P, P, U64, U32, I32, P, P, P]
         L.same_debug_thresholds.argtypes = [P, P, P, P, C.POINTER(C.c_int64), P, P, P]
+        L.same_step_graph.argtypes = [P, P, P, P, I32, I64, I64, I64, U64, P, P, P, U32, I32, P, C.POINTER(P)]
+        L.same_graph_launch.argtypes = [P, P]
+        L.same_graph_destroy.argtypes = [P]
+        L.same_graph_destroy.restype = None
         L.same_last_error.argtypes = []
         L.same_last_error.restype = C.c_char_p
         for f in ("same_create", "same_create_ex", "same_layout", "same_workspace_size", "same_sweep",
@@ -111,7 +115,8 @@ def load_library():
                   "same_kernel_times", "same_expand_observed", "same_init_latent",
                   "same_accumulate_hits", "same_predict", "same_counts_ema", "same_sample_cpts_ema",
                   "same_stream_pass_ema", "same_grow_replicas", "same_debug_thresholds",
-                  "same_counts_noalloc", "same_stream_compact_layout", "same_stream_pass_compact"):
+                  "same_counts_noalloc", "same_stream_compact_layout", "same_stream_pass_compact",
+                  "same_step_graph", "same_graph_launch"):
             getattr(L, f).restype = C.c_int
         _lib = L
         return L
@@ -264,6 +269,50 @@ def same_step(ctx, states, obs, cpts, m, n_cols, ld, col_offset, seed, sweep_id,
                                     int(n_cols), int(ld), int(col_offset), int(seed), int(sweep_id),
                                     _ptr(mb_counts), _ptr(totals), int(update_id), _ptr(workspace),
                                     _stream(stream)))
+
+
+class StepGraph:
+    """Handle of a captured step graph (same_step_graph); close() or garbage
+    collection frees it.  The tensors it was captured with are kept alive."""
+
+    def __init__(self, handle, keep):
+        self.handle = handle
+        self._keep = keep
+
+    def launch(self, stream=None):
+        same_graph_launch(self, stream)
+
+    def close(self):
+        if self.handle:
+            same_graph_destroy(self)
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def same_step_graph(ctx, states, obs, cpts, m, n_cols, ld, col_offset, seed, mb_counts, totals, ids,
+                    update_stride, steps, workspace):
+    """Captures `steps` same_step calls whose sweep and update ids are read
+    from the two-word device tensor `ids` (advanced by 1 and update_stride
+    after each step); returns a StepGraph."""
+    h = C.c_void_p()
+    _check(load_library().same_step_graph(ctx.handle, _ptr(states), _ptr(obs), _ptr(cpts), int(m), int(n_cols),
+                                          int(ld), int(col_offset), int(seed), _ptr(mb_counts), _ptr(totals),
+                                          _ptr(ids), int(update_stride), int(steps), _ptr(workspace),
+                                          C.byref(h)))
+    return StepGraph(h.value, (ctx, states, obs, cpts, mb_counts, totals, ids, workspace))
+
+
+def same_graph_launch(graph, stream=None):
+    _check(load_library().same_graph_launch(graph.handle, _stream(stream)))
+
+
+def same_graph_destroy(graph):
+    load_library().same_graph_destroy(graph.handle)
+    graph.handle = None
 
 
 def same_sweep_plan(ctx, m, n_cols):

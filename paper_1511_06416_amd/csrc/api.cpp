@@ -410,11 +410,34 @@ int do_sweep(same_ctx *ctx, void *states, const uint8_t *obs, const float *cpts,
     return SAME_OK;
 }
 
+// The Dirichlet resample of same_sample_cpts; ids (nullable, device) supplies
+// the update id at launch time instead (replayed step graphs).
+int sample_cpts(same_ctx *ctx, const int32_t *totals, float *cpts_out, uint64_t seed, uint32_t update_id,
+                const uint32_t *ids, void *workspace, void *stream) {
+    if (!ctx || !totals || !cpts_out || !workspace)
+        return set_error(SAME_EINVAL, "ctx, totals, cpts_out and workspace must be non-null");
+    if (!aligned(workspace, kAlign)) return set_error(SAME_EALIGN, "workspace must be 256-byte aligned");
+    same::DeviceTables *t = nullptr;
+    int rc = tables_for_current_device(ctx, &t);
+    if (rc) return rc;
+    hipStream_t s = (hipStream_t)stream;
+    const int64_t total = ctx->g.off[ctx->g.n];
+    double *gv = (double *)((char *)workspace + ctx->ws_gamma);
+    rc = check_hip(same::launch_gamma(totals, ctx->alpha, (uint32_t)seed, (uint32_t)(seed >> 32), update_id,
+                                      ids, gv, total, s),
+                   "gamma launch");
+    if (rc) return rc;
+    return check_hip(same::launch_normalize(*t, gv, cpts_out, ctx->g.n_rows, s), "normalize launch");
+}
+
 // Sweep, counts with the moving sum, and the Dirichlet resample of one
 // minibatch, tile by tile for the sweep and counts.
+// ids (nullable, device): the sweep and update ids are read there at launch
+// time instead of sweep_id and update_id.
 int do_step(same_ctx *ctx, void *states, const uint8_t *obs, float *cpts, int32_t m, int64_t n_cols,
             int64_t ld, int64_t col_offset, uint64_t seed, uint32_t sweep_id, int32_t *mb_counts,
-            int32_t *totals, uint32_t update_id, void *workspace, void *stream) {
+            int32_t *totals, uint32_t update_id, void *workspace, void *stream,
+            const uint32_t *ids = nullptr) {
     int rc = check_sweep_args(ctx, states, obs, cpts, m, n_cols, ld, col_offset, 0, 0, nullptr, workspace);
     if (rc) return rc;
     if (!mb_counts || !totals) return set_error(SAME_EINVAL, "mb_counts and totals must be non-null");
@@ -429,6 +452,7 @@ int do_step(same_ctx *ctx, void *states, const uint8_t *obs, float *cpts, int32_
     same::SweepParams P;
     rc = prepare_sweep(ctx, t, states, obs, cpts, m, n_cols, ld, col_offset, seed, sweep_id, 0, 0, nullptr,
                        workspace, s, P);
+    P.ids = ids;
     if (!rc) rc = check_hip(same::launch_fill_zero(newc, total, s), "count clear launch");
     if (rc) return rc;
     const int64_t T = tile_cols(ctx, m, n_cols);
@@ -442,7 +466,7 @@ int do_step(same_ctx *ctx, void *states, const uint8_t *obs, float *cpts, int32_
     }
     rc = check_hip(same::launch_moving_sum(newc, mb_counts, totals, total, s), "moving-sum launch");
     if (rc) return rc;
-    return same_sample_cpts(ctx, totals, cpts, seed, update_id, workspace, stream);
+    return sample_cpts(ctx, totals, cpts, seed, update_id, ids, workspace, stream);
 }
 
 // Device slot geometry of the out-of-core passes.
@@ -627,20 +651,7 @@ int same_counts(same_ctx *ctx, const void *states, int32_t m, int64_t n_cols, in
 
 int same_sample_cpts(same_ctx *ctx, const int32_t *totals, float *cpts_out, uint64_t seed,
                      uint32_t update_id, void *workspace, void *stream) {
-    if (!ctx || !totals || !cpts_out || !workspace)
-        return set_error(SAME_EINVAL, "ctx, totals, cpts_out and workspace must be non-null");
-    if (!aligned(workspace, kAlign)) return set_error(SAME_EALIGN, "workspace must be 256-byte aligned");
-    same::DeviceTables *t = nullptr;
-    int rc = tables_for_current_device(ctx, &t);
-    if (rc) return rc;
-    hipStream_t s = (hipStream_t)stream;
-    const int64_t total = ctx->g.off[ctx->g.n];
-    double *gv = (double *)((char *)workspace + ctx->ws_gamma);
-    rc = check_hip(same::launch_gamma(totals, ctx->alpha, (uint32_t)seed, (uint32_t)(seed >> 32), update_id,
-                                      gv, total, s),
-                   "gamma launch");
-    if (rc) return rc;
-    return check_hip(same::launch_normalize(*t, gv, cpts_out, ctx->g.n_rows, s), "normalize launch");
+    return sample_cpts(ctx, totals, cpts_out, seed, update_id, nullptr, workspace, stream);
 }
 
 int same_sweep_plan(const same_ctx *ctx, int32_t m, int64_t n_cols, int64_t *tile_cols_out,
@@ -851,7 +862,7 @@ int same_sample_cpts_ema(same_ctx *ctx, const double *totals, float *cpts_out, u
     const int64_t total = ctx->g.off[ctx->g.n];
     double *gv = (double *)((char *)workspace + ctx->ws_gamma);
     rc = check_hip(same::launch_gamma(totals, ctx->alpha, (uint32_t)seed, (uint32_t)(seed >> 32), update_id,
-                                      gv, total, s),
+                                      nullptr, gv, total, s),
                    "gamma launch");
     if (rc) return rc;
     return check_hip(same::launch_normalize(*t, gv, cpts_out, ctx->g.n_rows, s), "normalize launch");
@@ -1157,5 +1168,94 @@ int same_stream_pass_compact(same_ctx *ctx, void *lat_host, const int64_t *lat_o
             return rc;
     return SAME_OK;
 }
+
+}  // extern "C"
+
+// ------------------------------------------------ replayable step graphs
+
+// A captured sequence of SAME steps over one resident minibatch.
+struct same_graph {
+    int device = -1;
+    hipGraph_t graph = nullptr;
+    hipGraphExec_t exec = nullptr;
+};
+
+namespace {
+
+constexpr int32_t kMaxGraphSteps = 64;
+
+void free_graph(same_graph *g) {
+    if (!g) return;
+    if (g->exec) (void)hipGraphExecDestroy(g->exec);
+    if (g->graph) (void)hipGraphDestroy(g->graph);
+    delete g;
+}
+
+}  // namespace
+
+extern "C" {
+
+int same_step_graph(same_ctx *ctx, void *states, const uint8_t *obs, float *cpts, int32_t m, int64_t n_cols,
+                    int64_t ld, int64_t col_offset, uint64_t seed, int32_t *mb_counts, int32_t *totals,
+                    uint32_t *ids, uint32_t update_stride, int32_t steps, void *workspace, same_graph **out) {
+    if (!out) return set_error(SAME_EINVAL, "out is null");
+    *out = nullptr;
+    int rc = check_sweep_args(ctx, states, obs, cpts, m, n_cols, ld, col_offset, 0, 0, nullptr, workspace);
+    if (rc) return rc;
+    if (!mb_counts || !totals || !ids) return set_error(SAME_EINVAL, "mb_counts, totals and ids must be non-null");
+    if (!aligned(ids, 4)) return set_error(SAME_EALIGN, "ids must be 4-byte aligned");
+    if (steps < 1 || steps > kMaxGraphSteps) return set_error(SAME_EINVAL, "steps must be in [1, 64]");
+    if (n_cols < 1) return set_error(SAME_EINVAL, "n_cols must be positive");
+    if ((double)n_cols * (double)m >= 2147483648.0) return set_error(SAME_ESIZE, "n_cols * m must stay below 2^31");
+    // what is set up synchronously on first use happens before the capture
+    same::DeviceTables *t = nullptr;
+    rc = tables_for_current_device(ctx, &t);
+    StreamRes *sr = nullptr;
+    if (!rc) rc = stream_res_for_current_device(ctx, &sr);
+    if (rc) return rc;
+    same_graph *g = new (std::nothrow) same_graph();
+    if (!g) return set_error(SAME_ENOMEM, "out of host memory");
+    rc = check_hip(hipGetDevice(&g->device), "hipGetDevice");
+    hipStream_t cs = nullptr;
+    if (!rc) rc = check_hip(hipStreamCreateWithFlags(&cs, hipStreamNonBlocking), "hipStreamCreateWithFlags");
+    if (rc) {
+        free_graph(g);
+        return rc;
+    }
+    // per-launch timing records events; none go into the graph
+    const bool timing = ctx->timing.on;
+    ctx->timing.on = false;
+    rc = check_hip(hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal), "hipStreamBeginCapture");
+    if (!rc) {
+        for (int32_t k = 0; k < steps && !rc; ++k) {
+            rc = do_step(ctx, states, obs, cpts, m, n_cols, ld, col_offset, seed, 0, mb_counts, totals, 0,
+                         workspace, cs, ids);
+            if (!rc) rc = check_hip(same::launch_advance_ids(ids, 1, update_stride, cs), "id advance launch");
+        }
+        // the capture ends whether or not a launch failed
+        const int rc_end = check_hip(hipStreamEndCapture(cs, &g->graph), "hipStreamEndCapture");
+        if (!rc) rc = rc_end;
+    }
+    ctx->timing.on = timing;
+    (void)hipStreamDestroy(cs);
+    if (!rc) rc = check_hip(hipGraphInstantiate(&g->exec, g->graph, nullptr, nullptr, 0), "hipGraphInstantiate");
+    if (rc) {
+        free_graph(g);
+        return rc;
+    }
+    *out = g;
+    return SAME_OK;
+}
+
+int same_graph_launch(same_graph *g, void *stream) {
+    if (!g || !g->exec) return set_error(SAME_EINVAL, "graph is null");
+    int device = -1;
+    int rc = check_hip(hipGetDevice(&device), "hipGetDevice");
+    if (rc) return rc;
+    if (device != g->device) return set_error(SAME_EINVAL, "the graph was captured on another device");
+    return check_hip(hipGraphLaunch(g->exec, (hipStream_t)stream), "hipGraphLaunch");
+}
+
+void same_graph_destroy(same_graph *g) { free_graph(g); }
 
 }  // extern "C"

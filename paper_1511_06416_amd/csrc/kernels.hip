@@ -782,6 +782,7 @@ __device__ __forceinline__ void sweep_table(const SweepParams &P, const Work &W,
 // bound).
 template <typename ST, bool DEBUG, bool STAGED>
 __global__ __launch_bounds__(kSweepBlock, DEBUG ? 1 : kSweepWaves) void sweep_fast_kernel(SweepParams P) {
+    if (P.ids) P.sweep_id = P.ids[0];
     extern __shared__ float4 lds4[];
     __shared__ uint16_t lcol[4 * kSweepBlock];
     __shared__ int32_t wave_n[kSweepBlock / 64];
@@ -901,6 +902,7 @@ __device__ void sweep_wide(const SweepParams &P, const Work &W) {
 
 template <typename ST, bool DEBUG>
 __global__ __launch_bounds__(kSweepBlock) void sweep_wide_kernel(SweepParams P) {
+    if (P.ids) P.sweep_id = P.ids[0];
     const Work W = block_work(P);
     const int KP = W.d[1];
     if (KP == 2) sweep_wide<2, ST, DEBUG>(P, W);
@@ -942,6 +944,7 @@ __device__ float weight_ext(cint32_t *d, const float *__restrict__ tab, const ST
 
 template <typename ST, bool DEBUG>
 __global__ __launch_bounds__(kSweepBlock) void sweep_generic_kernel(SweepParams P) {
+    if (P.ids) P.sweep_id = P.ids[0];
     using Q = Quad<ST>;
     const Work W = block_work(P);
     cint32_t *d = W.d;
@@ -1351,10 +1354,20 @@ __device__ double gamma_mt(double a, uint32_t e, uint32_t q, uint32_t k0, uint32
 
 template <typename T>
 __global__ void gamma_kernel(const T *__restrict__ totals, double alpha, uint32_t k0, uint32_t k1,
-                             uint32_t update_id, double *__restrict__ g, int64_t total) {
+                             uint32_t update_id, const uint32_t *__restrict__ ids, double *__restrict__ g,
+                             int64_t total) {
     const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (e >= total) return;
-    g[e] = gamma_mt(alpha + (double)totals[e], (uint32_t)e, update_id, k0, k1);
+    const uint32_t u = ids ? ids[1] : update_id;
+    g[e] = gamma_mt(alpha + (double)totals[e], (uint32_t)e, u, k0, k1);
+}
+
+// The id pair of a replayed step graph moves on by (d0, d1) after the step.
+__global__ void advance_ids_kernel(uint32_t *ids, uint32_t d0, uint32_t d1) {
+    if (threadIdx.x == 0) {
+        ids[0] += d0;
+        ids[1] += d1;
+    }
 }
 
 // Exponential moving sum of the counts (Sec. 4, for datasets whose
@@ -1976,21 +1989,28 @@ hipError_t launch_moving_sum(const int32_t *newc, int32_t *mb, int32_t *totals, 
 
 template <typename T>
 hipError_t launch_gamma_t(const T *totals, double alpha, uint32_t key0, uint32_t key1, uint32_t update_id,
-                          double *g, int64_t total, hipStream_t stream) {
+                          const uint32_t *ids, double *g, int64_t total, hipStream_t stream) {
     if (total <= 0) return hipSuccess;
     hipLaunchKernelGGL(dev::gamma_kernel<T>, dim3(blocks_for(total, dev::kBlock)), dim3(dev::kBlock), 0, stream,
-                       totals, alpha, key0, key1, update_id, g, total);
+                       totals, alpha, key0, key1, update_id, ids, g, total);
     return hipGetLastError();
 }
 
 hipError_t launch_gamma(const int32_t *totals, double alpha, uint32_t key0, uint32_t key1,
-                        uint32_t update_id, double *g, int64_t total, hipStream_t stream) {
-    return launch_gamma_t(totals, alpha, key0, key1, update_id, g, total, stream);
+                        uint32_t update_id, const uint32_t *ids, double *g, int64_t total,
+                        hipStream_t stream) {
+    return launch_gamma_t(totals, alpha, key0, key1, update_id, ids, g, total, stream);
 }
 
 hipError_t launch_gamma(const double *totals, double alpha, uint32_t key0, uint32_t key1,
-                        uint32_t update_id, double *g, int64_t total, hipStream_t stream) {
-    return launch_gamma_t(totals, alpha, key0, key1, update_id, g, total, stream);
+                        uint32_t update_id, const uint32_t *ids, double *g, int64_t total,
+                        hipStream_t stream) {
+    return launch_gamma_t(totals, alpha, key0, key1, update_id, ids, g, total, stream);
+}
+
+hipError_t launch_advance_ids(uint32_t *ids, uint32_t d0, uint32_t d1, hipStream_t stream) {
+    hipLaunchKernelGGL(dev::advance_ids_kernel, dim3(1), dim3(64), 0, stream, ids, d0, d1);
+    return hipGetLastError();
 }
 
 hipError_t launch_ema(const int32_t *newc, double *totals, double decay, int64_t total, hipStream_t stream) {

@@ -57,6 +57,9 @@ struct SweepParams {
     int32_t reverse;               // 1: slabs in descending order (see block_work)
     float *probs;
     int32_t max_card;
+    // nullable: when set, the sweep id is read from ids[0] on the device at
+    // launch time instead of sweep_id (replayed HIP graphs of a step)
+    const uint32_t *ids;
 };
 
 hipError_t launch_build_tables(const DeviceTables &t, const float *cpts, float *table,
@@ -129,10 +132,16 @@ hipError_t launch_grow(const void *src, int32_t m, void *dst, int32_t m2, int32_
 hipError_t launch_moving_sum(const int32_t *newc, int32_t *mb, int32_t *totals, int64_t total,
                              hipStream_t stream);
 
+// ids (nullable): the update id is read from ids[1] on the device instead.
 hipError_t launch_gamma(const int32_t *totals, double alpha, uint32_t key0, uint32_t key1,
-                        uint32_t update_id, double *g, int64_t total, hipStream_t stream);
+                        uint32_t update_id, const uint32_t *ids, double *g, int64_t total,
+                        hipStream_t stream);
 hipError_t launch_gamma(const double *totals, double alpha, uint32_t key0, uint32_t key1,
-                        uint32_t update_id, double *g, int64_t total, hipStream_t stream);
+                        uint32_t update_id, const uint32_t *ids, double *g, int64_t total,
+                        hipStream_t stream);
+
+// ids[0] += d0, ids[1] += d1 (one thread; the last node of a graphed step).
+hipError_t launch_advance_ids(uint32_t *ids, uint32_t d0, uint32_t d1, hipStream_t stream);
 
 // Exponential moving sum: totals = decay * totals + newc (fp64).
 hipError_t launch_ema(const int32_t *newc, double *totals, double decay, int64_t total, hipStream_t stream);

@@ -298,3 +298,37 @@ def test_grow_replicas_argument_errors():
     assert L.same_grow_replicas(h, a, 3, P((1 << 20) + 16), 4, 8, None) == same.SAME_EINVAL  # overlap
     assert L.same_grow_replicas(h, a, 3, b, 4, 6, None) == same.SAME_EALIGN          # ld % 4
     ctx.close()
+
+
+def test_step_graph_argument_errors():
+    """same_step_graph validates before any device call; launch and destroy
+    reject or ignore a null graph."""
+    ctx = _ctx(koller())
+    L = same.load_library()
+    P = C.c_void_p
+    good = dict(st=FAKE, ob=FAKE, cp=FAKE, m=2, n_cols=1000, ld=1024, col_offset=0, mb=FAKE, tot=FAKE,
+                ids=FAKE, stride=1, steps=1, ws=FAKE)
+
+    def call(**kw):
+        a = dict(good)
+        a.update(kw)
+        out = P()
+        rc = L.same_step_graph(ctx.handle, P(a["st"]), P(a["ob"]), P(a["cp"]), a["m"], a["n_cols"], a["ld"],
+                               a["col_offset"], 1, P(a["mb"]), P(a["tot"]), P(a["ids"]), a["stride"],
+                               a["steps"], P(a["ws"]), C.byref(out))
+        assert out.value is None
+        return rc
+
+    assert call(ids=None) == same.SAME_EINVAL
+    assert call(mb=None) == same.SAME_EINVAL
+    assert call(st=None) == same.SAME_EINVAL
+    assert call(steps=0) == same.SAME_EINVAL
+    assert call(steps=65) == same.SAME_EINVAL
+    assert call(n_cols=0) == same.SAME_EINVAL
+    assert call(ids=FAKE + 2) == same.SAME_EALIGN
+    assert call(ld=1022) == same.SAME_EALIGN
+    assert call(col_offset=(1 << 32) - 512) == same.SAME_ESIZE
+    assert L.same_step_graph(ctx.handle, P(FAKE), P(FAKE), P(FAKE), 2, 1000, 1024, 0, 1, P(FAKE), P(FAKE),
+                             P(FAKE), 1, 1, P(FAKE), None) == same.SAME_EINVAL
+    assert L.same_graph_launch(None, None) == same.SAME_EINVAL
+    L.same_graph_destroy(None)
