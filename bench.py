@@ -46,6 +46,8 @@ def parse():
                    help="SAME steps (sweep + counts + resample) of the oracle baseline")
     p.add_argument("--copy-calibration", action="store_true",
                    help="(kept for older profile commands: the 1 GiB copy now always runs)")
+    p.add_argument("--graph-steps", type=int, default=8,
+                   help="SAME steps per captured graph in the graphed timing (single-minibatch workloads)")
     p.add_argument("--roofline-steps", type=int, default=1,
                    help="instrumented passes after the timed ones, for the per-launch roofline")
     p.add_argument("--parity-cols", type=int, default=32_768,
@@ -179,7 +181,7 @@ def main():
     copy_gbs = copy_peak(dev, stream)
     roofline = sweep_roofline(w, net, mbs, hidden, node_samples_r, kt, wall_r, args, copy_gbs)
     graphed = graph_timing(w, ctx, mbs, cpts, mb, tot, ws, args.warmup + args.steps + rsteps, args.steps, dev,
-                           stream)
+                           stream, args.graph_steps)
     log("graphed %d passes: %.3f ms per pass" % (args.steps, graphed["ms_per_step"]))
 
 
@@ -248,16 +250,19 @@ ALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12   # one 32-bit VALU op per lane per cloc
 PHILOX_OPS_PER_DRAW = 23                   # 80 ops per Philox4x32-10 block / 4 words + U24
 
 
-def graph_timing(w, ctx, mbs, cpts, mb, tot, ws, first_pass, passes, dev, stream):
+def graph_timing(w, ctx, mbs, cpts, mb, tot, ws, first_pass, passes, dev, stream, per_graph):
     """The timed loop again with every minibatch's step replayed from a
     captured HIP graph (same_step_graph, one per minibatch, ids advanced on the
-    device) instead of issued launch by launch; beside `value`, never it."""
+    device) instead of issued launch by launch; beside `value`, never it.  With
+    a single minibatch one graph holds `per_graph` consecutive steps."""
     import torch
 
     import paper_1511_06416_amd as same
+    k = per_graph if len(mbs) == 1 else 1
+    passes = (passes + k - 1) // k * k
     ids = torch.tensor([[first_pass, first_pass * w.M + b] for b in mbs], dtype=torch.int32, device=dev)
     graphs = [same.same_step_graph(ctx, w.states[b], w.obs[b], cpts, w.m, w.mb_cols(b), w.ld, b * w.nb, w.seed,
-                                   mb[b], tot, ids[i], w.M, 1, ws) for i, b in enumerate(mbs)]
+                                   mb[b], tot, ids[i], w.M, k, ws) for i, b in enumerate(mbs)]
     for g in graphs:
         g.launch(stream)
     torch.cuda.synchronize()
@@ -265,7 +270,7 @@ def graph_timing(w, ctx, mbs, cpts, mb, tot, ws, first_pass, passes, dev, stream
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     ev0.record(stream)
-    for _ in range(passes):
+    for _ in range(passes // k):
         for g in graphs:
             g.launch(stream)
     ev1.record(stream)
@@ -274,7 +279,7 @@ def graph_timing(w, ctx, mbs, cpts, mb, tot, ws, first_pass, passes, dev, stream
     for g in graphs:
         g.close()
     ns = float(w.net.n) * sum(w.mb_cols(b) for b in mbs) * w.m * passes
-    return {"value": round(ns / el, 1), "unit": "node-samples/s", "passes": passes,
+    return {"value": round(ns / el, 1), "unit": "node-samples/s", "passes": passes, "steps_per_graph": k,
             "ms_per_step": round(el * 1e3 / passes, 4)}
 
 

@@ -265,16 +265,16 @@ int check_sweep_args(same_ctx *ctx, void *states, const uint8_t *obs, const floa
     return SAME_OK;
 }
 
-// Builds this call's tables from cpts and fills the sweep parameters.
+// Builds this call's tables from cpts (and clears zero[0 .. zero_count) in
+// the same launch) and fills the sweep parameters.
 int prepare_sweep(same_ctx *ctx, same::DeviceTables *t, void *states, const uint8_t *obs,
                   const float *cpts, int32_t m, int64_t n_cols, int64_t ld, int64_t col_offset,
                   uint64_t seed, uint32_t sweep_id, int64_t win_begin, int64_t win, float *probs,
-                  void *workspace, hipStream_t s, same::SweepParams &P) {
+                  void *workspace, hipStream_t s, same::SweepParams &P, int32_t *zero = nullptr,
+                  int64_t zero_count = 0) {
     float *table = (float *)((char *)workspace + ctx->ws_table);
     uint32_t *cond = (uint32_t *)((char *)workspace + ctx->ws_cond);
-    int rc = check_hip(same::launch_build_tables(*t, cpts, table, s), "table build launch");
-    if (rc) return rc;
-    rc = check_hip(same::launch_build_thresholds(*t, cpts, cond, s), "threshold build launch");
+    int rc = check_hip(same::launch_prepare(*t, cpts, table, cond, zero, zero_count, s), "table build launch");
     if (rc) return rc;
     P = same::SweepParams{};
     P.desc = t->desc;
@@ -410,26 +410,6 @@ int do_sweep(same_ctx *ctx, void *states, const uint8_t *obs, const float *cpts,
     return SAME_OK;
 }
 
-// The Dirichlet resample of same_sample_cpts; ids (nullable, device) supplies
-// the update id at launch time instead (replayed step graphs).
-int sample_cpts(same_ctx *ctx, const int32_t *totals, float *cpts_out, uint64_t seed, uint32_t update_id,
-                const uint32_t *ids, void *workspace, void *stream) {
-    if (!ctx || !totals || !cpts_out || !workspace)
-        return set_error(SAME_EINVAL, "ctx, totals, cpts_out and workspace must be non-null");
-    if (!aligned(workspace, kAlign)) return set_error(SAME_EALIGN, "workspace must be 256-byte aligned");
-    same::DeviceTables *t = nullptr;
-    int rc = tables_for_current_device(ctx, &t);
-    if (rc) return rc;
-    hipStream_t s = (hipStream_t)stream;
-    const int64_t total = ctx->g.off[ctx->g.n];
-    double *gv = (double *)((char *)workspace + ctx->ws_gamma);
-    rc = check_hip(same::launch_gamma(totals, ctx->alpha, (uint32_t)seed, (uint32_t)(seed >> 32), update_id,
-                                      ids, gv, total, s),
-                   "gamma launch");
-    if (rc) return rc;
-    return check_hip(same::launch_normalize(*t, gv, cpts_out, ctx->g.n_rows, s), "normalize launch");
-}
-
 // Sweep, counts with the moving sum, and the Dirichlet resample of one
 // minibatch, tile by tile for the sweep and counts.
 // ids (nullable, device): the sweep and update ids are read there at launch
@@ -451,10 +431,9 @@ int do_step(same_ctx *ctx, void *states, const uint8_t *obs, float *cpts, int32_
     int32_t *newc = (int32_t *)((char *)workspace + ctx->ws_counts);
     same::SweepParams P;
     rc = prepare_sweep(ctx, t, states, obs, cpts, m, n_cols, ld, col_offset, seed, sweep_id, 0, 0, nullptr,
-                       workspace, s, P);
-    P.ids = ids;
-    if (!rc) rc = check_hip(same::launch_fill_zero(newc, total, s), "count clear launch");
+                       workspace, s, P, newc, total);
     if (rc) return rc;
+    P.ids = ids;
     const int64_t T = tile_cols(ctx, m, n_cols);
     for (int64_t t0 = 0; t0 < n_cols; t0 += T) {
         const int64_t nt = n_cols - t0 < T ? n_cols - t0 : T;
@@ -464,9 +443,14 @@ int do_step(same_ctx *ctx, void *states, const uint8_t *obs, float *cpts, int32_
                        "count launch");
         if (rc) return rc;
     }
-    rc = check_hip(same::launch_moving_sum(newc, mb_counts, totals, total, s), "moving-sum launch");
+    // the moving sum and the Dirichlet resample (same_sample_cpts), with the
+    // moving sum fused into the Gamma launch
+    double *gv = (double *)((char *)workspace + ctx->ws_gamma);
+    rc = check_hip(same::launch_moving_sum_gamma(newc, mb_counts, totals, ctx->alpha, (uint32_t)seed,
+                                                 (uint32_t)(seed >> 32), update_id, ids, gv, total, s),
+                   "moving-sum and gamma launch");
     if (rc) return rc;
-    return sample_cpts(ctx, totals, cpts, seed, update_id, ids, workspace, stream);
+    return check_hip(same::launch_normalize(*t, gv, cpts, ctx->g.n_rows, s), "normalize launch");
 }
 
 // Device slot geometry of the out-of-core passes.
@@ -651,7 +635,20 @@ int same_counts(same_ctx *ctx, const void *states, int32_t m, int64_t n_cols, in
 
 int same_sample_cpts(same_ctx *ctx, const int32_t *totals, float *cpts_out, uint64_t seed,
                      uint32_t update_id, void *workspace, void *stream) {
-    return sample_cpts(ctx, totals, cpts_out, seed, update_id, nullptr, workspace, stream);
+    if (!ctx || !totals || !cpts_out || !workspace)
+        return set_error(SAME_EINVAL, "ctx, totals, cpts_out and workspace must be non-null");
+    if (!aligned(workspace, kAlign)) return set_error(SAME_EALIGN, "workspace must be 256-byte aligned");
+    same::DeviceTables *t = nullptr;
+    int rc = tables_for_current_device(ctx, &t);
+    if (rc) return rc;
+    hipStream_t s = (hipStream_t)stream;
+    const int64_t total = ctx->g.off[ctx->g.n];
+    double *gv = (double *)((char *)workspace + ctx->ws_gamma);
+    rc = check_hip(same::launch_gamma(totals, ctx->alpha, (uint32_t)seed, (uint32_t)(seed >> 32), update_id,
+                                      nullptr, gv, total, s),
+                   "gamma launch");
+    if (rc) return rc;
+    return check_hip(same::launch_normalize(*t, gv, cpts_out, ctx->g.n_rows, s), "normalize launch");
 }
 
 int same_sweep_plan(const same_ctx *ctx, int32_t m, int64_t n_cols, int64_t *tile_cols_out,

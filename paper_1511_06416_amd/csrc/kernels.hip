@@ -1006,14 +1006,14 @@ __global__ __launch_bounds__(kSweepBlock) void sweep_generic_kernel(SweepParams 
 // T_k = ceil(2^24 * S_k / Z) for k < K-1, padded with 2^24.
 constexpr int kMaxBlanketTable = 24;
 
-__global__ __launch_bounds__(kBlock) void build_thresholds_kernel(
-    const int32_t *__restrict__ cprog, const int32_t *__restrict__ cprog_off,
+__device__ __forceinline__ void build_thresholds_block(
+    int32_t blk, const int32_t *__restrict__ cprog, const int32_t *__restrict__ cprog_off,
     const int32_t *__restrict__ blk_prog, const int32_t *__restrict__ blk_first,
     const float *__restrict__ cpts, uint32_t *__restrict__ cond) {
 #pragma clang fp contract(off)
-    const int32_t *P = cprog + cprog_off[blk_prog[blockIdx.x]];
+    const int32_t *P = cprog + cprog_off[blk_prog[blk]];
     const int K = P[0], KT = P[1], coff = P[2], ncfg = P[3], nbl = P[4];
-    const int cfg = blk_first[blockIdx.x] + (int)threadIdx.x;
+    const int cfg = blk_first[blk] + (int)threadIdx.x;
     if (cfg >= ncfg) return;
     int xb[kMaxBlanketTable];
     int rem = cfg;
@@ -1058,13 +1058,20 @@ __global__ __launch_bounds__(kBlock) void build_thresholds_kernel(
         dst[k] = t;
     }
 }
+
+__global__ __launch_bounds__(kBlock) void build_thresholds_kernel(
+    const int32_t *__restrict__ cprog, const int32_t *__restrict__ cprog_off,
+    const int32_t *__restrict__ blk_prog, const int32_t *__restrict__ blk_first,
+    const float *__restrict__ cpts, uint32_t *__restrict__ cond) {
+    build_thresholds_block((int32_t)blockIdx.x, cprog, cprog_off, blk_prog, blk_first, cpts, cond);
+}
 // ---------------------------------------------------------------- table build
 
-__global__ __launch_bounds__(kBlock) void build_tables_kernel(
-    const Segment *__restrict__ segs, const int32_t *__restrict__ blk_seg,
+__device__ __forceinline__ void build_tables_block(
+    int32_t blk, const Segment *__restrict__ segs, const int32_t *__restrict__ blk_seg,
     const int32_t *__restrict__ blk_first, const float *__restrict__ cpts, float *__restrict__ table) {
-    const Segment sg = segs[blk_seg[blockIdx.x]];
-    const int32_t grp = blk_first[blockIdx.x] + (int32_t)threadIdx.x;
+    const Segment sg = segs[blk_seg[blk]];
+    const int32_t grp = blk_first[blk] + (int32_t)threadIdx.x;
     if (grp >= sg.n_groups) return;
     int64_t src, step;
     if (sg.own) {
@@ -1085,12 +1092,48 @@ __global__ __launch_bounds__(kBlock) void build_tables_kernel(
     for (int k = sg.K; k < sg.KP; ++k) dst[k] = 0.f;
 }
 
+__global__ __launch_bounds__(kBlock) void build_tables_kernel(
+    const Segment *__restrict__ segs, const int32_t *__restrict__ blk_seg,
+    const int32_t *__restrict__ blk_first, const float *__restrict__ cpts, float *__restrict__ table) {
+    build_tables_block((int32_t)blockIdx.x, segs, blk_seg, blk_first, cpts, table);
+}
+
 // ---------------------------------------------------------------- counts
 
 __global__ void fill_zero_kernel(int32_t *p, int64_t count) {
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count;
          i += (int64_t)gridDim.x * blockDim.x)
         p[i] = 0;
+}
+
+// What precedes a step's sweep, in one launch: blocks [0, n_build) build the
+// k-vector tables, the next n_cond blocks the threshold tables (both from the
+// CPTs), and the last n_zero blocks clear the count histogram (grid-stride).
+// Each part runs the same code per element as its own kernel; on small
+// minibatches a step's launches cost more than their work.
+struct PrepareArgs {
+    const Segment *segs;
+    const int32_t *blk_seg, *blk_first;
+    float *table;
+    const int32_t *cprog, *cprog_off, *cblk_prog, *cblk_first;
+    uint32_t *cond;
+    const float *cpts;
+    int32_t *zero;
+    int64_t zero_count;
+    int32_t n_build, n_cond, n_zero;
+};
+
+__global__ __launch_bounds__(kBlock) void prepare_step_kernel(PrepareArgs A) {
+    const int32_t b = (int32_t)blockIdx.x;
+    if (b < A.n_build) {
+        build_tables_block(b, A.segs, A.blk_seg, A.blk_first, A.cpts, A.table);
+    } else if (b < A.n_build + A.n_cond) {
+        build_thresholds_block(b - A.n_build, A.cprog, A.cprog_off, A.cblk_prog, A.cblk_first, A.cpts, A.cond);
+    } else {
+        const int64_t z = b - A.n_build - A.n_cond;
+        for (int64_t i = z * kBlock + threadIdx.x; i < A.zero_count; i += (int64_t)A.n_zero * kBlock)
+            A.zero[i] = 0;
+    }
 }
 
 // Histogram of (parent row, state) for one node over a run of columns and all
@@ -1360,6 +1403,24 @@ __global__ void gamma_kernel(const T *__restrict__ totals, double alpha, uint32_
     if (e >= total) return;
     const uint32_t u = ids ? ids[1] : update_id;
     g[e] = gamma_mt(alpha + (double)totals[e], (uint32_t)e, u, k0, k1);
+}
+
+// The moving sum of a step's counts and the Gamma draw of every CPT entry
+// from the updated total, in one launch: per entry, the arithmetic of
+// moving_sum_kernel followed by that of gamma_kernel<int32_t>.
+__global__ void moving_sum_gamma_kernel(const int32_t *__restrict__ newc, int32_t *__restrict__ mb,
+                                        int32_t *__restrict__ totals, double alpha, uint32_t k0, uint32_t k1,
+                                        uint32_t update_id, const uint32_t *__restrict__ ids,
+                                        double *__restrict__ g, int64_t total) {
+    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= total) return;
+    const int32_t nv = newc[e];
+    const int32_t delta = nv - mb[e];
+    mb[e] = nv;
+    const int32_t t = totals[e] + delta;
+    totals[e] = t;
+    const uint32_t u = ids ? ids[1] : update_id;
+    g[e] = gamma_mt(alpha + (double)t, (uint32_t)e, u, k0, k1);
 }
 
 // The id pair of a replayed step graph moves on by (d0, d1) after the step.
@@ -1810,6 +1871,41 @@ hipError_t launch_build_thresholds(const DeviceTables &t, const float *cpts, uin
     if (t.n_cond_blocks == 0) return hipSuccess;
     hipLaunchKernelGGL(dev::build_thresholds_kernel, dim3(t.n_cond_blocks), dim3(dev::kBlock), 0,
                        stream, t.cprog, t.cprog_off, t.cblk_prog, t.cblk_first, cpts, cond);
+    return hipGetLastError();
+}
+
+hipError_t launch_prepare(const DeviceTables &t, const float *cpts, float *table, uint32_t *cond, int32_t *zero,
+                          int64_t zero_count, hipStream_t stream) {
+    dev::PrepareArgs A;
+    A.segs = t.segs;
+    A.blk_seg = t.blk_seg;
+    A.blk_first = t.blk_first;
+    A.table = table;
+    A.cprog = t.cprog;
+    A.cprog_off = t.cprog_off;
+    A.cblk_prog = t.cblk_prog;
+    A.cblk_first = t.cblk_first;
+    A.cond = cond;
+    A.cpts = cpts;
+    A.zero = zero;
+    A.zero_count = zero_count > 0 ? zero_count : 0;
+    A.n_build = t.n_build_blocks;
+    A.n_cond = t.n_cond_blocks;
+    int64_t nz = A.zero_count > 0 ? (int64_t)blocks_for(A.zero_count, dev::kBlock) : 0;
+    if (nz > 1024) nz = 1024;
+    A.n_zero = (int32_t)nz;
+    const int64_t blocks = (int64_t)A.n_build + A.n_cond + A.n_zero;
+    if (blocks == 0) return hipSuccess;
+    hipLaunchKernelGGL(dev::prepare_step_kernel, dim3((unsigned)blocks), dim3(dev::kBlock), 0, stream, A);
+    return hipGetLastError();
+}
+
+hipError_t launch_moving_sum_gamma(const int32_t *newc, int32_t *mb, int32_t *totals, double alpha, uint32_t key0,
+                                   uint32_t key1, uint32_t update_id, const uint32_t *ids, double *g, int64_t total,
+                                   hipStream_t stream) {
+    if (total <= 0) return hipSuccess;
+    hipLaunchKernelGGL(dev::moving_sum_gamma_kernel, dim3(blocks_for(total, dev::kBlock)), dim3(dev::kBlock), 0,
+                       stream, newc, mb, totals, alpha, key0, key1, update_id, ids, g, total);
     return hipGetLastError();
 }
 

@@ -68,6 +68,11 @@ hipError_t launch_build_tables(const DeviceTables &t, const float *cpts, float *
 hipError_t launch_build_thresholds(const DeviceTables &t, const float *cpts, uint32_t *cond,
                                    hipStream_t stream);
 
+// launch_build_tables, launch_build_thresholds and (zero_count > 0) a clear of
+// zero[0 .. zero_count) in one launch.
+hipError_t launch_prepare(const DeviceTables &t, const float *cpts, float *table, uint32_t *cond, int32_t *zero,
+                          int64_t zero_count, hipStream_t stream);
+
 // Nodes order[begin .. begin+count) of one colour, all of launch class klass
 // (0: fast kernel, tables staged in lds_bytes of LDS; 1: fast kernel, tables
 // in global memory; 2: wide kernel; 3: generic kernel).
@@ -139,6 +144,12 @@ hipError_t launch_gamma(const int32_t *totals, double alpha, uint32_t key0, uint
 hipError_t launch_gamma(const double *totals, double alpha, uint32_t key0, uint32_t key1,
                         uint32_t update_id, const uint32_t *ids, double *g, int64_t total,
                         hipStream_t stream);
+
+// launch_moving_sum (totals non-null) followed by launch_gamma on the
+// updated totals, in one launch.
+hipError_t launch_moving_sum_gamma(const int32_t *newc, int32_t *mb, int32_t *totals, double alpha, uint32_t key0,
+                                   uint32_t key1, uint32_t update_id, const uint32_t *ids, double *g, int64_t total,
+                                   hipStream_t stream);
 
 // ids[0] += d0, ids[1] += d1 (one thread; the last node of a graphed step).
 hipError_t launch_advance_ids(uint32_t *ids, uint32_t d0, uint32_t d1, hipStream_t stream);
