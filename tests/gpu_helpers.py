@@ -49,8 +49,8 @@ def gpu_sweep_both(ctx, states_np, obs_np, theta_np, m, n_cols, col_offset, seed
     """The production sweep (same_sweep) on one copy of the inputs and, when a
     window is asked for, the debug sweep (same_sweep_debug, which also writes
     the conditionals) on another.  The two are separate kernel builds (the
-    production one draws replica pairs at a higher occupancy bound), so each
-    is compared with the oracle on its own.  Returns (production states,
+    production one is compiled for a higher occupancy bound and writes no
+    conditionals), so each is compared with the oracle on its own.  Returns (production states,
     debug states or None, probs or None)."""
     prod, _ = gpu_sweep(ctx, states_np, obs_np, theta_np, m, n_cols, col_offset, seed, sweep_id)
     if win is None:

@@ -59,7 +59,7 @@ def _sweep_case(w, b=0, sweep_id=3, win=None, theta=None, n_threads=0, table_lim
     (3, dict(n_cols=9_000), (8_000, 1000)),              # 100-node random DAG, ragged tail
     (4, {}, (0, 600)),                                   # two-layer concepts, m=20
     (5, dict(n_cols=5_000), (4_600, 400)),               # 1000-node random DAG, m=10
-    (5, dict(n_cols=3_000, m=5), (0, 300)),              # odd m: replica pairs, then one
+    (5, dict(n_cols=3_000, m=5), (0, 300)),              # odd m: a replica quad, then a partial one
     (5, dict(n_cols=2_001, m=7), (1_700, 301)),          # odd m and a ragged tail
 ])
 @pytest.mark.parametrize("table_limit", [None, 0], ids=["tables", "products"])
