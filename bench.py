@@ -132,14 +132,19 @@ def main():
     cols_timed = sum(w.mb_cols(b) for b in mbs)
     hidden = latent / float(net.n * cols_timed)
     del obs_host
+    # the library's replica-quad layout of the timed minibatches (input
+    # preparation, on the device); the generator's row layout stays for the
+    # oracle's sample and the host-side preparations
+    w.pk = {b: same.pack_states(w.states[b]) for b in mbs}
+    torch.cuda.synchronize()
 
     # count-only pre-pass initialises the per-minibatch counts and their sum
     for b in mbs:
-        same.same_counts(ctx, w.states[b], w.m, w.mb_cols(b), w.ld, mb[b], tot, ws)
+        same.same_counts(ctx, w.pk[b], w.m, w.mb_cols(b), w.ld, mb[b], tot, ws)
 
     def one_pass(s):
         for b in mbs:
-            same.same_step(ctx, w.states[b], w.obs[b], cpts, w.m, w.mb_cols(b), w.ld, b * w.nb,
+            same.same_step(ctx, w.pk[b], w.obs[b], cpts, w.m, w.mb_cols(b), w.ld, b * w.nb,
                            w.seed, s, mb[b], tot, s * w.M + b, ws)
 
     for s in range(args.warmup):
@@ -261,7 +266,7 @@ def graph_timing(w, ctx, mbs, cpts, mb, tot, ws, first_pass, passes, dev, stream
     k = per_graph if len(mbs) == 1 else 1
     passes = (passes + k - 1) // k * k
     ids = torch.tensor([[first_pass, first_pass * w.M + b] for b in mbs], dtype=torch.int32, device=dev)
-    graphs = [same.same_step_graph(ctx, w.states[b], w.obs[b], cpts, w.m, w.mb_cols(b), w.ld, b * w.nb, w.seed,
+    graphs = [same.same_step_graph(ctx, w.pk[b], w.obs[b], cpts, w.m, w.mb_cols(b), w.ld, b * w.nb, w.seed,
                                    mb[b], tot, ids[i], w.M, k, ws) for i, b in enumerate(mbs)]
     for g in graphs:
         g.launch(stream)
@@ -366,11 +371,11 @@ def first_sweep_parity(w, ctx, cpts0, ws, sample, cols, dev):
     cols = min(cols, _cols) // 4 * 4
     pre = np.ascontiguousarray(st[:, :, :cols])
     obs = np.ascontiguousarray(ob[:, :cols])
-    d_st = torch.from_numpy(pre).to(dev)
+    d_st = torch.from_numpy(same.pack_states(pre)).to(dev)
     d_ob = torch.from_numpy(obs).to(dev)
     same.same_sweep(ctx, d_st, d_ob, cpts0, w.m, cols, cols, 0, w.seed, 0, ws)
     torch.cuda.synchronize()
-    gpu = d_st.cpu().numpy()
+    gpu = same.unpack_states(d_st.cpu().numpy(), w.m)
     del d_st, d_ob
     ref = pre.copy()
     color = oracle.graph(net.parents, net.card)["color"]
@@ -576,7 +581,7 @@ def ingest_timing(w, ctx, b, dev, stream, reps=5):
     col_idx = cols.to(torch.int32)
     values = w.states[b][:, 0, :nc][known].contiguous()
     del rows, cols, known
-    st = torch.empty_like(w.states[b])
+    st = torch.empty_like(w.pk[b])
     obs = torch.empty_like(ob)
     torch.cuda.synchronize()
 
@@ -630,7 +635,7 @@ def heldout_timing(w, ctx, b, dev, stream, train_steps=60, pred_sweeps=20):
     pptr, pidx, card = net.csr()
     hctx = same.same_create(pptr, pidx, card, h.alpha)
     hws = hctx.new_workspace(dev)
-    st = h.states[0]
+    st = same.pack_states(h.states[0])
     ob = torch.from_numpy(obs_train).to(dev)
     tg = torch.from_numpy(target).to(dev)
     same.same_init_latent(hctx, st, ob, h.m, h.n_cols, h.ld, 0, h.seed + 17)
@@ -661,12 +666,12 @@ def heldout_timing(w, ctx, b, dev, stream, train_steps=60, pred_sweeps=20):
     pick = (torch.rand(w.obs[b].shape, generator=g, device=dev) < 0.2) & (w.obs[b] == 1)
     tgt = torch.where(pick, w.states[b][:, 0, :], torch.full_like(w.states[b][:, 0, :], -1)).contiguous()
     hc = torch.zeros((n, ld), dtype=torch.int32, device=dev)
-    same.same_accumulate_hits(ctx, w.states[b], tgt, m, nc, ld, hc)
+    same.same_accumulate_hits(ctx, w.pk[b], tgt, m, nc, ld, hc)
     torch.cuda.synchronize()
     reps = 5
     e0.record(stream)
     for _ in range(reps):
-        same.same_accumulate_hits(ctx, w.states[b], tgt, m, nc, ld, hc)
+        same.same_accumulate_hits(ctx, w.pk[b], tgt, m, nc, ld, hc)
     e1.record(stream)
     torch.cuda.synchronize()
     t_hits = e0.elapsed_time(e1) / reps
@@ -738,7 +743,7 @@ def m_study_cfg(cfg, dev, stream, steps=200, checkpoints=(10, 25, 50, 100, 150, 
 
     def run(schedule):
         m = schedule(0)
-        st = base.states[0][:, :1, :].expand(-1, m, -1).contiguous() if m > 1 else base.states[0].clone()
+        st = same.pack_states(base.states[0][:, :1, :].expand(-1, m, -1).contiguous())
         cpts = torch.from_numpy(base.init_theta).to(dev)
         mb = torch.zeros(ctx.cpt_total, dtype=torch.int32, device=dev)
         tot = torch.zeros(ctx.cpt_total, dtype=torch.int32, device=dev)
@@ -750,7 +755,7 @@ def m_study_cfg(cfg, dev, stream, steps=200, checkpoints=(10, 25, 50, 100, 150, 
             e0.record(stream)
             m2 = schedule(s)
             if m2 != m:  # anneal: more replicas, then the counts over all of them
-                grown = torch.empty((net.n, m2, ld), dtype=st.dtype, device=dev)
+                grown = torch.empty(same.state_shape(net.n, m2, ld), dtype=st.dtype, device=dev)
                 same.same_grow_replicas(ctx, st, m, grown, m2, ld)
                 st, m = grown, m2
                 mb.zero_()
@@ -792,12 +797,12 @@ def stream_timing(w, ctx, cpts, ws, dev, steps):
     net = w.net
     host_ld = (w.n_cols + 3) // 4 * 4
     t0 = time.time()
-    hs = torch.empty((net.n, w.m, host_ld), dtype=w.states[0].dtype, pin_memory=True)
+    hs = torch.empty(same.state_shape(net.n, w.m, host_ld), dtype=w.states[0].dtype, pin_memory=True)
     ho = torch.empty((net.n, host_ld), dtype=torch.uint8, pin_memory=True)
     for b in range(w.M):
         c0, nc = b * w.nb, w.mb_cols(b)
         for i in range(net.n):
-            hs[i, :, c0:c0 + nc].copy_(w.states[b][i, :, :nc])
+            hs[i, :, c0:c0 + nc, :].copy_(w.pk[b][i, :, :nc, :])
             ho[i, c0:c0 + nc].copy_(w.obs[b][i, :nc])
     torch.cuda.synchronize()
     log("pinned host copy of the data (%.1f GB) in %.1f s" % (
@@ -817,7 +822,7 @@ def stream_timing(w, ctx, cpts, ws, dev, steps):
     torch.cuda.synchronize()
     dt = time.perf_counter() - t
     ns = float(net.n) * w.n_cols * w.m * steps
-    state_bytes = float(net.n) * w.m * w.n_cols * hs.element_size()
+    state_bytes = float(net.n) * 4 * ((w.m + 3) // 4) * w.n_cols * hs.element_size()  # padding slots included
     h2d = state_bytes + float(net.n) * w.n_cols
     log("streamed %d passes in %.3f s" % (steps, dt))
     # the same passes with the exponential moving sum of the counts (Sec. 4

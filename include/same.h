@@ -24,11 +24,18 @@
  * CPTs:   one flat fp32 array of cpt_total entries; node i owns
  *         [cpt_off[i], cpt_off[i+1]) = R_i rows of K_i entries, entry
  *         cpt_off[i] + u*K_i + k = P(x_i = k | parents in configuration u).
- * States: device array [n][m][ld] of int8 (every K_i <= 127) or int16
- *         (some K_i >= 128), node-major, then replica, then column; column j
- *         of a minibatch is global column col_offset + j.  Observed entries
- *         must hold the observed value in every replica.  Values must lie in
- *         [0, K_i) (out-of-range values are undefined behaviour).
+ * States: device array [n][mq][ld][4] of int8 (every K_i <= 127) or int16
+ *         (some K_i >= 128), mq = ceil(m / 4): replica r of node i at
+ *         minibatch column j, written states[i][r][j] below, is element
+ *         ((i * mq + r / 4) * ld + j) * 4 + r % 4.  The four replicas
+ *         4q .. 4q + 3 of one column (a state quad) are adjacent, so the
+ *         sweep reads and writes them with one access.  Column j of a
+ *         minibatch is global column col_offset + j.  Observed entries must
+ *         hold the observed value in every replica.  Values must lie in
+ *         [0, K_i) (out-of-range values are undefined behaviour).  Slots
+ *         r >= m of the last quad are padding and may hold anything: the
+ *         sweep reads them as state 0 and writes valid draws there, and
+ *         counts, hits and replica growth skip them.
  * Obs:    device array [n][ld] of uint8, 1 = observed, 0 = latent; shared by
  *         the m replicas.  Columns [n_cols, ld) are never drawn or counted.
  * Counts: int32, laid out like the CPTs.
@@ -169,7 +176,8 @@ int same_workspace_size(const same_ctx *ctx, size_t *bytes);
  * integer thresholds ceil(2^24 S_k / Z) precomputed in fp64 for every blanket
  * configuration; the others multiply fp32 CPT entries (relative error below
  * (1 + children) * 2^-24 per weight) at every draw.
- * states [n][m][ld] (in/out), obs [n][ld], cpts [cpt_total]: device pointers.
+ * states (in/out, the layout above), obs [n][ld], cpts [cpt_total]: device
+ * pointers.
  * col_offset and ld must be multiples of 4 and states/obs 4-byte aligned.
  * seed and sweep_id select the Philox stream.  The colour groups launch in
  * order on `stream`.  Inside a group, the nodes whose tables are read from
@@ -217,7 +225,7 @@ int same_debug_thresholds(same_ctx *ctx, const float *cpts, int64_t *node_off, i
 /*
  * Sufficient statistics and their moving sum (Sec. 4): histogram of
  * (parent configuration, state) over columns [0, n_cols) and all m replicas of
- * states [n][m][ld].  mb_counts [cpt_total] holds this minibatch's previous
+ * states (the layout above).  mb_counts [cpt_total] holds this minibatch's previous
  * counts on entry (zeros on its first visit) and its new counts on return;
  * totals [cpt_total] (nullable) += new - previous.  Device pointers.  Counts
  * are exact (integer) and independent of launch order; n_cols * m * (number
@@ -280,7 +288,7 @@ int same_step(same_ctx *ctx, void *states, const uint8_t *obs, float *cpts, int3
  * device and streams the data; Sec. 6: the GPU's memory, not the data size,
  * limits the problem).  The data stay in host memory -- pinned (page-locked)
  * for the copies to overlap -- laid out like a device minibatch but with the
- * full column range: states [n][m][host_ld], obs [n][host_ld], column j is
+ * full column range: states [n][mq][host_ld][4], obs [n][host_ld], column j is
  * global column j.  Minibatch b covers columns [b*nb, min((b+1)*nb, n_cols)).
  *
  * same_stream_pass runs one pass over all M = ceil(n_cols / nb) minibatches:
@@ -437,11 +445,12 @@ int same_predict(same_ctx *ctx, void *states, const uint8_t *obs, const float *c
 
 /*
  * SAME annealing (Sec. 3: the replication factor m acts as a temperature and
- * can be raised during sampling to anneal the sampler): copies states
- * [n][m][ld] into dst [n][m2][ld], m2 >= m.  Replica r < m is copied and
- * replica r >= m starts as a copy of replica r mod m, a valid state of the
- * enlarged SAME joint (every copy agrees with the known data).  All ld columns
- * are copied.  After growing, the counts of the minibatch must be recomputed
+ * can be raised during sampling to anneal the sampler): copies states (m
+ * replicas) into dst (m2 >= m replicas), both in the state layout with
+ * leading dimension ld.  Replica r < m is copied and replica r >= m starts as
+ * a copy of replica r mod m, a valid state of the enlarged SAME joint (every
+ * copy agrees with the known data); dst's padding slots follow the same rule.
+ * All ld columns are copied.  After growing, the counts of the minibatch must be recomputed
  * over the m2 replicas (same_counts with zeroed previous counts, or the
  * count-only pre-pass).  Device pointers owned by the caller; states and dst
  * must not overlap.  Errors: SAME_EINVAL (null, m2 < m, overlap), SAME_EALIGN,

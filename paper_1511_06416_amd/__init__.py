@@ -23,6 +23,7 @@ __all__ = [
     "same_accumulate_hits", "same_predict", "same_counts_ema", "same_sample_cpts_ema", "same_stream_pass_ema",
     "same_grow_replicas", "same_debug_thresholds", "same_counts_noalloc", "same_stream_compact_layout",
     "same_stream_pass_compact", "same_step_graph", "same_graph_launch", "same_graph_destroy", "StepGraph",
+    "pack_states", "unpack_states", "state_shape",
     "library_path", "load_library",
 ]
 
@@ -140,6 +141,56 @@ def _ptr(t):
     return C.c_void_p(t.data_ptr())
 
 
+def state_shape(n, m, ld):
+    """Shape of a states array of n nodes, m replicas and leading dimension
+    ld: replica quads [n][ceil(m / 4)][ld][4] (see include/same.h)."""
+    return (int(n), (int(m) + 3) // 4, int(ld), 4)
+
+
+def pack_states(states):
+    """[n][m][ld] (replica rows) -> the library's [n][ceil(m/4)][ld][4]
+    (replica quads, padding slots 0).  torch tensor (same device) or numpy
+    array; a layout permutation for callers, not part of any entry point."""
+    n, m, ld = states.shape
+    mq = (m + 3) // 4
+    pad = 4 * mq - m
+    if isinstance(states, np.ndarray):
+        if pad:
+            states = np.concatenate([states, np.zeros((n, pad, ld), dtype=states.dtype)], axis=1)
+        return np.ascontiguousarray(states.reshape(n, mq, 4, ld).transpose(0, 1, 3, 2))
+    if pad:
+        states = torch_cat([states, states.new_zeros((n, pad, ld))], 1)
+    return states.reshape(n, mq, 4, ld).permute(0, 1, 3, 2).contiguous()
+
+
+def unpack_states(quads, m):
+    """The library's [n][mq][ld][4] -> [n][m][ld] (padding slots dropped)."""
+    n, mq, ld, four = quads.shape
+    assert four == 4 and 4 * mq >= m
+    if isinstance(quads, np.ndarray):
+        return np.ascontiguousarray(quads.transpose(0, 1, 3, 2).reshape(n, 4 * mq, ld)[:, :m])
+    return quads.permute(0, 1, 3, 2).reshape(n, 4 * mq, ld)[:, :m].contiguous()
+
+
+def torch_cat(ts, dim):
+    import torch
+    return torch.cat(ts, dim)
+
+
+def _st(ctx, t, m, ld, what="states"):
+    """A states tensor must have the library's layout and be contiguous: a
+    tensor in another layout is refused here, before any device call."""
+    if t is None or isinstance(t, int):
+        return t
+    want = state_shape(ctx.n_nodes, m, ld)
+    if tuple(t.shape) != want:
+        raise SameError(SAME_EINVAL, "%s must have shape %s ([n][ceil(m/4)][ld][4], see pack_states), got %s"
+                        % (what, want, tuple(t.shape)))
+    if hasattr(t, "is_contiguous") and not t.is_contiguous():
+        raise SameError(SAME_EINVAL, "%s must be contiguous" % what)
+    return t
+
+
 def _stream(stream):
     if stream is None:
         import torch
@@ -232,21 +283,21 @@ def same_workspace_size(ctx: Context) -> int:
 
 def same_sweep(ctx, states, obs, cpts, m, n_cols, ld, col_offset, seed, sweep_id, workspace,
                stream=None):
-    _check(load_library().same_sweep(ctx.handle, _ptr(states), _ptr(obs), _ptr(cpts), int(m),
+    _check(load_library().same_sweep(ctx.handle, _ptr(_st(ctx, states, m, ld)), _ptr(obs), _ptr(cpts), int(m),
                                      int(n_cols), int(ld), int(col_offset), int(seed),
                                      int(sweep_id), _ptr(workspace), _stream(stream)))
 
 
 def same_sweep_debug(ctx, states, obs, cpts, m, n_cols, ld, col_offset, seed, sweep_id,
                      win_begin, win, probs, workspace, stream=None):
-    _check(load_library().same_sweep_debug(ctx.handle, _ptr(states), _ptr(obs), _ptr(cpts), int(m),
+    _check(load_library().same_sweep_debug(ctx.handle, _ptr(_st(ctx, states, m, ld)), _ptr(obs), _ptr(cpts), int(m),
                                            int(n_cols), int(ld), int(col_offset), int(seed),
                                            int(sweep_id), int(win_begin), int(win), _ptr(probs),
                                            _ptr(workspace), _stream(stream)))
 
 
 def same_counts(ctx, states, m, n_cols, ld, mb_counts, totals, workspace, stream=None):
-    _check(load_library().same_counts(ctx.handle, _ptr(states), int(m), int(n_cols), int(ld),
+    _check(load_library().same_counts(ctx.handle, _ptr(_st(ctx, states, m, ld)), int(m), int(n_cols), int(ld),
                                       _ptr(mb_counts), _ptr(totals), _ptr(workspace),
                                       _stream(stream)))
 
@@ -254,7 +305,7 @@ def same_counts(ctx, states, m, n_cols, ld, mb_counts, totals, workspace, stream
 def same_counts_noalloc(ctx, states, m, n_cols, ld, mb_counts, totals, stream=None):
     """same_counts without a workspace: the histogram lives in the library's
     per-device scratch array (see include/same.h)."""
-    _check(load_library().same_counts_noalloc(ctx.handle, _ptr(states), int(m), int(n_cols), int(ld),
+    _check(load_library().same_counts_noalloc(ctx.handle, _ptr(_st(ctx, states, m, ld)), int(m), int(n_cols), int(ld),
                                               _ptr(mb_counts), _ptr(totals), _stream(stream)))
 
 
@@ -265,7 +316,7 @@ def same_sample_cpts(ctx, totals, cpts_out, seed, update_id, workspace, stream=N
 
 def same_step(ctx, states, obs, cpts, m, n_cols, ld, col_offset, seed, sweep_id, mb_counts, totals,
               update_id, workspace, stream=None):
-    _check(load_library().same_step(ctx.handle, _ptr(states), _ptr(obs), _ptr(cpts), int(m),
+    _check(load_library().same_step(ctx.handle, _ptr(_st(ctx, states, m, ld)), _ptr(obs), _ptr(cpts), int(m),
                                     int(n_cols), int(ld), int(col_offset), int(seed), int(sweep_id),
                                     _ptr(mb_counts), _ptr(totals), int(update_id), _ptr(workspace),
                                     _stream(stream)))
@@ -299,7 +350,7 @@ def same_step_graph(ctx, states, obs, cpts, m, n_cols, ld, col_offset, seed, mb_
     from the two-word device tensor `ids` (advanced by 1 and update_stride
     after each step); returns a StepGraph."""
     h = C.c_void_p()
-    _check(load_library().same_step_graph(ctx.handle, _ptr(states), _ptr(obs), _ptr(cpts), int(m), int(n_cols),
+    _check(load_library().same_step_graph(ctx.handle, _ptr(_st(ctx, states, m, ld)), _ptr(obs), _ptr(cpts), int(m), int(n_cols),
                                           int(ld), int(col_offset), int(seed), _ptr(mb_counts), _ptr(totals),
                                           _ptr(ids), int(update_stride), int(steps), _ptr(workspace),
                                           C.byref(h)))
@@ -331,7 +382,7 @@ def same_stream_slots_size(ctx, m, nb) -> int:
 def same_stream_pass(ctx, host_states, host_obs, host_ld, n_cols, nb, m, cpts, mb_counts, totals,
                      seed, pass_id, flags, slots, workspace, stream=None):
     """host_states / host_obs: pinned host tensors (or addresses); the rest device."""
-    _check(load_library().same_stream_pass(ctx.handle, _ptr(host_states), _ptr(host_obs),
+    _check(load_library().same_stream_pass(ctx.handle, _ptr(_st(ctx, host_states, m, host_ld, "host_states")), _ptr(host_obs),
                                            int(host_ld), int(n_cols), int(nb), int(m), _ptr(cpts),
                                            _ptr(mb_counts), _ptr(totals), int(seed), int(pass_id),
                                            int(flags), _ptr(slots), _ptr(workspace),
@@ -355,29 +406,29 @@ def same_kernel_times(ctx):
 
 def same_expand_observed(ctx, row_ptr, col_idx, values, nnz, m, n_cols, ld, states, obs, stream=None):
     _check(load_library().same_expand_observed(ctx.handle, _ptr(row_ptr), _ptr(col_idx), _ptr(values),
-                                               int(nnz), int(m), int(n_cols), int(ld), _ptr(states),
+                                               int(nnz), int(m), int(n_cols), int(ld), _ptr(_st(ctx, states, m, ld)),
                                                _ptr(obs), _stream(stream)))
 
 
 def same_init_latent(ctx, states, obs, m, n_cols, ld, col_offset, seed, stream=None):
-    _check(load_library().same_init_latent(ctx.handle, _ptr(states), _ptr(obs), int(m), int(n_cols),
+    _check(load_library().same_init_latent(ctx.handle, _ptr(_st(ctx, states, m, ld)), _ptr(obs), int(m), int(n_cols),
                                            int(ld), int(col_offset), int(seed), _stream(stream)))
 
 
 def same_accumulate_hits(ctx, states, target, m, n_cols, ld, hits, stream=None):
-    _check(load_library().same_accumulate_hits(ctx.handle, _ptr(states), _ptr(target), int(m), int(n_cols),
+    _check(load_library().same_accumulate_hits(ctx.handle, _ptr(_st(ctx, states, m, ld)), _ptr(target), int(m), int(n_cols),
                                                int(ld), _ptr(hits), _stream(stream)))
 
 
 def same_predict(ctx, states, obs, cpts, target, m, n_cols, ld, col_offset, seed, sweep_id0, n_sweeps, hits,
                  workspace, stream=None):
-    _check(load_library().same_predict(ctx.handle, _ptr(states), _ptr(obs), _ptr(cpts), _ptr(target), int(m),
+    _check(load_library().same_predict(ctx.handle, _ptr(_st(ctx, states, m, ld)), _ptr(obs), _ptr(cpts), _ptr(target), int(m),
                                        int(n_cols), int(ld), int(col_offset), int(seed), int(sweep_id0),
                                        int(n_sweeps), _ptr(hits), _ptr(workspace), _stream(stream)))
 
 
 def same_counts_ema(ctx, states, m, n_cols, ld, decay, totals, workspace, stream=None):
-    _check(load_library().same_counts_ema(ctx.handle, _ptr(states), int(m), int(n_cols), int(ld), float(decay),
+    _check(load_library().same_counts_ema(ctx.handle, _ptr(_st(ctx, states, m, ld)), int(m), int(n_cols), int(ld), float(decay),
                                           _ptr(totals), _ptr(workspace), _stream(stream)))
 
 
@@ -389,14 +440,14 @@ def same_sample_cpts_ema(ctx, totals, cpts_out, seed, update_id, workspace, stre
 def same_stream_pass_ema(ctx, host_states, host_obs, host_ld, n_cols, nb, m, cpts, totals, decay, seed, pass_id,
                          flags, slots, workspace, stream=None):
     """host_states / host_obs: pinned host tensors (or addresses); the rest device (totals fp64)."""
-    _check(load_library().same_stream_pass_ema(ctx.handle, _ptr(host_states), _ptr(host_obs), int(host_ld),
+    _check(load_library().same_stream_pass_ema(ctx.handle, _ptr(_st(ctx, host_states, m, host_ld, "host_states")), _ptr(host_obs), int(host_ld),
                                                int(n_cols), int(nb), int(m), _ptr(cpts), _ptr(totals),
                                                float(decay), int(seed), int(pass_id), int(flags), _ptr(slots),
                                                _ptr(workspace), _stream(stream)))
 
 
 def same_grow_replicas(ctx, states, m, dst, m2, ld, stream=None):
-    _check(load_library().same_grow_replicas(ctx.handle, _ptr(states), int(m), _ptr(dst), int(m2), int(ld),
+    _check(load_library().same_grow_replicas(ctx.handle, _ptr(_st(ctx, states, m, ld)), int(m), _ptr(_st(ctx, dst, m2, ld, "dst")), int(m2), int(ld),
                                              _stream(stream)))
 
 

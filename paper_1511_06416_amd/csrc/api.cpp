@@ -27,6 +27,13 @@ constexpr int64_t kCompactChunkCols = 1024;  // columns per block of the compact
 
 inline size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
+// States are stored as replica quads, [n][mq][ld][4] with mq = ceil(m / 4):
+// one node's block holds mq * ld * 4 states.
+inline int64_t replica_quads(int32_t m) { return ((int64_t)m + 3) / 4; }
+inline double node_state_bytes(int32_t m, int64_t ld, int32_t sb) {
+    return (double)replica_quads(m) * 4.0 * (double)ld * (double)sb;
+}
+
 }  // namespace
 
 // Copy streams and events of the out-of-core passes, per device.
@@ -226,9 +233,9 @@ int check_minibatch(const same_ctx *ctx, const void *states, int32_t m, int64_t 
     if (ld % 4 != 0) return set_error(SAME_EALIGN, "ld must be a multiple of 4");
     if (!aligned(states, 4 * (size_t)ctx->g.state_bytes))
         return set_error(SAME_EALIGN, "states must be aligned to 4 state elements");
-    if ((double)m * (double)ld * ctx->g.state_bytes >= 2147483648.0)
-        return set_error(SAME_ESIZE, "one node's replica block m * ld must stay below 2^31 bytes");
-    if ((double)ctx->g.n * (double)m * (double)ld * ctx->g.state_bytes > 9.0e18)
+    if (node_state_bytes(m, ld, ctx->g.state_bytes) >= 2147483648.0)
+        return set_error(SAME_ESIZE, "one node's state quads (4 * ceil(m / 4) * ld states) must stay below 2^31 bytes");
+    if ((double)ctx->g.n * node_state_bytes(m, ld, ctx->g.state_bytes) > 9.0e18)
         return set_error(SAME_ESIZE, "states array too large");
     return SAME_OK;
 }
@@ -240,7 +247,7 @@ int check_minibatch(const same_ctx *ctx, const void *states, int32_t m, int64_t 
 // cost more than the cache saves, so the default is one tile.
 int64_t tile_cols(const same_ctx *ctx, int32_t m, int64_t n_cols) {
     if (ctx->tile_bytes <= 0.0) return n_cols;
-    const double per_col = (double)ctx->g.n * ((double)m * ctx->g.state_bytes + 1.0);
+    const double per_col = (double)ctx->g.n * (4.0 * (double)replica_quads(m) * ctx->g.state_bytes + 1.0);
     int64_t t = (int64_t)(ctx->tile_bytes / per_col) / 1024 * 1024;
     if (t < 1024) t = 1024;
     return t >= n_cols ? n_cols : t;
@@ -302,7 +309,7 @@ int prepare_sweep(same_ctx *ctx, same::DeviceTables *t, void *states, const uint
 int sweep_tile(same_ctx *ctx, const same::SweepParams &P0, int64_t t0, int64_t nt, hipStream_t s) {
     const same::Compiled &g = ctx->g;
     same::SweepParams P = P0;
-    P.states = (char *)P0.states + t0 * g.state_bytes;
+    P.states = (char *)P0.states + t0 * 4 * g.state_bytes;  // column t0 of every quad row
     P.obs = P0.obs + t0;
     P.n_cols = nt;
     P.col_offset = P0.col_offset + t0;
@@ -463,7 +470,7 @@ struct SlotGeom {
 SlotGeom slot_geom(const same_ctx *ctx, int32_t m, int64_t nb) {
     SlotGeom s;
     s.ld = (nb + 63) / 64 * 64;
-    s.states = align_up((size_t)ctx->g.n * (size_t)m * (size_t)s.ld * ctx->g.state_bytes);
+    s.states = align_up((size_t)ctx->g.n * (size_t)node_state_bytes(m, s.ld, ctx->g.state_bytes));
     s.bytes = s.states + align_up((size_t)ctx->g.n * (size_t)s.ld);
     return s;
 }
@@ -699,8 +706,8 @@ int stream_pass_impl(same_ctx *ctx, void *host_states, const uint8_t *host_obs, 
     int rc = stream_res_for_current_device(ctx, &sr);
     if (rc) return rc;
     hipStream_t cs = (hipStream_t)stream;
-    const size_t sb = (size_t)ctx->g.state_bytes;
-    const int64_t rows = (int64_t)ctx->g.n * m;
+    const size_t sb = 4 * (size_t)ctx->g.state_bytes;  // bytes of one column of a quad row
+    const int64_t rows = (int64_t)ctx->g.n * replica_quads(m);
     const int64_t M = (n_cols + nb - 1) / nb;
     for (int64_t b = 0; b < M; ++b) {
         const int s = (int)(b & 1);
@@ -972,10 +979,11 @@ extern "C" int same_grow_replicas(same_ctx *ctx, const void *states, int32_t m, 
     if (rc) return rc;
     if (m2 < m) return set_error(SAME_EINVAL, "m2 must be >= m");
     const char *a = (const char *)states, *b = (const char *)dst;
-    const size_t sb = (size_t)ctx->g.state_bytes;
-    if (a < b + (size_t)ctx->g.n * m2 * ld * sb && b < a + (size_t)ctx->g.n * m * ld * sb)
+    const int32_t sb = ctx->g.state_bytes;
+    if (a < b + (size_t)(ctx->g.n * node_state_bytes(m2, ld, sb)) &&
+        b < a + (size_t)(ctx->g.n * node_state_bytes(m, ld, sb)))
         return set_error(SAME_EINVAL, "states and dst must not overlap");
-    return check_hip(same::launch_grow(states, m, dst, m2, ctx->g.n, ld * (int64_t)sb, (hipStream_t)stream),
+    return check_hip(same::launch_grow(states, m, dst, m2, ctx->g.n, ld, sb, (hipStream_t)stream),
                      "replica growth launch");
 }
 

@@ -32,6 +32,22 @@ constexpr int kSweepBlock = 256;     // threads of a sweep block
 constexpr int kSweepWaves = 5;       // waves per SIMD the fast sweep kernel is compiled for
 
 // ---------------------------------------------------------------- state quads
+//
+// States are stored as replica quads: states[n][mq][ld][4] with mq = ceil(m/4),
+// so that replica r of node i at column j is element
+// ((i * mq + r / 4) * ld + j) * 4 + r % 4.  The four replicas 4 rq .. 4 rq + 3
+// of one column -- a state quad, slots 0..3 -- are adjacent (4 bytes for int8,
+// 8 for int16) and travel in one load or store.  Slots >= m of the last quad
+// are padding.
+
+// Elements per node: mq quads of ld columns.
+__device__ __forceinline__ int64_t node_stride(int32_t m, int64_t ld) { return (int64_t)((m + 3) >> 2) * ld * 4; }
+
+// Byte offset of quad rq at column j inside a node's block.
+template <typename ST>
+__device__ __forceinline__ uint32_t quad_boff(int rq, int64_t ld, int64_t j) {
+    return (uint32_t)(((int64_t)rq * ld + j) * 4 * (int64_t)sizeof(ST));
+}
 
 template <typename ST>
 struct Quad;
@@ -44,15 +60,20 @@ struct Quad<int8_t> {
         return __builtin_amdgcn_raw_buffer_load_b32(r, (int)boff, 0, 0);
     }
     __device__ static void store(int8_t *p, V v) { *reinterpret_cast<uint32_t *>(p) = v; }
+    __device__ static void store_buffer(__amdgpu_buffer_rsrc_t r, uint32_t boff, V v) {
+        __builtin_amdgcn_raw_buffer_store_b32(v, r, (int)boff, 0, 0);
+    }
+    // the same state in all four slots
+    __device__ static V splat(int x) { return (uint32_t)(x & 0xff) * 0x01010101u; }
     __device__ static int get(V v, int c) { return (int)((v >> (8 * c)) & 0xffu); }
     __device__ static V put(V v, int c, int x) {
-        return (v & ~(0xffu << (8 * c))) | ((uint32_t)x << (8 * c));
+        return (v & ~(0xffu << (8 * c))) | ((uint32_t)(x & 0xff) << (8 * c));
     }
-    // keeps the first nvalid (1..4) columns, zeroes the rest
+    // keeps the first nvalid (1..4) slots, zeroes the rest
     __device__ static V keep(V v, int nvalid) {
         return nvalid >= 4 ? v : (v & ((1u << (8 * nvalid)) - 1u));
     }
-    // the 4 states as 16-bit lanes: p[0] = columns (0, 2), p[1] = (1, 3)
+    // the 4 states as 16-bit lanes: p[0] = slots (0, 2), p[1] = (1, 3)
     __device__ static void split(V v, uint32_t (&p)[2]) {
         p[0] = v & 0x00ff00ffu;
         p[1] = __builtin_amdgcn_perm(0u, v, 0x0c030c01u);
@@ -72,14 +93,23 @@ struct Quad<int16_t> {
         return make_uint2(v.x, v.y);
     }
     __device__ static void store(int16_t *p, V v) { *reinterpret_cast<uint2 *>(p) = v; }
+    __device__ static void store_buffer(__amdgpu_buffer_rsrc_t r, uint32_t boff, V v) {
+        typedef uint32_t w2 __attribute__((ext_vector_type(2)));
+        const w2 x = {v.x, v.y};
+        __builtin_amdgcn_raw_buffer_store_b64(x, r, (int)boff, 0, 0);
+    }
+    __device__ static V splat(int x) {
+        const uint32_t h = (uint32_t)(x & 0xffff) * 0x10001u;
+        return make_uint2(h, h);
+    }
     __device__ static int get(V v, int c) {
         const uint32_t w = c < 2 ? v.x : v.y;
         return (int)((w >> (16 * (c & 1))) & 0xffffu);
     }
     __device__ static V put(V v, int c, int x) {
         const uint32_t sh = 16 * (c & 1);
-        if (c < 2) v.x = (v.x & ~(0xffffu << sh)) | ((uint32_t)x << sh);
-        else v.y = (v.y & ~(0xffffu << sh)) | ((uint32_t)x << sh);
+        if (c < 2) v.x = (v.x & ~(0xffffu << sh)) | ((uint32_t)(x & 0xffff) << sh);
+        else v.y = (v.y & ~(0xffffu << sh)) | ((uint32_t)(x & 0xffff) << sh);
         return v;
     }
     __device__ static V keep(V v, int nvalid) {
@@ -92,7 +122,7 @@ struct Quad<int16_t> {
         }
         return v;
     }
-    // the 4 states as 16-bit lanes: p[0] = columns (0, 1), p[1] = (2, 3)
+    // the 4 states as 16-bit lanes: p[0] = slots (0, 1), p[1] = (2, 3)
     __device__ static void split(V v, uint32_t (&p)[2]) {
         p[0] = v.x;
         p[1] = v.y;
@@ -125,8 +155,8 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void *base, 
                                              kBufferWord3);
 }
 
-// State quad of row `node` (n_bytes = m * ld * sizeof(state) < 2^31) at the
-// lane's byte offset.
+// State quad of node `node` (its block of vstride elements, under 2^31 bytes)
+// at the lane's byte offset.
 template <typename ST>
 __device__ __forceinline__ typename Quad<ST>::V load_row(const ST *__restrict__ states, int32_t node,
                                                          int64_t vstride, uint32_t lane_boff) {
@@ -293,8 +323,8 @@ __device__ __forceinline__ void renorm(float (&w)[KP]) {
 }
 
 // Same conditional from the wide list (32-bit float offsets, any record
-// size): wide kernel, table-mode debug output.  Columns >= nvalid read their
-// states as 0.
+// size) for the four slots of a state quad: wide kernel, table-mode debug
+// output.  Slots >= nvalid read their states as 0.
 template <int KP, typename ST, bool RESCALE>
 __device__ __forceinline__ void wide_product(cint32_t *g, int n_groups, const float *__restrict__ tab,
                                              const ST *__restrict__ states, int64_t vstride,
@@ -380,7 +410,7 @@ constexpr uint32_t kXcds = 8;
 constexpr int kSweepQuadsPerLane = 1;  // column quads per lane in one sweep block
 constexpr int kMinSweepBlocks = 4096;  // replicas are split below this many blocks
 constexpr int64_t kMinSweepQuads = 64;  // narrowest column chunk of a fast sweep block (quads)
-constexpr int kCountQuadsPerLane = 4;  // adjacent column quads per lane in one count block
+constexpr int kCountQuadsPerLane = 4;  // adjacent columns (state quads) per lane and iteration of a count block
 
 __device__ __forceinline__ void decode_block(uint32_t b, uint32_t count, uint32_t &local,
                                              int64_t &slab) {
@@ -441,13 +471,6 @@ __device__ __forceinline__ Philox4 gibbs_block(const SweepParams &P, int node, i
                          P.key1);
 }
 
-// The Gibbs uniform word of one (node, replica r, minibatch column j).
-__device__ __forceinline__ uint32_t gibbs_word(const SweepParams &P, int node, int r, int64_t j) {
-    const Philox4 b = gibbs_block(P, node, r >> 2, j);
-    const int c = r & 3;
-    return c == 0 ? b.w[0] : c == 1 ? b.w[1] : c == 2 ? b.w[2] : b.w[3];
-}
-
 __device__ __forceinline__ float uniform24(uint32_t word) { return (float)(word >> 8) * 0x1p-24f; }
 
 // ------------------------------------------------------- sweep items
@@ -457,83 +480,71 @@ __device__ __forceinline__ float uniform24(uint32_t word) { return (float)(word 
 // end of the replica range).  All four draws of an item are latent -- the
 // obs mask is shared by the replicas -- so no lane computes a conditional
 // that nobody draws, and one Philox block gives the item's four uniforms.
-// Replica slot c of an item reads row (node, 4 rq + c) at column j; the four
-// slots' states are packed as two words of 16-bit lanes, slots (0, 2) and
-// (1, 3), for the v_pk_mad_u16 index arithmetic.
+// The item's four states of any blanket node are one state quad (4 or 8
+// bytes at quad_boff(rq, j)), read with one load and split into two words of
+// 16-bit lanes (Quad<ST>::split) for the v_pk_mad_u16 index arithmetic.
+// Padding slots of a partial quad (replicas >= m) are masked to state 0
+// before use, so every index stays inside the node's tables whatever they
+// hold; the item's store writes their draws back (valid states).
 
-// Packed index of replica slot c.
-__device__ __forceinline__ uint32_t slot_index(const uint32_t (&Pk)[2], int c) {
-    const uint32_t v = Pk[c & 1];
-    return (c >> 1) ? v >> 16 : v & 0xffffu;
-}
-
-template <typename ST>
-__device__ __forceinline__ uint32_t load_state(__amdgpu_buffer_rsrc_t r, uint32_t boff) {
-    if constexpr (sizeof(ST) == 1) return (uint32_t)__builtin_amdgcn_raw_buffer_load_b8(r, (int)boff, 0, 0);
-    else return (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(r, (int)boff, 0, 0);
-}
-
-template <typename ST>
-__device__ __forceinline__ void store_state(__amdgpu_buffer_rsrc_t r, uint32_t boff, int x) {
-    if constexpr (sizeof(ST) == 1) __builtin_amdgcn_raw_buffer_store_b8((uint8_t)x, r, (int)boff, 0, 0);
-    else __builtin_amdgcn_raw_buffer_store_b16((uint16_t)x, r, (int)boff, 0, 0);
-}
-
-// Buffer resource over node `node`'s m replica rows (offsets past them read 0).
+// Buffer resource over node `node`'s state quads (offsets past them read 0).
 template <typename ST>
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t node_rsrc(const ST *states, int32_t node, int64_t vstride) {
     return buffer_rsrc(states + (int64_t)node * vstride, (uint32_t)(vstride * (int64_t)sizeof(ST)));
 }
 
-constexpr int kItemBatch = 4;  // blanket entries whose 4 replica loads are in flight together
+constexpr int kItemBatch = 4;  // blanket entries whose state quads are in flight together
 
 // Adds the N entries (node, mult) at e to the item's packed index: every
-// entry's four replica states are loaded before the first is used.
+// entry's state quad is loaded before the first is used; slots >= nrep read 0.
 template <int N, typename ST>
 __device__ __forceinline__ void item_entries(cint32_t *e, const ST *__restrict__ states, int64_t vstride,
-                                             const uint32_t (&boff)[4], uint32_t (&Pk)[2]) {
-    uint32_t v[N][4];
+                                             uint32_t qoff, int nrep, uint32_t (&Pk)[2]) {
+    using Q = Quad<ST>;
+    typename Q::V v[N];
 #pragma unroll
-    for (int t = 0; t < N; ++t) {
-        const __amdgpu_buffer_rsrc_t r = node_rsrc<ST>(states, e[2 * t], vstride);
-#pragma unroll
-        for (int c = 0; c < 4; ++c) v[t][c] = load_state<ST>(r, boff[c]);
-    }
+    for (int t = 0; t < N; ++t) v[t] = Q::load_buffer(node_rsrc<ST>(states, e[2 * t], vstride), qoff);
 #pragma unroll
     for (int t = 0; t < N; ++t) {
         const uint32_t mult = (uint32_t)e[2 * t + 1];
-        Pk[0] = pk_mad_u16(v[t][0] | (v[t][2] << 16), mult, Pk[0]);
-        Pk[1] = pk_mad_u16(v[t][1] | (v[t][3] << 16), mult, Pk[1]);
+        uint32_t p[2];
+        Q::split(Q::keep(v[t], nrep), p);
+        Pk[0] = pk_mad_u16(p[0], mult, Pk[0]);
+        Pk[1] = pk_mad_u16(p[1], mult, Pk[1]);
     }
 }
 
-// Packed index of one group of a fast list for an item; advances g.
+// Packed index of one group of a fast list for an item; advances g.  The
+// scheduling barrier keeps the compiler from hoisting the next group's loads
+// above this group's use of its own (which needs more registers than the
+// occupancy bound allows).
 template <typename ST>
 __device__ __forceinline__ void item_group(cint32_t *&g, const ST *__restrict__ states, int64_t vstride,
-                                           const uint32_t (&boff)[4], uint32_t (&Pk)[2]) {
+                                           uint32_t qoff, int nrep, uint32_t (&Pk)[2]) {
+    __builtin_amdgcn_sched_barrier(0);
     int n_e = g[0];
     Pk[0] = Pk[1] = (uint32_t)g[1];
     cint32_t *e = g + 2;
     g += 2 + 2 * n_e;
     for (; n_e > 0; n_e -= kItemBatch, e += 2 * kItemBatch) {
         switch (n_e < kItemBatch ? n_e : kItemBatch) {
-        case 1: item_entries<1, ST>(e, states, vstride, boff, Pk); break;
-        case 2: item_entries<2, ST>(e, states, vstride, boff, Pk); break;
-        case 3: item_entries<3, ST>(e, states, vstride, boff, Pk); break;
-        default: item_entries<4, ST>(e, states, vstride, boff, Pk); break;
+        case 1: item_entries<1, ST>(e, states, vstride, qoff, nrep, Pk); break;
+        case 2: item_entries<2, ST>(e, states, vstride, qoff, nrep, Pk); break;
+        case 3: item_entries<3, ST>(e, states, vstride, qoff, nrep, Pk); break;
+        default: item_entries<4, ST>(e, states, vstride, qoff, nrep, Pk); break;
         }
     }
 }
 
 // Multiplies the k-vectors of a group into the four slots' weights (from LDS
 // when FROM_LDS, else from global memory).
-template <int KP, bool FROM_LDS, bool RESCALE>
+template <int KP, typename ST, bool FROM_LDS, bool RESCALE>
 __device__ __forceinline__ void item_multiply(lds_char *lds, global_char *gtab, const uint32_t (&Pk)[2],
                                               float (&w)[4][KP]) {
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
         float f[KP];
-        fast_kvec<KP, FROM_LDS>(lds, gtab, slot_index(Pk, c), f);
+        fast_kvec<KP, FROM_LDS>(lds, gtab, packed_index<ST>(Pk, c), f);
 #pragma unroll
         for (int k = 0; k < KP; ++k) w[c][k] *= f[k];
         if (RESCALE) renorm<KP>(w[c]);
@@ -549,7 +560,7 @@ __device__ __forceinline__ void item_multiply(lds_char *lds, global_char *gtab, 
 template <int KP, typename ST, bool STAGED, bool RESCALE>
 __device__ __forceinline__ void item_product(cint32_t *g, int n_groups, int n_staged, lds_char *lds,
                                              global_char *gtab, const ST *__restrict__ states, int64_t vstride,
-                                             const uint32_t (&boff)[4], float (&w)[4][KP]) {
+                                             uint32_t qoff, int nrep, float (&w)[4][KP]) {
 #pragma unroll
     for (int c = 0; c < 4; ++c)
 #pragma unroll
@@ -560,13 +571,13 @@ __device__ __forceinline__ void item_product(cint32_t *g, int n_groups, int n_st
     int j = 0;
     if (STAGED) {
         for (; j < n_staged; ++j) {
-            item_group<ST>(g, states, vstride, boff, Pk);
-            item_multiply<KP, true, RESCALE>(lds, gtab, Pk, w);
+            item_group<ST>(g, states, vstride, qoff, nrep, Pk);
+            item_multiply<KP, ST, true, RESCALE>(lds, gtab, Pk, w);
         }
     }
     for (; j < n_groups; ++j) {
-        item_group<ST>(g, states, vstride, boff, Pk);
-        item_multiply<KP, false, RESCALE>(lds, gtab, Pk, w);
+        item_group<ST>(g, states, vstride, qoff, nrep, Pk);
+        item_multiply<KP, ST, false, RESCALE>(lds, gtab, Pk, w);
     }
 }
 
@@ -603,18 +614,16 @@ __device__ __forceinline__ void sweep_product(const SweepParams &P, const Work &
     const int K = d[0], n_groups = d[8], n_staged = STAGED ? d[13] : 0;
     cint32_t *grp = d + d[9];
     ST *states = reinterpret_cast<ST *>(P.states);
-    const int64_t vstride = (int64_t)P.m * P.ld;
+    const int64_t vstride = node_stride(P.m, P.ld);
     const __amdgpu_buffer_rsrc_t own = node_rsrc<ST>(states, W.node, vstride);
     const int n_items = I.ncl * I.nrq;
     for (int t = threadIdx.x; t < n_items; t += kSweepBlock) {
         int64_t j;
         int rb, nrep;
         item_of(I, t, j, rb, nrep);
-        uint32_t boff[4];
-#pragma unroll
-        for (int c = 0; c < 4; ++c) boff[c] = (uint32_t)((rb + c) * P.ld + j) * (uint32_t)sizeof(ST);
+        const uint32_t qoff = quad_boff<ST>(rb >> 2, P.ld, j);
         float w[4][KP];
-        item_product<KP, ST, STAGED, false>(grp, n_groups, n_staged, lds, gtab, states, vstride, boff, w);
+        item_product<KP, ST, STAGED, false>(grp, n_groups, n_staged, lds, gtab, states, vstride, qoff, nrep, w);
         float wd[4][KP];
         if (DEBUG) {
 #pragma unroll
@@ -629,7 +638,7 @@ __device__ __forceinline__ void sweep_product(const SweepParams &P, const Work &
             low |= c < nrep && !(w[c][KP - 1] >= kUnderflowZ);
         }
         if (low) {
-            item_product<KP, ST, STAGED, true>(grp, n_groups, n_staged, lds, gtab, states, vstride, boff, w);
+            item_product<KP, ST, STAGED, true>(grp, n_groups, n_staged, lds, gtab, states, vstride, qoff, nrep, w);
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
                 if (DEBUG) {
@@ -640,29 +649,29 @@ __device__ __forceinline__ void sweep_product(const SweepParams &P, const Work &
             }
         }
         const Philox4 rnd = gibbs_block(P, W.node, rb >> 2, j);
+        typename Quad<ST>::V out{};
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
-            if (c < nrep) {
-                store_state<ST>(own, boff[c], draw_sums<KP>(w[c], K, uniform24(rnd.w[c])));
-                if (DEBUG) write_probs(P, W.node, rb + c, j, wd[c], K, w[c][KP - 1]);
-            }
+            out = Quad<ST>::put(out, c, draw_sums<KP>(w[c], K, uniform24(rnd.w[c])));
+            if (DEBUG && c < nrep) write_probs(P, W.node, rb + c, j, wd[c], K, w[c][KP - 1]);
         }
+        Quad<ST>::store_buffer(own, qoff, out);
     }
 }
 
 // Debug conditional of a table-mode node for replica r and column j, from
-// its wide list (global tables): the product over the quad of columns that
-// holds j, of which column j is written out.
+// its wide list (global tables): the product over the state quad that holds
+// replica r, of which slot r % 4 is written out.
 template <typename ST>
 __device__ void table_debug_prob(const SweepParams &P, const Work &W, int r, int64_t j) {
     cint32_t *d = W.d;
     const int K = d[0], KP = d[1];
     const ST *states = reinterpret_cast<const ST *>(P.states);
-    const int64_t col = j & ~int64_t(3);
-    const int nvalid = P.n_cols - col < 4 ? (int)(P.n_cols - col) : 4;
-    const int c = (int)(j - col);
-    const uint32_t lane_boff = (uint32_t)(r * P.ld + col) * (uint32_t)sizeof(ST);
-    const int64_t vstride = (int64_t)P.m * P.ld;
+    const int rb = r & ~3;
+    const int nvalid = P.m - rb < 4 ? P.m - rb : 4;
+    const int c = r & 3;
+    const uint32_t lane_boff = quad_boff<ST>(rb >> 2, P.ld, j);
+    const int64_t vstride = node_stride(P.m, P.ld);
     const float *tab = P.table + d[3];
 #define SAME_TABLE_DEBUG(KPV)                                                                     \
     {                                                                                             \
@@ -740,32 +749,32 @@ __device__ __forceinline__ void sweep_table(const SweepParams &P, const Work &W,
     cint32_t *grp = d + d[9];
     const bool tab_lds = STAGED && d[13] > 0;  // uniform: thresholds staged in LDS
     ST *states = reinterpret_cast<ST *>(P.states);
-    const int64_t vstride = (int64_t)P.m * P.ld;
+    const int64_t vstride = node_stride(P.m, P.ld);
     const __amdgpu_buffer_rsrc_t own = node_rsrc<ST>(states, W.node, vstride);
     const int n_items = I.ncl * I.nrq;
     for (int t = threadIdx.x; t < n_items; t += kSweepBlock) {
         int64_t j;
         int rb, nrep;
         item_of(I, t, j, rb, nrep);
-        uint32_t boff[4];
-#pragma unroll
-        for (int c = 0; c < 4; ++c) boff[c] = (uint32_t)((rb + c) * P.ld + j) * (uint32_t)sizeof(ST);
+        const uint32_t qoff = quad_boff<ST>(rb >> 2, P.ld, j);
         cint32_t *g = grp;
         uint32_t Pk[2];
-        item_group<ST>(g, states, vstride, boff, Pk);
+        item_group<ST>(g, states, vstride, qoff, nrep, Pk);
         const Philox4 rnd = gibbs_block(P, W.node, rb >> 2, j);
+        typename Quad<ST>::V out{};
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
-            if (c < nrep) {
-                const uint32_t u24 = rnd.w[c] >> 8;
-                uint32_t th[KT];
-                read_thresholds<KT>(tab_lds, lds, gcond, slot_index(Pk, c), th);
-                int pick = 0;
+            const uint32_t u24 = rnd.w[c] >> 8;
+            uint32_t th[KT];
+            read_thresholds<KT>(tab_lds, lds, gcond, packed_index<ST>(Pk, c), th);
+            int pick = 0;
 #pragma unroll
-                for (int k = 0; k < KT; ++k) pick += th[k] <= u24 ? 1 : 0;
-                store_state<ST>(own, boff[c], pick);
-                if (DEBUG) table_debug_prob<ST>(P, W, rb + c, j);
-            }
+            for (int k = 0; k < KT; ++k) pick += th[k] <= u24 ? 1 : 0;
+            out = Quad<ST>::put(out, c, pick);
+        }
+        Quad<ST>::store_buffer(own, qoff, out);
+        if (DEBUG) {
+            for (int c = 0; c < nrep; ++c) table_debug_prob<ST>(P, W, rb + c, j);
         }
     }
 }
@@ -860,43 +869,46 @@ __device__ void sweep_wide(const SweepParams &P, const Work &W) {
     cint32_t *grp = d + d[11];
     const float *tab = P.table + d[3];
     ST *states = reinterpret_cast<ST *>(P.states);
-    const int64_t vstride = (int64_t)P.m * P.ld;
-    for (int64_t q = W.q0 + threadIdx.x; q < W.q1; q += kSweepBlock) {
-        const int64_t col = q * 4;
-        const int lat = latent_bits(P, W.node, col);
-        if (!lat) continue;
-        const int nvalid = P.n_cols - col < 4 ? (int)(P.n_cols - col) : 4;
-        for (int r = W.r0; r < W.r1; ++r) {
-            const uint32_t lane_boff = (uint32_t)(r * P.ld + col) * (uint32_t)sizeof(ST);
-            typename Q::V cur = load_row<ST>(states, W.node, vstride, lane_boff);
-            float w[4][KP];
-            wide_product<KP, ST, false>(grp, n_groups, tab, states, vstride, lane_boff, nvalid, w);
-            bool low = false;
+    const int64_t vstride = node_stride(P.m, P.ld);
+    const __amdgpu_buffer_rsrc_t own = node_rsrc<ST>(states, W.node, vstride);
+    // lanes take (column, replica quad) pairs, consecutive lanes consecutive
+    // columns of one quad
+    const int64_t c0 = W.q0 * 4;
+    const int ncols = (int)((W.q1 * 4 < P.n_cols ? W.q1 * 4 : P.n_cols) - c0);
+    const int nrq = (W.r1 - W.r0 + 3) >> 2;
+    for (int t = threadIdx.x; t < ncols * nrq; t += kSweepBlock) {
+        const int rq = t / ncols;
+        const int64_t j = c0 + (t - rq * ncols);
+        if (P.obs[(int64_t)W.node * P.ld + j] != 0) continue;
+        const int rb = W.r0 + 4 * rq;
+        const int nrep = W.r1 - rb < 4 ? W.r1 - rb : 4;
+        const uint32_t qoff = quad_boff<ST>(rb >> 2, P.ld, j);
+        typename Q::V cur = load_row<ST>(states, W.node, vstride, qoff);
+        float w[4][KP];
+        wide_product<KP, ST, false>(grp, n_groups, tab, states, vstride, qoff, nrep, w);
+        bool low = false;
 #pragma unroll
-            for (int c = 0; c < 4; ++c) {
+        for (int c = 0; c < 4; ++c) {
+            float Z = 0.f;
+#pragma unroll
+            for (int k = 0; k < KP; ++k) Z += w[c][k];
+            low |= c < nrep && !(Z >= kUnderflowZ);
+        }
+        if (low) wide_product<KP, ST, true>(grp, n_groups, tab, states, vstride, qoff, nrep, w);
+        const Philox4 rnd = gibbs_block(P, W.node, rb >> 2, j);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            if (c >= nrep) continue;
+            if (DEBUG) {
                 float Z = 0.f;
 #pragma unroll
                 for (int k = 0; k < KP; ++k) Z += w[c][k];
-                low |= ((lat >> c) & 1) && !(Z >= kUnderflowZ);
+                write_probs(P, W.node, rb + c, j, w[c], K, Z);
             }
-            if (low) wide_product<KP, ST, true>(grp, n_groups, tab, states, vstride, lane_boff, nvalid, w);
-#pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                if (!((lat >> c) & 1)) continue;
-                const uint32_t word = gibbs_word(P, W.node, r, col + c);
-                if (DEBUG) {
-                    float Z = 0.f;
-#pragma unroll
-                    for (int k = 0; k < KP; ++k) Z += w[c][k];
-                    write_probs(P, W.node, r, col + c, w[c], K, Z);
-                }
-                running_sums<KP>(w[c]);
-                cur = Q::put(cur, c, draw_sums<KP>(w[c], K, uniform24(word)));
-            }
-            Q::store(reinterpret_cast<ST *>(reinterpret_cast<char *>(states + (int64_t)W.node * vstride) +
-                                            lane_boff),
-                     cur);
+            running_sums<KP>(w[c]);
+            cur = Q::put(cur, c, draw_sums<KP>(w[c], K, uniform24(rnd.w[c])));
         }
+        Q::store_buffer(own, qoff, cur);
     }
 }
 
@@ -951,50 +963,51 @@ __global__ __launch_bounds__(kSweepBlock) void sweep_generic_kernel(SweepParams 
     const int K = d[0];
     const float *tab = P.table + d[3];
     ST *states = reinterpret_cast<ST *>(P.states);
-    const int64_t vstride = (int64_t)P.m * P.ld;
-    for (int64_t q = W.q0 + threadIdx.x; q < W.q1; q += kSweepBlock) {
-        const int64_t col = q * 4;
-        const int lat = latent_bits(P, W.node, col);
-        if (!lat) continue;
-        for (int r = W.r0; r < W.r1; ++r) {
-            const ST *base = states + (int64_t)r * P.ld + col;
-            ST *own = states + ((int64_t)W.node * P.m + r) * P.ld + col;
-            typename Q::V cur = Q::load(own);
-            for (int c = 0; c < 4; ++c) {
-                if (!((lat >> c) & 1)) continue;
-                int E = -100000;
-                for (int k = 0; k < K; ++k) {
-                    int e;
-                    const float mk = weight_ext<ST>(d, tab, base, vstride, c, k, e);
-                    if (mk > 0.f && e > E) E = e;
-                }
-                float Z = 0.f;
-                for (int k = 0; k < K; ++k) {
-                    int e;
-                    const float mk = weight_ext<ST>(d, tab, base, vstride, c, k, e);
-                    Z += __builtin_ldexpf(mk, e - E);
-                }
-                const float t = uniform24(gibbs_word(P, W.node, r, col + c)) * Z;
-                float S = 0.f;
-                int pick = -1, last_pos = 0;
-                for (int k = 0; k < K; ++k) {
-                    int e;
-                    const float wk = __builtin_ldexpf(weight_ext<ST>(d, tab, base, vstride, c, k, e), e - E);
-                    S += wk;
-                    if (wk > 0.f) last_pos = k;
-                    if (pick < 0 && t < S) pick = k;
-                    if (DEBUG) {
-                        const int64_t j = col + c;
-                        if (j >= P.win_begin && j < P.win_begin + P.win)
-                            P.probs[(((int64_t)W.node * P.m + r) * P.win + (j - P.win_begin)) *
-                                        P.max_card + k] = wk / Z;
-                    }
-                }
-                if (pick < 0) pick = last_pos;
-                cur = Q::put(cur, c, pick);
+    const int64_t vstride = node_stride(P.m, P.ld);
+    const int64_t c0 = W.q0 * 4;
+    const int ncols = (int)((W.q1 * 4 < P.n_cols ? W.q1 * 4 : P.n_cols) - c0);
+    const int nrq = (W.r1 - W.r0 + 3) >> 2;
+    for (int t = threadIdx.x; t < ncols * nrq; t += kSweepBlock) {
+        const int rq = t / ncols;
+        const int64_t j = c0 + (t - rq * ncols);
+        if (P.obs[(int64_t)W.node * P.ld + j] != 0) continue;
+        const int rb = W.r0 + 4 * rq;
+        const int nrep = W.r1 - rb < 4 ? W.r1 - rb : 4;
+        const int64_t qe = ((int64_t)(rb >> 2) * P.ld + j) * 4;  // the quad's element offset in a node block
+        const ST *base = states + qe;
+        ST *own = states + (int64_t)W.node * vstride + qe;
+        typename Q::V cur = Q::load(own);
+        const Philox4 rnd = gibbs_block(P, W.node, rb >> 2, j);
+        for (int c = 0; c < nrep; ++c) {
+            int E = -100000;
+            for (int k = 0; k < K; ++k) {
+                int e;
+                const float mk = weight_ext<ST>(d, tab, base, vstride, c, k, e);
+                if (mk > 0.f && e > E) E = e;
             }
-            Q::store(own, cur);
+            float Z = 0.f;
+            for (int k = 0; k < K; ++k) {
+                int e;
+                const float mk = weight_ext<ST>(d, tab, base, vstride, c, k, e);
+                Z += __builtin_ldexpf(mk, e - E);
+            }
+            const float t_u = uniform24(rnd.w[c]) * Z;
+            float S = 0.f;
+            int pick = -1, last_pos = 0;
+            for (int k = 0; k < K; ++k) {
+                int e;
+                const float wk = __builtin_ldexpf(weight_ext<ST>(d, tab, base, vstride, c, k, e), e - E);
+                S += wk;
+                if (wk > 0.f) last_pos = k;
+                if (pick < 0 && t_u < S) pick = k;
+                if (DEBUG && j >= P.win_begin && j < P.win_begin + P.win)
+                    P.probs[(((int64_t)W.node * P.m + rb + c) * P.win + (j - P.win_begin)) * P.max_card + k] =
+                        wk / Z;
+            }
+            if (pick < 0) pick = last_pos;
+            cur = Q::put(cur, c, pick);
         }
+        Q::store(own, cur);
     }
 }
 
@@ -1150,11 +1163,12 @@ constexpr int kRepBins = 256;
 constexpr int kLdsBins = kCountLdsBins;
 static_assert(kCopies * kRepBins <= kLdsBins, "LDS budget");
 
-// kCountQuadsPerLane adjacent column quads of one row at byte offset boff.
-// WIDE (rows of at least 4 * NQ columns): one 16-byte load per 16 bytes of
-// states (8-byte for two int8 quads); a lane whose quads would run past the
-// end of the row (whole false) loads them one at a time instead, each wholly
-// inside or wholly past the node's buffer.  Not WIDE: always one at a time.
+// The state quads of NQ adjacent columns of one replica quad at byte offset
+// boff.  WIDE (rows of at least NQ columns): one 16-byte load per 16 bytes of
+// states (8-byte for two int8 quads); a lane whose columns would run past the
+// end of the row (whole false) loads its quads one at a time instead, each
+// wholly inside or wholly past the node's buffer.  Not WIDE: always one at a
+// time.
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
@@ -1202,19 +1216,20 @@ struct Span {
     }
 };
 
-constexpr int kCountReps = 5;  // replicas whose rows are loaded together (measured best on m = 10)
+constexpr int kCountQuads = 3;  // replica quads whose rows are loaded together (m = 10: all of them)
 
-// Histogram of (parent row, state) for one node over a slab of columns and all
-// m replicas (block geometry as the sweep's, decode_block).  Bins are counted
-// with packed 16-bit arithmetic (two lanes per word, as in the sweep) when the
-// node has at most 2^16 bins, else with 32-bit indices.
+// Histogram of (parent row, state) for one node over a slab of columns and a
+// range of replica quads (block geometry as the sweep's, decode_block).  Bins
+// are counted with packed 16-bit arithmetic (two lanes per word, as in the
+// sweep) when the node has at most 2^16 bins, else with 32-bit indices.
+// Padding slots (replicas >= m) and columns past the slab are not counted.
 template <typename ST, bool WIDE>
 __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict__ cdesc,
                                                       const int32_t *__restrict__ cdesc_off,
                                                       const int32_t *__restrict__ cwork,
                                                       int32_t count, int64_t n_slabs,
                                                       int64_t cols_per_block, int32_t rsplit,
-                                                      int32_t reps_per_block,
+                                                      int32_t quads_per_block,
                                                       const ST *__restrict__ states, int32_t m,
                                                       int64_t col0, int64_t n_cols, int64_t ld,
                                                       int32_t *__restrict__ counts) {
@@ -1235,15 +1250,16 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
     for (int b = threadIdx.x; b < lds_words; b += kBlock) hist[b] = 0;
     __syncthreads();
     const int copy = threadIdx.x & (kCopies - 1);
-    // a slab is a column run and a replica range [rb, re); absolute columns
-    // of the row: [c0, c1) inside [col0, col0 + n_cols)
+    // a slab is a column run and a range [qb, qe) of replica quads; absolute
+    // columns of the row: [c0, c1) inside [col0, col0 + n_cols)
     const int rpart = (int)(slab % rsplit);
     slab /= rsplit;
-    const int rb = rpart * reps_per_block;
-    const int re = rb + reps_per_block < m ? rb + reps_per_block : m;
+    const int mq = (m + 3) >> 2;
+    const int qb = rpart * quads_per_block;
+    const int qe = qb + quads_per_block < mq ? qb + quads_per_block : mq;
     const int64_t c0 = col0 + slab * cols_per_block;
     const int64_t c1 = c0 + cols_per_block < col0 + n_cols ? c0 + cols_per_block : col0 + n_cols;
-    const int64_t vstride = (int64_t)m * ld;
+    const int64_t vstride = node_stride(m, ld);
     const bool packed = nbins <= 65536;
     auto add = [&](int bin) {
         if (mode == 0) {
@@ -1255,16 +1271,18 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
             atomicAdd(&counts[off + bin], 1);
         }
     };
-    // a lane covers NQ adjacent column quads, read with wide loads per row
+    // a lane covers NQ adjacent columns (one state quad each), read with wide
+    // loads per replica quad
     constexpr int NQ = kCountQuadsPerLane;
     using S = Span<ST, NQ>;
-    for (int64_t col = c0 + 4 * NQ * (int64_t)threadIdx.x; col < c1; col += 4 * NQ * kBlock) {
-        const int nvalid = c1 - col < 4 * NQ ? (int)(c1 - col) : 4 * NQ;
-        const bool whole = col + 4 * NQ <= ld;
+    for (int64_t col = c0 + NQ * (int64_t)threadIdx.x; col < c1; col += NQ * kBlock) {
+        const int nvalid = c1 - col < NQ ? (int)(c1 - col) : NQ;
+        const bool whole = col + NQ <= ld;
         if (!packed) {
-            // 32-bit indices (more than 2^16 bins): one replica at a time
-            for (int r = rb; r < re; ++r) {
-                const uint32_t boff = (uint32_t)(r * ld + col) * (uint32_t)sizeof(ST);
+            // 32-bit indices (more than 2^16 bins): one replica quad at a time
+            for (int rq = qb; rq < qe; ++rq) {
+                const int nrep = m - 4 * rq < 4 ? m - 4 * rq : 4;
+                const uint32_t boff = quad_boff<ST>(rq, ld, col);
                 S own;
                 own.template load<WIDE>(states, node, vstride, boff, whole);
                 uint32_t u[NQ][4];
@@ -1285,39 +1303,40 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
                 for (int h = 0; h < NQ; ++h)
 #pragma unroll
                     for (int c = 0; c < 4; ++c)
-                        if (4 * h + c < nvalid) add((int)(u[h][c] * (uint32_t)K + (uint32_t)Q::get(own.q[h], c)));
+                        if (h < nvalid && c < nrep)
+                            add((int)(u[h][c] * (uint32_t)K + (uint32_t)Q::get(own.q[h], c)));
             }
             continue;
         }
-        for (int r0 = rb; r0 < re; r0 += kCountReps) {
-            const int nr = re - r0 < kCountReps ? re - r0 : kCountReps;
-            uint32_t boff[kCountReps];
-            S own[kCountReps];
+        for (int rq0 = qb; rq0 < qe; rq0 += kCountQuads) {
+            const int nq = qe - rq0 < kCountQuads ? qe - rq0 : kCountQuads;
+            uint32_t boff[kCountQuads];
+            S own[kCountQuads];
             // every slot loads (a fixed count keeps all loads in flight at
-            // once); slots past the last replica read through the node's
+            // once); slots past the last replica quad read through the node's
             // buffer resource past its end, which returns 0 without a memory
             // access, and their values are never used
 #pragma unroll
-            for (int t = 0; t < kCountReps; ++t) {
-                boff[t] = (uint32_t)((r0 + t) * ld + col) * (uint32_t)sizeof(ST);
+            for (int t = 0; t < kCountQuads; ++t) {
+                boff[t] = quad_boff<ST>(rq0 + t, ld, col);
                 own[t].template load<WIDE>(states, node, vstride, boff[t], whole);
             }
             // bin = sum over parents of x_p * (stride_p * K) + x_node
-            uint32_t Pk[kCountReps][NQ][2];
+            uint32_t Pk[kCountQuads][NQ][2];
 #pragma unroll
-            for (int t = 0; t < kCountReps; ++t)
+            for (int t = 0; t < kCountQuads; ++t)
 #pragma unroll
                 for (int h = 0; h < NQ; ++h) Q::split(own[t].q[h], Pk[t][h]);
             for (int q = 0; q < n_par; ++q) {
                 const uint32_t mult = (uint32_t)(par[2 * q + 1] * K) * 0x10001u;
-                S sp[kCountReps];
+                S sp[kCountQuads];
 #pragma unroll
-                for (int t = 0; t < kCountReps; ++t)
+                for (int t = 0; t < kCountQuads; ++t)
                     sp[t].template load<WIDE>(states, par[2 * q], vstride, boff[t], whole);
-                // slots past the last replica compute on zeros and are never
+                // slots past the last quad compute on zeros and are never
                 // counted: no exit from the unrolled loop
 #pragma unroll
-                for (int t = 0; t < kCountReps; ++t) {
+                for (int t = 0; t < kCountQuads; ++t) {
 #pragma unroll
                     for (int h = 0; h < NQ; ++h) {
                         uint32_t p2[2];
@@ -1328,13 +1347,14 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
                 }
             }
 #pragma unroll
-            for (int t = 0; t < kCountReps; ++t) {
-                if (t < nr) {  // uniform
+            for (int t = 0; t < kCountQuads; ++t) {
+                if (t < nq) {  // uniform
+                    const int nrep = m - 4 * (rq0 + t) < 4 ? m - 4 * (rq0 + t) : 4;
 #pragma unroll
                     for (int h = 0; h < NQ; ++h)
 #pragma unroll
                         for (int c = 0; c < 4; ++c)
-                            if (4 * h + c < nvalid) add((int)packed_index<ST>(Pk[t][h], c));
+                            if (h < nvalid && c < nrep) add((int)packed_index<ST>(Pk[t][h], c));
                 }
             }
         }
@@ -1492,17 +1512,21 @@ __global__ __launch_bounds__(kBlock) void expand_kernel(const int64_t *__restric
     if (j < 0 || j >= n_cols) return;
     if (e + 1 < row_ptr[lo + 1] && col_idx[e + 1] == j) return;  // a later entry of this column
     obs[(int64_t)lo * ld + j] = 1;
-    const ST v = values[e];
-    ST *dst = states + (int64_t)lo * m * ld + j;
-    for (int r = 0; r < m; ++r) dst[(int64_t)r * ld] = v;
+    // every slot of the column's state quads, padding included, takes the value
+    const typename Quad<ST>::V v = Quad<ST>::splat((int)values[e]);
+    ST *dst = states + (int64_t)lo * node_stride(m, ld) + 4 * j;
+    const int mq = (m + 3) >> 2;
+    for (int rq = 0; rq < mq; ++rq) Quad<ST>::store(dst + (int64_t)rq * ld * 4, v);
 }
 
 // Random initial latent states (Sec. 5.2): one thread per (node, column
-// quad), looping over the replicas; the quad's Philox block at counter
-// {g >> 2, i, r | 2 << 24, 0} gives word c to column c, and the state is
-// ((w >> 8) * K_i) >> 24 = floor(U * K_i) exactly.  The quad's obs dword is
-// read once; each replica's state quad is read, its latent columns replaced,
-// and written back.  Observed entries keep their values.
+// quad), looping over the replicas; for replica r the Philox block at counter
+// {g >> 2, i, r | 2 << 24, 0} (g the global column of the quad's first
+// column) gives word c to column c, and the state is ((w >> 8) * K_i) >> 24 =
+// floor(U * K_i) exactly.  The quad's obs dword is read once; for each
+// replica quad, the state quads of the four columns are read, the latent
+// columns' real slots replaced, and written back.  Observed entries and
+// padding slots keep their values.
 template <typename ST>
 __global__ __launch_bounds__(kBlock) void init_latent_kernel(const int32_t *__restrict__ cdesc,
                                                              const int32_t *__restrict__ cdesc_off,
@@ -1524,15 +1548,22 @@ __global__ __launch_bounds__(kBlock) void init_latent_kernel(const int32_t *__re
         if (((ob >> (8 * c)) & 0xffu) == 0 && col + c < n_cols) lat |= 1 << c;
     if (!lat) return;
     const uint32_t K = (uint32_t)cdesc[cdesc_off[i]];
-    for (int r = 0; r < m; ++r) {
-        const Philox4 b = philox4x32_10((uint32_t)((col_offset >> 2) + q), (uint32_t)i,
-                                        (uint32_t)r | (2u << 24), 0u, k0, k1);
-        ST *p = states + ((int64_t)i * m + r) * ld + col;
-        typename Q::V v = Q::load(p);
+    const int mq = (m + 3) >> 2;
+    for (int rq = 0; rq < mq; ++rq) {
+        ST *p = states + (int64_t)i * node_stride(m, ld) + ((int64_t)rq * ld + col) * 4;
+        typename Q::V v[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) v[c] = Q::load(p + 4 * c);
+        for (int s = 0; s < 4 && 4 * rq + s < m; ++s) {
+            const Philox4 b = philox4x32_10((uint32_t)((col_offset >> 2) + q), (uint32_t)i,
+                                            (uint32_t)(4 * rq + s) | (2u << 24), 0u, k0, k1);
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+                if ((lat >> c) & 1) v[c] = Q::put(v[c], s, (int)(((uint64_t)(b.w[c] >> 8) * K) >> 24));
+        }
 #pragma unroll
         for (int c = 0; c < 4; ++c)
-            if ((lat >> c) & 1) v = Q::put(v, c, (int)(((uint64_t)(b.w[c] >> 8) * K) >> 24));
-        Q::store(p, v);
+            if ((lat >> c) & 1) Q::store(p + 4 * c, v[c]);
     }
 }
 
@@ -1564,10 +1595,16 @@ __global__ __launch_bounds__(kBlock) void hits_kernel(const ST *__restrict__ sta
     }
     if (!any) return;
     int add[4] = {0, 0, 0, 0};
-    for (int r = 0; r < m; ++r) {
-        const typename Q::V v = Q::load(states + ((int64_t)i * m + r) * ld + col);
+    const int mq = (m + 3) >> 2;
+    for (int rq = 0; rq < mq; ++rq) {
+        const ST *p = states + (int64_t)i * node_stride(m, ld) + ((int64_t)rq * ld + col) * 4;
+        const int nrep = m - 4 * rq < 4 ? m - 4 * rq : 4;
 #pragma unroll
-        for (int c = 0; c < 4; ++c) add[c] += Q::get(v, c) == (want[c] & (sizeof(ST) == 1 ? 0xff : 0xffff)) ? 1 : 0;
+        for (int c = 0; c < 4; ++c) {
+            const typename Q::V v = Q::load(p + 4 * c);  // column col + c, four replica slots
+            for (int sl = 0; sl < nrep; ++sl)
+                add[c] += Q::get(v, sl) == (want[c] & (sizeof(ST) == 1 ? 0xff : 0xffff)) ? 1 : 0;
+        }
     }
     int4 *h = reinterpret_cast<int4 *>(hits + (int64_t)i * ld + col);
     int4 cur = *h;
@@ -1675,9 +1712,10 @@ __device__ __forceinline__ int compact_rank(const uint8_t *__restrict__ obs, int
 }
 
 // Dense slot of a minibatch from the device-resident known data and the
-// compact latent states: every replica's row takes the known value at an
-// observed column and its compact latent state at a latent one; the slot's
-// obs rows are copied as well.  Columns [cols, slot_ld) are left untouched.
+// compact latent states: every replica takes the known value at an observed
+// column and its compact latent state at a latent one (padding slots: the
+// known value, or 0 at a latent column); the slot's obs rows are copied as
+// well.  Columns [cols, slot_ld) are left untouched.
 template <typename ST>
 __global__ __launch_bounds__(kBlock) void expand_compact_kernel(
     const uint8_t *__restrict__ obs, const ST *__restrict__ data, int64_t obs_ld, int64_t c0, int64_t cols,
@@ -1695,14 +1733,24 @@ __global__ __launch_bounds__(kBlock) void expand_compact_kernel(
     const ST *lat_node = lat_states + (node_off[node] - off0);
     *reinterpret_cast<uint32_t *>(obs_slot + (int64_t)node * slot_ld + j) =
         *reinterpret_cast<const uint32_t *>(obs + (int64_t)node * obs_ld + c0 + j);
-    const typename Q::V known = Q::load(data + (int64_t)node * obs_ld + c0 + j);
-    for (int r = 0; r < m; ++r) {
-        typename Q::V v = known;
+    const typename Q::V known = Q::load(data + (int64_t)node * obs_ld + c0 + j);  // columns j .. j + 3
+    int kc[4];  // compact rank of each latent column of the lane
+    {
         int k = rank;
 #pragma unroll
-        for (int c = 0; c < 4; ++c)
-            if ((lat >> c) & 1) v = Q::put(v, c, (int)lat_node[(int64_t)r * L + k++]);
-        Q::store(states + ((int64_t)node * m + r) * slot_ld + j, v);
+        for (int c = 0; c < 4; ++c) kc[c] = ((lat >> c) & 1) ? k++ : -1;
+    }
+    const int mq = (m + 3) >> 2;
+    ST *dst = states + (int64_t)node * node_stride(m, slot_ld) + 4 * j;
+    for (int rq = 0; rq < mq; ++rq) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            typename Q::V v = Q::splat(kc[c] >= 0 ? 0 : Q::get(known, c));
+            if (kc[c] >= 0)
+                for (int sl = 0; sl < 4 && 4 * rq + sl < m; ++sl)
+                    v = Q::put(v, sl, (int)lat_node[(int64_t)(4 * rq + sl) * L + kc[c]]);
+            Q::store(dst + ((int64_t)rq * slot_ld + c) * 4, v);
+        }
     }
 }
 
@@ -1721,36 +1769,47 @@ __global__ __launch_bounds__(kBlock) void gather_compact_kernel(
     if (j >= cols || !lat) return;
     const int64_t L = (node_off[node + 1] - node_off[node]) / m;
     ST *lat_node = lat_states + (node_off[node] - off0);
-    for (int r = 0; r < m; ++r) {
-        const typename Q::V v = Q::load(states + ((int64_t)node * m + r) * slot_ld + j);
-        int k = rank;
+    const int mq = (m + 3) >> 2;
+    const ST *src = states + (int64_t)node * node_stride(m, slot_ld) + 4 * j;
+    int k = rank;
 #pragma unroll
-        for (int c = 0; c < 4; ++c)
-            if ((lat >> c) & 1) lat_node[(int64_t)r * L + k++] = (ST)Q::get(v, c);
+    for (int c = 0; c < 4; ++c) {
+        if (!((lat >> c) & 1)) continue;
+        for (int rq = 0; rq < mq; ++rq) {
+            const typename Q::V v = Q::load(src + ((int64_t)rq * slot_ld + c) * 4);
+            for (int sl = 0; sl < 4 && 4 * rq + sl < m; ++sl)
+                lat_node[(int64_t)(4 * rq + sl) * L + k] = (ST)Q::get(v, sl);
+        }
+        ++k;
     }
 }
 
 // ---------------------------------------------------------------- annealing
 
 // SAME annealing (Sec. 3: raising the replication factor during sampling):
-// dst [n][m2][ld] takes replica r < m of states [n][m][ld] and, for r >= m, a
-// copy of replica r mod m.  One thread per 16 bytes of a destination row
-// (row bytes ld * sizeof(state) are a multiple of 4; the tail of a row that is
-// not a whole 16 bytes is copied in words).
-__global__ __launch_bounds__(kBlock) void grow_kernel(const uint8_t *__restrict__ src, int32_t m, uint8_t *__restrict__ dst,
-                                                      int32_t m2, int64_t row_bytes, int64_t rows2) {
-    const int64_t per_row = (row_bytes + 15) >> 4;
+// dst (m2 replicas) takes replica r < m of src (m replicas) and, for r >= m, a
+// copy of replica r mod m; padding slots of dst take the same rule.  One
+// thread per (node, column): the source quads of the column are read once and
+// the destination quads assembled slot by slot.
+template <typename ST>
+__global__ __launch_bounds__(kBlock) void grow_kernel(const ST *__restrict__ src, int32_t m, ST *__restrict__ dst,
+                                                      int32_t m2, int32_t n, int64_t ld) {
+    using Q = Quad<ST>;
     const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (t >= rows2 * per_row) return;
-    const int64_t row = t / per_row, off = (t - row * per_row) * 16;
-    const int64_t i = row / m2, r = row - i * m2;
-    const uint8_t *s = src + (i * m + r % m) * row_bytes + off;
-    uint8_t *d = dst + row * row_bytes + off;
-    if (off + 16 <= row_bytes && ((reinterpret_cast<uintptr_t>(s) | reinterpret_cast<uintptr_t>(d)) & 15) == 0) {
-        *reinterpret_cast<uint4 *>(d) = *reinterpret_cast<const uint4 *>(s);
-    } else {
-        for (int64_t k = 0; k < 16 && off + k < row_bytes; k += 4)
-            *reinterpret_cast<uint32_t *>(d + k) = *reinterpret_cast<const uint32_t *>(s + k);
+    if (t >= (int64_t)n * ld) return;
+    const int i = (int)(t / ld);
+    const int64_t j = t - (int64_t)i * ld;
+    const ST *s = src + (int64_t)i * node_stride(m, ld) + 4 * j;
+    ST *d = dst + (int64_t)i * node_stride(m2, ld) + 4 * j;
+    const int mq2 = (m2 + 3) >> 2;
+    for (int rq = 0; rq < mq2; ++rq) {
+        typename Q::V v{};
+#pragma unroll
+        for (int sl = 0; sl < 4; ++sl) {
+            const int r = (4 * rq + sl) % m;
+            v = Q::put(v, sl, Q::get(Q::load(s + (int64_t)(r >> 2) * ld * 4), r & 3));
+        }
+        Q::store(d + (int64_t)rq * ld * 4, v);
     }
 }
 
@@ -1824,12 +1883,14 @@ void sweep_class(const SweepParams &P, int32_t klass, int32_t lds_bytes, dim3 gr
 hipError_t launch_sweep(SweepParams P, int32_t begin, int32_t count, int32_t klass,
                         int32_t lds_bytes, int32_t state_bytes, hipStream_t stream) {
     if (count <= 0 || P.n_cols <= 0) return hipSuccess;
-    // Slabs of kSweepQuadsPerLane quads per lane.  A block that stages its
-    // node's table in LDS (class 0) takes all replicas, so that the copy is
-    // paid once per column chunk, and replicas are split only when that
+    // Slabs of kSweepQuadsPerLane column quads per lane.  A block that stages
+    // its node's table in LDS (class 0) takes all replicas, so that the copy
+    // is paid once per column chunk, and replicas are split only when that
     // leaves fewer than kMinSweepBlocks blocks; the other classes take one
-    // replica per block: smaller slabs keep the blanket rows and the global
-    // tables that the resident blocks gather from in L2 (measured faster).
+    // replica quad per block: smaller slabs keep the blanket rows and the
+    // global tables that the resident blocks gather from in L2 (measured
+    // faster).  A block's replica range is always whole state quads (the
+    // last one ends at m), so that no two blocks write one quad.
     const int64_t quads = (P.n_cols + 3) / 4;
     P.quads_per_block = (int64_t)dev::kSweepBlock * dev::kSweepQuadsPerLane;
     // the fast kernel draws replicas in quads (one Philox block each), so a
@@ -1844,16 +1905,11 @@ hipError_t launch_sweep(SweepParams P, int32_t begin, int32_t count, int32_t kla
             P.quads_per_block /= 2;
     const int64_t chunks = (quads + P.quads_per_block - 1) / P.quads_per_block;
     int64_t rsplit = klass == 0 ? (dev::kMinSweepBlocks + count * chunks - 1) / (count * chunks) : m_quads;
-    if (klass >= 2) rsplit = P.m;
-    if (rsplit > (klass >= 2 ? P.m : m_quads)) rsplit = klass >= 2 ? P.m : m_quads;
+    if (rsplit > m_quads) rsplit = m_quads;
     if (rsplit < 1) rsplit = 1;
-    if (klass >= 2) {
-        P.reps_per_block = (int32_t)((P.m + rsplit - 1) / rsplit);
-    } else {
-        P.reps_per_block = (int32_t)(4 * ((m_quads + rsplit - 1) / rsplit));
-        if (P.reps_per_block > P.m) P.reps_per_block = P.m;
-    }
-    P.rsplit = (int32_t)((P.m + P.reps_per_block - 1) / P.reps_per_block);
+    const int64_t quads_per_block = (m_quads + rsplit - 1) / rsplit;
+    P.rsplit = (int32_t)((m_quads + quads_per_block - 1) / quads_per_block);
+    P.reps_per_block = (int32_t)(4 * quads_per_block);
     P.n_slabs = chunks * P.rsplit;
     P.count = count;
     P.begin = begin;
@@ -1922,18 +1978,20 @@ hipError_t launch_counts(const DeviceTables &t, const void *states, int32_t stat
                          hipStream_t stream) {
     if (n_cols <= 0) return hipSuccess;
     const int32_t n = t.n_cwork;
-    // one node x kCountQuadsPerLane quads per lane x all replicas per block,
-    // XCD-swizzled like the sweep
+    // one node x 4096 columns (kCountQuadsPerLane columns per lane and
+    // iteration) x all replica quads per block, XCD-swizzled like the sweep
     const int64_t cols_per_block = 4 * dev::kBlock * dev::kCountQuadsPerLane;
     const int64_t col_slabs = (n_cols + cols_per_block - 1) / cols_per_block;
-    // small launches split the replicas (in runs of kCountReps) over blocks
-    // until there are kMinSweepBlocks blocks, so that they fill the device
-    const int64_t rep_runs = (m + dev::kCountReps - 1) / dev::kCountReps;
+    // small launches split the replica quads (in runs of kCountQuads) over
+    // blocks until there are kMinSweepBlocks blocks, so that they fill the
+    // device
+    const int64_t mq = (m + 3) / 4;
+    const int64_t quad_runs = (mq + dev::kCountQuads - 1) / dev::kCountQuads;
     int64_t rparts = (dev::kMinSweepBlocks + (int64_t)n * col_slabs - 1) / ((int64_t)n * col_slabs);
-    if (rparts > rep_runs) rparts = rep_runs;
+    if (rparts > quad_runs) rparts = quad_runs;
     if (rparts < 1) rparts = 1;
-    const int32_t reps_per_block = (int32_t)(dev::kCountReps * ((rep_runs + rparts - 1) / rparts));
-    const int32_t rsplit = (int32_t)((m + reps_per_block - 1) / reps_per_block);
+    const int32_t quads_per_block = (int32_t)(dev::kCountQuads * ((quad_runs + rparts - 1) / rparts));
+    const int32_t rsplit = (int32_t)((mq + quads_per_block - 1) / quads_per_block);
     const int64_t n_slabs = col_slabs * rsplit;
     const int64_t rounds = (n_slabs + dev::kXcds - 1) / dev::kXcds;
     const int64_t blocks = rounds * dev::kXcds * n;
@@ -1941,14 +1999,14 @@ hipError_t launch_counts(const DeviceTables &t, const void *states, int32_t stat
     const dim3 grid((unsigned)blocks);
 #define SAME_LAUNCH_COUNTS(ST, WIDE)                                                                    \
     hipLaunchKernelGGL((dev::count_kernel<ST, WIDE>), grid, dim3(dev::kBlock), 0, stream, t.cdesc, t.cdesc_off, \
-                       t.cwork, n, n_slabs, cols_per_block, rsplit, reps_per_block, (const ST *)states, m, col0, \
+                       t.cwork, n, n_slabs, cols_per_block, rsplit, quads_per_block, (const ST *)states, m, col0, \
                        n_cols, ld, counts)
-    // rows of at least 4 * kCountQuadsPerLane columns take the wide loads
+    // rows of at least kCountQuadsPerLane columns take the wide loads
     if (state_bytes == 1) {
-        if (ld >= 4 * dev::kCountQuadsPerLane) SAME_LAUNCH_COUNTS(int8_t, true);
+        if (ld >= dev::kCountQuadsPerLane) SAME_LAUNCH_COUNTS(int8_t, true);
         else SAME_LAUNCH_COUNTS(int8_t, false);
     } else {
-        if (ld >= 4 * dev::kCountQuadsPerLane) SAME_LAUNCH_COUNTS(int16_t, true);
+        if (ld >= dev::kCountQuadsPerLane) SAME_LAUNCH_COUNTS(int16_t, true);
         else SAME_LAUNCH_COUNTS(int16_t, false);
     }
 #undef SAME_LAUNCH_COUNTS
@@ -2061,15 +2119,18 @@ hipError_t launch_gather_compact(const uint8_t *obs, int64_t obs_ld, int64_t c0,
     return hipGetLastError();
 }
 
-hipError_t launch_grow(const void *src, int32_t m, void *dst, int32_t m2, int32_t n, int64_t row_bytes,
-                       hipStream_t stream) {
-    const int64_t rows2 = (int64_t)n * m2;
-    const int64_t items = rows2 * ((row_bytes + 15) / 16);
+hipError_t launch_grow(const void *src, int32_t m, void *dst, int32_t m2, int32_t n, int64_t ld,
+                       int32_t state_bytes, hipStream_t stream) {
+    const int64_t items = (int64_t)n * ld;
     if (items <= 0) return hipSuccess;
     const int64_t blocks = (items + dev::kBlock - 1) / dev::kBlock;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(dev::grow_kernel, dim3((unsigned)blocks), dim3(dev::kBlock), 0, stream,
-                       (const uint8_t *)src, m, (uint8_t *)dst, m2, row_bytes, rows2);
+    if (state_bytes == 1)
+        hipLaunchKernelGGL(dev::grow_kernel<int8_t>, dim3((unsigned)blocks), dim3(dev::kBlock), 0, stream,
+                           (const int8_t *)src, m, (int8_t *)dst, m2, n, ld);
+    else
+        hipLaunchKernelGGL(dev::grow_kernel<int16_t>, dim3((unsigned)blocks), dim3(dev::kBlock), 0, stream,
+                           (const int16_t *)src, m, (int16_t *)dst, m2, n, ld);
     return hipGetLastError();
 }
 

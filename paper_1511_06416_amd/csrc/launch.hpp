@@ -130,9 +130,10 @@ hipError_t launch_gather_compact(const uint8_t *obs, int64_t obs_ld, int64_t c0,
                                  const int32_t *prefix, const int64_t *node_off, int64_t off0, const void *states,
                                  int64_t slot_ld, void *lat_states, int32_t state_bytes, hipStream_t stream);
 
-// SAME annealing: dst [n][m2] rows from src [n][m] rows (replica r mod m).
-hipError_t launch_grow(const void *src, int32_t m, void *dst, int32_t m2, int32_t n, int64_t row_bytes,
-                       hipStream_t stream);
+// SAME annealing: dst (m2 replicas) from src (m replicas), replica r of dst
+// taking replica r mod m; both in the state-quad layout with leading dimension ld.
+hipError_t launch_grow(const void *src, int32_t m, void *dst, int32_t m2, int32_t n, int64_t ld,
+                       int32_t state_bytes, hipStream_t stream);
 
 hipError_t launch_moving_sum(const int32_t *newc, int32_t *mb, int32_t *totals, int64_t total,
                              hipStream_t stream);

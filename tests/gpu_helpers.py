@@ -27,13 +27,14 @@ def context_for(net, prior=1.0, table_limit=None, tile_bytes=0, lds_limit=None, 
 
 def gpu_sweep(ctx, states_np, obs_np, theta_np, m, n_cols, col_offset, seed, sweep_id, win=None,
               stream=None):
-    """Runs one library sweep on copies of the given host arrays; returns
-    (states after, probs or None)."""
-    st = torch.from_numpy(np.ascontiguousarray(states_np)).cuda()
+    """Runs one library sweep on copies of the given host arrays (states
+    [n][m][ld], packed into the library's replica quads); returns (states
+    after, as [n][m][ld], probs or None)."""
+    st = torch.from_numpy(same.pack_states(np.ascontiguousarray(states_np))).cuda()
     ob = torch.from_numpy(np.ascontiguousarray(obs_np)).cuda()
     th = torch.from_numpy(np.ascontiguousarray(theta_np, dtype=np.float32)).cuda()
     ws = ctx.new_workspace()
-    ld = st.shape[-1]
+    ld = st.shape[2]
     probs = None
     if win is not None:
         probs = torch.full((ctx.n_nodes, m, win[1], ctx.max_card), float("nan"), device="cuda")
@@ -42,7 +43,7 @@ def gpu_sweep(ctx, states_np, obs_np, theta_np, m, n_cols, col_offset, seed, swe
     else:
         same.same_sweep(ctx, st, ob, th, m, n_cols, ld, col_offset, seed, sweep_id, ws, stream)
     torch.cuda.synchronize()
-    return st.cpu().numpy(), (probs.cpu().numpy() if probs is not None else None)
+    return same.unpack_states(st.cpu().numpy(), m), (probs.cpu().numpy() if probs is not None else None)
 
 
 def gpu_sweep_both(ctx, states_np, obs_np, theta_np, m, n_cols, col_offset, seed, sweep_id, win=None):

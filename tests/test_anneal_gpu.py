@@ -25,10 +25,14 @@ def test_grow_replicas_matches_oracle(cfg, kw, m2):
     st = w.states[0].numpy()
     ref = oracle.grow_replicas(st, m2)
     ctx = H.context_for(w.net)
-    dst = torch.full(ref.shape, 77, dtype=w.states[0].dtype, device="cuda")
-    same.same_grow_replicas(ctx, w.states[0].cuda(), w.m, dst, m2, w.ld)
+    dst = torch.full(same.state_shape(w.net.n, m2, w.ld), 77, dtype=w.states[0].dtype, device="cuda")
+    same.same_grow_replicas(ctx, same.pack_states(w.states[0]).cuda(), w.m, dst, m2, w.ld)
     torch.cuda.synchronize()
-    assert np.array_equal(dst.cpu().numpy(), ref)
+    assert np.array_equal(same.unpack_states(dst.cpu().numpy(), m2), ref)
+    # padding slots of the last destination quad follow the same rule (a valid state)
+    full = same.unpack_states(dst.cpu().numpy(), 4 * ((m2 + 3) // 4))
+    for r in range(m2, full.shape[1]):
+        assert np.array_equal(full[:, r], st[:, r % w.m])
     ctx.close()
 
 
@@ -36,10 +40,10 @@ def test_grow_replicas_int16_ragged_rows():
     card = np.array([300, 3], dtype=np.int32)
     ctx = H.context_for(Network("custom", [[], [0]], card))
     rng = np.random.default_rng(4)
-    st = rng.integers(0, 3, (2, 3, 20)).astype(np.int16)  # rows of 40 bytes: 16-byte pieces and a tail
+    st = rng.integers(0, 3, (2, 3, 20)).astype(np.int16)  # 20 columns, m = 3 grown to 5
     ref = oracle.grow_replicas(st, 5)
-    dst = torch.zeros(ref.shape, dtype=torch.int16, device="cuda")
-    same.same_grow_replicas(ctx, torch.from_numpy(st).cuda(), 3, dst, 5, 20)
+    dst = torch.zeros(same.state_shape(2, 5, 20), dtype=torch.int16, device="cuda")
+    same.same_grow_replicas(ctx, torch.from_numpy(same.pack_states(st)).cuda(), 3, dst, 5, 20)
     torch.cuda.synchronize()
-    assert np.array_equal(dst.cpu().numpy(), ref)
+    assert np.array_equal(same.unpack_states(dst.cpu().numpy(), 5), ref)
     ctx.close()

@@ -33,7 +33,7 @@ def test_counts_ema_bit_exact(cfg, kw, decay):
     ref = t0.copy()
     oracle.ema(ref, decay, oracle.counts(net.parents, net.card, st, w.m, w.mb_cols(0)))
     g = torch.from_numpy(t0).cuda()
-    same.same_counts_ema(ctx, w.states[0].cuda(), w.m, w.mb_cols(0), w.ld, decay, g, ws)
+    same.same_counts_ema(ctx, same.pack_states(w.states[0]).cuda(), w.m, w.mb_cols(0), w.ld, decay, g, ws)
     torch.cuda.synchronize()
     assert np.array_equal(g.cpu().numpy(), ref)
     ctx.close()
@@ -62,7 +62,7 @@ def test_stream_pass_ema_equals_resident():
     decay = 1.0 - 1.0 / M
     passes = 2
     # resident: the same calls in the same order on device minibatches
-    dev = [s.cuda() for s in w.states]
+    dev = [same.pack_states(s).cuda() for s in w.states]
     obs = [o.cuda() for o in w.obs]
     ws = ctx.new_workspace()
     cpts = torch.from_numpy(w.init_theta).cuda()
@@ -89,7 +89,8 @@ def test_stream_pass_ema_equals_resident():
     torch.cuda.synchronize()
     assert np.array_equal(tot2.cpu().numpy(), tot.cpu().numpy())
     assert np.array_equal(cp2.cpu().numpy(), cpts.cpu().numpy())
+    hs = same.unpack_states(hst, w.m)
     for b in range(M):
         c0, nc = b * w.nb, w.mb_cols(b)
-        assert np.array_equal(hst[:, :, c0:c0 + nc].numpy(), dev[b][:, :, :nc].cpu().numpy())
+        assert np.array_equal(hs[:, :, c0:c0 + nc].numpy(), same.unpack_states(dev[b].cpu(), w.m)[:, :, :nc].numpy())
     ctx.close()

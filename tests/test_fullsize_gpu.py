@@ -45,10 +45,11 @@ def test_full_minibatch_step_matches_oracle():
     mb = torch.zeros(ctx.cpt_total, dtype=torch.int32, device=dev)
     tot = torch.zeros(ctx.cpt_total, dtype=torch.int32, device=dev)
     sweep_id = update_id = 3
-    same.same_counts(ctx, w.states[0], m, nc, ld, mb, tot, ws)  # the pre-pass
-    same.same_step(ctx, w.states[0], w.obs[0], cpts, m, nc, ld, 0, w.seed, sweep_id, mb, tot, update_id, ws)
+    st = same.pack_states(w.states[0])  # the library's replica-quad layout, on the device
+    same.same_counts(ctx, st, m, nc, ld, mb, tot, ws)  # the pre-pass
+    same.same_step(ctx, st, w.obs[0], cpts, m, nc, ld, 0, w.seed, sweep_id, mb, tot, update_id, ws)
     torch.cuda.synchronize()
-    post = w.states[0].cpu().numpy()
+    post = same.unpack_states(st.cpu().numpy(), m)
     obs = w.obs[0].cpu().numpy()
     color = oracle.graph(net.parents, net.card)["color"]
     assert np.array_equal(ctx.color, color)

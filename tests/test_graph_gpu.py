@@ -31,7 +31,7 @@ class _Run:
     count-only pre-pass."""
 
     def __init__(self, w, ctx):
-        self.states = [s.cuda() for s in w.states]
+        self.states = [same.pack_states(s).cuda() for s in w.states]
         self.obs = [o.cuda() for o in w.obs]
         self.ws = ctx.new_workspace()
         self.cpts = torch.from_numpy(w.init_theta).cuda()

@@ -29,13 +29,14 @@ def _expand_case(net, st, ob, n_cols, m, sentinel=99):
     ref_ob = np.full_like(ob, 3)
     oracle.expand(n, n_cols, m, ld, row_ptr, col, val, ref_st, ref_ob)
     ctx = H.context_for(net)
-    g_st = torch.full(st.shape, sentinel, dtype=torch.from_numpy(st[:1, :1, :1]).dtype, device="cuda")
+    g_st = torch.full(same.state_shape(n, m, ld), sentinel, dtype=torch.from_numpy(st[:1, :1, :1]).dtype,
+                      device="cuda")
     g_ob = torch.full(ob.shape, 3, dtype=torch.uint8, device="cuda")
     rp, ci, vv = (torch.from_numpy(a).cuda() for a in (row_ptr, col, val))
     same.same_expand_observed(ctx, rp, ci, vv, len(col), m, n_cols, ld, g_st, g_ob)
     torch.cuda.synchronize()
     assert np.array_equal(g_ob.cpu().numpy(), ref_ob)
-    assert np.array_equal(g_st.cpu().numpy(), ref_st)
+    assert np.array_equal(same.unpack_states(g_st.cpu().numpy(), m), ref_st)
     ctx.close()
     return len(col)
 
@@ -70,10 +71,10 @@ def test_init_latent_matches_oracle(cfg, kw, col_offset):
     ref = st.copy()
     oracle.init_latent(w.net.card, w.n_cols, w.m, col_offset, w.seed, ref, ob)
     ctx = H.context_for(w.net)
-    g = torch.from_numpy(st).cuda()
+    g = torch.from_numpy(same.pack_states(st)).cuda()
     same.same_init_latent(ctx, g, torch.from_numpy(ob).cuda(), w.m, w.n_cols, w.ld, col_offset, w.seed)
     torch.cuda.synchronize()
-    assert np.array_equal(g.cpu().numpy(), ref)
+    assert np.array_equal(same.unpack_states(g.cpu().numpy(), w.m), ref)
     ctx.close()
 
 
@@ -87,8 +88,8 @@ def test_init_latent_int16():
     ref = st.copy()
     oracle.init_latent(card, n_cols, m, 12, 99, ref, ob)
     ctx = H.context_for(Network("custom", parents, card))
-    g = torch.from_numpy(st).cuda()
+    g = torch.from_numpy(same.pack_states(st)).cuda()
     same.same_init_latent(ctx, g, torch.from_numpy(ob).cuda(), m, n_cols, ld, 12, 99)
     torch.cuda.synchronize()
-    assert np.array_equal(g.cpu().numpy(), ref)
+    assert np.array_equal(same.unpack_states(g.cpu().numpy(), m), ref)
     ctx.close()

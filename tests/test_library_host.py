@@ -332,3 +332,40 @@ def test_step_graph_argument_errors():
                              P(FAKE), 1, 1, P(FAKE), None) == same.SAME_EINVAL
     assert L.same_graph_launch(None, None) == same.SAME_EINVAL
     L.same_graph_destroy(None)
+
+
+@pytest.mark.parametrize("m", [1, 3, 4, 10, 37])
+def test_state_quad_layout_helpers(m):
+    """pack_states places replica r of node i at column j at element
+    ((i * mq + r // 4) * ld + j) * 4 + r % 4 of the flat array (the layout
+    include/same.h documents), padding slots 0; unpack_states inverts it, for
+    numpy arrays and torch tensors alike."""
+    import torch
+    rng = np.random.default_rng(m)
+    n, ld = 3, 12
+    rows = rng.integers(0, 100, (n, m, ld)).astype(np.int8)
+    q = same.pack_states(rows)
+    mq = (m + 3) // 4
+    assert q.shape == same.state_shape(n, m, ld) == (n, mq, ld, 4)
+    flat = q.reshape(-1)
+    for i in range(n):
+        for r in range(m):
+            for j in range(ld):
+                assert flat[((i * mq + r // 4) * ld + j) * 4 + r % 4] == rows[i, r, j]
+    pad = same.unpack_states(q, 4 * mq)[:, m:]
+    assert (pad == 0).all()
+    assert np.array_equal(same.unpack_states(q, m), rows)
+    t = same.pack_states(torch.from_numpy(rows.astype(np.int16)))
+    assert t.is_contiguous() and tuple(t.shape) == q.shape
+    assert np.array_equal(t.numpy(), q.astype(np.int16))
+    assert np.array_equal(same.unpack_states(t, m).numpy(), rows.astype(np.int16))
+
+
+def test_binding_refuses_states_in_another_layout():
+    """A states tensor that is not [n][ceil(m/4)][ld][4] is refused by the
+    binding before any device call."""
+    import torch
+    ctx = _ctx(koller())
+    with pytest.raises(same.SameError) as e:
+        same.same_counts(ctx, torch.zeros((ctx.n_nodes, 2, 8), dtype=torch.int8), 2, 8, 8, None, None, None)
+    assert e.value.code == same.SAME_EINVAL and "ceil(m/4)" in str(e.value)

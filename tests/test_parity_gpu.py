@@ -121,7 +121,7 @@ def test_column_tiles_and_step_are_bit_identical():
     _sweep_case(w, win=(3_000, 600), sweep_id=2)
     outs = []
     for ctx, fused in ((tiled, True), (whole, False)):
-        st = w.states[0].cuda()
+        st = same.pack_states(w.states[0]).cuda()
         ob = w.obs[0].cuda()
         th = torch.from_numpy(w.init_theta).cuda()
         mb = torch.zeros(ctx.cpt_total, dtype=torch.int32, device="cuda")
@@ -200,7 +200,7 @@ def test_ragged_tails(n_cols, ld):
     _custom_case(net, st, ob, th, 3, n_cols, win=(0, min(n_cols, 64)))
     ctx = H.context_for(net)
     mb = torch.zeros(ctx.cpt_total, dtype=torch.int32, device="cuda")
-    same.same_counts(ctx, torch.from_numpy(st).cuda(), 3, n_cols, ld, mb, None, ctx.new_workspace())
+    same.same_counts(ctx, torch.from_numpy(same.pack_states(st)).cuda(), 3, n_cols, ld, mb, None, ctx.new_workspace())
     torch.cuda.synchronize()
     assert np.array_equal(mb.cpu().numpy(), oracle.counts(net.parents, net.card, st, 3, n_cols))
 
@@ -303,7 +303,7 @@ def test_counts_bit_exact_and_moving_sum(cfg, kw):
     mb = torch.from_numpy(prev.copy()).cuda()
     tot = torch.from_numpy(tot0.astype(np.int32)).cuda()
     ws = ctx.new_workspace()
-    same.same_counts(ctx, st.cuda(), w.m, ncols, w.ld, mb, tot, ws)
+    same.same_counts(ctx, same.pack_states(st).cuda(), w.m, ncols, w.ld, mb, tot, ws)
     torch.cuda.synchronize()
     assert np.array_equal(mb.cpu().numpy(), want)
     assert np.array_equal(tot.cpu().numpy(), tot0 - prev + want)
@@ -311,7 +311,7 @@ def test_counts_bit_exact_and_moving_sum(cfg, kw):
     for i in range(net.n):
         assert want[off[i]:off[i + 1]].sum() == ncols * w.m
     # nullable totals; counting twice gives the same counts
-    same.same_counts(ctx, st.cuda(), w.m, ncols, w.ld, mb, None, ws)
+    same.same_counts(ctx, same.pack_states(st).cuda(), w.m, ncols, w.ld, mb, None, ws)
     torch.cuda.synchronize()
     assert np.array_equal(mb.cpu().numpy(), want)
 
@@ -327,7 +327,7 @@ def test_counts_large_cpt(n_par, K):
     net, st, _, _ = _custom(parents, card, 5000, 3, 0.0, 12)
     ctx = H.context_for(net)
     mb = torch.zeros(ctx.cpt_total, dtype=torch.int32, device="cuda")
-    same.same_counts(ctx, torch.from_numpy(st).cuda(), 3, 5000, st.shape[-1], mb, None,
+    same.same_counts(ctx, torch.from_numpy(same.pack_states(st)).cuda(), 3, 5000, st.shape[-1], mb, None,
                      ctx.new_workspace())
     torch.cuda.synchronize()
     assert np.array_equal(mb.cpu().numpy(), oracle.counts(parents, card, st, 3, 5000))
@@ -344,7 +344,7 @@ def test_counts_ragged_rows(n_cols, ld, big):
     st[:, :, n_cols:] = 120
     ctx = H.context_for(net)
     mb = torch.zeros(ctx.cpt_total, dtype=torch.int32, device="cuda")
-    same.same_counts(ctx, torch.from_numpy(st).cuda(), 3, n_cols, ld, mb, None, ctx.new_workspace())
+    same.same_counts(ctx, torch.from_numpy(same.pack_states(st)).cuda(), 3, n_cols, ld, mb, None, ctx.new_workspace())
     torch.cuda.synchronize()
     assert np.array_equal(mb.cpu().numpy(), oracle.counts(parents, card, st, 3, n_cols))
 
@@ -401,7 +401,7 @@ def test_lockstep_loop(cfg, kw, sweeps):
             new = oracle.counts(net.parents, net.card, states[b], w.m, nc)
             d_mb = torch.from_numpy(mb[b].astype(np.int32)).cuda()
             d_tot = torch.from_numpy(totals.astype(np.int32)).cuda()
-            same.same_counts(ctx, torch.from_numpy(states[b]).cuda(), w.m, nc, w.ld, d_mb, d_tot, ws)
+            same.same_counts(ctx, torch.from_numpy(same.pack_states(states[b])).cuda(), w.m, nc, w.ld, d_mb, d_tot, ws)
             totals = oracle.moving_sum(totals, mb[b], new)
             mb[b] = new
             th_gpu = torch.empty(ctx.cpt_total, dtype=torch.float32, device="cuda")
@@ -422,7 +422,7 @@ def test_independent_loops_agree_until_first_flagged_draw():
     ctx = H.context_for(net)
     color = oracle.graph(net.parents, net.card)["color"]
     ws = ctx.new_workspace()
-    d_st = w.states[0].cuda()
+    d_st = same.pack_states(w.states[0]).cuda()
     d_ob = w.obs[0].cuda()
     d_th = torch.from_numpy(w.init_theta).cuda()
     d_mb = torch.zeros(ctx.cpt_total, dtype=torch.int32, device="cuda")
@@ -444,7 +444,7 @@ def test_independent_loops_agree_until_first_flagged_draw():
         mb = new
         theta = oracle.dirichlet(net.parents, net.card, tot, w.alpha, w.seed, s)
         torch.cuda.synchronize()
-        g_st = d_st.cpu().numpy()
+        g_st = same.unpack_states(d_st.cpu().numpy(), w.m)
         if not np.array_equal(g_st, st):
             H.compare_states(g_st, st, res["flags"], color, w.n_cols)
             print("diverged at sweep", s, "on a flagged draw")
@@ -492,7 +492,7 @@ def test_tiled_step_counts_with_unaligned_rows(big):
     outs = []
     for tb in (1, 0):
         ctx = H.context_for(net, tile_bytes=tb)
-        d_st = torch.from_numpy(st.copy()).cuda()
+        d_st = torch.from_numpy(same.pack_states(st)).cuda()
         d_ob = torch.from_numpy(ob).cuda()
         d_th = torch.from_numpy(th.astype(np.float32)).cuda()
         mb = torch.zeros(ctx.cpt_total, dtype=torch.int32, device="cuda")
@@ -503,4 +503,36 @@ def test_tiled_step_counts_with_unaligned_rows(big):
         outs.append([x.cpu().numpy() for x in (d_st, mb, tot, d_th)])
     for x, y in zip(*outs):
         assert np.array_equal(x, y)
-    assert np.array_equal(outs[0][1], oracle.counts(parents, card, outs[0][0], m, n_cols))
+    assert np.array_equal(outs[0][1], oracle.counts(parents, card, same.unpack_states(outs[0][0], m), m, n_cols))
+
+
+@pytest.mark.parametrize("big", [False, True], ids=["int8", "int16"])
+def test_padding_slots_may_hold_anything(big):
+    """The padding slots of the last replica quad (m = 5: slots 5..7) may hold
+    any value, out of range included: the sweep reads them as state 0 and the
+    counts skip them, so a step (pre-pass counts, sweep, counts, resample)
+    gives the same real replicas, counts and CPTs whatever they hold."""
+    card = [130 if big else 3, 3, 200 if big else 4, 2, 5]
+    parents = [[], [0], [0, 1], [2], [1, 2, 3]]
+    n_cols, ld, m = 3001, 3004, 5
+    net, st, ob, th = _custom(parents, card, n_cols, m, 0.5, 31, ld=ld)
+    outs = []
+    for fill in (0, 30000 if big else 120):
+        q = same.pack_states(st)
+        q[:, -1, :, m % 4:] = fill
+        ctx = H.context_for(net)
+        d_st = torch.from_numpy(q).cuda()
+        d_ob = torch.from_numpy(ob).cuda()
+        d_th = torch.from_numpy(th.astype(np.float32)).cuda()
+        mb = torch.zeros(ctx.cpt_total, dtype=torch.int32, device="cuda")
+        tot = torch.zeros(ctx.cpt_total, dtype=torch.int32, device="cuda")
+        ws = ctx.new_workspace()
+        same.same_counts(ctx, d_st, m, n_cols, ld, mb, tot, ws)
+        for s in range(2):
+            same.same_step(ctx, d_st, d_ob, d_th, m, n_cols, ld, 0, 5, s, mb, tot, s, ws)
+        torch.cuda.synchronize()
+        outs.append([same.unpack_states(d_st.cpu().numpy(), m), mb.cpu().numpy(), tot.cpu().numpy(),
+                     d_th.cpu().numpy()])
+    for x, y in zip(*outs):
+        assert np.array_equal(x, y)
+    assert np.array_equal(outs[1][1], oracle.counts(parents, card, outs[1][0], m, n_cols))

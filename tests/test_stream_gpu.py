@@ -21,20 +21,22 @@ def _gpu():
 
 
 def _host_arrays(w):
-    """Pinned host [n][m][host_ld] states and [n][host_ld] obs holding all columns."""
+    """Pinned host states in the library's layout ([n][mq][host_ld][4]) and
+    [n][host_ld] obs holding all columns."""
     n = w.net.n
     host_ld = (w.n_cols + 3) // 4 * 4
-    st = torch.zeros((n, w.m, host_ld), dtype=w.states[0].dtype, pin_memory=True)
+    full = torch.zeros((n, w.m, host_ld), dtype=w.states[0].dtype)
     ob = torch.ones((n, host_ld), dtype=torch.uint8, pin_memory=True)
     for b in range(w.M):
         c0, nc = b * w.nb, w.mb_cols(b)
-        st[:, :, c0:c0 + nc] = w.states[b][:, :, :nc]
+        full[:, :, c0:c0 + nc] = w.states[b][:, :, :nc]
         ob[:, c0:c0 + nc] = w.obs[b][:, :nc]
-    return st, ob, host_ld
+    return same.pack_states(full).pin_memory(), ob, host_ld
 
 
 def _resident(w, ctx, passes):
-    dev = [s.cuda() for s in w.states]
+    """The device-resident call sequence; returns the states as [n][m][ld]."""
+    dev = [same.pack_states(s).cuda() for s in w.states]
     obs = [o.cuda() for o in w.obs]
     ws = ctx.new_workspace()
     cpts = torch.from_numpy(w.init_theta).cuda()
@@ -49,7 +51,7 @@ def _resident(w, ctx, passes):
             same.same_counts(ctx, dev[b], w.m, w.mb_cols(b), w.ld, mb[b], tot, ws)
             same.same_sample_cpts(ctx, tot, cpts, w.seed, s * w.M + b, ws)
     torch.cuda.synchronize()
-    return [d.cpu() for d in dev], mb.cpu(), tot.cpu(), cpts.cpu()
+    return [same.unpack_states(d.cpu(), w.m) for d in dev], mb.cpu(), tot.cpu(), cpts.cpu()
 
 
 def _streamed(w, ctx, passes, on_pass=None):
@@ -66,9 +68,9 @@ def _streamed(w, ctx, passes, on_pass=None):
                               slots, ws)
         if on_pass is not None:
             torch.cuda.synchronize()
-            on_pass(s, st, mb, tot, cpts)
+            on_pass(s, same.unpack_states(st, w.m), mb, tot, cpts)
     torch.cuda.synchronize()
-    return st, mb.cpu(), tot.cpu(), cpts.cpu()
+    return same.unpack_states(st, w.m), mb.cpu(), tot.cpu(), cpts.cpu()
 
 
 @pytest.mark.parametrize("cfg,kw", [

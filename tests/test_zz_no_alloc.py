@@ -44,7 +44,7 @@ def test_noalloc_counts_equal_same_counts(cfg, kw):
     w = make_workload(cfg, **kw)
     ctx = H.context_for(w.net)
     rng = np.random.default_rng(cfg)
-    st = w.states[0].cuda()
+    st = same.pack_states(w.states[0]).cuda()
     # first call: the whole minibatch; second: a smaller column range
     for n_cols in (w.mb_cols(0), w.mb_cols(0) // 3 + 1):
         prev = rng.integers(0, 500, ctx.cpt_total).astype(np.int32)
@@ -66,7 +66,7 @@ def test_noalloc_counts_without_totals_and_int16():
         st[i, :, :n_cols] = rng.integers(0, k, (m, n_cols))
     st[:, :, n_cols:] = 120
     ctx = H.context_for(Network("custom", parents, card))
-    d_st = torch.from_numpy(st).cuda()
+    d_st = torch.from_numpy(same.pack_states(st)).cuda()
     for cols in (n_cols, 1001):
         a = torch.zeros(ctx.cpt_total, dtype=torch.int32, device="cuda")
         b = torch.zeros(ctx.cpt_total, dtype=torch.int32, device="cuda")
@@ -81,7 +81,7 @@ def test_noalloc_errors():
     w = make_workload(1, n_cols=64)
     ctx = H.context_for(w.net)
     mb = torch.zeros(ctx.cpt_total, dtype=torch.int32, device="cuda")
-    st = w.states[0].cuda()
+    st = same.pack_states(w.states[0]).cuda()
     with pytest.raises(same.SameError) as e:
         same.same_counts_noalloc(ctx, st, w.m, 64, w.ld, mb, None)
     assert e.value.code == same.SAME_EINVAL
@@ -91,6 +91,6 @@ def test_noalloc_errors():
     big = H.context_for(Network("big", parents, [8] * 7))
     assert big.cpt_total > (1 << 21)
     with pytest.raises(same.SameError) as e:
-        same.same_counts_noalloc(big, torch.zeros((7, 1, 4), dtype=torch.int8, device="cuda"), 1, 4, 4,
+        same.same_counts_noalloc(big, torch.zeros(same.state_shape(7, 1, 4), dtype=torch.int8, device="cuda"), 1, 4, 4,
                                  torch.zeros(8, dtype=torch.int32, device="cuda"), None)
     assert e.value.code == same.SAME_ESIZE
