@@ -29,7 +29,7 @@ __device__ __forceinline__ cint32_t *as_const(const int32_t *p) { return (cint32
 
 constexpr int kBlock = 256;          // 4 wavefronts of 64
 constexpr int kSweepBlock = 256;     // threads of a sweep block
-constexpr int kSweepWaves = 5;       // waves per SIMD the fast sweep kernel is compiled for
+constexpr int kSweepWaves = 6;       // waves per SIMD the fast sweep kernel is compiled for
 
 // ---------------------------------------------------------------- state quads
 //
@@ -410,7 +410,7 @@ constexpr uint32_t kXcds = 8;
 constexpr int kSweepQuadsPerLane = 1;  // column quads per lane in one sweep block
 constexpr int kMinSweepBlocks = 4096;  // replicas are split below this many blocks
 constexpr int64_t kMinSweepQuads = 64;  // narrowest column chunk of a fast sweep block (quads)
-constexpr int kCountQuadsPerLane = 4;  // adjacent columns (state quads) per lane and iteration of a count block
+constexpr int kCountQuadsPerLane = 8;  // adjacent columns (state quads) per lane and iteration of a count block
 
 __device__ __forceinline__ void decode_block(uint32_t b, uint32_t count, uint32_t &local,
                                              int64_t &slab) {
@@ -1978,9 +1978,9 @@ hipError_t launch_counts(const DeviceTables &t, const void *states, int32_t stat
                          hipStream_t stream) {
     if (n_cols <= 0) return hipSuccess;
     const int32_t n = t.n_cwork;
-    // one node x 4096 columns (kCountQuadsPerLane columns per lane and
-    // iteration) x all replica quads per block, XCD-swizzled like the sweep
-    const int64_t cols_per_block = 4 * dev::kBlock * dev::kCountQuadsPerLane;
+    // one node x 4096 columns (two lane iterations of kCountQuadsPerLane
+    // columns) x all replica quads per block, XCD-swizzled like the sweep
+    const int64_t cols_per_block = 2 * dev::kBlock * dev::kCountQuadsPerLane;
     const int64_t col_slabs = (n_cols + cols_per_block - 1) / cols_per_block;
     // small launches split the replica quads (in runs of kCountQuads) over
     // blocks until there are kMinSweepBlocks blocks, so that they fill the
