@@ -29,7 +29,9 @@
  *         minibatch column j, written states[i][r][j] below, is element
  *         ((i * mq + r / 4) * ld + j) * 4 + r % 4.  The four replicas
  *         4q .. 4q + 3 of one column (a state quad) are adjacent, so the
- *         sweep reads and writes them with one access.  Column j of a
+ *         sweep reads and writes them with one access.  With 4-bit states
+ *         (same_options_t.state_bits = 4) the array is [n][mq][ld] of 16-bit
+ *         words, one state quad each, replica 4q + s in bits 4s .. 4s + 3.  Column j of a
  *         minibatch is global column col_offset + j.  Observed entries must
  *         hold the observed value in every replica.  Values must lie in
  *         [0, K_i) (out-of-range values are undefined behaviour).  Slots
@@ -84,10 +86,12 @@ typedef struct {
     int32_t n_colors;     /* colour groups of the moralized graph */
     int64_t cpt_total;    /* CPT entries */
     int64_t n_rows;       /* CPT rows (distributions) */
-    int32_t state_bytes;  /* 1: int8 states, 2: int16 states */
+    int32_t state_bytes;  /* bytes of one state in the element arrays (CSR values, targets,
+                             compact host states): 1, or 2 for 16-bit states */
     int32_t max_card;     /* largest K_i */
     int32_t sweep_launches;  /* sweep kernel launches per same_sweep call */
     int32_t table_nodes;     /* nodes drawing from precomputed threshold tables */
+    int32_t state_bits;      /* bits per state in the states array: 4, 8 or 16 (see States) */
 } same_layout_t;
 
 /*
@@ -139,6 +143,11 @@ typedef struct {
      * first-fit colouring as it is.  The colouring fixes the order of the
      * sequential scan the sweep equals, so it changes the sample path. */
     int32_t first_fit_colours;
+    /* 0 (default): 8-bit states (16-bit when some K > 127); 4: 4-bit states,
+     * a state quad in one 16-bit word (every K must be <= 16, else
+     * SAME_ECARD).  The states array's format follows (see States); results
+     * do not depend on it. */
+    int32_t state_bits;
 } same_options_t;
 
 /* same_create with options (opts may be NULL for the defaults). */

@@ -47,7 +47,7 @@ class SameError(RuntimeError):
 
 class _Options(C.Structure):
     _fields_ = [("table_limit", C.c_int64), ("tile_bytes", C.c_int64), ("lds_limit", C.c_int64),
-                ("packed_indices", C.c_int32), ("first_fit_colours", C.c_int32)]
+                ("packed_indices", C.c_int32), ("first_fit_colours", C.c_int32), ("state_bits", C.c_int32)]
 
 
 class _KernelTimes(C.Structure):
@@ -58,7 +58,7 @@ class _KernelTimes(C.Structure):
 class _Layout(C.Structure):
     _fields_ = [("n_nodes", C.c_int32), ("n_colors", C.c_int32), ("cpt_total", C.c_int64),
                 ("n_rows", C.c_int64), ("state_bytes", C.c_int32), ("max_card", C.c_int32),
-                ("sweep_launches", C.c_int32), ("table_nodes", C.c_int32)]
+                ("sweep_launches", C.c_int32), ("table_nodes", C.c_int32), ("state_bits", C.c_int32)]
 
 
 def library_path() -> str:
@@ -141,30 +141,57 @@ def _ptr(t):
     return C.c_void_p(t.data_ptr())
 
 
-def state_shape(n, m, ld):
+def state_shape(n, m, ld, bits=8):
     """Shape of a states array of n nodes, m replicas and leading dimension
-    ld: replica quads [n][ceil(m / 4)][ld][4] (see include/same.h)."""
-    return (int(n), (int(m) + 3) // 4, int(ld), 4)
+    ld: replica quads [n][ceil(m / 4)][ld][4] of 8- or 16-bit states, or
+    [n][ceil(m / 4)][ld] 16-bit words of four 4-bit states (see
+    include/same.h)."""
+    mq = (int(m) + 3) // 4
+    return (int(n), mq, int(ld)) if bits == 4 else (int(n), mq, int(ld), 4)
 
 
-def pack_states(states):
-    """[n][m][ld] (replica rows) -> the library's [n][ceil(m/4)][ld][4]
-    (replica quads, padding slots 0).  torch tensor (same device) or numpy
-    array; a layout permutation for callers, not part of any entry point."""
+def pack_states(states, bits=None):
+    """[n][m][ld] (replica rows) -> the library's replica quads (padding slots
+    0): [n][ceil(m/4)][ld][4] in the same dtype, or with bits=4 (values below
+    16) [n][ceil(m/4)][ld] int16 words, replica 4q + s in bits 4s .. 4s + 3.
+    torch tensor (same device) or numpy array; a layout permutation for
+    callers, not part of any entry point."""
     n, m, ld = states.shape
     mq = (m + 3) // 4
     pad = 4 * mq - m
     if isinstance(states, np.ndarray):
         if pad:
             states = np.concatenate([states, np.zeros((n, pad, ld), dtype=states.dtype)], axis=1)
-        return np.ascontiguousarray(states.reshape(n, mq, 4, ld).transpose(0, 1, 3, 2))
+        q = np.ascontiguousarray(states.reshape(n, mq, 4, ld).transpose(0, 1, 3, 2))
+        if bits == 4:
+            w = q.astype(np.int32) & 0xF
+            q = (w[..., 0] | (w[..., 1] << 4) | (w[..., 2] << 8) | (w[..., 3] << 12)).astype(np.uint16).view(np.int16)
+            q = np.ascontiguousarray(q)
+        return q
     if pad:
         states = torch_cat([states, states.new_zeros((n, pad, ld))], 1)
-    return states.reshape(n, mq, 4, ld).permute(0, 1, 3, 2).contiguous()
+    q = states.reshape(n, mq, 4, ld).permute(0, 1, 3, 2).contiguous()
+    if bits == 4:
+        import torch
+        w = q.to(torch.int32) & 0xF
+        q = (w[..., 0] | (w[..., 1] << 4) | (w[..., 2] << 8) | (w[..., 3] << 12))
+        q = torch.where(q >= 0x8000, q - 0x10000, q).to(torch.int16).contiguous()
+    return q
 
 
-def unpack_states(quads, m):
-    """The library's [n][mq][ld][4] -> [n][m][ld] (padding slots dropped)."""
+def unpack_states(quads, m, bits=None):
+    """The library's replica quads -> [n][m][ld] (padding slots dropped); with
+    bits=4 the int16 words of four 4-bit states, returned as int8."""
+    if bits == 4:
+        n, mq, ld = quads.shape
+        if isinstance(quads, np.ndarray):
+            w = quads.view(np.uint16).astype(np.int32)
+            q = np.stack([(w >> (4 * s)) & 0xF for s in range(4)], axis=-1).astype(np.int8)
+        else:
+            import torch
+            w = quads.to(torch.int32) & 0xFFFF
+            q = torch.stack([(w >> (4 * s)) & 0xF for s in range(4)], dim=-1).to(torch.int8)
+        quads = q
     n, mq, ld, four = quads.shape
     assert four == 4 and 4 * mq >= m
     if isinstance(quads, np.ndarray):
@@ -182,9 +209,9 @@ def _st(ctx, t, m, ld, what="states"):
     tensor in another layout is refused here, before any device call."""
     if t is None or isinstance(t, int):
         return t
-    want = state_shape(ctx.n_nodes, m, ld)
+    want = state_shape(ctx.n_nodes, m, ld, ctx.state_bits)
     if tuple(t.shape) != want:
-        raise SameError(SAME_EINVAL, "%s must have shape %s ([n][ceil(m/4)][ld][4], see pack_states), got %s"
+        raise SameError(SAME_EINVAL, "%s must have shape %s (replica quads, see pack_states), got %s"
                         % (what, want, tuple(t.shape)))
     if hasattr(t, "is_contiguous") and not t.is_contiguous():
         raise SameError(SAME_EINVAL, "%s must be contiguous" % what)
@@ -204,19 +231,20 @@ class Context:
     """Owns one same_ctx (one network)."""
 
     def __init__(self, parent_ptr, parent_idx, card, dirichlet_prior=1.0, table_limit=None,
-                 tile_bytes=0, lds_limit=None, packed_indices=True, first_fit_colours=False):
+                 tile_bytes=0, lds_limit=None, packed_indices=True, first_fit_colours=False, state_bits=0):
         L = load_library()
         self._pptr = np.ascontiguousarray(parent_ptr, dtype=np.int32)
         self._pidx = np.ascontiguousarray(parent_idx if len(parent_idx) else [0], dtype=np.int32)
         self._card = np.ascontiguousarray(card, dtype=np.int32)
         h = C.c_void_p()
-        if table_limit is None and not tile_bytes and lds_limit is None and packed_indices and not first_fit_colours:
+        if (table_limit is None and not tile_bytes and lds_limit is None and packed_indices and not first_fit_colours
+                and not state_bits):
             _check(L.same_create(len(self._card), self._pptr.ctypes.data, self._pidx.ctypes.data,
                                  self._card.ctypes.data, float(dirichlet_prior), C.byref(h)))
         else:
             opts = _Options(-1 if table_limit is None else int(table_limit), int(tile_bytes),
                             -1 if lds_limit is None else int(lds_limit), 1 if packed_indices else 0,
-                            1 if first_fit_colours else 0)
+                            1 if first_fit_colours else 0, int(state_bits))
             _check(L.same_create_ex(len(self._card), self._pptr.ctypes.data,
                                     self._pidx.ctypes.data, self._card.ctypes.data,
                                     float(dirichlet_prior), C.byref(opts), C.byref(h)))
@@ -229,6 +257,7 @@ class Context:
         self.cpt_total, self.n_rows = lay.cpt_total, lay.n_rows
         self.state_bytes, self.max_card = lay.state_bytes, lay.max_card
         self.sweep_launches, self.table_nodes = lay.sweep_launches, lay.table_nodes
+        self.state_bits = lay.state_bits
         self.cpt_off, self.color = off, col
         ws = C.c_size_t()
         _check(L.same_workspace_size(self._h, C.byref(ws)))
@@ -260,10 +289,11 @@ def same_create(parent_ptr, parent_idx, card, dirichlet_prior=1.0) -> Context:
 
 
 def same_create_ex(parent_ptr, parent_idx, card, dirichlet_prior=1.0, table_limit=-1,
-                   tile_bytes=0, lds_limit=-1, packed_indices=True, first_fit_colours=False) -> Context:
+                   tile_bytes=0, lds_limit=-1, packed_indices=True, first_fit_colours=False,
+                   state_bits=0) -> Context:
     return Context(parent_ptr, parent_idx, card, dirichlet_prior, table_limit=table_limit,
                    tile_bytes=tile_bytes, lds_limit=lds_limit, packed_indices=packed_indices,
-                   first_fit_colours=first_fit_colours)
+                   first_fit_colours=first_fit_colours, state_bits=state_bits)
 
 
 def same_destroy(ctx: Context) -> None:
@@ -273,7 +303,7 @@ def same_destroy(ctx: Context) -> None:
 def same_layout(ctx: Context) -> dict:
     return {"n_nodes": ctx.n_nodes, "n_colors": ctx.n_colors, "cpt_total": ctx.cpt_total,
             "n_rows": ctx.n_rows, "state_bytes": ctx.state_bytes, "max_card": ctx.max_card,
-            "sweep_launches": ctx.sweep_launches, "table_nodes": ctx.table_nodes,
+            "sweep_launches": ctx.sweep_launches, "table_nodes": ctx.table_nodes, "state_bits": ctx.state_bits,
             "cpt_off": ctx.cpt_off.copy(), "color": ctx.color.copy()}
 
 

@@ -30,8 +30,9 @@ inline size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 // States are stored as replica quads, [n][mq][ld][4] with mq = ceil(m / 4):
 // one node's block holds mq * ld * 4 states.
 inline int64_t replica_quads(int32_t m) { return ((int64_t)m + 3) / 4; }
-inline double node_state_bytes(int32_t m, int64_t ld, int32_t sb) {
-    return (double)replica_quads(m) * 4.0 * (double)ld * (double)sb;
+// quad_bytes: 2, 4 or 8 (4-, 8- or 16-bit states)
+inline double node_state_bytes(int32_t m, int64_t ld, int32_t quad_bytes) {
+    return (double)replica_quads(m) * (double)ld * (double)quad_bytes;
 }
 
 }  // namespace
@@ -231,11 +232,11 @@ int check_minibatch(const same_ctx *ctx, const void *states, int32_t m, int64_t 
     if (m < 1 || m > 65535) return set_error(SAME_EINVAL, "m must be in [1, 65535]");
     if (n_cols < 0 || ld < n_cols) return set_error(SAME_EINVAL, "need 0 <= n_cols <= ld");
     if (ld % 4 != 0) return set_error(SAME_EALIGN, "ld must be a multiple of 4");
-    if (!aligned(states, 4 * (size_t)ctx->g.state_bytes))
-        return set_error(SAME_EALIGN, "states must be aligned to 4 state elements");
-    if (node_state_bytes(m, ld, ctx->g.state_bytes) >= 2147483648.0)
+    if (!aligned(states, (size_t)ctx->g.quad_bytes))
+        return set_error(SAME_EALIGN, "states must be aligned to a state quad");
+    if (node_state_bytes(m, ld, ctx->g.quad_bytes) >= 2147483648.0)
         return set_error(SAME_ESIZE, "one node's state quads (4 * ceil(m / 4) * ld states) must stay below 2^31 bytes");
-    if ((double)ctx->g.n * node_state_bytes(m, ld, ctx->g.state_bytes) > 9.0e18)
+    if ((double)ctx->g.n * node_state_bytes(m, ld, ctx->g.quad_bytes) > 9.0e18)
         return set_error(SAME_ESIZE, "states array too large");
     return SAME_OK;
 }
@@ -247,7 +248,7 @@ int check_minibatch(const same_ctx *ctx, const void *states, int32_t m, int64_t 
 // cost more than the cache saves, so the default is one tile.
 int64_t tile_cols(const same_ctx *ctx, int32_t m, int64_t n_cols) {
     if (ctx->tile_bytes <= 0.0) return n_cols;
-    const double per_col = (double)ctx->g.n * (4.0 * (double)replica_quads(m) * ctx->g.state_bytes + 1.0);
+    const double per_col = (double)ctx->g.n * ((double)replica_quads(m) * ctx->g.quad_bytes + 1.0);
     int64_t t = (int64_t)(ctx->tile_bytes / per_col) / 1024 * 1024;
     if (t < 1024) t = 1024;
     return t >= n_cols ? n_cols : t;
@@ -309,7 +310,7 @@ int prepare_sweep(same_ctx *ctx, same::DeviceTables *t, void *states, const uint
 int sweep_tile(same_ctx *ctx, const same::SweepParams &P0, int64_t t0, int64_t nt, hipStream_t s) {
     const same::Compiled &g = ctx->g;
     same::SweepParams P = P0;
-    P.states = (char *)P0.states + t0 * 4 * g.state_bytes;  // column t0 of every quad row
+    P.states = (char *)P0.states + t0 * g.quad_bytes;  // column t0 of every quad row
     P.obs = P0.obs + t0;
     P.n_cols = nt;
     P.col_offset = P0.col_offset + t0;
@@ -348,7 +349,7 @@ int sweep_tile(same_ctx *ctx, const same::SweepParams &P0, int64_t t0, int64_t n
                 if (!rc) rc = check_hip(hipEventRecord(rec.start, ls), "hipEventRecord");
                 if (rc) return rc;
             }
-            rc = check_hip(same::launch_sweep(P, b, e - b, k, g.launch_lds[c * L + k], g.state_bytes, ls),
+            rc = check_hip(same::launch_sweep(P, b, e - b, k, g.launch_lds[c * L + k], g.state_bits, ls),
                            "sweep launch");
             if (rc) return rc;
             if (timed) {
@@ -446,7 +447,7 @@ int do_step(same_ctx *ctx, void *states, const uint8_t *obs, float *cpts, int32_
         const int64_t nt = n_cols - t0 < T ? n_cols - t0 : T;
         rc = sweep_tile(ctx, P, t0, nt, s);
         if (rc) return rc;
-        rc = check_hip(same::launch_counts(*t, states, ctx->g.state_bytes, m, t0, nt, ld, newc, s),
+        rc = check_hip(same::launch_counts(*t, states, ctx->g.state_bits, m, t0, nt, ld, newc, s),
                        "count launch");
         if (rc) return rc;
     }
@@ -470,7 +471,7 @@ struct SlotGeom {
 SlotGeom slot_geom(const same_ctx *ctx, int32_t m, int64_t nb) {
     SlotGeom s;
     s.ld = (nb + 63) / 64 * 64;
-    s.states = align_up((size_t)ctx->g.n * (size_t)node_state_bytes(m, s.ld, ctx->g.state_bytes));
+    s.states = align_up((size_t)ctx->g.n * (size_t)node_state_bytes(m, s.ld, ctx->g.quad_bytes));
     s.bytes = s.states + align_up((size_t)ctx->g.n * (size_t)s.ld);
     return s;
 }
@@ -504,6 +505,9 @@ int same_create_ex(int32_t n_nodes, const int32_t *parent_ptr, const int32_t *pa
     if (opts && opts->first_fit_colours != 0 && opts->first_fit_colours != 1)
         return set_error(SAME_EINVAL, "first_fit_colours must be 0 or 1");
     const bool balance = !opts || opts->first_fit_colours == 0;
+    if (opts && opts->state_bits != 0 && opts->state_bits != 4)
+        return set_error(SAME_EINVAL, "state_bits must be 0 or 4");
+    const int32_t state_bits = opts ? opts->state_bits : 0;
     *out = nullptr;
     if (!(dirichlet_prior > 0.0)) return set_error(SAME_EINVAL, "dirichlet_prior must be > 0");
     same_ctx *ctx = new (std::nothrow) same_ctx();
@@ -512,7 +516,7 @@ int same_create_ex(int32_t n_nodes, const int32_t *parent_ptr, const int32_t *pa
     int rc;
     try {
         rc = same::compile_graph(n_nodes, parent_ptr, parent_idx, card, ctx->g, err, table_limit,
-                                 lds_limit, packed, balance);
+                                 lds_limit, packed, balance, state_bits);
     } catch (const std::bad_alloc &) {
         rc = SAME_ENOMEM;
         err = "out of host memory";
@@ -551,6 +555,7 @@ int same_layout(const same_ctx *ctx, same_layout_t *out, int64_t *cpt_off, int32
     out->cpt_total = g.off[g.n];
     out->n_rows = g.n_rows;
     out->state_bytes = g.state_bytes;
+    out->state_bits = g.state_bits;
     out->max_card = g.max_card;
     const int32_t L = same::kLaunchClasses;
     int32_t launches = 0;
@@ -634,7 +639,7 @@ int same_counts(same_ctx *ctx, const void *states, int32_t m, int64_t n_cols, in
     int32_t *newc = (int32_t *)((char *)workspace + ctx->ws_counts);
     rc = check_hip(same::launch_fill_zero(newc, total, s), "count clear launch");
     if (rc) return rc;
-    rc = check_hip(same::launch_counts(*t, states, ctx->g.state_bytes, m, 0, n_cols, ld, newc, s),
+    rc = check_hip(same::launch_counts(*t, states, ctx->g.state_bits, m, 0, n_cols, ld, newc, s),
                    "count launch");
     if (rc) return rc;
     return check_hip(same::launch_moving_sum(newc, mb_counts, totals, total, s), "moving-sum launch");
@@ -706,7 +711,7 @@ int stream_pass_impl(same_ctx *ctx, void *host_states, const uint8_t *host_obs, 
     int rc = stream_res_for_current_device(ctx, &sr);
     if (rc) return rc;
     hipStream_t cs = (hipStream_t)stream;
-    const size_t sb = 4 * (size_t)ctx->g.state_bytes;  // bytes of one column of a quad row
+    const size_t sb = (size_t)ctx->g.quad_bytes;  // bytes of one column of a quad row
     const int64_t rows = (int64_t)ctx->g.n * replica_quads(m);
     const int64_t M = (n_cols + nb - 1) / nb;
     for (int64_t b = 0; b < M; ++b) {
@@ -813,7 +818,7 @@ int same_counts_ema(same_ctx *ctx, const void *states, int32_t m, int64_t n_cols
     int32_t *newc = (int32_t *)((char *)workspace + ctx->ws_counts);
     rc = check_hip(same::launch_fill_zero(newc, total, s), "count clear launch");
     if (rc) return rc;
-    rc = check_hip(same::launch_counts(*t, states, ctx->g.state_bytes, m, 0, n_cols, ld, newc, s),
+    rc = check_hip(same::launch_counts(*t, states, ctx->g.state_bits, m, 0, n_cols, ld, newc, s),
                    "count launch");
     if (rc) return rc;
     return check_hip(same::launch_ema(newc, totals, decay, total, s), "moving-sum launch");
@@ -849,7 +854,7 @@ int same_counts_noalloc(same_ctx *ctx, const void *states, int32_t m, int64_t n_
     hipStream_t s = (hipStream_t)stream;
     rc = check_hip(same::launch_fill_zero(newc, total, s), "count clear launch");
     if (rc) return rc;
-    rc = check_hip(same::launch_counts(*t, states, ctx->g.state_bytes, m, 0, n_cols, ld, newc, s), "count launch");
+    rc = check_hip(same::launch_counts(*t, states, ctx->g.state_bits, m, 0, n_cols, ld, newc, s), "count launch");
     if (rc) return rc;
     return check_hip(same::launch_moving_sum(newc, mb_counts, totals, total, s), "moving-sum launch");
 }
@@ -908,7 +913,7 @@ extern "C" int same_expand_observed(same_ctx *ctx, const int64_t *row_ptr, const
     if (nnz > 0 && (!col_idx || !values)) return set_error(SAME_EINVAL, "col_idx and values must be non-null");
     if (!aligned(obs, 4)) return set_error(SAME_EALIGN, "obs must be 4-byte aligned");
     return check_hip(same::launch_expand(row_ptr, ctx->g.n, col_idx, values, nnz, m, n_cols, ld,
-                                         ctx->g.state_bytes, states, obs, (hipStream_t)stream),
+                                         ctx->g.state_bits, states, obs, (hipStream_t)stream),
                      "expand launch");
 }
 
@@ -926,7 +931,7 @@ extern "C" int same_init_latent(same_ctx *ctx, void *states, const uint8_t *obs,
     rc = tables_for_current_device(ctx, &t);
     if (rc) return rc;
     return check_hip(same::launch_init_latent(*t, ctx->g.n, m, n_cols, ld, col_offset, (uint32_t)seed,
-                                              (uint32_t)(seed >> 32), ctx->g.state_bytes, states, obs,
+                                              (uint32_t)(seed >> 32), ctx->g.state_bits, states, obs,
                                               (hipStream_t)stream),
                      "latent init launch");
 }
@@ -948,7 +953,7 @@ extern "C" int same_accumulate_hits(same_ctx *ctx, const void *states, const voi
                                     int64_t n_cols, int64_t ld, int32_t *hits, void *stream) {
     int rc = check_hits_args(ctx, states, target, m, n_cols, ld, hits);
     if (rc) return rc;
-    return check_hip(same::launch_hits(states, target, ctx->g.n, m, n_cols, ld, ctx->g.state_bytes, hits,
+    return check_hip(same::launch_hits(states, target, ctx->g.n, m, n_cols, ld, ctx->g.state_bits, hits,
                                        (hipStream_t)stream),
                      "hits launch");
 }
@@ -963,7 +968,7 @@ extern "C" int same_predict(same_ctx *ctx, void *states, const uint8_t *obs, con
         rc = do_sweep(ctx, states, obs, cpts, m, n_cols, ld, col_offset, seed, sweep_id0 + (uint32_t)s, 0, 0,
                       nullptr, workspace, stream);
         if (rc) return rc;
-        rc = check_hip(same::launch_hits(states, target, ctx->g.n, m, n_cols, ld, ctx->g.state_bytes, hits,
+        rc = check_hip(same::launch_hits(states, target, ctx->g.n, m, n_cols, ld, ctx->g.state_bits, hits,
                                          (hipStream_t)stream),
                        "hits launch");
         if (rc) return rc;
@@ -979,11 +984,11 @@ extern "C" int same_grow_replicas(same_ctx *ctx, const void *states, int32_t m, 
     if (rc) return rc;
     if (m2 < m) return set_error(SAME_EINVAL, "m2 must be >= m");
     const char *a = (const char *)states, *b = (const char *)dst;
-    const int32_t sb = ctx->g.state_bytes;
-    if (a < b + (size_t)(ctx->g.n * node_state_bytes(m2, ld, sb)) &&
-        b < a + (size_t)(ctx->g.n * node_state_bytes(m, ld, sb)))
+    const int32_t qb = ctx->g.quad_bytes;
+    if (a < b + (size_t)(ctx->g.n * node_state_bytes(m2, ld, qb)) &&
+        b < a + (size_t)(ctx->g.n * node_state_bytes(m, ld, qb)))
         return set_error(SAME_EINVAL, "states and dst must not overlap");
-    return check_hip(same::launch_grow(states, m, dst, m2, ctx->g.n, ld, sb, (hipStream_t)stream),
+    return check_hip(same::launch_grow(states, m, dst, m2, ctx->g.n, ld, ctx->g.state_bits, (hipStream_t)stream),
                      "replica growth launch");
 }
 
@@ -1142,7 +1147,7 @@ int same_stream_pass_compact(same_ctx *ctx, void *lat_host, const int64_t *lat_o
         if (!rc)
             rc = check_hip(same::launch_expand_compact(obs_dev, data_dev, ld_dev, c0, cols, n, m, prefix,
                                                        d_off + b * n, blk0, staging[sl], d_states, d_obs,
-                                                       cg.dense.ld, ctx->g.state_bytes, cs),
+                                                       cg.dense.ld, ctx->g.state_bits, cs),
                            "expand launch");
         if (rc) return rc;
         int32_t *mb = mb_counts + b * total;
@@ -1156,7 +1161,7 @@ int same_stream_pass_compact(same_ctx *ctx, void *lat_host, const int64_t *lat_o
         } else {
             rc = check_hip(same::launch_gather_compact(obs_dev, ld_dev, c0, cols, n, m, prefix, d_off + b * n,
                                                        blk0, d_states, cg.dense.ld, staging[sl],
-                                                       ctx->g.state_bytes, cs),
+                                                       ctx->g.state_bits, cs),
                            "gather launch");
             if (!rc) rc = check_hip(hipEventRecord(sr->ev_comp[sl], cs), "event");
             if (!rc) rc = check_hip(hipStreamWaitEvent(sr->down, sr->ev_comp[sl], 0), "wait");

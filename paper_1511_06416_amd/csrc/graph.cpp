@@ -88,7 +88,7 @@ static void balance_colours(const std::vector<std::vector<int32_t>> &nb, int32_t
 
 int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int32_t *card,
                   Compiled &g, std::string &err, int64_t table_limit, int64_t lds_limit, bool packed,
-                  bool balance) {
+                  bool balance, int32_t state_bits) {
     if (n <= 0) return fail(err, SAME_EINVAL, "n_nodes must be positive");
     if (!pptr || !card) return fail(err, SAME_EINVAL, "parent_ptr and card must be non-null");
     if (pptr[0] != 0) return fail(err, SAME_EGRAPH, "parent_ptr[0] must be 0");
@@ -118,7 +118,14 @@ int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int
             return fail(err, SAME_EGRAPH, "node " + std::to_string(i) + ": duplicate parent");
         g.max_card = std::max(g.max_card, card[i]);
     }
-    g.state_bytes = g.max_card <= 127 ? 1 : 2;
+    if (state_bits == 4) {
+        if (g.max_card > 16) return fail(err, SAME_ECARD, "4-bit states need every cardinality <= 16");
+        g.state_bits = 4;
+    } else {
+        g.state_bits = g.max_card <= 127 ? 8 : 16;
+    }
+    g.state_bytes = g.state_bits == 16 ? 2 : 1;
+    g.quad_bytes = g.state_bits / 2;
 
     // children with the slot they occupy in the child's parent list
     std::vector<std::vector<std::pair<int32_t, int32_t>>> kids(n);

@@ -106,7 +106,9 @@ struct Compiled {
     std::vector<int32_t> color;      // [n]
     int32_t n_colors = 0;
     std::vector<std::vector<int32_t>> groups;  // nodes of each colour, ascending
-    int32_t state_bytes = 1;
+    int32_t state_bytes = 1;   // bytes of one state in the non-quad arrays (values, targets, compact states)
+    int32_t state_bits = 8;    // bits per state in a state quad: 4, 8 or 16
+    int32_t quad_bytes = 4;    // bytes of one state quad (four replicas of a column): 2, 4 or 8
     int32_t max_card = 0;
     int64_t n_rows = 0;
 
@@ -172,8 +174,11 @@ struct Compiled {
 // record staged whole, and the most a larger record stages of its groups.
 // packed: false sends every product-mode node to the wide class.
 // balance: false keeps the first-fit colouring (no balancing moves).
+// state_bits: 0 picks 8-bit states (16-bit when some K > 127); 4 asks for
+// 4-bit states (every K <= 16, else SAME_ECARD).
 int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int32_t *card,
                   Compiled &out, std::string &err, int64_t table_limit = kDefaultTableLimit,
-                  int64_t lds_limit = kDefaultLdsBytes, bool packed = true, bool balance = true);
+                  int64_t lds_limit = kDefaultLdsBytes, bool packed = true, bool balance = true,
+                  int32_t state_bits = 0);
 
 }  // namespace same

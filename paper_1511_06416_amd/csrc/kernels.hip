@@ -40,14 +40,22 @@ constexpr int kSweepWaves = 6;       // waves per SIMD the fast sweep kernel is 
 // 8 for int16) and travel in one load or store.  Slots >= m of the last quad
 // are padding.
 
-// Elements per node: mq quads of ld columns.
-__device__ __forceinline__ int64_t node_stride(int32_t m, int64_t ld) { return (int64_t)((m + 3) >> 2) * ld * 4; }
+// With 4-bit states (the Nib format) a quad is one 16-bit word, replica slot
+// s in bits 4s .. 4s + 3.  Kernels address states in bytes: a node's block is
+// node_bytes long and quad (rq, j) sits quad_boff bytes into it.
 
-// Byte offset of quad rq at column j inside a node's block.
+struct Nib {};  // tag type of the 4-bit format
+
+// Element type of the arrays that hold single states (CSR values, targets,
+// compact states): the state type, int8 for 4-bit states.
 template <typename ST>
-__device__ __forceinline__ uint32_t quad_boff(int rq, int64_t ld, int64_t j) {
-    return (uint32_t)(((int64_t)rq * ld + j) * 4 * (int64_t)sizeof(ST));
-}
+struct ElemOf {
+    using T = ST;
+};
+template <>
+struct ElemOf<Nib> {
+    using T = int8_t;
+};
 
 template <typename ST>
 struct Quad;
@@ -55,7 +63,11 @@ struct Quad;
 template <>
 struct Quad<int8_t> {
     using V = uint32_t;
+    static constexpr int kBytes = 4;
+    static constexpr uint32_t kMask = 0xffu;  // one state's bits
     __device__ static V load(const int8_t *p) { return *reinterpret_cast<const uint32_t *>(p); }
+    __device__ static V load_at(const char *p) { return *reinterpret_cast<const uint32_t *>(p); }
+    __device__ static void store_at(char *p, V v) { *reinterpret_cast<uint32_t *>(p) = v; }
     __device__ static V load_buffer(__amdgpu_buffer_rsrc_t r, uint32_t boff) {
         return __builtin_amdgcn_raw_buffer_load_b32(r, (int)boff, 0, 0);
     }
@@ -85,7 +97,11 @@ struct Quad<int8_t> {
 template <>
 struct Quad<int16_t> {
     using V = uint2;
+    static constexpr int kBytes = 8;
+    static constexpr uint32_t kMask = 0xffffu;
     __device__ static V load(const int16_t *p) { return *reinterpret_cast<const uint2 *>(p); }
+    __device__ static V load_at(const char *p) { return *reinterpret_cast<const uint2 *>(p); }
+    __device__ static void store_at(char *p, V v) { *reinterpret_cast<uint2 *>(p) = v; }
     // one 8-byte load (the quad's offset is a multiple of 8 bytes)
     __device__ static V load_buffer(__amdgpu_buffer_rsrc_t r, uint32_t boff) {
         typedef uint32_t w2 __attribute__((ext_vector_type(2)));
@@ -131,6 +147,46 @@ struct Quad<int16_t> {
     __device__ static constexpr int half_of(int c) { return c & 1; }
 };
 
+template <>
+struct Quad<Nib> {
+    using V = uint32_t;  // the quad in the low 16 bits
+    static constexpr int kBytes = 2;
+    static constexpr uint32_t kMask = 0xfu;
+    __device__ static V load_at(const char *p) { return *reinterpret_cast<const uint16_t *>(p); }
+    __device__ static void store_at(char *p, V v) { *reinterpret_cast<uint16_t *>(p) = (uint16_t)v; }
+    __device__ static V load_buffer(__amdgpu_buffer_rsrc_t r, uint32_t boff) {
+        return (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(r, (int)boff, 0, 0);
+    }
+    __device__ static void store_buffer(__amdgpu_buffer_rsrc_t r, uint32_t boff, V v) {
+        __builtin_amdgcn_raw_buffer_store_b16((uint16_t)v, r, (int)boff, 0, 0);
+    }
+    __device__ static V splat(int x) { return (uint32_t)(x & 0xf) * 0x1111u; }
+    __device__ static int get(V v, int c) { return (int)((v >> (4 * c)) & 0xfu); }
+    __device__ static V put(V v, int c, int x) {
+        return (v & ~(0xfu << (4 * c))) | ((uint32_t)(x & 0xf) << (4 * c));
+    }
+    __device__ static V keep(V v, int nvalid) { return nvalid >= 4 ? v : (v & ((1u << (4 * nvalid)) - 1u)); }
+    // the 4 states as 16-bit lanes: p[0] = slots (0, 2), p[1] = (1, 3)
+    __device__ static void split(V v, uint32_t (&p)[2]) {
+        p[0] = (v & 0xfu) | ((v & 0xf00u) << 8);
+        p[1] = ((v >> 4) & 0xfu) | ((v & 0xf000u) << 4);
+    }
+    __device__ static constexpr int word_of(int c) { return c & 1; }
+    __device__ static constexpr int half_of(int c) { return c >> 1; }
+};
+
+// Bytes of one node's block: mq quads of ld columns.
+template <typename ST>
+__device__ __forceinline__ int64_t node_bytes(int32_t m, int64_t ld) {
+    return (int64_t)((m + 3) >> 2) * ld * Quad<ST>::kBytes;
+}
+
+// Byte offset of quad rq at column j inside a node's block.
+template <typename ST>
+__device__ __forceinline__ uint32_t quad_boff(int rq, int64_t ld, int64_t j) {
+    return (uint32_t)(((int64_t)rq * ld + j) * Quad<ST>::kBytes);
+}
+
 // ---------------------------------------------------------------- entry walks
 
 // Two 16-bit lanes per 32-bit word: v_pk_mad_u16 computes a * b + c in both.
@@ -155,13 +211,13 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void *base, 
                                              kBufferWord3);
 }
 
-// State quad of node `node` (its block of vstride elements, under 2^31 bytes)
-// at the lane's byte offset.
+// State quad of node `node` (its block of nbytes bytes, under 2^31) at the
+// lane's byte offset.
 template <typename ST>
-__device__ __forceinline__ typename Quad<ST>::V load_row(const ST *__restrict__ states, int32_t node,
-                                                         int64_t vstride, uint32_t lane_boff) {
+__device__ __forceinline__ typename Quad<ST>::V load_row(const void *__restrict__ states, int32_t node,
+                                                         int64_t nbytes, uint32_t lane_boff) {
     const __amdgpu_buffer_rsrc_t r =
-        buffer_rsrc(states + (int64_t)node * vstride, (uint32_t)(vstride * (int64_t)sizeof(ST)));
+        buffer_rsrc(reinterpret_cast<const char *>(states) + (int64_t)node * nbytes, (uint32_t)nbytes);
     return Quad<ST>::load_buffer(r, lane_boff);
 }
 
@@ -170,7 +226,7 @@ constexpr int kEntryBatch = 8;  // most state rows in flight per batch
 // Loads the state quads of the N entries (node, mult) at e, all before the
 // first use, and hands each to f with its multiplier.
 template <int N, typename ST, typename F>
-__device__ __forceinline__ void entry_batch(cint32_t *e, const ST *__restrict__ states,
+__device__ __forceinline__ void entry_batch(cint32_t *e, const void *__restrict__ states,
                                             int64_t vstride, uint32_t lane_boff, F &f) {
     typename Quad<ST>::V s[N];
 #pragma unroll
@@ -182,7 +238,7 @@ __device__ __forceinline__ void entry_batch(cint32_t *e, const ST *__restrict__ 
 // Walks the n_e entries at e in batches of at most kEntryBatch.  n_e is
 // uniform, so the size switch is a scalar branch and no slot is wasted.
 template <typename ST, typename F>
-__device__ __forceinline__ void walk_entries(cint32_t *e, int n_e, const ST *__restrict__ states,
+__device__ __forceinline__ void walk_entries(cint32_t *e, int n_e, const void *__restrict__ states,
                                              int64_t vstride, uint32_t lane_boff, F &f) {
     for (; n_e > 0; n_e -= kEntryBatch, e += 2 * kEntryBatch) {
         switch (n_e < kEntryBatch ? n_e : kEntryBatch) {
@@ -327,7 +383,7 @@ __device__ __forceinline__ void renorm(float (&w)[KP]) {
 // output.  Slots >= nvalid read their states as 0.
 template <int KP, typename ST, bool RESCALE>
 __device__ __forceinline__ void wide_product(cint32_t *g, int n_groups, const float *__restrict__ tab,
-                                             const ST *__restrict__ states, int64_t vstride,
+                                             const void *__restrict__ states, int64_t vstride,
                                              uint32_t lane_boff, int nvalid, float (&w)[4][KP]) {
     using Q = Quad<ST>;
     for (int j = 0; j < n_groups; ++j) {
@@ -489,8 +545,8 @@ __device__ __forceinline__ float uniform24(uint32_t word) { return (float)(word 
 
 // Buffer resource over node `node`'s state quads (offsets past them read 0).
 template <typename ST>
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t node_rsrc(const ST *states, int32_t node, int64_t vstride) {
-    return buffer_rsrc(states + (int64_t)node * vstride, (uint32_t)(vstride * (int64_t)sizeof(ST)));
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t node_rsrc(const void *states, int32_t node, int64_t nbytes) {
+    return buffer_rsrc(reinterpret_cast<const char *>(states) + (int64_t)node * nbytes, (uint32_t)nbytes);
 }
 
 constexpr int kItemBatch = 4;  // blanket entries whose state quads are in flight together
@@ -498,7 +554,7 @@ constexpr int kItemBatch = 4;  // blanket entries whose state quads are in fligh
 // Adds the N entries (node, mult) at e to the item's packed index: every
 // entry's state quad is loaded before the first is used; slots >= nrep read 0.
 template <int N, typename ST>
-__device__ __forceinline__ void item_entries(cint32_t *e, const ST *__restrict__ states, int64_t vstride,
+__device__ __forceinline__ void item_entries(cint32_t *e, const void *__restrict__ states, int64_t vstride,
                                              uint32_t qoff, int nrep, uint32_t (&Pk)[2]) {
     using Q = Quad<ST>;
     typename Q::V v[N];
@@ -519,7 +575,7 @@ __device__ __forceinline__ void item_entries(cint32_t *e, const ST *__restrict__
 // above this group's use of its own (which needs more registers than the
 // occupancy bound allows).
 template <typename ST>
-__device__ __forceinline__ void item_group(cint32_t *&g, const ST *__restrict__ states, int64_t vstride,
+__device__ __forceinline__ void item_group(cint32_t *&g, const void *__restrict__ states, int64_t vstride,
                                            uint32_t qoff, int nrep, uint32_t (&Pk)[2]) {
     __builtin_amdgcn_sched_barrier(0);
     int n_e = g[0];
@@ -559,7 +615,7 @@ __device__ __forceinline__ void item_multiply(lds_char *lds, global_char *gtab, 
 // renormalised after each factor, which keeps it away from fp32 underflow.
 template <int KP, typename ST, bool STAGED, bool RESCALE>
 __device__ __forceinline__ void item_product(cint32_t *g, int n_groups, int n_staged, lds_char *lds,
-                                             global_char *gtab, const ST *__restrict__ states, int64_t vstride,
+                                             global_char *gtab, const void *__restrict__ states, int64_t vstride,
                                              uint32_t qoff, int nrep, float (&w)[4][KP]) {
 #pragma unroll
     for (int c = 0; c < 4; ++c)
@@ -613,8 +669,8 @@ __device__ __forceinline__ void sweep_product(const SweepParams &P, const Work &
     cint32_t *d = W.d;
     const int K = d[0], n_groups = d[8], n_staged = STAGED ? d[13] : 0;
     cint32_t *grp = d + d[9];
-    ST *states = reinterpret_cast<ST *>(P.states);
-    const int64_t vstride = node_stride(P.m, P.ld);
+    char *states = reinterpret_cast<char *>(P.states);
+    const int64_t vstride = node_bytes<ST>(P.m, P.ld);
     const __amdgpu_buffer_rsrc_t own = node_rsrc<ST>(states, W.node, vstride);
     const int n_items = I.ncl * I.nrq;
     for (int t = threadIdx.x; t < n_items; t += kSweepBlock) {
@@ -666,12 +722,12 @@ template <typename ST>
 __device__ void table_debug_prob(const SweepParams &P, const Work &W, int r, int64_t j) {
     cint32_t *d = W.d;
     const int K = d[0], KP = d[1];
-    const ST *states = reinterpret_cast<const ST *>(P.states);
+    const char *states = reinterpret_cast<const char *>(P.states);
     const int rb = r & ~3;
     const int nvalid = P.m - rb < 4 ? P.m - rb : 4;
     const int c = r & 3;
     const uint32_t lane_boff = quad_boff<ST>(rb >> 2, P.ld, j);
-    const int64_t vstride = node_stride(P.m, P.ld);
+    const int64_t vstride = node_bytes<ST>(P.m, P.ld);
     const float *tab = P.table + d[3];
 #define SAME_TABLE_DEBUG(KPV)                                                                     \
     {                                                                                             \
@@ -748,8 +804,8 @@ __device__ __forceinline__ void sweep_table(const SweepParams &P, const Work &W,
     cint32_t *d = W.d;
     cint32_t *grp = d + d[9];
     const bool tab_lds = STAGED && d[13] > 0;  // uniform: thresholds staged in LDS
-    ST *states = reinterpret_cast<ST *>(P.states);
-    const int64_t vstride = node_stride(P.m, P.ld);
+    char *states = reinterpret_cast<char *>(P.states);
+    const int64_t vstride = node_bytes<ST>(P.m, P.ld);
     const __amdgpu_buffer_rsrc_t own = node_rsrc<ST>(states, W.node, vstride);
     const int n_items = I.ncl * I.nrq;
     for (int t = threadIdx.x; t < n_items; t += kSweepBlock) {
@@ -868,8 +924,8 @@ __device__ void sweep_wide(const SweepParams &P, const Work &W) {
     const int K = d[0], n_groups = d[10];
     cint32_t *grp = d + d[11];
     const float *tab = P.table + d[3];
-    ST *states = reinterpret_cast<ST *>(P.states);
-    const int64_t vstride = node_stride(P.m, P.ld);
+    char *states = reinterpret_cast<char *>(P.states);
+    const int64_t vstride = node_bytes<ST>(P.m, P.ld);
     const __amdgpu_buffer_rsrc_t own = node_rsrc<ST>(states, W.node, vstride);
     // lanes take (column, replica quad) pairs, consecutive lanes consecutive
     // columns of one quad
@@ -932,7 +988,7 @@ __global__ __launch_bounds__(kSweepBlock) void sweep_wide_kernel(SweepParams P) 
 // products by walking the node's wide list for one column.
 
 template <typename ST>
-__device__ float weight_ext(cint32_t *d, const float *__restrict__ tab, const ST *__restrict__ base,
+__device__ float weight_ext(cint32_t *d, const float *__restrict__ tab, const char *__restrict__ base,
                             int64_t vstride, int c, int k, int &e) {
     using Q = Quad<ST>;
     cint32_t *g = d + d[11];
@@ -943,7 +999,7 @@ __device__ float weight_ext(cint32_t *d, const float *__restrict__ tab, const ST
         const int n_e = g[0];
         uint32_t idx = (uint32_t)g[1];
         for (int t = 0; t < n_e; ++t)
-            idx += (uint32_t)Q::get(Q::load(base + (int64_t)g[2 + 2 * t] * vstride), c) *
+            idx += (uint32_t)Q::get(Q::load_at(base + (int64_t)g[2 + 2 * t] * vstride), c) *
                    (uint32_t)g[3 + 2 * t];
         g += 2 + 2 * n_e;
         mnt *= tab[idx + k];
@@ -962,8 +1018,8 @@ __global__ __launch_bounds__(kSweepBlock) void sweep_generic_kernel(SweepParams 
     cint32_t *d = W.d;
     const int K = d[0];
     const float *tab = P.table + d[3];
-    ST *states = reinterpret_cast<ST *>(P.states);
-    const int64_t vstride = node_stride(P.m, P.ld);
+    char *states = reinterpret_cast<char *>(P.states);
+    const int64_t vstride = node_bytes<ST>(P.m, P.ld);
     const int64_t c0 = W.q0 * 4;
     const int ncols = (int)((W.q1 * 4 < P.n_cols ? W.q1 * 4 : P.n_cols) - c0);
     const int nrq = (W.r1 - W.r0 + 3) >> 2;
@@ -973,10 +1029,10 @@ __global__ __launch_bounds__(kSweepBlock) void sweep_generic_kernel(SweepParams 
         if (P.obs[(int64_t)W.node * P.ld + j] != 0) continue;
         const int rb = W.r0 + 4 * rq;
         const int nrep = W.r1 - rb < 4 ? W.r1 - rb : 4;
-        const int64_t qe = ((int64_t)(rb >> 2) * P.ld + j) * 4;  // the quad's element offset in a node block
-        const ST *base = states + qe;
-        ST *own = states + (int64_t)W.node * vstride + qe;
-        typename Q::V cur = Q::load(own);
+        const int64_t qe = quad_boff<ST>(rb >> 2, P.ld, j);  // the quad's byte offset in a node block
+        const char *base = states + qe;
+        char *own = states + (int64_t)W.node * vstride + qe;
+        typename Q::V cur = Q::load_at(own);
         const Philox4 rnd = gibbs_block(P, W.node, rb >> 2, j);
         for (int c = 0; c < nrep; ++c) {
             int E = -100000;
@@ -1007,7 +1063,7 @@ __global__ __launch_bounds__(kSweepBlock) void sweep_generic_kernel(SweepParams 
             if (pick < 0) pick = last_pos;
             cur = Q::put(cur, c, pick);
         }
-        Q::store(own, cur);
+        Q::store_at(own, cur);
     }
 }
 
@@ -1175,14 +1231,13 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 template <typename ST, int NQ>
 struct Span {
     using V = typename Quad<ST>::V;
-    static constexpr int kWords = NQ * (int)sizeof(ST);  // 32-bit words of NQ quads
+    static constexpr int kWords = NQ * Quad<ST>::kBytes / 4;  // 32-bit words of NQ quads
     V q[NQ];
 
     template <bool WIDE>
-    __device__ void load(const ST *__restrict__ states, int32_t node, int64_t vstride, uint32_t boff,
+    __device__ void load(const void *__restrict__ states, int32_t node, int64_t vstride, uint32_t boff,
                          bool whole) {
-        const __amdgpu_buffer_rsrc_t r =
-            buffer_rsrc(states + (int64_t)node * vstride, (uint32_t)(vstride * (int64_t)sizeof(ST)));
+        const __amdgpu_buffer_rsrc_t r = node_rsrc<ST>(states, node, vstride);
         if (WIDE && whole) {
             uint32_t w[kWords];
             if constexpr (kWords == 2) {
@@ -1204,14 +1259,15 @@ struct Span {
             for (int j = 0; j < NQ; ++j) q[j] = from_words(w, j);
         } else {
 #pragma unroll
-            for (int j = 0; j < NQ; ++j) q[j] = Quad<ST>::load_buffer(r, boff + 4u * j * (uint32_t)sizeof(ST));
+            for (int j = 0; j < NQ; ++j) q[j] = Quad<ST>::load_buffer(r, boff + (uint32_t)(j * Quad<ST>::kBytes));
         }
     }
 
   private:
     template <int N>
     __device__ static V from_words(const uint32_t (&w)[N], int j) {
-        if constexpr (sizeof(ST) == 1) return w[j];
+        if constexpr (Quad<ST>::kBytes == 2) return (w[j >> 1] >> (16 * (j & 1))) & 0xffffu;
+        else if constexpr (Quad<ST>::kBytes == 4) return w[j];
         else return make_uint2(w[2 * j], w[2 * j + 1]);
     }
 };
@@ -1230,7 +1286,7 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
                                                       int32_t count, int64_t n_slabs,
                                                       int64_t cols_per_block, int32_t rsplit,
                                                       int32_t quads_per_block,
-                                                      const ST *__restrict__ states, int32_t m,
+                                                      const void *__restrict__ states, int32_t m,
                                                       int64_t col0, int64_t n_cols, int64_t ld,
                                                       int32_t *__restrict__ counts) {
     using Q = Quad<ST>;
@@ -1259,7 +1315,7 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
     const int qe = qb + quads_per_block < mq ? qb + quads_per_block : mq;
     const int64_t c0 = col0 + slab * cols_per_block;
     const int64_t c1 = c0 + cols_per_block < col0 + n_cols ? c0 + cols_per_block : col0 + n_cols;
-    const int64_t vstride = node_stride(m, ld);
+    const int64_t vstride = node_bytes<ST>(m, ld);
     const bool packed = nbins <= 65536;
     auto add = [&](int bin) {
         if (mode == 0) {
@@ -1497,9 +1553,9 @@ __device__ __forceinline__ int row_of(const int64_t *__restrict__ row_ptr, int l
 template <typename ST>
 __global__ __launch_bounds__(kBlock) void expand_kernel(const int64_t *__restrict__ row_ptr, int32_t n,
                                                         const int32_t *__restrict__ col_idx,
-                                                        const ST *__restrict__ values, int64_t nnz,
-                                                        int32_t m, int64_t n_cols, int64_t ld,
-                                                        ST *__restrict__ states, uint8_t *__restrict__ obs) {
+                                                        const typename ElemOf<ST>::T *__restrict__ values,
+                                                        int64_t nnz, int32_t m, int64_t n_cols, int64_t ld,
+                                                        char *__restrict__ states, uint8_t *__restrict__ obs) {
     __shared__ int32_t span[2];
     const int64_t e0 = (int64_t)blockIdx.x * kBlock;
     const int64_t e_last = e0 + kBlock <= nnz ? e0 + kBlock - 1 : nnz - 1;
@@ -1514,9 +1570,9 @@ __global__ __launch_bounds__(kBlock) void expand_kernel(const int64_t *__restric
     obs[(int64_t)lo * ld + j] = 1;
     // every slot of the column's state quads, padding included, takes the value
     const typename Quad<ST>::V v = Quad<ST>::splat((int)values[e]);
-    ST *dst = states + (int64_t)lo * node_stride(m, ld) + 4 * j;
+    char *dst = states + (int64_t)lo * node_bytes<ST>(m, ld) + quad_boff<ST>(0, ld, j);
     const int mq = (m + 3) >> 2;
-    for (int rq = 0; rq < mq; ++rq) Quad<ST>::store(dst + (int64_t)rq * ld * 4, v);
+    for (int rq = 0; rq < mq; ++rq) Quad<ST>::store_at(dst + (int64_t)rq * ld * Quad<ST>::kBytes, v);
 }
 
 // Random initial latent states (Sec. 5.2): one thread per (node, column
@@ -1532,7 +1588,7 @@ __global__ __launch_bounds__(kBlock) void init_latent_kernel(const int32_t *__re
                                                              const int32_t *__restrict__ cdesc_off,
                                                              int32_t n, int32_t m, int64_t n_cols,
                                                              int64_t ld, int64_t col_offset, uint32_t k0,
-                                                             uint32_t k1, ST *__restrict__ states,
+                                                             uint32_t k1, char *__restrict__ states,
                                                              const uint8_t *__restrict__ obs) {
     using Q = Quad<ST>;
     const int64_t quads = (n_cols + 3) >> 2;
@@ -1550,10 +1606,10 @@ __global__ __launch_bounds__(kBlock) void init_latent_kernel(const int32_t *__re
     const uint32_t K = (uint32_t)cdesc[cdesc_off[i]];
     const int mq = (m + 3) >> 2;
     for (int rq = 0; rq < mq; ++rq) {
-        ST *p = states + (int64_t)i * node_stride(m, ld) + ((int64_t)rq * ld + col) * 4;
+        char *p = states + (int64_t)i * node_bytes<ST>(m, ld) + quad_boff<ST>(rq, ld, col);
         typename Q::V v[4];
 #pragma unroll
-        for (int c = 0; c < 4; ++c) v[c] = Q::load(p + 4 * c);
+        for (int c = 0; c < 4; ++c) v[c] = Q::load_at(p + c * Q::kBytes);
         for (int s = 0; s < 4 && 4 * rq + s < m; ++s) {
             const Philox4 b = philox4x32_10((uint32_t)((col_offset >> 2) + q), (uint32_t)i,
                                             (uint32_t)(4 * rq + s) | (2u << 24), 0u, k0, k1);
@@ -1563,7 +1619,7 @@ __global__ __launch_bounds__(kBlock) void init_latent_kernel(const int32_t *__re
         }
 #pragma unroll
         for (int c = 0; c < 4; ++c)
-            if ((lat >> c) & 1) Q::store(p + 4 * c, v[c]);
+            if ((lat >> c) & 1) Q::store_at(p + c * Q::kBytes, v[c]);
     }
 }
 
@@ -1575,21 +1631,24 @@ __global__ __launch_bounds__(kBlock) void init_latent_kernel(const int32_t *__re
 // and hit counters are read once, the replicas' state quads are compared in
 // turn, and the counters are written back.
 template <typename ST>
-__global__ __launch_bounds__(kBlock) void hits_kernel(const ST *__restrict__ states, const ST *__restrict__ target,
+__global__ __launch_bounds__(kBlock) void hits_kernel(const char *__restrict__ states,
+                                                      const typename ElemOf<ST>::T *__restrict__ target,
                                                       int32_t n, int32_t m, int64_t n_cols, int64_t ld,
                                                       int32_t *__restrict__ hits) {
     using Q = Quad<ST>;
+    using E = typename ElemOf<ST>::T;
+    using QE = Quad<E>;  // four adjacent targets
     const int64_t quads = (n_cols + 3) >> 2;
     const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (t >= (int64_t)n * quads) return;
     const int64_t q = t % quads;
     const int i = (int)(t / quads);
     const int64_t col = 4 * q;
-    const typename Q::V tg = Q::load(target + (int64_t)i * ld + col);
+    const typename QE::V tg = QE::load(target + (int64_t)i * ld + col);
     int want[4], any = 0;
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-        want[c] = (int)(sizeof(ST) == 1 ? (int8_t)Q::get(tg, c) : (int16_t)Q::get(tg, c));
+        want[c] = (int)(E)QE::get(tg, c);
         if (col + c >= n_cols) want[c] = -1;
         any |= want[c] >= 0;
     }
@@ -1597,13 +1656,13 @@ __global__ __launch_bounds__(kBlock) void hits_kernel(const ST *__restrict__ sta
     int add[4] = {0, 0, 0, 0};
     const int mq = (m + 3) >> 2;
     for (int rq = 0; rq < mq; ++rq) {
-        const ST *p = states + (int64_t)i * node_stride(m, ld) + ((int64_t)rq * ld + col) * 4;
+        const char *p = states + (int64_t)i * node_bytes<ST>(m, ld) + quad_boff<ST>(rq, ld, col);
         const int nrep = m - 4 * rq < 4 ? m - 4 * rq : 4;
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
-            const typename Q::V v = Q::load(p + 4 * c);  // column col + c, four replica slots
+            const typename Q::V v = Q::load_at(p + c * Q::kBytes);  // column col + c, four replica slots
             for (int sl = 0; sl < nrep; ++sl)
-                add[c] += Q::get(v, sl) == (want[c] & (sizeof(ST) == 1 ? 0xff : 0xffff)) ? 1 : 0;
+                add[c] += (uint32_t)Q::get(v, sl) == ((uint32_t)want[c] & Q::kMask) ? 1 : 0;
         }
     }
     int4 *h = reinterpret_cast<int4 *>(hits + (int64_t)i * ld + col);
@@ -1718,11 +1777,15 @@ __device__ __forceinline__ int compact_rank(const uint8_t *__restrict__ obs, int
 // well.  Columns [cols, slot_ld) are left untouched.
 template <typename ST>
 __global__ __launch_bounds__(kBlock) void expand_compact_kernel(
-    const uint8_t *__restrict__ obs, const ST *__restrict__ data, int64_t obs_ld, int64_t c0, int64_t cols,
+    const uint8_t *__restrict__ obs, const typename ElemOf<ST>::T *__restrict__ data, int64_t obs_ld, int64_t c0,
+    int64_t cols,
     int32_t m, int32_t chunks, const int32_t *__restrict__ prefix, const int64_t *__restrict__ node_off,
-    int64_t off0, const ST *__restrict__ lat_states, ST *__restrict__ states, uint8_t *__restrict__ obs_slot,
+    int64_t off0, const typename ElemOf<ST>::T *__restrict__ lat_states, char *__restrict__ states,
+    uint8_t *__restrict__ obs_slot,
     int64_t slot_ld) {
     using Q = Quad<ST>;
+    using E = typename ElemOf<ST>::T;
+    using QE = Quad<E>;
     __shared__ int32_t wave_n[kBlock / 64];
     const int node = (int)(blockIdx.x / chunks), chunk = (int)(blockIdx.x % chunks);
     int lat;
@@ -1730,10 +1793,10 @@ __global__ __launch_bounds__(kBlock) void expand_compact_kernel(
     const int64_t j = (int64_t)chunk * kCompactChunk + 4 * threadIdx.x;
     if (j >= cols) return;
     const int64_t L = (node_off[node + 1] - node_off[node]) / m;
-    const ST *lat_node = lat_states + (node_off[node] - off0);
+    const E *lat_node = lat_states + (node_off[node] - off0);
     *reinterpret_cast<uint32_t *>(obs_slot + (int64_t)node * slot_ld + j) =
         *reinterpret_cast<const uint32_t *>(obs + (int64_t)node * obs_ld + c0 + j);
-    const typename Q::V known = Q::load(data + (int64_t)node * obs_ld + c0 + j);  // columns j .. j + 3
+    const typename QE::V known = QE::load(data + (int64_t)node * obs_ld + c0 + j);  // columns j .. j + 3
     int kc[4];  // compact rank of each latent column of the lane
     {
         int k = rank;
@@ -1741,15 +1804,15 @@ __global__ __launch_bounds__(kBlock) void expand_compact_kernel(
         for (int c = 0; c < 4; ++c) kc[c] = ((lat >> c) & 1) ? k++ : -1;
     }
     const int mq = (m + 3) >> 2;
-    ST *dst = states + (int64_t)node * node_stride(m, slot_ld) + 4 * j;
+    char *dst = states + (int64_t)node * node_bytes<ST>(m, slot_ld) + quad_boff<ST>(0, slot_ld, j);
     for (int rq = 0; rq < mq; ++rq) {
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
-            typename Q::V v = Q::splat(kc[c] >= 0 ? 0 : Q::get(known, c));
+            typename Q::V v = Q::splat(kc[c] >= 0 ? 0 : QE::get(known, c));
             if (kc[c] >= 0)
                 for (int sl = 0; sl < 4 && 4 * rq + sl < m; ++sl)
                     v = Q::put(v, sl, (int)lat_node[(int64_t)(4 * rq + sl) * L + kc[c]]);
-            Q::store(dst + ((int64_t)rq * slot_ld + c) * 4, v);
+            Q::store_at(dst + ((int64_t)rq * slot_ld + c) * Q::kBytes, v);
         }
     }
 }
@@ -1759,7 +1822,7 @@ template <typename ST>
 __global__ __launch_bounds__(kBlock) void gather_compact_kernel(
     const uint8_t *__restrict__ obs, int64_t obs_ld, int64_t c0, int64_t cols, int32_t m, int32_t chunks,
     const int32_t *__restrict__ prefix, const int64_t *__restrict__ node_off, int64_t off0,
-    const ST *__restrict__ states, int64_t slot_ld, ST *__restrict__ lat_states) {
+    const char *__restrict__ states, int64_t slot_ld, typename ElemOf<ST>::T *__restrict__ lat_states) {
     using Q = Quad<ST>;
     __shared__ int32_t wave_n[kBlock / 64];
     const int node = (int)(blockIdx.x / chunks), chunk = (int)(blockIdx.x % chunks);
@@ -1768,17 +1831,17 @@ __global__ __launch_bounds__(kBlock) void gather_compact_kernel(
     const int64_t j = (int64_t)chunk * kCompactChunk + 4 * threadIdx.x;
     if (j >= cols || !lat) return;
     const int64_t L = (node_off[node + 1] - node_off[node]) / m;
-    ST *lat_node = lat_states + (node_off[node] - off0);
+    typename ElemOf<ST>::T *lat_node = lat_states + (node_off[node] - off0);
     const int mq = (m + 3) >> 2;
-    const ST *src = states + (int64_t)node * node_stride(m, slot_ld) + 4 * j;
+    const char *src = states + (int64_t)node * node_bytes<ST>(m, slot_ld) + quad_boff<ST>(0, slot_ld, j);
     int k = rank;
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
         if (!((lat >> c) & 1)) continue;
         for (int rq = 0; rq < mq; ++rq) {
-            const typename Q::V v = Q::load(src + ((int64_t)rq * slot_ld + c) * 4);
+            const typename Q::V v = Q::load_at(src + ((int64_t)rq * slot_ld + c) * Q::kBytes);
             for (int sl = 0; sl < 4 && 4 * rq + sl < m; ++sl)
-                lat_node[(int64_t)(4 * rq + sl) * L + k] = (ST)Q::get(v, sl);
+                lat_node[(int64_t)(4 * rq + sl) * L + k] = (typename ElemOf<ST>::T)Q::get(v, sl);
         }
         ++k;
     }
@@ -1792,24 +1855,24 @@ __global__ __launch_bounds__(kBlock) void gather_compact_kernel(
 // thread per (node, column): the source quads of the column are read once and
 // the destination quads assembled slot by slot.
 template <typename ST>
-__global__ __launch_bounds__(kBlock) void grow_kernel(const ST *__restrict__ src, int32_t m, ST *__restrict__ dst,
+__global__ __launch_bounds__(kBlock) void grow_kernel(const char *__restrict__ src, int32_t m, char *__restrict__ dst,
                                                       int32_t m2, int32_t n, int64_t ld) {
     using Q = Quad<ST>;
     const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (t >= (int64_t)n * ld) return;
     const int i = (int)(t / ld);
     const int64_t j = t - (int64_t)i * ld;
-    const ST *s = src + (int64_t)i * node_stride(m, ld) + 4 * j;
-    ST *d = dst + (int64_t)i * node_stride(m2, ld) + 4 * j;
+    const char *s = src + (int64_t)i * node_bytes<ST>(m, ld) + quad_boff<ST>(0, ld, j);
+    char *d = dst + (int64_t)i * node_bytes<ST>(m2, ld) + quad_boff<ST>(0, ld, j);
     const int mq2 = (m2 + 3) >> 2;
     for (int rq = 0; rq < mq2; ++rq) {
         typename Q::V v{};
 #pragma unroll
         for (int sl = 0; sl < 4; ++sl) {
             const int r = (4 * rq + sl) % m;
-            v = Q::put(v, sl, Q::get(Q::load(s + (int64_t)(r >> 2) * ld * 4), r & 3));
+            v = Q::put(v, sl, Q::get(Q::load_at(s + (int64_t)(r >> 2) * ld * Q::kBytes), r & 3));
         }
-        Q::store(d + (int64_t)rq * ld * 4, v);
+        Q::store_at(d + (int64_t)rq * ld * Q::kBytes, v);
     }
 }
 
@@ -1819,6 +1882,15 @@ __global__ __launch_bounds__(kBlock) void grow_kernel(const ST *__restrict__ src
 
 namespace {
 inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
+
+// Calls f with a value of the state type of a format: 4-bit (Nib), 8- or
+// 16-bit states.
+template <typename F>
+void by_format(int32_t bits, F &&f) {
+    if (bits == 4) f(dev::Nib{});
+    else if (bits == 8) f(int8_t{});
+    else f(int16_t{});
+}
 
 // Count histogram of the allocation-free count entry point: a file-scope
 // device array (each device holds its own copy until the process ends).  In
@@ -1881,7 +1953,7 @@ void sweep_class(const SweepParams &P, int32_t klass, int32_t lds_bytes, dim3 gr
 }  // namespace
 
 hipError_t launch_sweep(SweepParams P, int32_t begin, int32_t count, int32_t klass,
-                        int32_t lds_bytes, int32_t state_bytes, hipStream_t stream) {
+                        int32_t lds_bytes, int32_t state_bits, hipStream_t stream) {
     if (count <= 0 || P.n_cols <= 0) return hipSuccess;
     // Slabs of kSweepQuadsPerLane column quads per lane.  A block that stages
     // its node's table in LDS (class 0) takes all replicas, so that the copy
@@ -1917,8 +1989,7 @@ hipError_t launch_sweep(SweepParams P, int32_t begin, int32_t count, int32_t kla
     const int64_t blocks = rounds * dev::kXcds * count;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
     const dim3 grid((unsigned)blocks);
-    if (state_bytes == 1) sweep_class<int8_t>(P, klass, lds_bytes, grid, stream);
-    else sweep_class<int16_t>(P, klass, lds_bytes, grid, stream);
+    by_format(state_bits, [&](auto tag) { sweep_class<decltype(tag)>(P, klass, lds_bytes, grid, stream); });
     return hipGetLastError();
 }
 
@@ -1973,7 +2044,7 @@ hipError_t launch_fill_zero(int32_t *p, int64_t count, hipStream_t stream) {
     return hipGetLastError();
 }
 
-hipError_t launch_counts(const DeviceTables &t, const void *states, int32_t state_bytes,
+hipError_t launch_counts(const DeviceTables &t, const void *states, int32_t state_bits,
                          int32_t m, int64_t col0, int64_t n_cols, int64_t ld, int32_t *counts,
                          hipStream_t stream) {
     if (n_cols <= 0) return hipSuccess;
@@ -1999,68 +2070,62 @@ hipError_t launch_counts(const DeviceTables &t, const void *states, int32_t stat
     const dim3 grid((unsigned)blocks);
 #define SAME_LAUNCH_COUNTS(ST, WIDE)                                                                    \
     hipLaunchKernelGGL((dev::count_kernel<ST, WIDE>), grid, dim3(dev::kBlock), 0, stream, t.cdesc, t.cdesc_off, \
-                       t.cwork, n, n_slabs, cols_per_block, rsplit, quads_per_block, (const ST *)states, m, col0, \
+                       t.cwork, n, n_slabs, cols_per_block, rsplit, quads_per_block, states, m, col0, \
                        n_cols, ld, counts)
     // rows of at least kCountQuadsPerLane columns take the wide loads
-    if (state_bytes == 1) {
-        if (ld >= dev::kCountQuadsPerLane) SAME_LAUNCH_COUNTS(int8_t, true);
-        else SAME_LAUNCH_COUNTS(int8_t, false);
-    } else {
-        if (ld >= dev::kCountQuadsPerLane) SAME_LAUNCH_COUNTS(int16_t, true);
-        else SAME_LAUNCH_COUNTS(int16_t, false);
-    }
+    by_format(state_bits, [&](auto tag) {
+        using ST = decltype(tag);
+        if (ld >= dev::kCountQuadsPerLane) SAME_LAUNCH_COUNTS(ST, true);
+        else SAME_LAUNCH_COUNTS(ST, false);
+    });
 #undef SAME_LAUNCH_COUNTS
     return hipGetLastError();
 }
 
 hipError_t launch_expand(const int64_t *row_ptr, int32_t n, const int32_t *col_idx, const void *values,
-                         int64_t nnz, int32_t m, int64_t n_cols, int64_t ld, int32_t state_bytes,
+                         int64_t nnz, int32_t m, int64_t n_cols, int64_t ld, int32_t state_bits,
                          void *states, uint8_t *obs, hipStream_t stream) {
     // obs [n][ld] bytes (ld a multiple of 4) cleared as words, then the entries
     hipError_t e = launch_fill_zero(reinterpret_cast<int32_t *>(obs), (int64_t)n * ld / 4, stream);
     if (e != hipSuccess || nnz <= 0) return e;
     const int64_t blocks = (nnz + dev::kBlock - 1) / dev::kBlock;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-    if (state_bytes == 1)
-        hipLaunchKernelGGL(dev::expand_kernel<int8_t>, dim3((unsigned)blocks), dim3(dev::kBlock), 0, stream,
-                           row_ptr, n, col_idx, (const int8_t *)values, nnz, m, n_cols, ld, (int8_t *)states,
-                           obs);
-    else
-        hipLaunchKernelGGL(dev::expand_kernel<int16_t>, dim3((unsigned)blocks), dim3(dev::kBlock), 0, stream,
-                           row_ptr, n, col_idx, (const int16_t *)values, nnz, m, n_cols, ld,
-                           (int16_t *)states, obs);
+    by_format(state_bits, [&](auto tag) {
+        using ST = decltype(tag);
+        using E = typename dev::ElemOf<ST>::T;
+        hipLaunchKernelGGL(dev::expand_kernel<ST>, dim3((unsigned)blocks), dim3(dev::kBlock), 0, stream, row_ptr, n,
+                           col_idx, (const E *)values, nnz, m, n_cols, ld, (char *)states, obs);
+    });
     return hipGetLastError();
 }
 
 hipError_t launch_init_latent(const DeviceTables &t, int32_t n, int32_t m, int64_t n_cols, int64_t ld,
-                              int64_t col_offset, uint32_t key0, uint32_t key1, int32_t state_bytes,
+                              int64_t col_offset, uint32_t key0, uint32_t key1, int32_t state_bits,
                               void *states, const uint8_t *obs, hipStream_t stream) {
     const int64_t items = (int64_t)n * ((n_cols + 3) / 4);
     if (items <= 0) return hipSuccess;
     const int64_t blocks = (items + dev::kBlock - 1) / dev::kBlock;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-    if (state_bytes == 1)
-        hipLaunchKernelGGL(dev::init_latent_kernel<int8_t>, dim3((unsigned)blocks), dim3(dev::kBlock), 0, stream,
-                           t.cdesc, t.cdesc_off, n, m, n_cols, ld, col_offset, key0, key1, (int8_t *)states, obs);
-    else
-        hipLaunchKernelGGL(dev::init_latent_kernel<int16_t>, dim3((unsigned)blocks), dim3(dev::kBlock), 0,
-                           stream, t.cdesc, t.cdesc_off, n, m, n_cols, ld, col_offset, key0, key1,
-                           (int16_t *)states, obs);
+    by_format(state_bits, [&](auto tag) {
+        hipLaunchKernelGGL(dev::init_latent_kernel<decltype(tag)>, dim3((unsigned)blocks), dim3(dev::kBlock), 0,
+                           stream, t.cdesc, t.cdesc_off, n, m, n_cols, ld, col_offset, key0, key1, (char *)states,
+                           obs);
+    });
     return hipGetLastError();
 }
 
 hipError_t launch_hits(const void *states, const void *target, int32_t n, int32_t m, int64_t n_cols, int64_t ld,
-                       int32_t state_bytes, int32_t *hits, hipStream_t stream) {
+                       int32_t state_bits, int32_t *hits, hipStream_t stream) {
     const int64_t items = (int64_t)n * ((n_cols + 3) / 4);
     if (items <= 0) return hipSuccess;
     const int64_t blocks = (items + dev::kBlock - 1) / dev::kBlock;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-    if (state_bytes == 1)
-        hipLaunchKernelGGL(dev::hits_kernel<int8_t>, dim3((unsigned)blocks), dim3(dev::kBlock), 0, stream,
-                           (const int8_t *)states, (const int8_t *)target, n, m, n_cols, ld, hits);
-    else
-        hipLaunchKernelGGL(dev::hits_kernel<int16_t>, dim3((unsigned)blocks), dim3(dev::kBlock), 0, stream,
-                           (const int16_t *)states, (const int16_t *)target, n, m, n_cols, ld, hits);
+    by_format(state_bits, [&](auto tag) {
+        using ST = decltype(tag);
+        using E = typename dev::ElemOf<ST>::T;
+        hipLaunchKernelGGL(dev::hits_kernel<ST>, dim3((unsigned)blocks), dim3(dev::kBlock), 0, stream,
+                           (const char *)states, (const E *)target, n, m, n_cols, ld, hits);
+    });
     return hipGetLastError();
 }
 
@@ -2087,50 +2152,45 @@ hipError_t launch_compact_counts(const uint8_t *obs, int64_t obs_ld, int64_t c0,
 hipError_t launch_expand_compact(const uint8_t *obs, const void *data, int64_t obs_ld, int64_t c0, int64_t cols,
                                  int32_t n, int32_t m, const int32_t *prefix, const int64_t *node_off, int64_t off0,
                                  const void *lat_states, void *states, uint8_t *obs_slot, int64_t slot_ld,
-                                 int32_t state_bytes, hipStream_t stream) {
+                                 int32_t state_bits, hipStream_t stream) {
     const int32_t chunks = (int32_t)((cols + dev::kCompactChunk - 1) / dev::kCompactChunk);
     if (cols <= 0 || n <= 0) return hipSuccess;
     const dim3 grid((unsigned)((int64_t)n * chunks));
-    if (state_bytes == 1)
-        hipLaunchKernelGGL(dev::expand_compact_kernel<int8_t>, grid, dim3(dev::kBlock), 0, stream, obs,
-                           (const int8_t *)data, obs_ld, c0, cols, m, chunks, prefix, node_off, off0,
-                           (const int8_t *)lat_states, (int8_t *)states, obs_slot, slot_ld);
-    else
-        hipLaunchKernelGGL(dev::expand_compact_kernel<int16_t>, grid, dim3(dev::kBlock), 0, stream, obs,
-                           (const int16_t *)data, obs_ld, c0, cols, m, chunks, prefix, node_off, off0,
-                           (const int16_t *)lat_states, (int16_t *)states, obs_slot, slot_ld);
+    by_format(state_bits, [&](auto tag) {
+        using ST = decltype(tag);
+        using E = typename dev::ElemOf<ST>::T;
+        hipLaunchKernelGGL(dev::expand_compact_kernel<ST>, grid, dim3(dev::kBlock), 0, stream, obs, (const E *)data,
+                           obs_ld, c0, cols, m, chunks, prefix, node_off, off0, (const E *)lat_states,
+                           (char *)states, obs_slot, slot_ld);
+    });
     return hipGetLastError();
 }
 
 hipError_t launch_gather_compact(const uint8_t *obs, int64_t obs_ld, int64_t c0, int64_t cols, int32_t n, int32_t m,
                                  const int32_t *prefix, const int64_t *node_off, int64_t off0, const void *states,
-                                 int64_t slot_ld, void *lat_states, int32_t state_bytes, hipStream_t stream) {
+                                 int64_t slot_ld, void *lat_states, int32_t state_bits, hipStream_t stream) {
     const int32_t chunks = (int32_t)((cols + dev::kCompactChunk - 1) / dev::kCompactChunk);
     if (cols <= 0 || n <= 0) return hipSuccess;
     const dim3 grid((unsigned)((int64_t)n * chunks));
-    if (state_bytes == 1)
-        hipLaunchKernelGGL(dev::gather_compact_kernel<int8_t>, grid, dim3(dev::kBlock), 0, stream, obs, obs_ld, c0,
-                           cols, m, chunks, prefix, node_off, off0, (const int8_t *)states, slot_ld,
-                           (int8_t *)lat_states);
-    else
-        hipLaunchKernelGGL(dev::gather_compact_kernel<int16_t>, grid, dim3(dev::kBlock), 0, stream, obs, obs_ld,
-                           c0, cols, m, chunks, prefix, node_off, off0, (const int16_t *)states, slot_ld,
-                           (int16_t *)lat_states);
+    by_format(state_bits, [&](auto tag) {
+        using ST = decltype(tag);
+        using E = typename dev::ElemOf<ST>::T;
+        hipLaunchKernelGGL(dev::gather_compact_kernel<ST>, grid, dim3(dev::kBlock), 0, stream, obs, obs_ld, c0, cols,
+                           m, chunks, prefix, node_off, off0, (const char *)states, slot_ld, (E *)lat_states);
+    });
     return hipGetLastError();
 }
 
 hipError_t launch_grow(const void *src, int32_t m, void *dst, int32_t m2, int32_t n, int64_t ld,
-                       int32_t state_bytes, hipStream_t stream) {
+                       int32_t state_bits, hipStream_t stream) {
     const int64_t items = (int64_t)n * ld;
     if (items <= 0) return hipSuccess;
     const int64_t blocks = (items + dev::kBlock - 1) / dev::kBlock;
     if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-    if (state_bytes == 1)
-        hipLaunchKernelGGL(dev::grow_kernel<int8_t>, dim3((unsigned)blocks), dim3(dev::kBlock), 0, stream,
-                           (const int8_t *)src, m, (int8_t *)dst, m2, n, ld);
-    else
-        hipLaunchKernelGGL(dev::grow_kernel<int16_t>, dim3((unsigned)blocks), dim3(dev::kBlock), 0, stream,
-                           (const int16_t *)src, m, (int16_t *)dst, m2, n, ld);
+    by_format(state_bits, [&](auto tag) {
+        hipLaunchKernelGGL(dev::grow_kernel<decltype(tag)>, dim3((unsigned)blocks), dim3(dev::kBlock), 0, stream,
+                           (const char *)src, m, (char *)dst, m2, n, ld);
+    });
     return hipGetLastError();
 }
 

@@ -77,7 +77,7 @@ hipError_t launch_prepare(const DeviceTables &t, const float *cpts, float *table
 // (0: fast kernel, tables staged in lds_bytes of LDS; 1: fast kernel, tables
 // in global memory; 2: wide kernel; 3: generic kernel).
 hipError_t launch_sweep(SweepParams P, int32_t begin, int32_t count, int32_t klass,
-                        int32_t lds_bytes, int32_t state_bytes, hipStream_t stream);
+                        int32_t lds_bytes, int32_t state_bits, hipStream_t stream);
 
 hipError_t launch_fill_zero(int32_t *p, int64_t count, hipStream_t stream);
 
@@ -92,24 +92,24 @@ hipError_t scratch_counts(int device, int32_t **out);
 
 // Histograms of every node's family (the count work items of t) over the
 // columns [col0, col0 + n_cols) of states [n][m][ld].
-hipError_t launch_counts(const DeviceTables &t, const void *states, int32_t state_bytes,
+hipError_t launch_counts(const DeviceTables &t, const void *states, int32_t state_bits,
                          int32_t m, int64_t col0, int64_t n_cols, int64_t ld, int32_t *counts,
                          hipStream_t stream);
 
 // Dense minibatch from CSR known entries (rows = nodes): clears obs, then
 // one thread per entry writes obs and every replica's state.
 hipError_t launch_expand(const int64_t *row_ptr, int32_t n, const int32_t *col_idx, const void *values,
-                         int64_t nnz, int32_t m, int64_t n_cols, int64_t ld, int32_t state_bytes,
+                         int64_t nnz, int32_t m, int64_t n_cols, int64_t ld, int32_t state_bits,
                          void *states, uint8_t *obs, hipStream_t stream);
 
 // Random initial states of the latent entries (Philox tag 2).
 hipError_t launch_init_latent(const DeviceTables &t, int32_t n, int32_t m, int64_t n_cols, int64_t ld,
-                              int64_t col_offset, uint32_t key0, uint32_t key1, int32_t state_bytes,
+                              int64_t col_offset, uint32_t key0, uint32_t key1, int32_t state_bits,
                               void *states, const uint8_t *obs, hipStream_t stream);
 
 // Held-out prediction: hits[i][j] += replicas whose state equals target[i][j] >= 0.
 hipError_t launch_hits(const void *states, const void *target, int32_t n, int32_t m, int64_t n_cols, int64_t ld,
-                       int32_t state_bytes, int32_t *hits, hipStream_t stream);
+                       int32_t state_bits, int32_t *hits, hipStream_t stream);
 
 // Compact host state of the out-of-core passes: latent columns per (node,
 // chunk of 1024 columns) of the minibatch [c0, c0 + cols) of obs [n][obs_ld]
@@ -125,15 +125,15 @@ hipError_t launch_compact_node_counts(const uint8_t *obs, int64_t obs_ld, int64_
 hipError_t launch_expand_compact(const uint8_t *obs, const void *data, int64_t obs_ld, int64_t c0, int64_t cols,
                                  int32_t n, int32_t m, const int32_t *prefix, const int64_t *node_off, int64_t off0,
                                  const void *lat_states, void *states, uint8_t *obs_slot, int64_t slot_ld,
-                                 int32_t state_bytes, hipStream_t stream);
+                                 int32_t state_bits, hipStream_t stream);
 hipError_t launch_gather_compact(const uint8_t *obs, int64_t obs_ld, int64_t c0, int64_t cols, int32_t n, int32_t m,
                                  const int32_t *prefix, const int64_t *node_off, int64_t off0, const void *states,
-                                 int64_t slot_ld, void *lat_states, int32_t state_bytes, hipStream_t stream);
+                                 int64_t slot_ld, void *lat_states, int32_t state_bits, hipStream_t stream);
 
 // SAME annealing: dst (m2 replicas) from src (m replicas), replica r of dst
 // taking replica r mod m; both in the state-quad layout with leading dimension ld.
 hipError_t launch_grow(const void *src, int32_t m, void *dst, int32_t m2, int32_t n, int64_t ld,
-                       int32_t state_bytes, hipStream_t stream);
+                       int32_t state_bits, hipStream_t stream);
 
 hipError_t launch_moving_sum(const int32_t *newc, int32_t *mb, int32_t *totals, int64_t total,
                              hipStream_t stream);

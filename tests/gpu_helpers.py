@@ -12,17 +12,34 @@ REL_TOL = 1e-5       # conditionals, fp32 vs fp64
 TINY = 1e-30         # below this the oracle's probability is not compared relatively
 
 
-def context_for(net, prior=1.0, table_limit=None, tile_bytes=0, lds_limit=None, packed=True):
+def context_for(net, prior=1.0, table_limit=None, tile_bytes=0, lds_limit=None, packed=True, state_bits=0):
     """Library context; table_limit=0 forces every node onto the product path,
     a small tile_bytes forces sweeps over several column tiles, lds_limit=0
     reads every table from global memory, packed=False sends every
-    product-mode node through the 32-bit index kernel."""
+    product-mode node through the 32-bit index kernel, state_bits=4 stores
+    4-bit states."""
     pptr, pidx, card = net.csr()
-    if table_limit is None and not tile_bytes and lds_limit is None and packed:
+    if table_limit is None and not tile_bytes and lds_limit is None and packed and not state_bits:
         return same.same_create(pptr, pidx, card, prior)
     return same.same_create_ex(pptr, pidx, card, prior,
                                -1 if table_limit is None else table_limit, tile_bytes,
-                               -1 if lds_limit is None else lds_limit, packed)
+                               -1 if lds_limit is None else lds_limit, packed, state_bits=state_bits)
+
+
+def bits_of(ctx):
+    """pack_states/unpack_states argument for a context's state format."""
+    return 4 if ctx.state_bits == 4 else None
+
+
+def to_device(ctx, states):
+    """[n][m][ld] numpy array or tensor -> the context's state layout on the GPU."""
+    q = same.pack_states(states, bits_of(ctx))
+    return (torch.from_numpy(q) if isinstance(q, np.ndarray) else q).cuda()
+
+
+def from_device(ctx, quads, m):
+    """The context's state layout (device tensor) -> [n][m][ld] numpy array."""
+    return same.unpack_states(quads.cpu().numpy(), m, bits_of(ctx))
 
 
 def gpu_sweep(ctx, states_np, obs_np, theta_np, m, n_cols, col_offset, seed, sweep_id, win=None,
@@ -30,7 +47,7 @@ def gpu_sweep(ctx, states_np, obs_np, theta_np, m, n_cols, col_offset, seed, swe
     """Runs one library sweep on copies of the given host arrays (states
     [n][m][ld], packed into the library's replica quads); returns (states
     after, as [n][m][ld], probs or None)."""
-    st = torch.from_numpy(same.pack_states(np.ascontiguousarray(states_np))).cuda()
+    st = to_device(ctx, np.ascontiguousarray(states_np))
     ob = torch.from_numpy(np.ascontiguousarray(obs_np)).cuda()
     th = torch.from_numpy(np.ascontiguousarray(theta_np, dtype=np.float32)).cuda()
     ws = ctx.new_workspace()
@@ -43,7 +60,7 @@ def gpu_sweep(ctx, states_np, obs_np, theta_np, m, n_cols, col_offset, seed, swe
     else:
         same.same_sweep(ctx, st, ob, th, m, n_cols, ld, col_offset, seed, sweep_id, ws, stream)
     torch.cuda.synchronize()
-    return same.unpack_states(st.cpu().numpy(), m), (probs.cpu().numpy() if probs is not None else None)
+    return from_device(ctx, st, m), (probs.cpu().numpy() if probs is not None else None)
 
 
 def gpu_sweep_both(ctx, states_np, obs_np, theta_np, m, n_cols, col_offset, seed, sweep_id, win=None):

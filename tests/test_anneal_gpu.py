@@ -47,3 +47,16 @@ def test_grow_replicas_int16_ragged_rows():
     torch.cuda.synchronize()
     assert np.array_equal(same.unpack_states(dst.cpu().numpy(), 5), ref)
     ctx.close()
+
+
+@pytest.mark.parametrize("m,m2", [(2, 7), (3, 10), (5, 5)])
+def test_grow_replicas_4bit(m, m2):
+    w = make_workload(5, n_cols=2_001, m=m)
+    st = w.states[0].numpy()
+    ref = oracle.grow_replicas(st, m2)
+    ctx = H.context_for(w.net, state_bits=4)
+    dst = torch.full(same.state_shape(w.net.n, m2, w.ld, 4), -1, dtype=torch.int16, device="cuda")
+    same.same_grow_replicas(ctx, H.to_device(ctx, st), m, dst, m2, w.ld)
+    torch.cuda.synchronize()
+    assert np.array_equal(H.from_device(ctx, dst, m2), ref)
+    ctx.close()

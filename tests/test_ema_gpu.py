@@ -55,14 +55,15 @@ def test_sample_cpts_ema_matches_oracle(cfg):
     ctx.close()
 
 
-def test_stream_pass_ema_equals_resident():
+@pytest.mark.parametrize("bits", [0, 4], ids=["8bit", "4bit"])
+def test_stream_pass_ema_equals_resident(bits):
     w = make_workload(3, n_cols=9_001, nb=3_000, m=3)
-    ctx = H.context_for(w.net)
+    ctx = H.context_for(w.net, state_bits=bits)
     M = w.M
     decay = 1.0 - 1.0 / M
     passes = 2
     # resident: the same calls in the same order on device minibatches
-    dev = [same.pack_states(s).cuda() for s in w.states]
+    dev = [H.to_device(ctx, s) for s in w.states]
     obs = [o.cuda() for o in w.obs]
     ws = ctx.new_workspace()
     cpts = torch.from_numpy(w.init_theta).cuda()
@@ -76,7 +77,7 @@ def test_stream_pass_ema_equals_resident():
             same.same_sample_cpts_ema(ctx, tot, cpts, w.seed, s * M + b, ws)
     torch.cuda.synchronize()
     # streamed from pinned host memory
-    hst, hob, host_ld = _host_arrays(w)
+    hst, hob, host_ld = _host_arrays(w, H.bits_of(ctx))
     ws2 = ctx.new_workspace()
     slots = torch.empty(same.same_stream_slots_size(ctx, w.m, w.nb), dtype=torch.uint8, device="cuda")
     cp2 = torch.from_numpy(w.init_theta).cuda()
@@ -89,8 +90,8 @@ def test_stream_pass_ema_equals_resident():
     torch.cuda.synchronize()
     assert np.array_equal(tot2.cpu().numpy(), tot.cpu().numpy())
     assert np.array_equal(cp2.cpu().numpy(), cpts.cpu().numpy())
-    hs = same.unpack_states(hst, w.m)
+    hs = same.unpack_states(hst, w.m, H.bits_of(ctx))
     for b in range(M):
         c0, nc = b * w.nb, w.mb_cols(b)
-        assert np.array_equal(hs[:, :, c0:c0 + nc].numpy(), same.unpack_states(dev[b].cpu(), w.m)[:, :, :nc].numpy())
+        assert np.array_equal(hs[:, :, c0:c0 + nc].numpy(), H.from_device(ctx, dev[b], w.m)[:, :, :nc])
     ctx.close()

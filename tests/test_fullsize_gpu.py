@@ -32,24 +32,25 @@ def _gpu():
     same.load_library()
 
 
-def test_full_minibatch_step_matches_oracle():
+@pytest.mark.parametrize("bits", [0, 4], ids=["8bit", "4bit"])
+def test_full_minibatch_step_matches_oracle(bits):
     dev = torch.device("cuda:0")
     w = make_workload(5, device=dev, minibatches=[0])
     net = w.net
     nc, ld, m = w.mb_cols(0), w.ld, w.m
     assert (nc, m, net.n) == (250_000, 10, 1000)
-    ctx = H.context_for(net)
+    ctx = H.context_for(net, state_bits=bits)
     ws = ctx.new_workspace(dev)
     pre = w.states[0].clone()
     cpts = torch.from_numpy(w.init_theta).to(dev)
     mb = torch.zeros(ctx.cpt_total, dtype=torch.int32, device=dev)
     tot = torch.zeros(ctx.cpt_total, dtype=torch.int32, device=dev)
     sweep_id = update_id = 3
-    st = same.pack_states(w.states[0])  # the library's replica-quad layout, on the device
+    st = same.pack_states(w.states[0], H.bits_of(ctx))  # the library's replica-quad layout, on the device
     same.same_counts(ctx, st, m, nc, ld, mb, tot, ws)  # the pre-pass
     same.same_step(ctx, st, w.obs[0], cpts, m, nc, ld, 0, w.seed, sweep_id, mb, tot, update_id, ws)
     torch.cuda.synchronize()
-    post = same.unpack_states(st.cpu().numpy(), m)
+    post = H.from_device(ctx, st, m)
     obs = w.obs[0].cpu().numpy()
     color = oracle.graph(net.parents, net.card)["color"]
     assert np.array_equal(ctx.color, color)

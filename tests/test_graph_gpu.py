@@ -31,7 +31,7 @@ class _Run:
     count-only pre-pass."""
 
     def __init__(self, w, ctx):
-        self.states = [same.pack_states(s).cuda() for s in w.states]
+        self.states = [H.to_device(ctx, s) for s in w.states]
         self.obs = [o.cuda() for o in w.obs]
         self.ws = ctx.new_workspace()
         self.cpts = torch.from_numpy(w.init_theta).cuda()
@@ -56,10 +56,13 @@ def _assert_equal(E, G, w, what):
     (4, dict(), 3),                                  # three steps per replay
     (3, dict(n_cols=10_000, nb=2_048, m=3), 1),      # 5 minibatches, ragged last one, update stride 5
     (5, dict(n_cols=6_000, nb=1_500, m=2), 2),       # 1000 nodes (every launch class), 4 minibatches
+    (5, dict(n_cols=6_000, nb=1_500, m=5, state_bits=4), 1),   # 4-bit states
 ])
 def test_graph_replays_equal_eager(cfg, kw, steps):
+    kw = dict(kw)
+    bits = kw.pop("state_bits", 0)
     w = make_workload(cfg, **kw)
-    ctx = H.context_for(w.net)
+    ctx = H.context_for(w.net, state_bits=bits)
     E, G = _Run(w, ctx), _Run(w, ctx)
     _assert_equal(E, G, w, "start")
     # minibatch b's ids start at {0, b}; a step moves them by {1, M}

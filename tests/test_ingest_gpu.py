@@ -93,3 +93,32 @@ def test_init_latent_int16():
     torch.cuda.synchronize()
     assert np.array_equal(same.unpack_states(g.cpu().numpy(), m), ref)
     ctx.close()
+
+
+@pytest.mark.parametrize("cfg,kw", [(4, {}), (5, dict(n_cols=3_001, m=3))])
+def test_expand_and_init_latent_4bit(cfg, kw):
+    """4-bit states: the expanded known part and the random start equal the
+    oracle's (latent entries of the expansion keep their value)."""
+    w = make_workload(cfg, **kw)
+    net = w.net
+    st, ob = w.states[0].numpy(), w.obs[0].numpy()
+    n, m, ld = st.shape
+    row_ptr, col, val = csr_of_observed(st, ob, w.n_cols)
+    ref_st = np.full_like(st, 9)
+    ref_ob = np.full_like(ob, 3)
+    oracle.expand(n, w.n_cols, m, ld, row_ptr, col, val, ref_st, ref_ob)
+    ctx = H.context_for(net, state_bits=4)
+    g_st = H.to_device(ctx, np.full_like(st, 9))
+    g_ob = torch.full(ob.shape, 3, dtype=torch.uint8, device="cuda")
+    rp, ci, vv = (torch.from_numpy(a).cuda() for a in (row_ptr, col, val))
+    same.same_expand_observed(ctx, rp, ci, vv, len(col), m, w.n_cols, ld, g_st, g_ob)
+    torch.cuda.synchronize()
+    assert np.array_equal(g_ob.cpu().numpy(), ref_ob)
+    assert np.array_equal(H.from_device(ctx, g_st, m), ref_st)
+    ref = st.copy()
+    oracle.init_latent(net.card, w.n_cols, m, 4096, w.seed, ref, ob)
+    g = H.to_device(ctx, st)
+    same.same_init_latent(ctx, g, torch.from_numpy(ob).cuda(), m, w.n_cols, ld, 4096, w.seed)
+    torch.cuda.synchronize()
+    assert np.array_equal(H.from_device(ctx, g, m), ref)
+    ctx.close()

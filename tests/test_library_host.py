@@ -368,4 +368,27 @@ def test_binding_refuses_states_in_another_layout():
     ctx = _ctx(koller())
     with pytest.raises(same.SameError) as e:
         same.same_counts(ctx, torch.zeros((ctx.n_nodes, 2, 8), dtype=torch.int8), 2, 8, 8, None, None, None)
-    assert e.value.code == same.SAME_EINVAL and "ceil(m/4)" in str(e.value)
+    assert e.value.code == same.SAME_EINVAL and "replica quads" in str(e.value)
+
+
+def test_state_bits_option():
+    """state_bits = 4 stores 4-bit states when every K <= 16; otherwise the
+    context is refused (SAME_ECARD); other values are SAME_EINVAL.  The
+    colouring and CPT layout do not depend on it."""
+    net = koller()
+    pptr, pidx, card = net.csr()
+    a = same.same_create(pptr, pidx, card)
+    b = same.same_create_ex(pptr, pidx, card, state_bits=4)
+    assert (a.state_bits, b.state_bits) == (8, 4)
+    assert np.array_equal(a.color, b.color) and np.array_equal(a.cpt_off, b.cpt_off)
+    assert same.same_layout(b)["state_bits"] == 4 and b.state_bytes == 1
+    big = np.array(card, dtype=np.int32)
+    big[0] = 17
+    with pytest.raises(same.SameError) as e:
+        same.same_create_ex(pptr, pidx, big, state_bits=4)
+    assert e.value.code == same.SAME_ECARD
+    with pytest.raises(same.SameError) as e:
+        same.same_create_ex(pptr, pidx, card, state_bits=5)
+    assert e.value.code == same.SAME_EINVAL
+    big[0] = 200
+    assert same.same_create(pptr, pidx, big).state_bits == 16

@@ -536,3 +536,145 @@ def test_padding_slots_may_hold_anything(big):
     for x, y in zip(*outs):
         assert np.array_equal(x, y)
     assert np.array_equal(outs[1][1], oracle.counts(parents, card, outs[1][0], m, n_cols))
+
+
+# ------------------------------------------------------------ 4-bit states
+
+@pytest.mark.parametrize("cfg,kw,win", [
+    (1, {}, (0, 2000)),
+    (2, dict(n_cols=20_000), (1000, 3000)),
+    (3, dict(n_cols=9_000), (8_000, 1000)),
+    (4, {}, (0, 600)),
+    (5, dict(n_cols=3_000, m=5), (0, 300)),             # odd m: a replica quad, then a partial one
+    (5, dict(n_cols=2_001, m=7), (1_700, 301)),         # odd m and a ragged tail
+])
+def test_sweep_parity_4bit(cfg, kw, win):
+    """4-bit states (a replica quad in one 16-bit word): the production and
+    debug sweeps against the oracle, as for 8-bit states."""
+    w = make_workload(cfg, **kw)
+    out = _sweep_case(w, win=win, state_bits=4)
+    assert out["states"]["draws"] > 0
+
+
+@pytest.mark.parametrize("cfg,kw", [(1, {}), (3, dict(n_cols=7_001)), (4, {}), (5, dict(n_cols=3_000))])
+def test_counts_4bit(cfg, kw):
+    w = make_workload(cfg, **kw)
+    net = w.net
+    ctx = H.context_for(net, state_bits=4)
+    ncols = w.mb_cols(0)
+    want = oracle.counts(net.parents, net.card, w.states[0].numpy(), w.m, ncols)
+    mb = torch.zeros(ctx.cpt_total, dtype=torch.int32, device="cuda")
+    tot = torch.zeros(ctx.cpt_total, dtype=torch.int32, device="cuda")
+    same.same_counts(ctx, H.to_device(ctx, w.states[0]), w.m, ncols, w.ld, mb, tot, ctx.new_workspace())
+    torch.cuda.synchronize()
+    assert np.array_equal(mb.cpu().numpy(), want)
+    assert np.array_equal(tot.cpu().numpy(), want)
+
+
+@pytest.mark.parametrize("n_par,K", [(4, 3), (5, 3)], ids=["12288-bins-2-ranges", "98304-bins-32bit-global"])
+def test_counts_large_cpt_4bit(n_par, K):
+    parents = [[] for _ in range(n_par)] + [list(range(n_par))]
+    card = [8] * n_par + [K]
+    net, st, _, _ = _custom(parents, card, 5000, 3, 0.0, 12)
+    ctx = H.context_for(net, state_bits=4)
+    mb = torch.zeros(ctx.cpt_total, dtype=torch.int32, device="cuda")
+    same.same_counts(ctx, H.to_device(ctx, st), 3, 5000, st.shape[-1], mb, None, ctx.new_workspace())
+    torch.cuda.synchronize()
+    assert np.array_equal(mb.cpu().numpy(), oracle.counts(parents, card, st, 3, 5000))
+
+
+@pytest.mark.parametrize("n_cols,ld", [(3, 4), (4097, 4100), (6000, 6004)])
+def test_counts_ragged_rows_4bit(n_cols, ld):
+    card = [16, 3, 4, 2, 5]
+    parents = [[], [0], [0, 1], [2], [1, 2, 3]]
+    net, st, _, _ = _custom(parents, card, n_cols, 3, 0.0, 21, ld=ld)
+    st[:, :, n_cols:] = 15
+    ctx = H.context_for(net, state_bits=4)
+    mb = torch.zeros(ctx.cpt_total, dtype=torch.int32, device="cuda")
+    same.same_counts(ctx, H.to_device(ctx, st), 3, n_cols, ld, mb, None, ctx.new_workspace())
+    torch.cuda.synchronize()
+    assert np.array_equal(mb.cpu().numpy(), oracle.counts(parents, card, st, 3, n_cols))
+
+
+def test_step_tiles_and_8bit_agree_4bit():
+    """With 4-bit states a tiled step equals an untiled one and equals the
+    same step on 8-bit states (the format does not change any result):
+    states, counts, moving sum and CPTs, bit for bit."""
+    w = make_workload(5, n_cols=5_000, m=3)
+    net = w.net
+    outs = []
+    for kw in (dict(state_bits=4, tile_bytes=1), dict(state_bits=4), {}):
+        ctx = H.context_for(net, **kw)
+        st = H.to_device(ctx, w.states[0])
+        ob = w.obs[0].cuda()
+        th = torch.from_numpy(w.init_theta).cuda()
+        mb = torch.zeros(ctx.cpt_total, dtype=torch.int32, device="cuda")
+        tot = torch.zeros(ctx.cpt_total, dtype=torch.int32, device="cuda")
+        ws = ctx.new_workspace()
+        same.same_counts(ctx, st, w.m, 5_000, w.ld, mb, tot, ws)
+        for s in range(2):
+            same.same_step(ctx, st, ob, th, w.m, 5_000, w.ld, 0, w.seed, s, mb, tot, s, ws)
+        torch.cuda.synchronize()
+        outs.append([H.from_device(ctx, st, w.m), mb.cpu().numpy(), tot.cpu().numpy(), th.cpu().numpy()])
+    for o in outs[1:]:
+        for x, y in zip(outs[0], o):
+            assert np.array_equal(x, y)
+
+
+def test_lockstep_loop_4bit():
+    w = make_workload(4, n_cols=1_000)
+    net = w.net
+    ctx = H.context_for(net, state_bits=4)
+    color = oracle.graph(net.parents, net.card)["color"]
+    ws = ctx.new_workspace()
+    theta = w.init_theta.copy()
+    st = w.states[0].numpy().copy()
+    obs = w.obs[0].numpy()
+    mb = oracle.counts(net.parents, net.card, st, w.m, w.n_cols)
+    totals = mb.copy()
+    for s in range(4):
+        pre = st.copy()
+        res = oracle.sweep(net.parents, net.card, theta, color, st, obs, w.m, w.n_cols, 0, w.seed, s,
+                           want_flags=True)
+        gpu, _ = H.gpu_sweep(ctx, pre, obs, theta, w.m, w.n_cols, 0, w.seed, s)
+        H.compare_states(gpu, st, res["flags"], color, w.n_cols)
+        new = oracle.counts(net.parents, net.card, st, w.m, w.n_cols)
+        d_mb = torch.from_numpy(mb.astype(np.int32)).cuda()
+        d_tot = torch.from_numpy(totals.astype(np.int32)).cuda()
+        same.same_counts(ctx, H.to_device(ctx, st), w.m, w.n_cols, w.ld, d_mb, d_tot, ws)
+        totals = oracle.moving_sum(totals, mb, new)
+        mb = new
+        th_gpu = torch.empty(ctx.cpt_total, dtype=torch.float32, device="cuda")
+        same.same_sample_cpts(ctx, d_tot, th_gpu, w.seed, s, ws)
+        torch.cuda.synchronize()
+        assert np.array_equal(d_mb.cpu().numpy(), new)
+        assert np.array_equal(d_tot.cpu().numpy(), totals)
+        theta = oracle.dirichlet(net.parents, net.card, totals, w.alpha, w.seed, s)
+        assert np.mean(th_gpu.cpu().numpy() == theta) >= 1.0 - 1e-5
+
+
+def test_padding_slots_may_hold_anything_4bit():
+    card = [3, 3, 4, 2, 5]
+    parents = [[], [0], [0, 1], [2], [1, 2, 3]]
+    n_cols, ld, m = 3001, 3004, 5
+    net, st, ob, th = _custom(parents, card, n_cols, m, 0.5, 31, ld=ld)
+    outs = []
+    for fill in (False, True):
+        q = same.pack_states(st, 4)
+        if fill:  # slots 1..3 of the last quad (replicas 5..7) hold 15, out of range for every node
+            q[:, -1, :] = (q[:, -1, :].view(np.uint16) | np.uint16(0xFFF0)).view(np.int16)
+        ctx = H.context_for(net, state_bits=4)
+        d_st = torch.from_numpy(q).cuda()
+        d_ob = torch.from_numpy(ob).cuda()
+        d_th = torch.from_numpy(th.astype(np.float32)).cuda()
+        mb = torch.zeros(ctx.cpt_total, dtype=torch.int32, device="cuda")
+        tot = torch.zeros(ctx.cpt_total, dtype=torch.int32, device="cuda")
+        ws = ctx.new_workspace()
+        same.same_counts(ctx, d_st, m, n_cols, ld, mb, tot, ws)
+        for s in range(2):
+            same.same_step(ctx, d_st, d_ob, d_th, m, n_cols, ld, 0, 5, s, mb, tot, s, ws)
+        torch.cuda.synchronize()
+        outs.append([H.from_device(ctx, d_st, m), mb.cpu().numpy(), tot.cpu().numpy(), d_th.cpu().numpy()])
+    for x, y in zip(*outs):
+        assert np.array_equal(x, y)
+    assert np.array_equal(outs[1][1], oracle.counts(parents, card, outs[1][0], m, n_cols))

@@ -20,9 +20,9 @@ def _gpu():
     same.load_library()
 
 
-def _host_arrays(w):
-    """Pinned host states in the library's layout ([n][mq][host_ld][4]) and
-    [n][host_ld] obs holding all columns."""
+def _host_arrays(w, bits=None):
+    """Pinned host states in the library's layout (replica quads, 4-bit with
+    bits=4) and [n][host_ld] obs holding all columns."""
     n = w.net.n
     host_ld = (w.n_cols + 3) // 4 * 4
     full = torch.zeros((n, w.m, host_ld), dtype=w.states[0].dtype)
@@ -31,12 +31,12 @@ def _host_arrays(w):
         c0, nc = b * w.nb, w.mb_cols(b)
         full[:, :, c0:c0 + nc] = w.states[b][:, :, :nc]
         ob[:, c0:c0 + nc] = w.obs[b][:, :nc]
-    return same.pack_states(full).pin_memory(), ob, host_ld
+    return same.pack_states(full, bits).pin_memory(), ob, host_ld
 
 
 def _resident(w, ctx, passes):
     """The device-resident call sequence; returns the states as [n][m][ld]."""
-    dev = [same.pack_states(s).cuda() for s in w.states]
+    dev = [H.to_device(ctx, s) for s in w.states]
     obs = [o.cuda() for o in w.obs]
     ws = ctx.new_workspace()
     cpts = torch.from_numpy(w.init_theta).cuda()
@@ -51,11 +51,11 @@ def _resident(w, ctx, passes):
             same.same_counts(ctx, dev[b], w.m, w.mb_cols(b), w.ld, mb[b], tot, ws)
             same.same_sample_cpts(ctx, tot, cpts, w.seed, s * w.M + b, ws)
     torch.cuda.synchronize()
-    return [same.unpack_states(d.cpu(), w.m) for d in dev], mb.cpu(), tot.cpu(), cpts.cpu()
+    return [torch.from_numpy(H.from_device(ctx, d, w.m)) for d in dev], mb.cpu(), tot.cpu(), cpts.cpu()
 
 
 def _streamed(w, ctx, passes, on_pass=None):
-    st, ob, host_ld = _host_arrays(w)
+    st, ob, host_ld = _host_arrays(w, H.bits_of(ctx))
     ws = ctx.new_workspace()
     slots = torch.empty(same.same_stream_slots_size(ctx, w.m, w.nb), dtype=torch.uint8, device="cuda")
     cpts = torch.from_numpy(w.init_theta).cuda()
@@ -68,9 +68,9 @@ def _streamed(w, ctx, passes, on_pass=None):
                               slots, ws)
         if on_pass is not None:
             torch.cuda.synchronize()
-            on_pass(s, same.unpack_states(st, w.m), mb, tot, cpts)
+            on_pass(s, same.unpack_states(st, w.m, H.bits_of(ctx)), mb, tot, cpts)
     torch.cuda.synchronize()
-    return same.unpack_states(st, w.m), mb.cpu(), tot.cpu(), cpts.cpu()
+    return same.unpack_states(st, w.m, H.bits_of(ctx)), mb.cpu(), tot.cpu(), cpts.cpu()
 
 
 @pytest.mark.parametrize("cfg,kw", [
@@ -78,9 +78,10 @@ def _streamed(w, ctx, passes, on_pass=None):
     (5, dict(n_cols=6_000, nb=1_500, m=2)),      # 1000 nodes, 4 minibatches
     (1, dict(n_cols=1_000, nb=4_096, m=2)),      # one minibatch smaller than nb
 ])
-def test_stream_equals_resident(cfg, kw):
+@pytest.mark.parametrize("bits", [0, 4], ids=["8bit", "4bit"])
+def test_stream_equals_resident(cfg, kw, bits):
     w = make_workload(cfg, **kw)
-    ctx = H.context_for(w.net)
+    ctx = H.context_for(w.net, state_bits=bits)
     res_states, res_mb, res_tot, res_cpts = _resident(w, ctx, passes=2)
     st, mb, tot, cpts = _streamed(w, ctx, passes=2)
     for b in range(w.M):
@@ -202,12 +203,13 @@ def _compact_case(w, ctx, passes):
     (1, dict(n_cols=1_000, nb=4_096, m=2)),
     (4, dict(n_cols=3_000, nb=1_000, m=5)),      # concepts never observed
 ])
-def test_compact_stream_equals_resident(cfg, kw):
+@pytest.mark.parametrize("bits", [0, 4], ids=["8bit", "4bit"])
+def test_compact_stream_equals_resident(cfg, kw, bits):
     """Out-of-core passes that move only the compacted latent states over PCIe
     (known data resident on the device) equal the device-resident call
     sequence bit for bit: states, per-minibatch counts, totals and CPTs."""
     w = make_workload(cfg, **kw)
-    ctx = H.context_for(w.net)
+    ctx = H.context_for(w.net, state_bits=bits)
     res_states, res_mb, res_tot, res_cpts = _resident(w, ctx, passes=2)
     dense, mb, tot, cpts = _compact_case(w, ctx, passes=2)
     for b in range(w.M):

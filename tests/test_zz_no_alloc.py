@@ -94,3 +94,18 @@ def test_noalloc_errors():
         same.same_counts_noalloc(big, torch.zeros(same.state_shape(7, 1, 4), dtype=torch.int8, device="cuda"), 1, 4, 4,
                                  torch.zeros(8, dtype=torch.int32, device="cuda"), None)
     assert e.value.code == same.SAME_ESIZE
+
+
+def test_noalloc_counts_4bit():
+    """4-bit states: same_counts_noalloc equals same_counts on two calls in a
+    row, the second over fewer columns."""
+    w = make_workload(5, n_cols=9_000, m=10)
+    ctx = H.context_for(w.net, state_bits=4)
+    rng = np.random.default_rng(44)
+    st = H.to_device(ctx, w.states[0])
+    for n_cols in (w.mb_cols(0), w.mb_cols(0) // 3 + 1):
+        prev = rng.integers(0, 500, ctx.cpt_total).astype(np.int32)
+        tot0 = (prev + rng.integers(0, 500, ctx.cpt_total)).astype(np.int32)
+        (mb_a, tot_a), (mb_b, tot_b) = _both(ctx, st, w.m, n_cols, w.ld, prev, tot0)
+        assert np.array_equal(mb_a, mb_b)
+        assert np.array_equal(tot_a, tot_b)
