@@ -46,6 +46,9 @@ def parse():
                    help="SAME steps (sweep + counts + resample) of the oracle baseline")
     p.add_argument("--copy-calibration", action="store_true",
                    help="(kept for older profile commands: the 1 GiB copy now always runs)")
+    p.add_argument("--state-bits", type=int, default=-1,
+                   help="bits per state in the library's state quads: 4 (every K <= 16), 0 for 8/16-bit; "
+                        "default: 4 when the network allows it")
     p.add_argument("--graph-steps", type=int, default=8,
                    help="SAME steps per captured graph in the graphed timing (single-minibatch workloads)")
     p.add_argument("--roofline-steps", type=int, default=1,
@@ -117,10 +120,10 @@ def main():
         sample = (cols, np.ascontiguousarray(w.states[0][:, :, :cols4].cpu().numpy()),
                   np.ascontiguousarray(w.obs[0][:, :cols4].cpu().numpy()))
     pptr, pidx, card = net.csr()
-    if args.table_limit is None:
-        ctx = same.same_create(pptr, pidx, card, w.alpha)
-    else:
-        ctx = same.same_create_ex(pptr, pidx, card, w.alpha, args.table_limit)
+    bits = args.state_bits if args.state_bits >= 0 else (4 if int(net.card.max()) <= 16 else 0)
+    ctx = same.same_create_ex(pptr, pidx, card, w.alpha, -1 if args.table_limit is None else args.table_limit,
+                              state_bits=bits)
+    w.bits = 4 if ctx.state_bits == 4 else None   # pack_states / unpack_states argument
     ws = ctx.new_workspace(dev)
     cpts = torch.from_numpy(w.init_theta).to(dev)
     cpts0 = cpts.clone()
@@ -135,7 +138,7 @@ def main():
     # the library's replica-quad layout of the timed minibatches (input
     # preparation, on the device); the generator's row layout stays for the
     # oracle's sample and the host-side preparations
-    w.pk = {b: same.pack_states(w.states[b]) for b in mbs}
+    w.pk = {b: same.pack_states(w.states[b], w.bits) for b in mbs}
     torch.cuda.synchronize()
 
     # count-only pre-pass initialises the per-minibatch counts and their sum
@@ -184,7 +187,7 @@ def main():
     node_samples_r = float(net.n) * cols_timed * w.m * rsteps
 
     copy_gbs = copy_peak(dev, stream)
-    roofline = sweep_roofline(w, net, mbs, hidden, node_samples_r, kt, wall_r, args, copy_gbs)
+    roofline = sweep_roofline(w, net, mbs, hidden, node_samples_r, kt, wall_r, args, copy_gbs, ctx)
     graphed = graph_timing(w, ctx, mbs, cpts, mb, tot, ws, args.warmup + args.steps + rsteps, args.steps, dev,
                            stream, args.graph_steps)
     log("graphed %d passes: %.3f ms per pass" % (args.steps, graphed["ms_per_step"]))
@@ -233,11 +236,12 @@ def main():
             "replicas": w.m,
             "nodes": net.n,
             "colors": ctx.n_colors,
+            "state_bits": ctx.state_bits,
             "hidden_fraction": round(hidden, 4),
             "parallelism": "single-gpu",
         },
         "latent_draws_per_s": round(value * hidden, 1),
-        "hbm_gbs_algorithmic_step": round(node_samples * (1.0 + hidden + 1.0 / w.m) / elapsed / 1e9, 1),
+        "hbm_gbs_algorithmic_step": round(node_samples * bytes_per_node_sample(ctx, hidden, w.m) / elapsed / 1e9, 1),
         "roofline": roofline,
         "graphed": graphed,
         "parity": parity,
@@ -321,15 +325,20 @@ def traffic_path(cfg):
     return os.path.join(ROOT, "profiles", "sweep_fast_kernel.%s.traffic.json" % CONFIGS[cfg]["name"])
 
 
-def measured_traffic(cfg):
+def state_type_name(bits):
+    return {4: "Nib", 8: "int8", 16: "int16"}[bits]
+
+
+def measured_traffic(cfg, bits):
     """HBM bytes per sweep-kernel launch from the committed counter summary of
-    this workload, if it was taken on the current kernel sources (else None)."""
+    this workload, if it was taken on the current kernel sources and state
+    format (else None)."""
     path = traffic_path(cfg)
     if not os.path.exists(path):
         return None
     with open(path) as fh:
         t = json.load(fh)
-    if t.get("sources_sha256") != source_hash():
+    if t.get("sources_sha256") != source_hash() or t.get("state_bits") != bits:
         return None
     return t
 
@@ -371,11 +380,11 @@ def first_sweep_parity(w, ctx, cpts0, ws, sample, cols, dev):
     cols = min(cols, _cols) // 4 * 4
     pre = np.ascontiguousarray(st[:, :, :cols])
     obs = np.ascontiguousarray(ob[:, :cols])
-    d_st = torch.from_numpy(same.pack_states(pre)).to(dev)
+    d_st = torch.from_numpy(same.pack_states(pre, w.bits)).to(dev)
     d_ob = torch.from_numpy(obs).to(dev)
     same.same_sweep(ctx, d_st, d_ob, cpts0, w.m, cols, cols, 0, w.seed, 0, ws)
     torch.cuda.synchronize()
-    gpu = same.unpack_states(d_st.cpu().numpy(), w.m)
+    gpu = same.unpack_states(d_st.cpu().numpy(), w.m, w.bits)
     del d_st, d_ob
     ref = pre.copy()
     color = oracle.graph(net.parents, net.card)["color"]
@@ -398,9 +407,17 @@ def first_sweep_parity(w, ctx, cpts0, ws, sample, cols, dev):
             "unexcused_mismatches": unexcused, "ok": unexcused == 0 and n_chains < 1e-5 * draws}
 
 
-def sweep_roofline(w, net, mbs, hidden, node_samples, kt, elapsed, args, copy_gbs):
+def bytes_per_node_sample(ctx, hidden, m):
+    """Algorithmic bytes per (node, column, replica) slot of a sweep: read
+    every state once, write every latent state once (bits / 8 bytes each) and
+    read the obs byte once per column (shared by the m replicas)."""
+    sb = ctx.state_bits / 8.0
+    return sb * (1.0 + hidden) + 1.0 / m
+
+
+def sweep_roofline(w, net, mbs, hidden, node_samples, kt, elapsed, args, copy_gbs, ctx):
     """Roofline of the dominant kernel, the LDS-staged sweep kernel
-    (sweep_fast_kernel<int8, false, true>, launch class 0), which draws almost
+    (sweep_fast_kernel, LDS-staged, launch class 0), which draws almost
     every node of the workload in one launch per colour group: the algorithmic
     bytes of the (node, column, replica) slots its launches covered per second
     of its own launch time, against HBM peak.  Beside it: algorithmic 32-bit
@@ -411,7 +428,7 @@ def sweep_roofline(w, net, mbs, hidden, node_samples, kt, elapsed, args, copy_gb
     import numpy as np
     assert kt["launches"][2] == 0 and kt["launches"][3] == 0, \
         "this workload is expected to run entirely in the fast sweep kernel"
-    bytes_per_ns = 1.0 + hidden + 1.0 / w.m   # read each state, write each latent, obs per column
+    bytes_per_ns = bytes_per_node_sample(ctx, hidden, w.m)
     alg_bytes = node_samples * bytes_per_ns
     # latent draws per node per step, from the obs masks of the timed minibatches
     lat = np.zeros(net.n)
@@ -424,12 +441,12 @@ def sweep_roofline(w, net, mbs, hidden, node_samples, kt, elapsed, args, copy_gb
     secs0 = ms0 / 1e3
     hbm = bytes0 / secs0 / 1e9
     alu = ops0 / secs0 / 1e12
-    traffic = measured_traffic(args.cfg)
+    traffic = measured_traffic(args.cfg, ctx.state_bits)
     avg_ms = ms0 / n0
     phase_s = kt["phase_ms"] / 1e3
     out = {
-        "kernel": "sweep_fast_kernel<int8, false, true> (tables staged in LDS, whole or in part; "
-                  "every launch of the timed passes)",
+        "kernel": "sweep_fast_kernel<%s, false, true> (tables staged in LDS, whole or in part; "
+                  "every launch of the timed passes)" % state_type_name(ctx.state_bits),
         "bound": "hbm",
         "achieved": round(hbm, 1),
         "peak": HBM_PEAK_GBS,
@@ -536,8 +553,11 @@ def counters_summary(paths, cfg):
     wb, nw = per_launch("WRITE_SIZE")
     fb *= f_scale
     wb *= w_scale
+    names = " ".join(sweep)
+    bits = 4 if "Nib" in names else (16 if "short" in names else 8)
     out = {
-        "kernel": "sweep_fast_kernel<int8, false, true> (LDS-staged, non-debug)",
+        "kernel": "sweep_fast_kernel<%s, false, true> (LDS-staged, non-debug)" % state_type_name(bits),
+        "state_bits": bits,
         "workload_cfg": cfg,
         "copy_kernel": copy[0],
         "copy_counters_kib": {"FETCH_SIZE": fetch_copy, "WRITE_SIZE": copy[2]},
@@ -797,12 +817,12 @@ def stream_timing(w, ctx, cpts, ws, dev, steps):
     net = w.net
     host_ld = (w.n_cols + 3) // 4 * 4
     t0 = time.time()
-    hs = torch.empty(same.state_shape(net.n, w.m, host_ld), dtype=w.states[0].dtype, pin_memory=True)
+    hs = torch.empty(same.state_shape(net.n, w.m, host_ld, ctx.state_bits), dtype=w.pk[0].dtype, pin_memory=True)
     ho = torch.empty((net.n, host_ld), dtype=torch.uint8, pin_memory=True)
     for b in range(w.M):
         c0, nc = b * w.nb, w.mb_cols(b)
         for i in range(net.n):
-            hs[i, :, c0:c0 + nc, :].copy_(w.pk[b][i, :, :nc, :])
+            hs[i, :, c0:c0 + nc, ...].copy_(w.pk[b][i, :, :nc, ...])
             ho[i, c0:c0 + nc].copy_(w.obs[b][i, :nc])
     torch.cuda.synchronize()
     log("pinned host copy of the data (%.1f GB) in %.1f s" % (
@@ -822,7 +842,7 @@ def stream_timing(w, ctx, cpts, ws, dev, steps):
     torch.cuda.synchronize()
     dt = time.perf_counter() - t
     ns = float(net.n) * w.n_cols * w.m * steps
-    state_bytes = float(net.n) * 4 * ((w.m + 3) // 4) * w.n_cols * hs.element_size()  # padding slots included
+    state_bytes = float(net.n) * ((w.m + 3) // 4) * w.n_cols * (ctx.state_bits // 2)  # quads, padding included
     h2d = state_bytes + float(net.n) * w.n_cols
     log("streamed %d passes in %.3f s" % (steps, dt))
     # the same passes with the exponential moving sum of the counts (Sec. 4

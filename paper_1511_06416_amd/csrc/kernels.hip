@@ -1232,14 +1232,13 @@ template <typename ST, int NQ>
 struct Span {
     using V = typename Quad<ST>::V;
     static constexpr int kWords = NQ * Quad<ST>::kBytes / 4;  // 32-bit words of NQ quads
-    V q[NQ];
+    uint32_t w[kWords];                                       // the quads as loaded
 
     template <bool WIDE>
     __device__ void load(const void *__restrict__ states, int32_t node, int64_t vstride, uint32_t boff,
                          bool whole) {
         const __amdgpu_buffer_rsrc_t r = node_rsrc<ST>(states, node, vstride);
         if (WIDE && whole) {
-            uint32_t w[kWords];
             if constexpr (kWords == 2) {
                 const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, (int)boff, 0, 0);
                 w[0] = v.x;
@@ -1255,20 +1254,62 @@ struct Span {
                     w[4 * i + 3] = v.w;
                 }
             }
-#pragma unroll
-            for (int j = 0; j < NQ; ++j) q[j] = from_words(w, j);
         } else {
 #pragma unroll
-            for (int j = 0; j < NQ; ++j) q[j] = Quad<ST>::load_buffer(r, boff + (uint32_t)(j * Quad<ST>::kBytes));
+            for (int j = 0; j < NQ; ++j) {
+                const V q = Quad<ST>::load_buffer(r, boff + (uint32_t)(j * Quad<ST>::kBytes));
+                if constexpr (Quad<ST>::kBytes == 2) {
+                    if (j & 1) w[j >> 1] |= q << 16;
+                    else w[j >> 1] = q;
+                } else if constexpr (Quad<ST>::kBytes == 4) {
+                    w[j] = q;
+                } else {
+                    w[2 * j] = q.x;
+                    w[2 * j + 1] = q.y;
+                }
+            }
         }
     }
 
-  private:
-    template <int N>
-    __device__ static V from_words(const uint32_t (&w)[N], int j) {
+    // state quad of column j
+    __device__ V quad(int j) const {
         if constexpr (Quad<ST>::kBytes == 2) return (w[j >> 1] >> (16 * (j & 1))) & 0xffffu;
         else if constexpr (Quad<ST>::kBytes == 4) return w[j];
         else return make_uint2(w[2 * j], w[2 * j + 1]);
+    }
+
+    // The span's NQ x 4 states as 16-bit lanes, 2 NQ words: for 8- and
+    // 16-bit states two slots of one column per word (Quad::split); for 4-bit
+    // states one slot of two adjacent columns per word (a 32-bit word holds
+    // the quads of columns 2p and 2p + 1, so one shift and mask per slot).
+    __device__ void lanes(uint32_t (&L)[2 * NQ]) const {
+        if constexpr (Quad<ST>::kBytes == 2) {
+#pragma unroll
+            for (int p = 0; p < NQ / 2; ++p)
+#pragma unroll
+                for (int c = 0; c < 4; ++c) L[4 * p + c] = (w[p] >> (4 * c)) & 0x000f000fu;
+        } else {
+#pragma unroll
+            for (int h = 0; h < NQ; ++h) {
+                uint32_t p2[2];
+                Quad<ST>::split(quad(h), p2);
+                L[2 * h] = p2[0];
+                L[2 * h + 1] = p2[1];
+            }
+        }
+    }
+
+    // the 16-bit lane of (column h, slot c) in the layout of lanes()
+    __device__ static uint32_t lane_of(const uint32_t (&L)[2 * NQ], int h, int c) {
+        uint32_t v, hi;
+        if constexpr (Quad<ST>::kBytes == 2) {
+            v = L[4 * (h >> 1) + c];
+            hi = h & 1;
+        } else {
+            v = L[2 * h + Quad<ST>::word_of(c)];
+            hi = Quad<ST>::half_of(c);
+        }
+        return hi ? v >> 16 : v & 0xffffu;
     }
 };
 
@@ -1353,14 +1394,14 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
 #pragma unroll
                     for (int h = 0; h < NQ; ++h)
 #pragma unroll
-                        for (int c = 0; c < 4; ++c) u[h][c] += (uint32_t)Q::get(sp.q[h], c) * stride;
+                        for (int c = 0; c < 4; ++c) u[h][c] += (uint32_t)Q::get(sp.quad(h), c) * stride;
                 }
 #pragma unroll
                 for (int h = 0; h < NQ; ++h)
 #pragma unroll
                     for (int c = 0; c < 4; ++c)
                         if (h < nvalid && c < nrep)
-                            add((int)(u[h][c] * (uint32_t)K + (uint32_t)Q::get(own.q[h], c)));
+                            add((int)(u[h][c] * (uint32_t)K + (uint32_t)Q::get(own.quad(h), c)));
             }
             continue;
         }
@@ -1378,11 +1419,9 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
                 own[t].template load<WIDE>(states, node, vstride, boff[t], whole);
             }
             // bin = sum over parents of x_p * (stride_p * K) + x_node
-            uint32_t Pk[kCountQuads][NQ][2];
+            uint32_t Pk[kCountQuads][2 * NQ];
 #pragma unroll
-            for (int t = 0; t < kCountQuads; ++t)
-#pragma unroll
-                for (int h = 0; h < NQ; ++h) Q::split(own[t].q[h], Pk[t][h]);
+            for (int t = 0; t < kCountQuads; ++t) own[t].lanes(Pk[t]);
             for (int q = 0; q < n_par; ++q) {
                 const uint32_t mult = (uint32_t)(par[2 * q + 1] * K) * 0x10001u;
                 S sp[kCountQuads];
@@ -1393,13 +1432,10 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
                 // counted: no exit from the unrolled loop
 #pragma unroll
                 for (int t = 0; t < kCountQuads; ++t) {
+                    uint32_t L[2 * NQ];
+                    sp[t].lanes(L);
 #pragma unroll
-                    for (int h = 0; h < NQ; ++h) {
-                        uint32_t p2[2];
-                        Q::split(sp[t].q[h], p2);
-                        Pk[t][h][0] = pk_mad_u16(p2[0], mult, Pk[t][h][0]);
-                        Pk[t][h][1] = pk_mad_u16(p2[1], mult, Pk[t][h][1]);
-                    }
+                    for (int i = 0; i < 2 * NQ; ++i) Pk[t][i] = pk_mad_u16(L[i], mult, Pk[t][i]);
                 }
             }
 #pragma unroll
@@ -1410,7 +1446,7 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
                     for (int h = 0; h < NQ; ++h)
 #pragma unroll
                         for (int c = 0; c < 4; ++c)
-                            if (h < nvalid && c < nrep) add((int)packed_index<ST>(Pk[t][h], c));
+                            if (h < nvalid && c < nrep) add((int)S::lane_of(Pk[t], h, c));
                 }
             }
         }
