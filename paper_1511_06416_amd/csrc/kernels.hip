@@ -8,6 +8,7 @@
 // loads of a wavefront fall in a few cache lines per replica row.  The count
 // and ingest kernels read whole column quads (dwords) per lane.
 #include <hip/hip_runtime.h>
+#include <type_traits>
 
 #include <cfloat>
 #include <cstdint>
@@ -1341,9 +1342,11 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
     cint32_t *d = as_const(cdesc) + as_const(cdesc_off)[node];
     const int K = d[0], n_par = d[1], nbins = d[2], off = d[3];
     cint32_t *par = d + 4;
-    const int mode = nbins <= kRepBins ? 0 : (lo >= 0 ? 1 : 2);
-    const int range = nbins - lo < kLdsBins ? nbins - lo : kLdsBins;  // mode 1: this item's bins
-    const int lds_words = mode == 0 ? nbins * kCopies : (mode == 1 ? range : 0);
+    // histogram modes: 0 interleaved copies, 1 the whole CPT in one shared
+    // histogram, 3 one bin range of a larger CPT in it, 2 global atomics
+    const int mode = nbins <= kRepBins ? 0 : (lo < 0 ? 2 : (lo == 0 && nbins <= kLdsBins ? 1 : 3));
+    const int range = nbins - lo < kLdsBins ? nbins - lo : kLdsBins;  // modes 1, 3: this item's bins
+    const int lds_words = mode == 0 ? nbins * kCopies : (mode == 2 ? 0 : range);
     for (int b = threadIdx.x; b < lds_words; b += kBlock) hist[b] = 0;
     __syncthreads();
     const int copy = threadIdx.x & (kCopies - 1);
@@ -1358,25 +1361,16 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
     const int64_t c1 = c0 + cols_per_block < col0 + n_cols ? c0 + cols_per_block : col0 + n_cols;
     const int64_t vstride = node_bytes<ST>(m, ld);
     const bool packed = nbins <= 65536;
-    auto add = [&](int bin) {
-        if (mode == 0) {
-            atomicAdd(&hist[bin * kCopies + copy], 1);
-        } else if (mode == 1) {
-            const uint32_t hb = (uint32_t)(bin - lo);
-            if (hb < (uint32_t)range) atomicAdd(&hist[hb], 1);
-        } else {
-            atomicAdd(&counts[off + bin], 1);
-        }
-    };
     // a lane covers NQ adjacent columns (one state quad each), read with wide
     // loads per replica quad
     constexpr int NQ = kCountQuadsPerLane;
     using S = Span<ST, NQ>;
-    for (int64_t col = c0 + NQ * (int64_t)threadIdx.x; col < c1; col += NQ * kBlock) {
-        const int nvalid = c1 - col < NQ ? (int)(c1 - col) : NQ;
-        const bool whole = col + NQ <= ld;
-        if (!packed) {
-            // 32-bit indices (more than 2^16 bins): one replica quad at a time
+    if (!packed) {
+        // 32-bit indices (more than 2^16 bins, global atomics): one replica
+        // quad at a time
+        for (int64_t col = c0 + NQ * (int64_t)threadIdx.x; col < c1; col += NQ * kBlock) {
+            const int nvalid = c1 - col < NQ ? (int)(c1 - col) : NQ;
+            const bool whole = col + NQ <= ld;
             for (int rq = qb; rq < qe; ++rq) {
                 const int nrep = m - 4 * rq < 4 ? m - 4 * rq : 4;
                 const uint32_t boff = quad_boff<ST>(rq, ld, col);
@@ -1401,56 +1395,92 @@ __global__ __launch_bounds__(kBlock) void count_kernel(const int32_t *__restrict
 #pragma unroll
                     for (int c = 0; c < 4; ++c)
                         if (h < nvalid && c < nrep)
-                            add((int)(u[h][c] * (uint32_t)K + (uint32_t)Q::get(own.quad(h), c)));
+                            atomicAdd(&counts[off + u[h][c] * (uint32_t)K + (uint32_t)Q::get(own.quad(h), c)], 1);
             }
-            continue;
         }
-        for (int rq0 = qb; rq0 < qe; rq0 += kCountQuads) {
-            const int nq = qe - rq0 < kCountQuads ? qe - rq0 : kCountQuads;
-            uint32_t boff[kCountQuads];
-            S own[kCountQuads];
-            // every slot loads (a fixed count keeps all loads in flight at
-            // once); slots past the last replica quad read through the node's
-            // buffer resource past its end, which returns 0 without a memory
-            // access, and their values are never used
-#pragma unroll
-            for (int t = 0; t < kCountQuads; ++t) {
-                boff[t] = quad_boff<ST>(rq0 + t, ld, col);
-                own[t].template load<WIDE>(states, node, vstride, boff[t], whole);
+        return;
+    }
+    // packed 16-bit bins.  The histogram mode is uniform per block, so each
+    // mode has its own copy of the column loop: no per-slot dispatch.
+    auto run = [&](auto md) {
+        constexpr int MD = decltype(md)::value;
+        auto add = [&](uint32_t bin) {
+            if constexpr (MD == 0) {
+                atomicAdd(&hist[bin * kCopies + copy], 1);
+            } else if constexpr (MD == 1) {
+                atomicAdd(&hist[bin], 1);
+            } else if constexpr (MD == 3) {
+                const uint32_t hb = bin - (uint32_t)lo;
+                if (hb < (uint32_t)range) atomicAdd(&hist[hb], 1);
+            } else {
+                atomicAdd(&counts[off + bin], 1);
             }
-            // bin = sum over parents of x_p * (stride_p * K) + x_node
-            uint32_t Pk[kCountQuads][2 * NQ];
-#pragma unroll
-            for (int t = 0; t < kCountQuads; ++t) own[t].lanes(Pk[t]);
-            for (int q = 0; q < n_par; ++q) {
-                const uint32_t mult = (uint32_t)(par[2 * q + 1] * K) * 0x10001u;
-                S sp[kCountQuads];
-#pragma unroll
-                for (int t = 0; t < kCountQuads; ++t)
-                    sp[t].template load<WIDE>(states, par[2 * q], vstride, boff[t], whole);
-                // slots past the last quad compute on zeros and are never
-                // counted: no exit from the unrolled loop
+        };
+        for (int64_t col = c0 + NQ * (int64_t)threadIdx.x; col < c1; col += NQ * kBlock) {
+            const int nvalid = c1 - col < NQ ? (int)(c1 - col) : NQ;
+            const bool whole = col + NQ <= ld;
+            // every lane of the wave holds NQ columns (uniform)
+            const bool full = __all(nvalid == NQ);
+            for (int rq0 = qb; rq0 < qe; rq0 += kCountQuads) {
+                const int nq = qe - rq0 < kCountQuads ? qe - rq0 : kCountQuads;
+                uint32_t boff[kCountQuads];
+                S own[kCountQuads];
+                // every slot loads (a fixed count keeps all loads in flight at
+                // once); slots past the last replica quad read through the
+                // node's buffer resource past its end, which returns 0 without
+                // a memory access, and their values are never used
 #pragma unroll
                 for (int t = 0; t < kCountQuads; ++t) {
-                    uint32_t L[2 * NQ];
-                    sp[t].lanes(L);
-#pragma unroll
-                    for (int i = 0; i < 2 * NQ; ++i) Pk[t][i] = pk_mad_u16(L[i], mult, Pk[t][i]);
+                    boff[t] = quad_boff<ST>(rq0 + t, ld, col);
+                    own[t].template load<WIDE>(states, node, vstride, boff[t], whole);
                 }
-            }
+                // bin = sum over parents of x_p * (stride_p * K) + x_node
+                uint32_t Pk[kCountQuads][2 * NQ];
 #pragma unroll
-            for (int t = 0; t < kCountQuads; ++t) {
-                if (t < nq) {  // uniform
+                for (int t = 0; t < kCountQuads; ++t) own[t].lanes(Pk[t]);
+                for (int q = 0; q < n_par; ++q) {
+                    const uint32_t mult = (uint32_t)(par[2 * q + 1] * K) * 0x10001u;
+                    S sp[kCountQuads];
+#pragma unroll
+                    for (int t = 0; t < kCountQuads; ++t)
+                        sp[t].template load<WIDE>(states, par[2 * q], vstride, boff[t], whole);
+                    // slots past the last quad compute on zeros and are never
+                    // counted: no exit from the unrolled loop
+#pragma unroll
+                    for (int t = 0; t < kCountQuads; ++t) {
+                        uint32_t L[2 * NQ];
+                        sp[t].lanes(L);
+#pragma unroll
+                        for (int i = 0; i < 2 * NQ; ++i) Pk[t][i] = pk_mad_u16(L[i], mult, Pk[t][i]);
+                    }
+                }
+#pragma unroll
+                for (int t = 0; t < kCountQuads; ++t) {
+                    if (t >= nq) continue;  // uniform
                     const int nrep = m - 4 * (rq0 + t) < 4 ? m - 4 * (rq0 + t) : 4;
-#pragma unroll
-                    for (int h = 0; h < NQ; ++h)
+                    if (full) {
+                        // uniform branches only
 #pragma unroll
                         for (int c = 0; c < 4; ++c)
-                            if (h < nvalid && c < nrep) add((int)S::lane_of(Pk[t], h, c));
+                            if (c < nrep)
+#pragma unroll
+                                for (int h = 0; h < NQ; ++h) add(S::lane_of(Pk[t], h, c));
+                    } else {
+#pragma unroll
+                        for (int c = 0; c < 4; ++c)
+                            if (c < nrep)
+#pragma unroll
+                                for (int h = 0; h < NQ; ++h)
+                                    if (h < nvalid) add(S::lane_of(Pk[t], h, c));
+                    }
                 }
             }
         }
-    }
+    };
+    if (mode == 0) run(std::integral_constant<int, 0>{});
+    else if (mode == 1) run(std::integral_constant<int, 1>{});
+    else if (mode == 3) run(std::integral_constant<int, 3>{});
+    else run(std::integral_constant<int, 2>{});
     if (mode == 2) return;
     __syncthreads();
     for (int b = threadIdx.x; b < (mode == 0 ? nbins : range); b += kBlock) {
