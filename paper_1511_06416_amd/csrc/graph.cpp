@@ -527,6 +527,29 @@ int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int
         }
     }
 
+    // count work ordered by each family's smallest parent (a root by itself,
+    // just before the families whose smallest parent it is): families that
+    // share a parent run together, so its rows are re-read from L2 rather
+    // than from memory.  The order changes no count (integer atomics).
+    {
+        const size_t nw = g.cwork.size() / 2;
+        std::vector<std::pair<int64_t, size_t>> key(nw);
+        for (size_t w = 0; w < nw; ++w) {
+            const int32_t i = g.cwork[2 * w];
+            int64_t k = 2 * (int64_t)i;
+            for (int32_t a = pptr[i]; a < pptr[i + 1]; ++a) k = std::min(k, 2 * (int64_t)g.pidx[a] + 1);
+            key[w] = {k, w};
+        }
+        std::stable_sort(key.begin(), key.end());
+        std::vector<int32_t> cw;
+        cw.reserve(g.cwork.size());
+        for (const auto &kw : key) {
+            cw.push_back(g.cwork[2 * kw.second]);
+            cw.push_back(g.cwork[2 * kw.second + 1]);
+        }
+        g.cwork.swap(cw);
+    }
+
     // launch order: per colour, the nodes of each launch class in turn, and
     // per (colour, class) the LDS bytes the launch needs
     g.launch.assign((size_t)g.n_colors * (kLaunchClasses + 1), 0);
