@@ -167,10 +167,12 @@ struct Quad<Nib> {
         return (v & ~(0xfu << (4 * c))) | ((uint32_t)(x & 0xf) << (4 * c));
     }
     __device__ static V keep(V v, int nvalid) { return nvalid >= 4 ? v : (v & ((1u << (4 * nvalid)) - 1u)); }
-    // the 4 states as 16-bit lanes: p[0] = slots (0, 2), p[1] = (1, 3)
+    // the 4 states as 16-bit lanes: p[0] = slots (0, 2), p[1] = (1, 3); the
+    // quad's two bytes (slots 0, 1 and slots 2, 3) first go to the two lanes
     __device__ static void split(V v, uint32_t (&p)[2]) {
-        p[0] = (v & 0xfu) | ((v & 0xf00u) << 8);
-        p[1] = ((v >> 4) & 0xfu) | ((v & 0xf000u) << 4);
+        const uint32_t t = __builtin_amdgcn_perm(0u, v, 0x0c010c00u);
+        p[0] = t & 0x000f000fu;
+        p[1] = (t >> 4) & 0x000f000fu;
     }
     __device__ static constexpr int word_of(int c) { return c & 1; }
     __device__ static constexpr int half_of(int c) { return c >> 1; }
@@ -218,7 +220,8 @@ template <typename ST>
 __device__ __forceinline__ typename Quad<ST>::V load_row(const void *__restrict__ states, int32_t node,
                                                          int64_t nbytes, uint32_t lane_boff) {
     const __amdgpu_buffer_rsrc_t r =
-        buffer_rsrc(reinterpret_cast<const char *>(states) + (int64_t)node * nbytes, (uint32_t)nbytes);
+        buffer_rsrc(reinterpret_cast<const char *>(states) + (uint64_t)(uint32_t)node * (uint32_t)nbytes,
+                    (uint32_t)nbytes);
     return Quad<ST>::load_buffer(r, lane_boff);
 }
 
@@ -545,9 +548,11 @@ __device__ __forceinline__ float uniform24(uint32_t word) { return (float)(word 
 // hold; the item's store writes their draws back (valid states).
 
 // Buffer resource over node `node`'s state quads (offsets past them read 0).
+// (node >= 0 and nbytes < 2^31: a 32 x 32 -> 64-bit product)
 template <typename ST>
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t node_rsrc(const void *states, int32_t node, int64_t nbytes) {
-    return buffer_rsrc(reinterpret_cast<const char *>(states) + (int64_t)node * nbytes, (uint32_t)nbytes);
+    return buffer_rsrc(reinterpret_cast<const char *>(states) + (uint64_t)(uint32_t)node * (uint32_t)nbytes,
+                       (uint32_t)nbytes);
 }
 
 constexpr int kItemBatch = 4;  // blanket entries whose state quads are in flight together
@@ -594,8 +599,9 @@ __device__ __forceinline__ void item_group(cint32_t *&g, const void *__restrict_
 }
 
 // Multiplies the k-vectors of a group into the four slots' weights (from LDS
-// when FROM_LDS, else from global memory).
-template <int KP, typename ST, bool FROM_LDS, bool RESCALE>
+// when FROM_LDS, else from global memory); FIRST: the group's k-vectors are
+// the weights (the product of one factor).
+template <int KP, typename ST, bool FROM_LDS, bool RESCALE, bool FIRST = false>
 __device__ __forceinline__ void item_multiply(lds_char *lds, global_char *gtab, const uint32_t (&Pk)[2],
                                               float (&w)[4][KP]) {
 #pragma unroll
@@ -603,7 +609,7 @@ __device__ __forceinline__ void item_multiply(lds_char *lds, global_char *gtab, 
         float f[KP];
         fast_kvec<KP, FROM_LDS>(lds, gtab, packed_index<ST>(Pk, c), f);
 #pragma unroll
-        for (int k = 0; k < KP; ++k) w[c][k] *= f[k];
+        for (int k = 0; k < KP; ++k) w[c][k] = FIRST ? f[k] : w[c][k] * f[k];
         if (RESCALE) renorm<KP>(w[c]);
     }
 }
@@ -612,20 +618,20 @@ __device__ __forceinline__ void item_multiply(lds_char *lds, global_char *gtab, 
 // entries) of the item's four replica slots from a fast product list: the
 // first n_staged groups read their k-vectors from the LDS copy of the record
 // (byte indices), the others from global memory (k-vector units).  The
-// weights start at one (exact).  With RESCALE every running product is
-// renormalised after each factor, which keeps it away from fp32 underflow.
+// list's first group (every list has one) gives the weights; each later group
+// multiplies into them, in list order.  With RESCALE every running product is renormalised
+// after each factor, which keeps it away from fp32 underflow.
 template <int KP, typename ST, bool STAGED, bool RESCALE>
 __device__ __forceinline__ void item_product(cint32_t *g, int n_groups, int n_staged, lds_char *lds,
                                              global_char *gtab, const void *__restrict__ states, int64_t vstride,
                                              uint32_t qoff, int nrep, float (&w)[4][KP]) {
-#pragma unroll
-    for (int c = 0; c < 4; ++c)
-#pragma unroll
-        for (int k = 0; k < KP; ++k) w[c][k] = 1.f;
     uint32_t Pk[2];
+    item_group<ST>(g, states, vstride, qoff, nrep, Pk);
+    if (STAGED && n_staged > 0) item_multiply<KP, ST, true, RESCALE, true>(lds, gtab, Pk, w);
+    else item_multiply<KP, ST, false, RESCALE, true>(lds, gtab, Pk, w);
     // the staged groups, then the global ones: two loops, so that each keeps
     // only its own addressing live
-    int j = 0;
+    int j = 1;
     if (STAGED) {
         for (; j < n_staged; ++j) {
             item_group<ST>(g, states, vstride, qoff, nrep, Pk);
