@@ -2122,14 +2122,18 @@ hipError_t launch_counts(const DeviceTables &t, const void *states, int32_t stat
     if (n_cols <= 0) return hipSuccess;
     const int32_t n = t.n_cwork;
     // one node x 4096 columns (two lane iterations of kCountQuadsPerLane
-    // columns) x all replica quads per block, XCD-swizzled like the sweep
-    const int64_t cols_per_block = 2 * dev::kBlock * dev::kCountQuadsPerLane;
+    // columns) x all replica quads per block, XCD-swizzled like the sweep;
+    // launches with few blocks take one lane iteration (2048 columns) per
+    // block
+    const int64_t mq = (m + 3) / 4;
+    const int64_t quad_runs = (mq + dev::kCountQuads - 1) / dev::kCountQuads;
+    int64_t cols_per_block = 2 * dev::kBlock * dev::kCountQuadsPerLane;
+    if ((int64_t)n * ((n_cols + cols_per_block - 1) / cols_per_block) * quad_runs < dev::kMinSweepBlocks)
+        cols_per_block /= 2;
     const int64_t col_slabs = (n_cols + cols_per_block - 1) / cols_per_block;
     // small launches split the replica quads (in runs of kCountQuads) over
     // blocks until there are kMinSweepBlocks blocks, so that they fill the
     // device
-    const int64_t mq = (m + 3) / 4;
-    const int64_t quad_runs = (mq + dev::kCountQuads - 1) / dev::kCountQuads;
     int64_t rparts = (dev::kMinSweepBlocks + (int64_t)n * col_slabs - 1) / ((int64_t)n * col_slabs);
     if (rparts > quad_runs) rparts = quad_runs;
     if (rparts < 1) rparts = 1;
