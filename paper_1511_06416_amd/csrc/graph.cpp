@@ -554,15 +554,33 @@ int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int
     // per (colour, class) the LDS bytes the launch needs
     g.launch.assign((size_t)g.n_colors * (kLaunchClasses + 1), 0);
     g.launch_lds.assign((size_t)g.n_colors * kLaunchClasses, 0);
+    // a node's sweep cost per item, estimated from its fast list: the
+    // entries' loads and, per group, the k-vector products or thresholds
+    auto sweep_cost = [&](int32_t i) {
+        const int32_t *d = g.desc.data() + g.desc_off[i];
+        const int32_t *gl = d + d[9];
+        const int32_t width = d[2] == kModeTable ? d[7] : d[1];
+        int64_t cost = 0;
+        for (int32_t t = 0; t < d[8]; ++t) {
+            cost += gl[0] + width;
+            gl += 2 + 2 * gl[0];
+        }
+        return cost;
+    };
     for (int32_t c = 0; c < g.n_colors; ++c) {
         for (int32_t k = 0; k < kLaunchClasses; ++k) {
             g.launch[c * (kLaunchClasses + 1) + k] = (int32_t)g.order.size();
+            std::vector<std::pair<int64_t, int32_t>> nodes;
             for (int32_t i : g.groups[c]) {
                 if (g.klass[i] != k) continue;
-                g.order.push_back(i);
+                nodes.push_back({k <= 1 ? -sweep_cost(i) : 0, i});
                 int32_t &lb = g.launch_lds[c * kLaunchClasses + k];
                 lb = std::max(lb, g.lds_bytes[i]);
             }
+            // the costliest nodes first: their blocks of every column slab
+            // start before the cheap ones, which shortens the launch's tail
+            std::stable_sort(nodes.begin(), nodes.end());
+            for (const auto &ni : nodes) g.order.push_back(ni.second);
         }
         g.launch[c * (kLaunchClasses + 1) + kLaunchClasses] = (int32_t)g.order.size();
     }
