@@ -502,6 +502,27 @@ int compile_graph(int32_t n, const int32_t *pptr, const int32_t *pidx, const int
                     // staged groups count bytes into LDS, the rest k-vectors
                     ok = ok && emit(gb, (int32_t)t < n_staged ? 1 : unit, true);
                 }
+                if (ok) {
+                    // the same list flat: per entry [node, mult, group base,
+                    // flags: 1 first of its group, 2 last, 4 staged group];
+                    // an empty group is one entry of the node itself with
+                    // multiplier 0
+                    std::vector<int32_t> flat;
+                    int64_t pos = base + g.desc[base + 9];
+                    for (size_t t = 0; t < groups.size(); ++t) {
+                        const int32_t ne = g.desc[pos], gbase = g.desc[pos + 1];
+                        const int32_t st = (int32_t)t < n_staged ? 4 : 0;
+                        if (ne == 0) flat.insert(flat.end(), {i, 0, gbase, 1 | 2 | st});
+                        for (int32_t q = 0; q < ne; ++q)
+                            flat.insert(flat.end(), {g.desc[pos + 2 + 2 * q], g.desc[pos + 3 + 2 * q], gbase,
+                                                     (q == 0 ? 1 : 0) | (q == ne - 1 ? 2 : 0) | st});
+                        pos += 2 + 2 * ne;
+                    }
+                    g.desc[base + 15] = (int32_t)g.desc.size() - base;
+                    g.desc.push_back((int32_t)(flat.size() / 4));
+                    g.desc.insert(g.desc.end(), {0, 0, 0});
+                    g.desc.insert(g.desc.end(), flat.begin(), flat.end());
+                }
             }
             // the class test above bounds every index below 2^16 units
             if (!ok) return fail(err, SAME_ESIZE, "packed sweep index overflow");

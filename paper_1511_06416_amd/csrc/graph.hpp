@@ -84,6 +84,11 @@ constexpr int64_t kCountSplitBins = 4 * kCountLdsBins;  // largest CPT counted i
 //        LDS (byte indices), the rest from global memory; in table mode 1
 //        when the threshold table is staged
 //   [14] words a block copies into LDS before drawing (multiple of 4)
+//   [15] product modes of classes 0 and 1: relative word index of the flat
+//        list, the fast list's entries in list order, four words each after
+//        a four-word header [E, 0, 0, 0]: [node, mult, group base, flags]
+//        with flags 1 = first entry of its group, 2 = last, 4 = staged
+//        group; an empty group is one entry of the node itself with mult 0
 // A group list is a sequence of groups [n_e, base, (node, mult) * n_e]; the
 // group's index is base + sum of mult * state over its entries.
 //   wide list (every node): group 0 is the node's own row (entries: its

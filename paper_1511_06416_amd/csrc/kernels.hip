@@ -556,6 +556,7 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t node_rsrc(const void *states, 
 }
 
 constexpr int kItemBatch = 4;  // blanket entries whose state quads are in flight together
+constexpr int kFlatGroups = 4;  // product nodes with this many groups take the flat entry walk
 
 // Adds the N entries (node, mult) at e to the item's packed index: every
 // entry's state quad is loaded before the first is used; slots >= nrep read 0.
@@ -644,6 +645,57 @@ __device__ __forceinline__ void item_product(cint32_t *g, int n_groups, int n_st
     }
 }
 
+// The n entries of a flat batch at e (4 words each): every entry's state
+// quad is loaded before the first use.
+template <int N, typename ST>
+__device__ __forceinline__ void flat_loads(cint32_t *e, const void *__restrict__ states, int64_t vstride,
+                                           uint32_t qoff, typename Quad<ST>::V (&v)[kItemBatch]) {
+#pragma unroll
+    for (int t = 0; t < N; ++t) v[t] = Quad<ST>::load_buffer(node_rsrc<ST>(states, e[4 * t], vstride), qoff);
+}
+
+// The product over a node's flat entry list (every group's k-vectors from
+// LDS when FROM_LDS, else from global memory): entries are loaded in batches
+// of kItemBatch across group boundaries, and a group's factor is applied as
+// soon as its last entry has been added.  The weights start at one (exact).
+template <int KP, typename ST, bool FROM_LDS>
+__device__ __forceinline__ void item_product_flat(cint32_t *f, lds_char *lds, global_char *gtab,
+                                                  const void *__restrict__ states, int64_t vstride, uint32_t qoff,
+                                                  int nrep, float (&w)[4][KP]) {
+    using Q = Quad<ST>;
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+#pragma unroll
+        for (int k = 0; k < KP; ++k) w[c][k] = 1.f;
+    const int E = f[0];
+    cint32_t *e = f + 4;
+    uint32_t Pk[2] = {0u, 0u};
+    for (int b = 0; b < E; b += kItemBatch, e += 4 * kItemBatch) {
+        __builtin_amdgcn_sched_barrier(0);
+        const int n = E - b < kItemBatch ? E - b : kItemBatch;
+        typename Q::V v[kItemBatch];
+        switch (n) {
+        case 1: flat_loads<1, ST>(e, states, vstride, qoff, v); break;
+        case 2: flat_loads<2, ST>(e, states, vstride, qoff, v); break;
+        case 3: flat_loads<3, ST>(e, states, vstride, qoff, v); break;
+        default: flat_loads<4, ST>(e, states, vstride, qoff, v); break;
+        }
+#pragma unroll
+        for (int s = 0; s < kItemBatch; ++s) {
+            if (s >= n) break;  // uniform
+            __builtin_amdgcn_sched_barrier(0);
+            cint32_t *x = e + 4 * s;
+            const int flags = x[3];
+            if (flags & 1) Pk[0] = Pk[1] = (uint32_t)x[2];
+            uint32_t p[2];
+            Q::split(Q::keep(v[s], nrep), p);
+            Pk[0] = pk_mad_u16(p[0], (uint32_t)x[1], Pk[0]);
+            Pk[1] = pk_mad_u16(p[1], (uint32_t)x[1], Pk[1]);
+            if (flags & 2) item_multiply<KP, ST, FROM_LDS, false>(lds, gtab, Pk, w);
+        }
+    }
+}
+
 // The block's latent columns and its replica range, as items.
 struct Items {
     const uint16_t *col;  // latent columns of the chunk, as offsets from c0 (LDS)
@@ -686,7 +738,14 @@ __device__ __forceinline__ void sweep_product(const SweepParams &P, const Work &
         item_of(I, t, j, rb, nrep);
         const uint32_t qoff = quad_boff<ST>(rb >> 2, P.ld, j);
         float w[4][KP];
-        item_product<KP, ST, STAGED, false>(grp, n_groups, n_staged, lds, gtab, states, vstride, qoff, nrep, w);
+        // nodes with many groups (all from LDS, or all from global memory)
+        // walk their flat entry list: fewer dependent loads per item
+        if (n_groups < kFlatGroups || (STAGED && n_staged != n_groups))
+            item_product<KP, ST, STAGED, false>(grp, n_groups, n_staged, lds, gtab, states, vstride, qoff, nrep, w);
+        else if (!STAGED)
+            item_product_flat<KP, ST, false>(d + d[15], lds, gtab, states, vstride, qoff, nrep, w);
+        else
+            item_product_flat<KP, ST, true>(d + d[15], lds, gtab, states, vstride, qoff, nrep, w);
         float wd[4][KP];
         if (DEBUG) {
 #pragma unroll
