@@ -647,17 +647,18 @@ __device__ __forceinline__ void item_product(cint32_t *g, int n_groups, int n_st
 
 // The n entries of a flat batch at e (4 words each): every entry's state
 // quad is loaded before the first use.
-template <int N, typename ST>
+template <int N, typename ST, int NB>
 __device__ __forceinline__ void flat_loads(cint32_t *e, const void *__restrict__ states, int64_t vstride,
-                                           uint32_t qoff, typename Quad<ST>::V (&v)[kItemBatch]) {
+                                           uint32_t qoff, typename Quad<ST>::V (&v)[NB]) {
 #pragma unroll
     for (int t = 0; t < N; ++t) v[t] = Quad<ST>::load_buffer(node_rsrc<ST>(states, e[4 * t], vstride), qoff);
 }
 
 // The product over a node's flat entry list (every group's k-vectors from
 // LDS when FROM_LDS, else from global memory): entries are loaded in batches
-// of kItemBatch across group boundaries, and a group's factor is applied as
-// soon as its last entry has been added.  The weights start at one (exact).
+// (of kItemBatch, twice that for two-state nodes) across group boundaries,
+// and a group's factor is applied as soon as its last entry has been added.
+// The weights start at one (exact).
 template <int KP, typename ST, bool FROM_LDS>
 __device__ __forceinline__ void item_product_flat(cint32_t *f, lds_char *lds, global_char *gtab,
                                                   const void *__restrict__ states, int64_t vstride, uint32_t qoff,
@@ -670,18 +671,24 @@ __device__ __forceinline__ void item_product_flat(cint32_t *f, lds_char *lds, gl
     const int E = f[0];
     cint32_t *e = f + 4;
     uint32_t Pk[2] = {0u, 0u};
-    for (int b = 0; b < E; b += kItemBatch, e += 4 * kItemBatch) {
+    // two-state nodes keep twice as many entries in flight (few registers)
+    constexpr int NB = KP <= 2 ? 2 * kItemBatch : kItemBatch;
+    for (int b = 0; b < E; b += NB, e += 4 * NB) {
         __builtin_amdgcn_sched_barrier(0);
-        const int n = E - b < kItemBatch ? E - b : kItemBatch;
-        typename Q::V v[kItemBatch];
+        const int n = E - b < NB ? E - b : NB;
+        typename Q::V v[NB];
         switch (n) {
-        case 1: flat_loads<1, ST>(e, states, vstride, qoff, v); break;
-        case 2: flat_loads<2, ST>(e, states, vstride, qoff, v); break;
-        case 3: flat_loads<3, ST>(e, states, vstride, qoff, v); break;
-        default: flat_loads<4, ST>(e, states, vstride, qoff, v); break;
+        case 1: flat_loads<1, ST, NB>(e, states, vstride, qoff, v); break;
+        case 2: flat_loads<2, ST, NB>(e, states, vstride, qoff, v); break;
+        case 3: flat_loads<3, ST, NB>(e, states, vstride, qoff, v); break;
+        case 4: flat_loads<4, ST, NB>(e, states, vstride, qoff, v); break;
+        case 5: flat_loads<NB >= 5 ? 5 : 4, ST, NB>(e, states, vstride, qoff, v); break;
+        case 6: flat_loads<NB >= 6 ? 6 : 4, ST, NB>(e, states, vstride, qoff, v); break;
+        case 7: flat_loads<NB >= 7 ? 7 : 4, ST, NB>(e, states, vstride, qoff, v); break;
+        default: flat_loads<NB, ST, NB>(e, states, vstride, qoff, v); break;
         }
 #pragma unroll
-        for (int s = 0; s < kItemBatch; ++s) {
+        for (int s = 0; s < NB; ++s) {
             if (s >= n) break;  // uniform
             __builtin_amdgcn_sched_barrier(0);
             cint32_t *x = e + 4 * s;
