@@ -205,6 +205,24 @@ def test_ragged_tails(n_cols, ld):
     assert np.array_equal(mb.cpu().numpy(), oracle.counts(net.parents, net.card, st, 3, n_cols))
 
 
+@pytest.mark.parametrize("bits", [0, 4])
+@pytest.mark.parametrize("lds", [None, 0, 256], ids=["staged", "global", "small-budget"])
+def test_many_group_nodes(bits, lds):
+    """Product nodes with four or more CPT groups walk their flat entry list
+    (entries loaded across group boundaries): the roots 0 and 1 (empty own
+    group, 7 groups each; K = 2 loads eight entries per batch, K = 5 four) and
+    node 2 (a parent and 5 child groups).  Records staged in LDS, read from
+    global memory, and a budget that stages only part of some records (those
+    nodes keep the group walk)."""
+    parents = [[], [], [0], [0, 1], [0, 2], [0, 1, 2], [0, 2], [1, 2], [0, 1], [1], [2, 1]]
+    card = [2, 5, 3, 2, 2, 2, 3, 2, 2, 2, 2]
+    net, st, ob, th = _custom(parents, card, 1000, 6, 0.5, 11)
+    kw = dict(state_bits=bits) if bits else {}
+    if lds is not None:
+        kw["lds_limit"] = lds
+    _custom_case(net, st, ob, th, 6, 1000, win=(0, 64), table_limit=0, **kw)
+
+
 def test_zero_columns_is_noop():
     net, st, ob, th = _custom([[], [0]], [2, 2], 8, 2, 0.5, 1, ld=8)
     ctx = H.context_for(net)
