@@ -84,8 +84,8 @@ def main():
         counters_summary(args.counters_summary, args.cfg)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
-              "(see the design notes for how the sampler would shard columns)", file=sys.stderr)
+        print("bench.py runs on exactly one GPU: the library has no multi-GPU path (columns would shard "
+              "across GPUs with an all-reduce of the int32 count deltas per CPT update)", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
