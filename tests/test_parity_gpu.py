@@ -205,7 +205,7 @@ def test_ragged_tails(n_cols, ld):
     assert np.array_equal(mb.cpu().numpy(), oracle.counts(net.parents, net.card, st, 3, n_cols))
 
 
-@pytest.mark.parametrize("bits", [0, 4])
+@pytest.mark.parametrize("bits", [0, 4, 16])
 @pytest.mark.parametrize("lds", [None, 0, 256], ids=["staged", "global", "small-budget"])
 def test_many_group_nodes(bits, lds):
     """Product nodes with four or more CPT groups walk their flat entry list
@@ -213,9 +213,12 @@ def test_many_group_nodes(bits, lds):
     group, 7 groups each; K = 2 loads eight entries per batch, K = 5 four) and
     node 2 (a parent and 5 child groups).  Records staged in LDS, read from
     global memory, and a budget that stages only part of some records (those
-    nodes keep the group walk)."""
+    nodes keep the group walk).  bits = 16: an isolated 130-state node makes
+    every state a 16-bit one."""
     parents = [[], [], [0], [0, 1], [0, 2], [0, 1, 2], [0, 2], [1, 2], [0, 1], [1], [2, 1]]
     card = [2, 5, 3, 2, 2, 2, 3, 2, 2, 2, 2]
+    if bits == 16:
+        parents, card, bits = parents + [[]], card + [130], 0
     net, st, ob, th = _custom(parents, card, 1000, 6, 0.5, 11)
     kw = dict(state_bits=bits) if bits else {}
     if lds is not None:
